@@ -1,0 +1,193 @@
+#!/usr/bin/env python3
+"""Throughput of the BH t-SNE gradient iteration on one MI355X.
+
+A step is one full iteration of the library (bounding box, Morton codes,
+radix sort, quadtree build and summaries, Barnes-Hut repulsion with Z, CSR
+attraction, gradient and gains/momentum update) on the 1.3M-point workload
+with 30 Dirichlet(1) clusters and 90 within-cluster neighbours per point
+(about 2.34e8 stored entries of P), theta = 0.5, following the 1000-iteration
+schedule (exaggeration 12 and momentum 0.5 for the first 250 iterations, then
+1 and 0.8; learning rate N/12).  Inputs are seeded synthetic data resident in
+HBM before timing starts.
+
+Prints one JSON line on stdout.  Progress goes to stderr.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "BH t-SNE gradient iterations/s at N=1.3M, theta=0.5; repulsive interactions/s"
+HBM_PEAK_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1000)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", type=int, default=2)
+    ap.add_argument("--n", type=int, default=None, help="override the workload size")
+    ap.add_argument("--theta", type=float, default=0.5)
+    ap.add_argument("--cpu-iters", type=int, default=2, help="oracle iterations for the CPU baseline")
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-count", action="store_true", help="skip the interaction-counting replay")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: the multi-GPU path is a design note, "
+              "not a built component (use --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2212_11506_amd as bh
+    import synth
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    bh.load_library()
+    w = synth.WORKLOADS[args.workload]
+    t0 = time.time()
+    inp = synth.make_inputs(args.workload, n=args.n, progress=log)
+    log(f"[bench] inputs: n={inp.n} nnz={inp.nnz} generated in {time.time() - t0:.1f}s")
+    n, nnz = inp.n, inp.nnz
+    dev = torch.device("cuda:0")
+    Y0 = torch.from_numpy(inp.Y).to(dev)
+    P = bh.Csr.from_numpy(inp.row_ptr, inp.col, inp.val, device=dev)
+    ws = torch.empty(bh.workspace_size(n, nnz), dtype=torch.uint8, device=dev)
+    Y = Y0.clone()
+    u = torch.zeros_like(Y)
+    gains = torch.ones_like(Y)
+
+    def reset():
+        Y.copy_(Y0)
+        u.zero_()
+        gains.fill_(1.0)
+
+    def run(k, per_step=None):
+        for it in range(k):
+            s = w.schedule(it)
+            bh.step(Y, P, args.theta, s["exaggeration"], s["learning_rate"], s["momentum"], 0.01, u,
+                    gains, workspace=ws)
+            if per_step:
+                per_step(it)
+
+    # warm-up (code-object loading, caches), then back to the initial state
+    run(args.warmup)
+    torch.cuda.synchronize()
+    reset()
+    torch.cuda.synchronize()
+
+    bh.timing_read(reset=True)
+    bh.timing_enable(True)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    run(args.steps)
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    bh.timing_enable(False)
+    phases = bh.timing_read(reset=True)
+    elapsed = t2 - t1
+    its = args.steps / elapsed
+    log(f"[bench] {args.steps} steps in {elapsed:.3f}s -> {its:.1f} it/s")
+    stats_last = bh.get_stats(ws)
+    y_final = Y.cpu().numpy()
+
+    inter_total = None
+    if not args.no_count:
+        # deterministic kernels: replaying the same trajectory gives the same trees,
+        # so the per-step interaction counts belong to the timed run
+        reset()
+        counts = []
+        run(args.steps, per_step=lambda it: counts.append(bh.get_stats(ws)["interactions"]))
+        torch.cuda.synchronize()
+        same = np.array_equal(Y.cpu().numpy(), y_final)
+        log(f"[bench] replay identical to timed run: {same}")
+        inter_total = int(sum(counts)) if same else None
+
+    kernels = {}
+    for name, (ms, cnt) in phases.items():
+        per = ms / max(cnt, 1)
+        kernels[name] = {"ms_per_launch": per, "launches": cnt}
+    rep_ms = kernels["repulsive"]["ms_per_launch"]
+    att_ms = kernels["attractive"]["ms_per_launch"]
+    # algorithmic bytes per launch: repulsion 16 B per interaction + 20 B per point;
+    # attraction+update 8 B per stored entry (col, val) + 64 B per point
+    if inter_total is not None:
+        rep_bytes = 16.0 * inter_total / args.steps + 20.0 * n
+        kernels["repulsive"]["gbs"] = rep_bytes / (rep_ms * 1e-3) / 1e9
+        kernels["repulsive"]["frac_hbm"] = kernels["repulsive"]["gbs"] / HBM_PEAK_GBS
+        kernels["repulsive"]["interactions_per_s"] = inter_total / args.steps / (rep_ms * 1e-3)
+    att_bytes = 8.0 * nnz + 64.0 * n
+    kernels["attractive"]["gbs"] = att_bytes / (att_ms * 1e-3) / 1e9
+    kernels["attractive"]["frac_hbm"] = kernels["attractive"]["gbs"] / HBM_PEAK_GBS
+    dominant = max(("repulsive", "attractive"), key=lambda k: kernels[k]["ms_per_launch"])
+    if dominant == "repulsive" and inter_total is not None:
+        roof = {"kernel": "repulsive", "bound": "hbm", "achieved": kernels["repulsive"]["gbs"],
+                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": kernels["repulsive"]["frac_hbm"],
+                "traffic": None,
+                "model": "16 B per interaction (one cell summary or one point) + 20 B per point"}
+    else:
+        roof = {"kernel": "attractive", "bound": "hbm", "achieved": kernels["attractive"]["gbs"],
+                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": kernels["attractive"]["frac_hbm"],
+                "traffic": None, "model": "8 B per stored entry + 64 B per point"}
+
+    cpu = None
+    if not args.no_cpu and args.cpu_iters > 0:
+        import oracle
+
+        y = inp.Y.astype(np.float64)
+        uo = np.zeros_like(y)
+        go = np.ones_like(y)
+        tc = time.perf_counter()
+        for it in range(args.cpu_iters):
+            s = w.schedule(it)
+            oracle.step(y, uo, go, inp.row_ptr, inp.col, inp.val, args.theta, s["exaggeration"],
+                        s["learning_rate"], s["momentum"], 0.01)
+            log(f"[bench] oracle iteration {it} done at {time.perf_counter() - tc:.1f}s")
+        dt = time.perf_counter() - tc
+        cpu = {"value": args.cpu_iters / dt, "unit": "iterations/s", "cores": oracle.threads(),
+               "kind": "oracle",
+               "sample": f"first {args.cpu_iters} iterations of the same workload and schedule, "
+                         f"fp64 oracle, {dt:.1f}s"}
+
+    out = {
+        "metric": METRIC,
+        "value": its,
+        "unit": "iterations/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": 1e3 * elapsed / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{w.description} (workload {w.cid})", "n": n, "nnz": nnz,
+                   "theta": args.theta, "iterations": f"0..{args.steps - 1} of the schedule"},
+        "interactions_per_s": (inter_total / elapsed) if inter_total is not None else None,
+        "interactions_per_iteration": (inter_total / args.steps) if inter_total is not None else None,
+        "nodes_last": stats_last["nodes"],
+        "kernels": kernels,
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,168 @@
+/*
+ * bhtsne.h - C ABI of the MI355X (gfx950) Barnes-Hut t-SNE gradient library.
+ *
+ * One call computes the gradient of the t-SNE cost for a 2-D embedding Y and a
+ * sparse symmetric affinity matrix P, following the paper's per-iteration
+ * steps (Background, "Brief overview of the Barnes Hut t-SNE Algorithm"):
+ * quadtree building, summarization, attractive forces and repulsive forces,
+ * then the gradient (Gradient Descent, split-gradient equation)
+ *
+ *     dC/dy_i = 4 (alpha F_attr,i - F_rep,i / Z)
+ *     F_attr,i = sum_j p_ij (1 + |y_i - y_j|^2)^-1 (y_i - y_j)     (Algorithm 2)
+ *     F_rep,i  ~ sum_j (1 + |y_i - y_j|^2)^-2 (y_i - y_j)         (Barnes-Hut)
+ *     Z        ~ sum_{k != l} (1 + |y_k - y_l|^2)^-1                (q_ij definition)
+ *
+ * where the repulsive sums and Z are Barnes-Hut approximations: a quadtree
+ * cell of side s whose centre of mass c lies at distance d from y_i stands in
+ * for all of its points when s^2 < theta^2 d^2 (Repulsive Force Computation;
+ * the cell "radius" read as the side of the square cell).  theta = 0 gives the
+ * exact O(N^2) sums.  alpha is the early-exaggeration factor; it scales P.
+ *
+ * Conventions shared by every entry point:
+ *  - Arrays named as device arrays are device pointers on the GPU that is
+ *    current when the call is made; they stay owned by the caller.  The
+ *    library never allocates or frees device memory: all scratch space is
+ *    the caller's `workspace` (bhtsne_workspace_size bytes, 256-byte aligned).
+ *  - Y, grad, update and gains are n x 2 float32, row-major ((x, y) per point).
+ *  - All work is enqueued on `stream`; a call returns before it completes
+ *    unless it must return a host value (Z or a node count), in which case it
+ *    synchronises the stream first.  Calls that share a workspace must be
+ *    ordered (same stream); distinct workspaces may run concurrently.
+ *  - Every call returns a bhtsne_status code and never throws.  Arguments are
+ *    checked on the host before anything is enqueued; nothing is enqueued when
+ *    a check fails.  Conditions found on the GPU (a non-finite coordinate, a
+ *    corrupted intermediate) are latched in the workspace; they are reported
+ *    by calls that synchronise and by bhtsne_get_stats.
+ */
+#ifndef BHTSNE_H
+#define BHTSNE_H
+
+#include <hip/hip_runtime_api.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    BHTSNE_OK = 0,
+    BHTSNE_EINVAL = -1,     /* an argument failed a host-side check */
+    BHTSNE_EWORKSPACE = -2, /* workspace missing, misaligned or too small */
+    BHTSNE_ENONFINITE = -3, /* Y held a NaN or an infinity */
+    BHTSNE_EDEVICE = -4     /* a HIP call failed or the GPU flagged an internal error */
+} bhtsne_status;
+
+/* Sparse symmetric P in CSR form (0-based columns).  Expected, not checked:
+ * p_ij = p_ji >= 0, p_ii = 0, sum p = 1 (Background, "Input similarity
+ * computation").  row_ptr is non-decreasing with row_ptr[0] = 0 and
+ * row_ptr[n] = nnz; columns outside [0, n) and entries outside [0, nnz) are
+ * skipped on the GPU and flagged as a device error. */
+typedef struct bhtsne_csr {
+    int64_t n;              /* points; 2 <= n <= 67108863 */
+    int64_t nnz;            /* stored entries, >= 0 */
+    const int64_t *row_ptr; /* device, n + 1 entries */
+    const int32_t *col;     /* device, nnz entries (may be NULL when nnz == 0) */
+    const float *val;       /* device, nnz entries (may be NULL when nnz == 0) */
+} bhtsne_csr;
+
+/* Scalars of the last call on a workspace (bhtsne_get_stats). */
+typedef struct bhtsne_stats {
+    double Z;             /* normaliser (ordered pairs) */
+    int64_t interactions; /* accepted cell summaries + exact point pairs */
+    int64_t nodes;        /* nodes of the compressed quadtree */
+    double bbox[4];       /* min x, max x, min y, max y */
+    double r_span;        /* half side of the square domain */
+    uint32_t device_flags;/* 1 non-finite input, 2 look-back timeout, 4 index out of range */
+} bhtsne_stats;
+
+/* Kernel phases timed by bhtsne_timing_*. */
+enum {
+    BHTSNE_PHASE_BBOX_MORTON = 0, /* bounding box + Morton codes */
+    BHTSNE_PHASE_SORT = 1,        /* radix sort of the codes + gather of Y */
+    BHTSNE_PHASE_TREE = 2,        /* quadtree build + summaries */
+    BHTSNE_PHASE_REPULSIVE = 3,   /* Barnes-Hut traversal + Z */
+    BHTSNE_PHASE_ATTRACTIVE = 4,  /* CSR attractive forces + gradient + update */
+    BHTSNE_NUM_PHASES = 5
+};
+
+typedef struct bhtsne_timing {
+    double ms[BHTSNE_NUM_PHASES];   /* summed GPU time per phase (hipEvent pairs on the call's stream) */
+    int64_t count[BHTSNE_NUM_PHASES];
+} bhtsne_timing;
+
+/* Bytes of workspace needed for n points and nnz entries (0 if n is out of
+ * range).  Pure host arithmetic; the same value for every call with these
+ * sizes. */
+size_t bhtsne_workspace_size(int64_t n, int64_t nnz);
+
+/* Gradient of the t-SNE cost at Y (see the top of this file).
+ *   Y      device, n x 2, read only.
+ *   P      host struct describing the device CSR arrays; P->n is n.
+ *   theta  Barnes-Hut angle, finite, >= 0 (0 = exact).
+ *   exaggeration  alpha, finite, > 0.
+ *   grad   device, n x 2, written.
+ *   Z      host, nullable: when given, the stream is synchronised and the
+ *          normaliser is stored; device flags are then checked as well.
+ * Errors: BHTSNE_EINVAL (bad argument), BHTSNE_EWORKSPACE, BHTSNE_ENONFINITE,
+ * BHTSNE_EDEVICE. */
+int bhtsne_gradient(const float *Y, const bhtsne_csr *P, float theta, float exaggeration, float *grad,
+                    double *Z, void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* One gradient-descent iteration in place: the gradient as above, then per
+ * coordinate (the delta-bar-delta gains of the usual t-SNE optimiser; the
+ * paper only states that the experiments keep scikit-learn's defaults,
+ * Experimental setup)
+ *     gain = (u * g < 0) ? gain + 0.2 : gain * 0.8;  gain = max(gain, min_gain)
+ *     u    = momentum * u - learning_rate * gain * g
+ *     y    = y + u
+ *   Y       device, n x 2, read and overwritten with the new embedding.
+ *   update  device, n x 2, momentum buffer u (zero before the first step).
+ *   gains   device, n x 2 (one before the first step).
+ *   grad    device, n x 2, nullable: the gradient at the old Y.
+ *   learning_rate finite > 0; momentum in [0, 1); min_gain finite >= 0.
+ * Other arguments and errors as bhtsne_gradient. */
+int bhtsne_step(float *Y, const bhtsne_csr *P, float theta, float exaggeration, float learning_rate,
+                float momentum, float min_gain, float *update, float *gains, float *grad, double *Z,
+                void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Copy the scalars of the last call on `workspace` to *out; synchronises
+ * `stream`.  Returns BHTSNE_ENONFINITE / BHTSNE_EDEVICE when the last call
+ * latched a device flag (the stats are still filled in). */
+int bhtsne_get_stats(const void *workspace, bhtsne_stats *out, hipStream_t stream);
+
+/* Static English text for a status code. */
+const char *bhtsne_status_string(int status);
+
+/* Per-phase GPU timing.  While enabled, every later call records a hipEvent
+ * pair around each phase on its stream (process-wide switch, thread safe).
+ * bhtsne_timing_read waits for the recorded events, returns the summed
+ * milliseconds per phase, and with reset != 0 starts a new accumulation. */
+int bhtsne_timing_enable(int enable);
+int bhtsne_timing_read(bhtsne_timing *out, int reset);
+
+/* Test export: bounding box, Morton codes and their sort (Quadtree Building,
+ * Algorithm 1).  codes (original order), sorted_codes and perm (sorted
+ * position -> original index) are device arrays of n entries, each nullable.
+ * params is a host array of 10 doubles {min x, max x, min y, max y, cent x,
+ * cent y, r_span, y_root x, y_root y, scale}, nullable; when given the
+ * stream is synchronised. */
+int bhtsne_debug_sort(const float *Y, int64_t n, uint64_t *codes, uint64_t *sorted_codes, uint32_t *perm,
+                      double *params, void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Test export: the compressed quadtree and its summaries (Quadtree Building,
+ * Parallel Summarization) in depth-first pre-order, i.e. sorted by (begin,
+ * level).  Device arrays of 2n entries (summary: 2n x 4 floats {com x, com y,
+ * count, threshold}), each nullable; *n_nodes (host, required) receives the
+ * node count after a stream synchronisation.  kind: 0 internal, 1 bucket of
+ * identical codes, 2 single point.  meta: skip index (internal nodes) or
+ * begin | 0x80000000 (leaves). */
+int bhtsne_debug_tree(const float *Y, int64_t n, float theta, int64_t *n_nodes, uint8_t *level, uint8_t *kind,
+                      uint32_t *begin, uint32_t *end, float *summary, uint32_t *meta, void *workspace,
+                      size_t workspace_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BHTSNE_H */

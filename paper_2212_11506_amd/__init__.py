@@ -1,0 +1,28 @@
+"""MI355X (gfx950) Barnes-Hut t-SNE gradient step.
+
+A thin ctypes binding over ``lib/libbhtsne.so`` (C ABI in ``include/bhtsne.h``).
+PyTorch only provides device memory and the current stream; every step of
+the computation runs in the library's HIP kernels.  The functions keep the C
+names without the ``bhtsne_`` prefix.
+"""
+from ._binding import (  # noqa: F401
+    BHTSNE_EDEVICE,
+    BHTSNE_EINVAL,
+    BHTSNE_ENONFINITE,
+    BHTSNE_EWORKSPACE,
+    BHTSNE_OK,
+    PHASES,
+    BhtsneError,
+    Csr,
+    debug_sort,
+    debug_tree,
+    get_stats,
+    gradient,
+    library_path,
+    load_library,
+    status_string,
+    step,
+    timing_enable,
+    timing_read,
+    workspace_size,
+)

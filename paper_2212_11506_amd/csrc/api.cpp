@@ -1,0 +1,325 @@
+// C ABI of the library: argument checks, workspace carving, launch order and
+// per-phase timing.  See include/bhtsne.h for the contract of each call.
+#include "bhtsne.h"
+
+#include <array>
+#include <cmath>
+#include <cstring>
+#include <mutex>
+#include <vector>
+
+#include "kernels.hpp"
+
+using namespace bht;
+
+namespace {
+
+// ------------------------------------------------------------------ timing
+struct Timing {
+    std::mutex mu;
+    bool enabled = false;
+    std::vector<hipEvent_t> pool;
+    struct Pending {
+        int phase;
+        hipEvent_t a, b;
+    };
+    std::vector<Pending> pending;
+    double ms[BHTSNE_NUM_PHASES] = {};
+    int64_t count[BHTSNE_NUM_PHASES] = {};
+
+    hipEvent_t get()
+    {
+        if (!pool.empty()) {
+            hipEvent_t e = pool.back();
+            pool.pop_back();
+            return e;
+        }
+        hipEvent_t e = nullptr;
+        if (hipEventCreate(&e) != hipSuccess) return nullptr;
+        return e;
+    }
+};
+
+Timing &timing()
+{
+    static Timing t;
+    return t;
+}
+
+// Records an event pair around one phase when timing is on.
+class PhaseTimer {
+  public:
+    PhaseTimer(int phase, hipStream_t st) : phase_(phase), st_(st)
+    {
+        Timing &t = timing();
+        std::lock_guard<std::mutex> g(t.mu);
+        if (!t.enabled) return;
+        a_ = t.get();
+        b_ = t.get();
+        if (a_ && b_) hipEventRecord(a_, st_);
+    }
+    ~PhaseTimer()
+    {
+        if (!a_ || !b_) return;
+        hipEventRecord(b_, st_);
+        Timing &t = timing();
+        std::lock_guard<std::mutex> g(t.mu);
+        t.pending.push_back({phase_, a_, b_});
+    }
+
+  private:
+    int phase_;
+    hipStream_t st_;
+    hipEvent_t a_ = nullptr, b_ = nullptr;
+};
+
+bool finite_f(float x) { return std::isfinite(x); }
+
+bool aligned(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 255u) == 0; }
+
+int check_ws(int64_t n, int64_t nnz, void *ws, size_t bytes)
+{
+    if (!ws || !aligned(ws)) return BHTSNE_EWORKSPACE;
+    size_t need = bhtsne_workspace_size(n, nnz);
+    if (need == 0) return BHTSNE_EINVAL;
+    if (bytes < need) return BHTSNE_EWORKSPACE;
+    return BHTSNE_OK;
+}
+
+int check_csr(const bhtsne_csr *P)
+{
+    if (!P) return BHTSNE_EINVAL;
+    if (P->n < 2 || P->n > kMaxPoints) return BHTSNE_EINVAL;
+    if (P->nnz < 0 || !P->row_ptr) return BHTSNE_EINVAL;
+    if (P->nnz > 0 && (!P->col || !P->val)) return BHTSNE_EINVAL;
+    return BHTSNE_OK;
+}
+
+int flags_status(uint32_t flags)
+{
+    if (flags & kErrNonFinite) return BHTSNE_ENONFINITE;
+    if (flags & (kErrLookback | kErrRange)) return BHTSNE_EDEVICE;
+    return BHTSNE_OK;
+}
+
+int read_header(const void *ws, Header *h, hipStream_t st)
+{
+    if (hipMemcpyAsync(h, ws, sizeof(Header), hipMemcpyDeviceToHost, st) != hipSuccess) return BHTSNE_EDEVICE;
+    if (hipStreamSynchronize(st) != hipSuccess) return BHTSNE_EDEVICE;
+    return BHTSNE_OK;
+}
+
+// Steps a1..a6 of the iteration: box, codes, sort, tree and summaries.
+void build_tree(const float *Y, int64_t n, float theta, void *ws, const Layout &L, const TreeDebug &dbg,
+                hipStream_t st)
+{
+    {
+        PhaseTimer pt(BHTSNE_PHASE_BBOX_MORTON, st);
+        launch_bbox(Y, n, ws, L, st);
+        launch_morton(Y, n, ws, L, st);
+    }
+    {
+        PhaseTimer pt(BHTSNE_PHASE_SORT, st);
+        launch_sort(n, ws, L, st);
+    }
+    {
+        PhaseTimer pt(BHTSNE_PHASE_TREE, st);
+        launch_tree(n, theta, ws, L, dbg, st);
+    }
+}
+
+int run(float *Y, const bhtsne_csr *P, float theta, const StepArgs &a, float *update, float *gains, float *grad,
+        double *Z, void *ws, size_t ws_bytes, hipStream_t st)
+{
+    const int64_t n = P->n;
+    const Layout L = make_layout(n, P->nnz);
+    build_tree(Y, n, theta, ws, L, TreeDebug{}, st);
+    {
+        PhaseTimer pt(BHTSNE_PHASE_REPULSIVE, st);
+        launch_repulsive(n, ws, L, st);
+    }
+    {
+        PhaseTimer pt(BHTSNE_PHASE_ATTRACTIVE, st);
+        launch_attract(P->row_ptr, P->col, P->val, n, P->nnz, a, Y, update, gains, grad, ws, L, st);
+    }
+    if (hipGetLastError() != hipSuccess) return BHTSNE_EDEVICE;
+    if (Z) {
+        Header h;
+        int rc = read_header(ws, &h, st);
+        if (rc != BHTSNE_OK) return rc;
+        *Z = h.Z;
+        return flags_status(h.flags);
+    }
+    return BHTSNE_OK;
+}
+
+} // namespace
+
+extern "C" {
+
+size_t bhtsne_workspace_size(int64_t n, int64_t nnz)
+{
+    if (n < 2 || n > kMaxPoints || nnz < 0) return 0;
+    return make_layout(n, nnz).total;
+}
+
+int bhtsne_gradient(const float *Y, const bhtsne_csr *P, float theta, float exaggeration, float *grad, double *Z,
+                    void *workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    int rc = check_csr(P);
+    if (rc != BHTSNE_OK) return rc;
+    if (!Y || !grad) return BHTSNE_EINVAL;
+    if (!finite_f(theta) || theta < 0.0f) return BHTSNE_EINVAL;
+    if (!finite_f(exaggeration) || !(exaggeration > 0.0f)) return BHTSNE_EINVAL;
+    rc = check_ws(P->n, P->nnz, workspace, workspace_bytes);
+    if (rc != BHTSNE_OK) return rc;
+    StepArgs a{exaggeration, 0.0f, 0.0f, 0.0f, 0};
+    return run(const_cast<float *>(Y), P, theta, a, nullptr, nullptr, grad, Z, workspace, workspace_bytes, stream);
+}
+
+int bhtsne_step(float *Y, const bhtsne_csr *P, float theta, float exaggeration, float learning_rate, float momentum,
+                float min_gain, float *update, float *gains, float *grad, double *Z, void *workspace,
+                size_t workspace_bytes, hipStream_t stream)
+{
+    int rc = check_csr(P);
+    if (rc != BHTSNE_OK) return rc;
+    if (!Y || !update || !gains) return BHTSNE_EINVAL;
+    if (!finite_f(theta) || theta < 0.0f) return BHTSNE_EINVAL;
+    if (!finite_f(exaggeration) || !(exaggeration > 0.0f)) return BHTSNE_EINVAL;
+    if (!finite_f(learning_rate) || !(learning_rate > 0.0f)) return BHTSNE_EINVAL;
+    if (!finite_f(momentum) || momentum < 0.0f || !(momentum < 1.0f)) return BHTSNE_EINVAL;
+    if (!finite_f(min_gain) || min_gain < 0.0f) return BHTSNE_EINVAL;
+    rc = check_ws(P->n, P->nnz, workspace, workspace_bytes);
+    if (rc != BHTSNE_OK) return rc;
+    StepArgs a{exaggeration, learning_rate, momentum, min_gain, 1};
+    return run(Y, P, theta, a, update, gains, grad, Z, workspace, workspace_bytes, stream);
+}
+
+int bhtsne_get_stats(const void *workspace, bhtsne_stats *out, hipStream_t stream)
+{
+    if (!workspace || !out || !aligned(workspace)) return BHTSNE_EINVAL;
+    Header h;
+    int rc = read_header(workspace, &h, stream);
+    if (rc != BHTSNE_OK) return rc;
+    out->Z = h.Z;
+    out->interactions = int64_t(h.interactions);
+    out->nodes = int64_t(h.nodes);
+    out->bbox[0] = h.bmin[0];
+    out->bbox[1] = h.bmax[0];
+    out->bbox[2] = h.bmin[1];
+    out->bbox[3] = h.bmax[1];
+    out->r_span = h.rspan;
+    out->device_flags = h.flags;
+    return flags_status(h.flags);
+}
+
+const char *bhtsne_status_string(int status)
+{
+    switch (status) {
+    case BHTSNE_OK: return "ok";
+    case BHTSNE_EINVAL: return "invalid argument";
+    case BHTSNE_EWORKSPACE: return "workspace missing, misaligned or too small";
+    case BHTSNE_ENONFINITE: return "non-finite coordinate in Y";
+    case BHTSNE_EDEVICE: return "HIP error or device-side consistency failure";
+    default: return "unknown status";
+    }
+}
+
+int bhtsne_timing_enable(int enable)
+{
+    Timing &t = timing();
+    std::lock_guard<std::mutex> g(t.mu);
+    t.enabled = enable != 0;
+    return BHTSNE_OK;
+}
+
+int bhtsne_timing_read(bhtsne_timing *out, int reset)
+{
+    if (!out) return BHTSNE_EINVAL;
+    Timing &t = timing();
+    std::lock_guard<std::mutex> g(t.mu);
+    int rc = BHTSNE_OK;
+    for (auto &p : t.pending) {
+        float ms = 0.0f;
+        if (hipEventSynchronize(p.b) != hipSuccess || hipEventElapsedTime(&ms, p.a, p.b) != hipSuccess)
+            rc = BHTSNE_EDEVICE;
+        t.ms[p.phase] += ms;
+        t.count[p.phase] += 1;
+        t.pool.push_back(p.a);
+        t.pool.push_back(p.b);
+    }
+    t.pending.clear();
+    for (int k = 0; k < BHTSNE_NUM_PHASES; ++k) {
+        out->ms[k] = t.ms[k];
+        out->count[k] = t.count[k];
+        if (reset) {
+            t.ms[k] = 0.0;
+            t.count[k] = 0;
+        }
+    }
+    return rc;
+}
+
+int bhtsne_debug_sort(const float *Y, int64_t n, uint64_t *codes, uint64_t *sorted_codes, uint32_t *perm,
+                      double *params, void *workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    if (!Y || n < 2 || n > kMaxPoints) return BHTSNE_EINVAL;
+    int rc = check_ws(n, 0, workspace, workspace_bytes);
+    if (rc != BHTSNE_OK) return rc;
+    const Layout L = make_layout(n, 0);
+    launch_bbox(Y, n, workspace, L, stream);
+    launch_morton(Y, n, workspace, L, stream);
+    if (codes && hipMemcpyAsync(codes, at<void>(workspace, L.codes0), 8 * size_t(n), hipMemcpyDeviceToDevice,
+                                stream) != hipSuccess)
+        return BHTSNE_EDEVICE;
+    launch_sort(n, workspace, L, stream);
+    if (sorted_codes && hipMemcpyAsync(sorted_codes, at<void>(workspace, L.codes0), 8 * size_t(n),
+                                       hipMemcpyDeviceToDevice, stream) != hipSuccess)
+        return BHTSNE_EDEVICE;
+    if (perm && hipMemcpyAsync(perm, at<void>(workspace, L.idx0), 4 * size_t(n), hipMemcpyDeviceToDevice,
+                               stream) != hipSuccess)
+        return BHTSNE_EDEVICE;
+    if (hipGetLastError() != hipSuccess) return BHTSNE_EDEVICE;
+    if (params) {
+        Header h;
+        rc = read_header(workspace, &h, stream);
+        if (rc != BHTSNE_OK) return rc;
+        double p[10] = {h.bmin[0], h.bmax[0], h.bmin[1], h.bmax[1], h.cent[0],
+                        h.cent[1], h.rspan,   h.yroot[0], h.yroot[1], h.scale};
+        std::memcpy(params, p, sizeof(p));
+        return flags_status(h.flags);
+    }
+    return BHTSNE_OK;
+}
+
+int bhtsne_debug_tree(const float *Y, int64_t n, float theta, int64_t *n_nodes, uint8_t *level, uint8_t *kind,
+                      uint32_t *begin, uint32_t *end, float *summary, uint32_t *meta, void *workspace,
+                      size_t workspace_bytes, hipStream_t stream)
+{
+    if (!Y || !n_nodes || n < 2 || n > kMaxPoints) return BHTSNE_EINVAL;
+    if (!finite_f(theta) || theta < 0.0f) return BHTSNE_EINVAL;
+    if ((level || kind || begin || end) && !(level && kind && begin && end)) return BHTSNE_EINVAL;
+    int rc = check_ws(n, 0, workspace, workspace_bytes);
+    if (rc != BHTSNE_OK) return rc;
+    const Layout L = make_layout(n, 0);
+    TreeDebug dbg;
+    dbg.level = level;
+    dbg.kind = kind;
+    dbg.begin = begin;
+    dbg.end = end;
+    build_tree(Y, n, theta, workspace, L, dbg, stream);
+    if (summary && hipMemcpyAsync(summary, at<void>(workspace, L.nodes), 16 * size_t(2 * n),
+                                  hipMemcpyDeviceToDevice, stream) != hipSuccess)
+        return BHTSNE_EDEVICE;
+    if (meta && hipMemcpyAsync(meta, at<void>(workspace, L.meta), 4 * size_t(2 * n), hipMemcpyDeviceToDevice,
+                               stream) != hipSuccess)
+        return BHTSNE_EDEVICE;
+    if (hipGetLastError() != hipSuccess) return BHTSNE_EDEVICE;
+    Header h;
+    rc = read_header(workspace, &h, stream);
+    if (rc != BHTSNE_OK) return rc;
+    *n_nodes = int64_t(h.nodes);
+    return flags_status(h.flags);
+}
+
+} // extern "C"

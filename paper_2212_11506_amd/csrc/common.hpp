@@ -1,0 +1,158 @@
+// Shared device-side definitions of the BH t-SNE gradient library (gfx950).
+//
+// Workspace layout, node record format and small wave64 helpers used by the
+// kernels in this directory.  Nothing here is visible through the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace bht {
+
+constexpr int kWave = 64;
+constexpr int kRadixBits = 8;
+constexpr int kRadix = 1 << kRadixBits;
+constexpr int kSortPasses = 64 / kRadixBits;
+constexpr int kSortBlock = 256;                    // 4 waves
+constexpr int kSortItems = 8;                      // keys per thread
+constexpr int kSortTile = kSortBlock * kSortItems; // keys per tile
+constexpr int kScanBlock = 256;
+constexpr int kScanItems = 16;
+constexpr int kScanTile = kScanBlock * kScanItems;
+constexpr int kBBoxBlocks = 512;
+constexpr int kRepBlock = 256;
+constexpr uint32_t kLeafBit = 0x80000000u;
+constexpr int64_t kMaxPoints = (int64_t(1) << 26) - 1; // node records hold counts in fp32 exactly
+
+// Status words of the decoupled look-back: 2 flag bits + 30-bit count.
+constexpr uint32_t kFlagAggregate = 1u << 30;
+constexpr uint32_t kFlagInclusive = 2u << 30;
+constexpr uint32_t kValueMask = (1u << 30) - 1;
+constexpr uint32_t kSpinLimit = 1u << 22;
+
+// Device-side error flags (Header::flags).
+constexpr uint32_t kErrNonFinite = 1u;
+constexpr uint32_t kErrLookback = 2u;
+constexpr uint32_t kErrRange = 4u;
+
+// Per-call scalars, written by the kernels, read back by the host on demand.
+struct Header {
+    float bmin[2], bmax[2];   // bounding box (exact fp32 min/max)
+    double cent[2];           // box centre
+    double rspan;             // half of the widest extent
+    double yroot[2];          // lower-left corner of the square domain
+    double scale;             // 2^31 / r_span (0 when r_span == 0)
+    double Z;                 // normaliser of the last call
+    unsigned long long interactions;
+    uint32_t nodes;           // node count of the last tree
+    uint32_t flags;           // kErr* bits, sticky until the host clears them
+    uint32_t tile_counter[kSortPasses];
+    uint32_t ticket_bbox;
+    uint32_t ticket_rep;
+    uint32_t pad[6];
+};
+
+// A node of the pre-order tree: summary record + meta word.
+//   rec = {com.x, com.y, count (float), thr}
+//   thr = side^2 / theta^2 (+inf when theta == 0); a cell is summarised for a
+//         point at squared distance d2 iff d2 > thr.  Single points carry
+//         thr = -1 and are always taken exactly.
+//   meta = skip index (internal)  |  begin | kLeafBit (leaf)
+struct Layout {
+    int64_t n, nnz, sort_tiles, scan_tiles, rep_blocks;
+    size_t header, hist, bbox_part, codes0, codes1, idx0, idx1, status, ycopy, ys, levelmask,
+        split_b, split_e, base, psum, scan_cnt, scan_sum, nodes, meta, frep, zpart, ipart, total;
+};
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+inline int64_t rep_blocks_for(int64_t n)
+{
+    int64_t b = (n + kRepBlock - 1) / kRepBlock;
+    return (b + 7) / 8 * 8; // multiple of 8 for the XCD-contiguous remap
+}
+
+inline Layout make_layout(int64_t n, int64_t nnz)
+{
+    Layout L{};
+    L.n = n;
+    L.nnz = nnz;
+    L.sort_tiles = (n + kSortTile - 1) / kSortTile;
+    L.scan_tiles = (n + 1 + kScanTile - 1) / kScanTile;
+    L.rep_blocks = rep_blocks_for(n);
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        size_t o = off;
+        off = align_up(off + bytes, 256);
+        return o;
+    };
+    L.header = take(sizeof(Header));
+    L.hist = take(sizeof(uint32_t) * kSortPasses * kRadix);
+    L.bbox_part = take(32 * kBBoxBlocks); // {min x, max x, min y, max y, non-finite flag}
+    L.codes0 = take(8 * size_t(n));
+    L.codes1 = take(8 * size_t(n));
+    L.idx0 = take(4 * size_t(n));
+    L.idx1 = take(4 * size_t(n));
+    L.status = take(4 * size_t(kSortPasses) * kRadix * size_t(L.sort_tiles));
+    L.ycopy = take(8 * size_t(n));
+    L.ys = take(8 * size_t(n));
+    L.levelmask = take(4 * size_t(n));
+    L.split_b = take(4 * size_t(n));
+    L.split_e = take(4 * size_t(n));
+    L.base = take(4 * size_t(n + 1));
+    L.psum = take(16 * size_t(n + 1));
+    L.scan_cnt = take(4 * size_t(L.scan_tiles + 1));
+    L.scan_sum = take(16 * size_t(L.scan_tiles + 1));
+    L.nodes = take(16 * size_t(2 * n));
+    L.meta = take(4 * size_t(2 * n));
+    L.frep = take(8 * size_t(n));
+    L.zpart = take(8 * size_t(L.rep_blocks));
+    L.ipart = take(8 * size_t(L.rep_blocks));
+    L.total = off;
+    return L;
+}
+
+template <typename T> __host__ __device__ inline T *at(void *ws, size_t off)
+{
+    return reinterpret_cast<T *>(static_cast<char *>(ws) + off);
+}
+
+// ---------------------------------------------------------------- wave64 helpers
+__device__ inline int lane_id() { return __lane_id(); }
+
+__device__ inline unsigned long long ballot(bool p) { return __ballot(p); }
+
+__device__ inline uint32_t uniform(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
+
+template <typename T> __device__ inline T wave_sum(T v)
+{
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+    return v;
+}
+
+__device__ inline float wave_min(float v)
+{
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fminf(v, __shfl_xor(v, o, kWave));
+    return v;
+}
+
+__device__ inline float wave_max(float v)
+{
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+    return v;
+}
+
+// Logical block index such that each of the 8 XCDs (blocks are dealt to XCDs
+// round-robin) receives one contiguous range of logical blocks.  `nblocks`
+// must be a multiple of 8.
+__device__ inline uint32_t xcd_contiguous(uint32_t b, uint32_t nblocks)
+{
+    uint32_t per = nblocks >> 3;
+    return (b & 7u) * per + (b >> 3);
+}
+
+} // namespace bht

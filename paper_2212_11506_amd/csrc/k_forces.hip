@@ -1,0 +1,243 @@
+// Repulsive (Barnes-Hut) and attractive forces, gradient and update (gfx950).
+//
+// Repulsive Force Computation: every point walks the tree depth first; a
+// cell whose side is small against its distance (side^2 < theta^2 d^2) is
+// replaced by its summary, otherwise its children are visited; leaves are
+// taken point by point, excluding the point itself.  The normaliser Z (the
+// q_ij definition) is the sum of all the kernel values used.
+//
+// GPU design: points are processed in Morton order, one lane per point, and a
+// wavefront walks the pre-order node array together.  The current node index
+// is wave-uniform (scalar loads of the 20-byte node record); a lane that
+// summarises a cell parks itself until the walk reaches the cell's skip
+// index, so its own interaction list is exactly the depth-first one, while the
+// wave only descends where some lane needs it.  No stack is needed.
+//
+// Attractive Force Computation (Algorithm 2): a group of lanes per CSR row,
+// coalesced column/value reads, fused with the gradient assembly
+// g = 4 (alpha F_attr - F_rep / Z) and the gains/momentum update.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace bht {
+
+__device__ inline float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+
+__global__ __launch_bounds__(kRepBlock) void repulsive_kernel(
+    const float4 *__restrict__ nodes, const uint32_t *__restrict__ meta, const float2 *__restrict__ ys,
+    const uint32_t *__restrict__ perm, Header *__restrict__ hdr, int64_t n, float2 *__restrict__ frep,
+    double *__restrict__ zpart, unsigned long long *__restrict__ ipart)
+{
+    const uint32_t nb = gridDim.x;
+    const uint32_t lb = xcd_contiguous(blockIdx.x, nb);
+    const int64_t si64 = int64_t(lb) * kRepBlock + threadIdx.x;
+    const bool valid = si64 < n;
+    const uint32_t si = uint32_t(si64);
+    const float2 yi = valid ? ys[si] : make_float2(0.0f, 0.0f);
+    uint32_t total = uniform(hdr->nodes);
+    const uint32_t cap = uint32_t(2 * n);
+    total = total < cap ? total : cap;
+
+    uint32_t cur = 0;
+    uint32_t resume = valid ? 0u : 0xffffffffu;
+    float fx = 0.0f, fy = 0.0f, z = 0.0f;
+    unsigned long long inter = 0;
+
+    while (cur < total) {
+        const float4 r = nodes[cur];
+        const uint32_t m = meta[cur];
+        const float dx = yi.x - r.x, dy = yi.y - r.y;
+        const float d2 = fmaf(dx, dx, dy * dy);
+        const bool active = cur >= resume;
+        const bool leaf = (m & kLeafBit) != 0u;
+        bool take = active && (d2 > r.w);
+        if (leaf && r.w < 0.0f) take = take && ((m & ~kLeafBit) != si); // a single point, not itself
+        if (take) {
+            const float w = fast_rcp(1.0f + d2);
+            const float nw = r.z * w;
+            z += nw;
+            const float nw2 = nw * w;
+            fx = fmaf(nw2, dx, fx);
+            fy = fmaf(nw2, dy, fy);
+        }
+        inter += __popcll(ballot(take));
+        const bool rej = active && !take;
+        uint32_t nxt;
+        if (leaf) {
+            if (r.w >= 0.0f && ballot(rej)) { // bucket: its members one by one
+                const uint32_t b = m & ~kLeafBit;
+                uint32_t e = b + uint32_t(r.z);
+                e = e < uint32_t(n) ? e : uint32_t(n);
+                for (uint32_t j = b; j < e; ++j) {
+                    const float2 yj = ys[j];
+                    const bool doit = rej && j != si;
+                    if (doit) {
+                        const float ex = yi.x - yj.x, ey = yi.y - yj.y;
+                        const float w = fast_rcp(1.0f + fmaf(ex, ex, ey * ey));
+                        z += w;
+                        const float w2 = w * w;
+                        fx = fmaf(w2, ex, fx);
+                        fy = fmaf(w2, ey, fy);
+                    }
+                    inter += __popcll(ballot(doit));
+                }
+            }
+            nxt = cur + 1;
+        } else {
+            if (take) resume = m;
+            nxt = ballot(rej) ? cur + 1 : m;
+        }
+        cur = uniform(nxt > cur ? nxt : cur + 1);
+    }
+
+    if (valid) {
+        uint32_t p = perm[si];
+        if (p < uint32_t(n)) frep[p] = make_float2(fx, fy);
+    }
+    // deterministic Z: wave -> block partial -> fixed-order sum in the last block
+    double zw = wave_sum(double(z));
+    __shared__ double s_z[kRepBlock / kWave];
+    __shared__ unsigned long long s_i[kRepBlock / kWave];
+    __shared__ bool s_last;
+    const int w = threadIdx.x / kWave;
+    if (lane_id() == 0) {
+        s_z[w] = zw;
+        s_i[w] = inter;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double zb = 0.0;
+        unsigned long long ib = 0;
+        for (int k = 0; k < kRepBlock / kWave; ++k) {
+            zb += s_z[k];
+            ib += s_i[k];
+        }
+        zpart[lb] = zb;
+        ipart[lb] = ib;
+        __threadfence();
+        s_last = atomicAdd(&hdr->ticket_rep, 1u) == nb - 1;
+    }
+    __syncthreads();
+    if (!s_last) return;
+    __threadfence();
+    // last block: each thread sums a fixed contiguous chunk, then a fixed tree
+    const uint32_t per = (nb + kRepBlock - 1) / kRepBlock;
+    double zs = 0.0;
+    unsigned long long is = 0;
+    for (uint32_t k = threadIdx.x * per; k < (threadIdx.x + 1) * per && k < nb; ++k) {
+        zs += zpart[k];
+        is += ipart[k];
+    }
+    zs = wave_sum(zs);
+    is = wave_sum(is);
+    __syncthreads();
+    if (lane_id() == 0) {
+        s_z[w] = zs;
+        s_i[w] = is;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double Z = 0.0;
+        unsigned long long I = 0;
+        for (int k = 0; k < kRepBlock / kWave; ++k) {
+            Z += s_z[k];
+            I += s_i[k];
+        }
+        hdr->Z = Z;
+        hdr->interactions = I;
+    }
+}
+
+template <int G, bool kUpdate>
+__global__ __launch_bounds__(256) void attract_kernel(
+    const int64_t *__restrict__ row_ptr, const int32_t *__restrict__ col, const float *__restrict__ val,
+    const float2 *__restrict__ ycopy, const float2 *__restrict__ frep, Header *__restrict__ hdr,
+    int64_t n, int64_t nnz, StepArgs a, float2 *__restrict__ Y, float2 *__restrict__ upd, float2 *__restrict__ gains,
+    float2 *__restrict__ grad)
+{
+    const int sub = lane_id() % G;
+    constexpr int kRows = 256 / G;
+    const float inv_z = float(1.0 / hdr->Z);
+    for (int64_t row0 = int64_t(blockIdx.x) * kRows; row0 < n; row0 += int64_t(gridDim.x) * kRows) {
+        const int64_t i = row0 + threadIdx.x / G;
+        const bool valid = i < n;
+        float fx = 0.0f, fy = 0.0f;
+        float2 yi = make_float2(0.0f, 0.0f);
+        if (valid) {
+            yi = ycopy[i];
+            int64_t s = row_ptr[i], e = row_ptr[i + 1];
+            if (s < 0 || e > nnz) { // malformed row: skip what lies outside the arrays
+                if (sub == 0) atomicOr(&hdr->flags, kErrRange);
+                s = s < 0 ? 0 : s;
+                e = e > nnz ? nnz : e;
+            }
+            for (int64_t k = s + sub; k < e; k += G) {
+                const int32_t j = col[k];
+                if (uint32_t(j) >= uint32_t(n)) {
+                    atomicOr(&hdr->flags, kErrRange);
+                    continue;
+                }
+                const float p = val[k];
+                const float2 yj = ycopy[j];
+                const float dx = yi.x - yj.x, dy = yi.y - yj.y;
+                const float pw = p * fast_rcp(1.0f + fmaf(dx, dx, dy * dy));
+                fx = fmaf(pw, dx, fx);
+                fy = fmaf(pw, dy, fy);
+            }
+        }
+#pragma unroll
+        for (int o = G / 2; o > 0; o >>= 1) {
+            fx += __shfl_xor(fx, o, kWave);
+            fy += __shfl_xor(fy, o, kWave);
+        }
+        if (valid && sub == 0) {
+            const float2 fr = frep[i];
+            const float gx = 4.0f * (a.alpha * fx - fr.x * inv_z);
+            const float gy = 4.0f * (a.alpha * fy - fr.y * inv_z);
+            if (grad) grad[i] = make_float2(gx, gy);
+            if (kUpdate) {
+                float2 u = upd[i], gn = gains[i];
+                gn.x = (u.x * gx < 0.0f) ? gn.x + 0.2f : gn.x * 0.8f;
+                gn.y = (u.y * gy < 0.0f) ? gn.y + 0.2f : gn.y * 0.8f;
+                gn.x = fmaxf(gn.x, a.min_gain);
+                gn.y = fmaxf(gn.y, a.min_gain);
+                u.x = a.momentum * u.x - a.learning_rate * gn.x * gx;
+                u.y = a.momentum * u.y - a.learning_rate * gn.y * gy;
+                Y[i] = make_float2(yi.x + u.x, yi.y + u.y);
+                upd[i] = u;
+                gains[i] = gn;
+            }
+        }
+    }
+}
+
+// ------------------------------------------------------------------ launchers
+void launch_repulsive(int64_t n, void *ws, const Layout &L, hipStream_t st)
+{
+    repulsive_kernel<<<unsigned(L.rep_blocks), kRepBlock, 0, st>>>(
+        at<float4>(ws, L.nodes), at<uint32_t>(ws, L.meta), at<float2>(ws, L.ys), at<uint32_t>(ws, L.idx0),
+        at<Header>(ws, L.header), n, at<float2>(ws, L.frep), at<double>(ws, L.zpart),
+        at<unsigned long long>(ws, L.ipart));
+}
+
+void launch_attract(const int64_t *row_ptr, const int32_t *col, const float *val, int64_t n, int64_t nnz,
+                    const StepArgs &a, float *Y, float *upd, float *gains, float *grad, void *ws, const Layout &L,
+                    hipStream_t st)
+{
+    constexpr int G = 16;
+    int64_t blocks = (n + (256 / G) - 1) / (256 / G);
+    if (blocks > 65535 * 8) blocks = 65535 * 8;
+    const float2 *yc = at<float2>(ws, L.ycopy);
+    const float2 *fr = at<float2>(ws, L.frep);
+    Header *hdr = at<Header>(ws, L.header);
+    if (a.update)
+        attract_kernel<G, true><<<unsigned(blocks), 256, 0, st>>>(
+            row_ptr, col, val, yc, fr, hdr, n, nnz, a, reinterpret_cast<float2 *>(Y), reinterpret_cast<float2 *>(upd),
+            reinterpret_cast<float2 *>(gains), reinterpret_cast<float2 *>(grad));
+    else
+        attract_kernel<G, false><<<unsigned(blocks), 256, 0, st>>>(row_ptr, col, val, yc, fr, hdr, n, nnz, a, nullptr,
+                                                                 nullptr, nullptr,
+                                                                 reinterpret_cast<float2 *>(grad));
+}
+
+} // namespace bht

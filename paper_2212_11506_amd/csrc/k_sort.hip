@@ -1,0 +1,395 @@
+// Bounding box, Morton codes and the radix sort of the codes (gfx950).
+//
+// Quadtree Building (Algorithm 1 and the paragraph on Morton codes): the
+// square domain is centred on the bounding box with half-side r_span, each
+// coordinate is quantised to 32 bits and the two are bit-interleaved with
+// dimension 0 in the even bits.  Sorting the codes puts points of a cell next
+// to each other, which is what the tree build and the repulsive traversal
+// rely on.
+//
+// The sort is an LSD radix sort over 8-bit digits (8 passes).  The global
+// digit histograms of all passes are accumulated while the codes are formed;
+// each pass is then a single kernel that ranks a tile in LDS, finds the
+// tile's global offsets with a decoupled look-back over the tiles before it,
+// and writes the tile out digit by digit.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace bht {
+
+// ------------------------------------------------------------------ bbox
+__global__ __launch_bounds__(256) void bbox_partial_kernel(const float2 *__restrict__ Y, int64_t n,
+                                                           float *__restrict__ part)
+{
+    float mnx = INFINITY, mny = INFINITY, mxx = -INFINITY, mxy = -INFINITY;
+    uint32_t bad = 0;
+    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n;
+         i += int64_t(gridDim.x) * blockDim.x) {
+        float2 y = Y[i];
+        bad |= !(isfinite(y.x) && isfinite(y.y));
+        mnx = fminf(mnx, y.x);
+        mxx = fmaxf(mxx, y.x);
+        mny = fminf(mny, y.y);
+        mxy = fmaxf(mxy, y.y);
+    }
+    mnx = wave_min(mnx);
+    mny = wave_min(mny);
+    mxx = wave_max(mxx);
+    mxy = wave_max(mxy);
+    bool anybad = ballot(bad != 0) != 0;
+    __shared__ float s[4][4];
+    __shared__ uint32_t sb[4];
+    int w = threadIdx.x / kWave;
+    if (lane_id() == 0) {
+        s[w][0] = mnx;
+        s[w][1] = mxx;
+        s[w][2] = mny;
+        s[w][3] = mxy;
+        sb[w] = anybad;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float r[4] = {s[0][0], s[0][1], s[0][2], s[0][3]};
+        uint32_t b = sb[0];
+        for (int k = 1; k < 4; ++k) {
+            r[0] = fminf(r[0], s[k][0]);
+            r[1] = fmaxf(r[1], s[k][1]);
+            r[2] = fminf(r[2], s[k][2]);
+            r[3] = fmaxf(r[3], s[k][3]);
+            b |= sb[k];
+        }
+        float *o = part + 8 * blockIdx.x;
+        o[0] = r[0];
+        o[1] = r[1];
+        o[2] = r[2];
+        o[3] = r[3];
+        reinterpret_cast<uint32_t *>(o)[4] = b;
+    }
+}
+
+// One block: finish the box, derive the quantisation parameters in fp64 and
+// reset the per-call counters and histograms.
+__global__ __launch_bounds__(256) void bbox_final_kernel(const float *__restrict__ part, int nparts,
+                                                         Header *__restrict__ hdr,
+                                                         uint32_t *__restrict__ hist)
+{
+    float mnx = INFINITY, mny = INFINITY, mxx = -INFINITY, mxy = -INFINITY;
+    uint32_t bad = 0;
+    for (int k = threadIdx.x; k < nparts; k += blockDim.x) {
+        const float *p = part + 8 * k;
+        mnx = fminf(mnx, p[0]);
+        mxx = fmaxf(mxx, p[1]);
+        mny = fminf(mny, p[2]);
+        mxy = fmaxf(mxy, p[3]);
+        bad |= reinterpret_cast<const uint32_t *>(p)[4];
+    }
+    mnx = wave_min(mnx);
+    mny = wave_min(mny);
+    mxx = wave_max(mxx);
+    mxy = wave_max(mxy);
+    bool anybad = ballot(bad != 0) != 0;
+    __shared__ float s[4][4];
+    __shared__ uint32_t sb[4];
+    int w = threadIdx.x / kWave;
+    if (lane_id() == 0) {
+        s[w][0] = mnx;
+        s[w][1] = mxx;
+        s[w][2] = mny;
+        s[w][3] = mxy;
+        sb[w] = anybad;
+    }
+    for (int k = threadIdx.x; k < kSortPasses * kRadix; k += blockDim.x) hist[k] = 0;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float r[4] = {s[0][0], s[0][1], s[0][2], s[0][3]};
+        uint32_t b = sb[0];
+        for (int k = 1; k < 4; ++k) {
+            r[0] = fminf(r[0], s[k][0]);
+            r[1] = fmaxf(r[1], s[k][1]);
+            r[2] = fminf(r[2], s[k][2]);
+            r[3] = fmaxf(r[3], s[k][3]);
+            b |= sb[k];
+        }
+        hdr->bmin[0] = r[0];
+        hdr->bmax[0] = r[1];
+        hdr->bmin[1] = r[2];
+        hdr->bmax[1] = r[3];
+        // fp64, fixed operation order: the codes depend on these bits
+        double c0 = (double(r[0]) + double(r[1])) * 0.5;
+        double c1 = (double(r[2]) + double(r[3])) * 0.5;
+        double e0 = double(r[1]) - double(r[0]);
+        double e1 = double(r[3]) - double(r[2]);
+        double rs = 0.5 * (e0 > e1 ? e0 : e1);
+        hdr->cent[0] = c0;
+        hdr->cent[1] = c1;
+        hdr->rspan = rs;
+        hdr->yroot[0] = c0 - rs;
+        hdr->yroot[1] = c1 - rs;
+        hdr->scale = rs > 0.0 ? 2147483648.0 / rs : 0.0;
+        hdr->flags = b ? kErrNonFinite : 0u;
+        hdr->Z = 0.0;
+        hdr->interactions = 0;
+        for (int k = 0; k < kSortPasses; ++k) hdr->tile_counter[k] = 0;
+        hdr->ticket_bbox = 0;
+        hdr->ticket_rep = 0;
+    }
+}
+
+// ------------------------------------------------------------------ Morton
+__device__ inline uint32_t quantise(float y, double yroot, double scale)
+{
+    double q = (double(y) - yroot) * scale;
+    if (!(q > 0.0)) return 0u; // also catches NaN
+    if (q >= 4294967295.0) return 0xffffffffu;
+    return uint32_t(q); // truncation toward zero
+}
+
+// Spread the 32 bits of v to the even positions of a 64-bit word.
+__device__ inline uint64_t spread_even(uint32_t v)
+{
+    uint64_t x = v;
+    x = (x | (x << 16)) & 0x0000ffff0000ffffull;
+    x = (x | (x << 8)) & 0x00ff00ff00ff00ffull;
+    x = (x | (x << 4)) & 0x0f0f0f0f0f0f0f0full;
+    x = (x | (x << 2)) & 0x3333333333333333ull;
+    x = (x | (x << 1)) & 0x5555555555555555ull;
+    return x;
+}
+
+// Codes of one tile of points, the private copy of Y, the 8 global digit
+// histograms; also clears the per-position tree masks and this tile's
+// look-back status words of every pass.
+__global__ __launch_bounds__(kSortBlock) void morton_kernel(
+    const float2 *__restrict__ Y, int64_t n, const Header *__restrict__ hdr,
+    uint64_t *__restrict__ codes, float2 *__restrict__ ycopy, uint32_t *__restrict__ hist,
+    uint32_t *__restrict__ levelmask, uint32_t *__restrict__ status, int64_t tiles)
+{
+    __shared__ uint32_t sh[kSortPasses * kRadix];
+    for (int k = threadIdx.x; k < kSortPasses * kRadix; k += kSortBlock) sh[k] = 0;
+    // clear this tile's look-back words of every pass
+    for (int k = threadIdx.x; k < kSortPasses * kRadix; k += kSortBlock) {
+        int pass = k / kRadix, d = k % kRadix;
+        status[(int64_t(pass) * tiles + blockIdx.x) * kRadix + d] = 0;
+    }
+    __syncthreads();
+    const double yr0 = hdr->yroot[0], yr1 = hdr->yroot[1], sc = hdr->scale;
+    const int64_t base = int64_t(blockIdx.x) * kSortTile;
+#pragma unroll
+    for (int r = 0; r < kSortItems; ++r) {
+        int64_t i = base + r * kSortBlock + threadIdx.x;
+        if (i < n) {
+            float2 y = Y[i];
+            ycopy[i] = y;
+            uint64_t code = spread_even(quantise(y.x, yr0, sc)) |
+                            (spread_even(quantise(y.y, yr1, sc)) << 1);
+            codes[i] = code;
+            levelmask[i] = 0;
+#pragma unroll
+            for (int p = 0; p < kSortPasses; ++p)
+                atomicAdd(&sh[p * kRadix + int((code >> (p * kRadixBits)) & (kRadix - 1))], 1u);
+        }
+    }
+    __syncthreads();
+    for (int k = threadIdx.x; k < kSortPasses * kRadix; k += kSortBlock)
+        if (sh[k]) atomicAdd(&hist[k], sh[k]);
+}
+
+// ------------------------------------------------------------------ onesweep pass
+// Block-wide exclusive scan of one value per thread (256 threads).
+__device__ inline uint32_t block_exclusive_scan256(uint32_t v, uint32_t *s_wave /*[4]*/,
+                                                   uint32_t *total)
+{
+    int lane = lane_id(), w = threadIdx.x / kWave;
+    uint32_t x = v;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        uint32_t y = __shfl_up(x, o, kWave);
+        if (lane >= o) x += y;
+    }
+    if (lane == kWave - 1) s_wave[w] = x;
+    __syncthreads();
+    uint32_t off = 0, tot = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        uint32_t t = s_wave[k];
+        off += (k < w) ? t : 0u;
+        tot += t;
+    }
+    if (total) *total = tot;
+    return off + x - v;
+}
+
+__device__ inline void publish(uint32_t *p, uint32_t word)
+{
+    __hip_atomic_store(p, word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ inline uint32_t peek(const uint32_t *p)
+{
+    return __hip_atomic_load(const_cast<uint32_t *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <bool kFirst, bool kLast>
+__global__ __launch_bounds__(kSortBlock) void onesweep_kernel(
+    const uint64_t *__restrict__ keys_in, const uint32_t *__restrict__ idx_in,
+    uint64_t *__restrict__ keys_out, uint32_t *__restrict__ idx_out,
+    uint32_t *__restrict__ status, const uint32_t *__restrict__ hist, Header *__restrict__ hdr,
+    int pass, int64_t n, const float2 *__restrict__ ycopy, float2 *__restrict__ ys)
+{
+    constexpr int kWaves = kSortBlock / kWave;
+    constexpr int kSeg = kWave * kSortItems; // keys per wave segment
+    __shared__ uint32_t s_tile;
+    __shared__ uint32_t s_wcnt[kWaves][kRadix];
+    __shared__ uint32_t s_lstart[kRadix];
+    __shared__ uint32_t s_gofs[kRadix];
+    __shared__ uint32_t s_scan[4];
+    __shared__ uint64_t s_keys[kSortTile];
+    __shared__ uint32_t s_idx[kSortTile];
+
+    const int t = threadIdx.x, w = t / kWave, lane = lane_id();
+    const int shift = pass * kRadixBits;
+    if (t == 0) s_tile = atomicAdd(&hdr->tile_counter[pass], 1u);
+    for (int k = t; k < kWaves * kRadix; k += kSortBlock) (&s_wcnt[0][0])[k] = 0;
+    __syncthreads();
+    const uint32_t tile = s_tile;
+    const int64_t base = int64_t(tile) * kSortTile;
+    const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
+
+    uint64_t key[kSortItems];
+    uint32_t rank[kSortItems];
+#pragma unroll
+    for (int r = 0; r < kSortItems; ++r) {
+        int64_t p = base + w * kSeg + r * kWave + lane;
+        bool valid = p < n;
+        key[r] = valid ? keys_in[p] : ~0ull;
+        uint32_t d = uint32_t(key[r] >> shift) & (kRadix - 1);
+        uint64_t peers = ballot(valid);
+#pragma unroll
+        for (int b = 0; b < kRadixBits; ++b) {
+            bool bit = (d >> b) & 1u;
+            uint64_t m = ballot(bit);
+            peers &= bit ? m : ~m;
+        }
+        int leader = peers ? __ffsll((unsigned long long)peers) - 1 : lane;
+        uint32_t old = 0;
+        if (valid && lane == leader) {
+            old = s_wcnt[w][d];
+            s_wcnt[w][d] = old + uint32_t(__popcll(peers));
+        }
+        old = __shfl(old, leader, kWave);
+        rank[r] = old + uint32_t(__popcll(peers & lt_mask));
+    }
+    __syncthreads();
+
+    // thread t owns digit t: per-wave offsets, tile count, look-back
+    const uint32_t d = t;
+    uint32_t c[kWaves], tot = 0;
+#pragma unroll
+    for (int k = 0; k < kWaves; ++k) {
+        c[k] = s_wcnt[k][d];
+        s_wcnt[k][d] = tot;
+        tot += c[k];
+    }
+    uint32_t *my = status + int64_t(tile) * kRadix + d;
+    publish(my, (tile == 0 ? kFlagInclusive : kFlagAggregate) | tot);
+    uint32_t lstart = block_exclusive_scan256(tot, s_scan, nullptr);
+    s_lstart[d] = lstart;
+    // global start of digit d: exclusive scan of the histogram
+    uint32_t h = hist[pass * kRadix + d];
+    __syncthreads();
+    uint32_t dbase = block_exclusive_scan256(h, s_scan, nullptr);
+    uint32_t excl = 0;
+    if (tile > 0) {
+        int64_t tt = int64_t(tile) - 1;
+        uint32_t spins = 0;
+        while (tt >= 0) {
+            uint32_t s = peek(status + tt * kRadix + d);
+            if ((s & ~kValueMask) == 0) {
+                if (++spins > kSpinLimit) { // a predecessor never published: give up loudly
+                    atomicOr(&hdr->flags, kErrLookback);
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(1);
+                continue;
+            }
+            excl += s & kValueMask;
+            if (s & kFlagInclusive) break;
+            --tt;
+        }
+        publish(my, kFlagInclusive | (excl + tot));
+    }
+    s_gofs[d] = dbase + excl;
+    __syncthreads();
+
+    // rank -> position inside the tile, staged through LDS
+#pragma unroll
+    for (int r = 0; r < kSortItems; ++r) {
+        int64_t p = base + w * kSeg + r * kWave + lane;
+        if (p < n) {
+            uint32_t dd = uint32_t(key[r] >> shift) & (kRadix - 1);
+            uint32_t lp = s_lstart[dd] + s_wcnt[w][dd] + rank[r];
+            s_keys[lp] = key[r];
+            s_idx[lp] = kFirst ? uint32_t(p) : idx_in[p];
+        }
+    }
+    __syncthreads();
+    const int tile_n = int(n - base < kSortTile ? n - base : kSortTile);
+    for (int j = t; j < tile_n; j += kSortBlock) {
+        uint64_t k = s_keys[j];
+        uint32_t dd = uint32_t(k >> shift) & (kRadix - 1);
+        uint32_t out = s_gofs[dd] + (uint32_t(j) - s_lstart[dd]);
+        if (out < uint32_t(n)) {
+            keys_out[out] = k;
+            uint32_t ix = s_idx[j];
+            idx_out[out] = ix;
+            if (kLast) ys[out] = ix < uint32_t(n) ? ycopy[ix] : make_float2(0.0f, 0.0f);
+        } else {
+            atomicOr(&hdr->flags, kErrRange);
+        }
+    }
+}
+
+// ------------------------------------------------------------------ launchers
+void launch_bbox(const float *Y, int64_t n, void *ws, const Layout &L, hipStream_t st)
+{
+    int blocks = int((n + 255) / 256);
+    if (blocks > kBBoxBlocks) blocks = kBBoxBlocks;
+    bbox_partial_kernel<<<blocks, 256, 0, st>>>(reinterpret_cast<const float2 *>(Y), n,
+                                                at<float>(ws, L.bbox_part));
+    bbox_final_kernel<<<1, 256, 0, st>>>(at<float>(ws, L.bbox_part), blocks,
+                                         at<Header>(ws, L.header), at<uint32_t>(ws, L.hist));
+}
+
+void launch_morton(const float *Y, int64_t n, void *ws, const Layout &L, hipStream_t st)
+{
+    morton_kernel<<<unsigned(L.sort_tiles), kSortBlock, 0, st>>>(
+        reinterpret_cast<const float2 *>(Y), n, at<Header>(ws, L.header),
+        at<uint64_t>(ws, L.codes0), at<float2>(ws, L.ycopy), at<uint32_t>(ws, L.hist),
+        at<uint32_t>(ws, L.levelmask), at<uint32_t>(ws, L.status), L.sort_tiles);
+}
+
+void launch_sort(int64_t n, void *ws, const Layout &L, hipStream_t st)
+{
+    uint64_t *k[2] = {at<uint64_t>(ws, L.codes0), at<uint64_t>(ws, L.codes1)};
+    uint32_t *x[2] = {at<uint32_t>(ws, L.idx0), at<uint32_t>(ws, L.idx1)};
+    Header *hdr = at<Header>(ws, L.header);
+    const uint32_t *hist = at<uint32_t>(ws, L.hist);
+    const float2 *yc = at<float2>(ws, L.ycopy);
+    float2 *ys = at<float2>(ws, L.ys);
+    for (int p = 0; p < kSortPasses; ++p) {
+        uint32_t *status = at<uint32_t>(ws, L.status) + int64_t(p) * L.sort_tiles * kRadix;
+        int src = p & 1, dst = src ^ 1;
+        dim3 g(unsigned(L.sort_tiles));
+        if (p == 0)
+            onesweep_kernel<true, false><<<g, kSortBlock, 0, st>>>(k[src], nullptr, k[dst], x[dst],
+                                                                  status, hist, hdr, p, n, yc, ys);
+        else if (p == kSortPasses - 1)
+            onesweep_kernel<false, true><<<g, kSortBlock, 0, st>>>(k[src], x[src], k[dst], x[dst],
+                                                                  status, hist, hdr, p, n, yc, ys);
+        else
+            onesweep_kernel<false, false><<<g, kSortBlock, 0, st>>>(k[src], x[src], k[dst], x[dst],
+                                                                   status, hist, hdr, p, n, yc, ys);
+    }
+}
+
+} // namespace bht

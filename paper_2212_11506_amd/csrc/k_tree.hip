@@ -1,0 +1,377 @@
+// Compressed quadtree over the sorted Morton codes, with cell summaries.
+//
+// Quadtree Building: a cell at level L is the set of codes that share their
+// top 2L bits, so every cell is a contiguous range of the sorted codes.  A
+// cell is a node of the compressed tree when its points fall into at least
+// two quadrants (the root always is one); runs of identical codes form a
+// single bucket leaf at level 32, and unique codes are single-point leaves.
+//
+// Parallel construction, one thread per sorted position:
+//   1. For each adjacent pair (s, s+1) the split level is
+//      lambda_s = floor(clz(M_s ^ M_s+1) / 2).  The cell at that level around
+//      s is found by galloping searches; the first split of a cell owns it and
+//      marks bit L of levelmask[begin].
+//   2. Nodes are numbered in depth-first pre-order, which is the order of
+//      (begin, level).  With cnt(x) = leaf starting at x + popcount(levelmask[x])
+//      and base = exclusive scan of cnt, node (L, [b,e)) sits at
+//      base[b] + popcount(levelmask[b] & (2^L - 1)), and the first node after
+//      its subtree is base[e].
+//   3. Summaries (Parallel Summarization) come from fp64 prefix sums of the
+//      sorted coordinates: com = (S[e] - S[b]) / (e - b), so no bottom-up
+//      level sweep is needed (cells of up to 32 points sum their points
+//      directly instead).
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace bht {
+
+__device__ inline int split_level(uint64_t a, uint64_t b) { return __clzll((long long)(a ^ b)) >> 1; }
+
+__device__ inline uint32_t quad_digit(uint64_t code, int L) { return uint32_t(code >> (62 - 2 * L)) & 3u; }
+
+// first index in [0, s] whose code shares the top (64 - sh) bits of key
+__device__ inline int64_t gallop_left(const uint64_t *__restrict__ codes, int64_t s, uint64_t key, int sh)
+{
+    int64_t hi = s, lo = -1, step = 1;
+    for (;;) {
+        int64_t probe = s - step;
+        if (probe < 0) break;
+        if (((codes[probe] ^ key) >> sh) != 0) {
+            lo = probe;
+            break;
+        }
+        hi = probe;
+        step <<= 1;
+    }
+    while (hi - lo > 1) {
+        int64_t mid = lo + (hi - lo) / 2;
+        if (((codes[mid] ^ key) >> sh) == 0)
+            hi = mid;
+        else
+            lo = mid;
+    }
+    return hi;
+}
+
+// one past the last index >= s whose code shares the top (64 - sh) bits of key
+__device__ inline int64_t gallop_right(const uint64_t *__restrict__ codes, int64_t s, int64_t n,
+                                       uint64_t key, int sh)
+{
+    int64_t lo = s, hi = n, step = 1;
+    for (;;) {
+        int64_t probe = s + step;
+        if (probe >= n) break;
+        if (((codes[probe] ^ key) >> sh) != 0) {
+            hi = probe;
+            break;
+        }
+        lo = probe;
+        step <<= 1;
+    }
+    while (hi - lo > 1) {
+        int64_t mid = lo + (hi - lo) / 2;
+        if (((codes[mid] ^ key) >> sh) == 0)
+            lo = mid;
+        else
+            hi = mid;
+    }
+    return hi;
+}
+
+// equality run of identical codes starting at x
+__device__ inline int64_t run_end(const uint64_t *__restrict__ codes, int64_t x, int64_t n)
+{
+    uint64_t k = codes[x];
+    if (x + 1 >= n || codes[x + 1] != k) return x + 1;
+    int64_t lo = x + 1, hi = n, step = 2;
+    for (;;) {
+        int64_t probe = x + step;
+        if (probe >= n) break;
+        if (codes[probe] != k) {
+            hi = probe;
+            break;
+        }
+        lo = probe;
+        step <<= 1;
+    }
+    while (hi - lo > 1) {
+        int64_t mid = lo + (hi - lo) / 2;
+        if (codes[mid] == k)
+            lo = mid;
+        else
+            hi = mid;
+    }
+    return hi;
+}
+
+// ------------------------------------------------------------------ 1. splits
+__global__ __launch_bounds__(256) void tree_splits_kernel(const uint64_t *__restrict__ codes, int64_t n,
+                                                          uint32_t *__restrict__ levelmask,
+                                                          uint32_t *__restrict__ split_b,
+                                                          uint32_t *__restrict__ split_e)
+{
+    int64_t s = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (s == 0) atomicOr(&levelmask[0], 1u); // the root always exists
+    if (s >= n - 1) return;
+    uint64_t ms = codes[s], mn = codes[s + 1];
+    if (ms == mn) {
+        split_e[s] = 0;
+        return;
+    }
+    int L = split_level(ms, mn);
+    int64_t b = 0, e = n;
+    if (L > 0) {
+        int sh = 64 - 2 * L;
+        b = gallop_left(codes, s, ms, sh);
+        e = gallop_right(codes, s + 1, n, ms, sh);
+    }
+    bool owner = quad_digit(codes[b], L) == quad_digit(ms, L);
+    if (owner) {
+        atomicOr(&levelmask[b], 1u << L);
+        split_b[s] = uint32_t(b);
+        split_e[s] = uint32_t(e);
+    } else {
+        split_e[s] = 0;
+    }
+}
+
+// ------------------------------------------------------------------ 2. scans
+struct ScanVal {
+    uint32_t c;
+    double x, y;
+};
+
+__device__ inline ScanVal scan_add(ScanVal a, ScanVal b) { return {a.c + b.c, a.x + b.x, a.y + b.y}; }
+
+__device__ inline ScanVal element(const uint64_t *__restrict__ codes, const uint32_t *__restrict__ levelmask,
+                                  const float2 *__restrict__ ys, int64_t x, double c0, double c1)
+{
+    uint32_t leaf = (x == 0 || codes[x - 1] != codes[x]) ? 1u : 0u;
+    float2 y = ys[x];
+    return {leaf + uint32_t(__popc(levelmask[x])), double(y.x) - c0, double(y.y) - c1};
+}
+
+// exclusive block scan of one ScanVal per thread (256 threads); returns the block total
+__device__ inline ScanVal block_scan_excl(ScanVal v, ScanVal *s_wave /*[4]*/, ScanVal *out_total)
+{
+    int lane = lane_id(), w = threadIdx.x / kWave;
+    ScanVal x = v;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        ScanVal y{__shfl_up(x.c, o, kWave), __shfl_up(x.x, o, kWave), __shfl_up(x.y, o, kWave)};
+        if (lane >= o) x = scan_add(y, x);
+    }
+    if (lane == kWave - 1) s_wave[w] = x;
+    __syncthreads();
+    ScanVal off{0, 0.0, 0.0}, tot{0, 0.0, 0.0};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        if (k < w) off = scan_add(off, s_wave[k]);
+        tot = scan_add(tot, s_wave[k]);
+    }
+    *out_total = tot;
+    // exclusive: total of earlier waves + inclusive-in-wave of the previous lane
+    ScanVal prev{__shfl_up(x.c, 1, kWave), __shfl_up(x.x, 1, kWave), __shfl_up(x.y, 1, kWave)};
+    if (lane == 0) prev = {0, 0.0, 0.0};
+    return scan_add(off, prev);
+}
+
+__global__ __launch_bounds__(kScanBlock) void scan_reduce_kernel(
+    const uint64_t *__restrict__ codes, const uint32_t *__restrict__ levelmask,
+    const float2 *__restrict__ ys, const Header *__restrict__ hdr, int64_t n,
+    uint32_t *__restrict__ tile_cnt, double2 *__restrict__ tile_sum)
+{
+    __shared__ ScanVal s_wave[4];
+    const double c0 = hdr->cent[0], c1 = hdr->cent[1];
+    int64_t first = int64_t(blockIdx.x) * kScanTile + int64_t(threadIdx.x) * kScanItems;
+    ScanVal acc{0, 0.0, 0.0};
+    for (int k = 0; k < kScanItems; ++k) {
+        int64_t x = first + k;
+        if (x < n) acc = scan_add(acc, element(codes, levelmask, ys, x, c0, c1));
+    }
+    ScanVal tot;
+    block_scan_excl(acc, s_wave, &tot);
+    if (threadIdx.x == 0) {
+        tile_cnt[blockIdx.x] = tot.c;
+        tile_sum[blockIdx.x] = make_double2(tot.x, tot.y);
+    }
+}
+
+// one block: exclusive scan over the tile totals, in place; totals -> base[n], psum[n]
+__global__ __launch_bounds__(kScanBlock) void scan_top_kernel(uint32_t *__restrict__ tile_cnt,
+                                                              double2 *__restrict__ tile_sum, int64_t tiles,
+                                                              int64_t n, uint32_t *__restrict__ base,
+                                                              double2 *__restrict__ psum,
+                                                              Header *__restrict__ hdr)
+{
+    __shared__ ScanVal s_wave[4];
+    int64_t per = (tiles + kScanBlock - 1) / kScanBlock;
+    int64_t first = int64_t(threadIdx.x) * per;
+    ScanVal acc{0, 0.0, 0.0};
+    for (int64_t k = 0; k < per; ++k) {
+        int64_t t = first + k;
+        if (t < tiles) {
+            double2 s = tile_sum[t];
+            acc = scan_add(acc, ScanVal{tile_cnt[t], s.x, s.y});
+        }
+    }
+    ScanVal tot;
+    ScanVal run = block_scan_excl(acc, s_wave, &tot);
+    for (int64_t k = 0; k < per; ++k) {
+        int64_t t = first + k;
+        if (t < tiles) {
+            double2 s = tile_sum[t];
+            ScanVal v{tile_cnt[t], s.x, s.y};
+            tile_cnt[t] = run.c;
+            tile_sum[t] = make_double2(run.x, run.y);
+            run = scan_add(run, v);
+        }
+    }
+    if (threadIdx.x == 0) {
+        base[n] = tot.c;
+        psum[n] = make_double2(tot.x, tot.y);
+        hdr->nodes = tot.c;
+    }
+}
+
+__global__ __launch_bounds__(kScanBlock) void scan_down_kernel(
+    const uint64_t *__restrict__ codes, const uint32_t *__restrict__ levelmask,
+    const float2 *__restrict__ ys, const Header *__restrict__ hdr, int64_t n,
+    const uint32_t *__restrict__ tile_cnt, const double2 *__restrict__ tile_sum,
+    uint32_t *__restrict__ base, double2 *__restrict__ psum)
+{
+    __shared__ ScanVal s_wave[4];
+    const double c0 = hdr->cent[0], c1 = hdr->cent[1];
+    int64_t first = int64_t(blockIdx.x) * kScanTile + int64_t(threadIdx.x) * kScanItems;
+    ScanVal loc[kScanItems];
+    ScanVal acc{0, 0.0, 0.0};
+#pragma unroll
+    for (int k = 0; k < kScanItems; ++k) {
+        int64_t x = first + k;
+        loc[k] = (x < n) ? element(codes, levelmask, ys, x, c0, c1) : ScanVal{0, 0.0, 0.0};
+        acc = scan_add(acc, loc[k]);
+    }
+    ScanVal tot;
+    ScanVal run = block_scan_excl(acc, s_wave, &tot);
+    double2 ts = tile_sum[blockIdx.x];
+    run = scan_add(ScanVal{tile_cnt[blockIdx.x], ts.x, ts.y}, run);
+#pragma unroll
+    for (int k = 0; k < kScanItems; ++k) {
+        int64_t x = first + k;
+        if (x < n) {
+            base[x] = run.c;
+            psum[x] = make_double2(run.x, run.y);
+        }
+        run = scan_add(run, loc[k]);
+    }
+}
+
+// ------------------------------------------------------------------ 3. nodes
+__device__ inline float accept_threshold(double rspan, int L, double theta2)
+{
+    if (!(theta2 > 0.0)) return INFINITY;
+    double side = ldexp(2.0 * rspan, -L);
+    return float(side * side / theta2);
+}
+
+// Centre of mass of the sorted points [b, e).  Small cells sum their points
+// directly (fp64, relative to the first point, so nothing cancels); larger
+// cells take the difference of the fp64 prefix sums, whose rounding error
+// divided by the count stays far below fp32 resolution.
+constexpr int64_t kDirectSum = 32;
+
+__device__ inline float2 centre_of_mass(const double2 *__restrict__ psum, const float2 *__restrict__ ys,
+                                        int64_t b, int64_t e, double c0, double c1)
+{
+    const double inv = 1.0 / double(e - b);
+    if (e - b <= kDirectSum) {
+        const float2 y0 = ys[b];
+        double sx = 0.0, sy = 0.0;
+        for (int64_t s = b + 1; s < e; ++s) {
+            const float2 y = ys[s];
+            sx += double(y.x) - double(y0.x);
+            sy += double(y.y) - double(y0.y);
+        }
+        return make_float2(float(double(y0.x) + sx * inv), float(double(y0.y) + sy * inv));
+    }
+    double2 hi = psum[e], lo = psum[b];
+    return make_float2(float(c0 + (hi.x - lo.x) * inv), float(c1 + (hi.y - lo.y) * inv));
+}
+
+__global__ __launch_bounds__(256) void tree_nodes_kernel(
+    const uint64_t *__restrict__ codes, int64_t n, const uint32_t *__restrict__ levelmask,
+    const uint32_t *__restrict__ split_b, const uint32_t *__restrict__ split_e,
+    const uint32_t *__restrict__ base, const double2 *__restrict__ psum, const float2 *__restrict__ ys,
+    Header *__restrict__ hdr, float theta, float4 *__restrict__ nodes, uint32_t *__restrict__ meta,
+    TreeDebug dbg)
+{
+    int64_t x = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (x >= n) return;
+    const double c0 = hdr->cent[0], c1 = hdr->cent[1], rspan = hdr->rspan;
+    const double theta2 = double(theta) * double(theta);
+    auto emit = [&](int64_t pre, float2 com, int64_t b, int64_t e, int L, float thr, uint32_t m, int kind) {
+        if (pre >= 2 * n) { // only reachable from a corrupted sort
+            atomicOr(&hdr->flags, kErrRange);
+            return;
+        }
+        nodes[pre] = make_float4(com.x, com.y, float(e - b), thr);
+        meta[pre] = m;
+        if (dbg.level) {
+            dbg.level[pre] = uint8_t(L);
+            dbg.kind[pre] = uint8_t(kind);
+            dbg.begin[pre] = uint32_t(b);
+            dbg.end[pre] = uint32_t(e);
+        }
+    };
+    // (a) the internal node owned by split x
+    if (x < n - 1 && split_e[x] != 0) {
+        int64_t b = split_b[x], e = split_e[x];
+        int L = split_level(codes[x], codes[x + 1]);
+        int64_t pre = base[b] + __popc(levelmask[b] & ((1u << L) - 1u));
+        emit(pre, centre_of_mass(psum, ys, b, e, c0, c1), b, e, L, accept_threshold(rspan, L, theta2), base[e],
+             0);
+    }
+    // (b) the root, when no split lies at level 0 (all points in one quadrant)
+    if (x == 0 && quad_digit(codes[0], 0) == quad_digit(codes[n - 1], 0))
+        emit(0, centre_of_mass(psum, ys, 0, n, c0, c1), 0, n, 0, accept_threshold(rspan, 0, theta2), base[n], 0);
+    // (c) the leaf that starts at x
+    if (x == 0 || codes[x - 1] != codes[x]) {
+        int64_t e = run_end(codes, x, n);
+        int64_t pre = base[x] + __popc(levelmask[x]);
+        if (e == x + 1) {
+            int lv = -1;
+            if (x > 0) lv = split_level(codes[x - 1], codes[x]);
+            if (x + 1 < n) {
+                int r = split_level(codes[x], codes[x + 1]);
+                lv = r > lv ? r : lv;
+            }
+            emit(pre, ys[x], x, e, lv + 1, -1.0f, uint32_t(x) | kLeafBit, 2);
+        } else {
+            emit(pre, centre_of_mass(psum, ys, x, e, c0, c1), x, e, 32, accept_threshold(rspan, 32, theta2),
+                 uint32_t(x) | kLeafBit, 1);
+        }
+    }
+}
+
+// ------------------------------------------------------------------ launchers
+void launch_tree(int64_t n, float theta, void *ws, const Layout &L, const TreeDebug &dbg, hipStream_t st)
+{
+    const uint64_t *codes = at<uint64_t>(ws, L.codes0);
+    uint32_t *lm = at<uint32_t>(ws, L.levelmask);
+    uint32_t *sb = at<uint32_t>(ws, L.split_b), *se = at<uint32_t>(ws, L.split_e);
+    const float2 *ys = at<float2>(ws, L.ys);
+    Header *hdr = at<Header>(ws, L.header);
+    uint32_t *base = at<uint32_t>(ws, L.base);
+    double2 *psum = at<double2>(ws, L.psum);
+    uint32_t *tc = at<uint32_t>(ws, L.scan_cnt);
+    double2 *ts = at<double2>(ws, L.scan_sum);
+    unsigned gn = unsigned((n + 255) / 256);
+    tree_splits_kernel<<<gn, 256, 0, st>>>(codes, n, lm, sb, se);
+    scan_reduce_kernel<<<unsigned(L.scan_tiles), kScanBlock, 0, st>>>(codes, lm, ys, hdr, n, tc, ts);
+    scan_top_kernel<<<1, kScanBlock, 0, st>>>(tc, ts, L.scan_tiles, n, base, psum, hdr);
+    scan_down_kernel<<<unsigned(L.scan_tiles), kScanBlock, 0, st>>>(codes, lm, ys, hdr, n, tc, ts, base, psum);
+    tree_nodes_kernel<<<gn, 256, 0, st>>>(codes, n, lm, sb, se, base, psum, ys, hdr, theta,
+                                          at<float4>(ws, L.nodes), at<uint32_t>(ws, L.meta), dbg);
+}
+
+} // namespace bht

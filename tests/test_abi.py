@@ -1,0 +1,146 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, exports
+every function declared in include/bhtsne.h, sizes workspaces, and rejects
+bad arguments before touching the device."""
+import ctypes as C
+import os
+import re
+
+import pytest
+import torch  # noqa: F401  (loads the HIP runtime the library links against)
+
+import paper_2212_11506_amd as bh
+from paper_2212_11506_amd._binding import _Csr
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    src = open(os.path.join(ROOT, "include", "bhtsne.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(bhtsne_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_function():
+    lib = bh.load_library()
+    names = _declared_functions()
+    assert "bhtsne_gradient" in names and "bhtsne_step" in names
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_library_has_gfx950_code_object():
+    data = open(bh.library_path(), "rb").read()
+    assert b"gfx950" in data
+
+
+def test_workspace_size():
+    assert bh.workspace_size(1, 0) == 0
+    assert bh.workspace_size(-5, 0) == 0
+    assert bh.workspace_size(2, -1) == 0
+    assert bh.workspace_size(1 << 26, 0) == 0
+    a = bh.workspace_size(1000, 10)
+    b = bh.workspace_size(2000, 10)
+    assert 0 < a < b
+    assert a % 256 == 0
+    # O(n) bytes: ~ a few hundred bytes per point
+    big = bh.workspace_size(1_300_000, 233_000_000)
+    assert 50 * 1_300_000 < big < 400 * 1_300_000
+
+
+def test_status_strings():
+    for s in (bh.BHTSNE_OK, bh.BHTSNE_EINVAL, bh.BHTSNE_EWORKSPACE, bh.BHTSNE_ENONFINITE,
+              bh.BHTSNE_EDEVICE):
+        assert bh.status_string(s) and bh.status_string(s) != "unknown status"
+    assert bh.status_string(12345) == "unknown status"
+
+
+FAKE = 1 << 20  # non-null, 256-aligned fake device addresses: never dereferenced on rejection
+
+
+def _grad(lib, P, theta=0.5, alpha=1.0, Y=FAKE, grad=FAKE, ws=FAKE, wsb=1 << 40):
+    return lib.bhtsne_gradient(C.c_void_p(Y) if Y else None, C.byref(P) if P is not None else None,
+                               theta, alpha, C.c_void_p(grad) if grad else None, None,
+                               C.c_void_p(ws) if ws else None, wsb, None)
+
+
+@pytest.mark.parametrize("case", ["null_P", "n1", "nnz_neg", "null_rowptr", "null_col", "null_Y",
+                                  "null_grad", "theta_neg", "theta_nan", "alpha_zero",
+                                  "alpha_inf", "too_many"])
+def test_gradient_rejects_bad_arguments(case):
+    lib = bh.load_library()
+    P = _Csr(100, 10, FAKE, FAKE, FAKE)
+    kw = {}
+    if case == "null_P":
+        P = None
+    elif case == "n1":
+        P.n = 1
+    elif case == "nnz_neg":
+        P.nnz = -1
+    elif case == "null_rowptr":
+        P.row_ptr = None
+    elif case == "null_col":
+        P.col = None
+    elif case == "null_Y":
+        kw["Y"] = 0
+    elif case == "null_grad":
+        kw["grad"] = 0
+    elif case == "theta_neg":
+        kw["theta"] = -0.1
+    elif case == "theta_nan":
+        kw["theta"] = float("nan")
+    elif case == "alpha_zero":
+        kw["alpha"] = 0.0
+    elif case == "alpha_inf":
+        kw["alpha"] = float("inf")
+    elif case == "too_many":
+        P.n = 1 << 26
+    assert _grad(lib, P, **kw) == bh.BHTSNE_EINVAL
+
+
+def test_gradient_rejects_bad_workspace():
+    lib = bh.load_library()
+    P = _Csr(100, 10, FAKE, FAKE, FAKE)
+    need = lib.bhtsne_workspace_size(100, 10)
+    assert _grad(lib, P, ws=0) == bh.BHTSNE_EWORKSPACE
+    assert _grad(lib, P, ws=FAKE + 8) == bh.BHTSNE_EWORKSPACE  # misaligned
+    assert _grad(lib, P, wsb=need - 1) == bh.BHTSNE_EWORKSPACE
+
+
+@pytest.mark.parametrize("lr,mu,mg,ok", [(0.0, 0.5, 0.01, False), (200.0, 1.0, 0.01, False),
+                                         (200.0, -0.1, 0.01, False), (200.0, 0.5, -1.0, False),
+                                         (float("nan"), 0.5, 0.01, False)])
+def test_step_rejects_bad_optimiser_arguments(lr, mu, mg, ok):
+    lib = bh.load_library()
+    P = _Csr(100, 10, FAKE, FAKE, FAKE)
+    rc = lib.bhtsne_step(C.c_void_p(FAKE), C.byref(P), 0.5, 12.0, lr, mu, mg, C.c_void_p(FAKE),
+                         C.c_void_p(FAKE), None, None, C.c_void_p(FAKE), 1 << 40, None)
+    assert rc == bh.BHTSNE_EINVAL
+
+
+def test_step_rejects_missing_state():
+    lib = bh.load_library()
+    P = _Csr(100, 10, FAKE, FAKE, FAKE)
+    rc = lib.bhtsne_step(C.c_void_p(FAKE), C.byref(P), 0.5, 12.0, 200.0, 0.5, 0.01, None,
+                         C.c_void_p(FAKE), None, None, C.c_void_p(FAKE), 1 << 40, None)
+    assert rc == bh.BHTSNE_EINVAL
+
+
+def test_debug_entry_points_reject_bad_arguments():
+    lib = bh.load_library()
+    nn = C.c_int64(0)
+    assert lib.bhtsne_debug_sort(None, 10, None, None, None, None, C.c_void_p(FAKE), 1 << 40,
+                                 None) == bh.BHTSNE_EINVAL
+    assert lib.bhtsne_debug_sort(C.c_void_p(FAKE), 1, None, None, None, None, C.c_void_p(FAKE),
+                                 1 << 40, None) == bh.BHTSNE_EINVAL
+    assert lib.bhtsne_debug_tree(C.c_void_p(FAKE), 10, 0.5, None, None, None, None, None, None,
+                                 None, C.c_void_p(FAKE), 1 << 40, None) == bh.BHTSNE_EINVAL
+    # partial set of per-node export arrays
+    assert lib.bhtsne_debug_tree(C.c_void_p(FAKE), 10, 0.5, C.byref(nn), C.c_void_p(FAKE), None,
+                                 None, None, None, None, C.c_void_p(FAKE), 1 << 40,
+                                 None) == bh.BHTSNE_EINVAL
+
+
+def test_binding_refuses_cpu_tensors():
+    with pytest.raises(ValueError):
+        bh.Csr(torch.zeros(3, dtype=torch.int64), torch.zeros(2, dtype=torch.int32),
+               torch.zeros(2, dtype=torch.float32))

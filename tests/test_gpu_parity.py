@@ -1,0 +1,314 @@
+"""GPU parity: the HIP path against the fp64 oracle on identical seeded inputs.
+
+Bars (per the method's definition and the tolerances of this build):
+  * bounding box, quantisation parameters, Morton codes, sorted order and the
+    tree topology: bit-exact;
+  * cell summaries: fp32 rounding of the oracle's fp64 centre of mass;
+  * gradient relative L2 <= 1e-4 at theta = 0 (exact) and <= 1e-3 at
+    theta > 0 (against the oracle's Barnes-Hut on the same Y);
+  * Z relative error <= 1e-5;
+  * KL after a full run within 1% of the oracle's run.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    import paper_2212_11506_amd as bh
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def rel_l2(a, b):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
+
+
+def dev_y(y):
+    return torch.from_numpy(np.ascontiguousarray(y, np.float32)).cuda()
+
+
+def dev_p(rp, col, val):
+    return bh.Csr.from_numpy(rp, col, val)
+
+
+# ------------------------------------------------------------------ edge-case embeddings
+def _case(name):
+    if name == "c0":
+        return synth.make_inputs(0).Y
+    if name.startswith("rand"):
+        n = int(name[4:])
+        return synth.random_y(n, seed=n, scale=1.0)
+    if name == "dups":
+        return synth.random_y(3000, seed=9, scale=1.0, dups=600)
+    if name == "identical":
+        return np.full((1000, 2), 0.375, np.float32)
+    if name == "identical2":
+        return np.array([[1.0, 2.0], [1.0, 2.0]], np.float32)
+    if name == "huge":
+        return synth.random_y(4000, seed=10, scale=1e35)
+    if name == "tiny":
+        return synth.random_y(4000, seed=11, scale=1e-20)
+    if name == "outlier":
+        y = synth.random_y(5000, seed=12, scale=1e-3)
+        y[17] = (1e4, -3e3)
+        return y
+    if name == "line":
+        t = np.linspace(-1, 1, 3001, dtype=np.float32)
+        return np.stack([t, t], 1)
+    if name == "late":
+        return synth.make_inputs(4, n=20000).Y
+    raise KeyError(name)
+
+
+SORT_CASES = ["c0", "rand2", "rand3", "rand63", "rand64", "rand65", "rand2047", "rand2048",
+              "rand2049", "rand4097", "rand70001", "dups", "identical", "identical2", "huge",
+              "tiny", "outlier", "line", "late"]
+
+
+@pytest.mark.parametrize("case", SORT_CASES)
+def test_morton_and_sort_bit_exact(case):
+    y = _case(case)
+    say(f"[sort] case={case} n={y.shape[0]}")
+    codes, scodes, perm, params = bh.debug_sort(dev_y(y))
+    with oracle.State(y) as s:
+        t = s.tree()
+    box = t.box
+    assert params[0:4] == [box[0], box[1], box[2], box[3]]
+    assert params[4] == box[4] and params[5] == box[5] and params[6] == box[6]
+    assert params[7] == t.yrs[0] and params[8] == t.yrs[1]
+    assert params[9] == t.yrs[2]
+    assert np.array_equal(codes.cpu().numpy().view(np.uint64), t.codes)
+    assert np.array_equal(scodes.cpu().numpy().view(np.uint64), t.sorted_codes)
+    assert np.array_equal(perm.cpu().numpy().view(np.uint32), t.perm)
+
+
+@pytest.mark.parametrize("case", SORT_CASES)
+def test_tree_and_summaries(case):
+    y = _case(case)
+    theta = 0.5
+    say(f"[tree] case={case} n={y.shape[0]}")
+    g = bh.debug_tree(dev_y(y), theta)
+    with oracle.State(y) as s:
+        t = s.tree()
+    assert g["nodes"] == t.nodes
+    assert np.array_equal(g["level"].cpu().numpy(), t.level)
+    assert np.array_equal(g["kind"].cpu().numpy(), t.kind)
+    assert np.array_equal(g["begin"].cpu().numpy().view(np.uint32), t.begin)
+    assert np.array_equal(g["end"].cpu().numpy().view(np.uint32), t.end)
+    summ = g["summary"].cpu().numpy().astype(np.float64)
+    assert np.array_equal(summ[:, 2], t.count.astype(np.float64))
+    # centre of mass: the fp32 rounding of the fp64 definition, plus (cells of more
+    # than 32 points) the rounding of a difference of two fp64 prefix sums of
+    # (y - box centre), i.e. a few ulps of sum|y - centre| spread over the count
+    err = np.abs(summ[:, :2] - t.com)
+    smax = np.abs(y.astype(np.float64) - t.box[4:6]).sum(0)
+    cnt = t.count.astype(np.float64)[:, None]
+    tol = 7e-8 * np.abs(t.com) + np.where(cnt > 32, 8 * 2.0 ** -52 * smax / cnt, 0.0) + 1e-38
+    assert np.all(err <= tol), float((err / tol).max())
+    single = t.kind == oracle.SINGLE
+    assert np.all(summ[single, 3] == -1.0)
+    side2 = (2 * t.box[6] * np.exp2(-t.level[~single].astype(np.float64))) ** 2 / theta ** 2
+    with np.errstate(over="ignore"):
+        side2_f32 = side2.astype(np.float32).astype(np.float64)  # squared lengths live in fp32
+    assert np.allclose(summ[~single, 3], side2_f32, rtol=1e-6, atol=1e-45)
+    # skip pointers: internal -> first node past the subtree, leaves -> begin | leaf bit
+    meta = g["meta"].cpu().numpy().view(np.uint32)
+    internal = t.kind == oracle.INTERNAL
+    order_end = np.searchsorted(t.begin.astype(np.int64) * 64 + t.level,
+                                t.end.astype(np.int64) * 64, side="left")
+    assert np.array_equal(meta[internal], order_end[internal].astype(np.uint32))
+    assert np.array_equal(meta[~internal], t.begin[~internal] | np.uint32(0x80000000))
+
+
+# ------------------------------------------------------------------ gradients
+def _p_for(y, seed=3, k=8):
+    return synth.random_p(y.shape[0], seed=seed, k=k)
+
+
+GRAD_CASES = ["c0", "rand2", "rand3", "rand65", "rand2049", "dups", "identical", "line", "late"]
+
+
+@pytest.mark.parametrize("case", GRAD_CASES)
+@pytest.mark.parametrize("theta", [0.0, 0.5])
+def test_gradient_parity(case, theta):
+    if case == "c0":
+        inp = synth.make_inputs(0)
+        y, (rp, col, val) = inp.Y, (inp.row_ptr, inp.col, inp.val)
+    else:
+        y = _case(case)
+        if theta == 0.0 and y.shape[0] > 5000:
+            pytest.skip("exact O(n^2) oracle limited to small n")
+        rp, col, val = _p_for(y)
+    alpha = 12.0
+    say(f"[grad] case={case} theta={theta} n={y.shape[0]} nnz={col.size}")
+    g, Z = bh.gradient(dev_y(y), dev_p(rp, col, val), theta, alpha)
+    g = g.cpu().numpy()
+    go, Zo, inter_o, nodes_o = oracle.gradient(y, rp, col, val, theta, alpha)
+    tol = 1e-4 if theta == 0.0 else 1e-3
+    if np.linalg.norm(go) == 0.0:
+        assert np.abs(g).max() <= 1e-6
+    else:
+        assert rel_l2(g, go) <= tol, rel_l2(g, go)
+    assert abs(Z - Zo) <= 1e-5 * Zo, (Z, Zo)
+
+
+@pytest.mark.parametrize("theta", [0.2, 0.8])
+def test_gradient_parity_other_angles(theta):
+    y = _case("late")
+    rp, col, val = _p_for(y, seed=5)
+    say(f"[grad-angle] theta={theta}")
+    ws = torch.empty(bh.workspace_size(y.shape[0], col.size), dtype=torch.uint8, device="cuda")
+    g, Z = bh.gradient(dev_y(y), dev_p(rp, col, val), theta, 1.0, workspace=ws)
+    stats = bh.get_stats(ws)
+    go, Zo, inter_o, nodes_o = oracle.gradient(y, rp, col, val, theta, 1.0)
+    assert rel_l2(g.cpu().numpy(), go) <= 1e-3
+    assert abs(Z - Zo) <= 1e-5 * Zo
+    assert stats["nodes"] == nodes_o
+    assert abs(stats["interactions"] - inter_o) <= 1e-3 * inter_o
+
+
+def test_theta0_against_exact_definition():
+    # theta = 0 must reproduce the exact O(n^2) gradient of the paper's equation
+    inp = synth.make_inputs(0)
+    say("[exact] c0 theta=0")
+    g, Z = bh.gradient(dev_y(inp.Y), dev_p(inp.row_ptr, inp.col, inp.val), 0.0, 1.0)
+    n = inp.n
+    Zex = oracle.z_exact(inp.Y)
+    assert abs(Z - Zex) <= 1e-5 * Zex
+    go, _, inter, _ = oracle.gradient(inp.Y, inp.row_ptr, inp.col, inp.val, 0.0, 1.0)
+    assert inter == n * (n - 1)
+    assert rel_l2(g.cpu().numpy(), go) <= 1e-4
+
+
+def test_empty_and_ragged_p():
+    n = 3000
+    y = synth.random_y(n, seed=21, scale=2.0)
+    rp, col, val = synth.random_p(n, seed=21, k=6)
+    # drop every entry touching points 0..499: those rows become empty, P stays symmetric
+    r = np.repeat(np.arange(n), np.diff(rp))
+    keep = (r >= 500) & (col >= 500)
+    counts = np.bincount(r[keep], minlength=n)
+    rp2 = np.concatenate([[0], np.cumsum(counts)]).astype(np.int64)
+    col2, val2 = col[keep], val[keep]
+    for (a, b, c) in [(rp2, col2, val2),
+                      (np.zeros(n + 1, np.int64), np.zeros(0, np.int32), np.zeros(0, np.float32))]:
+        say(f"[ragged] nnz={b.size}")
+        g, Z = bh.gradient(dev_y(y), dev_p(a, b, c), 0.5, 4.0)
+        go, Zo, _, _ = oracle.gradient(y, a, b, c, 0.5, 4.0)
+        assert rel_l2(g.cpu().numpy(), go) <= 1e-3
+        assert abs(Z - Zo) <= 1e-5 * Zo
+
+
+# ------------------------------------------------------------------ update / full runs
+def test_step_matches_update_rule():
+    inp = synth.make_inputs(0)
+    w = inp.workload
+    Y = dev_y(inp.Y)
+    P = dev_p(inp.row_ptr, inp.col, inp.val)
+    u = torch.zeros_like(Y)
+    gains = torch.ones_like(Y)
+    grad = torch.empty_like(Y)
+    y64 = inp.Y.astype(np.float64)
+    u64 = np.zeros_like(y64)
+    g64 = np.ones_like(y64)
+    for it in range(3):
+        sch = w.schedule(it)
+        say(f"[step] it={it}")
+        bh.step(Y, P, 0.5, sch["exaggeration"], sch["learning_rate"], sch["momentum"], 0.01, u,
+                gains, grad=grad)
+        gd = grad.cpu().numpy().astype(np.float64)
+        oracle.update(y64, u64, g64, gd, sch["learning_rate"], sch["momentum"], 0.01)
+        assert np.allclose(gains.cpu().numpy(), g64, rtol=1e-6, atol=0)
+        assert np.allclose(u.cpu().numpy(), u64, rtol=2e-5, atol=1e-6 * np.abs(u64).max())
+        assert np.allclose(Y.cpu().numpy(), y64, rtol=2e-5, atol=1e-6 * np.abs(y64).max())
+        # keep the fp64 replay on the GPU's state so steps stay comparable
+        y64 = Y.cpu().numpy().astype(np.float64)
+        u64 = u.cpu().numpy().astype(np.float64)
+        g64 = gains.cpu().numpy().astype(np.float64)
+
+
+def _run_gpu(inp, iters, theta):
+    w = inp.workload
+    Y = dev_y(inp.Y)
+    P = dev_p(inp.row_ptr, inp.col, inp.val)
+    u = torch.zeros_like(Y)
+    gains = torch.ones_like(Y)
+    ws = torch.empty(bh.workspace_size(inp.n, inp.nnz), dtype=torch.uint8, device="cuda")
+    for it in range(iters):
+        s = w.schedule(it)
+        bh.step(Y, P, theta, s["exaggeration"], s["learning_rate"], s["momentum"], 0.01, u, gains,
+                workspace=ws)
+    torch.cuda.synchronize()
+    return Y.cpu().numpy()
+
+
+def _run_oracle(inp, iters, theta):
+    w = inp.workload
+    y = inp.Y.astype(np.float64)
+    u = np.zeros_like(y)
+    gains = np.ones_like(y)
+    for it in range(iters):
+        s = w.schedule(it)
+        oracle.step(y, u, gains, inp.row_ptr, inp.col, inp.val, theta, s["exaggeration"],
+                    s["learning_rate"], s["momentum"], 0.01)
+    return y
+
+
+def test_full_run_kl_small_workload():
+    inp = synth.make_inputs(0)
+    say("[kl] workload 0, 50 iterations")
+    yg = _run_gpu(inp, inp.workload.iters, 0.5)
+    yo = _run_oracle(inp, inp.workload.iters, 0.5)
+    klg = oracle.kl(yg, inp.row_ptr, inp.col, inp.val)
+    klo = oracle.kl(yo, inp.row_ptr, inp.col, inp.val)
+    kl0 = oracle.kl(inp.Y, inp.row_ptr, inp.col, inp.val)
+    say(f"[kl] gpu={klg:.6f} oracle={klo:.6f} start={kl0:.6f}")
+    assert klg < kl0 and klo < kl0
+    assert abs(klg - klo) <= 0.01 * klo
+
+
+# ------------------------------------------------------------------ robustness
+def test_deterministic():
+    inp = synth.make_inputs(0)
+    Y, P = dev_y(inp.Y), dev_p(inp.row_ptr, inp.col, inp.val)
+    g1, Z1 = bh.gradient(Y, P, 0.5, 12.0)
+    g2, Z2 = bh.gradient(Y, P, 0.5, 12.0)
+    assert Z1 == Z2
+    assert torch.equal(g1, g2)
+
+
+def test_nonfinite_input_is_reported():
+    y = synth.random_y(500, seed=3)
+    y[7, 1] = np.nan
+    rp, col, val = _p_for(y)
+    with pytest.raises(bh.BhtsneError) as e:
+        bh.gradient(dev_y(y), dev_p(rp, col, val), 0.5, 1.0)
+    assert e.value.status == bh.BHTSNE_ENONFINITE
+
+
+def test_timing_records_every_phase():
+    inp = synth.make_inputs(0)
+    Y, P = dev_y(inp.Y), dev_p(inp.row_ptr, inp.col, inp.val)
+    bh.timing_read(reset=True)
+    bh.timing_enable(True)
+    try:
+        for _ in range(3):
+            bh.gradient(Y, P, 0.5, 12.0, return_z=False)
+        t = bh.timing_read(reset=True)
+    finally:
+        bh.timing_enable(False)
+    for name in bh.PHASES:
+        ms, cnt = t[name]
+        assert cnt == 3 and ms > 0.0, (name, t[name])
