@@ -172,12 +172,13 @@ __global__ __launch_bounds__(256) void attract_kernel(
                 e = e > nnz ? nnz : e;
             }
             for (int64_t k = s + sub; k < e; k += G) {
-                const int32_t j = col[k];
+                // P is streamed once per call: keep it out of the caches that hold Y
+                const int32_t j = __builtin_nontemporal_load(col + k);
                 if (uint32_t(j) >= uint32_t(n)) {
                     atomicOr(&hdr->flags, kErrRange);
                     continue;
                 }
-                const float p = val[k];
+                const float p = __builtin_nontemporal_load(val + k);
                 const float2 yj = ycopy[j];
                 const float dx = yi.x - yj.x, dy = yi.y - yj.y;
                 const float pw = p * fast_rcp(1.0f + fmaf(dx, dx, dy * dy));
@@ -224,7 +225,7 @@ void launch_attract(const int64_t *row_ptr, const int32_t *col, const float *val
                     const StepArgs &a, float *Y, float *upd, float *gains, float *grad, void *ws, const Layout &L,
                     hipStream_t st)
 {
-    constexpr int G = 16;
+    constexpr int G = 64; // one wave per row: rows hold ~100-200 entries
     int64_t blocks = (n + (256 / G) - 1) / (256 / G);
     if (blocks > 65535 * 8) blocks = 65535 * 8;
     const float2 *yc = at<float2>(ws, L.ycopy);
