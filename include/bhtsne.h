@@ -66,6 +66,17 @@ typedef struct bhtsne_csr {
     const float *val;       /* device, nnz entries (may be NULL when nnz == 0) */
 } bhtsne_csr;
 
+/* A locality layout of P: a relabelled copy that speeds up the attractive
+ * forces (Attractive Force Computation).  The struct is a host-side handle
+ * filled by bhtsne_layout_build; `mem` is caller-owned device memory of at
+ * least bhtsne_layout_size bytes that holds the copy. */
+typedef struct bhtsne_layout {
+    int64_t n, nnz;
+    void *mem;
+    size_t bytes;
+    uint64_t magic;
+} bhtsne_layout;
+
 /* Scalars of the last call on a workspace (bhtsne_get_stats). */
 typedef struct bhtsne_stats {
     double Z;             /* normaliser (ordered pairs) */
@@ -125,6 +136,37 @@ int bhtsne_gradient(const float *Y, const bhtsne_csr *P, float theta, float exag
 int bhtsne_step(float *Y, const bhtsne_csr *P, float theta, float exaggeration, float learning_rate,
                 float momentum, float min_gain, float *update, float *gains, float *grad, double *Z,
                 void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Bytes of device memory a layout of P needs (0 if n or nnz is out of range):
+ * about 8 bytes per stored entry + 16 bytes per point. */
+size_t bhtsne_layout_size(int64_t n, int64_t nnz);
+
+/* Build a locality layout of P (once per matrix; may be rebuilt as Y evolves).
+ * Points are renumbered by (connected component of P's graph, Morton code of
+ * Y); the copy stores P's rows in that order with renumbered columns, so the
+ * columns of consecutive rows fall into compact index windows.  The
+ * gradient does not depend on the order; only the speed of the attractive
+ * step does.
+ *   P      the matrix (as for bhtsne_gradient; nnz < 2^31).
+ *   Y      device, n x 2, nullable: without it points keep their index order
+ *          inside a component.
+ *   layout_mem, layout_bytes  caller device memory (256-byte aligned).
+ *   out    host handle, filled on success.
+ *   workspace  as for bhtsne_gradient (its contents are overwritten).
+ * Synchronises the stream (the component search iterates until no label
+ * changes).  Errors: BHTSNE_EINVAL, BHTSNE_EWORKSPACE, BHTSNE_EDEVICE. */
+int bhtsne_layout_build(const bhtsne_csr *P, const float *Y, void *layout_mem, size_t layout_bytes,
+                        bhtsne_layout *out, void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* bhtsne_gradient / bhtsne_step taking P through a layout built by
+ * bhtsne_layout_build (the original CSR arrays are not read).  Arguments,
+ * outputs (in the caller's point order) and errors as the plain calls;
+ * BHTSNE_EINVAL also for a handle that bhtsne_layout_build did not fill. */
+int bhtsne_gradient_layout(const float *Y, const bhtsne_layout *layout, float theta, float exaggeration,
+                           float *grad, double *Z, void *workspace, size_t workspace_bytes, hipStream_t stream);
+int bhtsne_step_layout(float *Y, const bhtsne_layout *layout, float theta, float exaggeration, float learning_rate,
+                       float momentum, float min_gain, float *update, float *gains, float *grad, double *Z,
+                       void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Copy the scalars of the last call on `workspace` to *out; synchronises
  * `stream`.  Returns BHTSNE_ENONFINITE / BHTSNE_EDEVICE when the last call

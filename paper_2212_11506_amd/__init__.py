@@ -14,10 +14,12 @@ from ._binding import (  # noqa: F401
     PHASES,
     BhtsneError,
     Csr,
+    Layout,
     debug_sort,
     debug_tree,
     get_stats,
     gradient,
+    layout_size,
     library_path,
     load_library,
     status_string,

@@ -31,6 +31,11 @@ class _Csr(C.Structure):
                 ("col", C.c_void_p), ("val", C.c_void_p)]
 
 
+class _Layout(C.Structure):
+    _fields_ = [("n", C.c_int64), ("nnz", C.c_int64), ("mem", C.c_void_p), ("bytes", C.c_size_t),
+                ("magic", C.c_uint64)]
+
+
 class _Stats(C.Structure):
     _fields_ = [("Z", C.c_double), ("interactions", C.c_int64), ("nodes", C.c_int64),
                 ("bbox", C.c_double * 4), ("r_span", C.c_double), ("device_flags", C.c_uint32)]
@@ -62,6 +67,12 @@ def load_library():
         "bhtsne_step": (C.c_int, [vp, C.POINTER(_Csr), f32, f32, f32, f32, f32, vp, vp, vp, f64p, vp,
                                   C.c_size_t, vp]),
         "bhtsne_get_stats": (C.c_int, [vp, C.POINTER(_Stats), vp]),
+        "bhtsne_layout_size": (C.c_size_t, [i64, i64]),
+        "bhtsne_layout_build": (C.c_int, [C.POINTER(_Csr), vp, vp, C.c_size_t, C.POINTER(_Layout), vp,
+                                          C.c_size_t, vp]),
+        "bhtsne_gradient_layout": (C.c_int, [vp, C.POINTER(_Layout), f32, f32, vp, f64p, vp, C.c_size_t, vp]),
+        "bhtsne_step_layout": (C.c_int, [vp, C.POINTER(_Layout), f32, f32, f32, f32, f32, vp, vp, vp, f64p, vp,
+                                         C.c_size_t, vp]),
         "bhtsne_status_string": (C.c_char_p, [C.c_int]),
         "bhtsne_timing_enable": (C.c_int, [C.c_int]),
         "bhtsne_timing_read": (C.c_int, [C.POINTER(_Timing), C.c_int]),
@@ -137,36 +148,64 @@ def _workspace(n, nnz, ws):
     return ws, need
 
 
-def gradient(Y: torch.Tensor, P: Csr, theta: float, exaggeration: float = 1.0,
+class Layout:
+    """A locality layout of P (relabelled copy in device memory) for the *_layout calls."""
+
+    def __init__(self, P: Csr, Y: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None):
+        lib = load_library()
+        self.n, self.nnz = P.n, P.nnz
+        need = int(lib.bhtsne_layout_size(P.n, P.nnz))
+        if need == 0:
+            raise BhtsneError(BHTSNE_EINVAL, "bhtsne_layout_size")
+        self.mem = torch.empty(need, dtype=torch.uint8, device="cuda")
+        ws, _ = _workspace(P.n, P.nnz, workspace)
+        self._s = _Layout()
+        rc = lib.bhtsne_layout_build(P.struct, _ptr(Y, torch.float32, "Y"), _ptr(self.mem), need,
+                                     C.byref(self._s), _ptr(ws), ws.numel(), _stream())
+        _check(rc, "bhtsne_layout_build")
+
+    @property
+    def struct(self):
+        return C.byref(self._s)
+
+
+def layout_size(n: int, nnz: int) -> int:
+    return int(load_library().bhtsne_layout_size(int(n), int(nnz)))
+
+
+def gradient(Y: torch.Tensor, P, theta: float, exaggeration: float = 1.0,
              grad: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
              return_z: bool = True):
-    """bhtsne_gradient: returns (grad, Z or None)."""
+    """bhtsne_gradient (P a Csr) or bhtsne_gradient_layout (P a Layout): returns (grad, Z or None)."""
     lib = load_library()
     if grad is None:
         grad = torch.empty_like(Y)
     ws, _ = _workspace(P.n, P.nnz, workspace)
     z = C.c_double(0.0)
-    rc = lib.bhtsne_gradient(_ptr(Y, torch.float32, "Y"), P.struct, float(theta), float(exaggeration),
+    fn = lib.bhtsne_gradient_layout if isinstance(P, Layout) else lib.bhtsne_gradient
+    rc = fn(_ptr(Y, torch.float32, "Y"), P.struct, float(theta), float(exaggeration),
                              _ptr(grad, torch.float32, "grad"), C.byref(z) if return_z else None,
                              _ptr(ws, None, "workspace"), ws.numel(), _stream())
-    _check(rc, "bhtsne_gradient")
+    _check(rc, fn.__name__)
     return grad, (z.value if return_z else None)
 
 
-def step(Y: torch.Tensor, P: Csr, theta: float, exaggeration: float, learning_rate: float,
+def step(Y: torch.Tensor, P, theta: float, exaggeration: float, learning_rate: float,
          momentum: float, min_gain: float, update: torch.Tensor, gains: torch.Tensor,
          grad: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
          return_z: bool = False):
-    """bhtsne_step: Y, update and gains are updated in place; returns Z or None."""
+    """bhtsne_step (P a Csr) or bhtsne_step_layout (P a Layout): Y, update and gains are
+    updated in place; returns Z or None."""
     lib = load_library()
     ws, _ = _workspace(P.n, P.nnz, workspace)
     z = C.c_double(0.0)
-    rc = lib.bhtsne_step(_ptr(Y, torch.float32, "Y"), P.struct, float(theta), float(exaggeration),
+    fn = lib.bhtsne_step_layout if isinstance(P, Layout) else lib.bhtsne_step
+    rc = fn(_ptr(Y, torch.float32, "Y"), P.struct, float(theta), float(exaggeration),
                          float(learning_rate), float(momentum), float(min_gain),
                          _ptr(update, torch.float32, "update"), _ptr(gains, torch.float32, "gains"),
                          _ptr(grad, torch.float32, "grad"), C.byref(z) if return_z else None,
                          _ptr(ws, None, "workspace"), ws.numel(), _stream())
-    _check(rc, "bhtsne_step")
+    _check(rc, fn.__name__)
     return z.value if return_z else None
 
 

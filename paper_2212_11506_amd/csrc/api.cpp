@@ -4,6 +4,7 @@
 
 #include <array>
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 #include <mutex>
 #include <vector>
@@ -109,18 +110,19 @@ int read_header(const void *ws, Header *h, hipStream_t st)
     return BHTSNE_OK;
 }
 
-// Steps a1..a6 of the iteration: box, codes, sort, tree and summaries.
-void build_tree(const float *Y, int64_t n, float theta, void *ws, const Layout &L, const TreeDebug &dbg,
-                hipStream_t st)
+// Box, codes, sort, tree and summaries.  `rank` (nullable) puts the private
+// copy of Y in a layout's order.
+void build_tree(const float *Y, int64_t n, float theta, const uint32_t *rank, void *ws, const Layout &L,
+                const TreeDebug &dbg, hipStream_t st)
 {
     {
         PhaseTimer pt(BHTSNE_PHASE_BBOX_MORTON, st);
         launch_bbox(Y, n, ws, L, st);
-        launch_morton(Y, n, ws, L, st);
+        launch_morton(Y, n, rank, ws, L, st);
     }
     {
         PhaseTimer pt(BHTSNE_PHASE_SORT, st);
-        launch_sort(n, ws, L, st);
+        launch_sort(n, Y, ws, L, st);
     }
     {
         PhaseTimer pt(BHTSNE_PHASE_TREE, st);
@@ -128,20 +130,8 @@ void build_tree(const float *Y, int64_t n, float theta, void *ws, const Layout &
     }
 }
 
-int run(float *Y, const bhtsne_csr *P, float theta, const StepArgs &a, float *update, float *gains, float *grad,
-        double *Z, void *ws, size_t ws_bytes, hipStream_t st)
+int finish(double *Z, void *ws, hipStream_t st)
 {
-    const int64_t n = P->n;
-    const Layout L = make_layout(n, P->nnz);
-    build_tree(Y, n, theta, ws, L, TreeDebug{}, st);
-    {
-        PhaseTimer pt(BHTSNE_PHASE_REPULSIVE, st);
-        launch_repulsive(n, ws, L, st);
-    }
-    {
-        PhaseTimer pt(BHTSNE_PHASE_ATTRACTIVE, st);
-        launch_attract(P->row_ptr, P->col, P->val, n, P->nnz, a, Y, update, gains, grad, ws, L, st);
-    }
     if (hipGetLastError() != hipSuccess) return BHTSNE_EDEVICE;
     if (Z) {
         Header h;
@@ -150,6 +140,72 @@ int run(float *Y, const bhtsne_csr *P, float theta, const StepArgs &a, float *up
         *Z = h.Z;
         return flags_status(h.flags);
     }
+    return BHTSNE_OK;
+}
+
+int run(float *Y, const bhtsne_csr *P, float theta, const StepArgs &a, float *update, float *gains, float *grad,
+        double *Z, void *ws, hipStream_t st)
+{
+    const int64_t n = P->n;
+    const Layout L = make_layout(n, P->nnz);
+    build_tree(Y, n, theta, nullptr, ws, L, TreeDebug{}, st);
+    {
+        PhaseTimer pt(BHTSNE_PHASE_REPULSIVE, st);
+        launch_repulsive(n, ws, L, st);
+    }
+    {
+        PhaseTimer pt(BHTSNE_PHASE_ATTRACTIVE, st);
+        launch_attract(P->row_ptr, P->col, P->val, n, P->nnz, a, Y, update, gains, grad, ws, L, st);
+    }
+    return finish(Z, ws, st);
+}
+
+constexpr uint64_t kLayoutMagic = 0x62687473654c3031ull; // "bhtseL01"
+
+int stage_segments()
+{
+    static int v = [] {
+        const char *e = std::getenv("BHTSNE_STAGE_SEGMENTS");
+        int x = e ? std::atoi(e) : 16;
+        return x < 0 ? 0 : x;
+    }();
+    return v;
+}
+
+int check_layout(const bhtsne_layout *lay)
+{
+    if (!lay || lay->magic != kLayoutMagic || !lay->mem || !aligned(lay->mem)) return BHTSNE_EINVAL;
+    if (lay->n < 2 || lay->n > kMaxPoints || lay->nnz < 0) return BHTSNE_EINVAL;
+    if (lay->bytes < layout_view(nullptr, lay->n, lay->nnz).bytes) return BHTSNE_EINVAL;
+    return BHTSNE_OK;
+}
+
+int run_layout(float *Y, const bhtsne_layout *lay, float theta, const StepArgs &a, float *update, float *gains,
+               float *grad, double *Z, void *ws, hipStream_t st)
+{
+    const int64_t n = lay->n;
+    const Layout L = make_layout(n, lay->nnz);
+    const LayoutView lv = layout_view(lay->mem, n, lay->nnz);
+    build_tree(Y, n, theta, lv.rank, ws, L, TreeDebug{}, st);
+    {
+        PhaseTimer pt(BHTSNE_PHASE_REPULSIVE, st);
+        launch_repulsive(n, ws, L, st);
+    }
+    {
+        PhaseTimer pt(BHTSNE_PHASE_ATTRACTIVE, st);
+        launch_attract_layout(lv, n, lay->nnz, stage_segments(), ws, L, st);
+        launch_update(lv, n, a, Y, update, gains, grad, ws, L, st);
+    }
+    return finish(Z, ws, st);
+}
+
+int check_step_args(float theta, float exaggeration, float learning_rate, float momentum, float min_gain)
+{
+    if (!finite_f(theta) || theta < 0.0f) return BHTSNE_EINVAL;
+    if (!finite_f(exaggeration) || !(exaggeration > 0.0f)) return BHTSNE_EINVAL;
+    if (!finite_f(learning_rate) || !(learning_rate > 0.0f)) return BHTSNE_EINVAL;
+    if (!finite_f(momentum) || momentum < 0.0f || !(momentum < 1.0f)) return BHTSNE_EINVAL;
+    if (!finite_f(min_gain) || min_gain < 0.0f) return BHTSNE_EINVAL;
     return BHTSNE_OK;
 }
 
@@ -174,7 +230,7 @@ int bhtsne_gradient(const float *Y, const bhtsne_csr *P, float theta, float exag
     rc = check_ws(P->n, P->nnz, workspace, workspace_bytes);
     if (rc != BHTSNE_OK) return rc;
     StepArgs a{exaggeration, 0.0f, 0.0f, 0.0f, 0};
-    return run(const_cast<float *>(Y), P, theta, a, nullptr, nullptr, grad, Z, workspace, workspace_bytes, stream);
+    return run(const_cast<float *>(Y), P, theta, a, nullptr, nullptr, grad, Z, workspace, stream);
 }
 
 int bhtsne_step(float *Y, const bhtsne_csr *P, float theta, float exaggeration, float learning_rate, float momentum,
@@ -184,15 +240,74 @@ int bhtsne_step(float *Y, const bhtsne_csr *P, float theta, float exaggeration, 
     int rc = check_csr(P);
     if (rc != BHTSNE_OK) return rc;
     if (!Y || !update || !gains) return BHTSNE_EINVAL;
-    if (!finite_f(theta) || theta < 0.0f) return BHTSNE_EINVAL;
-    if (!finite_f(exaggeration) || !(exaggeration > 0.0f)) return BHTSNE_EINVAL;
-    if (!finite_f(learning_rate) || !(learning_rate > 0.0f)) return BHTSNE_EINVAL;
-    if (!finite_f(momentum) || momentum < 0.0f || !(momentum < 1.0f)) return BHTSNE_EINVAL;
-    if (!finite_f(min_gain) || min_gain < 0.0f) return BHTSNE_EINVAL;
+    rc = check_step_args(theta, exaggeration, learning_rate, momentum, min_gain);
+    if (rc != BHTSNE_OK) return rc;
     rc = check_ws(P->n, P->nnz, workspace, workspace_bytes);
     if (rc != BHTSNE_OK) return rc;
     StepArgs a{exaggeration, learning_rate, momentum, min_gain, 1};
-    return run(Y, P, theta, a, update, gains, grad, Z, workspace, workspace_bytes, stream);
+    return run(Y, P, theta, a, update, gains, grad, Z, workspace, stream);
+}
+
+size_t bhtsne_layout_size(int64_t n, int64_t nnz)
+{
+    if (n < 2 || n > kMaxPoints || nnz < 0) return 0;
+    return layout_view(nullptr, n, nnz).bytes;
+}
+
+int bhtsne_layout_build(const bhtsne_csr *P, const float *Y, void *layout_mem, size_t layout_bytes,
+                        bhtsne_layout *out, void *workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    int rc = check_csr(P);
+    if (rc != BHTSNE_OK) return rc;
+    if (!out || !layout_mem || !aligned(layout_mem)) return BHTSNE_EINVAL;
+    if (layout_bytes < bhtsne_layout_size(P->n, P->nnz)) return BHTSNE_EINVAL;
+    // padded entries are addressed with int32 offsets
+    if (P->nnz + 3 * P->n + 4 >= (int64_t(1) << 31)) return BHTSNE_EINVAL;
+    rc = check_ws(P->n, P->nnz, workspace, workspace_bytes);
+    if (rc != BHTSNE_OK) return rc;
+    const Layout L = make_layout(P->n, P->nnz);
+    const LayoutView lv = layout_view(layout_mem, P->n, P->nnz);
+    if (launch_layout_build(P->row_ptr, P->col, P->val, P->n, P->nnz, Y, lv, workspace, L, stream) != 0)
+        return BHTSNE_EDEVICE;
+    Header h;
+    rc = read_header(workspace, &h, stream);
+    if (rc != BHTSNE_OK) return rc;
+    if (h.flags & (kErrLookback | kErrRange)) return BHTSNE_EDEVICE;
+    out->n = P->n;
+    out->nnz = P->nnz;
+    out->mem = layout_mem;
+    out->bytes = layout_bytes;
+    out->magic = kLayoutMagic;
+    return BHTSNE_OK;
+}
+
+int bhtsne_gradient_layout(const float *Y, const bhtsne_layout *layout, float theta, float exaggeration, float *grad,
+                           double *Z, void *workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    int rc = check_layout(layout);
+    if (rc != BHTSNE_OK) return rc;
+    if (!Y || !grad) return BHTSNE_EINVAL;
+    if (!finite_f(theta) || theta < 0.0f) return BHTSNE_EINVAL;
+    if (!finite_f(exaggeration) || !(exaggeration > 0.0f)) return BHTSNE_EINVAL;
+    rc = check_ws(layout->n, layout->nnz, workspace, workspace_bytes);
+    if (rc != BHTSNE_OK) return rc;
+    StepArgs a{exaggeration, 0.0f, 0.0f, 0.0f, 0};
+    return run_layout(const_cast<float *>(Y), layout, theta, a, nullptr, nullptr, grad, Z, workspace, stream);
+}
+
+int bhtsne_step_layout(float *Y, const bhtsne_layout *layout, float theta, float exaggeration, float learning_rate,
+                       float momentum, float min_gain, float *update, float *gains, float *grad, double *Z,
+                       void *workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    int rc = check_layout(layout);
+    if (rc != BHTSNE_OK) return rc;
+    if (!Y || !update || !gains) return BHTSNE_EINVAL;
+    rc = check_step_args(theta, exaggeration, learning_rate, momentum, min_gain);
+    if (rc != BHTSNE_OK) return rc;
+    rc = check_ws(layout->n, layout->nnz, workspace, workspace_bytes);
+    if (rc != BHTSNE_OK) return rc;
+    StepArgs a{exaggeration, learning_rate, momentum, min_gain, 1};
+    return run_layout(Y, layout, theta, a, update, gains, grad, Z, workspace, stream);
 }
 
 int bhtsne_get_stats(const void *workspace, bhtsne_stats *out, hipStream_t stream)
@@ -268,11 +383,11 @@ int bhtsne_debug_sort(const float *Y, int64_t n, uint64_t *codes, uint64_t *sort
     if (rc != BHTSNE_OK) return rc;
     const Layout L = make_layout(n, 0);
     launch_bbox(Y, n, workspace, L, stream);
-    launch_morton(Y, n, workspace, L, stream);
+    launch_morton(Y, n, nullptr, workspace, L, stream);
     if (codes && hipMemcpyAsync(codes, at<void>(workspace, L.codes0), 8 * size_t(n), hipMemcpyDeviceToDevice,
                                 stream) != hipSuccess)
         return BHTSNE_EDEVICE;
-    launch_sort(n, workspace, L, stream);
+    launch_sort(n, Y, workspace, L, stream);
     if (sorted_codes && hipMemcpyAsync(sorted_codes, at<void>(workspace, L.codes0), 8 * size_t(n),
                                        hipMemcpyDeviceToDevice, stream) != hipSuccess)
         return BHTSNE_EDEVICE;
@@ -307,7 +422,7 @@ int bhtsne_debug_tree(const float *Y, int64_t n, float theta, int64_t *n_nodes, 
     dbg.kind = kind;
     dbg.begin = begin;
     dbg.end = end;
-    build_tree(Y, n, theta, workspace, L, dbg, stream);
+    build_tree(Y, n, theta, nullptr, workspace, L, dbg, stream);
     if (summary && hipMemcpyAsync(summary, at<void>(workspace, L.nodes), 16 * size_t(2 * n),
                                   hipMemcpyDeviceToDevice, stream) != hipSuccess)
         return BHTSNE_EDEVICE;

@@ -24,6 +24,7 @@ constexpr int kBBoxBlocks = 512;
 constexpr int kRepBlock = 256;
 constexpr uint32_t kLeafBit = 0x80000000u;
 constexpr int64_t kMaxPoints = (int64_t(1) << 26) - 1; // node records hold counts in fp32 exactly
+constexpr int64_t kYPad = 16384 + 2;                   // padding points after the private copy of Y
 
 // Status words of the decoupled look-back: 2 flag bits + 30-bit count.
 constexpr uint32_t kFlagAggregate = 1u << 30;
@@ -62,7 +63,7 @@ struct Header {
 struct Layout {
     int64_t n, nnz, sort_tiles, scan_tiles, rep_blocks;
     size_t header, hist, bbox_part, codes0, codes1, idx0, idx1, status, ycopy, ys, levelmask,
-        split_b, split_e, base, psum, scan_cnt, scan_sum, nodes, meta, frep, zpart, ipart, total;
+        split_b, split_e, base, psum, scan_cnt, scan_sum, nodes, meta, frep, fattr, zpart, ipart, total;
 };
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -95,7 +96,8 @@ inline Layout make_layout(int64_t n, int64_t nnz)
     L.idx0 = take(4 * size_t(n));
     L.idx1 = take(4 * size_t(n));
     L.status = take(4 * size_t(kSortPasses) * kRadix * size_t(L.sort_tiles));
-    L.ycopy = take(8 * size_t(n));
+    // + one LDS segment of padding: segment loads past the last point stay inside the buffer
+    L.ycopy = take(8 * size_t(n + kYPad));
     L.ys = take(8 * size_t(n));
     L.levelmask = take(4 * size_t(n));
     L.split_b = take(4 * size_t(n));
@@ -107,6 +109,7 @@ inline Layout make_layout(int64_t n, int64_t nnz)
     L.nodes = take(16 * size_t(2 * n));
     L.meta = take(4 * size_t(2 * n));
     L.frep = take(8 * size_t(n));
+    L.fattr = take(8 * size_t(n));
     L.zpart = take(8 * size_t(L.rep_blocks));
     L.ipart = take(8 * size_t(L.rep_blocks));
     L.total = off;

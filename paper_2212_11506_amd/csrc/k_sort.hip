@@ -156,13 +156,13 @@ __device__ inline uint64_t spread_even(uint32_t v)
     return x;
 }
 
-// Codes of one tile of points, the private copy of Y, the 8 global digit
-// histograms; also clears the per-position tree masks and this tile's
+// Codes of one tile of points, the private copy of Y (in the caller's order,
+// or in a layout order when `rank` is given), the 8 global digit histograms; also clears the per-position tree masks and this tile's
 // look-back status words of every pass.
 __global__ __launch_bounds__(kSortBlock) void morton_kernel(
     const float2 *__restrict__ Y, int64_t n, const Header *__restrict__ hdr,
-    uint64_t *__restrict__ codes, float2 *__restrict__ ycopy, uint32_t *__restrict__ hist,
-    uint32_t *__restrict__ levelmask, uint32_t *__restrict__ status, int64_t tiles)
+    uint64_t *__restrict__ codes, float2 *__restrict__ ycopy, const uint32_t *__restrict__ rank,
+    uint32_t *__restrict__ hist, uint32_t *__restrict__ levelmask, uint32_t *__restrict__ status, int64_t tiles)
 {
     __shared__ uint32_t sh[kSortPasses * kRadix];
     for (int k = threadIdx.x; k < kSortPasses * kRadix; k += kSortBlock) sh[k] = 0;
@@ -179,7 +179,12 @@ __global__ __launch_bounds__(kSortBlock) void morton_kernel(
         int64_t i = base + r * kSortBlock + threadIdx.x;
         if (i < n) {
             float2 y = Y[i];
-            ycopy[i] = y;
+            if (rank) {
+                const uint32_t r = rank[i];
+                if (r < uint32_t(n)) ycopy[r] = y;
+            } else {
+                ycopy[i] = y;
+            }
             uint64_t code = spread_even(quantise(y.x, yr0, sc)) |
                             (spread_even(quantise(y.y, yr1, sc)) << 1);
             codes[i] = code;
@@ -234,7 +239,7 @@ __global__ __launch_bounds__(kSortBlock) void onesweep_kernel(
     const uint64_t *__restrict__ keys_in, const uint32_t *__restrict__ idx_in,
     uint64_t *__restrict__ keys_out, uint32_t *__restrict__ idx_out,
     uint32_t *__restrict__ status, const uint32_t *__restrict__ hist, Header *__restrict__ hdr,
-    int pass, int64_t n, const float2 *__restrict__ ycopy, float2 *__restrict__ ys)
+    int pass, int64_t n, const float2 *__restrict__ ysrc, float2 *__restrict__ ys)
 {
     constexpr int kWaves = kSortBlock / kWave;
     constexpr int kSeg = kWave * kSortItems; // keys per wave segment
@@ -342,7 +347,7 @@ __global__ __launch_bounds__(kSortBlock) void onesweep_kernel(
             keys_out[out] = k;
             uint32_t ix = s_idx[j];
             idx_out[out] = ix;
-            if (kLast) ys[out] = ix < uint32_t(n) ? ycopy[ix] : make_float2(0.0f, 0.0f);
+            if (kLast) ys[out] = ix < uint32_t(n) ? ysrc[ix] : make_float2(0.0f, 0.0f);
         } else {
             atomicOr(&hdr->flags, kErrRange);
         }
@@ -360,21 +365,21 @@ void launch_bbox(const float *Y, int64_t n, void *ws, const Layout &L, hipStream
                                          at<Header>(ws, L.header), at<uint32_t>(ws, L.hist));
 }
 
-void launch_morton(const float *Y, int64_t n, void *ws, const Layout &L, hipStream_t st)
+void launch_morton(const float *Y, int64_t n, const uint32_t *rank, void *ws, const Layout &L, hipStream_t st)
 {
     morton_kernel<<<unsigned(L.sort_tiles), kSortBlock, 0, st>>>(
         reinterpret_cast<const float2 *>(Y), n, at<Header>(ws, L.header),
-        at<uint64_t>(ws, L.codes0), at<float2>(ws, L.ycopy), at<uint32_t>(ws, L.hist),
+        at<uint64_t>(ws, L.codes0), at<float2>(ws, L.ycopy), rank, at<uint32_t>(ws, L.hist),
         at<uint32_t>(ws, L.levelmask), at<uint32_t>(ws, L.status), L.sort_tiles);
 }
 
-void launch_sort(int64_t n, void *ws, const Layout &L, hipStream_t st)
+void launch_sort(int64_t n, const float *ysrc, void *ws, const Layout &L, hipStream_t st)
 {
     uint64_t *k[2] = {at<uint64_t>(ws, L.codes0), at<uint64_t>(ws, L.codes1)};
     uint32_t *x[2] = {at<uint32_t>(ws, L.idx0), at<uint32_t>(ws, L.idx1)};
     Header *hdr = at<Header>(ws, L.header);
     const uint32_t *hist = at<uint32_t>(ws, L.hist);
-    const float2 *yc = at<float2>(ws, L.ycopy);
+    const float2 *yc = reinterpret_cast<const float2 *>(ysrc);
     float2 *ys = at<float2>(ws, L.ys);
     for (int p = 0; p < kSortPasses; ++p) {
         uint32_t *status = at<uint32_t>(ws, L.status) + int64_t(p) * L.sort_tiles * kRadix;

@@ -21,13 +21,33 @@ struct TreeDebug {
     uint32_t *end = nullptr;
 };
 
+// Device arrays of a locality layout (relabelled copy of P) inside caller memory.
+struct LayoutView {
+    uint32_t *perm = nullptr; // new position -> original index
+    uint32_t *rank = nullptr; // original index -> new position
+    int64_t *row_ptr = nullptr;
+    int32_t *col = nullptr;
+    float *val = nullptr;
+    size_t bytes = 0;
+};
+
 void launch_bbox(const float *Y, int64_t n, void *ws, const Layout &L, hipStream_t st);
-void launch_morton(const float *Y, int64_t n, void *ws, const Layout &L, hipStream_t st);
-void launch_sort(int64_t n, void *ws, const Layout &L, hipStream_t st);
+// rank (nullable): write the private copy of Y in that order instead of the caller's
+void launch_morton(const float *Y, int64_t n, const uint32_t *rank, void *ws, const Layout &L, hipStream_t st);
+// ysrc: Y in the original order, gathered into Morton order by the last pass
+void launch_sort(int64_t n, const float *ysrc, void *ws, const Layout &L, hipStream_t st);
 void launch_tree(int64_t n, float theta, void *ws, const Layout &L, const TreeDebug &dbg, hipStream_t st);
 void launch_repulsive(int64_t n, void *ws, const Layout &L, hipStream_t st);
 void launch_attract(const int64_t *row_ptr, const int32_t *col, const float *val, int64_t n, int64_t nnz,
                     const StepArgs &a, float *Y, float *upd, float *gains, float *grad, void *ws, const Layout &L,
                     hipStream_t st);
+
+LayoutView layout_view(void *mem, int64_t n, int64_t nnz);
+int launch_layout_build(const int64_t *row_ptr, const int32_t *col, const float *val, int64_t n, int64_t nnz,
+                        const float *Y, const LayoutView &lv, void *ws, const Layout &L, hipStream_t st);
+void launch_attract_layout(const LayoutView &lv, int64_t n, int64_t nnz, int max_segs, void *ws, const Layout &L,
+                           hipStream_t st);
+void launch_update(const LayoutView &lv, int64_t n, const StepArgs &a, float *Y, float *upd, float *gains, float *grad,
+                   void *ws, const Layout &L, hipStream_t st);
 
 } // namespace bht

@@ -1,0 +1,179 @@
+"""GPU tests of the locality layout of P and the LDS-staged attractive path.
+
+The layout only renumbers points, so every result must match the oracle to
+the same bars as the plain path; the layout itself must be an exact
+relabelling of P."""
+import os
+import subprocess
+import sys
+
+import numpy as np
+import pytest
+import scipy.sparse as sp
+import torch
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    import paper_2212_11506_amd as bh
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def rel_l2(a, b):
+    return float(np.linalg.norm(np.asarray(a, np.float64) - b) / np.linalg.norm(b))
+
+
+def _layout_arrays(lay):
+    """perm, rank, row_ptr, col, val of a layout, read back from device memory."""
+    n, nnz = lay.n, lay.nnz
+    mem = lay.mem.cpu().numpy()
+    off = 0
+
+    def take(nbytes, dtype, count):
+        nonlocal off
+        a = mem[off:off + nbytes].view(dtype)[:count]
+        off = (off + nbytes + 255) // 256 * 256
+        return a
+
+    cap = nnz + 3 * n + 4  # rows padded to 4-entry vectors, plus a sentinel vector
+    perm = take(4 * n, np.uint32, n)
+    rank = take(4 * n, np.uint32, n)
+    rp = take(8 * (n + 1), np.int64, n + 1)
+    col = take(4 * cap, np.int32, cap)
+    val = take(4 * cap, np.float32, cap)
+    return perm, rank, rp, col, val
+
+
+NO_COLUMN = 0x7FFFFFFF
+
+
+def _hub_p(n, seed, sizes=(300, 450, 5000)):
+    """Symmetric P whose first rows hold many more entries than the register slots
+    (and one more than the in-LDS row sort takes)."""
+    rp, col, val = synth.random_p(n, seed=seed, k=6)
+    P = sp.csr_matrix((val.astype(np.float64), col, rp), shape=(n, n))
+    rng = np.random.default_rng(seed)
+    hubs = sp.lil_matrix((n, n))
+    for h, size in enumerate(sizes):
+        others = rng.choice(np.arange(len(sizes), n), size=size, replace=False)
+        for o in others:
+            hubs[h, o] = 1e-5
+            hubs[o, h] = 1e-5
+    P = (P + hubs.tocsr()).tocsr()
+    P.sum_duplicates()
+    P.sort_indices()
+    P.data /= P.data.sum()
+    return P.indptr.astype(np.int64), P.indices.astype(np.int32), P.data.astype(np.float32)
+
+
+@pytest.mark.parametrize("with_y", [False, True])
+def test_layout_is_a_relabelling(with_y):
+    inp = synth.make_inputs(0)
+    P = bh.Csr.from_numpy(inp.row_ptr, inp.col, inp.val)
+    Y = torch.from_numpy(inp.Y).cuda()
+    say(f"[layout] build with_y={with_y}")
+    lay = bh.Layout(P, Y if with_y else None)
+    perm, rank, rp, col, val = _layout_arrays(lay)
+    n = inp.n
+    assert np.array_equal(np.sort(perm), np.arange(n, dtype=np.uint32))
+    assert np.array_equal(rank[perm], np.arange(n, dtype=np.uint32))
+    # rows start on 16-byte boundaries and end with padding entries only
+    assert np.all(rp % 4 == 0)
+    used = rp[-1]
+    assert np.all(col[used:used + 4] == NO_COLUMN) and np.all(val[used:used + 4] == 0)
+    rows = np.repeat(np.arange(n), np.diff(rp))
+    c, v = col[:used], val[:used]
+    real = c != NO_COLUMN
+    assert np.all(v[~real] == 0)
+    Po = sp.csr_matrix((inp.val, inp.col, inp.row_ptr), shape=(n, n))
+    Pn = sp.csr_matrix((v[real], (rows[real], c[real])), shape=(n, n))
+    ref = Po[perm.astype(np.int64)][:, perm.astype(np.int64)]
+    assert abs(Pn - ref).max() == 0.0
+    assert Pn.nnz == inp.nnz
+    # columns ascend within every row (padding last)
+    ok = (np.diff(c.astype(np.int64)) > 0) | (np.diff(rows) != 0) | ((c[1:] == NO_COLUMN) & (c[:-1] == NO_COLUMN))
+    assert np.all(ok)
+    # each cluster (a connected component of this P) occupies one contiguous range
+    lab = inp.labels[perm]
+    changes = np.count_nonzero(lab[1:] != lab[:-1])
+    assert changes == inp.workload.clusters - 1
+
+
+@pytest.mark.parametrize("case", ["c0", "hubs", "late"])
+@pytest.mark.parametrize("theta", [0.0, 0.5])
+def test_gradient_through_layout(case, theta):
+    if case == "c0":
+        inp = synth.make_inputs(0)
+        y, rp, col, val = inp.Y, inp.row_ptr, inp.col, inp.val
+    elif case == "hubs":
+        y = synth.random_y(6000, seed=4, scale=2.0)
+        rp, col, val = _hub_p(6000, seed=4)
+    else:
+        if theta == 0.0:
+            pytest.skip("exact O(n^2) oracle limited to small n")
+        inp = synth.make_inputs(4, n=20000)
+        y, rp, col, val = inp.Y, inp.row_ptr, inp.col, inp.val
+    say(f"[layout-grad] case={case} theta={theta} max row={np.diff(rp).max()}")
+    Y = torch.from_numpy(np.ascontiguousarray(y)).cuda()
+    P = bh.Csr.from_numpy(rp, col, val)
+    lay = bh.Layout(P, Y)
+    g, Z = bh.gradient(Y, lay, theta, 12.0)
+    go, Zo, _, _ = oracle.gradient(y, rp, col, val, theta, 12.0)
+    assert rel_l2(g.cpu().numpy(), go) <= (1e-4 if theta == 0.0 else 1e-3)
+    assert abs(Z - Zo) <= 1e-5 * Zo
+    gp, Zp = bh.gradient(Y, P, theta, 12.0)
+    assert Zp == Z  # same tree, same repulsion
+    assert rel_l2(g.cpu().numpy(), gp.cpu().numpy().astype(np.float64)) <= 1e-5
+
+
+def test_layout_steps_track_plain_steps():
+    inp = synth.make_inputs(0)
+    w = inp.workload
+    P = bh.Csr.from_numpy(inp.row_ptr, inp.col, inp.val)
+    Ya = torch.from_numpy(inp.Y).cuda()
+    Yb = Ya.clone()
+    lay = bh.Layout(P, Ya)
+    ua, ub = torch.zeros_like(Ya), torch.zeros_like(Ya)
+    ga, gb = torch.ones_like(Ya), torch.ones_like(Ya)
+    for it in range(5):
+        s = w.schedule(it)
+        bh.step(Ya, P, 0.5, s["exaggeration"], s["learning_rate"], s["momentum"], 0.01, ua, ga)
+        bh.step(Yb, lay, 0.5, s["exaggeration"], s["learning_rate"], s["momentum"], 0.01, ub, gb)
+    a, b = Ya.cpu().numpy(), Yb.cpu().numpy()
+    assert np.abs(a - b).max() <= 1e-4 * np.abs(a).max()
+
+
+def test_direct_gather_fallback_in_subprocess():
+    # with LDS staging disabled every block takes y_j straight from memory
+    code = (
+        "import sys; sys.path.insert(0, %r)\n"
+        "import numpy as np, torch, synth, oracle, paper_2212_11506_amd as bh\n"
+        "inp = synth.make_inputs(0)\n"
+        "Y = torch.from_numpy(inp.Y).cuda(); P = bh.Csr.from_numpy(inp.row_ptr, inp.col, inp.val)\n"
+        "g, Z = bh.gradient(Y, bh.Layout(P, Y), 0.5, 12.0)\n"
+        "go, Zo, _, _ = oracle.gradient(inp.Y, inp.row_ptr, inp.col, inp.val, 0.5, 12.0)\n"
+        "e = np.linalg.norm(g.cpu().numpy() - go) / np.linalg.norm(go)\n"
+        "print('relL2', e); assert e <= 1e-3 and abs(Z - Zo) <= 1e-5 * Zo\n" % ROOT)
+    env = dict(os.environ, BHTSNE_STAGE_SEGMENTS="0")
+    r = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True, timeout=300)
+    say(r.stdout, r.stderr[-2000:])
+    assert r.returncode == 0
+
+
+def test_layout_rejects_bad_handles():
+    inp = synth.make_inputs(0)
+    Y = torch.from_numpy(inp.Y).cuda()
+    P = bh.Csr.from_numpy(inp.row_ptr, inp.col, inp.val)
+    lay = bh.Layout(P, Y)
+    lay._s.magic = 0
+    with pytest.raises(bh.BhtsneError) as e:
+        bh.gradient(Y, lay, 0.5, 1.0)
+    assert e.value.status == bh.BHTSNE_EINVAL
