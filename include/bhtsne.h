@@ -197,8 +197,8 @@ int bhtsne_debug_sort(const float *Y, int64_t n, uint64_t *codes, uint64_t *sort
  * level).  Device arrays of 2n entries (summary: 2n x 4 floats {com x, com y,
  * count, threshold}), each nullable; *n_nodes (host, required) receives the
  * node count after a stream synchronisation.  kind: 0 internal, 1 bucket of
- * identical codes, 2 single point.  meta: skip index (internal nodes) or
- * begin | 0x80000000 (leaves). */
+ * identical codes, 2 single point.  meta: skip index (internal nodes),
+ * begin | 0x80000000 (buckets) or begin | 0xC0000000 (single points). */
 int bhtsne_debug_tree(const float *Y, int64_t n, float theta, int64_t *n_nodes, uint8_t *level, uint8_t *kind,
                       uint32_t *begin, uint32_t *end, float *summary, uint32_t *meta, void *workspace,
                       size_t workspace_bytes, hipStream_t stream);

@@ -22,7 +22,9 @@ constexpr int kScanItems = 16;
 constexpr int kScanTile = kScanBlock * kScanItems;
 constexpr int kBBoxBlocks = 512;
 constexpr int kRepBlock = 256;
-constexpr uint32_t kLeafBit = 0x80000000u;
+constexpr uint32_t kLeafBit = 0x80000000u;   // meta: leaf (single point or bucket)
+constexpr uint32_t kSingleBit = 0x40000000u; // meta: single-point leaf
+constexpr uint32_t kIndexMask = 0x3fffffffu; // meta: begin of a leaf
 constexpr int64_t kMaxPoints = (int64_t(1) << 26) - 1; // node records hold counts in fp32 exactly
 constexpr int64_t kYPad = 16384 + 2;                   // padding points after the private copy of Y
 
@@ -59,7 +61,8 @@ struct Header {
 //   thr = side^2 / theta^2 (+inf when theta == 0); a cell is summarised for a
 //         point at squared distance d2 iff d2 > thr.  Single points carry
 //         thr = -1 and are always taken exactly.
-//   meta = skip index (internal)  |  begin | kLeafBit (leaf)
+//   meta = skip index (internal)  |  begin | kLeafBit (bucket)
+//          | begin | kLeafBit | kSingleBit (single point)
 struct Layout {
     int64_t n, nnz, sort_tiles, scan_tiles, rep_blocks;
     size_t header, hist, bbox_part, codes0, codes1, idx0, idx1, status, ycopy, ys, levelmask,

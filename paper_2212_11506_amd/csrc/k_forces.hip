@@ -23,6 +23,8 @@ namespace bht {
 
 __device__ inline float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
 
+// One lane per point.  The branch on the node kind is wave-uniform, so single
+// points skip the acceptance test and internal cells skip the self test.
 __global__ __launch_bounds__(kRepBlock) void repulsive_kernel(
     const float4 *__restrict__ nodes, const uint32_t *__restrict__ meta, const float2 *__restrict__ ys,
     const uint32_t *__restrict__ perm, Header *__restrict__ hdr, int64_t n, float2 *__restrict__ frep,
@@ -30,76 +32,85 @@ __global__ __launch_bounds__(kRepBlock) void repulsive_kernel(
 {
     const uint32_t nb = gridDim.x;
     const uint32_t lb = xcd_contiguous(blockIdx.x, nb);
-    const int64_t si64 = int64_t(lb) * kRepBlock + threadIdx.x;
-    const bool valid = si64 < n;
-    const uint32_t si = uint32_t(si64);
-    const float2 yi = valid ? ys[si] : make_float2(0.0f, 0.0f);
+    const int w = threadIdx.x / kWave;
+    const int64_t s64 = int64_t(lb) * kRepBlock + threadIdx.x;
+    const bool valid = s64 < n;
+    const uint32_t si = uint32_t(s64);
+    const float2 yi = valid ? ys[s64] : make_float2(0.0f, 0.0f);
+    uint32_t resume = valid ? 0u : 0xffffffffu;
+    float fx = 0.0f, fy = 0.0f, z = 0.0f;
     uint32_t total = uniform(hdr->nodes);
     const uint32_t cap = uint32_t(2 * n);
     total = total < cap ? total : cap;
 
     uint32_t cur = 0;
-    uint32_t resume = valid ? 0u : 0xffffffffu;
-    float fx = 0.0f, fy = 0.0f, z = 0.0f;
-    unsigned long long inter = 0;
-
+    uint32_t cnt = 0; // this lane's interactions
     while (cur < total) {
         const float4 r = nodes[cur];
         const uint32_t m = meta[cur];
-        const float dx = yi.x - r.x, dy = yi.y - r.y;
-        const float d2 = fmaf(dx, dx, dy * dy);
-        const bool active = cur >= resume;
-        const bool leaf = (m & kLeafBit) != 0u;
-        bool take = active && (d2 > r.w);
-        if (leaf && r.w < 0.0f) take = take && ((m & ~kLeafBit) != si); // a single point, not itself
-        if (take) {
-            const float w = fast_rcp(1.0f + d2);
-            const float nw = r.z * w;
-            z += nw;
-            const float nw2 = nw * w;
-            fx = fmaf(nw2, dx, fx);
-            fy = fmaf(nw2, dy, fy);
-        }
-        inter += __popcll(ballot(take));
-        const bool rej = active && !take;
-        uint32_t nxt;
-        if (leaf) {
-            if (r.w >= 0.0f && ballot(rej)) { // bucket: its members one by one
-                const uint32_t b = m & ~kLeafBit;
-                uint32_t e = b + uint32_t(r.z);
-                e = e < uint32_t(n) ? e : uint32_t(n);
-                for (uint32_t j = b; j < e; ++j) {
-                    const float2 yj = ys[j];
-                    const bool doit = rej && j != si;
-                    if (doit) {
-                        const float ex = yi.x - yj.x, ey = yi.y - yj.y;
-                        const float w = fast_rcp(1.0f + fmaf(ex, ex, ey * ey));
-                        z += w;
-                        const float w2 = w * w;
-                        fx = fmaf(w2, ex, fx);
-                        fy = fmaf(w2, ey, fy);
-                    }
-                    inter += __popcll(ballot(doit));
-                }
+        uint32_t nxt = cur + 1;
+        if (m & kSingleBit) { // an exact pair with one point (not itself)
+            if (cur >= resume && (m & kIndexMask) != si) {
+                ++cnt;
+                const float dx = yi.x - r.x, dy = yi.y - r.y;
+                const float wgt = fast_rcp(1.0f + fmaf(dx, dx, dy * dy));
+                z += wgt;
+                const float w2 = wgt * wgt;
+                fx = fmaf(w2, dx, fx);
+                fy = fmaf(w2, dy, fy);
             }
-            nxt = cur + 1;
-        } else {
-            if (take) resume = m;
-            nxt = ballot(rej) ? cur + 1 : m;
+        } else { // a cell: summary when far enough
+            const float dx = yi.x - r.x, dy = yi.y - r.y;
+            const float d2 = fmaf(dx, dx, dy * dy);
+            const bool active = cur >= resume;
+            const bool take = active && (d2 > r.w);
+            if (take) {
+                ++cnt;
+                const float wgt = fast_rcp(1.0f + d2);
+                const float nw = r.z * wgt;
+                z += nw;
+                const float nw2 = nw * wgt;
+                fx = fmaf(nw2, dx, fx);
+                fy = fmaf(nw2, dy, fy);
+                if (!(m & kLeafBit)) resume = m; // park until the walk leaves the cell
+            }
+            const uint64_t rej = ballot(active && !take);
+            if (m & kLeafBit) {
+                if (rej) { // bucket: its members one by one
+                    const bool lrej = (rej >> lane_id()) & 1ull;
+                    const uint32_t b = m & kIndexMask;
+                    uint32_t e = b + uint32_t(r.z);
+                    e = e < uint32_t(n) ? e : uint32_t(n);
+                    for (uint32_t j = b; j < e; ++j) {
+                        const float2 yj = ys[j];
+                        if (lrej && j != si) {
+                            ++cnt;
+                            const float ex = yi.x - yj.x, ey = yi.y - yj.y;
+                            const float wgt = fast_rcp(1.0f + fmaf(ex, ex, ey * ey));
+                            z += wgt;
+                            const float w2 = wgt * wgt;
+                            fx = fmaf(w2, ex, fx);
+                            fy = fmaf(w2, ey, fy);
+                        }
+                    }
+                }
+            } else if (!rej) {
+                nxt = m;
+            }
         }
         cur = uniform(nxt > cur ? nxt : cur + 1);
     }
 
     if (valid) {
-        uint32_t p = perm[si];
+        const uint32_t p = perm[si];
         if (p < uint32_t(n)) frep[p] = make_float2(fx, fy);
     }
     // deterministic Z: wave -> block partial -> fixed-order sum in the last block
     double zw = wave_sum(double(z));
+    const unsigned long long inter = wave_sum((unsigned long long)cnt);
     __shared__ double s_z[kRepBlock / kWave];
     __shared__ unsigned long long s_i[kRepBlock / kWave];
     __shared__ bool s_last;
-    const int w = threadIdx.x / kWave;
     if (lane_id() == 0) {
         s_z[w] = zw;
         s_i[w] = inter;

@@ -345,7 +345,7 @@ __global__ __launch_bounds__(256) void tree_nodes_kernel(
                 int r = split_level(codes[x], codes[x + 1]);
                 lv = r > lv ? r : lv;
             }
-            emit(pre, ys[x], x, e, lv + 1, -1.0f, uint32_t(x) | kLeafBit, 2);
+            emit(pre, ys[x], x, e, lv + 1, -1.0f, uint32_t(x) | kLeafBit | kSingleBit, 2);
         } else {
             emit(pre, centre_of_mass(psum, ys, x, e, c0, c1), x, e, 32, accept_threshold(rspan, 32, theta2),
                  uint32_t(x) | kLeafBit, 1);

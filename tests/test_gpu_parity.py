@@ -123,13 +123,16 @@ def test_tree_and_summaries(case):
     with np.errstate(over="ignore"):
         side2_f32 = side2.astype(np.float32).astype(np.float64)  # squared lengths live in fp32
     assert np.allclose(summ[~single, 3], side2_f32, rtol=1e-6, atol=1e-45)
-    # skip pointers: internal -> first node past the subtree, leaves -> begin | leaf bit
+    # skip pointers: internal -> first node past the subtree; buckets -> begin | leaf
+    # bit; single points -> begin | leaf bit | single bit
     meta = g["meta"].cpu().numpy().view(np.uint32)
     internal = t.kind == oracle.INTERNAL
+    bucket = t.kind == oracle.BUCKET
     order_end = np.searchsorted(t.begin.astype(np.int64) * 64 + t.level,
                                 t.end.astype(np.int64) * 64, side="left")
     assert np.array_equal(meta[internal], order_end[internal].astype(np.uint32))
-    assert np.array_equal(meta[~internal], t.begin[~internal] | np.uint32(0x80000000))
+    assert np.array_equal(meta[bucket], t.begin[bucket] | np.uint32(0x80000000))
+    assert np.array_equal(meta[single], t.begin[single] | np.uint32(0xC0000000))
 
 
 # ------------------------------------------------------------------ gradients
@@ -153,9 +156,16 @@ def test_gradient_parity(case, theta):
         rp, col, val = _p_for(y)
     alpha = 12.0
     say(f"[grad] case={case} theta={theta} n={y.shape[0]} nnz={col.size}")
-    g, Z = bh.gradient(dev_y(y), dev_p(rp, col, val), theta, alpha)
+    ws = torch.empty(bh.workspace_size(y.shape[0], col.size), dtype=torch.uint8, device="cuda")
+    g, Z = bh.gradient(dev_y(y), dev_p(rp, col, val), theta, alpha, workspace=ws)
     g = g.cpu().numpy()
+    stats = bh.get_stats(ws)
     go, Zo, inter_o, nodes_o = oracle.gradient(y, rp, col, val, theta, alpha)
+    assert stats["nodes"] == nodes_o
+    if theta == 0.0:
+        assert stats["interactions"] == inter_o == y.shape[0] * (y.shape[0] - 1)
+    else:  # an acceptance may flip where fp32 and fp64 distances straddle the threshold
+        assert abs(stats["interactions"] - inter_o) <= 1e-3 * inter_o + 2
     tol = 1e-4 if theta == 0.0 else 1e-3
     if np.linalg.norm(go) == 0.0:
         assert np.abs(g).max() <= 1e-6
