@@ -78,7 +78,7 @@ def main():
         Pl = bh.Layout(P, Y0, workspace=ws)
         torch.cuda.synchronize()
         layout_s = time.perf_counter() - tl
-        log(f"[bench] layout built in {layout_s:.3f}s")
+        log(f"[bench] layout built in {layout_s:.3f}s, {Pl.tiles} column tiles")
         P = Pl
     Y = Y0.clone()
     u = torch.zeros_like(Y)
@@ -196,6 +196,7 @@ def main():
         "nodes_last": stats_last["nodes"],
         "attractive_path": "plain CSR" if args.plain else "locality layout + LDS staging",
         "layout_build_s": layout_s,
+        "layout_tiles": None if args.plain else P.tiles,
         "kernels": kernels,
         "roofline": roof,
         "cpu_baseline": cpu,

@@ -74,6 +74,8 @@ typedef struct bhtsne_layout {
     int64_t n, nnz;
     void *mem;
     size_t bytes;
+    int64_t tiles;  /* tiles of the (row block x column segment) copy; 0 = row-block path */
+    int64_t items;  /* work items of the tiled kernel (runs of tiles sharing a segment) */
     uint64_t magic;
 } bhtsne_layout;
 
@@ -138,13 +140,17 @@ int bhtsne_step(float *Y, const bhtsne_csr *P, float theta, float exaggeration, 
                 void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Bytes of device memory a layout of P needs (0 if n or nnz is out of range):
- * about 8 bytes per stored entry + 16 bytes per point. */
+ * about 14 bytes per stored entry + 220 bytes per point (a row-sorted copy
+ * and a tiled copy with 16-bit column offsets). */
 size_t bhtsne_layout_size(int64_t n, int64_t nnz);
 
 /* Build a locality layout of P (once per matrix; may be rebuilt as Y evolves).
  * Points are renumbered by (connected component of P's graph, Morton code of
  * Y); the copy stores P's rows in that order with renumbered columns, so the
- * columns of consecutive rows fall into compact index windows.  The
+ * columns of consecutive rows fall into compact index windows.  When every
+ * block of 1024 rows spans at most 16 windows of 16384 columns, a second,
+ * tiled copy groups each row's entries by window so that one window of Y in
+ * LDS serves all 1024 rows (out->tiles > 0).  The
  * gradient does not depend on the order; only the speed of the attractive
  * step does.
  *   P      the matrix (as for bhtsne_gradient; nnz < 2^31).

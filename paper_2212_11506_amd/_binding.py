@@ -33,7 +33,7 @@ class _Csr(C.Structure):
 
 class _Layout(C.Structure):
     _fields_ = [("n", C.c_int64), ("nnz", C.c_int64), ("mem", C.c_void_p), ("bytes", C.c_size_t),
-                ("magic", C.c_uint64)]
+                ("tiles", C.c_int64), ("items", C.c_int64), ("magic", C.c_uint64)]
 
 
 class _Stats(C.Structure):
@@ -163,6 +163,14 @@ class Layout:
         rc = lib.bhtsne_layout_build(P.struct, _ptr(Y, torch.float32, "Y"), _ptr(self.mem), need,
                                      C.byref(self._s), _ptr(ws), ws.numel(), _stream())
         _check(rc, "bhtsne_layout_build")
+
+    @property
+    def tiles(self) -> int:
+        return int(self._s.tiles)
+
+    @property
+    def items(self) -> int:
+        return int(self._s.items)
 
     @property
     def struct(self):

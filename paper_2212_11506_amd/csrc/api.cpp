@@ -172,11 +172,24 @@ int stage_segments()
     return v;
 }
 
+// BHTSNE_TILES=0 keeps the row-block attractive kernel (for comparisons and tests)
+bool tile_path_enabled()
+{
+    static bool v = [] {
+        const char *e = std::getenv("BHTSNE_TILES");
+        return !(e && std::atoi(e) == 0);
+    }();
+    return v;
+}
+
 int check_layout(const bhtsne_layout *lay)
 {
     if (!lay || lay->magic != kLayoutMagic || !lay->mem || !aligned(lay->mem)) return BHTSNE_EINVAL;
     if (lay->n < 2 || lay->n > kMaxPoints || lay->nnz < 0) return BHTSNE_EINVAL;
-    if (lay->bytes < layout_view(nullptr, lay->n, lay->nnz).bytes) return BHTSNE_EINVAL;
+    const LayoutView v = layout_view(nullptr, lay->n, lay->nnz);
+    if (lay->bytes < v.bytes) return BHTSNE_EINVAL;
+    if (lay->tiles < 0 || lay->tiles > v.max_tiles) return BHTSNE_EINVAL;
+    if (lay->items < 0 || lay->items > lay->tiles || (lay->tiles > 0) != (lay->items > 0)) return BHTSNE_EINVAL;
     return BHTSNE_OK;
 }
 
@@ -193,8 +206,9 @@ int run_layout(float *Y, const bhtsne_layout *lay, float theta, const StepArgs &
     }
     {
         PhaseTimer pt(BHTSNE_PHASE_ATTRACTIVE, st);
-        launch_attract_layout(lv, n, lay->nnz, stage_segments(), ws, L, st);
-        launch_update(lv, n, a, Y, update, gains, grad, ws, L, st);
+        const int tiles = int(lay->tiles);
+        launch_attract_layout(lv, n, lay->nnz, tiles, int(lay->items), stage_segments(), ws, L, st);
+        launch_update(lv, n, tiles > 0, a, Y, update, gains, grad, ws, L, st);
     }
     return finish(Z, ws, st);
 }
@@ -267,7 +281,8 @@ int bhtsne_layout_build(const bhtsne_csr *P, const float *Y, void *layout_mem, s
     if (rc != BHTSNE_OK) return rc;
     const Layout L = make_layout(P->n, P->nnz);
     const LayoutView lv = layout_view(layout_mem, P->n, P->nnz);
-    if (launch_layout_build(P->row_ptr, P->col, P->val, P->n, P->nnz, Y, lv, workspace, L, stream) != 0)
+    TilePlan plan;
+    if (launch_layout_build(P->row_ptr, P->col, P->val, P->n, P->nnz, Y, lv, &plan, workspace, L, stream) != 0)
         return BHTSNE_EDEVICE;
     Header h;
     rc = read_header(workspace, &h, stream);
@@ -277,6 +292,9 @@ int bhtsne_layout_build(const bhtsne_csr *P, const float *Y, void *layout_mem, s
     out->nnz = P->nnz;
     out->mem = layout_mem;
     out->bytes = layout_bytes;
+    const bool tiled = plan.tiled && tile_path_enabled();
+    out->tiles = tiled ? plan.tiles : 0;
+    out->items = tiled ? plan.items : 0;
     out->magic = kLayoutMagic;
     return BHTSNE_OK;
 }

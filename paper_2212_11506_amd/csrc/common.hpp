@@ -27,6 +27,13 @@ constexpr uint32_t kSingleBit = 0x40000000u; // meta: single-point leaf
 constexpr uint32_t kIndexMask = 0x3fffffffu; // meta: begin of a leaf
 constexpr int64_t kMaxPoints = (int64_t(1) << 26) - 1; // node records hold counts in fp32 exactly
 constexpr int64_t kYPad = 16384 + 2;                   // padding points after the private copy of Y
+// tiled attractive step: rows in blocks of kTileRows, columns in segments of
+// kTileSeg points; row blocks spanning more than kTileMaxSeg segments keep the
+// row-block kernel
+constexpr int kTileRows = 1024;
+constexpr int kTileSeg = 16384; // 128 KB of Y in LDS
+constexpr int kTileMaxSeg = 16;
+constexpr int kItemMaxTiles = 64; // tiles of one segment handled by one block
 
 // Status words of the decoupled look-back: 2 flag bits + 30-bit count.
 constexpr uint32_t kFlagAggregate = 1u << 30;
@@ -66,7 +73,7 @@ struct Header {
 struct Layout {
     int64_t n, nnz, sort_tiles, scan_tiles, rep_blocks;
     size_t header, hist, bbox_part, codes0, codes1, idx0, idx1, status, ycopy, ys, levelmask,
-        split_b, split_e, base, psum, scan_cnt, scan_sum, nodes, meta, frep, fattr, zpart, ipart, total;
+        split_b, split_e, base, psum, scan_cnt, scan_sum, nodes, meta, frep, fattr, partial, zpart, ipart, total;
 };
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -113,6 +120,8 @@ inline Layout make_layout(int64_t n, int64_t nnz)
     L.meta = take(4 * size_t(2 * n));
     L.frep = take(8 * size_t(n));
     L.fattr = take(8 * size_t(n));
+    // per-tile partial attractive sums: up to kTileMaxSeg tiles per row block
+    L.partial = take(8 * size_t((n + kTileRows - 1) / kTileRows) * kTileRows * kTileMaxSeg);
     L.zpart = take(8 * size_t(L.rep_blocks));
     L.ipart = take(8 * size_t(L.rep_blocks));
     L.total = off;

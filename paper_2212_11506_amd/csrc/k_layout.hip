@@ -26,6 +26,10 @@
 #include "common.hpp"
 #include "kernels.hpp"
 
+#include <algorithm>
+#include <utility>
+#include <vector>
+
 namespace bht {
 
 // ------------------------------------------------------------------ components
@@ -305,6 +309,160 @@ __global__ __launch_bounds__(256) void layout_sort_rows_kernel(const int64_t *__
     }
 }
 
+// ------------------------------------------------------------------ tiled copy
+// Segment range of each row block (its real entries' smallest and largest column).
+__global__ __launch_bounds__(256) void tile_block_range_kernel(const int64_t *__restrict__ row_ptr,
+                                                               const int32_t *__restrict__ col, int64_t n,
+                                                               int32_t *__restrict__ seg_lo, int32_t *__restrict__ nseg)
+{
+    __shared__ int s_lo[4], s_hi[4];
+    const int64_t b = blockIdx.x;
+    const int64_t r0 = b * kTileRows, r1 = (b + 1) * kTileRows < n ? (b + 1) * kTileRows : n;
+    int lo = 0x7fffffff, hi = -1;
+    for (int64_t k = row_ptr[r0] + threadIdx.x; k < row_ptr[r1]; k += blockDim.x) {
+        const int32_t c = col[k];
+        if (c != kNoColumn) {
+            lo = min(lo, c);
+            hi = max(hi, c);
+        }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        lo = min(lo, __shfl_xor(lo, o, kWave));
+        hi = max(hi, __shfl_xor(hi, o, kWave));
+    }
+    if (lane_id() == 0) {
+        s_lo[threadIdx.x / kWave] = lo;
+        s_hi[threadIdx.x / kWave] = hi;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < 4; ++w) {
+            lo = min(lo, s_lo[w]);
+            hi = max(hi, s_hi[w]);
+        }
+        lo = min(lo, s_lo[0]);
+        hi = max(hi, s_hi[0]);
+        seg_lo[b] = hi >= 0 ? lo / kTileSeg : 0;
+        nseg[b] = hi >= 0 ? hi / kTileSeg - lo / kTileSeg + 1 : 0;
+    }
+}
+
+// first position in the sorted row [a, e) whose column is >= key
+__device__ inline int64_t row_lower_bound(const int32_t *__restrict__ col, int64_t a, int64_t e, int32_t key)
+{
+    while (a < e) {
+        const int64_t m = a + (e - a) / 2;
+        if (col[m] < key)
+            a = m + 1;
+        else
+            e = m;
+    }
+    return a;
+}
+
+// Padded run length of every (row, tile) of the tiled row blocks; one wave per
+// row, one lane per segment of the row's block.  Rows past n get empty runs.
+__global__ __launch_bounds__(256) void tile_run_len_kernel(const int64_t *__restrict__ row_ptr,
+                                                           const int32_t *__restrict__ col, int64_t n, int64_t rows,
+                                                           const int32_t *__restrict__ seg_lo,
+                                                           const int32_t *__restrict__ nseg,
+                                                           const int32_t *__restrict__ blk_tiles, int32_t *__restrict__ run_len)
+{
+    const int lane = lane_id();
+    for (int64_t r = (int64_t(blockIdx.x) * blockDim.x + threadIdx.x) / kWave; r < rows;
+         r += int64_t(gridDim.x) * (blockDim.x / kWave)) {
+        const int64_t b = r / kTileRows, rl = r % kTileRows;
+        const int ns = nseg[b];
+        if (lane >= ns) continue;
+        int32_t len = 0;
+        if (r < n) {
+            const int64_t a = row_ptr[r], e = row_ptr[r + 1];
+            const int32_t s0 = (seg_lo[b] + lane) * kTileSeg;
+            const int64_t x = row_lower_bound(col, a, e, s0), y = row_lower_bound(col, a, e, s0 + kTileSeg);
+            len = int32_t((y - x + 3) & ~int64_t(3));
+        }
+        run_len[int64_t(blk_tiles[b * kTileMaxSeg + lane]) * kTileRows + rl] = len;
+    }
+}
+
+// Copy every real entry of a row into its tile run (16-bit column offset within
+// the segment), then pad each run with zero-valued entries.
+__global__ __launch_bounds__(256) void tile_copy_kernel(const int64_t *__restrict__ row_ptr,
+                                                        const int32_t *__restrict__ col, const float *__restrict__ val,
+                                                        int64_t n, const int32_t *__restrict__ seg_lo,
+                                                        const int32_t *__restrict__ nseg,
+                                                        const int32_t *__restrict__ blk_tiles,
+                                                        const int32_t *__restrict__ run_off, int64_t max_entries,
+                                                        uint16_t *__restrict__ tcol, float *__restrict__ tval)
+{
+    const int lane = lane_id();
+    for (int64_t r = (int64_t(blockIdx.x) * blockDim.x + threadIdx.x) / kWave; r < n;
+         r += int64_t(gridDim.x) * (blockDim.x / kWave)) {
+        const int64_t b = r / kTileRows, rl = r % kTileRows;
+        const int64_t a = row_ptr[r], e = row_ptr[r + 1];
+        const int32_t lo = seg_lo[b];
+        const int ns = nseg[b];
+        for (int64_t j = a + lane; j < e; j += kWave) {
+            const int32_t c = col[j];
+            if (c == kNoColumn) continue;
+            const int32_t sg = c / kTileSeg, k = sg - lo;
+            if (k < 0 || k >= ns) continue;
+            const int64_t start = row_lower_bound(col, a, e, sg * kTileSeg);
+            const int64_t d = int64_t(run_off[int64_t(blk_tiles[b * kTileMaxSeg + k]) * kTileRows + rl]) + (j - start);
+            if (d < 0 || d >= max_entries) continue;
+            tcol[d] = uint16_t(c - sg * kTileSeg);
+            tval[d] = val[j];
+        }
+        if (lane < ns) { // zero padding at the end of this row's run in segment lo + lane
+            const int64_t t = int64_t(blk_tiles[b * kTileMaxSeg + lane]) * kTileRows + rl;
+            const int32_t s0 = (lo + lane) * kTileSeg;
+            const int64_t len = row_lower_bound(col, a, e, s0 + kTileSeg) - row_lower_bound(col, a, e, s0);
+            for (int64_t d = run_off[t] + len; d < run_off[t + 1]; ++d)
+                if (d >= 0 && d < max_entries) {
+                    tcol[d] = 0;
+                    tval[d] = 0.0f;
+                }
+        }
+    }
+}
+
+// in-place exclusive scan of int32 values (totals < 2^31): tile sums, one-block scan, tile scan
+__global__ __launch_bounds__(256) void i32_reduce_kernel(const int32_t *__restrict__ in, int64_t m,
+                                                         int64_t *__restrict__ tile_sum)
+{
+    __shared__ int64_t s_wave[4];
+    const int64_t first = int64_t(blockIdx.x) * kI64Tile + int64_t(threadIdx.x) * kI64Items;
+    int64_t acc = 0;
+    for (int k = 0; k < kI64Items; ++k)
+        if (first + k < m) acc += in[first + k];
+    int64_t tot;
+    block_excl_i64(acc, s_wave, &tot);
+    if (threadIdx.x == 0) tile_sum[blockIdx.x] = tot;
+}
+
+__global__ __launch_bounds__(256) void i32_down_kernel(int32_t *__restrict__ io, int64_t m,
+                                                       const int64_t *__restrict__ tile_off)
+{
+    __shared__ int64_t s_wave[4];
+    const int64_t first = int64_t(blockIdx.x) * kI64Tile + int64_t(threadIdx.x) * kI64Items;
+    int64_t loc[kI64Items], acc = 0;
+#pragma unroll
+    for (int k = 0; k < kI64Items; ++k) {
+        loc[k] = (first + k < m) ? io[first + k] : 0;
+        acc += loc[k];
+    }
+    int64_t tot;
+    int64_t run = block_excl_i64(acc, s_wave, &tot) + tile_off[blockIdx.x];
+#pragma unroll
+    for (int k = 0; k < kI64Items; ++k) {
+        if (first + k < m) io[first + k] = int32_t(run);
+        run += loc[k];
+    }
+}
+
+__global__ void i64_to_i32_kernel(const int64_t *__restrict__ x, int32_t *__restrict__ y) { *y = int32_t(*x); }
+
 // ------------------------------------------------------------------ staged attraction
 constexpr int kAttG = 16; // lanes per row
 constexpr int kAttV = 4;  // entries per 16-byte vector slot
@@ -466,11 +624,196 @@ __global__ __launch_bounds__(kAttBlock) void attract_staged_kernel(
     }
 }
 
+// ------------------------------------------------------------------ tiled attraction
+// Tiles are stored segment-major and handed out in items: up to kItemMaxTiles
+// consecutive tiles of one segment.  One block per item puts the segment's
+// 16384 points of Y in LDS once, then each wave walks the item's tiles without
+// further barriers.  In a tile, 4-lane group g owns the adjacent rows 4g..4g+3
+// (their runs are bounded by 5 consecutive run offsets) and takes 4 entries
+// per lane and row per step (an 8-byte column load and a 16-byte value load).
+// The loads of the next step, or of the next tile's first step, are issued
+// before the current entries are summed, into the other of two register
+// buffers; run offsets and y_i are fetched one tile ahead.  Plain loads: with
+// the non-temporal hint the half-used lines left the cache before the next
+// step came back for their other half.  No load sits in
+// divergent code (finished lanes load entry 0 and discard it), so each wait
+// covers only loads issued a step earlier.  Padding entries carry p = 0.  The
+// partial sum of row rl of block b for the k-th segment of the block goes to
+// partial[(b * kTileRows + rl) * kTileMaxSeg + k]; rows add them up later in
+// a fixed order, so the result does not depend on scheduling.
+constexpr int kTileBlock = 1024;
+constexpr int kTileG = 4;                                  // lanes per row group
+constexpr int kTileRPT = kTileRows / (kTileBlock / kTileG); // rows per lane group
+constexpr int kTileStep = 4 * kTileG;                       // entries per row and step
+static_assert(kTileRPT == 4, "a group's rows are read as one 16-byte vector of run offsets");
+
+typedef uint16_t v4u16 __attribute__((ext_vector_type(4)));
+typedef int32_t v4i32 __attribute__((ext_vector_type(4)));
+
+__device__ inline float quad_sum(float x)
+{
+    // sum over the 4 lanes of a group (DPP quad permutations); every lane of
+    // the group gets the same bits since float addition commutes
+    x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xF, 0xF, false)); // [1,0,3,2]
+    x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x4E, 0xF, 0xF, false)); // [2,3,0,1]
+    return x;
+}
+
+__global__ __launch_bounds__(kTileBlock) void attract_stream_kernel(
+    const int32_t *__restrict__ item_tile0, const int32_t *__restrict__ tile_blk,
+    const int32_t *__restrict__ tile_seg, const int32_t *__restrict__ tile_k, const int32_t *__restrict__ run_off, const uint16_t *__restrict__ tcol, const float *__restrict__ tval,
+    const float2 *__restrict__ ylay, int32_t nitems, float2 *__restrict__ partial)
+{
+    __shared__ float4 sy4[kTileSeg / 2];
+    __shared__ int32_t s_blk[kItemMaxTiles], s_k[kItemMaxTiles];
+    const float2 *sy = reinterpret_cast<const float2 *>(sy4);
+    const uint32_t it = xcd_contiguous(blockIdx.x, gridDim.x);
+    if (it >= uint32_t(nitems)) return; // block-uniform, before any barrier
+    const int32_t t0 = item_tile0[it], t1 = item_tile0[it + 1];
+    const int32_t sg = tile_seg[t0];
+    const int sub = lane_id() % kTileG, grp = threadIdx.x / kTileG;
+
+    // run offsets of rows 4 grp .. 4 grp + 4 and y_i of rows 4 grp + q in tile
+    // t.  Past the item's last tile a real tile is read and never used, so no
+    // load is guarded.
+    auto fetch_rows = [&](int32_t t, int32_t blk, v4i32 &b, int32_t &b4, float2 *yi) {
+        const int32_t *ro = run_off + int64_t(t) * kTileRows + 4 * grp;
+        b = *reinterpret_cast<const v4i32 *>(ro);
+        b4 = ro[4];
+        // rows past n lie in the padding of the Y copy and have empty runs
+        const float4 *y4 = reinterpret_cast<const float4 *>(ylay + int64_t(blk) * kTileRows + 4 * grp);
+        const float4 u = y4[0], w = y4[1];
+        yi[0] = make_float2(u.x, u.y);
+        yi[1] = make_float2(u.z, u.w);
+        yi[2] = make_float2(w.x, w.y);
+        yi[3] = make_float2(w.z, w.w);
+    };
+    v4i32 rb, nrb; // run starts of the current and of the next tile
+    int32_t rb4, nrb4; // end of the last run
+    float2 yi[kTileRPT], nyi[kTileRPT];
+    fetch_rows(t0, tile_blk[t0], rb, rb4, yi);
+    {
+        const int32_t tn = t0 + 1 < t1 ? t0 + 1 : t0;
+        fetch_rows(tn, tile_blk[tn], nrb, nrb4, nyi);
+    }
+    static_assert(kYPad >= kTileSeg + 2 && kYPad >= kTileRows, "padding must cover one segment and one block");
+    // the segment of Y, 8 independent 16-byte loads per thread, in flight
+    // together with the first entries below
+    constexpr int kStage = kTileSeg / 2 / kTileBlock;
+    v4f stage[kStage];
+    {
+        const v4f *src = reinterpret_cast<const v4f *>(ylay) + int64_t(sg) * (kTileSeg / 2) + threadIdx.x;
+#pragma unroll
+        for (int q = 0; q < kStage; ++q) stage[q] = src[q * kTileBlock];
+    }
+    auto run_end = [](const v4i32 &b, int32_t b4, int q) { return q < 3 ? b[q + 1] : b4; };
+    // entry index of this lane for row q at step offset `off` (0 once past the run)
+    auto entry = [&](const v4i32 &b, int32_t b4, int q, int32_t off) {
+        const int32_t at = b[q] + off + 4 * sub;
+        return at < run_end(b, b4, q) ? at : 0;
+    };
+    // two buffers of entries, used in turn: a step sums one while the other
+    // receives the next step's loads
+    v4u16 ca[kTileRPT], cb[kTileRPT];
+    v4f pa[kTileRPT], pb[kTileRPT];
+#pragma unroll
+    for (int q = 0; q < kTileRPT; ++q) {
+        const int32_t ia = entry(rb, rb4, q, 0);
+        ca[q] = *reinterpret_cast<const v4u16 *>(tcol + ia);
+        pa[q] = *reinterpret_cast<const v4f *>(tval + ia);
+    }
+    v4f *sv = reinterpret_cast<v4f *>(sy4);
+#pragma unroll
+    for (int q = 0; q < kStage; ++q) sv[q * kTileBlock + threadIdx.x] = stage[q];
+    for (int32_t j = threadIdx.x; j < t1 - t0; j += kTileBlock) {
+        s_blk[j] = tile_blk[t0 + j];
+        s_k[j] = tile_k[t0 + j];
+    }
+    __syncthreads();
+
+    float fx[kTileRPT], fy[kTileRPT];
+#pragma unroll
+    for (int q = 0; q < kTileRPT; ++q) fx[q] = fy[q] = 0.0f;
+    int32_t off = 0; // wave-uniform offset of the current step in the tile's runs
+    // one step: loads for the next step (or the next tile's first entries)
+    // into (cn, pn), then the sum over (cc, pc); returns whether this tile
+    // has another step for any row of the wave
+    auto step = [&](const v4u16(&cc)[kTileRPT], const v4f(&pc)[kTileRPT], v4u16(&cn)[kTileRPT],
+                    v4f(&pn)[kTileRPT]) -> bool {
+        bool mine = false;
+#pragma unroll
+        for (int q = 0; q < kTileRPT; ++q) mine |= rb[q] + off + kTileStep < run_end(rb, rb4, q);
+        const bool more = __builtin_amdgcn_ballot_w64(mine) != 0; // wave-uniform
+        if (more) {
+#pragma unroll
+            for (int q = 0; q < kTileRPT; ++q) {
+                const int32_t ia = entry(rb, rb4, q, off + kTileStep);
+                cn[q] = *reinterpret_cast<const v4u16 *>(tcol + ia);
+                pn[q] = *reinterpret_cast<const v4f *>(tval + ia);
+            }
+        } else {
+#pragma unroll
+            for (int q = 0; q < kTileRPT; ++q) {
+                const int32_t ia = entry(nrb, nrb4, q, 0);
+                cn[q] = *reinterpret_cast<const v4u16 *>(tcol + ia);
+                pn[q] = *reinterpret_cast<const v4f *>(tval + ia);
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < kTileRPT; ++q) {
+            float cx = 0.0f, cy = 0.0f;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) attract_add(yi[q], sy[cc[q][v] & (kTileSeg - 1)], pc[q][v], cx, cy);
+            const bool live = rb[q] + off + 4 * sub < run_end(rb, rb4, q);
+            fx[q] += live ? cx : 0.0f;
+            fy[q] += live ? cy : 0.0f;
+        }
+        off += kTileStep;
+        return more;
+    };
+    // end of tile t: lane sub stores the partial of row 4 grp + sub, then the
+    // rows move on to tile t + 1 and the offsets of tile t + 2 are fetched
+    auto tile_end = [&](int32_t t) {
+        const int32_t j = t - t0;
+        float ax = 0.0f, ay = 0.0f;
+#pragma unroll
+        for (int q = 0; q < kTileRPT; ++q) {
+            const float sx = quad_sum(fx[q]), sy_ = quad_sum(fy[q]);
+            ax = sub == q ? sx : ax;
+            ay = sub == q ? sy_ : ay;
+            fx[q] = fy[q] = 0.0f;
+            yi[q] = nyi[q];
+        }
+        partial[(int64_t(s_blk[j]) * kTileRows + 4 * grp + sub) * kTileMaxSeg + s_k[j]] = make_float2(ax, ay);
+        rb = nrb;
+        rb4 = nrb4;
+        off = 0;
+        const int32_t tn = t + 2 < t1 ? t + 2 : t;
+        fetch_rows(tn, s_blk[tn - t0], nrb, nrb4, nyi);
+    };
+
+    // steps alternate between the buffers across tile boundaries (two per trip)
+    int32_t t = t0;
+    for (;;) {
+        if (!step(ca, pa, cb, pb)) {
+            tile_end(t);
+            if (++t == t1) break;
+        }
+        if (!step(cb, pb, ca, pa)) {
+            tile_end(t);
+            if (++t == t1) break;
+        }
+    }
+}
+
 // ------------------------------------------------------------------ gradient + update
 // In the caller's order: g = 4 (alpha F_attr - F_rep / Z), then the gains /
 // momentum update of the optimiser (when a.update).
+// F_attr of a row in layout order: either one value per row, or (tiled) the
+// sum of the row's per-tile partials in tile order.
 __global__ __launch_bounds__(256) void update_kernel(const float2 *__restrict__ fattr_lay,
-                                                     const uint32_t *__restrict__ rank,
+                                                     const uint32_t *__restrict__ rank, int tiled,
+                                                     const int32_t *__restrict__ blk_nseg,
                                                      const float2 *__restrict__ frep, const Header *__restrict__ hdr,
                                                      int64_t n, StepArgs a, float2 *__restrict__ Y,
                                                      float2 *__restrict__ upd, float2 *__restrict__ gains,
@@ -480,7 +823,19 @@ __global__ __launch_bounds__(256) void update_kernel(const float2 *__restrict__ 
     if (i >= n) return;
     const float inv_z = float(1.0 / hdr->Z);
     const uint32_t r = rank[i];
-    const float2 fa = r < uint32_t(n) ? fattr_lay[r] : make_float2(0.0f, 0.0f);
+    float2 fa = make_float2(0.0f, 0.0f);
+    if (r < uint32_t(n)) {
+        if (tiled) { // the row's partials are adjacent: [row][segment of its block]
+            const int ns = blk_nseg[r / kTileRows];
+            const float2 *q = fattr_lay + int64_t(r) * kTileMaxSeg;
+            for (int k = 0; k < ns; ++k) {
+                fa.x += q[k].x;
+                fa.y += q[k].y;
+            }
+        } else {
+            fa = fattr_lay[r];
+        }
+    }
     const float2 fr = frep[i];
     const float gx = 4.0f * (a.alpha * fa.x - fr.x * inv_z);
     const float gy = 4.0f * (a.alpha * fa.y - fr.y * inv_z);
@@ -514,6 +869,16 @@ LayoutView layout_view(void *mem, int64_t n, int64_t nnz)
     // rows are padded to multiples of 4 entries, plus one 4-entry sentinel vector at the end
     const size_t cap = size_t(nnz) + 3 * size_t(n) + 4;
     size_t o_col = take(4 * cap), o_val = take(4 * cap);
+    // tiled copy: at most kTileMaxSeg tiles per row block, runs padded to 4 entries
+    const int64_t blocks = (n + kTileRows - 1) / kTileRows;
+    v.max_tiles = blocks * kTileMaxSeg;
+    v.max_entries = nnz + 3 * int64_t(kTileRows) * v.max_tiles + 8;
+    size_t o_lo = take(4 * size_t(blocks)), o_ns = take(4 * size_t(blocks)),
+           o_bt = take(4 * size_t(blocks) * kTileMaxSeg), o_tb = take(4 * size_t(v.max_tiles)),
+           o_ts = take(4 * size_t(v.max_tiles)), o_tk = take(4 * size_t(v.max_tiles)),
+           o_it = take(4 * size_t(v.max_tiles + 1)),
+           o_ro = take(4 * size_t(v.max_tiles * kTileRows + 1)), o_tc = take(2 * size_t(v.max_entries)),
+           o_tv = take(4 * size_t(v.max_entries));
     v.bytes = off;
     if (mem) {
         v.perm = at<uint32_t>(mem, o_perm);
@@ -521,12 +886,92 @@ LayoutView layout_view(void *mem, int64_t n, int64_t nnz)
         v.row_ptr = at<int64_t>(mem, o_ptr);
         v.col = at<int32_t>(mem, o_col);
         v.val = at<float>(mem, o_val);
+        v.blk_seg_lo = at<int32_t>(mem, o_lo);
+        v.blk_nseg = at<int32_t>(mem, o_ns);
+        v.blk_tiles = at<int32_t>(mem, o_bt);
+        v.tile_blk = at<int32_t>(mem, o_tb);
+        v.tile_seg = at<int32_t>(mem, o_ts);
+        v.tile_k = at<int32_t>(mem, o_tk);
+        v.item_tile0 = at<int32_t>(mem, o_it);
+        v.run_off = at<int32_t>(mem, o_ro);
+        v.tcol = at<uint16_t>(mem, o_tc);
+        v.tval = at<float>(mem, o_tv);
     }
     return v;
 }
 
+// The tiled copy of a built (sorted, padded) layout; plan->tiled stays false when
+// some row block spans more than kTileMaxSeg segments.
+static int build_tiles(const LayoutView &lv, int64_t n, TilePlan *plan, void *ws, const Layout &L, hipStream_t st)
+{
+    *plan = TilePlan{};
+    const int64_t blocks = (n + kTileRows - 1) / kTileRows;
+    plan->blocks = int32_t(blocks);
+    tile_block_range_kernel<<<unsigned(blocks), 256, 0, st>>>(lv.row_ptr, lv.col, n, lv.blk_seg_lo, lv.blk_nseg);
+    std::vector<int32_t> lo(blocks), ns(blocks);
+    if (hipMemcpyAsync(lo.data(), lv.blk_seg_lo, 4 * blocks, hipMemcpyDeviceToHost, st) != hipSuccess) return -1;
+    if (hipMemcpyAsync(ns.data(), lv.blk_nseg, 4 * blocks, hipMemcpyDeviceToHost, st) != hipSuccess) return -1;
+    if (hipStreamSynchronize(st) != hipSuccess) return -1;
+    // tiles in segment-major order, (block, k) -> tile, then items of up to
+    // `per` tiles that never straddle a segment (a few items per CU)
+    std::vector<std::pair<int32_t, int32_t>> order; // (segment, block)
+    for (int64_t b = 0; b < blocks; ++b) {
+        if (ns[b] > kTileMaxSeg) return 0; // too wide: keep the row-block kernel
+        for (int k = 0; k < ns[b]; ++k) order.emplace_back(lo[b] + k, int32_t(b));
+    }
+    const int64_t tiles = int64_t(order.size());
+    if (tiles == 0 || tiles > lv.max_tiles) return 0;
+    std::sort(order.begin(), order.end());
+    std::vector<int32_t> bt(size_t(blocks) * kTileMaxSeg, -1), tb(tiles), ts(tiles), tk(tiles), items;
+    for (int64_t t = 0; t < tiles; ++t) {
+        ts[t] = order[t].first;
+        tb[t] = order[t].second;
+        tk[t] = ts[t] - lo[tb[t]];
+        bt[size_t(tb[t]) * kTileMaxSeg + tk[t]] = int32_t(t);
+    }
+    int dev = 0, cus = 256;
+    if (hipGetDevice(&dev) == hipSuccess)
+        (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    const int64_t per = std::min<int64_t>(kItemMaxTiles, std::max<int64_t>(1, (tiles + 4 * cus - 1) / (4 * cus)));
+    for (int64_t t = 0; t < tiles; ++t)
+        if (items.empty() || ts[t] != ts[items.back()] || t - items.back() >= per) items.push_back(int32_t(t));
+    const int64_t nitems = int64_t(items.size());
+    items.push_back(int32_t(tiles));
+    if (hipMemcpyAsync(lv.blk_tiles, bt.data(), 4 * bt.size(), hipMemcpyHostToDevice, st) != hipSuccess) return -1;
+    if (hipMemcpyAsync(lv.tile_blk, tb.data(), 4 * tiles, hipMemcpyHostToDevice, st) != hipSuccess) return -1;
+    if (hipMemcpyAsync(lv.tile_seg, ts.data(), 4 * tiles, hipMemcpyHostToDevice, st) != hipSuccess) return -1;
+    if (hipMemcpyAsync(lv.tile_k, tk.data(), 4 * tiles, hipMemcpyHostToDevice, st) != hipSuccess) return -1;
+    if (hipMemcpyAsync(lv.item_tile0, items.data(), 4 * items.size(), hipMemcpyHostToDevice, st) != hipSuccess)
+        return -1;
+    const int64_t rows = blocks * kTileRows, m = tiles * kTileRows;
+    const unsigned gw = unsigned((rows + 3) / 4 < 65535 * 4 ? (rows + 3) / 4 : 65535 * 4);
+    tile_run_len_kernel<<<gw, 256, 0, st>>>(lv.row_ptr, lv.col, n, rows, lv.blk_seg_lo, lv.blk_nseg, lv.blk_tiles,
+                                            lv.run_off);
+    const int64_t st_tiles = (m + kI64Tile - 1) / kI64Tile;
+    int64_t *tsum = at<int64_t>(ws, L.codes1); // scratch: m / 4096 + 1 entries << n
+    int64_t *total = at<int64_t>(ws, L.codes1) + st_tiles + 1;
+    i32_reduce_kernel<<<unsigned(st_tiles), 256, 0, st>>>(lv.run_off, m, tsum);
+    i64_top_kernel<<<1, 256, 0, st>>>(tsum, st_tiles, total);
+    i32_down_kernel<<<unsigned(st_tiles), 256, 0, st>>>(lv.run_off, m, tsum);
+    i64_to_i32_kernel<<<1, 1, 0, st>>>(total, lv.run_off + m);
+    int64_t entries = 0;
+    if (hipMemcpyAsync(&entries, total, 8, hipMemcpyDeviceToHost, st) != hipSuccess) return -1;
+    if (hipStreamSynchronize(st) != hipSuccess) return -1;
+    if (entries > lv.max_entries) return 0;
+    tile_copy_kernel<<<unsigned(n < 65535 * 4 ? (n + 3) / 4 : 65535 * 4), 256, 0, st>>>(
+        lv.row_ptr, lv.col, lv.val, n, lv.blk_seg_lo, lv.blk_nseg, lv.blk_tiles, lv.run_off, lv.max_entries, lv.tcol,
+        lv.tval);
+    if (hipGetLastError() != hipSuccess) return -1;
+    plan->tiled = true;
+    plan->tiles = int32_t(tiles);
+    plan->items = int32_t(nitems);
+    plan->entries = entries;
+    return 0;
+}
+
 int launch_layout_build(const int64_t *row_ptr, const int32_t *col, const float *val, int64_t n, int64_t nnz,
-                        const float *Y, const LayoutView &lv, void *ws, const Layout &L, hipStream_t st)
+                        const float *Y, const LayoutView &lv, TilePlan *plan, void *ws, const Layout &L,
+                        hipStream_t st)
 {
     Header *hdr = at<Header>(ws, L.header);
     uint32_t *parent = at<uint32_t>(ws, L.split_b);
@@ -571,7 +1016,7 @@ int launch_layout_build(const int64_t *row_ptr, const int32_t *col, const float 
     layout_sentinel_kernel<<<1, 1, 0, st>>>(lv.row_ptr, n, lv.col, lv.val);
     layout_sort_rows_kernel<<<unsigned(n < 65535 * 16 ? n : 65535 * 16), 256, 0, st>>>(lv.row_ptr, lv.col, lv.val, n);
     if (hipGetLastError() != hipSuccess) return -1;
-    return 0;
+    return build_tiles(lv, n, plan, ws, L, st);
 }
 
 template <int B, int S, int RG>
@@ -584,19 +1029,26 @@ static void launch_staged(const LayoutView &lv, int64_t n, int64_t nnz, int max_
                                                                    n, max_segs, at<float2>(ws, L.fattr));
 }
 
-void launch_attract_layout(const LayoutView &lv, int64_t n, int64_t nnz, int max_segs, void *ws, const Layout &L,
-                           hipStream_t st)
+void launch_attract_layout(const LayoutView &lv, int64_t n, int64_t nnz, int tiles, int items, int max_segs, void *ws,
+                           const Layout &L, hipStream_t st)
 {
-    (void)nnz;
+    if (tiles > 0) {
+        const unsigned grid = unsigned((items + 7) / 8 * 8); // multiple of 8 for the XCD remap
+        attract_stream_kernel<<<grid, kTileBlock, 0, st>>>(lv.item_tile0, lv.tile_blk, lv.tile_seg, lv.tile_k,
+                                                           lv.run_off, lv.tcol, lv.tval, at<float2>(ws, L.ycopy),
+                                                           items, at<float2>(ws, L.partial));
+        return;
+    }
     // 1024 threads (one block per CU: the segment fills 128 KB of LDS), 2 rows per lane group
     launch_staged<1024, 16384, 2>(lv, n, nnz, max_segs, ws, L, st);
 }
 
-void launch_update(const LayoutView &lv, int64_t n, const StepArgs &a, float *Y, float *upd, float *gains, float *grad,
-                   void *ws, const Layout &L, hipStream_t st)
+void launch_update(const LayoutView &lv, int64_t n, int tiled, const StepArgs &a, float *Y, float *upd, float *gains,
+                   float *grad, void *ws, const Layout &L, hipStream_t st)
 {
     update_kernel<<<unsigned((n + 255) / 256), 256, 0, st>>>(
-        at<float2>(ws, L.fattr), lv.rank, at<float2>(ws, L.frep), at<Header>(ws, L.header), n, a,
+        at<float2>(ws, tiled ? L.partial : L.fattr), lv.rank, tiled, lv.blk_nseg, at<float2>(ws, L.frep),
+        at<Header>(ws, L.header), n, a,
         reinterpret_cast<float2 *>(Y), reinterpret_cast<float2 *>(upd), reinterpret_cast<float2 *>(gains),
         reinterpret_cast<float2 *>(grad));
 }

@@ -28,7 +28,28 @@ struct LayoutView {
     int64_t *row_ptr = nullptr;
     int32_t *col = nullptr;
     float *val = nullptr;
+    // tiled copy: rows in blocks of kTileRows, columns in segments of kTileSeg
+    // points; one tile = (row block, segment) with each row's entries of that
+    // segment as a run padded to 4 entries (16-bit column offsets in the segment)
+    int32_t *blk_seg_lo = nullptr; // [blocks] first segment of a row block
+    int32_t *blk_nseg = nullptr;   // [blocks] segments of a row block (0: none)
+    int32_t *blk_tiles = nullptr;  // [blocks * kTileMaxSeg] tile of (row block, k-th segment)
+    int32_t *tile_blk = nullptr;   // [max tiles] row block of a tile; tiles are segment-major
+    int32_t *tile_seg = nullptr;   // [max tiles] segment of a tile
+    int32_t *tile_k = nullptr;     // [max tiles] segment of a tile counted from its block's first
+    int32_t *item_tile0 = nullptr; // [items + 1] first tile of each item (tiles of one segment)
+    int32_t *run_off = nullptr;    // [max tiles * kTileRows + 1]
+    uint16_t *tcol = nullptr;      // [max entries]
+    float *tval = nullptr;         // [max entries]
+    int64_t max_tiles = 0, max_entries = 0;
     size_t bytes = 0;
+};
+
+// Host copy of the small tile tables, filled when a layout is built.
+struct TilePlan {
+    bool tiled = false;
+    int32_t blocks = 0, tiles = 0, items = 0;
+    int64_t entries = 0;
 };
 
 void launch_bbox(const float *Y, int64_t n, void *ws, const Layout &L, hipStream_t st);
@@ -43,11 +64,15 @@ void launch_attract(const int64_t *row_ptr, const int32_t *col, const float *val
                     hipStream_t st);
 
 LayoutView layout_view(void *mem, int64_t n, int64_t nnz);
+// Builds the layout (synchronises the stream); fills *plan with the tile tables' sizes.
 int launch_layout_build(const int64_t *row_ptr, const int32_t *col, const float *val, int64_t n, int64_t nnz,
-                        const float *Y, const LayoutView &lv, void *ws, const Layout &L, hipStream_t st);
-void launch_attract_layout(const LayoutView &lv, int64_t n, int64_t nnz, int max_segs, void *ws, const Layout &L,
-                           hipStream_t st);
-void launch_update(const LayoutView &lv, int64_t n, const StepArgs &a, float *Y, float *upd, float *gains, float *grad,
-                   void *ws, const Layout &L, hipStream_t st);
+                        const float *Y, const LayoutView &lv, TilePlan *plan, void *ws, const Layout &L,
+                        hipStream_t st);
+// Attractive forces through a layout: the streaming tile kernel when the
+// layout has tiles (tiles > 0, items > 0), else the row-block kernel.
+void launch_attract_layout(const LayoutView &lv, int64_t n, int64_t nnz, int tiles, int items, int max_segs, void *ws,
+                           const Layout &L, hipStream_t st);
+void launch_update(const LayoutView &lv, int64_t n, int tiled, const StepArgs &a, float *Y, float *upd, float *gains,
+                   float *grad, void *ws, const Layout &L, hipStream_t st);
 
 } // namespace bht

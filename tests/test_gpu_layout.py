@@ -31,8 +31,12 @@ def rel_l2(a, b):
     return float(np.linalg.norm(np.asarray(a, np.float64) - b) / np.linalg.norm(b))
 
 
-def _layout_arrays(lay):
-    """perm, rank, row_ptr, col, val of a layout, read back from device memory."""
+TILE_ROWS, TILE_SEG, TILE_MAX_SEG, ITEM_MAX_TILES = 1024, 16384, 16, 64
+
+
+def _layout_arrays(lay, tiles=False):
+    """perm, rank, row_ptr, col, val of a layout (and the tile tables), read back
+    from device memory in the order the library lays them out."""
     n, nnz = lay.n, lay.nnz
     mem = lay.mem.cpu().numpy()
     off = 0
@@ -49,7 +53,24 @@ def _layout_arrays(lay):
     rp = take(8 * (n + 1), np.int64, n + 1)
     col = take(4 * cap, np.int32, cap)
     val = take(4 * cap, np.float32, cap)
-    return perm, rank, rp, col, val
+    if not tiles:
+        return perm, rank, rp, col, val
+    blocks = (n + TILE_ROWS - 1) // TILE_ROWS
+    max_tiles = blocks * TILE_MAX_SEG
+    max_entries = nnz + 3 * TILE_ROWS * max_tiles + 8
+    seg_lo = take(4 * blocks, np.int32, blocks)
+    nseg = take(4 * blocks, np.int32, blocks)
+    blk_tiles = take(4 * blocks * TILE_MAX_SEG, np.int32, blocks * TILE_MAX_SEG).reshape(blocks, TILE_MAX_SEG)
+    tile_blk = take(4 * max_tiles, np.int32, max_tiles)
+    tile_seg = take(4 * max_tiles, np.int32, max_tiles)
+    tile_k = take(4 * max_tiles, np.int32, max_tiles)
+    item_tile0 = take(4 * (max_tiles + 1), np.int32, max_tiles + 1)
+    run_off = take(4 * (max_tiles * TILE_ROWS + 1), np.int32, max_tiles * TILE_ROWS + 1)
+    tcol = take(2 * max_entries, np.uint16, max_entries)
+    tval = take(4 * max_entries, np.float32, max_entries)
+    return (perm, rank, rp, col, val), dict(seg_lo=seg_lo, nseg=nseg, blk_tiles=blk_tiles, tile_blk=tile_blk,
+                                            tile_seg=tile_seg, tile_k=tile_k, item_tile0=item_tile0,
+                                            run_off=run_off, tcol=tcol, tval=tval)
 
 
 NO_COLUMN = 0x7FFFFFFF
@@ -177,3 +198,79 @@ def test_layout_rejects_bad_handles():
     with pytest.raises(bh.BhtsneError) as e:
         bh.gradient(Y, lay, 0.5, 1.0)
     assert e.value.status == bh.BHTSNE_EINVAL
+
+
+def test_tiled_copy_reproduces_p():
+    inp = synth.make_inputs(1, n=40000)
+    P = bh.Csr.from_numpy(inp.row_ptr, inp.col, inp.val)
+    Y = torch.from_numpy(inp.Y).cuda()
+    lay = bh.Layout(P, Y)
+    n = inp.n
+    assert lay.tiles > 0
+    (perm, rank, rp, col, val), tt = _layout_arrays(lay, tiles=True)
+    T, I = lay.tiles, lay.items
+    seg_lo, nseg, tile_blk, tile_seg, run_off, tcol, tval = (tt[k] for k in (
+        "seg_lo", "nseg", "tile_blk", "tile_seg", "run_off", "tcol", "tval"))
+    blocks = (n + TILE_ROWS - 1) // TILE_ROWS
+    # tiles: every (block, segment) pair once, segment-major, indexed both ways
+    assert T == int(nseg[:blocks].sum()) and 0 < I <= T
+    pairs = list(zip(tile_seg[:T].tolist(), tile_blk[:T].tolist()))
+    assert pairs == sorted(pairs) and len(set(pairs)) == T
+    for t in range(T):
+        b = tile_blk[t]
+        k = tile_seg[t] - seg_lo[b]
+        assert 0 <= k < nseg[b] and tt["tile_k"][t] == k and tt["blk_tiles"][b, k] == t
+    # items: consecutive runs of tiles of one segment covering every tile once
+    it0 = tt["item_tile0"][:I + 1]
+    assert it0[0] == 0 and it0[-1] == T and np.all(np.diff(it0) > 0) and np.all(np.diff(it0) <= ITEM_MAX_TILES)
+    for i in range(I):
+        assert len(set(tile_seg[it0[i]:it0[i + 1]].tolist())) == 1
+    rows_l, cols_l, vals_l = [], [], []
+    for t in range(T):
+        b, sg = tile_blk[t], tile_seg[t]
+        for rl in range(TILE_ROWS):
+            a, e = run_off[t * TILE_ROWS + rl], run_off[t * TILE_ROWS + rl + 1]
+            assert a % 4 == 0 and e % 4 == 0
+            r = b * TILE_ROWS + rl
+            if e > a:
+                assert r < n
+                rows_l.append(np.full(e - a, r))
+                cols_l.append(tcol[a:e].astype(np.int64) + sg * TILE_SEG)
+                vals_l.append(tval[a:e])
+    rows_a, cols_a, vals_a = map(np.concatenate, (rows_l, cols_l, vals_l))
+    keep = vals_a != 0  # padding carries zero values
+    Pt = sp.csr_matrix((vals_a[keep], (rows_a[keep], cols_a[keep])), shape=(n, n))
+    Po = sp.csr_matrix((inp.val, inp.col, inp.row_ptr), shape=(n, n))
+    ref = Po[perm.astype(np.int64)][:, perm.astype(np.int64)]
+    assert abs(Pt - ref).max() == 0.0 and Pt.nnz == inp.nnz
+
+
+def _subprocess_gradient(env_extra, n=None, wide=False):
+    code = (
+        "import sys; sys.path.insert(0, %r)\n"
+        "import numpy as np, torch, synth, oracle, paper_2212_11506_amd as bh\n"
+        "wide = %r\n"
+        "if wide:\n"
+        "    y = synth.random_y(300000, seed=8, scale=3.0); rp, col, val = synth.random_p(300000, seed=8, k=6)\n"
+        "else:\n"
+        "    inp = synth.make_inputs(1, n=%r); y, rp, col, val = inp.Y, inp.row_ptr, inp.col, inp.val\n"
+        "Y = torch.from_numpy(y).cuda(); P = bh.Csr.from_numpy(rp, col, val)\n"
+        "lay = bh.Layout(P, Y); print('tiles', lay.tiles)\n"
+        "g, Z = bh.gradient(Y, lay, 0.5, 12.0)\n"
+        "go, Zo, _, _ = oracle.gradient(y, rp, col, val, 0.5, 12.0)\n"
+        "e = np.linalg.norm(g.cpu().numpy() - go) / np.linalg.norm(go)\n"
+        "print('relL2', e); assert e <= 1e-3 and abs(Z - Zo) <= 1e-5 * Zo\n"
+        "sys.exit(3 if lay.tiles > 0 else 4)\n" % (ROOT, wide, n))
+    env = dict(os.environ, **env_extra)
+    r = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True, timeout=300)
+    say(r.stdout, r.stderr[-2000:])
+    return r.returncode
+
+
+def test_row_block_path_when_tiles_disabled():
+    assert _subprocess_gradient({"BHTSNE_TILES": "0"}, n=40000) == 4
+
+
+def test_wide_row_blocks_fall_back_from_tiles():
+    # random columns: every block of 1024 rows spans all ~19 windows of 16384 points
+    assert _subprocess_gradient({}, wide=True) == 4
