@@ -34,6 +34,10 @@ constexpr int kTileRows = 1024;
 constexpr int kTileSeg = 16384; // 128 KB of Y in LDS
 constexpr int kTileMaxSeg = 16;
 constexpr int kItemMaxTiles = 64; // tiles of one segment handled by one block
+// sliced copy of a tile: 64 rows per slice (one per lane), chunks of 4 entries per lane
+constexpr int kSellSlice = 64;
+constexpr int kSellChunk = 4 * kSellSlice;
+constexpr int kSlicesPerTile = kTileRows / kSellSlice;
 
 // Status words of the decoupled look-back: 2 flag bits + 30-bit count.
 constexpr uint32_t kFlagAggregate = 1u << 30;

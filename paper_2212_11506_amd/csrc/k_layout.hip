@@ -361,13 +361,15 @@ __device__ inline int64_t row_lower_bound(const int32_t *__restrict__ col, int64
     return a;
 }
 
-// Padded run length of every (row, tile) of the tiled row blocks; one wave per
-// row, one lane per segment of the row's block.  Rows past n get empty runs.
+// Run length (entries in the tile's segment) of every (row, tile) of the tiled
+// row blocks; one wave per row, one lane per segment of the row's block.
+// Rows past n get empty runs.
 __global__ __launch_bounds__(256) void tile_run_len_kernel(const int64_t *__restrict__ row_ptr,
                                                            const int32_t *__restrict__ col, int64_t n, int64_t rows,
                                                            const int32_t *__restrict__ seg_lo,
                                                            const int32_t *__restrict__ nseg,
-                                                           const int32_t *__restrict__ blk_tiles, int32_t *__restrict__ run_len)
+                                                           const int32_t *__restrict__ blk_tiles,
+                                                           int32_t *__restrict__ run_len)
 {
     const int lane = lane_id();
     for (int64_t r = (int64_t(blockIdx.x) * blockDim.x + threadIdx.x) / kWave; r < rows;
@@ -379,21 +381,71 @@ __global__ __launch_bounds__(256) void tile_run_len_kernel(const int64_t *__rest
         if (r < n) {
             const int64_t a = row_ptr[r], e = row_ptr[r + 1];
             const int32_t s0 = (seg_lo[b] + lane) * kTileSeg;
-            const int64_t x = row_lower_bound(col, a, e, s0), y = row_lower_bound(col, a, e, s0 + kTileSeg);
-            len = int32_t((y - x + 3) & ~int64_t(3));
+            len = int32_t(row_lower_bound(col, a, e, s0 + kTileSeg) - row_lower_bound(col, a, e, s0));
         }
         run_len[int64_t(blk_tiles[b * kTileMaxSeg + lane]) * kTileRows + rl] = len;
     }
 }
 
-// Copy every real entry of a row into its tile run (16-bit column offset within
-// the segment), then pad each run with zero-valued entries.
-__global__ __launch_bounds__(256) void tile_copy_kernel(const int64_t *__restrict__ row_ptr,
+// Rows of each tile in order of decreasing run length (ties by row): slice j
+// of a tile is the rows at sorted positions 64 j .. 64 j + 63, and needs
+// ceil(longest run / 4) chunks.  One block of kTileRows threads per tile,
+// bitonic sort of the unique keys (16384 - length, row) in LDS.
+__global__ __launch_bounds__(kTileRows) void tile_sort_kernel(const int32_t *__restrict__ run_len,
+                                                              uint16_t *__restrict__ tperm,
+                                                              uint16_t *__restrict__ tpos,
+                                                              int32_t *__restrict__ slice_chunks)
+{
+    static_assert(kTileSeg <= 16384 && kTileRows <= 1024, "sort key packs (16384 - length) and the row in 25 bits");
+    __shared__ uint32_t key[kTileRows];
+    const int64_t t = blockIdx.x;
+    const int i = threadIdx.x;
+    const int32_t len = run_len[t * kTileRows + i];
+    key[i] = (uint32_t(kTileSeg - len) << 10) | uint32_t(i);
+    __syncthreads();
+    for (int k = 2; k <= kTileRows; k <<= 1)
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            const int o = i ^ j;
+            if (o > i) {
+                const uint32_t a = key[i], b = key[o];
+                const bool up = (i & k) == 0;
+                if ((a > b) == up) {
+                    key[i] = b;
+                    key[o] = a;
+                }
+            }
+            __syncthreads();
+        }
+    const uint32_t rl = key[i] & 1023u;
+    tperm[t * kTileRows + i] = uint16_t(rl);
+    tpos[t * kTileRows + rl] = uint16_t(i);
+    if (i % kSellSlice == 0) {
+        const int32_t longest = kTileSeg - int32_t(key[i] >> 10);
+        slice_chunks[t * kSlicesPerTile + i / kSellSlice] = (longest + 3) / 4;
+    }
+}
+
+__global__ __launch_bounds__(256) void fill_zero_kernel(uint16_t *__restrict__ tcol, float *__restrict__ tval,
+                                                        int64_t m)
+{
+    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < m; i += int64_t(gridDim.x) * blockDim.x) {
+        tcol[i] = 0;
+        tval[i] = 0.0f;
+    }
+}
+
+// Copy every real entry of a row into the sliced copy: the row sits in lane
+// (sorted position % 64) of unit (tile, sorted position / 64); its e-th entry
+// in the segment goes to chunk e / 4, element e % 4 of that lane.  Everything
+// else was zeroed (padding carries p = 0).
+__global__ __launch_bounds__(256) void sell_copy_kernel(const int64_t *__restrict__ row_ptr,
                                                         const int32_t *__restrict__ col, const float *__restrict__ val,
                                                         int64_t n, const int32_t *__restrict__ seg_lo,
                                                         const int32_t *__restrict__ nseg,
                                                         const int32_t *__restrict__ blk_tiles,
-                                                        const int32_t *__restrict__ run_off, int64_t max_entries,
+                                                        const uint16_t *__restrict__ tpos,
+                                                        const int32_t *__restrict__ unit_of,
+                                                        const int32_t *__restrict__ unit_chunk0, int64_t max_entries,
                                                         uint16_t *__restrict__ tcol, float *__restrict__ tval)
 {
     const int lane = lane_id();
@@ -408,60 +460,17 @@ __global__ __launch_bounds__(256) void tile_copy_kernel(const int64_t *__restric
             if (c == kNoColumn) continue;
             const int32_t sg = c / kTileSeg, k = sg - lo;
             if (k < 0 || k >= ns) continue;
-            const int64_t start = row_lower_bound(col, a, e, sg * kTileSeg);
-            const int64_t d = int64_t(run_off[int64_t(blk_tiles[b * kTileMaxSeg + k]) * kTileRows + rl]) + (j - start);
+            const int64_t t = blk_tiles[b * kTileMaxSeg + k];
+            const int32_t pos = tpos[t * kTileRows + rl];
+            const int32_t u = unit_of[t * kSlicesPerTile + pos / kSellSlice];
+            const int64_t ei = j - row_lower_bound(col, a, e, sg * kTileSeg);
+            const int64_t d = (int64_t(unit_chunk0[u]) + ei / 4) * kSellChunk + (pos % kSellSlice) * 4 + ei % 4;
             if (d < 0 || d >= max_entries) continue;
             tcol[d] = uint16_t(c - sg * kTileSeg);
             tval[d] = val[j];
         }
-        if (lane < ns) { // zero padding at the end of this row's run in segment lo + lane
-            const int64_t t = int64_t(blk_tiles[b * kTileMaxSeg + lane]) * kTileRows + rl;
-            const int32_t s0 = (lo + lane) * kTileSeg;
-            const int64_t len = row_lower_bound(col, a, e, s0 + kTileSeg) - row_lower_bound(col, a, e, s0);
-            for (int64_t d = run_off[t] + len; d < run_off[t + 1]; ++d)
-                if (d >= 0 && d < max_entries) {
-                    tcol[d] = 0;
-                    tval[d] = 0.0f;
-                }
-        }
     }
 }
-
-// in-place exclusive scan of int32 values (totals < 2^31): tile sums, one-block scan, tile scan
-__global__ __launch_bounds__(256) void i32_reduce_kernel(const int32_t *__restrict__ in, int64_t m,
-                                                         int64_t *__restrict__ tile_sum)
-{
-    __shared__ int64_t s_wave[4];
-    const int64_t first = int64_t(blockIdx.x) * kI64Tile + int64_t(threadIdx.x) * kI64Items;
-    int64_t acc = 0;
-    for (int k = 0; k < kI64Items; ++k)
-        if (first + k < m) acc += in[first + k];
-    int64_t tot;
-    block_excl_i64(acc, s_wave, &tot);
-    if (threadIdx.x == 0) tile_sum[blockIdx.x] = tot;
-}
-
-__global__ __launch_bounds__(256) void i32_down_kernel(int32_t *__restrict__ io, int64_t m,
-                                                       const int64_t *__restrict__ tile_off)
-{
-    __shared__ int64_t s_wave[4];
-    const int64_t first = int64_t(blockIdx.x) * kI64Tile + int64_t(threadIdx.x) * kI64Items;
-    int64_t loc[kI64Items], acc = 0;
-#pragma unroll
-    for (int k = 0; k < kI64Items; ++k) {
-        loc[k] = (first + k < m) ? io[first + k] : 0;
-        acc += loc[k];
-    }
-    int64_t tot;
-    int64_t run = block_excl_i64(acc, s_wave, &tot) + tile_off[blockIdx.x];
-#pragma unroll
-    for (int k = 0; k < kI64Items; ++k) {
-        if (first + k < m) io[first + k] = int32_t(run);
-        run += loc[k];
-    }
-}
-
-__global__ void i64_to_i32_kernel(const int64_t *__restrict__ x, int32_t *__restrict__ y) { *y = int32_t(*x); }
 
 // ------------------------------------------------------------------ staged attraction
 constexpr int kAttG = 16; // lanes per row
@@ -625,80 +634,61 @@ __global__ __launch_bounds__(kAttBlock) void attract_staged_kernel(
 }
 
 // ------------------------------------------------------------------ tiled attraction
-// Tiles are stored segment-major and handed out in items: up to kItemMaxTiles
-// consecutive tiles of one segment.  One block per item puts the segment's
-// 16384 points of Y in LDS once, then each wave walks the item's tiles without
-// further barriers.  In a tile, 4-lane group g owns the adjacent rows 4g..4g+3
-// (their runs are bounded by 5 consecutive run offsets) and takes 4 entries
-// per lane and row per step (an 8-byte column load and a 16-byte value load).
-// The loads of the next step, or of the next tile's first step, are issued
-// before the current entries are summed, into the other of two register
-// buffers; run offsets and y_i are fetched one tile ahead.  Plain loads: with
-// the non-temporal hint the half-used lines left the cache before the next
-// step came back for their other half.  No load sits in
-// divergent code (finished lanes load entry 0 and discard it), so each wait
-// covers only loads issued a step earlier.  Padding entries carry p = 0.  The
-// partial sum of row rl of block b for the k-th segment of the block goes to
-// partial[(b * kTileRows + rl) * kTileMaxSeg + k]; rows add them up later in
-// a fixed order, so the result does not depend on scheduling.
+// The tiled copy is sliced: a unit is 64 rows of one tile (a slice, one row
+// per lane, rows sorted by run length so that a slice's runs are alike) and
+// holds ceil(longest run / 4) chunks; chunk k stores entries 4k .. 4k + 3 of
+// every lane's row, so a wave reads each chunk as one contiguous 512-byte
+// column block and one 1-KB value block.  Tiles are stored segment-major and
+// handed out in items (up to kItemMaxTiles tiles of one segment).  One block
+// per item puts the segment's 16384 points of Y in LDS once; each of its 16
+// waves then streams its own units, whose chunks the layout stores back to
+// back (units are dealt to waves longest first).  Chunk loads run
+// kSellRing ahead of the sums in a ring of registers, across unit
+// boundaries; a unit's row numbers and y_i are fetched two and one units
+// ahead.  Each lane sums its own row, so the partial of a (row, tile) is
+// formed in a fixed order; it goes to partial[row * kTileMaxSeg + k] (k: the
+// tile's segment counted from its block's first) and rows add their partials
+// later in a fixed order.
 constexpr int kTileBlock = 1024;
-constexpr int kTileG = 4;                                  // lanes per row group
-constexpr int kTileRPT = kTileRows / (kTileBlock / kTileG); // rows per lane group
-constexpr int kTileStep = 4 * kTileG;                       // entries per row and step
-static_assert(kTileRPT == 4, "a group's rows are read as one 16-byte vector of run offsets");
+constexpr int kSellRing = 4;
+constexpr int kSellWaves = kTileBlock / kWave;
+constexpr int kItemMaxUnits = kItemMaxTiles * kSlicesPerTile;
 
 typedef uint16_t v4u16 __attribute__((ext_vector_type(4)));
-typedef int32_t v4i32 __attribute__((ext_vector_type(4)));
 
-__device__ inline float quad_sum(float x)
+__global__ __launch_bounds__(kTileBlock) void attract_sell_kernel(
+    const int32_t *__restrict__ item_tile0, const int4 *__restrict__ item_units, const int4 *__restrict__ wave_units,
+    const int32_t *__restrict__ tile_blk, const int32_t *__restrict__ tile_seg, const int32_t *__restrict__ tile_k,
+    const int32_t *__restrict__ unit_chunks, const int32_t *__restrict__ unit_tj, const uint16_t *__restrict__ tperm,
+    const uint16_t *__restrict__ tcol, const float *__restrict__ tval, const float2 *__restrict__ ylay,
+    int32_t nitems, float2 *__restrict__ partial)
 {
-    // sum over the 4 lanes of a group (DPP quad permutations); every lane of
-    // the group gets the same bits since float addition commutes
-    x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xF, 0xF, false)); // [1,0,3,2]
-    x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x4E, 0xF, 0xF, false)); // [2,3,0,1]
-    return x;
-}
-
-__global__ __launch_bounds__(kTileBlock) void attract_stream_kernel(
-    const int32_t *__restrict__ item_tile0, const int32_t *__restrict__ tile_blk,
-    const int32_t *__restrict__ tile_seg, const int32_t *__restrict__ tile_k, const int32_t *__restrict__ run_off, const uint16_t *__restrict__ tcol, const float *__restrict__ tval,
-    const float2 *__restrict__ ylay, int32_t nitems, float2 *__restrict__ partial)
-{
-    __shared__ float4 sy4[kTileSeg / 2];
-    __shared__ int32_t s_blk[kItemMaxTiles], s_k[kItemMaxTiles];
+    __shared__ v4f sy4[kTileSeg / 2];
+    __shared__ int32_t s_row0[kItemMaxTiles], s_k[kItemMaxTiles];
+    __shared__ int32_t s_K[kItemMaxUnits], s_tj[kItemMaxUnits];
     const float2 *sy = reinterpret_cast<const float2 *>(sy4);
     const uint32_t it = xcd_contiguous(blockIdx.x, gridDim.x);
-    if (it >= uint32_t(nitems)) return; // block-uniform, before any barrier
+    if (it >= uint32_t(nitems)) return; // block-uniform, before the barrier
     const int32_t t0 = item_tile0[it], t1 = item_tile0[it + 1];
     const int32_t sg = tile_seg[t0];
-    const int sub = lane_id() % kTileG, grp = threadIdx.x / kTileG;
+    const int4 iu = item_units[it]; // units [x, z) of the item; those from y on have no entries
+    const int w = __builtin_amdgcn_readfirstlane(int(threadIdx.x) / kWave), lane = lane_id();
+    const int4 wu = wave_units[int64_t(it) * kSellWaves + w]; // units [x, y), chunks [z, z + w)
+    const int32_t G = wu.w;
 
-    // run offsets of rows 4 grp .. 4 grp + 4 and y_i of rows 4 grp + q in tile
-    // t.  Past the item's last tile a real tile is read and never used, so no
-    // load is guarded.
-    auto fetch_rows = [&](int32_t t, int32_t blk, v4i32 &b, int32_t &b4, float2 *yi) {
-        const int32_t *ro = run_off + int64_t(t) * kTileRows + 4 * grp;
-        b = *reinterpret_cast<const v4i32 *>(ro);
-        b4 = ro[4];
-        // rows past n lie in the padding of the Y copy and have empty runs
-        const float4 *y4 = reinterpret_cast<const float4 *>(ylay + int64_t(blk) * kTileRows + 4 * grp);
-        const float4 u = y4[0], w = y4[1];
-        yi[0] = make_float2(u.x, u.y);
-        yi[1] = make_float2(u.z, u.w);
-        yi[2] = make_float2(w.x, w.y);
-        yi[3] = make_float2(w.z, w.w);
+    // this wave's chunk g (clamped: loads past the end are issued and unused)
+    const uint16_t *tc = tcol + int64_t(wu.z) * kSellChunk + 4 * lane;
+    const float *tv = tval + int64_t(wu.z) * kSellChunk + 4 * lane;
+    v4u16 c[kSellRing];
+    v4f p[kSellRing];
+    auto issue = [&](int x, int32_t g) {
+        const int64_t at = int64_t(g < G ? g : (G > 0 ? G - 1 : 0)) * kSellChunk;
+        c[x] = *reinterpret_cast<const v4u16 *>(tc + at);
+        p[x] = *reinterpret_cast<const v4f *>(tv + at);
     };
-    v4i32 rb, nrb; // run starts of the current and of the next tile
-    int32_t rb4, nrb4; // end of the last run
-    float2 yi[kTileRPT], nyi[kTileRPT];
-    fetch_rows(t0, tile_blk[t0], rb, rb4, yi);
-    {
-        const int32_t tn = t0 + 1 < t1 ? t0 + 1 : t0;
-        fetch_rows(tn, tile_blk[tn], nrb, nrb4, nyi);
-    }
+    // the segment of Y (8 independent 16-byte loads per thread) and the first
+    // chunks are in flight together
     static_assert(kYPad >= kTileSeg + 2 && kYPad >= kTileRows, "padding must cover one segment and one block");
-    // the segment of Y, 8 independent 16-byte loads per thread, in flight
-    // together with the first entries below
     constexpr int kStage = kTileSeg / 2 / kTileBlock;
     v4f stage[kStage];
     {
@@ -706,103 +696,79 @@ __global__ __launch_bounds__(kTileBlock) void attract_stream_kernel(
 #pragma unroll
         for (int q = 0; q < kStage; ++q) stage[q] = src[q * kTileBlock];
     }
-    auto run_end = [](const v4i32 &b, int32_t b4, int q) { return q < 3 ? b[q + 1] : b4; };
-    // entry index of this lane for row q at step offset `off` (0 once past the run)
-    auto entry = [&](const v4i32 &b, int32_t b4, int q, int32_t off) {
-        const int32_t at = b[q] + off + 4 * sub;
-        return at < run_end(b, b4, q) ? at : 0;
-    };
-    // two buffers of entries, used in turn: a step sums one while the other
-    // receives the next step's loads
-    v4u16 ca[kTileRPT], cb[kTileRPT];
-    v4f pa[kTileRPT], pb[kTileRPT];
 #pragma unroll
-    for (int q = 0; q < kTileRPT; ++q) {
-        const int32_t ia = entry(rb, rb4, q, 0);
-        ca[q] = *reinterpret_cast<const v4u16 *>(tcol + ia);
-        pa[q] = *reinterpret_cast<const v4f *>(tval + ia);
-    }
+    for (int x = 0; x < kSellRing; ++x) issue(x, x);
     v4f *sv = reinterpret_cast<v4f *>(sy4);
 #pragma unroll
     for (int q = 0; q < kStage; ++q) sv[q * kTileBlock + threadIdx.x] = stage[q];
     for (int32_t j = threadIdx.x; j < t1 - t0; j += kTileBlock) {
-        s_blk[j] = tile_blk[t0 + j];
+        s_row0[j] = tile_blk[t0 + j] * kTileRows;
         s_k[j] = tile_k[t0 + j];
+    }
+    for (int32_t j = threadIdx.x; j < iu.z - iu.x; j += kTileBlock) {
+        s_K[j] = unit_chunks[iu.x + j];
+        s_tj[j] = unit_tj[iu.x + j];
     }
     __syncthreads();
 
-    float fx[kTileRPT], fy[kTileRPT];
-#pragma unroll
-    for (int q = 0; q < kTileRPT; ++q) fx[q] = fy[q] = 0.0f;
-    int32_t off = 0; // wave-uniform offset of the current step in the tile's runs
-    // one step: loads for the next step (or the next tile's first entries)
-    // into (cn, pn), then the sum over (cc, pc); returns whether this tile
-    // has another step for any row of the wave
-    auto step = [&](const v4u16(&cc)[kTileRPT], const v4f(&pc)[kTileRPT], v4u16(&cn)[kTileRPT],
-                    v4f(&pn)[kTileRPT]) -> bool {
-        bool mine = false;
-#pragma unroll
-        for (int q = 0; q < kTileRPT; ++q) mine |= rb[q] + off + kTileStep < run_end(rb, rb4, q);
-        const bool more = __builtin_amdgcn_ballot_w64(mine) != 0; // wave-uniform
-        if (more) {
-#pragma unroll
-            for (int q = 0; q < kTileRPT; ++q) {
-                const int32_t ia = entry(rb, rb4, q, off + kTileStep);
-                cn[q] = *reinterpret_cast<const v4u16 *>(tcol + ia);
-                pn[q] = *reinterpret_cast<const v4f *>(tval + ia);
-            }
-        } else {
-#pragma unroll
-            for (int q = 0; q < kTileRPT; ++q) {
-                const int32_t ia = entry(nrb, nrb4, q, 0);
-                cn[q] = *reinterpret_cast<const v4u16 *>(tcol + ia);
-                pn[q] = *reinterpret_cast<const v4f *>(tval + ia);
-            }
-        }
-#pragma unroll
-        for (int q = 0; q < kTileRPT; ++q) {
-            float cx = 0.0f, cy = 0.0f;
-#pragma unroll
-            for (int v = 0; v < 4; ++v) attract_add(yi[q], sy[cc[q][v] & (kTileSeg - 1)], pc[q][v], cx, cy);
-            const bool live = rb[q] + off + 4 * sub < run_end(rb, rb4, q);
-            fx[q] += live ? cx : 0.0f;
-            fy[q] += live ? cy : 0.0f;
-        }
-        off += kTileStep;
-        return more;
+    // LDS values that are the same in every lane, as scalars
+    auto uni = [](int32_t v) { return __builtin_amdgcn_readfirstlane(v); };
+    // row of this lane in its block for unit u (a load), the first row of the
+    // unit's block, and the unit's partial slot
+    auto unit_rl = [&](int32_t u) {
+        const int32_t tj = uni(s_tj[u - iu.x]), t = tj / kSlicesPerTile, j = tj % kSlicesPerTile;
+        return int32_t(tperm[int64_t(t) * kTileRows + j * kSellSlice + lane]);
     };
-    // end of tile t: lane sub stores the partial of row 4 grp + sub, then the
-    // rows move on to tile t + 1 and the offsets of tile t + 2 are fetched
-    auto tile_end = [&](int32_t t) {
-        const int32_t j = t - t0;
-        float ax = 0.0f, ay = 0.0f;
-#pragma unroll
-        for (int q = 0; q < kTileRPT; ++q) {
-            const float sx = quad_sum(fx[q]), sy_ = quad_sum(fy[q]);
-            ax = sub == q ? sx : ax;
-            ay = sub == q ? sy_ : ay;
-            fx[q] = fy[q] = 0.0f;
-            yi[q] = nyi[q];
-        }
-        partial[(int64_t(s_blk[j]) * kTileRows + 4 * grp + sub) * kTileMaxSeg + s_k[j]] = make_float2(ax, ay);
-        rb = nrb;
-        rb4 = nrb4;
-        off = 0;
-        const int32_t tn = t + 2 < t1 ? t + 2 : t;
-        fetch_rows(tn, s_blk[tn - t0], nrb, nrb4, nyi);
-    };
+    auto unit_row0 = [&](int32_t u) { return uni(s_row0[uni(s_tj[u - iu.x]) / kSlicesPerTile - t0]); };
+    auto unit_slot = [&](int32_t u) { return uni(s_k[uni(s_tj[u - iu.x]) / kSlicesPerTile - t0]); };
 
-    // steps alternate between the buffers across tile boundaries (two per trip)
-    int32_t t = t0;
-    for (;;) {
-        if (!step(ca, pa, cb, pb)) {
-            tile_end(t);
-            if (++t == t1) break;
+    // units without entries in their tile's segment: their rows' partials are 0
+    for (int32_t u = iu.y + w; u < iu.z; u += kSellWaves)
+        partial[int64_t(unit_row0(u) + unit_rl(u)) * kTileMaxSeg + unit_slot(u)] = make_float2(0.0f, 0.0f);
+    if (wu.x >= wu.y) return; // no units for this wave (no barrier follows)
+
+    const int32_t ulast = wu.y - 1;
+    int32_t u = wu.x;             // unit being summed (wave-uniform)
+    int32_t uend = uni(s_K[u - iu.x]); // its chunks end at this wave step
+    // rows (layout order) of the current and the next unit, the next-but-one
+    // unit's row in its block (added to its block's first row when it moves up)
+    auto clampu = [&](int32_t x) { return x <= ulast ? x : ulast; };
+    int32_t rowA = unit_row0(u) + unit_rl(u);
+    int32_t rowB = unit_row0(clampu(u + 1)) + unit_rl(clampu(u + 1));
+    int32_t rlC = unit_rl(clampu(u + 2));
+    float2 yA = ylay[rowA], yB = ylay[rowB];
+    // Wait here once for y of the first two units (the last loads issued):
+    // otherwise the loop head, where this entry path meets the back edge,
+    // would wait for them on every trip.  The empty statement only uses the
+    // registers, which makes the compiler complete their loads before it.
+    asm volatile("" ::"v"(yA.x), "v"(yA.y), "v"(yB.x), "v"(yB.y));
+    float fx = 0.0f, fy = 0.0f;
+
+    // one wave step: sum chunk g from ring slot x, refill the slot with chunk
+    // g + kSellRing, and close the unit when g was its last chunk
+    auto step = [&](int x, int32_t g) {
+        const bool live = g < G; // wave-uniform; dead steps only occur after the last chunk
+        float cx = 0.0f, cy = 0.0f;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) attract_add(yA, sy[c[x][v] & (kTileSeg - 1)], p[x][v], cx, cy);
+        fx += live ? cx : 0.0f;
+        fy += live ? cy : 0.0f;
+        issue(x, g + kSellRing);
+        if (live && g + 1 == uend) {
+            partial[int64_t(rowA) * kTileMaxSeg + unit_slot(u)] = make_float2(fx, fy);
+            fx = fy = 0.0f;
+            ++u;
+            if (u <= ulast) uend += uni(s_K[u - iu.x]);
+            rowA = rowB;
+            yA = yB;
+            rowB = unit_row0(clampu(u + 1)) + rlC;
+            yB = ylay[rowB];
+            rlC = unit_rl(clampu(u + 2));
         }
-        if (!step(cb, pb, ca, pa)) {
-            tile_end(t);
-            if (++t == t1) break;
-        }
+    };
+    for (int32_t g = 0; g < G; g += kSellRing) {
+#pragma unroll
+        for (int x = 0; x < kSellRing; ++x) step(x, g + x);
     }
 }
 
@@ -869,15 +835,22 @@ LayoutView layout_view(void *mem, int64_t n, int64_t nnz)
     // rows are padded to multiples of 4 entries, plus one 4-entry sentinel vector at the end
     const size_t cap = size_t(nnz) + 3 * size_t(n) + 4;
     size_t o_col = take(4 * cap), o_val = take(4 * cap);
-    // tiled copy: at most kTileMaxSeg tiles per row block, runs padded to 4 entries
+    // tiled copy: at most kTileMaxSeg tiles per row block, sliced
     const int64_t blocks = (n + kTileRows - 1) / kTileRows;
     v.max_tiles = blocks * kTileMaxSeg;
-    v.max_entries = nnz + 3 * int64_t(kTileRows) * v.max_tiles + 8;
+    // the sliced copy pads every run to its slice's longest run, rounded up to
+    // whole chunks; it is built only when that fits in a quarter of nnz plus
+    // one chunk per slice (else the row-block kernel is used)
+    v.max_entries = nnz + nnz / 4 + int64_t(kSellChunk) * kSlicesPerTile * v.max_tiles + kSellChunk;
+    const int64_t max_units = v.max_tiles * kSlicesPerTile;
     size_t o_lo = take(4 * size_t(blocks)), o_ns = take(4 * size_t(blocks)),
            o_bt = take(4 * size_t(blocks) * kTileMaxSeg), o_tb = take(4 * size_t(v.max_tiles)),
            o_ts = take(4 * size_t(v.max_tiles)), o_tk = take(4 * size_t(v.max_tiles)),
-           o_it = take(4 * size_t(v.max_tiles + 1)),
-           o_ro = take(4 * size_t(v.max_tiles * kTileRows + 1)), o_tc = take(2 * size_t(v.max_entries)),
+           o_it = take(4 * size_t(v.max_tiles + 1)), o_rl = take(4 * size_t(v.max_tiles) * kTileRows),
+           o_tp = take(2 * size_t(v.max_tiles) * kTileRows), o_tq = take(2 * size_t(v.max_tiles) * kTileRows),
+           o_uo = take(4 * size_t(max_units)), o_uk = take(4 * size_t(max_units)), o_uj = take(4 * size_t(max_units)),
+           o_uc = take(4 * size_t(max_units)), o_iu = take(16 * size_t(v.max_tiles)),
+           o_wu = take(16 * size_t(v.max_tiles) * (kTileRows / kWave)), o_tc = take(2 * size_t(v.max_entries)),
            o_tv = take(4 * size_t(v.max_entries));
     v.bytes = off;
     if (mem) {
@@ -893,7 +866,15 @@ LayoutView layout_view(void *mem, int64_t n, int64_t nnz)
         v.tile_seg = at<int32_t>(mem, o_ts);
         v.tile_k = at<int32_t>(mem, o_tk);
         v.item_tile0 = at<int32_t>(mem, o_it);
-        v.run_off = at<int32_t>(mem, o_ro);
+        v.run_len = at<int32_t>(mem, o_rl);
+        v.tperm = at<uint16_t>(mem, o_tp);
+        v.tpos = at<uint16_t>(mem, o_tq);
+        v.unit_of = at<int32_t>(mem, o_uo);
+        v.unit_chunks = at<int32_t>(mem, o_uk);
+        v.unit_tj = at<int32_t>(mem, o_uj);
+        v.unit_chunk0 = at<int32_t>(mem, o_uc);
+        v.item_units = at<int4>(mem, o_iu);
+        v.wave_units = at<int4>(mem, o_wu);
         v.tcol = at<uint16_t>(mem, o_tc);
         v.tval = at<float>(mem, o_tv);
     }
@@ -943,24 +924,86 @@ static int build_tiles(const LayoutView &lv, int64_t n, TilePlan *plan, void *ws
     if (hipMemcpyAsync(lv.tile_k, tk.data(), 4 * tiles, hipMemcpyHostToDevice, st) != hipSuccess) return -1;
     if (hipMemcpyAsync(lv.item_tile0, items.data(), 4 * items.size(), hipMemcpyHostToDevice, st) != hipSuccess)
         return -1;
-    const int64_t rows = blocks * kTileRows, m = tiles * kTileRows;
+    // run lengths, rows sorted by run length in every tile, chunks per slice
+    const int64_t rows = blocks * kTileRows;
     const unsigned gw = unsigned((rows + 3) / 4 < 65535 * 4 ? (rows + 3) / 4 : 65535 * 4);
     tile_run_len_kernel<<<gw, 256, 0, st>>>(lv.row_ptr, lv.col, n, rows, lv.blk_seg_lo, lv.blk_nseg, lv.blk_tiles,
-                                            lv.run_off);
-    const int64_t st_tiles = (m + kI64Tile - 1) / kI64Tile;
-    int64_t *tsum = at<int64_t>(ws, L.codes1); // scratch: m / 4096 + 1 entries << n
-    int64_t *total = at<int64_t>(ws, L.codes1) + st_tiles + 1;
-    i32_reduce_kernel<<<unsigned(st_tiles), 256, 0, st>>>(lv.run_off, m, tsum);
-    i64_top_kernel<<<1, 256, 0, st>>>(tsum, st_tiles, total);
-    i32_down_kernel<<<unsigned(st_tiles), 256, 0, st>>>(lv.run_off, m, tsum);
-    i64_to_i32_kernel<<<1, 1, 0, st>>>(total, lv.run_off + m);
-    int64_t entries = 0;
-    if (hipMemcpyAsync(&entries, total, 8, hipMemcpyDeviceToHost, st) != hipSuccess) return -1;
+                                            lv.run_len);
+    tile_sort_kernel<<<unsigned(tiles), kTileRows, 0, st>>>(lv.run_len, lv.tperm, lv.tpos, lv.unit_chunks);
+    const int64_t units = tiles * kSlicesPerTile;
+    std::vector<int32_t> sk(units); // chunks of slice (tile, j), indexed tile * 16 + j
+    if (hipMemcpyAsync(sk.data(), lv.unit_chunks, 4 * units, hipMemcpyDeviceToHost, st) != hipSuccess) return -1;
     if (hipStreamSynchronize(st) != hipSuccess) return -1;
-    if (entries > lv.max_entries) return 0;
-    tile_copy_kernel<<<unsigned(n < 65535 * 4 ? (n + 3) / 4 : 65535 * 4), 256, 0, st>>>(
-        lv.row_ptr, lv.col, lv.val, n, lv.blk_seg_lo, lv.blk_nseg, lv.blk_tiles, lv.run_off, lv.max_entries, lv.tcol,
-        lv.tval);
+    // Units of every item: the ones with chunks are dealt to the block's waves
+    // longest first, each to the wave with the least work so far (cost: chunks
+    // plus one for the unit's bookkeeping); a wave's units and their chunks
+    // are stored back to back.  Units without chunks come last.
+    constexpr int W = kTileRows / kWave;
+    std::vector<int32_t> uo(units), uk(units), uj(units), uc(units);
+    std::vector<int4> iu(nitems), wu(size_t(nitems) * W);
+    int64_t d = 0, chunk = 0;
+    std::vector<int32_t> order_u;
+    std::vector<std::vector<int32_t>> lists(W);
+    for (int64_t i = 0; i < nitems; ++i) {
+        order_u.clear();
+        for (int64_t t = items[i]; t < items[i + 1]; ++t)
+            for (int j = 0; j < kSlicesPerTile; ++j)
+                if (sk[t * kSlicesPerTile + j] > 0) order_u.push_back(int32_t(t * kSlicesPerTile + j));
+        std::stable_sort(order_u.begin(), order_u.end(), [&](int32_t a, int32_t b) { return sk[a] > sk[b]; });
+        int64_t load[W] = {};
+        for (auto &l : lists) l.clear();
+        for (int32_t tj : order_u) {
+            const int wmin = int(std::min_element(load, load + W) - load);
+            lists[wmin].push_back(tj);
+            load[wmin] += sk[tj] + 1;
+        }
+        iu[i].x = int32_t(d);
+        for (int w = 0; w < W; ++w) {
+            int4 &q = wu[size_t(i) * W + w];
+            q.x = int32_t(d);
+            q.z = lists[w].empty() ? 0 : int32_t(chunk);
+            for (int32_t tj : lists[w]) {
+                uo[tj] = int32_t(d);
+                uk[d] = sk[tj];
+                uj[d] = tj;
+                uc[d] = int32_t(chunk);
+                chunk += sk[tj];
+                ++d;
+            }
+            q.y = int32_t(d);
+            q.w = lists[w].empty() ? 0 : int32_t(chunk - q.z);
+        }
+        iu[i].y = int32_t(d);
+        for (int64_t t = items[i]; t < items[i + 1]; ++t)
+            for (int j = 0; j < kSlicesPerTile; ++j)
+                if (sk[t * kSlicesPerTile + j] == 0) {
+                    const int32_t tj = int32_t(t * kSlicesPerTile + j);
+                    uo[tj] = int32_t(d);
+                    uk[d] = 0;
+                    uj[d] = tj;
+                    uc[d] = int32_t(chunk);
+                    ++d;
+                }
+        iu[i].z = int32_t(d);
+        iu[i].w = 0;
+        if (chunk * kSellChunk > lv.max_entries - kSellChunk) return 0; // too much padding: row-block kernel
+    }
+    const int64_t entries = chunk * kSellChunk;
+    if (hipMemcpyAsync(lv.unit_of, uo.data(), 4 * units, hipMemcpyHostToDevice, st) != hipSuccess) return -1;
+    if (hipMemcpyAsync(lv.unit_chunks, uk.data(), 4 * units, hipMemcpyHostToDevice, st) != hipSuccess) return -1;
+    if (hipMemcpyAsync(lv.unit_tj, uj.data(), 4 * units, hipMemcpyHostToDevice, st) != hipSuccess) return -1;
+    if (hipMemcpyAsync(lv.unit_chunk0, uc.data(), 4 * units, hipMemcpyHostToDevice, st) != hipSuccess) return -1;
+    if (hipMemcpyAsync(lv.item_units, iu.data(), 16 * iu.size(), hipMemcpyHostToDevice, st) != hipSuccess) return -1;
+    if (hipMemcpyAsync(lv.wave_units, wu.data(), 16 * wu.size(), hipMemcpyHostToDevice, st) != hipSuccess) return -1;
+    // zeros everywhere (chunk 0 included, which lanes without work read), then the entries
+    const int64_t zero = entries > kSellChunk ? entries : kSellChunk;
+    fill_zero_kernel<<<unsigned(std::min<int64_t>((zero + 255) / 256, 65535 * 4)), 256, 0, st>>>(lv.tcol, lv.tval,
+                                                                                                 zero);
+    sell_copy_kernel<<<unsigned(n < 65535 * 4 ? (n + 3) / 4 : 65535 * 4), 256, 0, st>>>(
+        lv.row_ptr, lv.col, lv.val, n, lv.blk_seg_lo, lv.blk_nseg, lv.blk_tiles, lv.tpos, lv.unit_of, lv.unit_chunk0,
+        lv.max_entries, lv.tcol, lv.tval);
+    // the tables above must stay alive until the copies have been read
+    if (hipStreamSynchronize(st) != hipSuccess) return -1;
     if (hipGetLastError() != hipSuccess) return -1;
     plan->tiled = true;
     plan->tiles = int32_t(tiles);
@@ -1034,9 +1077,10 @@ void launch_attract_layout(const LayoutView &lv, int64_t n, int64_t nnz, int til
 {
     if (tiles > 0) {
         const unsigned grid = unsigned((items + 7) / 8 * 8); // multiple of 8 for the XCD remap
-        attract_stream_kernel<<<grid, kTileBlock, 0, st>>>(lv.item_tile0, lv.tile_blk, lv.tile_seg, lv.tile_k,
-                                                           lv.run_off, lv.tcol, lv.tval, at<float2>(ws, L.ycopy),
-                                                           items, at<float2>(ws, L.partial));
+        attract_sell_kernel<<<grid, kTileBlock, 0, st>>>(lv.item_tile0, lv.item_units, lv.wave_units, lv.tile_blk,
+                                                         lv.tile_seg, lv.tile_k, lv.unit_chunks, lv.unit_tj,
+                                                         lv.tperm, lv.tcol, lv.tval, at<float2>(ws, L.ycopy), items,
+                                                         at<float2>(ws, L.partial));
         return;
     }
     // 1024 threads (one block per CU: the segment fills 128 KB of LDS), 2 rows per lane group

@@ -29,18 +29,25 @@ struct LayoutView {
     int32_t *col = nullptr;
     float *val = nullptr;
     // tiled copy: rows in blocks of kTileRows, columns in segments of kTileSeg
-    // points; one tile = (row block, segment) with each row's entries of that
-    // segment as a run padded to 4 entries (16-bit column offsets in the segment)
-    int32_t *blk_seg_lo = nullptr; // [blocks] first segment of a row block
-    int32_t *blk_nseg = nullptr;   // [blocks] segments of a row block (0: none)
-    int32_t *blk_tiles = nullptr;  // [blocks * kTileMaxSeg] tile of (row block, k-th segment)
-    int32_t *tile_blk = nullptr;   // [max tiles] row block of a tile; tiles are segment-major
-    int32_t *tile_seg = nullptr;   // [max tiles] segment of a tile
-    int32_t *tile_k = nullptr;     // [max tiles] segment of a tile counted from its block's first
-    int32_t *item_tile0 = nullptr; // [items + 1] first tile of each item (tiles of one segment)
-    int32_t *run_off = nullptr;    // [max tiles * kTileRows + 1]
-    uint16_t *tcol = nullptr;      // [max entries]
-    float *tval = nullptr;         // [max entries]
+    // points; one tile = (row block, segment), sliced into units of 64 rows
+    int32_t *blk_seg_lo = nullptr;  // [blocks] first segment of a row block
+    int32_t *blk_nseg = nullptr;    // [blocks] segments of a row block (0: none)
+    int32_t *blk_tiles = nullptr;   // [blocks * kTileMaxSeg] tile of (row block, k-th segment)
+    int32_t *tile_blk = nullptr;    // [max tiles] row block of a tile; tiles are segment-major
+    int32_t *tile_seg = nullptr;    // [max tiles] segment of a tile
+    int32_t *tile_k = nullptr;      // [max tiles] segment of a tile counted from its block's first
+    int32_t *item_tile0 = nullptr;  // [items + 1] first tile of each item (tiles of one segment)
+    int32_t *run_len = nullptr;     // [max tiles * kTileRows] entries of a row in a tile's segment
+    uint16_t *tperm = nullptr;      // [max tiles * kTileRows] sorted position -> row in the block
+    uint16_t *tpos = nullptr;       // [max tiles * kTileRows] row in the block -> sorted position
+    int32_t *unit_of = nullptr;     // [max units] unit (tile * 16 + slice) -> stored unit
+    int32_t *unit_chunks = nullptr; // [max units] chunks of a stored unit
+    int32_t *unit_tj = nullptr;     // [max units] tile * 16 + slice of a stored unit
+    int32_t *unit_chunk0 = nullptr; // [max units] first chunk of a stored unit
+    int4 *item_units = nullptr;     // [items] stored units [x, z) of an item, those from y on empty
+    int4 *wave_units = nullptr;     // [items * 16] units [x, y) and chunks [z, z + w) of a wave
+    uint16_t *tcol = nullptr;       // [max entries] column offset in the segment
+    float *tval = nullptr;          // [max entries]
     int64_t max_tiles = 0, max_entries = 0;
     size_t bytes = 0;
 };

@@ -32,6 +32,7 @@ def rel_l2(a, b):
 
 
 TILE_ROWS, TILE_SEG, TILE_MAX_SEG, ITEM_MAX_TILES = 1024, 16384, 16, 64
+SLICE, SLICES, CHUNK = 64, 16, 256  # rows per unit, units per tile, entries per chunk
 
 
 def _layout_arrays(lay, tiles=False):
@@ -57,20 +58,23 @@ def _layout_arrays(lay, tiles=False):
         return perm, rank, rp, col, val
     blocks = (n + TILE_ROWS - 1) // TILE_ROWS
     max_tiles = blocks * TILE_MAX_SEG
-    max_entries = nnz + 3 * TILE_ROWS * max_tiles + 8
-    seg_lo = take(4 * blocks, np.int32, blocks)
-    nseg = take(4 * blocks, np.int32, blocks)
-    blk_tiles = take(4 * blocks * TILE_MAX_SEG, np.int32, blocks * TILE_MAX_SEG).reshape(blocks, TILE_MAX_SEG)
-    tile_blk = take(4 * max_tiles, np.int32, max_tiles)
-    tile_seg = take(4 * max_tiles, np.int32, max_tiles)
-    tile_k = take(4 * max_tiles, np.int32, max_tiles)
-    item_tile0 = take(4 * (max_tiles + 1), np.int32, max_tiles + 1)
-    run_off = take(4 * (max_tiles * TILE_ROWS + 1), np.int32, max_tiles * TILE_ROWS + 1)
-    tcol = take(2 * max_entries, np.uint16, max_entries)
-    tval = take(4 * max_entries, np.float32, max_entries)
-    return (perm, rank, rp, col, val), dict(seg_lo=seg_lo, nseg=nseg, blk_tiles=blk_tiles, tile_blk=tile_blk,
-                                            tile_seg=tile_seg, tile_k=tile_k, item_tile0=item_tile0,
-                                            run_off=run_off, tcol=tcol, tval=tval)
+    max_units = max_tiles * SLICES
+    max_entries = nnz + nnz // 4 + CHUNK * SLICES * max_tiles + CHUNK
+    t = dict(seg_lo=take(4 * blocks, np.int32, blocks), nseg=take(4 * blocks, np.int32, blocks))
+    t["blk_tiles"] = take(4 * blocks * TILE_MAX_SEG, np.int32, blocks * TILE_MAX_SEG).reshape(blocks, TILE_MAX_SEG)
+    for k in ("tile_blk", "tile_seg", "tile_k"):
+        t[k] = take(4 * max_tiles, np.int32, max_tiles)
+    t["item_tile0"] = take(4 * (max_tiles + 1), np.int32, max_tiles + 1)
+    t["run_len"] = take(4 * max_tiles * TILE_ROWS, np.int32, max_tiles * TILE_ROWS)
+    t["tperm"] = take(2 * max_tiles * TILE_ROWS, np.uint16, max_tiles * TILE_ROWS)
+    t["tpos"] = take(2 * max_tiles * TILE_ROWS, np.uint16, max_tiles * TILE_ROWS)
+    for k in ("unit_of", "unit_chunks", "unit_tj", "unit_chunk0"):
+        t[k] = take(4 * max_units, np.int32, max_units)
+    t["item_units"] = take(16 * max_tiles, np.int32, 4 * max_tiles).reshape(max_tiles, 4)
+    t["wave_units"] = take(16 * max_tiles * 16, np.int32, 4 * 16 * max_tiles).reshape(max_tiles, 16, 4)
+    t["tcol"] = take(2 * max_entries, np.uint16, max_entries)
+    t["tval"] = take(4 * max_entries, np.float32, max_entries)
+    return (perm, rank, rp, col, val), t
 
 
 NO_COLUMN = 0x7FFFFFFF
@@ -209,8 +213,7 @@ def test_tiled_copy_reproduces_p():
     assert lay.tiles > 0
     (perm, rank, rp, col, val), tt = _layout_arrays(lay, tiles=True)
     T, I = lay.tiles, lay.items
-    seg_lo, nseg, tile_blk, tile_seg, run_off, tcol, tval = (tt[k] for k in (
-        "seg_lo", "nseg", "tile_blk", "tile_seg", "run_off", "tcol", "tval"))
+    seg_lo, nseg, tile_blk, tile_seg = (tt[k] for k in ("seg_lo", "nseg", "tile_blk", "tile_seg"))
     blocks = (n + TILE_ROWS - 1) // TILE_ROWS
     # tiles: every (block, segment) pair once, segment-major, indexed both ways
     assert T == int(nseg[:blocks].sum()) and 0 < I <= T
@@ -220,25 +223,58 @@ def test_tiled_copy_reproduces_p():
         b = tile_blk[t]
         k = tile_seg[t] - seg_lo[b]
         assert 0 <= k < nseg[b] and tt["tile_k"][t] == k and tt["blk_tiles"][b, k] == t
-    # items: consecutive runs of tiles of one segment covering every tile once
+    # rows of a tile sorted by decreasing run length, tperm and tpos inverse
+    tperm = tt["tperm"][:T * TILE_ROWS].reshape(T, TILE_ROWS).astype(np.int64)
+    tpos = tt["tpos"][:T * TILE_ROWS].reshape(T, TILE_ROWS).astype(np.int64)
+    rlen = tt["run_len"][:T * TILE_ROWS].reshape(T, TILE_ROWS)
+    for t in range(T):
+        assert np.array_equal(np.sort(tperm[t]), np.arange(TILE_ROWS))
+        assert np.array_equal(tpos[t][tperm[t]], np.arange(TILE_ROWS))
+        assert np.all(np.diff(rlen[t][tperm[t]]) <= 0)
+    # items: runs of tiles of one segment; their units are every slice once,
+    # the ones with chunks split among 16 waves whose chunks are contiguous
     it0 = tt["item_tile0"][:I + 1]
     assert it0[0] == 0 and it0[-1] == T and np.all(np.diff(it0) > 0) and np.all(np.diff(it0) <= ITEM_MAX_TILES)
+    iu, wu = tt["item_units"][:I], tt["wave_units"][:I]
+    uk, uj, uc = tt["unit_chunks"], tt["unit_tj"], tt["unit_chunk0"]
+    assert iu[0, 0] == 0 and iu[-1, 2] == T * SLICES
+    seen = np.zeros(T * SLICES, bool)
+    chunk = 0
     for i in range(I):
         assert len(set(tile_seg[it0[i]:it0[i + 1]].tolist())) == 1
+        assert iu[i, 0] == (iu[i - 1, 2] if i else 0) and iu[i, 0] <= iu[i, 1] <= iu[i, 2]
+        assert iu[i, 2] - iu[i, 0] == SLICES * (it0[i + 1] - it0[i])
+        for w in range(16):
+            x, y, z, g = wu[i, w]
+            assert x == (wu[i, w - 1, 1] if w else iu[i, 0]) and y >= x
+            if y > x:
+                assert z == chunk and g == int(uk[x:y].sum()) and np.all(uk[x:y] > 0)
+                assert np.array_equal(uc[x:y], z + np.concatenate([[0], np.cumsum(uk[x:y])[:-1]]))
+                chunk += g
+        assert wu[i, 15, 1] == iu[i, 1] and np.all(uk[iu[i, 1]:iu[i, 2]] == 0)
+        for d in range(iu[i, 0], iu[i, 2]):
+            tj = uj[d]
+            assert it0[i] <= tj // SLICES < it0[i + 1] and not seen[tj] and tt["unit_of"][tj] == d
+            seen[tj] = True
+            t, j = divmod(int(tj), SLICES)
+            assert uk[d] == (int(rlen[t][tperm[t][j * SLICE]]) + 3) // 4
+    assert seen.all()
+    # the sliced copy holds exactly P (padding carries zero values)
     rows_l, cols_l, vals_l = [], [], []
-    for t in range(T):
-        b, sg = tile_blk[t], tile_seg[t]
-        for rl in range(TILE_ROWS):
-            a, e = run_off[t * TILE_ROWS + rl], run_off[t * TILE_ROWS + rl + 1]
-            assert a % 4 == 0 and e % 4 == 0
-            r = b * TILE_ROWS + rl
-            if e > a:
-                assert r < n
-                rows_l.append(np.full(e - a, r))
-                cols_l.append(tcol[a:e].astype(np.int64) + sg * TILE_SEG)
-                vals_l.append(tval[a:e])
+    tcol, tval = tt["tcol"], tt["tval"]
+    lanes = np.arange(SLICE)
+    for d in range(T * SLICES):
+        if uk[d] == 0:
+            continue
+        t, j = divmod(int(uj[d]), SLICES)
+        rows = tile_blk[t] * TILE_ROWS + tperm[t][j * SLICE + lanes]
+        idx = (uc[d] + np.arange(uk[d]))[:, None, None] * CHUNK + lanes[None, :, None] * 4 + np.arange(4)[None, None, :]
+        rows_l.append(np.broadcast_to(rows[None, :, None], idx.shape).ravel())
+        cols_l.append(tcol[idx].astype(np.int64).ravel() + tile_seg[t] * TILE_SEG)
+        vals_l.append(tval[idx].ravel())
     rows_a, cols_a, vals_a = map(np.concatenate, (rows_l, cols_l, vals_l))
-    keep = vals_a != 0  # padding carries zero values
+    keep = vals_a != 0
+    assert np.all(rows_a[keep] < n)
     Pt = sp.csr_matrix((vals_a[keep], (rows_a[keep], cols_a[keep])), shape=(n, n))
     Po = sp.csr_matrix((inp.val, inp.col, inp.row_ptr), shape=(n, n))
     ref = Po[perm.astype(np.int64)][:, perm.astype(np.int64)]
