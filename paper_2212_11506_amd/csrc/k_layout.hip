@@ -657,7 +657,7 @@ constexpr int kItemMaxUnits = kItemMaxTiles * kSlicesPerTile;
 typedef uint16_t v4u16 __attribute__((ext_vector_type(4)));
 
 __global__ __launch_bounds__(kTileBlock) void attract_sell_kernel(
-    const int32_t *__restrict__ item_tile0, const int4 *__restrict__ item_units, const int4 *__restrict__ wave_units,
+    const int2 *__restrict__ item_tiles, const int4 *__restrict__ item_units, const int4 *__restrict__ wave_units,
     const int32_t *__restrict__ tile_blk, const int32_t *__restrict__ tile_seg, const int32_t *__restrict__ tile_k,
     const int32_t *__restrict__ unit_chunks, const int32_t *__restrict__ unit_tj, const uint16_t *__restrict__ tperm,
     const uint16_t *__restrict__ tcol, const float *__restrict__ tval, const float2 *__restrict__ ylay,
@@ -667,9 +667,11 @@ __global__ __launch_bounds__(kTileBlock) void attract_sell_kernel(
     __shared__ int32_t s_row0[kItemMaxTiles], s_k[kItemMaxTiles];
     __shared__ int32_t s_K[kItemMaxUnits], s_tj[kItemMaxUnits];
     const float2 *sy = reinterpret_cast<const float2 *>(sy4);
-    const uint32_t it = xcd_contiguous(blockIdx.x, gridDim.x);
+    // items are stored largest first and taken in launch order
+    const uint32_t it = blockIdx.x;
     if (it >= uint32_t(nitems)) return; // block-uniform, before the barrier
-    const int32_t t0 = item_tile0[it], t1 = item_tile0[it + 1];
+    const int2 itr = item_tiles[it];
+    const int32_t t0 = itr.x, t1 = itr.y;
     const int32_t sg = tile_seg[t0];
     const int4 iu = item_units[it]; // units [x, z) of the item; those from y on have no entries
     const int w = __builtin_amdgcn_readfirstlane(int(threadIdx.x) / kWave), lane = lane_id();
@@ -846,7 +848,7 @@ LayoutView layout_view(void *mem, int64_t n, int64_t nnz)
     size_t o_lo = take(4 * size_t(blocks)), o_ns = take(4 * size_t(blocks)),
            o_bt = take(4 * size_t(blocks) * kTileMaxSeg), o_tb = take(4 * size_t(v.max_tiles)),
            o_ts = take(4 * size_t(v.max_tiles)), o_tk = take(4 * size_t(v.max_tiles)),
-           o_it = take(4 * size_t(v.max_tiles + 1)), o_rl = take(4 * size_t(v.max_tiles) * kTileRows),
+           o_it = take(8 * size_t(v.max_tiles)), o_rl = take(4 * size_t(v.max_tiles) * kTileRows),
            o_tp = take(2 * size_t(v.max_tiles) * kTileRows), o_tq = take(2 * size_t(v.max_tiles) * kTileRows),
            o_uo = take(4 * size_t(max_units)), o_uk = take(4 * size_t(max_units)), o_uj = take(4 * size_t(max_units)),
            o_uc = take(4 * size_t(max_units)), o_iu = take(16 * size_t(v.max_tiles)),
@@ -865,7 +867,7 @@ LayoutView layout_view(void *mem, int64_t n, int64_t nnz)
         v.tile_blk = at<int32_t>(mem, o_tb);
         v.tile_seg = at<int32_t>(mem, o_ts);
         v.tile_k = at<int32_t>(mem, o_tk);
-        v.item_tile0 = at<int32_t>(mem, o_it);
+        v.item_tiles = at<int2>(mem, o_it);
         v.run_len = at<int32_t>(mem, o_rl);
         v.tperm = at<uint16_t>(mem, o_tp);
         v.tpos = at<uint16_t>(mem, o_tq);
@@ -903,27 +905,17 @@ static int build_tiles(const LayoutView &lv, int64_t n, TilePlan *plan, void *ws
     const int64_t tiles = int64_t(order.size());
     if (tiles == 0 || tiles > lv.max_tiles) return 0;
     std::sort(order.begin(), order.end());
-    std::vector<int32_t> bt(size_t(blocks) * kTileMaxSeg, -1), tb(tiles), ts(tiles), tk(tiles), items;
+    std::vector<int32_t> bt(size_t(blocks) * kTileMaxSeg, -1), tb(tiles), ts(tiles), tk(tiles);
     for (int64_t t = 0; t < tiles; ++t) {
         ts[t] = order[t].first;
         tb[t] = order[t].second;
         tk[t] = ts[t] - lo[tb[t]];
         bt[size_t(tb[t]) * kTileMaxSeg + tk[t]] = int32_t(t);
     }
-    int dev = 0, cus = 256;
-    if (hipGetDevice(&dev) == hipSuccess)
-        (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    const int64_t per = std::min<int64_t>(kItemMaxTiles, std::max<int64_t>(1, (tiles + 4 * cus - 1) / (4 * cus)));
-    for (int64_t t = 0; t < tiles; ++t)
-        if (items.empty() || ts[t] != ts[items.back()] || t - items.back() >= per) items.push_back(int32_t(t));
-    const int64_t nitems = int64_t(items.size());
-    items.push_back(int32_t(tiles));
     if (hipMemcpyAsync(lv.blk_tiles, bt.data(), 4 * bt.size(), hipMemcpyHostToDevice, st) != hipSuccess) return -1;
     if (hipMemcpyAsync(lv.tile_blk, tb.data(), 4 * tiles, hipMemcpyHostToDevice, st) != hipSuccess) return -1;
     if (hipMemcpyAsync(lv.tile_seg, ts.data(), 4 * tiles, hipMemcpyHostToDevice, st) != hipSuccess) return -1;
     if (hipMemcpyAsync(lv.tile_k, tk.data(), 4 * tiles, hipMemcpyHostToDevice, st) != hipSuccess) return -1;
-    if (hipMemcpyAsync(lv.item_tile0, items.data(), 4 * items.size(), hipMemcpyHostToDevice, st) != hipSuccess)
-        return -1;
     // run lengths, rows sorted by run length in every tile, chunks per slice
     const int64_t rows = blocks * kTileRows;
     const unsigned gw = unsigned((rows + 3) / 4 < 65535 * 4 ? (rows + 3) / 4 : 65535 * 4);
@@ -934,6 +926,39 @@ static int build_tiles(const LayoutView &lv, int64_t n, TilePlan *plan, void *ws
     std::vector<int32_t> sk(units); // chunks of slice (tile, j), indexed tile * 16 + j
     if (hipMemcpyAsync(sk.data(), lv.unit_chunks, 4 * units, hipMemcpyDeviceToHost, st) != hipSuccess) return -1;
     if (hipStreamSynchronize(st) != hipSuccess) return -1;
+    // Items: runs of tiles of one segment holding about a sixteenth of a CU's
+    // share of the chunks (at most kItemMaxTiles tiles), launched largest
+    // first so that blocks handed to whichever CU frees up first balance out.
+    int dev = 0, cus = 256;
+    if (hipGetDevice(&dev) == hipSuccess)
+        (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    std::vector<int64_t> tcost(tiles, 0);
+    int64_t total = 0;
+    for (int64_t t = 0; t < tiles; ++t) {
+        for (int j = 0; j < kSlicesPerTile; ++j) tcost[t] += sk[t * kSlicesPerTile + j];
+        total += tcost[t];
+    }
+    const int64_t target = std::max<int64_t>(1, total / (16 * int64_t(cus)));
+    std::vector<int2> ranges;
+    std::vector<int64_t> rcost;
+    for (int64_t t = 0; t < tiles; ++t) {
+        const bool fresh = ranges.empty() || ts[t] != ts[ranges.back().x] || t - ranges.back().x >= kItemMaxTiles ||
+                           (rcost.back() > 0 && rcost.back() + tcost[t] > target);
+        if (fresh) {
+            ranges.push_back(make_int2(int32_t(t), int32_t(t)));
+            rcost.push_back(0);
+        }
+        ranges.back().y = int32_t(t + 1);
+        rcost.back() += tcost[t];
+    }
+    const int64_t nitems = int64_t(ranges.size());
+    std::vector<int32_t> iorder(nitems);
+    for (int64_t i = 0; i < nitems; ++i) iorder[i] = int32_t(i);
+    std::stable_sort(iorder.begin(), iorder.end(), [&](int32_t a, int32_t b) { return rcost[a] > rcost[b]; });
+    std::vector<int2> items(nitems);
+    for (int64_t i = 0; i < nitems; ++i) items[i] = ranges[iorder[i]];
+    if (hipMemcpyAsync(lv.item_tiles, items.data(), 8 * items.size(), hipMemcpyHostToDevice, st) != hipSuccess)
+        return -1;
     // Units of every item: the ones with chunks are dealt to the block's waves
     // longest first, each to the wave with the least work so far (cost: chunks
     // plus one for the unit's bookkeeping); a wave's units and their chunks
@@ -946,7 +971,7 @@ static int build_tiles(const LayoutView &lv, int64_t n, TilePlan *plan, void *ws
     std::vector<std::vector<int32_t>> lists(W);
     for (int64_t i = 0; i < nitems; ++i) {
         order_u.clear();
-        for (int64_t t = items[i]; t < items[i + 1]; ++t)
+        for (int64_t t = items[i].x; t < items[i].y; ++t)
             for (int j = 0; j < kSlicesPerTile; ++j)
                 if (sk[t * kSlicesPerTile + j] > 0) order_u.push_back(int32_t(t * kSlicesPerTile + j));
         std::stable_sort(order_u.begin(), order_u.end(), [&](int32_t a, int32_t b) { return sk[a] > sk[b]; });
@@ -974,7 +999,7 @@ static int build_tiles(const LayoutView &lv, int64_t n, TilePlan *plan, void *ws
             q.w = lists[w].empty() ? 0 : int32_t(chunk - q.z);
         }
         iu[i].y = int32_t(d);
-        for (int64_t t = items[i]; t < items[i + 1]; ++t)
+        for (int64_t t = items[i].x; t < items[i].y; ++t)
             for (int j = 0; j < kSlicesPerTile; ++j)
                 if (sk[t * kSlicesPerTile + j] == 0) {
                     const int32_t tj = int32_t(t * kSlicesPerTile + j);
@@ -1076,8 +1101,8 @@ void launch_attract_layout(const LayoutView &lv, int64_t n, int64_t nnz, int til
                            const Layout &L, hipStream_t st)
 {
     if (tiles > 0) {
-        const unsigned grid = unsigned((items + 7) / 8 * 8); // multiple of 8 for the XCD remap
-        attract_sell_kernel<<<grid, kTileBlock, 0, st>>>(lv.item_tile0, lv.item_units, lv.wave_units, lv.tile_blk,
+        const unsigned grid = unsigned(items);
+        attract_sell_kernel<<<grid, kTileBlock, 0, st>>>(lv.item_tiles, lv.item_units, lv.wave_units, lv.tile_blk,
                                                          lv.tile_seg, lv.tile_k, lv.unit_chunks, lv.unit_tj,
                                                          lv.tperm, lv.tcol, lv.tval, at<float2>(ws, L.ycopy), items,
                                                          at<float2>(ws, L.partial));

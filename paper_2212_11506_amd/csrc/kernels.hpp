@@ -36,7 +36,7 @@ struct LayoutView {
     int32_t *tile_blk = nullptr;    // [max tiles] row block of a tile; tiles are segment-major
     int32_t *tile_seg = nullptr;    // [max tiles] segment of a tile
     int32_t *tile_k = nullptr;      // [max tiles] segment of a tile counted from its block's first
-    int32_t *item_tile0 = nullptr;  // [items + 1] first tile of each item (tiles of one segment)
+    int2 *item_tiles = nullptr;     // [items] tiles [x, y) of an item (one segment), largest item first
     int32_t *run_len = nullptr;     // [max tiles * kTileRows] entries of a row in a tile's segment
     uint16_t *tperm = nullptr;      // [max tiles * kTileRows] sorted position -> row in the block
     uint16_t *tpos = nullptr;       // [max tiles * kTileRows] row in the block -> sorted position

@@ -64,7 +64,7 @@ def _layout_arrays(lay, tiles=False):
     t["blk_tiles"] = take(4 * blocks * TILE_MAX_SEG, np.int32, blocks * TILE_MAX_SEG).reshape(blocks, TILE_MAX_SEG)
     for k in ("tile_blk", "tile_seg", "tile_k"):
         t[k] = take(4 * max_tiles, np.int32, max_tiles)
-    t["item_tile0"] = take(4 * (max_tiles + 1), np.int32, max_tiles + 1)
+    t["item_tiles"] = take(8 * max_tiles, np.int32, 2 * max_tiles).reshape(max_tiles, 2)
     t["run_len"] = take(4 * max_tiles * TILE_ROWS, np.int32, max_tiles * TILE_ROWS)
     t["tperm"] = take(2 * max_tiles * TILE_ROWS, np.uint16, max_tiles * TILE_ROWS)
     t["tpos"] = take(2 * max_tiles * TILE_ROWS, np.uint16, max_tiles * TILE_ROWS)
@@ -231,19 +231,22 @@ def test_tiled_copy_reproduces_p():
         assert np.array_equal(np.sort(tperm[t]), np.arange(TILE_ROWS))
         assert np.array_equal(tpos[t][tperm[t]], np.arange(TILE_ROWS))
         assert np.all(np.diff(rlen[t][tperm[t]]) <= 0)
-    # items: runs of tiles of one segment; their units are every slice once,
-    # the ones with chunks split among 16 waves whose chunks are contiguous
-    it0 = tt["item_tile0"][:I + 1]
-    assert it0[0] == 0 and it0[-1] == T and np.all(np.diff(it0) > 0) and np.all(np.diff(it0) <= ITEM_MAX_TILES)
+    # items: runs of tiles of one segment covering every tile once (stored
+    # largest first); their units are every slice once, the ones with chunks
+    # split among 16 waves whose chunks are contiguous
+    itr = tt["item_tiles"][:I]
+    assert np.all(itr[:, 1] > itr[:, 0]) and np.all(itr[:, 1] - itr[:, 0] <= ITEM_MAX_TILES)
+    srt = itr[np.argsort(itr[:, 0])]
+    assert srt[0, 0] == 0 and srt[-1, 1] == T and np.array_equal(srt[1:, 0], srt[:-1, 1])
     iu, wu = tt["item_units"][:I], tt["wave_units"][:I]
     uk, uj, uc = tt["unit_chunks"], tt["unit_tj"], tt["unit_chunk0"]
     assert iu[0, 0] == 0 and iu[-1, 2] == T * SLICES
     seen = np.zeros(T * SLICES, bool)
     chunk = 0
     for i in range(I):
-        assert len(set(tile_seg[it0[i]:it0[i + 1]].tolist())) == 1
+        assert len(set(tile_seg[itr[i, 0]:itr[i, 1]].tolist())) == 1
         assert iu[i, 0] == (iu[i - 1, 2] if i else 0) and iu[i, 0] <= iu[i, 1] <= iu[i, 2]
-        assert iu[i, 2] - iu[i, 0] == SLICES * (it0[i + 1] - it0[i])
+        assert iu[i, 2] - iu[i, 0] == SLICES * (itr[i, 1] - itr[i, 0])
         for w in range(16):
             x, y, z, g = wu[i, w]
             assert x == (wu[i, w - 1, 1] if w else iu[i, 0]) and y >= x
@@ -254,11 +257,13 @@ def test_tiled_copy_reproduces_p():
         assert wu[i, 15, 1] == iu[i, 1] and np.all(uk[iu[i, 1]:iu[i, 2]] == 0)
         for d in range(iu[i, 0], iu[i, 2]):
             tj = uj[d]
-            assert it0[i] <= tj // SLICES < it0[i + 1] and not seen[tj] and tt["unit_of"][tj] == d
+            assert itr[i, 0] <= tj // SLICES < itr[i, 1] and not seen[tj] and tt["unit_of"][tj] == d
             seen[tj] = True
             t, j = divmod(int(tj), SLICES)
             assert uk[d] == (int(rlen[t][tperm[t][j * SLICE]]) + 3) // 4
     assert seen.all()
+    cost = [int(uk[iu[i, 0]:iu[i, 2]].sum()) for i in range(I)]
+    assert cost == sorted(cost, reverse=True)  # largest item first
     # the sliced copy holds exactly P (padding carries zero values)
     rows_l, cols_l, vals_l = [], [], []
     tcol, tval = tt["tcol"], tt["tval"]
