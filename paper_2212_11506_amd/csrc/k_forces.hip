@@ -23,8 +23,37 @@ namespace bht {
 
 __device__ inline float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
 
-// One lane per point.  The branch on the node kind is wave-uniform, so single
-// points skip the acceptance test and internal cells skip the self test.
+// Lane masks straight from the vector compares (one instruction each, no
+// conversion through a boolean per lane): predicates as in LLVM's icmp/fcmp.
+constexpr int kCmpUge = 35, kCmpNe = 33, kCmpFgt = 2;
+__device__ inline uint64_t mask_uge(uint32_t a, uint32_t b) { return __builtin_amdgcn_uicmp(a, b, kCmpUge); }
+__device__ inline uint64_t mask_ne(uint32_t a, uint32_t b) { return __builtin_amdgcn_uicmp(a, b, kCmpNe); }
+__device__ inline uint64_t mask_fgt(float a, float b) { return __builtin_amdgcn_fcmpf(a, b, kCmpFgt); }
+// x in the lanes whose bit of m is set, else 0 (one v_cndmask on the mask)
+__device__ inline float keep_lanes(uint64_t m, float x)
+{
+    float r;
+    asm("v_cndmask_b32_e64 %0, 0, %1, %2" : "=v"(r) : "v"(x), "s"(m));
+    return r;
+}
+// a in the lanes whose bit of m is set, else b
+__device__ inline uint32_t pick_lanes(uint64_t m, uint32_t a, uint32_t b)
+{
+    uint32_t r;
+    asm("v_cndmask_b32_e64 %0, %1, %2, %3" : "=v"(r) : "v"(b), "v"(a), "s"(m));
+    return r;
+}
+
+// One lane per point.  Every visit runs the same straight-line code: a single
+// point is a cell that is always accepted (its threshold is -1) unless it is
+// the lane's own point (its meta word then equals the lane's self code).  The
+// acceptance test yields a lane mask, the weight is zeroed outside it, the
+// interaction count is its population, and the next node is a scalar select
+// (the skip index when no lane descends into an internal cell).  Only a
+// bucket (a leaf of several points) that some lanes reject branches, to take
+// its members exactly for those lanes.  The walk is bound by instruction
+// issue, vector and scalar alike (one scalar unit serves a CU's four SIMDs),
+// so both kinds are kept to a minimum.
 __global__ __launch_bounds__(kRepBlock) void repulsive_kernel(
     const float4 *__restrict__ nodes, const uint32_t *__restrict__ meta, const float2 *__restrict__ ys,
     const uint32_t *__restrict__ perm, Header *__restrict__ hdr, int64_t n, float2 *__restrict__ frep,
@@ -36,69 +65,54 @@ __global__ __launch_bounds__(kRepBlock) void repulsive_kernel(
     const int64_t s64 = int64_t(lb) * kRepBlock + threadIdx.x;
     const bool valid = s64 < n;
     const uint32_t si = uint32_t(s64);
+    const uint32_t self = si | kLeafBit | kSingleBit; // meta word of this lane's own leaf
     const float2 yi = valid ? ys[s64] : make_float2(0.0f, 0.0f);
     uint32_t resume = valid ? 0u : 0xffffffffu;
     float fx = 0.0f, fy = 0.0f, z = 0.0f;
     uint32_t total = uniform(hdr->nodes);
     const uint32_t cap = uint32_t(2 * n);
     total = total < cap ? total : cap;
+    // node records by 32-bit byte offset (fewer than 2^27 nodes)
+    const char *nbase = reinterpret_cast<const char *>(nodes);
+    const char *mbase = reinterpret_cast<const char *>(meta);
 
     uint32_t cur = 0;
-    uint32_t cnt = 0; // this lane's interactions
+    uint32_t inter = 0; // this wave's interactions (a launch has fewer than 2^32 per wave)
     while (cur < total) {
-        const float4 r = nodes[cur];
-        const uint32_t m = meta[cur];
-        uint32_t nxt = cur + 1;
-        if (m & kSingleBit) { // an exact pair with one point (not itself)
-            if (cur >= resume && (m & kIndexMask) != si) {
-                ++cnt;
-                const float dx = yi.x - r.x, dy = yi.y - r.y;
-                const float wgt = fast_rcp(1.0f + fmaf(dx, dx, dy * dy));
-                z += wgt;
-                const float w2 = wgt * wgt;
-                fx = fmaf(w2, dx, fx);
-                fy = fmaf(w2, dy, fy);
-            }
-        } else { // a cell: summary when far enough
-            const float dx = yi.x - r.x, dy = yi.y - r.y;
-            const float d2 = fmaf(dx, dx, dy * dy);
-            const bool active = cur >= resume;
-            const bool take = active && (d2 > r.w);
-            if (take) {
-                ++cnt;
-                const float wgt = fast_rcp(1.0f + d2);
-                const float nw = r.z * wgt;
-                z += nw;
-                const float nw2 = nw * wgt;
-                fx = fmaf(nw2, dx, fx);
-                fy = fmaf(nw2, dy, fy);
-                if (!(m & kLeafBit)) resume = m; // park until the walk leaves the cell
-            }
-            const uint64_t rej = ballot(active && !take);
-            if (m & kLeafBit) {
-                if (rej) { // bucket: its members one by one
-                    const bool lrej = (rej >> lane_id()) & 1ull;
-                    const uint32_t b = m & kIndexMask;
-                    uint32_t e = b + uint32_t(r.z);
-                    e = e < uint32_t(n) ? e : uint32_t(n);
-                    for (uint32_t j = b; j < e; ++j) {
-                        const float2 yj = ys[j];
-                        if (lrej && j != si) {
-                            ++cnt;
-                            const float ex = yi.x - yj.x, ey = yi.y - yj.y;
-                            const float wgt = fast_rcp(1.0f + fmaf(ex, ex, ey * ey));
-                            z += wgt;
-                            const float w2 = wgt * wgt;
-                            fx = fmaf(w2, ex, fx);
-                            fy = fmaf(w2, ey, fy);
-                        }
-                    }
-                }
-            } else if (!rej) {
-                nxt = m;
+        const float4 r = *reinterpret_cast<const float4 *>(nbase + (cur << 4));
+        const uint32_t m = *reinterpret_cast<const uint32_t *>(mbase + (cur << 2));
+        const float dx = yi.x - r.x, dy = yi.y - r.y;
+        const float d2 = fmaf(dx, dx, dy * dy);
+        const uint64_t act = mask_uge(cur, resume);
+        const uint64_t take = act & mask_fgt(d2, r.w) & mask_ne(m, self);
+        const float wgt = fast_rcp(1.0f + d2);
+        const float nw = keep_lanes(take, r.z * wgt);
+        z += nw;
+        const float nw2 = nw * wgt;
+        fx = fmaf(nw2, dx, fx);
+        fy = fmaf(nw2, dy, fy);
+        inter += uint32_t(__builtin_popcountll(take));
+        const uint64_t rej = act & ~take;
+        const bool internal = !(m & kLeafBit);
+        // accepting lanes park until the walk leaves an internal cell
+        resume = pick_lanes(internal ? take : 0ull, m, resume);
+        if (!internal && !(m & kSingleBit) && rej) { // bucket: its members, exact, for the rejecting lanes
+            const uint32_t b = m & kIndexMask;
+            uint32_t e = b + uint32_t(r.z);
+            e = e < uint32_t(n) ? e : uint32_t(n);
+            for (uint32_t j = b; j < e; ++j) {
+                const float2 yj = ys[j];
+                const uint64_t pair = rej & mask_ne(j, si);
+                const float ex = yi.x - yj.x, ey = yi.y - yj.y;
+                const float pw = keep_lanes(pair, fast_rcp(1.0f + fmaf(ex, ex, ey * ey)));
+                z += pw;
+                const float w2 = pw * pw;
+                fx = fmaf(w2, ex, fx);
+                fy = fmaf(w2, ey, fy);
+                inter += uint32_t(__builtin_popcountll(pair));
             }
         }
-        cur = uniform(nxt > cur ? nxt : cur + 1);
+        cur = (internal && !rej) ? m : cur + 1; // a skip index lies beyond its cell
     }
 
     if (valid) {
@@ -107,7 +121,6 @@ __global__ __launch_bounds__(kRepBlock) void repulsive_kernel(
     }
     // deterministic Z: wave -> block partial -> fixed-order sum in the last block
     double zw = wave_sum(double(z));
-    const unsigned long long inter = wave_sum((unsigned long long)cnt);
     __shared__ double s_z[kRepBlock / kWave];
     __shared__ unsigned long long s_i[kRepBlock / kWave];
     __shared__ bool s_last;
