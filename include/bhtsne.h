@@ -203,8 +203,11 @@ int bhtsne_debug_sort(const float *Y, int64_t n, uint64_t *codes, uint64_t *sort
  * level).  Device arrays of 2n entries (summary: 2n x 4 floats {com x, com y,
  * count, threshold}), each nullable; *n_nodes (host, required) receives the
  * node count after a stream synchronisation.  kind: 0 internal, 1 bucket of
- * identical codes, 2 single point.  meta: skip index (internal nodes),
- * begin | 0x80000000 (buckets) or begin | 0xC0000000 (single points). */
+ * identical codes (level 32), 2 single point.  Every point has its own
+ * single-point node; a bucket's points follow it as its children, at level
+ * 33.  meta: skip index, the first node past the subtree (internal nodes and
+ * buckets), or begin | 0xC0000000 (single points); threshold: -1 for single
+ * points, else side^2 / theta^2. */
 int bhtsne_debug_tree(const float *Y, int64_t n, float theta, int64_t *n_nodes, uint8_t *level, uint8_t *kind,
                       uint32_t *begin, uint32_t *end, float *summary, uint32_t *meta, void *workspace,
                       size_t workspace_bytes, hipStream_t stream);

@@ -36,24 +36,22 @@ __device__ inline float keep_lanes(uint64_t m, float x)
     asm("v_cndmask_b32_e64 %0, 0, %1, %2" : "=v"(r) : "v"(x), "s"(m));
     return r;
 }
-// a in the lanes whose bit of m is set, else b
-__device__ inline uint32_t pick_lanes(uint64_t m, uint32_t a, uint32_t b)
+__device__ inline uint32_t keep_lanes_u(uint64_t m, uint32_t x)
 {
     uint32_t r;
-    asm("v_cndmask_b32_e64 %0, %1, %2, %3" : "=v"(r) : "v"(b), "v"(a), "s"(m));
+    asm("v_cndmask_b32_e64 %0, 0, %1, %2" : "=v"(r) : "v"(x), "s"(m));
     return r;
 }
 
 // One lane per point.  Every visit runs the same straight-line code: a single
 // point is a cell that is always accepted (its threshold is -1) unless it is
-// the lane's own point (its meta word then equals the lane's self code).  The
+// the lane's own point (its meta word then equals the lane's self code), and
+// a bucket of identical points is a cell whose children are its points.  The
 // acceptance test yields a lane mask, the weight is zeroed outside it, the
 // interaction count is its population, and the next node is a scalar select
-// (the skip index when no lane descends into an internal cell).  Only a
-// bucket (a leaf of several points) that some lanes reject branches, to take
-// its members exactly for those lanes.  The walk is bound by instruction
-// issue, vector and scalar alike (one scalar unit serves a CU's four SIMDs),
-// so both kinds are kept to a minimum.
+// (the skip index when no lane descends into the cell).  The walk is bound by
+// instruction issue, vector and scalar alike (one scalar unit serves a CU's
+// four SIMDs), so both kinds are kept to a minimum.
 __global__ __launch_bounds__(kRepBlock) void repulsive_kernel(
     const float4 *__restrict__ nodes, const uint32_t *__restrict__ meta, const float2 *__restrict__ ys,
     const uint32_t *__restrict__ perm, Header *__restrict__ hdr, int64_t n, float2 *__restrict__ frep,
@@ -93,26 +91,12 @@ __global__ __launch_bounds__(kRepBlock) void repulsive_kernel(
         fy = fmaf(nw2, dy, fy);
         inter += uint32_t(__builtin_popcountll(take));
         const uint64_t rej = act & ~take;
-        const bool internal = !(m & kLeafBit);
+        // the skip index of an internal cell, 0 for a leaf (kLeafBit is the sign bit)
+        const uint32_t skip = m & ~uint32_t(int32_t(m) >> 31);
         // accepting lanes park until the walk leaves an internal cell
-        resume = pick_lanes(internal ? take : 0ull, m, resume);
-        if (!internal && !(m & kSingleBit) && rej) { // bucket: its members, exact, for the rejecting lanes
-            const uint32_t b = m & kIndexMask;
-            uint32_t e = b + uint32_t(r.z);
-            e = e < uint32_t(n) ? e : uint32_t(n);
-            for (uint32_t j = b; j < e; ++j) {
-                const float2 yj = ys[j];
-                const uint64_t pair = rej & mask_ne(j, si);
-                const float ex = yi.x - yj.x, ey = yi.y - yj.y;
-                const float pw = keep_lanes(pair, fast_rcp(1.0f + fmaf(ex, ex, ey * ey)));
-                z += pw;
-                const float w2 = pw * pw;
-                fx = fmaf(w2, ex, fx);
-                fy = fmaf(w2, ey, fy);
-                inter += uint32_t(__builtin_popcountll(pair));
-            }
-        }
-        cur = (internal && !rej) ? m : cur + 1; // a skip index lies beyond its cell
+        resume = max(resume, keep_lanes_u(take, skip));
+        // a skip index lies beyond its cell: skip when no lane descends
+        cur = rej ? cur + 1 : max(cur + 1, skip);
     }
 
     if (valid) {

@@ -3,8 +3,10 @@
 // Quadtree Building: a cell at level L is the set of codes that share their
 // top 2L bits, so every cell is a contiguous range of the sorted codes.  A
 // cell is a node of the compressed tree when its points fall into at least
-// two quadrants (the root always is one); runs of identical codes form a
-// single bucket leaf at level 32, and unique codes are single-point leaves.
+// two quadrants (the root always is one); a run of identical codes forms a
+// bucket cell at level 32, and every point is a single-point leaf (the
+// members of a bucket are its children, so a walk treats a bucket like any
+// other cell: its summary when far enough, else its points one by one).
 //
 // Parallel construction, one thread per sorted position:
 //   1. For each adjacent pair (s, s+1) the split level is
@@ -12,7 +14,8 @@
 //      s is found by galloping searches; the first split of a cell owns it and
 //      marks bit L of levelmask[begin].
 //   2. Nodes are numbered in depth-first pre-order, which is the order of
-//      (begin, level).  With cnt(x) = leaf starting at x + popcount(levelmask[x])
+//      (begin, level), bucket members sitting at level 33.  With cnt(x) = 1
+//      (the point's leaf) + 1 if a bucket starts at x + popcount(levelmask[x])
 //      and base = exclusive scan of cnt, node (L, [b,e)) sits at
 //      base[b] + popcount(levelmask[b] & (2^L - 1)), and the first node after
 //      its subtree is base[e].
@@ -144,11 +147,12 @@ struct ScanVal {
 __device__ inline ScanVal scan_add(ScanVal a, ScanVal b) { return {a.c + b.c, a.x + b.x, a.y + b.y}; }
 
 __device__ inline ScanVal element(const uint64_t *__restrict__ codes, const uint32_t *__restrict__ levelmask,
-                                  const float2 *__restrict__ ys, int64_t x, double c0, double c1)
+                                  const float2 *__restrict__ ys, int64_t x, int64_t n, double c0, double c1)
 {
-    uint32_t leaf = (x == 0 || codes[x - 1] != codes[x]) ? 1u : 0u;
+    const uint64_t k = codes[x];
+    const uint32_t bucket = (x == 0 || codes[x - 1] != k) && x + 1 < n && codes[x + 1] == k ? 1u : 0u;
     float2 y = ys[x];
-    return {leaf + uint32_t(__popc(levelmask[x])), double(y.x) - c0, double(y.y) - c1};
+    return {1u + bucket + uint32_t(__popc(levelmask[x])), double(y.x) - c0, double(y.y) - c1};
 }
 
 // exclusive block scan of one ScanVal per thread (256 threads); returns the block total
@@ -187,7 +191,7 @@ __global__ __launch_bounds__(kScanBlock) void scan_reduce_kernel(
     ScanVal acc{0, 0.0, 0.0};
     for (int k = 0; k < kScanItems; ++k) {
         int64_t x = first + k;
-        if (x < n) acc = scan_add(acc, element(codes, levelmask, ys, x, c0, c1));
+        if (x < n) acc = scan_add(acc, element(codes, levelmask, ys, x, n, c0, c1));
     }
     ScanVal tot;
     block_scan_excl(acc, s_wave, &tot);
@@ -248,7 +252,7 @@ __global__ __launch_bounds__(kScanBlock) void scan_down_kernel(
 #pragma unroll
     for (int k = 0; k < kScanItems; ++k) {
         int64_t x = first + k;
-        loc[k] = (x < n) ? element(codes, levelmask, ys, x, c0, c1) : ScanVal{0, 0.0, 0.0};
+        loc[k] = (x < n) ? element(codes, levelmask, ys, x, n, c0, c1) : ScanVal{0, 0.0, 0.0};
         acc = scan_add(acc, loc[k]);
     }
     ScanVal tot;
@@ -334,7 +338,9 @@ __global__ __launch_bounds__(256) void tree_nodes_kernel(
     // (b) the root, when no split lies at level 0 (all points in one quadrant)
     if (x == 0 && quad_digit(codes[0], 0) == quad_digit(codes[n - 1], 0))
         emit(0, centre_of_mass(psum, ys, 0, n, c0, c1), 0, n, 0, accept_threshold(rspan, 0, theta2), base[n], 0);
-    // (c) the leaf that starts at x
+    // (c) the leaf of point x, preceded by its bucket when a run of identical
+    // codes starts at x (bucket members are leaves at level 33)
+    const uint32_t single = uint32_t(x) | kLeafBit | kSingleBit;
     if (x == 0 || codes[x - 1] != codes[x]) {
         int64_t e = run_end(codes, x, n);
         int64_t pre = base[x] + __popc(levelmask[x]);
@@ -345,11 +351,14 @@ __global__ __launch_bounds__(256) void tree_nodes_kernel(
                 int r = split_level(codes[x], codes[x + 1]);
                 lv = r > lv ? r : lv;
             }
-            emit(pre, ys[x], x, e, lv + 1, -1.0f, uint32_t(x) | kLeafBit | kSingleBit, 2);
+            emit(pre, ys[x], x, e, lv + 1, -1.0f, single, 2);
         } else {
             emit(pre, centre_of_mass(psum, ys, x, e, c0, c1), x, e, 32, accept_threshold(rspan, 32, theta2),
-                 uint32_t(x) | kLeafBit, 1);
+                 base[e], 1);
+            emit(pre + 1, ys[x], x, x + 1, 33, -1.0f, single, 2);
         }
+    } else {
+        emit(base[x], ys[x], x, x + 1, 33, -1.0f, single, 2); // a later member of a bucket
     }
 }
 

@@ -94,6 +94,39 @@ def test_morton_and_sort_bit_exact(case):
     assert np.array_equal(perm.cpu().numpy().view(np.uint32), t.perm)
 
 
+def _bucket_points(y):
+    """Points in buckets: the library stores each as a node of its own."""
+    with oracle.State(y) as s:
+        t = s.tree()
+    b = t.kind == oracle.BUCKET
+    return int((t.end[b].astype(np.int64) - t.begin[b]).sum())
+
+
+def _with_members(t, y):
+    """The oracle's tree laid out as the library stores it: every bucket leaf is
+    followed by its points as single-point nodes (level 33), in sorted order."""
+    from types import SimpleNamespace
+    idx, lev, kind, beg, end, cnt, com = [], [], [], [], [], [], []
+    ys = y.astype(np.float64)[t.perm.astype(np.int64)]
+    for i in range(t.nodes):
+        idx.append(i)
+        lev.append(t.level[i]); kind.append(t.kind[i]); beg.append(t.begin[i]); end.append(t.end[i])
+        cnt.append(t.count[i]); com.append(t.com[i])
+        if t.kind[i] == oracle.BUCKET:
+            for j in range(int(t.begin[i]), int(t.end[i])):
+                lev.append(33); kind.append(oracle.SINGLE); beg.append(j); end.append(j + 1)
+                cnt.append(1); com.append(ys[j])
+    u = SimpleNamespace(**{k: getattr(t, k) for k in ("box", "perm", "codes", "sorted_codes", "yrs")})
+    u.nodes = len(lev)
+    u.level = np.array(lev, dtype=t.level.dtype)
+    u.kind = np.array(kind, dtype=t.kind.dtype)
+    u.begin = np.array(beg, dtype=t.begin.dtype)
+    u.end = np.array(end, dtype=t.end.dtype)
+    u.count = np.array(cnt, dtype=t.count.dtype)
+    u.com = np.array(com, dtype=np.float64).reshape(-1, 2)
+    return u
+
+
 @pytest.mark.parametrize("case", SORT_CASES)
 def test_tree_and_summaries(case):
     y = _case(case)
@@ -101,7 +134,7 @@ def test_tree_and_summaries(case):
     say(f"[tree] case={case} n={y.shape[0]}")
     g = bh.debug_tree(dev_y(y), theta)
     with oracle.State(y) as s:
-        t = s.tree()
+        t = _with_members(s.tree(), y)
     assert g["nodes"] == t.nodes
     assert np.array_equal(g["level"].cpu().numpy(), t.level)
     assert np.array_equal(g["kind"].cpu().numpy(), t.kind)
@@ -123,15 +156,13 @@ def test_tree_and_summaries(case):
     with np.errstate(over="ignore"):
         side2_f32 = side2.astype(np.float32).astype(np.float64)  # squared lengths live in fp32
     assert np.allclose(summ[~single, 3], side2_f32, rtol=1e-6, atol=1e-45)
-    # skip pointers: internal -> first node past the subtree; buckets -> begin | leaf
-    # bit; single points -> begin | leaf bit | single bit
+    # skip pointers: cells (internal and buckets) -> first node past the subtree;
+    # single points -> begin | leaf bit | single bit
     meta = g["meta"].cpu().numpy().view(np.uint32)
-    internal = t.kind == oracle.INTERNAL
-    bucket = t.kind == oracle.BUCKET
+    cell = ~single
     order_end = np.searchsorted(t.begin.astype(np.int64) * 64 + t.level,
                                 t.end.astype(np.int64) * 64, side="left")
-    assert np.array_equal(meta[internal], order_end[internal].astype(np.uint32))
-    assert np.array_equal(meta[bucket], t.begin[bucket] | np.uint32(0x80000000))
+    assert np.array_equal(meta[cell], order_end[cell].astype(np.uint32))
     assert np.array_equal(meta[single], t.begin[single] | np.uint32(0xC0000000))
 
 
@@ -161,7 +192,7 @@ def test_gradient_parity(case, theta):
     g = g.cpu().numpy()
     stats = bh.get_stats(ws)
     go, Zo, inter_o, nodes_o = oracle.gradient(y, rp, col, val, theta, alpha)
-    assert stats["nodes"] == nodes_o
+    assert stats["nodes"] == nodes_o + _bucket_points(y)
     if theta == 0.0:
         assert stats["interactions"] == inter_o == y.shape[0] * (y.shape[0] - 1)
     else:  # an acceptance may flip where fp32 and fp64 distances straddle the threshold
@@ -183,6 +214,7 @@ def test_gradient_parity_other_angles(theta):
     g, Z = bh.gradient(dev_y(y), dev_p(rp, col, val), theta, 1.0, workspace=ws)
     stats = bh.get_stats(ws)
     go, Zo, inter_o, nodes_o = oracle.gradient(y, rp, col, val, theta, 1.0)
+    nodes_o += _bucket_points(y)
     assert rel_l2(g.cpu().numpy(), go) <= 1e-3
     assert abs(Z - Zo) <= 1e-5 * Zo
     assert stats["nodes"] == nodes_o
