@@ -24,6 +24,13 @@ if ROOT not in sys.path:
 
 METRIC = "BH t-SNE gradient iterations/s at N=1.3M, theta=0.5; repulsive interactions/s"
 HBM_PEAK_GBS = 8000.0
+# fp32 vector peak without packed math (the build disables packed fp32):
+# 256 CUs x 64 lanes x 2 flops (FMA) x 2.4 GHz
+ALU_PEAK_TFLOPS = 256 * 64 * 2 * 2.4e9 / 1e12
+# algorithmic flops of one interaction (summary or exact pair): dx, dy (2),
+# d^2 (3), 1 + d^2 (1), reciprocal (1), count x w and w^2 (2), Z (1), forces (4)
+FLOPS_PER_INTERACTION = 14
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_1p3M.md")
 
 
 def log(*a):
@@ -43,11 +50,57 @@ def parse():
     ap.add_argument("--no-count", action="store_true", help="skip the interaction-counting replay")
     ap.add_argument("--plain", action="store_true",
                     help="attractive step straight from the CSR arrays (no locality layout)")
+    ap.add_argument("--copy-calibrate", action="store_true",
+                    help="only run device-to-device copies of 1 GiB (for scaling HBM counters)")
     return ap.parse_args()
+
+
+def copy_calibrate():
+    """Ten copies of 1 GiB on the device: the known bytes that FETCH_SIZE and
+    WRITE_SIZE are scaled by."""
+    import torch
+    nbytes = 1 << 30
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(10):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration": True, "bytes_read_per_copy": nbytes, "bytes_written_per_copy": nbytes,
+                      "copies": 10}), flush=True)
+
+
+def source_hash(*names):
+    import hashlib
+    h = hashlib.sha256()
+    for name in names:
+        with open(os.path.join(ROOT, "paper_2212_11506_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel, sources):
+    """HBM bytes per launch of `kernel` from the committed counter summary,
+    or None when the summary is missing or the kernel's sources changed since."""
+    try:
+        lines = open(TRAFFIC_FILE).read().splitlines()
+    except OSError:
+        return None
+    for line in lines:
+        cells = [c.strip() for c in line.strip().strip("|").split("|")]
+        if len(cells) >= 4 and cells[0] == kernel:
+            try:
+                traffic = float(cells[1])
+            except ValueError:
+                return None
+            return traffic if cells[3] == source_hash(*sources) else None
+    return None
 
 
 def main():
     args = parse()
+    if args.copy_calibrate:
+        copy_calibrate()
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: the multi-GPU path is a design note, "
               "not a built component (use --gpus 1)", file=sys.stderr)
@@ -136,26 +189,36 @@ def main():
         kernels[name] = {"ms_per_launch": per, "launches": cnt}
     rep_ms = kernels["repulsive"]["ms_per_launch"]
     att_ms = kernels["attractive"]["ms_per_launch"]
-    # algorithmic bytes per launch: repulsion 16 B per interaction + 20 B per point;
-    # attraction+update 8 B per stored entry (col, val) + 64 B per point
+    # sources whose change invalidates the committed traffic counters
+    rep_src = ("k_forces.hip", "k_tree.hip", "common.hpp")
+    att_src = ("k_layout.hip", "common.hpp") if not args.plain else ("k_forces.hip", "common.hpp")
+    rep = kernels["repulsive"]
     if inter_total is not None:
-        rep_bytes = 16.0 * inter_total / args.steps + 20.0 * n
-        kernels["repulsive"]["gbs"] = rep_bytes / (rep_ms * 1e-3) / 1e9
-        kernels["repulsive"]["frac_hbm"] = kernels["repulsive"]["gbs"] / HBM_PEAK_GBS
-        kernels["repulsive"]["interactions_per_s"] = inter_total / args.steps / (rep_ms * 1e-3)
-    att_bytes = 8.0 * nnz + 64.0 * n
+        per_launch = inter_total / args.steps
+        rep["interactions_per_s"] = per_launch / (rep_ms * 1e-3)
+        rep["tflops"] = FLOPS_PER_INTERACTION * rep["interactions_per_s"] / 1e12
+        rep["frac_alu"] = rep["tflops"] / ALU_PEAK_TFLOPS
+        # the per-interaction byte model (16 B per summary or point + 20 B per
+        # point): nodes come from caches, so this exceeds what HBM moves
+        rep["model16_gbs"] = (16.0 * per_launch + 20.0 * n) / (rep_ms * 1e-3) / 1e9
+    # attraction and the update: 8 B per stored entry (column, value), 32 B per
+    # point for the row pointers, y_i and the output, and 72 B per point for the
+    # gradient assembly and update
+    att_bytes = 8.0 * nnz + 104.0 * n
     kernels["attractive"]["gbs"] = att_bytes / (att_ms * 1e-3) / 1e9
     kernels["attractive"]["frac_hbm"] = kernels["attractive"]["gbs"] / HBM_PEAK_GBS
     dominant = max(("repulsive", "attractive"), key=lambda k: kernels[k]["ms_per_launch"])
     if dominant == "repulsive" and inter_total is not None:
-        roof = {"kernel": "repulsive", "bound": "hbm", "achieved": kernels["repulsive"]["gbs"],
-                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": kernels["repulsive"]["frac_hbm"],
-                "traffic": None,
-                "model": "16 B per interaction (one cell summary or one point) + 20 B per point"}
+        roof = {"kernel": "repulsive", "bound": "alu", "achieved": rep["tflops"], "peak": ALU_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": rep["frac_alu"],
+                "traffic": measured_traffic("repulsive_kernel", rep_src),
+                "model": f"{FLOPS_PER_INTERACTION} fp32 flops per interaction (summary or exact pair); peak "
+                         "without packed fp32: 256 CUs x 64 lanes x 2 x 2.4 GHz"}
     else:
         roof = {"kernel": "attractive", "bound": "hbm", "achieved": kernels["attractive"]["gbs"],
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": kernels["attractive"]["frac_hbm"],
-                "traffic": None, "model": "8 B per stored entry + 64 B per point"}
+                "traffic": measured_traffic("attractive_phase", att_src),
+                "model": "8 B per stored entry + 104 B per point"}
 
     cpu = None
     if not args.no_cpu and args.cpu_iters > 0:
@@ -197,6 +260,7 @@ def main():
         "attractive_path": "plain CSR" if args.plain else "locality layout + LDS staging",
         "layout_build_s": layout_s,
         "layout_tiles": None if args.plain else P.tiles,
+        "layout_entries": None if args.plain else P.entries,
         "kernels": kernels,
         "roofline": roof,
         "cpu_baseline": cpu,

@@ -76,6 +76,7 @@ typedef struct bhtsne_layout {
     size_t bytes;
     int64_t tiles;  /* tiles of the (row block x column segment) copy; 0 = row-block path */
     int64_t items;  /* work items of the tiled kernel (runs of tiles sharing a segment) */
+    int64_t entries; /* entries of the sliced copy, padding included (0 without tiles) */
     uint64_t magic;
 } bhtsne_layout;
 
@@ -140,8 +141,8 @@ int bhtsne_step(float *Y, const bhtsne_csr *P, float theta, float exaggeration, 
                 void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Bytes of device memory a layout of P needs (0 if n or nnz is out of range):
- * about 14 bytes per stored entry + 220 bytes per point (a row-sorted copy
- * and a tiled copy with 16-bit column offsets). */
+ * about 15.5 bytes per stored entry + 560 bytes per point (a row-sorted copy,
+ * and room for a sliced copy with 16-bit column offsets and its tables). */
 size_t bhtsne_layout_size(int64_t n, int64_t nnz);
 
 /* Build a locality layout of P (once per matrix; may be rebuilt as Y evolves).
@@ -149,10 +150,13 @@ size_t bhtsne_layout_size(int64_t n, int64_t nnz);
  * Y); the copy stores P's rows in that order with renumbered columns, so the
  * columns of consecutive rows fall into compact index windows.  When every
  * block of 1024 rows spans at most 16 windows of 16384 columns, a second,
- * tiled copy groups each row's entries by window so that one window of Y in
- * LDS serves all 1024 rows (out->tiles > 0).  The
- * gradient does not depend on the order; only the speed of the attractive
- * step does.
+ * sliced copy is built: for each (row block, window) tile the rows are sorted
+ * by their number of entries in the window and cut into slices of 64 rows,
+ * stored entry-major, so that one window of Y in LDS serves many tiles and
+ * every load is contiguous (out->tiles > 0, out->items > 0).  The copy is
+ * skipped when its padding would exceed a quarter of nnz plus one chunk per
+ * slice.  The gradient does not depend on the order; only the speed of the
+ * attractive step does.
  *   P      the matrix (as for bhtsne_gradient; nnz < 2^31).
  *   Y      device, n x 2, nullable: without it points keep their index order
  *          inside a component.

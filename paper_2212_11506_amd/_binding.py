@@ -33,7 +33,7 @@ class _Csr(C.Structure):
 
 class _Layout(C.Structure):
     _fields_ = [("n", C.c_int64), ("nnz", C.c_int64), ("mem", C.c_void_p), ("bytes", C.c_size_t),
-                ("tiles", C.c_int64), ("items", C.c_int64), ("magic", C.c_uint64)]
+                ("tiles", C.c_int64), ("items", C.c_int64), ("entries", C.c_int64), ("magic", C.c_uint64)]
 
 
 class _Stats(C.Structure):
@@ -171,6 +171,10 @@ class Layout:
     @property
     def items(self) -> int:
         return int(self._s.items)
+
+    @property
+    def entries(self) -> int:
+        return int(self._s.entries)
 
     @property
     def struct(self):

@@ -295,6 +295,7 @@ int bhtsne_layout_build(const bhtsne_csr *P, const float *Y, void *layout_mem, s
     const bool tiled = plan.tiled && tile_path_enabled();
     out->tiles = tiled ? plan.tiles : 0;
     out->items = tiled ? plan.items : 0;
+    out->entries = tiled ? plan.entries : 0;
     out->magic = kLayoutMagic;
     return BHTSNE_OK;
 }

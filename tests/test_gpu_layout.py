@@ -262,6 +262,7 @@ def test_tiled_copy_reproduces_p():
             t, j = divmod(int(tj), SLICES)
             assert uk[d] == (int(rlen[t][tperm[t][j * SLICE]]) + 3) // 4
     assert seen.all()
+    assert lay.entries == chunk * CHUNK
     cost = [int(uk[iu[i, 0]:iu[i, 2]].sum()) for i in range(I)]
     assert cost == sorted(cost, reverse=True)  # largest item first
     # the sliced copy holds exactly P (padding carries zero values)
