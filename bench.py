@@ -183,8 +183,13 @@ def main():
         log(f"[bench] replay identical to timed run: {same}")
         inter_total = int(sum(counts)) if same else None
 
+    # per phase: time per launch from the library's hipEvent pairs; with a
+    # layout the attractive phase runs on a second stream beside the sort, tree
+    # and repulsive phases, so phase times add up to more than a step
     kernels = {}
     for name, (ms, cnt) in phases.items():
+        if cnt == 0:
+            continue
         per = ms / max(cnt, 1)
         kernels[name] = {"ms_per_launch": per, "launches": cnt}
     rep_ms = kernels["repulsive"]["ms_per_launch"]
@@ -201,12 +206,18 @@ def main():
         # the per-interaction byte model (16 B per summary or point + 20 B per
         # point): nodes come from caches, so this exceeds what HBM moves
         rep["model16_gbs"] = (16.0 * per_launch + 20.0 * n) / (rep_ms * 1e-3) / 1e9
-    # attraction and the update: 8 B per stored entry (column, value), 32 B per
-    # point for the row pointers, y_i and the output, and 72 B per point for the
-    # gradient assembly and update
-    att_bytes = 8.0 * nnz + 104.0 * n
+    # attraction: 8 B per stored entry (column, value) and 32 B per point (row
+    # pointers, y_i, output); with the plain CSR path the phase also holds the
+    # gradient assembly and update, 72 B per point, which the layout path times
+    # as its own phase
+    att_bytes = 8.0 * nnz + (104.0 if args.plain else 32.0) * n
     kernels["attractive"]["gbs"] = att_bytes / (att_ms * 1e-3) / 1e9
     kernels["attractive"]["frac_hbm"] = kernels["attractive"]["gbs"] / HBM_PEAK_GBS
+    if kernels.get("update", {}).get("launches"):
+        upd = kernels["update"]
+        upd["gbs"] = 72.0 * n / (upd["ms_per_launch"] * 1e-3) / 1e9
+        upd["frac_hbm"] = upd["gbs"] / HBM_PEAK_GBS
+        upd["traffic"] = measured_traffic("update_kernel", att_src)
     dominant = max(("repulsive", "attractive"), key=lambda k: kernels[k]["ms_per_launch"])
     if dominant == "repulsive" and inter_total is not None:
         roof = {"kernel": "repulsive", "bound": "alu", "achieved": rep["tflops"], "peak": ALU_PEAK_TFLOPS,
@@ -217,8 +228,8 @@ def main():
     else:
         roof = {"kernel": "attractive", "bound": "hbm", "achieved": kernels["attractive"]["gbs"],
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": kernels["attractive"]["frac_hbm"],
-                "traffic": measured_traffic("attractive_phase", att_src),
-                "model": "8 B per stored entry + 104 B per point"}
+                "traffic": measured_traffic("attract_sell_kernel" if not args.plain else "attract_kernel", att_src),
+                "model": "8 B per stored entry + %d B per point" % (104 if args.plain else 32)}
 
     cpu = None
     if not args.no_cpu and args.cpu_iters > 0:

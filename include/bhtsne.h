@@ -96,12 +96,13 @@ enum {
     BHTSNE_PHASE_SORT = 1,        /* radix sort of the codes + gather of Y */
     BHTSNE_PHASE_TREE = 2,        /* quadtree build + summaries */
     BHTSNE_PHASE_REPULSIVE = 3,   /* Barnes-Hut traversal + Z */
-    BHTSNE_PHASE_ATTRACTIVE = 4,  /* CSR attractive forces + gradient + update */
-    BHTSNE_NUM_PHASES = 5
+    BHTSNE_PHASE_ATTRACTIVE = 4,  /* attractive forces (plain CSR: with the gradient + update) */
+    BHTSNE_PHASE_UPDATE = 5,      /* gradient + update of the layout calls */
+    BHTSNE_NUM_PHASES = 6
 };
 
 typedef struct bhtsne_timing {
-    double ms[BHTSNE_NUM_PHASES];   /* summed GPU time per phase (hipEvent pairs on the call's stream) */
+    double ms[BHTSNE_NUM_PHASES];   /* summed GPU time per phase (hipEvent pairs on the phase's stream) */
     int64_t count[BHTSNE_NUM_PHASES];
 } bhtsne_timing;
 
@@ -171,7 +172,12 @@ int bhtsne_layout_build(const bhtsne_csr *P, const float *Y, void *layout_mem, s
 /* bhtsne_gradient / bhtsne_step taking P through a layout built by
  * bhtsne_layout_build (the original CSR arrays are not read).  Arguments,
  * outputs (in the caller's point order) and errors as the plain calls;
- * BHTSNE_EINVAL also for a handle that bhtsne_layout_build did not fill. */
+ * BHTSNE_EINVAL also for a handle that bhtsne_layout_build did not fill.
+ * The attractive forces run on a stream the library keeps per device (default
+ * priority), forked from `stream` after the Morton codes and joined back
+ * before the gradient assembly, so they overlap the sort, tree and repulsive
+ * phases; to the caller the call is ordered on `stream` as usual.  The
+ * device is the current one, which must be the device of `stream`. */
 int bhtsne_gradient_layout(const float *Y, const bhtsne_layout *layout, float theta, float exaggeration,
                            float *grad, double *Z, void *workspace, size_t workspace_bytes, hipStream_t stream);
 int bhtsne_step_layout(float *Y, const bhtsne_layout *layout, float theta, float exaggeration, float learning_rate,

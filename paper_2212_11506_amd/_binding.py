@@ -17,7 +17,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB = os.path.join(_HERE, "lib", "libbhtsne.so")
 
 BHTSNE_OK, BHTSNE_EINVAL, BHTSNE_EWORKSPACE, BHTSNE_ENONFINITE, BHTSNE_EDEVICE = 0, -1, -2, -3, -4
-PHASES = ("bbox_morton", "sort", "tree", "repulsive", "attractive")
+PHASES = ("bbox_morton", "sort", "tree", "repulsive", "attractive", "update")
 
 
 class BhtsneError(RuntimeError):
@@ -42,7 +42,7 @@ class _Stats(C.Structure):
 
 
 class _Timing(C.Structure):
-    _fields_ = [("ms", C.c_double * 5), ("count", C.c_int64 * 5)]
+    _fields_ = [("ms", C.c_double * 6), ("count", C.c_int64 * 6)]
 
 
 _lib = None

@@ -110,16 +110,18 @@ int read_header(const void *ws, Header *h, hipStream_t st)
     return BHTSNE_OK;
 }
 
-// Box, codes, sort, tree and summaries.  `rank` (nullable) puts the private
-// copy of Y in a layout's order.
-void build_tree(const float *Y, int64_t n, float theta, const uint32_t *rank, void *ws, const Layout &L,
-                const TreeDebug &dbg, hipStream_t st)
+// Box and codes.  `rank` (nullable) puts the private copy of Y in a layout's order.
+void build_codes(const float *Y, int64_t n, const uint32_t *rank, void *ws, const Layout &L, hipStream_t st)
 {
-    {
-        PhaseTimer pt(BHTSNE_PHASE_BBOX_MORTON, st);
-        launch_bbox(Y, n, ws, L, st);
-        launch_morton(Y, n, rank, ws, L, st);
-    }
+    PhaseTimer pt(BHTSNE_PHASE_BBOX_MORTON, st);
+    launch_bbox(Y, n, ws, L, st);
+    launch_morton(Y, n, rank, ws, L, st);
+}
+
+// Sort, tree and summaries.
+void build_sorted_tree(const float *Y, int64_t n, float theta, void *ws, const Layout &L, const TreeDebug &dbg,
+                       hipStream_t st)
+{
     {
         PhaseTimer pt(BHTSNE_PHASE_SORT, st);
         launch_sort(n, Y, ws, L, st);
@@ -128,6 +130,98 @@ void build_tree(const float *Y, int64_t n, float theta, const uint32_t *rank, vo
         PhaseTimer pt(BHTSNE_PHASE_TREE, st);
         launch_tree(n, theta, ws, L, dbg, st);
     }
+}
+
+void build_tree(const float *Y, int64_t n, float theta, const uint32_t *rank, void *ws, const Layout &L,
+                const TreeDebug &dbg, hipStream_t st)
+{
+    build_codes(Y, n, rank, ws, L, st);
+    build_sorted_tree(Y, n, theta, ws, L, dbg, st);
+}
+
+// ------------------------------------------------------------------ side stream
+// A second stream per device (default priority) for work that does not depend
+// on the tree: the attractive forces of the layout calls.  Forked from the
+// caller's stream with one event and joined back with another; the mutex keeps
+// the enqueue of a fork .. join sequence whole when several threads call in.
+struct Side {
+    std::mutex mu;
+    hipStream_t st = nullptr;
+    hipEvent_t fork = nullptr, join = nullptr;
+    bool failed = false;
+};
+
+constexpr int kMaxDevices = 64;
+
+Side *side_stream()
+{
+    static Side sides[kMaxDevices];
+    static std::mutex create_mu;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    Side &x = sides[dev];
+    std::lock_guard<std::mutex> g(create_mu);
+    if (x.failed) return nullptr;
+    if (!x.st) {
+        if (hipStreamCreateWithFlags(&x.st, hipStreamNonBlocking) != hipSuccess ||
+            hipEventCreateWithFlags(&x.fork, hipEventDisableTiming) != hipSuccess ||
+            hipEventCreateWithFlags(&x.join, hipEventDisableTiming) != hipSuccess) {
+            x.failed = true;
+            return nullptr;
+        }
+    }
+    return &x;
+}
+
+// BHTSNE_OVERLAP=0 runs the attractive forces on the caller's stream instead
+bool overlap_enabled()
+{
+    static bool v = [] {
+        const char *e = std::getenv("BHTSNE_OVERLAP");
+        return !(e && std::atoi(e) == 0);
+    }();
+    return v;
+}
+
+// where the attractive forces fork off: 0 after the codes, 1 after the sort,
+// 2 after the tree (BHTSNE_FORK; default 0).  Measured at 1.3M points the
+// sort, a chain of latency-bound passes, does best on the CUs the attractive
+// kernel leaves free (its blocks cannot share a CU's LDS with one), and the
+// tree and the repulsive walk lose more than they hide when forked later.
+int fork_point()
+{
+    static int v = [] {
+        const char *e = std::getenv("BHTSNE_FORK");
+        int x = e ? std::atoi(e) : 0;
+        return x < 0 ? 0 : (x > 2 ? 2 : x);
+    }();
+    return v;
+}
+
+int device_cus()
+{
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+        return 256;
+    return cus;
+}
+
+// Blocks of the persistent sliced attractive kernel (one per CU it holds):
+// all CUs when it runs alone; beside the tree phases a share of them
+// (BHTSNE_ATTRACT_CUS, percent of the CUs, default 75), so that the critical
+// path keeps CUs of its own; 0 gives one block per item.
+int attract_blocks(bool beside, int items)
+{
+    static int pct = [] {
+        const char *e = std::getenv("BHTSNE_ATTRACT_CUS");
+        int x = e ? std::atoi(e) : 75;
+        return x < 0 ? 0 : (x > 100 ? 100 : x);
+    }();
+    if (beside && pct == 0) return items > 0 ? items : 1;
+    const int cus = device_cus();
+    const int b = beside ? cus * pct / 100 : cus;
+    return b < 1 ? 1 : b;
 }
 
 int finish(double *Z, void *ws, hipStream_t st)
@@ -199,15 +293,49 @@ int run_layout(float *Y, const bhtsne_layout *lay, float theta, const StepArgs &
     const int64_t n = lay->n;
     const Layout L = make_layout(n, lay->nnz);
     const LayoutView lv = layout_view(lay->mem, n, lay->nnz);
-    build_tree(Y, n, theta, lv.rank, ws, L, TreeDebug{}, st);
+    const int tiles = int(lay->tiles);
+    // the attractive forces need only the layout-order copy of Y written with
+    // the codes, so they can run beside the sort, tree and repulsive phases
+    const int fork = fork_point();
+    build_codes(Y, n, lv.rank, ws, L, st);
+    if (fork >= 1) {
+        PhaseTimer pt(BHTSNE_PHASE_SORT, st);
+        launch_sort(n, Y, ws, L, st);
+    }
+    if (fork >= 2) {
+        PhaseTimer pt(BHTSNE_PHASE_TREE, st);
+        launch_tree(n, theta, ws, L, TreeDebug{}, st);
+    }
+    Side *side = overlap_enabled() ? side_stream() : nullptr;
+    std::unique_lock<std::mutex> lk;
+    if (side) {
+        lk = std::unique_lock<std::mutex>(side->mu);
+        if (hipEventRecord(side->fork, st) != hipSuccess || hipStreamWaitEvent(side->st, side->fork, 0) != hipSuccess)
+            return BHTSNE_EDEVICE;
+    }
+    const hipStream_t sa = side ? side->st : st;
+    {
+        PhaseTimer pt(BHTSNE_PHASE_ATTRACTIVE, sa);
+        launch_attract_layout(lv, n, lay->nnz, tiles, int(lay->items), attract_blocks(side != nullptr, int(lay->items)),
+                              stage_segments(), ws, L, sa);
+    }
+    if (side && hipEventRecord(side->join, sa) != hipSuccess) return BHTSNE_EDEVICE;
+    if (fork < 1) {
+        PhaseTimer pt(BHTSNE_PHASE_SORT, st);
+        launch_sort(n, Y, ws, L, st);
+    }
+    if (fork < 2) {
+        PhaseTimer pt(BHTSNE_PHASE_TREE, st);
+        launch_tree(n, theta, ws, L, TreeDebug{}, st);
+    }
     {
         PhaseTimer pt(BHTSNE_PHASE_REPULSIVE, st);
         launch_repulsive(n, ws, L, st);
     }
+    if (side && hipStreamWaitEvent(st, side->join, 0) != hipSuccess) return BHTSNE_EDEVICE;
+    if (lk.owns_lock()) lk.unlock();
     {
-        PhaseTimer pt(BHTSNE_PHASE_ATTRACTIVE, st);
-        const int tiles = int(lay->tiles);
-        launch_attract_layout(lv, n, lay->nnz, tiles, int(lay->items), stage_segments(), ws, L, st);
+        PhaseTimer pt(BHTSNE_PHASE_UPDATE, st);
         launch_update(lv, n, tiles > 0, a, Y, update, gains, grad, ws, L, st);
     }
     return finish(Z, ws, st);

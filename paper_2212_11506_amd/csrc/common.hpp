@@ -64,7 +64,8 @@ struct Header {
     uint32_t tile_counter[kSortPasses];
     uint32_t ticket_bbox;
     uint32_t ticket_rep;
-    uint32_t pad[6];
+    uint32_t attract_next; // next item of the persistent attractive kernel
+    uint32_t pad[5];
 };
 
 // A node of the pre-order tree: summary record + meta word.

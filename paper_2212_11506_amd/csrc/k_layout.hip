@@ -661,117 +661,126 @@ __global__ __launch_bounds__(kTileBlock) void attract_sell_kernel(
     const int32_t *__restrict__ tile_blk, const int32_t *__restrict__ tile_seg, const int32_t *__restrict__ tile_k,
     const int32_t *__restrict__ unit_chunks, const int32_t *__restrict__ unit_tj, const uint16_t *__restrict__ tperm,
     const uint16_t *__restrict__ tcol, const float *__restrict__ tval, const float2 *__restrict__ ylay,
-    int32_t nitems, float2 *__restrict__ partial)
+    int32_t nitems, Header *__restrict__ hdr, float2 *__restrict__ partial)
 {
     __shared__ v4f sy4[kTileSeg / 2];
     __shared__ int32_t s_row0[kItemMaxTiles], s_k[kItemMaxTiles];
-    __shared__ int32_t s_K[kItemMaxUnits], s_tj[kItemMaxUnits];
+    // per stored unit of the item: chunks (a run holds at most kTileSeg entries)
+    // and (tile - t0) * 16 + slice, both below 2^16
+    static_assert(kTileSeg / 4 < 65536 && kItemMaxUnits <= 65536, "unit tables are 16-bit");
+    __shared__ uint16_t s_K[kItemMaxUnits], s_tj[kItemMaxUnits];
+    __shared__ uint32_t s_item;
     const float2 *sy = reinterpret_cast<const float2 *>(sy4);
-    // items are stored largest first and taken in launch order
-    const uint32_t it = blockIdx.x;
-    if (it >= uint32_t(nitems)) return; // block-uniform, before the barrier
-    const int2 itr = item_tiles[it];
-    const int32_t t0 = itr.x, t1 = itr.y;
-    const int32_t sg = tile_seg[t0];
-    const int4 iu = item_units[it]; // units [x, z) of the item; those from y on have no entries
-    const int w = __builtin_amdgcn_readfirstlane(int(threadIdx.x) / kWave), lane = lane_id();
-    const int4 wu = wave_units[int64_t(it) * kSellWaves + w]; // units [x, y), chunks [z, z + w)
-    const int32_t G = wu.w;
+    // a fixed grid takes the items (stored largest first) from a counter; the
+    // barrier at the top also keeps the LDS of one item until every wave is done
+    for (;;) {
+        if (threadIdx.x == 0) s_item = atomicAdd(&hdr->attract_next, 1u);
+        __syncthreads();
+        const uint32_t it = s_item;
+        if (it >= uint32_t(nitems)) break; // block-uniform
+        const int2 itr = item_tiles[it];
+        const int32_t t0 = itr.x, t1 = itr.y;
+        const int32_t sg = tile_seg[t0];
+        const int4 iu = item_units[it]; // units [x, z) of the item; those from y on have no entries
+        const int w = __builtin_amdgcn_readfirstlane(int(threadIdx.x) / kWave), lane = lane_id();
+        const int4 wu = wave_units[int64_t(it) * kSellWaves + w]; // units [x, y), chunks [z, z + w)
+        const int32_t G = wu.w;
 
-    // this wave's chunk g (clamped: loads past the end are issued and unused)
-    const uint16_t *tc = tcol + int64_t(wu.z) * kSellChunk + 4 * lane;
-    const float *tv = tval + int64_t(wu.z) * kSellChunk + 4 * lane;
-    v4u16 c[kSellRing];
-    v4f p[kSellRing];
-    auto issue = [&](int x, int32_t g) {
-        const int64_t at = int64_t(g < G ? g : (G > 0 ? G - 1 : 0)) * kSellChunk;
-        c[x] = *reinterpret_cast<const v4u16 *>(tc + at);
-        p[x] = *reinterpret_cast<const v4f *>(tv + at);
-    };
-    // the segment of Y (8 independent 16-byte loads per thread) and the first
-    // chunks are in flight together
-    static_assert(kYPad >= kTileSeg + 2 && kYPad >= kTileRows, "padding must cover one segment and one block");
-    constexpr int kStage = kTileSeg / 2 / kTileBlock;
-    v4f stage[kStage];
-    {
-        const v4f *src = reinterpret_cast<const v4f *>(ylay) + int64_t(sg) * (kTileSeg / 2) + threadIdx.x;
+        // this wave's chunk g (clamped: loads past the end are issued and unused)
+        const uint16_t *tc = tcol + int64_t(wu.z) * kSellChunk + 4 * lane;
+        const float *tv = tval + int64_t(wu.z) * kSellChunk + 4 * lane;
+        v4u16 c[kSellRing];
+        v4f p[kSellRing];
+        auto issue = [&](int x, int32_t g) {
+            const int64_t at = int64_t(g < G ? g : (G > 0 ? G - 1 : 0)) * kSellChunk;
+            c[x] = *reinterpret_cast<const v4u16 *>(tc + at);
+            p[x] = *reinterpret_cast<const v4f *>(tv + at);
+        };
+        // the segment of Y (8 independent 16-byte loads per thread) and the first
+        // chunks are in flight together
+        static_assert(kYPad >= kTileSeg + 2 && kYPad >= kTileRows, "padding must cover one segment and one block");
+        constexpr int kStage = kTileSeg / 2 / kTileBlock;
+        v4f stage[kStage];
+        {
+            const v4f *src = reinterpret_cast<const v4f *>(ylay) + int64_t(sg) * (kTileSeg / 2) + threadIdx.x;
 #pragma unroll
-        for (int q = 0; q < kStage; ++q) stage[q] = src[q * kTileBlock];
-    }
-#pragma unroll
-    for (int x = 0; x < kSellRing; ++x) issue(x, x);
-    v4f *sv = reinterpret_cast<v4f *>(sy4);
-#pragma unroll
-    for (int q = 0; q < kStage; ++q) sv[q * kTileBlock + threadIdx.x] = stage[q];
-    for (int32_t j = threadIdx.x; j < t1 - t0; j += kTileBlock) {
-        s_row0[j] = tile_blk[t0 + j] * kTileRows;
-        s_k[j] = tile_k[t0 + j];
-    }
-    for (int32_t j = threadIdx.x; j < iu.z - iu.x; j += kTileBlock) {
-        s_K[j] = unit_chunks[iu.x + j];
-        s_tj[j] = unit_tj[iu.x + j];
-    }
-    __syncthreads();
-
-    // LDS values that are the same in every lane, as scalars
-    auto uni = [](int32_t v) { return __builtin_amdgcn_readfirstlane(v); };
-    // row of this lane in its block for unit u (a load), the first row of the
-    // unit's block, and the unit's partial slot
-    auto unit_rl = [&](int32_t u) {
-        const int32_t tj = uni(s_tj[u - iu.x]), t = tj / kSlicesPerTile, j = tj % kSlicesPerTile;
-        return int32_t(tperm[int64_t(t) * kTileRows + j * kSellSlice + lane]);
-    };
-    auto unit_row0 = [&](int32_t u) { return uni(s_row0[uni(s_tj[u - iu.x]) / kSlicesPerTile - t0]); };
-    auto unit_slot = [&](int32_t u) { return uni(s_k[uni(s_tj[u - iu.x]) / kSlicesPerTile - t0]); };
-
-    // units without entries in their tile's segment: their rows' partials are 0
-    for (int32_t u = iu.y + w; u < iu.z; u += kSellWaves)
-        partial[int64_t(unit_row0(u) + unit_rl(u)) * kTileMaxSeg + unit_slot(u)] = make_float2(0.0f, 0.0f);
-    if (wu.x >= wu.y) return; // no units for this wave (no barrier follows)
-
-    const int32_t ulast = wu.y - 1;
-    int32_t u = wu.x;             // unit being summed (wave-uniform)
-    int32_t uend = uni(s_K[u - iu.x]); // its chunks end at this wave step
-    // rows (layout order) of the current and the next unit, the next-but-one
-    // unit's row in its block (added to its block's first row when it moves up)
-    auto clampu = [&](int32_t x) { return x <= ulast ? x : ulast; };
-    int32_t rowA = unit_row0(u) + unit_rl(u);
-    int32_t rowB = unit_row0(clampu(u + 1)) + unit_rl(clampu(u + 1));
-    int32_t rlC = unit_rl(clampu(u + 2));
-    float2 yA = ylay[rowA], yB = ylay[rowB];
-    // Wait here once for y of the first two units (the last loads issued):
-    // otherwise the loop head, where this entry path meets the back edge,
-    // would wait for them on every trip.  The empty statement only uses the
-    // registers, which makes the compiler complete their loads before it.
-    asm volatile("" ::"v"(yA.x), "v"(yA.y), "v"(yB.x), "v"(yB.y));
-    float fx = 0.0f, fy = 0.0f;
-
-    // one wave step: sum chunk g from ring slot x, refill the slot with chunk
-    // g + kSellRing, and close the unit when g was its last chunk
-    auto step = [&](int x, int32_t g) {
-        const bool live = g < G; // wave-uniform; dead steps only occur after the last chunk
-        float cx = 0.0f, cy = 0.0f;
-#pragma unroll
-        for (int v = 0; v < 4; ++v) attract_add(yA, sy[c[x][v] & (kTileSeg - 1)], p[x][v], cx, cy);
-        fx += live ? cx : 0.0f;
-        fy += live ? cy : 0.0f;
-        issue(x, g + kSellRing);
-        if (live && g + 1 == uend) {
-            partial[int64_t(rowA) * kTileMaxSeg + unit_slot(u)] = make_float2(fx, fy);
-            fx = fy = 0.0f;
-            ++u;
-            if (u <= ulast) uend += uni(s_K[u - iu.x]);
-            rowA = rowB;
-            yA = yB;
-            rowB = unit_row0(clampu(u + 1)) + rlC;
-            yB = ylay[rowB];
-            rlC = unit_rl(clampu(u + 2));
+            for (int q = 0; q < kStage; ++q) stage[q] = src[q * kTileBlock];
         }
-    };
-    for (int32_t g = 0; g < G; g += kSellRing) {
 #pragma unroll
-        for (int x = 0; x < kSellRing; ++x) step(x, g + x);
-    }
+        for (int x = 0; x < kSellRing; ++x) issue(x, x);
+        v4f *sv = reinterpret_cast<v4f *>(sy4);
+#pragma unroll
+        for (int q = 0; q < kStage; ++q) sv[q * kTileBlock + threadIdx.x] = stage[q];
+        for (int32_t j = threadIdx.x; j < t1 - t0; j += kTileBlock) {
+            s_row0[j] = tile_blk[t0 + j] * kTileRows;
+            s_k[j] = tile_k[t0 + j];
+        }
+        for (int32_t j = threadIdx.x; j < iu.z - iu.x; j += kTileBlock) {
+            s_K[j] = uint16_t(unit_chunks[iu.x + j]);
+            s_tj[j] = uint16_t(unit_tj[iu.x + j] - t0 * kSlicesPerTile);
+        }
+        __syncthreads();
+
+        // LDS values that are the same in every lane, as scalars
+        auto uni = [](int32_t v) { return __builtin_amdgcn_readfirstlane(v); };
+        // row of this lane in its block for unit u (a load), the first row of the
+        // unit's block, and the unit's partial slot
+        auto unit_rl = [&](int32_t u) {
+            const int32_t tj = uni(s_tj[u - iu.x]), t = t0 + tj / kSlicesPerTile, j = tj % kSlicesPerTile;
+            return int32_t(tperm[int64_t(t) * kTileRows + j * kSellSlice + lane]);
+        };
+        auto unit_row0 = [&](int32_t u) { return uni(s_row0[uni(s_tj[u - iu.x]) / kSlicesPerTile]); };
+        auto unit_slot = [&](int32_t u) { return uni(s_k[uni(s_tj[u - iu.x]) / kSlicesPerTile]); };
+
+        // units without entries in their tile's segment: their rows' partials are 0
+        for (int32_t u = iu.y + w; u < iu.z; u += kSellWaves)
+            partial[int64_t(unit_row0(u) + unit_rl(u)) * kTileMaxSeg + unit_slot(u)] = make_float2(0.0f, 0.0f);
+        if (wu.x < wu.y) { // this wave has units
+        const int32_t ulast = wu.y - 1;
+        int32_t u = wu.x;             // unit being summed (wave-uniform)
+        int32_t uend = uni(s_K[u - iu.x]); // its chunks end at this wave step
+        // rows (layout order) of the current and the next unit, the next-but-one
+        // unit's row in its block (added to its block's first row when it moves up)
+        auto clampu = [&](int32_t x) { return x <= ulast ? x : ulast; };
+        int32_t rowA = unit_row0(u) + unit_rl(u);
+        int32_t rowB = unit_row0(clampu(u + 1)) + unit_rl(clampu(u + 1));
+        int32_t rlC = unit_rl(clampu(u + 2));
+        float2 yA = ylay[rowA], yB = ylay[rowB];
+        // Wait here once for y of the first two units (the last loads issued):
+        // otherwise the loop head, where this entry path meets the back edge,
+        // would wait for them on every trip.  The empty statement only uses the
+        // registers, which makes the compiler complete their loads before it.
+        asm volatile("" ::"v"(yA.x), "v"(yA.y), "v"(yB.x), "v"(yB.y));
+        float fx = 0.0f, fy = 0.0f;
+
+        // one wave step: sum chunk g from ring slot x, refill the slot with chunk
+        // g + kSellRing, and close the unit when g was its last chunk
+        auto step = [&](int x, int32_t g) {
+            const bool live = g < G; // wave-uniform; dead steps only occur after the last chunk
+            float cx = 0.0f, cy = 0.0f;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) attract_add(yA, sy[c[x][v] & (kTileSeg - 1)], p[x][v], cx, cy);
+            fx += live ? cx : 0.0f;
+            fy += live ? cy : 0.0f;
+            issue(x, g + kSellRing);
+            if (live && g + 1 == uend) {
+                partial[int64_t(rowA) * kTileMaxSeg + unit_slot(u)] = make_float2(fx, fy);
+                fx = fy = 0.0f;
+                ++u;
+                if (u <= ulast) uend += uni(s_K[u - iu.x]);
+                rowA = rowB;
+                yA = yB;
+                rowB = unit_row0(clampu(u + 1)) + rlC;
+                yB = ylay[rowB];
+                rlC = unit_rl(clampu(u + 2));
+            }
+        };
+        for (int32_t g = 0; g < G; g += kSellRing) {
+#pragma unroll
+            for (int x = 0; x < kSellRing; ++x) step(x, g + x);
+        }
+        } // this wave has units
+    }     // items
 }
 
 // ------------------------------------------------------------------ gradient + update
@@ -1097,15 +1106,15 @@ static void launch_staged(const LayoutView &lv, int64_t n, int64_t nnz, int max_
                                                                    n, max_segs, at<float2>(ws, L.fattr));
 }
 
-void launch_attract_layout(const LayoutView &lv, int64_t n, int64_t nnz, int tiles, int items, int max_segs, void *ws,
-                           const Layout &L, hipStream_t st)
+void launch_attract_layout(const LayoutView &lv, int64_t n, int64_t nnz, int tiles, int items, int blocks,
+                           int max_segs, void *ws, const Layout &L, hipStream_t st)
 {
     if (tiles > 0) {
-        const unsigned grid = unsigned(items);
+        const unsigned grid = unsigned(blocks < items ? blocks : items);
         attract_sell_kernel<<<grid, kTileBlock, 0, st>>>(lv.item_tiles, lv.item_units, lv.wave_units, lv.tile_blk,
                                                          lv.tile_seg, lv.tile_k, lv.unit_chunks, lv.unit_tj,
                                                          lv.tperm, lv.tcol, lv.tval, at<float2>(ws, L.ycopy), items,
-                                                         at<float2>(ws, L.partial));
+                                                         at<Header>(ws, L.header), at<float2>(ws, L.partial));
         return;
     }
     // 1024 threads (one block per CU: the segment fills 128 KB of LDS), 2 rows per lane group

@@ -132,6 +132,7 @@ __global__ __launch_bounds__(256) void bbox_final_kernel(const float *__restrict
         for (int k = 0; k < kSortPasses; ++k) hdr->tile_counter[k] = 0;
         hdr->ticket_bbox = 0;
         hdr->ticket_rep = 0;
+        hdr->attract_next = 0;
     }
 }
 
@@ -233,6 +234,8 @@ __device__ inline uint32_t peek(const uint32_t *p)
 {
     return __hip_atomic_load(const_cast<uint32_t *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+
+static_assert(kSortBlock == kRadix, "thread t owns digit t in the scans and the look-back");
 
 template <bool kFirst, bool kLast>
 __global__ __launch_bounds__(kSortBlock) void onesweep_kernel(

@@ -77,8 +77,9 @@ int launch_layout_build(const int64_t *row_ptr, const int32_t *col, const float 
                         hipStream_t st);
 // Attractive forces through a layout: the streaming tile kernel when the
 // layout has tiles (tiles > 0, items > 0), else the row-block kernel.
-void launch_attract_layout(const LayoutView &lv, int64_t n, int64_t nnz, int tiles, int items, int max_segs, void *ws,
-                           const Layout &L, hipStream_t st);
+// `blocks`: grid of the persistent sliced kernel (items are taken from a counter)
+void launch_attract_layout(const LayoutView &lv, int64_t n, int64_t nnz, int tiles, int items, int blocks,
+                           int max_segs, void *ws, const Layout &L, hipStream_t st);
 void launch_update(const LayoutView &lv, int64_t n, int tiled, const StepArgs &a, float *Y, float *upd, float *gains,
                    float *grad, void *ws, const Layout &L, hipStream_t st);
 

@@ -343,14 +343,21 @@ def test_nonfinite_input_is_reported():
 def test_timing_records_every_phase():
     inp = synth.make_inputs(0)
     Y, P = dev_y(inp.Y), dev_p(inp.row_ptr, inp.col, inp.val)
+    lay = bh.Layout(P, Y)
     bh.timing_read(reset=True)
     bh.timing_enable(True)
     try:
         for _ in range(3):
             bh.gradient(Y, P, 0.5, 12.0, return_z=False)
-        t = bh.timing_read(reset=True)
+        plain = bh.timing_read(reset=True)
+        for _ in range(3):
+            bh.gradient(Y, lay, 0.5, 12.0, return_z=False)
+        layout = bh.timing_read(reset=True)
     finally:
         bh.timing_enable(False)
+    # the plain path assembles the gradient inside the attractive phase
     for name in bh.PHASES:
-        ms, cnt = t[name]
-        assert cnt == 3 and ms > 0.0, (name, t[name])
+        ms, cnt = plain[name]
+        assert (cnt == 0) if name == "update" else (cnt == 3 and ms > 0.0), (name, plain[name])
+        ms, cnt = layout[name]
+        assert cnt == 3 and ms > 0.0, (name, layout[name])
