@@ -45,11 +45,14 @@ def parse():
     ap.add_argument("--workload", type=int, default=2)
     ap.add_argument("--n", type=int, default=None, help="override the workload size")
     ap.add_argument("--theta", type=float, default=0.5)
-    ap.add_argument("--cpu-iters", type=int, default=8, help="oracle iterations for the CPU baseline")
+    ap.add_argument("--cpu-iters", type=int, default=16, help="oracle iterations for the CPU baseline")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-count", action="store_true", help="skip the interaction-counting replay")
     ap.add_argument("--plain", action="store_true",
                     help="attractive step straight from the CSR arrays (no locality layout)")
+    ap.add_argument("--no-overlap", action="store_true",
+                    help="attractive forces on the main stream, not beside the sort, tree and walk "
+                         "(for counter collection, which takes one dispatch at a time)")
     ap.add_argument("--copy-calibrate", action="store_true",
                     help="only run device-to-device copies of 1 GiB (for scaling HBM counters)")
     return ap.parse_args()
@@ -98,6 +101,8 @@ def measured_traffic(kernel, sources):
 
 def main():
     args = parse()
+    if args.no_overlap:
+        os.environ["BHTSNE_OVERLAP"] = "0"  # read once by the library, at its first step
     if args.copy_calibrate:
         copy_calibrate()
         return

@@ -308,21 +308,38 @@ __global__ __launch_bounds__(kSortBlock) void onesweep_kernel(
     uint32_t dbase = block_exclusive_scan256(h, s_scan, nullptr);
     uint32_t excl = 0;
     if (tile > 0) {
+        // look back kLook predecessors per round trip: add their aggregates
+        // until an inclusive prefix; stop at a tile that has not published yet
+        // and read again from there
+        constexpr int kLook = 8;
         int64_t tt = int64_t(tile) - 1;
         uint32_t spins = 0;
-        while (tt >= 0) {
-            uint32_t s = peek(status + tt * kRadix + d);
-            if ((s & ~kValueMask) == 0) {
+        for (;;) {
+            uint32_t sv[kLook];
+#pragma unroll
+            for (int k = 0; k < kLook; ++k) sv[k] = tt - k >= 0 ? peek(status + (tt - k) * kRadix + d) : 0u;
+            int used = 0;
+            bool found = false;
+#pragma unroll
+            for (int k = 0; k < kLook; ++k) {
+                if (used != k || tt - k < 0 || (sv[k] & ~kValueMask) == 0) continue; // stopped earlier
+                excl += sv[k] & kValueMask;
+                used = k + 1;
+                if (sv[k] & kFlagInclusive) {
+                    found = true;
+                    used = kLook + 1; // stop consuming
+                }
+            }
+            if (found) break;
+            tt -= used;
+            if (tt < 0) break; // cannot happen: tile 0 publishes an inclusive prefix
+            if (used < kLook) { // tile tt has not published yet
                 if (++spins > kSpinLimit) { // a predecessor never published: give up loudly
                     atomicOr(&hdr->flags, kErrLookback);
                     break;
                 }
                 __builtin_amdgcn_s_sleep(1);
-                continue;
             }
-            excl += s & kValueMask;
-            if (s & kFlagInclusive) break;
-            --tt;
         }
         publish(my, kFlagInclusive | (excl + tot));
     }

@@ -69,12 +69,17 @@ def _case(name):
         return np.stack([t, t], 1)
     if name == "late":
         return synth.make_inputs(4, n=20000).Y
+    if name == "reps40":  # 3000 points, each 40 times, shuffled: 3000 runs of equal codes
+        y = np.repeat(synth.random_y(3000, seed=13, scale=1.0), 40, axis=0)
+        return y[np.random.default_rng(13).permutation(y.shape[0])]
+    if name == "identical20k":  # one run of equal codes longer than a block sorts in LDS
+        return np.full((20000, 2), -2.5, np.float32)
     raise KeyError(name)
 
 
 SORT_CASES = ["c0", "rand2", "rand3", "rand63", "rand64", "rand65", "rand2047", "rand2048",
               "rand2049", "rand4097", "rand70001", "dups", "identical", "identical2", "huge",
-              "tiny", "outlier", "line", "late"]
+              "tiny", "outlier", "line", "late", "reps40", "identical20k"]
 
 
 @pytest.mark.parametrize("case", SORT_CASES)
