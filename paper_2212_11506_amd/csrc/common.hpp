@@ -21,7 +21,9 @@ constexpr int kScanBlock = 256;
 constexpr int kScanItems = 16;
 constexpr int kScanTile = kScanBlock * kScanItems;
 constexpr int kBBoxBlocks = 512;
-constexpr int kRepBlock = 256;
+// repulsive walk: 16 waves of consecutive points per block share one CU, so
+// their walks, which overlap in most nodes, share the scalar cache's lines
+constexpr int kRepBlock = 1024;
 constexpr uint32_t kLeafBit = 0x80000000u;   // meta: leaf (single point or bucket)
 constexpr uint32_t kSingleBit = 0x40000000u; // meta: single-point leaf
 constexpr uint32_t kIndexMask = 0x3fffffffu; // meta: begin of a leaf

@@ -36,10 +36,11 @@ __device__ inline float keep_lanes(uint64_t m, float x)
     asm("v_cndmask_b32_e64 %0, 0, %1, %2" : "=v"(r) : "v"(x), "s"(m));
     return r;
 }
-__device__ inline uint32_t keep_lanes_u(uint64_t m, uint32_t x)
+// x in the lanes whose bit of m is set, else y
+__device__ inline uint32_t pick_lanes_u(uint64_t m, uint32_t x, uint32_t y)
 {
     uint32_t r;
-    asm("v_cndmask_b32_e64 %0, 0, %1, %2" : "=v"(r) : "v"(x), "s"(m));
+    asm("v_cndmask_b32_e64 %0, %1, %2, %3" : "=v"(r) : "v"(y), "v"(x), "s"(m));
     return r;
 }
 
@@ -93,8 +94,11 @@ __global__ __launch_bounds__(kRepBlock) void repulsive_kernel(
         const uint64_t rej = act & ~take;
         // the skip index of an internal cell, 0 for a leaf (kLeafBit is the sign bit)
         const uint32_t skip = m & ~uint32_t(int32_t(m) >> 31);
-        // accepting lanes park until the walk leaves an internal cell
-        resume = max(resume, keep_lanes_u(take, skip));
+        // accepting lanes park until the walk leaves an internal cell.  A
+        // lane that takes a node is active, so its old resume index is at most
+        // cur and the new one (skip, or 0 after a leaf) keeps every later node
+        // that the old one allowed: no max is needed
+        resume = pick_lanes_u(take, skip, resume);
         // a skip index lies beyond its cell: skip when no lane descends
         cur = rej ? cur + 1 : max(cur + 1, skip);
     }

@@ -693,8 +693,10 @@ __global__ __launch_bounds__(kTileBlock) void attract_sell_kernel(
         v4f p[kSellRing];
         auto issue = [&](int x, int32_t g) {
             const int64_t at = int64_t(g < G ? g : (G > 0 ? G - 1 : 0)) * kSellChunk;
-            c[x] = *reinterpret_cast<const v4u16 *>(tc + at);
-            p[x] = *reinterpret_cast<const v4f *>(tv + at);
+            // read once per iteration: streamed past the caches' retained lines, which
+            // the sort and tree running beside this kernel keep using
+            c[x] = __builtin_nontemporal_load(reinterpret_cast<const v4u16 *>(tc + at));
+            p[x] = __builtin_nontemporal_load(reinterpret_cast<const v4f *>(tv + at));
         };
         // the segment of Y (8 independent 16-byte loads per thread) and the first
         // chunks are in flight together
