@@ -336,7 +336,7 @@ int run_layout(float *Y, const bhtsne_layout *lay, float theta, const StepArgs &
     if (lk.owns_lock()) lk.unlock();
     {
         PhaseTimer pt(BHTSNE_PHASE_UPDATE, st);
-        launch_update(lv, n, tiles > 0, a, Y, update, gains, grad, ws, L, st);
+        launch_update(lv, n, a, Y, update, gains, grad, ws, L, st);
     }
     return finish(Z, ws, st);
 }

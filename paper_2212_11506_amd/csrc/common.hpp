@@ -127,7 +127,8 @@ inline Layout make_layout(int64_t n, int64_t nnz)
     L.meta = take(4 * size_t(2 * n));
     L.frep = take(8 * size_t(n));
     L.fattr = take(8 * size_t(n));
-    // per-tile partial attractive sums: up to kTileMaxSeg tiles per row block
+    // partial attractive sums, one per (tile, sorted row slot): up to
+    // kTileMaxSeg tiles of kTileRows rows per row block
     L.partial = take(8 * size_t((n + kTileRows - 1) / kTileRows) * kTileRows * kTileMaxSeg);
     L.zpart = take(8 * size_t(L.rep_blocks));
     L.ipart = take(8 * size_t(L.rep_blocks));

@@ -646,11 +646,15 @@ __global__ __launch_bounds__(kAttBlock) void attract_staged_kernel(
 // kSellRing ahead of the sums in a ring of registers, across unit
 // boundaries; a unit's row numbers and y_i are fetched two and one units
 // ahead.  Each lane sums its own row, so the partial of a (row, tile) is
-// formed in a fixed order; it goes to partial[row * kTileMaxSeg + k] (k: the
-// tile's segment counted from its block's first) and rows add their partials
-// later in a fixed order.
+// formed in a fixed order; it goes to the row's sorted slot of the tile,
+// partial[tile * kTileRows + position], so a unit's 64 lanes store one
+// contiguous 512-byte block and every tile fills its 8 KB of partials
+// (scattered 8-byte stores, one per row, cost a third of the kernel's time).
+// attract_rows_kernel then adds each row's partials in tile order.
 constexpr int kTileBlock = 1024;
-constexpr int kSellRing = 4;
+// two chunks in flight per wave (16 waves per CU) measured fastest at 1.3M
+// points: deeper rings (3, 4, 6, 8) streamed slower
+constexpr int kSellRing = 2;
 constexpr int kSellWaves = kTileBlock / kWave;
 constexpr int kItemMaxUnits = kItemMaxTiles * kSlicesPerTile;
 
@@ -658,13 +662,13 @@ typedef uint16_t v4u16 __attribute__((ext_vector_type(4)));
 
 __global__ __launch_bounds__(kTileBlock) void attract_sell_kernel(
     const int2 *__restrict__ item_tiles, const int4 *__restrict__ item_units, const int4 *__restrict__ wave_units,
-    const int32_t *__restrict__ tile_blk, const int32_t *__restrict__ tile_seg, const int32_t *__restrict__ tile_k,
+    const int32_t *__restrict__ tile_blk, const int32_t *__restrict__ tile_seg,
     const int32_t *__restrict__ unit_chunks, const int32_t *__restrict__ unit_tj, const uint16_t *__restrict__ tperm,
     const uint16_t *__restrict__ tcol, const float *__restrict__ tval, const float2 *__restrict__ ylay,
     int32_t nitems, Header *__restrict__ hdr, float2 *__restrict__ partial)
 {
     __shared__ v4f sy4[kTileSeg / 2];
-    __shared__ int32_t s_row0[kItemMaxTiles], s_k[kItemMaxTiles];
+    __shared__ int32_t s_row0[kItemMaxTiles];
     // per stored unit of the item: chunks (a run holds at most kTileSeg entries)
     // and (tile - t0) * 16 + slice, both below 2^16
     static_assert(kTileSeg / 4 < 65536 && kItemMaxUnits <= 65536, "unit tables are 16-bit");
@@ -713,10 +717,7 @@ __global__ __launch_bounds__(kTileBlock) void attract_sell_kernel(
         v4f *sv = reinterpret_cast<v4f *>(sy4);
 #pragma unroll
         for (int q = 0; q < kStage; ++q) sv[q * kTileBlock + threadIdx.x] = stage[q];
-        for (int32_t j = threadIdx.x; j < t1 - t0; j += kTileBlock) {
-            s_row0[j] = tile_blk[t0 + j] * kTileRows;
-            s_k[j] = tile_k[t0 + j];
-        }
+        for (int32_t j = threadIdx.x; j < t1 - t0; j += kTileBlock) s_row0[j] = tile_blk[t0 + j] * kTileRows;
         for (int32_t j = threadIdx.x; j < iu.z - iu.x; j += kTileBlock) {
             s_K[j] = uint16_t(unit_chunks[iu.x + j]);
             s_tj[j] = uint16_t(unit_tj[iu.x + j] - t0 * kSlicesPerTile);
@@ -725,18 +726,17 @@ __global__ __launch_bounds__(kTileBlock) void attract_sell_kernel(
 
         // LDS values that are the same in every lane, as scalars
         auto uni = [](int32_t v) { return __builtin_amdgcn_readfirstlane(v); };
-        // row of this lane in its block for unit u (a load), the first row of the
-        // unit's block, and the unit's partial slot
-        auto unit_rl = [&](int32_t u) {
+        // this lane's sorted slot of unit u in the whole copy (where its partial
+        // goes), its row in the block (a load), and the first row of the unit's block
+        auto unit_at = [&](int32_t u) {
             const int32_t tj = uni(s_tj[u - iu.x]), t = t0 + tj / kSlicesPerTile, j = tj % kSlicesPerTile;
-            return int32_t(tperm[int64_t(t) * kTileRows + j * kSellSlice + lane]);
+            return int64_t(t) * kTileRows + j * kSellSlice + lane;
         };
+        auto unit_rl = [&](int32_t u) { return int32_t(tperm[unit_at(u)]); };
         auto unit_row0 = [&](int32_t u) { return uni(s_row0[uni(s_tj[u - iu.x]) / kSlicesPerTile]); };
-        auto unit_slot = [&](int32_t u) { return uni(s_k[uni(s_tj[u - iu.x]) / kSlicesPerTile]); };
 
         // units without entries in their tile's segment: their rows' partials are 0
-        for (int32_t u = iu.y + w; u < iu.z; u += kSellWaves)
-            partial[int64_t(unit_row0(u) + unit_rl(u)) * kTileMaxSeg + unit_slot(u)] = make_float2(0.0f, 0.0f);
+        for (int32_t u = iu.y + w; u < iu.z; u += kSellWaves) partial[unit_at(u)] = make_float2(0.0f, 0.0f);
         if (wu.x < wu.y) { // this wave has units
         const int32_t ulast = wu.y - 1;
         int32_t u = wu.x;             // unit being summed (wave-uniform)
@@ -766,7 +766,7 @@ __global__ __launch_bounds__(kTileBlock) void attract_sell_kernel(
             fy += live ? cy : 0.0f;
             issue(x, g + kSellRing);
             if (live && g + 1 == uend) {
-                partial[int64_t(rowA) * kTileMaxSeg + unit_slot(u)] = make_float2(fx, fy);
+                partial[unit_at(u)] = make_float2(fx, fy);
                 fx = fy = 0.0f;
                 ++u;
                 if (u <= ulast) uend += uni(s_K[u - iu.x]);
@@ -785,14 +785,37 @@ __global__ __launch_bounds__(kTileBlock) void attract_sell_kernel(
     }     // items
 }
 
+// ------------------------------------------------------------------ attractive row sums
+// F_attr of each row in layout order: its partials of the block's tiles, k = 0,
+// 1, ... in segment order, each at the row's sorted position in that tile.
+// Consecutive rows read one tile's 8 KB of partials at a time.
+__global__ __launch_bounds__(256) void attract_rows_kernel(const float2 *__restrict__ partial,
+                                                           const int32_t *__restrict__ blk_nseg,
+                                                           const int32_t *__restrict__ blk_tiles,
+                                                           const uint16_t *__restrict__ tpos, int64_t n,
+                                                           float2 *__restrict__ fattr)
+{
+    const int64_t r = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (r >= n) return;
+    const int64_t b = r / kTileRows;
+    const int rr = int(r % kTileRows);
+    const int ns = blk_nseg[b];
+    float2 fa = make_float2(0.0f, 0.0f);
+    for (int k = 0; k < ns; ++k) {
+        const int64_t t = blk_tiles[b * kTileMaxSeg + k];
+        const float2 v = partial[t * kTileRows + tpos[t * kTileRows + rr]];
+        fa.x += v.x;
+        fa.y += v.y;
+    }
+    fattr[r] = fa;
+}
+
 // ------------------------------------------------------------------ gradient + update
 // In the caller's order: g = 4 (alpha F_attr - F_rep / Z), then the gains /
-// momentum update of the optimiser (when a.update).
-// F_attr of a row in layout order: either one value per row, or (tiled) the
-// sum of the row's per-tile partials in tile order.
+// momentum update of the optimiser (when a.update).  F_attr of a point is
+// that of its row in layout order.
 __global__ __launch_bounds__(256) void update_kernel(const float2 *__restrict__ fattr_lay,
-                                                     const uint32_t *__restrict__ rank, int tiled,
-                                                     const int32_t *__restrict__ blk_nseg,
+                                                     const uint32_t *__restrict__ rank,
                                                      const float2 *__restrict__ frep, const Header *__restrict__ hdr,
                                                      int64_t n, StepArgs a, float2 *__restrict__ Y,
                                                      float2 *__restrict__ upd, float2 *__restrict__ gains,
@@ -802,19 +825,7 @@ __global__ __launch_bounds__(256) void update_kernel(const float2 *__restrict__ 
     if (i >= n) return;
     const float inv_z = float(1.0 / hdr->Z);
     const uint32_t r = rank[i];
-    float2 fa = make_float2(0.0f, 0.0f);
-    if (r < uint32_t(n)) {
-        if (tiled) { // the row's partials are adjacent: [row][segment of its block]
-            const int ns = blk_nseg[r / kTileRows];
-            const float2 *q = fattr_lay + int64_t(r) * kTileMaxSeg;
-            for (int k = 0; k < ns; ++k) {
-                fa.x += q[k].x;
-                fa.y += q[k].y;
-            }
-        } else {
-            fa = fattr_lay[r];
-        }
-    }
+    const float2 fa = r < uint32_t(n) ? fattr_lay[r] : make_float2(0.0f, 0.0f);
     const float2 fr = frep[i];
     const float gx = 4.0f * (a.alpha * fa.x - fr.x * inv_z);
     const float gy = 4.0f * (a.alpha * fa.y - fr.y * inv_z);
@@ -1114,20 +1125,23 @@ void launch_attract_layout(const LayoutView &lv, int64_t n, int64_t nnz, int til
     if (tiles > 0) {
         const unsigned grid = unsigned(blocks < items ? blocks : items);
         attract_sell_kernel<<<grid, kTileBlock, 0, st>>>(lv.item_tiles, lv.item_units, lv.wave_units, lv.tile_blk,
-                                                         lv.tile_seg, lv.tile_k, lv.unit_chunks, lv.unit_tj,
+                                                         lv.tile_seg, lv.unit_chunks, lv.unit_tj,
                                                          lv.tperm, lv.tcol, lv.tval, at<float2>(ws, L.ycopy), items,
                                                          at<Header>(ws, L.header), at<float2>(ws, L.partial));
+        attract_rows_kernel<<<unsigned((n + 255) / 256), 256, 0, st>>>(at<float2>(ws, L.partial), lv.blk_nseg,
+                                                                      lv.blk_tiles, lv.tpos, n, at<float2>(ws, L.fattr));
         return;
     }
     // 1024 threads (one block per CU: the segment fills 128 KB of LDS), 2 rows per lane group
     launch_staged<1024, 16384, 2>(lv, n, nnz, max_segs, ws, L, st);
 }
 
-void launch_update(const LayoutView &lv, int64_t n, int tiled, const StepArgs &a, float *Y, float *upd, float *gains,
+void launch_update(const LayoutView &lv, int64_t n, const StepArgs &a, float *Y, float *upd, float *gains,
                    float *grad, void *ws, const Layout &L, hipStream_t st)
 {
+    // both attractive kernels leave F_attr per row in layout order
     update_kernel<<<unsigned((n + 255) / 256), 256, 0, st>>>(
-        at<float2>(ws, tiled ? L.partial : L.fattr), lv.rank, tiled, lv.blk_nseg, at<float2>(ws, L.frep),
+        at<float2>(ws, L.fattr), lv.rank, at<float2>(ws, L.frep),
         at<Header>(ws, L.header), n, a,
         reinterpret_cast<float2 *>(Y), reinterpret_cast<float2 *>(upd), reinterpret_cast<float2 *>(gains),
         reinterpret_cast<float2 *>(grad));

@@ -80,7 +80,7 @@ int launch_layout_build(const int64_t *row_ptr, const int32_t *col, const float 
 // `blocks`: grid of the persistent sliced kernel (items are taken from a counter)
 void launch_attract_layout(const LayoutView &lv, int64_t n, int64_t nnz, int tiles, int items, int blocks,
                            int max_segs, void *ws, const Layout &L, hipStream_t st);
-void launch_update(const LayoutView &lv, int64_t n, int tiled, const StepArgs &a, float *Y, float *upd, float *gains,
+void launch_update(const LayoutView &lv, int64_t n, const StepArgs &a, float *Y, float *upd, float *gains,
                    float *grad, void *ws, const Layout &L, hipStream_t st);
 
 } // namespace bht
