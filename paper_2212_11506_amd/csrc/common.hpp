@@ -18,7 +18,7 @@ constexpr int kSortBlock = 256;                    // 4 waves
 constexpr int kSortItems = 8;                      // keys per thread
 constexpr int kSortTile = kSortBlock * kSortItems; // keys per tile
 constexpr int kScanBlock = 256;
-constexpr int kScanItems = 16;
+constexpr int kScanItems = 4;
 constexpr int kScanTile = kScanBlock * kScanItems;
 constexpr int kBBoxBlocks = 512;
 // repulsive walk: 16 waves of consecutive points per block share one CU, so
