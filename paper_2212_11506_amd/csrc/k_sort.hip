@@ -264,12 +264,14 @@ __global__ __launch_bounds__(kSortBlock) void onesweep_kernel(
     const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
 
     uint64_t key[kSortItems];
-    uint32_t rank[kSortItems];
+    uint32_t rank[kSortItems], ixv[kSortItems];
 #pragma unroll
     for (int r = 0; r < kSortItems; ++r) {
         int64_t p = base + w * kSeg + r * kWave + lane;
         bool valid = p < n;
         key[r] = valid ? keys_in[p] : ~0ull;
+        // the payload is loaded with the key, so its latency is not exposed after the look-back
+        ixv[r] = kFirst ? uint32_t(p) : (valid ? idx_in[p] : 0u);
         uint32_t d = uint32_t(key[r] >> shift) & (kRadix - 1);
         uint64_t peers = ballot(valid);
 #pragma unroll
@@ -354,7 +356,7 @@ __global__ __launch_bounds__(kSortBlock) void onesweep_kernel(
             uint32_t dd = uint32_t(key[r] >> shift) & (kRadix - 1);
             uint32_t lp = s_lstart[dd] + s_wcnt[w][dd] + rank[r];
             s_keys[lp] = key[r];
-            s_idx[lp] = kFirst ? uint32_t(p) : idx_in[p];
+            s_idx[lp] = ixv[r];
         }
     }
     __syncthreads();
