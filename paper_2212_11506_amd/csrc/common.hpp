@@ -35,7 +35,7 @@ constexpr int64_t kYPad = 16384 + 2;                   // padding points after t
 constexpr int kTileRows = 1024;
 constexpr int kTileSeg = 16384; // 128 KB of Y in LDS
 constexpr int kTileMaxSeg = 16;
-constexpr int kItemMaxTiles = 64; // tiles of one segment handled by one block
+constexpr int kItemMaxTiles = 128; // tiles of one segment handled by one block
 // sliced copy of a tile: 64 rows per slice (one per lane), chunks of 4 entries per lane
 constexpr int kSellSlice = 64;
 constexpr int kSellChunk = 4 * kSellSlice;

@@ -948,9 +948,11 @@ static int build_tiles(const LayoutView &lv, int64_t n, TilePlan *plan, void *ws
     std::vector<int32_t> sk(units); // chunks of slice (tile, j), indexed tile * 16 + j
     if (hipMemcpyAsync(sk.data(), lv.unit_chunks, 4 * units, hipMemcpyDeviceToHost, st) != hipSuccess) return -1;
     if (hipStreamSynchronize(st) != hipSuccess) return -1;
-    // Items: runs of tiles of one segment holding about a sixteenth of a CU's
+    // Items: runs of tiles of one segment holding about a quarter of a CU's
     // share of the chunks (at most kItemMaxTiles tiles), launched largest
     // first so that blocks handed to whichever CU frees up first balance out.
+    // Each item stages its segment of Y once: coarser items stage less (a
+    // sixteenth of a share per item measured 7% slower at 1.3M points).
     int dev = 0, cus = 256;
     if (hipGetDevice(&dev) == hipSuccess)
         (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
@@ -960,7 +962,7 @@ static int build_tiles(const LayoutView &lv, int64_t n, TilePlan *plan, void *ws
         for (int j = 0; j < kSlicesPerTile; ++j) tcost[t] += sk[t * kSlicesPerTile + j];
         total += tcost[t];
     }
-    const int64_t target = std::max<int64_t>(1, total / (16 * int64_t(cus)));
+    const int64_t target = std::max<int64_t>(1, total / (4 * int64_t(cus)));
     std::vector<int2> ranges;
     std::vector<int64_t> rcost;
     for (int64_t t = 0; t < tiles; ++t) {

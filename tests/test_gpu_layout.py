@@ -31,7 +31,7 @@ def rel_l2(a, b):
     return float(np.linalg.norm(np.asarray(a, np.float64) - b) / np.linalg.norm(b))
 
 
-TILE_ROWS, TILE_SEG, TILE_MAX_SEG, ITEM_MAX_TILES = 1024, 16384, 16, 64
+TILE_ROWS, TILE_SEG, TILE_MAX_SEG, ITEM_MAX_TILES = 1024, 16384, 16, 128
 SLICE, SLICES, CHUNK = 64, 16, 256  # rows per unit, units per tile, entries per chunk
 
 
