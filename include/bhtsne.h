@@ -59,7 +59,7 @@ typedef enum {
  * row_ptr[n] = nnz; columns outside [0, n) and entries outside [0, nnz) are
  * skipped on the GPU and flagged as a device error. */
 typedef struct bhtsne_csr {
-    int64_t n;              /* points; 2 <= n <= 67108863 */
+    int64_t n;              /* points; 2 <= n <= 16777215 */
     int64_t nnz;            /* stored entries, >= 0 */
     const int64_t *row_ptr; /* device, n + 1 entries */
     const int32_t *col;     /* device, nnz entries (may be NULL when nnz == 0) */

@@ -570,12 +570,7 @@ int bhtsne_debug_tree(const float *Y, int64_t n, float theta, int64_t *n_nodes, 
     dbg.begin = begin;
     dbg.end = end;
     build_tree(Y, n, theta, nullptr, workspace, L, dbg, stream);
-    if (summary && hipMemcpyAsync(summary, at<void>(workspace, L.nodes), 16 * size_t(2 * n),
-                                  hipMemcpyDeviceToDevice, stream) != hipSuccess)
-        return BHTSNE_EDEVICE;
-    if (meta && hipMemcpyAsync(meta, at<void>(workspace, L.meta), 4 * size_t(2 * n), hipMemcpyDeviceToDevice,
-                               stream) != hipSuccess)
-        return BHTSNE_EDEVICE;
+    if (summary || meta) launch_tree_unpack(n, workspace, L, summary, meta, stream);
     if (hipGetLastError() != hipSuccess) return BHTSNE_EDEVICE;
     Header h;
     rc = read_header(workspace, &h, stream);

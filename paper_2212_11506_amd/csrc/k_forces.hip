@@ -25,10 +25,14 @@ __device__ inline float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
 
 // Lane masks straight from the vector compares (one instruction each, no
 // conversion through a boolean per lane): predicates as in LLVM's icmp/fcmp.
-constexpr int kCmpUge = 35, kCmpNe = 33, kCmpFgt = 2;
+constexpr int kCmpUge = 35, kCmpNe = 33, kCmpSgt = 38;
 __device__ inline uint64_t mask_uge(uint32_t a, uint32_t b) { return __builtin_amdgcn_uicmp(a, b, kCmpUge); }
 __device__ inline uint64_t mask_ne(uint32_t a, uint32_t b) { return __builtin_amdgcn_uicmp(a, b, kCmpNe); }
-__device__ inline uint64_t mask_fgt(float a, float b) { return __builtin_amdgcn_fcmpf(a, b, kCmpFgt); }
+// the predicate, not the operand type, decides signedness
+__device__ inline uint64_t mask_sgt(int32_t a, int32_t b)
+{
+    return __builtin_amdgcn_uicmp(uint32_t(a), uint32_t(b), kCmpSgt);
+}
 // x in the lanes whose bit of m is set, else 0 (one v_cndmask on the mask)
 __device__ inline float keep_lanes(uint64_t m, float x)
 {
@@ -50,11 +54,55 @@ __device__ inline uint32_t pick_lanes_u(uint64_t m, uint32_t x, uint32_t y)
 // a bucket of identical points is a cell whose children are its points.  The
 // acceptance test yields a lane mask, the weight is zeroed outside it, the
 // interaction count is its population, and the next node is a scalar select
-// (the skip index when no lane descends into the cell).  The walk is bound by
-// instruction issue, vector and scalar alike (one scalar unit serves a CU's
-// four SIMDs), so both kinds are kept to a minimum.
+// (the skip index when no lane descends into the cell).  One 16-byte record per
+// node (the meta word in its fourth component) is one scalar load per visit.
+//
+// The threshold of a cell of level L is side(L)^2 / theta^2 = thr(0) * 4^-L,
+// so unless it leaves the normal range its float bits are those of thr(0)
+// minus L << 24; the walk forms them from the meta word's level field in
+// scalar code.  A single point's field is all ones, which takes the bits below
+// zero as an integer, and for squared distances (never negative) the integer
+// order of the bits is the float order, so one signed compare accepts every
+// single point and tests every cell.  When the shortcut does not reproduce the
+// thresholds (theta = 0, or a domain so small or large that thr leaves the
+// normal range) the walk reads each threshold from the table instead.
+template <bool kShift>
+__device__ inline void repulsive_walk(const char *nbase, const uint32_t *__restrict__ thr_table, uint32_t thr0,
+                                      uint32_t total, float2 yi, uint32_t self, uint32_t &resume, float &fx,
+                                      float &fy, float &z, uint32_t &inter)
+{
+    uint32_t cur = 0;
+    while (cur < total) {
+        const float4 r = *reinterpret_cast<const float4 *>(nbase + (cur << 4));
+        const uint32_t m = __float_as_uint(r.w);
+        const uint32_t lv = m >> kMetaLevelShift;
+        const uint32_t thr = kShift ? thr0 - (lv << 24) : thr_table[lv];
+        const float dx = yi.x - r.x, dy = yi.y - r.y;
+        const float d2 = fmaf(dx, dx, dy * dy);
+        const uint64_t act = mask_uge(cur, resume);
+        const uint64_t take = act & mask_sgt(__float_as_int(d2), int32_t(thr)) & mask_ne(m, self);
+        const float wgt = fast_rcp(1.0f + d2);
+        const float nw = keep_lanes(take, r.z * wgt);
+        z += nw;
+        const float nw2 = nw * wgt;
+        fx = fmaf(nw2, dx, fx);
+        fy = fmaf(nw2, dy, fy);
+        inter += uint32_t(__builtin_popcountll(take));
+        const uint64_t rej = act & ~take;
+        // the skip index of a cell, 0 for a single point (negative meta word)
+        const uint32_t skip = uint32_t(max(int32_t(m), 0)) & kMetaSkipMask;
+        // accepting lanes park until the walk leaves a cell.  A lane that
+        // takes a node is active, so its old resume index is at most cur and
+        // the new one (skip, or 0 after a single point) keeps every later node
+        // that the old one allowed: no max is needed
+        resume = pick_lanes_u(take, skip, resume);
+        // a skip index lies beyond its cell: skip when no lane descends
+        cur = rej ? cur + 1 : max(cur + 1, skip);
+    }
+}
+
 __global__ __launch_bounds__(kRepBlock) void repulsive_kernel(
-    const float4 *__restrict__ nodes, const uint32_t *__restrict__ meta, const float2 *__restrict__ ys,
+    const float4 *__restrict__ nodes, const uint32_t *__restrict__ thr_table, const float2 *__restrict__ ys,
     const uint32_t *__restrict__ perm, Header *__restrict__ hdr, int64_t n, float2 *__restrict__ frep,
     double *__restrict__ zpart, unsigned long long *__restrict__ ipart)
 {
@@ -64,44 +112,28 @@ __global__ __launch_bounds__(kRepBlock) void repulsive_kernel(
     const int64_t s64 = int64_t(lb) * kRepBlock + threadIdx.x;
     const bool valid = s64 < n;
     const uint32_t si = uint32_t(s64);
-    const uint32_t self = si | kLeafBit | kSingleBit; // meta word of this lane's own leaf
+    const uint32_t self = kMetaSingle | si; // meta word of this lane's own single-point node
     const float2 yi = valid ? ys[s64] : make_float2(0.0f, 0.0f);
     uint32_t resume = valid ? 0u : 0xffffffffu;
     float fx = 0.0f, fy = 0.0f, z = 0.0f;
     uint32_t total = uniform(hdr->nodes);
     const uint32_t cap = uint32_t(2 * n);
     total = total < cap ? total : cap;
+    // does thr(0) - (L << 24) reproduce the thresholds of levels 0..32, and
+    // stay above the bits of every single point's field?
+    const uint32_t thr0 = uniform(thr_table[0]);
+    const int lane = lane_id();
+    const uint32_t tl = thr_table[lane < 33 ? lane : 0];
+    const bool shift_ok = lane >= 33 || tl == thr0 - (uint32_t(lane) << 24);
+    const bool shift = ballot(shift_ok) == ~0ull && thr0 < 0x7F000000u;
     // node records by 32-bit byte offset (fewer than 2^27 nodes)
     const char *nbase = reinterpret_cast<const char *>(nodes);
-    const char *mbase = reinterpret_cast<const char *>(meta);
 
-    uint32_t cur = 0;
     uint32_t inter = 0; // this wave's interactions (a launch has fewer than 2^32 per wave)
-    while (cur < total) {
-        const float4 r = *reinterpret_cast<const float4 *>(nbase + (cur << 4));
-        const uint32_t m = *reinterpret_cast<const uint32_t *>(mbase + (cur << 2));
-        const float dx = yi.x - r.x, dy = yi.y - r.y;
-        const float d2 = fmaf(dx, dx, dy * dy);
-        const uint64_t act = mask_uge(cur, resume);
-        const uint64_t take = act & mask_fgt(d2, r.w) & mask_ne(m, self);
-        const float wgt = fast_rcp(1.0f + d2);
-        const float nw = keep_lanes(take, r.z * wgt);
-        z += nw;
-        const float nw2 = nw * wgt;
-        fx = fmaf(nw2, dx, fx);
-        fy = fmaf(nw2, dy, fy);
-        inter += uint32_t(__builtin_popcountll(take));
-        const uint64_t rej = act & ~take;
-        // the skip index of an internal cell, 0 for a leaf (kLeafBit is the sign bit)
-        const uint32_t skip = m & ~uint32_t(int32_t(m) >> 31);
-        // accepting lanes park until the walk leaves an internal cell.  A
-        // lane that takes a node is active, so its old resume index is at most
-        // cur and the new one (skip, or 0 after a leaf) keeps every later node
-        // that the old one allowed: no max is needed
-        resume = pick_lanes_u(take, skip, resume);
-        // a skip index lies beyond its cell: skip when no lane descends
-        cur = rej ? cur + 1 : max(cur + 1, skip);
-    }
+    if (shift)
+        repulsive_walk<true>(nbase, thr_table, thr0, total, yi, self, resume, fx, fy, z, inter);
+    else
+        repulsive_walk<false>(nbase, thr_table, thr0, total, yi, self, resume, fx, fy, z, inter);
 
     if (valid) {
         const uint32_t p = perm[si];
@@ -228,7 +260,7 @@ __global__ __launch_bounds__(256) void attract_kernel(
 void launch_repulsive(int64_t n, void *ws, const Layout &L, hipStream_t st)
 {
     repulsive_kernel<<<unsigned(L.rep_blocks), kRepBlock, 0, st>>>(
-        at<float4>(ws, L.nodes), at<uint32_t>(ws, L.meta), at<float2>(ws, L.ys), at<uint32_t>(ws, L.idx0),
+        at<float4>(ws, L.nodes), at<uint32_t>(ws, L.thr_table), at<float2>(ws, L.ys), at<uint32_t>(ws, L.idx0),
         at<Header>(ws, L.header), n, at<float2>(ws, L.frep), at<double>(ws, L.zpart),
         at<unsigned long long>(ws, L.ipart));
 }

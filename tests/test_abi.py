@@ -38,6 +38,9 @@ def test_workspace_size():
     assert bh.workspace_size(-5, 0) == 0
     assert bh.workspace_size(2, -1) == 0
     assert bh.workspace_size(1 << 26, 0) == 0
+    # skip indices of the 2n - 1 node records take 25 bits: n < 2^24
+    assert bh.workspace_size(1 << 24, 0) == 0
+    assert bh.workspace_size((1 << 24) - 1, 0) > 0
     a = bh.workspace_size(1000, 10)
     b = bh.workspace_size(2000, 10)
     assert 0 < a < b
