@@ -161,7 +161,11 @@ def main():
     reset()
     torch.cuda.synchronize()
 
+    # the timed run records hipEvents around the two force phases only (the
+    # roofline's kernels): each event is a timestamp packet of a few
+    # microseconds between kernels, and all six phases cost 3.5% of a step
     bh.timing_read(reset=True)
+    bh.timing_phases(["repulsive", "attractive"])
     bh.timing_enable(True)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
@@ -169,12 +173,22 @@ def main():
     torch.cuda.synchronize()
     t2 = time.perf_counter()
     bh.timing_enable(False)
+    bh.timing_phases(None)
     phases = bh.timing_read(reset=True)
     elapsed = t2 - t1
     its = args.steps / elapsed
     log(f"[bench] {args.steps} steps in {elapsed:.3f}s -> {its:.1f} it/s")
     stats_last = bh.get_stats(ws)
     y_final = Y.cpu().numpy()
+
+    # the other phases: a replay of the first iterations with every phase timed
+    reset()
+    bh.timing_enable(True)
+    breakdown_steps = min(args.steps, 200)
+    run(breakdown_steps)
+    torch.cuda.synchronize()
+    bh.timing_enable(False)
+    breakdown = bh.timing_read(reset=True)
 
     inter_total = None
     if not args.no_count:
@@ -194,9 +208,13 @@ def main():
     kernels = {}
     for name, (ms, cnt) in phases.items():
         if cnt == 0:
+            ms, cnt = breakdown[name]
+            if cnt == 0:
+                continue
+            kernels[name] = {"ms_per_launch": ms / cnt, "launches": cnt,
+                             "timed": f"replay of iterations 0..{breakdown_steps - 1}, every phase timed"}
             continue
-        per = ms / max(cnt, 1)
-        kernels[name] = {"ms_per_launch": per, "launches": cnt}
+        kernels[name] = {"ms_per_launch": ms / cnt, "launches": cnt, "timed": "timed run"}
     rep_ms = kernels["repulsive"]["ms_per_launch"]
     att_ms = kernels["attractive"]["ms_per_launch"]
     # sources whose change invalidates the committed traffic counters

@@ -193,10 +193,15 @@ int bhtsne_get_stats(const void *workspace, bhtsne_stats *out, hipStream_t strea
 const char *bhtsne_status_string(int status);
 
 /* Per-phase GPU timing.  While enabled, every later call records a hipEvent
- * pair around each phase on its stream (process-wide switch, thread safe).
- * bhtsne_timing_read waits for the recorded events, returns the summed
- * milliseconds per phase, and with reset != 0 starts a new accumulation. */
+ * pair around each selected phase on its stream (process-wide switch, thread
+ * safe).  bhtsne_timing_read waits for the recorded events, returns the summed
+ * milliseconds per phase, and with reset != 0 starts a new accumulation.
+ * bhtsne_timing_phases selects the phases by bit (1 << BHTSNE_PHASE_*; all by
+ * default): each event is a timestamp packet between two kernels, a few
+ * microseconds of GPU time, so a throughput measurement times only the phases
+ * it needs.  A mask with bits at or above BHTSNE_NUM_PHASES is BHTSNE_EINVAL. */
 int bhtsne_timing_enable(int enable);
+int bhtsne_timing_phases(uint32_t phase_mask);
 int bhtsne_timing_read(bhtsne_timing *out, int reset);
 
 /* Test export: bounding box, Morton codes and their sort (Quadtree Building,

@@ -25,6 +25,7 @@ from ._binding import (  # noqa: F401
     status_string,
     step,
     timing_enable,
+    timing_phases,
     timing_read,
     workspace_size,
 )

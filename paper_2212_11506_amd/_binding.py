@@ -75,6 +75,7 @@ def load_library():
                                          C.c_size_t, vp]),
         "bhtsne_status_string": (C.c_char_p, [C.c_int]),
         "bhtsne_timing_enable": (C.c_int, [C.c_int]),
+        "bhtsne_timing_phases": (C.c_int, [C.c_uint32]),
         "bhtsne_timing_read": (C.c_int, [C.POINTER(_Timing), C.c_int]),
         "bhtsne_debug_sort": (C.c_int, [vp, i64, vp, vp, vp, f64p, vp, C.c_size_t, vp]),
         "bhtsne_debug_tree": (C.c_int, [vp, i64, f32, C.POINTER(C.c_int64), vp, vp, vp, vp, vp, vp, vp,
@@ -233,6 +234,12 @@ def get_stats(workspace: torch.Tensor, check: bool = True) -> dict:
 
 def timing_enable(on: bool = True):
     _check(load_library().bhtsne_timing_enable(1 if on else 0), "bhtsne_timing_enable")
+
+
+def timing_phases(names=None):
+    """Phases that record events while timing is on (None: all of them)."""
+    mask = (1 << len(PHASES)) - 1 if names is None else sum(1 << PHASES.index(p) for p in set(names))
+    _check(load_library().bhtsne_timing_phases(mask), "bhtsne_timing_phases")
 
 
 def timing_read(reset: bool = True) -> dict:

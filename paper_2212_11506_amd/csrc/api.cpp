@@ -19,6 +19,7 @@ namespace {
 struct Timing {
     std::mutex mu;
     bool enabled = false;
+    uint32_t phases = (1u << BHTSNE_NUM_PHASES) - 1u; // phases that record events
     std::vector<hipEvent_t> pool;
     struct Pending {
         int phase;
@@ -54,7 +55,7 @@ class PhaseTimer {
     {
         Timing &t = timing();
         std::lock_guard<std::mutex> g(t.mu);
-        if (!t.enabled) return;
+        if (!t.enabled || !((t.phases >> phase) & 1u)) return;
         a_ = t.get();
         b_ = t.get();
         if (a_ && b_) hipEventRecord(a_, st_);
@@ -492,6 +493,15 @@ int bhtsne_timing_enable(int enable)
     Timing &t = timing();
     std::lock_guard<std::mutex> g(t.mu);
     t.enabled = enable != 0;
+    return BHTSNE_OK;
+}
+
+int bhtsne_timing_phases(uint32_t phase_mask)
+{
+    if (phase_mask >> BHTSNE_NUM_PHASES) return BHTSNE_EINVAL;
+    Timing &t = timing();
+    std::lock_guard<std::mutex> g(t.mu);
+    t.phases = phase_mask;
     return BHTSNE_OK;
 }
 

@@ -100,6 +100,14 @@ def test_gradient_rejects_bad_arguments(case):
     assert _grad(lib, P, **kw) == bh.BHTSNE_EINVAL
 
 
+def test_timing_phase_mask():
+    lib = bh.load_library()
+    assert lib.bhtsne_timing_phases(1 << len(bh.PHASES)) == bh.BHTSNE_EINVAL
+    assert lib.bhtsne_timing_phases(0xFFFFFFFF) == bh.BHTSNE_EINVAL
+    assert lib.bhtsne_timing_phases(1 << bh.PHASES.index("repulsive")) == bh.BHTSNE_OK
+    assert lib.bhtsne_timing_phases((1 << len(bh.PHASES)) - 1) == bh.BHTSNE_OK
+
+
 def test_gradient_rejects_bad_workspace():
     lib = bh.load_library()
     P = _Csr(100, 10, FAKE, FAKE, FAKE)

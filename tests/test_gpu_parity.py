@@ -366,3 +366,16 @@ def test_timing_records_every_phase():
         assert (cnt == 0) if name == "update" else (cnt == 3 and ms > 0.0), (name, plain[name])
         ms, cnt = layout[name]
         assert cnt == 3 and ms > 0.0, (name, layout[name])
+    # a phase mask limits the events to the selected phases
+    bh.timing_phases(["repulsive", "attractive"])
+    bh.timing_enable(True)
+    try:
+        for _ in range(2):
+            bh.gradient(Y, lay, 0.5, 12.0, return_z=False)
+        some = bh.timing_read(reset=True)
+    finally:
+        bh.timing_enable(False)
+        bh.timing_phases(None)
+    for name in bh.PHASES:
+        ms, cnt = some[name]
+        assert (cnt == 2 and ms > 0.0) if name in ("repulsive", "attractive") else cnt == 0, (name, some[name])
