@@ -108,27 +108,136 @@ __device__ inline int64_t run_end(const uint64_t *__restrict__ codes, int64_t x,
 }
 
 // ------------------------------------------------------------------ 1. splits
-__global__ __launch_bounds__(256) void tree_splits_kernel(const uint64_t *__restrict__ codes, int64_t n,
-                                                          uint32_t *__restrict__ levelmask,
-                                                          uint32_t *__restrict__ split_b,
-                                                          uint32_t *__restrict__ split_e)
+// One block per kSplitBlock consecutive splits.  The sorted codes around the
+// block, kSplitWin on either side, are staged in LDS and each split gallops
+// there for the two ends of its cell.  An end beyond the window (a cell of
+// more than kSplitWin points past the block) is found by one wave for the
+// whole block: 64 probes per round narrow the range 65-fold, so four or five
+// rounds of loads replace the twenty-odd dependent loads of a gallop through
+// global memory, which the other lanes of its wave would have waited for.
+constexpr int kSplitBlock = 256;
+constexpr int kSplitWin = 1024;
+
+__device__ inline bool same_cell(uint64_t c, uint64_t key, int sh) { return ((c ^ key) >> sh) == 0; }
+
+// first index in (lo, hi] whose code shares the top (64 - sh) bits of key, where
+// the codes sharing them are a suffix of (lo, hi] that includes hi (one wave)
+__device__ inline int64_t wave_first_same(const uint64_t *__restrict__ codes, int64_t lo, int64_t hi,
+                                          uint64_t key, int sh)
 {
-    int64_t s = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    const int lane = lane_id();
+    while (hi - lo > 1) {
+        const int64_t span = hi - lo - 1; // candidates lo + 1 .. hi - 1
+        const int64_t step = span <= kWave ? 1 : (span + kWave) / (kWave + 1);
+        const int64_t p = lo + (int64_t(lane) + 1) * step;
+        const bool in = p < hi;
+        const uint64_t yes = ballot(in && same_cell(codes[p], key, sh));
+        const uint64_t inm = ballot(in);
+        if (yes) {
+            const int k = __ffsll((unsigned long long)yes) - 1;
+            hi = lo + (int64_t(k) + 1) * step;
+            lo = k > 0 ? lo + int64_t(k) * step : lo;
+        } else {
+            const int k = 63 - __clzll((long long)inm); // last probe in range
+            lo = lo + (int64_t(k) + 1) * step;
+        }
+    }
+    return hi;
+}
+
+// first index in [lo, hi) whose code does not share the top bits of key, where
+// the codes sharing them are a prefix of [lo, hi) that includes lo (hi if none)
+__device__ inline int64_t wave_first_other(const uint64_t *__restrict__ codes, int64_t lo, int64_t hi,
+                                           uint64_t key, int sh)
+{
+    const int lane = lane_id();
+    // invariant: codes[lo] shares, index hi differs (or is the end)
+    while (hi - lo > 1) {
+        const int64_t span = hi - lo - 1;
+        const int64_t step = span <= kWave ? 1 : (span + kWave) / (kWave + 1);
+        const int64_t p = lo + (int64_t(lane) + 1) * step;
+        const bool in = p < hi;
+        const uint64_t no = ballot(in && !same_cell(codes[p], key, sh));
+        const uint64_t inm = ballot(in);
+        if (no) {
+            const int k = __ffsll((unsigned long long)no) - 1;
+            hi = lo + (int64_t(k) + 1) * step;
+            lo = k > 0 ? lo + int64_t(k) * step : lo;
+        } else {
+            const int k = 63 - __clzll((long long)inm);
+            lo = lo + (int64_t(k) + 1) * step;
+        }
+    }
+    return hi;
+}
+
+__global__ __launch_bounds__(kSplitBlock) void tree_splits_kernel(const uint64_t *__restrict__ codes, int64_t n,
+                                                                  uint32_t *__restrict__ levelmask,
+                                                                  uint32_t *__restrict__ split_b,
+                                                                  uint32_t *__restrict__ split_e)
+{
+    __shared__ uint64_t s_c[kSplitBlock + 2 * kSplitWin + 1];
+    __shared__ int64_t s_b[kSplitBlock], s_e[kSplitBlock];
+    __shared__ uint16_t s_hard[2 * kSplitBlock];
+    __shared__ uint32_t s_nhard;
+    const int t = threadIdx.x;
+    const int64_t base = int64_t(blockIdx.x) * kSplitBlock;
+    const int64_t wlo = base > kSplitWin ? base - kSplitWin : 0;
+    const int64_t whi = base + kSplitBlock + kSplitWin < n ? base + kSplitBlock + kSplitWin : n;
+    for (int64_t i = t; i < whi - wlo; i += kSplitBlock) s_c[i] = codes[wlo + i];
+    if (t == 0) s_nhard = 0;
+    __syncthreads();
+
+    const int64_t s = base + t;
     if (s == 0) atomicOr(&levelmask[0], 1u); // the root always exists
-    if (s >= n - 1) return;
-    uint64_t ms = codes[s], mn = codes[s + 1];
-    if (ms == mn) {
-        split_e[s] = 0;
+    bool split = false;
+    int L = 0;
+    uint64_t ms = 0;
+    if (s < n - 1) {
+        ms = s_c[s - wlo];
+        const uint64_t mn = s_c[s + 1 - wlo];
+        split = ms != mn;
+        if (split) L = split_level(ms, mn);
+    }
+    int64_t b = 0, e = n;
+    if (split && L > 0) {
+        const int sh = 64 - 2 * L;
+        // in window coordinates; the window holds s and s + 1
+        const int64_t bl = gallop_left(s_c, s - wlo, ms, sh);
+        const int64_t el = gallop_right(s_c, s + 1 - wlo, whi - wlo, ms, sh);
+        b = wlo + bl;
+        e = wlo + el;
+        if (bl == 0 && wlo > 0) s_hard[atomicAdd(&s_nhard, 1u)] = uint16_t(2 * t);      // begin before the window
+        if (el == whi - wlo && whi < n) s_hard[atomicAdd(&s_nhard, 1u)] = uint16_t(2 * t + 1); // end after it
+    }
+    s_b[t] = b;
+    s_e[t] = e;
+    __syncthreads();
+    // cell ends past the window: one wave each
+    const uint32_t nh = s_nhard;
+    for (uint32_t h = uint32_t(t / kWave); h < nh; h += kSplitBlock / kWave) {
+        const int owner = s_hard[h] >> 1, dir = s_hard[h] & 1;
+        const uint64_t key = s_c[base + owner - wlo];
+        const int sh = 64 - 2 * split_level(key, s_c[base + owner + 1 - wlo]);
+        if (dir == 0) {
+            // codes[wlo] shares the cell; find its first index in [0, wlo]
+            const int64_t r = wave_first_same(codes, -1, wlo, key, sh);
+            if (lane_id() == 0) s_b[owner] = r;
+        } else {
+            // codes[whi - 1] shares the cell; find the first index past it
+            const int64_t r = wave_first_other(codes, whi - 1, n, key, sh);
+            if (lane_id() == 0) s_e[owner] = r;
+        }
+    }
+    __syncthreads();
+    if (!split) {
+        if (s < n - 1) split_e[s] = 0;
         return;
     }
-    int L = split_level(ms, mn);
-    int64_t b = 0, e = n;
-    if (L > 0) {
-        int sh = 64 - 2 * L;
-        b = gallop_left(codes, s, ms, sh);
-        e = gallop_right(codes, s + 1, n, ms, sh);
-    }
-    bool owner = quad_digit(codes[b], L) == quad_digit(ms, L);
+    b = s_b[t];
+    e = s_e[t];
+    const uint64_t cb = b >= wlo ? s_c[b - wlo] : codes[b];
+    const bool owner = quad_digit(cb, L) == quad_digit(ms, L);
     if (owner) {
         atomicOr(&levelmask[b], 1u << L);
         split_b[s] = uint32_t(b);
