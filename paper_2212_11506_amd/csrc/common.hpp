@@ -17,6 +17,10 @@ constexpr int kSortPasses = 64 / kRadixBits;
 constexpr int kSortBlock = 256;                    // 4 waves
 constexpr int kSortItems = 8;                      // keys per thread
 constexpr int kSortTile = kSortBlock * kSortItems; // keys per tile
+// digit histograms of the sort: one copy per XCD (tile % 8), summed by the
+// readers, so that the tiles' atomic adds spread over eight sets of addresses
+constexpr int kHistCopies = 8;
+constexpr int kHistWords = kSortPasses * (1 << kRadixBits);
 constexpr int kScanBlock = 256;
 constexpr int kScanItems = 4;
 constexpr int kScanTile = kScanBlock * kScanItems;
@@ -112,7 +116,7 @@ inline Layout make_layout(int64_t n, int64_t nnz)
         return o;
     };
     L.header = take(sizeof(Header));
-    L.hist = take(sizeof(uint32_t) * kSortPasses * kRadix);
+    L.hist = take(sizeof(uint32_t) * kHistCopies * kHistWords);
     L.bbox_part = take(32 * kBBoxBlocks); // {min x, max x, min y, max y, non-finite flag}
     L.codes0 = take(8 * size_t(n));
     L.codes1 = take(8 * size_t(n));

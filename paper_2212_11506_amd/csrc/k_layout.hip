@@ -117,13 +117,14 @@ __global__ __launch_bounds__(kSortBlock) void keys_hist_kernel(const uint64_t *_
         }
     }
     __syncthreads();
+    uint32_t *hc = hist + (blockIdx.x % kHistCopies) * kHistWords;
     for (int k = threadIdx.x; k < kSortPasses * kRadix; k += kSortBlock)
-        if (sh[k]) atomicAdd(&hist[k], sh[k]);
+        if (sh[k]) atomicAdd(&hc[k], sh[k]);
 }
 
 __global__ void sort_reset_kernel(Header *__restrict__ hdr, uint32_t *__restrict__ hist)
 {
-    for (int k = threadIdx.x; k < kSortPasses * kRadix; k += blockDim.x) hist[k] = 0;
+    for (int k = threadIdx.x; k < kHistCopies * kHistWords; k += blockDim.x) hist[k] = 0;
     if (threadIdx.x == 0) {
         for (int k = 0; k < kSortPasses; ++k) hdr->tile_counter[k] = 0;
         hdr->flags = 0;

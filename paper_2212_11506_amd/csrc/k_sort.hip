@@ -98,7 +98,7 @@ __global__ __launch_bounds__(256) void bbox_final_kernel(const float *__restrict
         s[w][3] = mxy;
         sb[w] = anybad;
     }
-    for (int k = threadIdx.x; k < kSortPasses * kRadix; k += blockDim.x) hist[k] = 0;
+    for (int k = threadIdx.x; k < kHistCopies * kHistWords; k += blockDim.x) hist[k] = 0;
     __syncthreads();
     if (threadIdx.x == 0) {
         float r[4] = {s[0][0], s[0][1], s[0][2], s[0][3]};
@@ -196,8 +196,9 @@ __global__ __launch_bounds__(kSortBlock) void morton_kernel(
         }
     }
     __syncthreads();
+    uint32_t *hc = hist + (blockIdx.x % kHistCopies) * kHistWords;
     for (int k = threadIdx.x; k < kSortPasses * kRadix; k += kSortBlock)
-        if (sh[k]) atomicAdd(&hist[k], sh[k]);
+        if (sh[k]) atomicAdd(&hc[k], sh[k]);
 }
 
 // ------------------------------------------------------------------ onesweep pass
@@ -305,7 +306,9 @@ __global__ __launch_bounds__(kSortBlock) void onesweep_kernel(
     uint32_t lstart = block_exclusive_scan256(tot, s_scan, nullptr);
     s_lstart[d] = lstart;
     // global start of digit d: exclusive scan of the histogram
-    uint32_t h = hist[pass * kRadix + d];
+    uint32_t h = 0;
+#pragma unroll
+    for (int c = 0; c < kHistCopies; ++c) h += hist[c * kHistWords + pass * kRadix + d];
     __syncthreads();
     uint32_t dbase = block_exclusive_scan256(h, s_scan, nullptr);
     uint32_t excl = 0;
