@@ -237,8 +237,9 @@ class Inputs:
                                 ("col", self.col), ("val", self.val))}
 
 
-def make_inputs(cid: int, n: Optional[int] = None, progress=None) -> Inputs:
-    """Generate workload ``cid``; ``n`` overrides the size (cluster shares are kept)."""
+def make_inputs(cid: int, n: Optional[int] = None, progress=None, k: int = K_NEIGHBOURS) -> Inputs:
+    """Generate workload ``cid``; ``n`` overrides the size (cluster shares are kept)
+    and ``k`` the neighbours per row of the conditional matrix."""
     t0 = time.time()
     w = WORKLOADS[cid]
     n = w.n if n is None else int(n)
@@ -252,7 +253,7 @@ def make_inputs(cid: int, n: Optional[int] = None, progress=None) -> Inputs:
         off += sizes[c]
     if progress:
         progress(f"[synth] workload {cid}: n={n}, drawing P")
-    row_ptr, col, val = make_p(w, n, perm, sizes, rng_nb, rng_w)
+    row_ptr, col, val = make_p(w, n, perm, sizes, rng_nb, rng_w, k=k)
     if progress:
         progress(f"[synth] workload {cid}: nnz={col.size}, drawing Y")
     Y = make_y(w, n, perm, sizes, rng_y)
