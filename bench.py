@@ -167,11 +167,21 @@ def main():
     bh.timing_read(reset=True)
     bh.timing_phases(["repulsive", "attractive"])
     bh.timing_enable(True)
+    # stream events at the schedule's switch (exaggeration off, momentum 0.8 from
+    # iteration 250): the two stretches' means, without a sync in the loop
+    split = 250 if args.steps > 250 else None
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
     torch.cuda.synchronize()
+    ev[0].record()
     t1 = time.perf_counter()
-    run(args.steps)
+    run(args.steps, per_step=(lambda it: ev[1].record() if it == split - 1 else None) if split else None)
+    ev[2].record()
     torch.cuda.synchronize()
     t2 = time.perf_counter()
+    segments = None
+    if split:
+        a, b = ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2])
+        segments = {f"0..{split - 1}": split / (a * 1e-3), f"{split}..{args.steps - 1}": (args.steps - split) / (b * 1e-3)}
     bh.timing_enable(False)
     bh.timing_phases(None)
     phases = bh.timing_read(reset=True)
@@ -288,6 +298,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{w.description} (workload {w.cid})", "n": n, "nnz": nnz,
                    "theta": args.theta, "iterations": f"0..{args.steps - 1} of the schedule"},
+        "iterations_per_s_by_stretch": segments,
         "interactions_per_s": (inter_total / elapsed) if inter_total is not None else None,
         "interactions_per_iteration": (inter_total / args.steps) if inter_total is not None else None,
         "nodes_last": stats_last["nodes"],
