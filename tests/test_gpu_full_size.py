@@ -92,3 +92,38 @@ def test_full_workload_3_5m_late_phase():
 
 def test_full_workload_4_duplicates_theta_sweep():
     _check(4, [0.2, 0.5, 0.8], synth.WORKLOADS[4].schedule(0)["exaggeration"])
+
+
+def test_full_run_kl_workload_1():
+    """1000 iterations of the 70k workload's schedule through the locality layout
+    and in the oracle (fp64, its own trajectory): the final KL divergences, both
+    with the exact O(n^2) Z, agree within 1%."""
+    inp = synth.make_inputs(1)
+    w = inp.workload
+    dev = torch.device("cuda:0")
+    Y = torch.from_numpy(inp.Y).to(dev)
+    P = bh.Csr.from_numpy(inp.row_ptr, inp.col, inp.val, device=dev)
+    ws = torch.empty(bh.workspace_size(inp.n, inp.nnz), dtype=torch.uint8, device=dev)
+    lay = bh.Layout(P, Y, workspace=ws)
+    u = torch.zeros_like(Y)
+    gains = torch.ones_like(Y)
+    for it in range(w.iters):
+        s = w.schedule(it)
+        bh.step(Y, lay, 0.5, s["exaggeration"], s["learning_rate"], s["momentum"], 0.01, u, gains, workspace=ws)
+    yg = Y.cpu().numpy()
+    say(f"[kl] workload 1: {w.iters} GPU iterations done")
+    y = inp.Y.astype(np.float64)
+    uo = np.zeros_like(y)
+    go = np.ones_like(y)
+    for it in range(w.iters):
+        s = w.schedule(it)
+        oracle.step(y, uo, go, inp.row_ptr, inp.col, inp.val, 0.5, s["exaggeration"], s["learning_rate"],
+                    s["momentum"], 0.01)
+        if it % 200 == 199:
+            say(f"[kl] workload 1: oracle iteration {it + 1}")
+    klg = oracle.kl(yg, inp.row_ptr, inp.col, inp.val)
+    klo = oracle.kl(y, inp.row_ptr, inp.col, inp.val)
+    kl0 = oracle.kl(inp.Y, inp.row_ptr, inp.col, inp.val)
+    say(f"[kl] workload 1: gpu {klg:.6f} oracle {klo:.6f} start {kl0:.6f}")
+    assert klg < kl0 and klo < kl0
+    assert abs(klg - klo) <= 0.01 * klo
