@@ -127,6 +127,7 @@ def main():
     dev = torch.device("cuda:0")
     Y0 = torch.from_numpy(inp.Y).to(dev)
     P = bh.Csr.from_numpy(inp.row_ptr, inp.col, inp.val, device=dev)
+    Pcsr = P  # kept for the KL evaluation
     ws = torch.empty(bh.workspace_size(n, nnz), dtype=torch.uint8, device=dev)
     layout_s = None
     if not args.plain:
@@ -190,6 +191,20 @@ def main():
     log(f"[bench] {args.steps} steps in {elapsed:.3f}s -> {its:.1f} it/s")
     stats_last = bh.get_stats(ws)
     y_final = Y.cpu().numpy()
+
+    # the run's cost: KL of the first and last embedding with the exact Z (all
+    # n^2 pairs), the exact-Z kernel timed on the stream
+    Pc = Pcsr
+    kl_initial = bh.kl(Y0, Pc, bh.z_exact(Y0, workspace=ws), workspace=ws)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    z_final = bh.z_exact(Y, workspace=ws)
+    e1.record()
+    torch.cuda.synchronize()
+    z_ms = e0.elapsed_time(e1)
+    cost = {"kl_initial": kl_initial, "kl_final": bh.kl(Y, Pc, z_final, workspace=ws), "z_exact_final": z_final,
+            "z_exact_ms": z_ms, "z_pair_terms_per_s": float(n) * n / (z_ms * 1e-3)}
+    log(f"[bench] KL {cost['kl_initial']:.5f} -> {cost['kl_final']:.5f}, exact Z in {z_ms:.1f} ms")
 
     # the other phases: a replay of the first iterations with every phase timed
     reset()
@@ -299,6 +314,7 @@ def main():
         "config": {"workload": f"{w.description} (workload {w.cid})", "n": n, "nnz": nnz,
                    "theta": args.theta, "iterations": f"0..{args.steps - 1} of the schedule"},
         "iterations_per_s_by_stretch": segments,
+        "cost": cost,
         "interactions_per_s": (inter_total / elapsed) if inter_total is not None else None,
         "interactions_per_iteration": (inter_total / args.steps) if inter_total is not None else None,
         "nodes_last": stats_last["nodes"],

@@ -204,6 +204,28 @@ int bhtsne_timing_enable(int enable);
 int bhtsne_timing_phases(uint32_t phase_mask);
 int bhtsne_timing_read(bhtsne_timing *out, int reset);
 
+/* Cost evaluation (Background: the KL divergence of P and Q), outside an
+ * iteration; a run calls it to report its cost.  Both calls clear the device
+ * flags of the workspace like a step, synchronise the stream and return their
+ * result on the host.
+ *
+ * bhtsne_z_exact: the exact normaliser of q_ij, Z = sum over ordered pairs
+ * i != j of (1 + |y_i - y_j|^2)^-1, over all n^2 pairs (fp32 pair terms, fp64
+ * accumulation in a fixed order, so the result is reproducible).  Y: device,
+ * n x 2 fp32; Z: host.  The workspace is sized as for
+ * bhtsne_workspace_size(n, 0) or larger.  A non-finite result is
+ * BHTSNE_ENONFINITE.
+ *
+ * bhtsne_kl: KL(P || Q) = sum over the stored entries with p_ij > 0 of
+ * p_ij log(p_ij / q_ij), q_ij = (1 + |y_i - y_j|^2)^-1 / Z, for a given
+ * Z > 0 (the exact one, or a step's Barnes-Hut estimate), in fp64 from the
+ * fp32 inputs.  A column outside [0, n) is skipped and reported as
+ * BHTSNE_EDEVICE. */
+int bhtsne_z_exact(const float *Y, int64_t n, double *Z, void *workspace, size_t workspace_bytes,
+                   hipStream_t stream);
+int bhtsne_kl(const float *Y, const bhtsne_csr *P, double Z, double *kl, void *workspace, size_t workspace_bytes,
+              hipStream_t stream);
+
 /* Test export: bounding box, Morton codes and their sort (Quadtree Building,
  * Algorithm 1).  codes (original order), sorted_codes and perm (sorted
  * position -> original index) are device arrays of n entries, each nullable.

@@ -28,4 +28,6 @@ from ._binding import (  # noqa: F401
     timing_phases,
     timing_read,
     workspace_size,
+    z_exact,
+    kl,
 )

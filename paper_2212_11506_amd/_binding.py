@@ -76,6 +76,8 @@ def load_library():
         "bhtsne_status_string": (C.c_char_p, [C.c_int]),
         "bhtsne_timing_enable": (C.c_int, [C.c_int]),
         "bhtsne_timing_phases": (C.c_int, [C.c_uint32]),
+        "bhtsne_z_exact": (C.c_int, [vp, i64, C.POINTER(C.c_double), vp, C.c_size_t, vp]),
+        "bhtsne_kl": (C.c_int, [vp, C.POINTER(_Csr), C.c_double, C.POINTER(C.c_double), vp, C.c_size_t, vp]),
         "bhtsne_timing_read": (C.c_int, [C.POINTER(_Timing), C.c_int]),
         "bhtsne_debug_sort": (C.c_int, [vp, i64, vp, vp, vp, f64p, vp, C.c_size_t, vp]),
         "bhtsne_debug_tree": (C.c_int, [vp, i64, f32, C.POINTER(C.c_int64), vp, vp, vp, vp, vp, vp, vp,
@@ -201,6 +203,29 @@ def gradient(Y: torch.Tensor, P, theta: float, exaggeration: float = 1.0,
                              _ptr(ws, None, "workspace"), ws.numel(), _stream())
     _check(rc, fn.__name__)
     return grad, (z.value if return_z else None)
+
+
+def z_exact(Y: torch.Tensor, workspace: Optional[torch.Tensor] = None) -> float:
+    """bhtsne_z_exact: the exact normaliser over all ordered pairs i != j."""
+    lib = load_library()
+    n = Y.shape[0]
+    ws, _ = _workspace(n, 0, workspace)
+    z = C.c_double(0.0)
+    _check(lib.bhtsne_z_exact(_ptr(Y, torch.float32, "Y"), n, C.byref(z), _ptr(ws, None, "workspace"),
+                              ws.numel(), _stream()), "bhtsne_z_exact")
+    return z.value
+
+
+def kl(Y: torch.Tensor, P: "Csr", Z: float, workspace: Optional[torch.Tensor] = None) -> float:
+    """bhtsne_kl: KL(P || Q) over P's stored entries for the given normaliser Z."""
+    lib = load_library()
+    if not isinstance(P, Csr):
+        raise TypeError("kl takes P as a Csr")
+    ws, _ = _workspace(P.n, 0, workspace)
+    out = C.c_double(0.0)
+    _check(lib.bhtsne_kl(_ptr(Y, torch.float32, "Y"), P.struct, float(Z), C.byref(out),
+                         _ptr(ws, None, "workspace"), ws.numel(), _stream()), "bhtsne_kl")
+    return out.value
 
 
 def step(Y: torch.Tensor, P, theta: float, exaggeration: float, learning_rate: float,

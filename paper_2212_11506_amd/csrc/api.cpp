@@ -564,6 +564,42 @@ int bhtsne_debug_sort(const float *Y, int64_t n, uint64_t *codes, uint64_t *sort
     return BHTSNE_OK;
 }
 
+int bhtsne_z_exact(const float *Y, int64_t n, double *Z, void *workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    if (!Y || !Z || n < 2 || n > kMaxPoints) return BHTSNE_EINVAL;
+    int rc = check_ws(n, 0, workspace, workspace_bytes);
+    if (rc != BHTSNE_OK) return rc;
+    const Layout L = make_layout(n, 0);
+    launch_z_exact(Y, n, workspace, L, stream);
+    if (hipGetLastError() != hipSuccess) return BHTSNE_EDEVICE;
+    Header h;
+    rc = read_header(workspace, &h, stream);
+    if (rc != BHTSNE_OK) return rc;
+    *Z = h.eval;
+    if (!std::isfinite(h.eval)) return BHTSNE_ENONFINITE;
+    return flags_status(h.flags);
+}
+
+int bhtsne_kl(const float *Y, const bhtsne_csr *P, double Z, double *kl, void *workspace, size_t workspace_bytes,
+              hipStream_t stream)
+{
+    if (!Y || !kl) return BHTSNE_EINVAL;
+    int rc = check_csr(P);
+    if (rc != BHTSNE_OK) return rc;
+    if (!std::isfinite(Z) || !(Z > 0.0)) return BHTSNE_EINVAL;
+    rc = check_ws(P->n, 0, workspace, workspace_bytes);
+    if (rc != BHTSNE_OK) return rc;
+    const Layout L = make_layout(P->n, 0);
+    launch_kl(Y, P->row_ptr, P->col, P->val, P->n, std::log(Z), workspace, L, stream);
+    if (hipGetLastError() != hipSuccess) return BHTSNE_EDEVICE;
+    Header h;
+    rc = read_header(workspace, &h, stream);
+    if (rc != BHTSNE_OK) return rc;
+    *kl = h.eval;
+    if (!std::isfinite(h.eval)) return BHTSNE_ENONFINITE;
+    return flags_status(h.flags);
+}
+
 int bhtsne_debug_tree(const float *Y, int64_t n, float theta, int64_t *n_nodes, uint8_t *level, uint8_t *kind,
                       uint32_t *begin, uint32_t *end, float *summary, uint32_t *meta, void *workspace,
                       size_t workspace_bytes, hipStream_t stream)

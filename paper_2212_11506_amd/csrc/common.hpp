@@ -25,6 +25,10 @@ constexpr int kScanBlock = 256;
 constexpr int kScanItems = 4;
 constexpr int kScanTile = kScanBlock * kScanItems;
 constexpr int kBBoxBlocks = 512;
+// evaluation kernels: the exact Z takes blocks of kZEvalPoints points, the KL
+// at most kEvalMaxBlocks blocks striding over the rows
+constexpr int kZEvalPoints = 2048;
+constexpr int kEvalMaxBlocks = 2048;
 // repulsive walk: 16 waves of consecutive points per block share one CU, so
 // their walks, which overlap in most nodes, share the scalar cache's lines
 constexpr int kRepBlock = 1024;
@@ -78,7 +82,9 @@ struct Header {
     uint32_t ticket_bbox;
     uint32_t ticket_rep;
     uint32_t attract_next; // next item of the persistent attractive kernel
-    uint32_t pad[5];
+    uint32_t ticket_eval;  // blocks done of an evaluation kernel (exact Z, KL)
+    uint32_t pad[4];
+    double eval;           // result of the last evaluation call
 };
 
 // A node of the pre-order tree: one 16-byte record
@@ -90,7 +96,7 @@ struct Header {
 struct Layout {
     int64_t n, nnz, sort_tiles, scan_tiles, rep_blocks;
     size_t header, hist, bbox_part, codes0, codes1, idx0, idx1, status, ycopy, ys, levelmask,
-        split_b, split_e, base, psum, scan_cnt, scan_sum, nodes, thr_table, frep, fattr, partial, zpart, ipart, total;
+        split_b, split_e, base, psum, scan_cnt, scan_sum, nodes, thr_table, frep, fattr, partial, zpart, ipart, eval_part, total;
 };
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -141,6 +147,8 @@ inline Layout make_layout(int64_t n, int64_t nnz)
     // kTileMaxSeg tiles of kTileRows rows per row block
     L.partial = take(8 * size_t((n + kTileRows - 1) / kTileRows) * kTileRows * kTileMaxSeg);
     L.zpart = take(8 * size_t(L.rep_blocks));
+    const int64_t zb = (n + kZEvalPoints - 1) / kZEvalPoints;
+    L.eval_part = take(8 * size_t(zb > kEvalMaxBlocks ? zb : kEvalMaxBlocks));
     L.ipart = take(8 * size_t(L.rep_blocks));
     L.total = off;
     return L;

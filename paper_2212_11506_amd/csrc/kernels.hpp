@@ -65,6 +65,10 @@ void launch_morton(const float *Y, int64_t n, const uint32_t *rank, void *ws, co
 // ysrc: Y in the original order, gathered into Morton order by the last pass
 void launch_sort(int64_t n, const float *ysrc, void *ws, const Layout &L, hipStream_t st);
 void launch_tree(int64_t n, float theta, void *ws, const Layout &L, const TreeDebug &dbg, hipStream_t st);
+// evaluation: exact Z and KL, results in the header's eval field
+void launch_z_exact(const float *Y, int64_t n, void *ws, const Layout &L, hipStream_t st);
+void launch_kl(const float *Y, const int64_t *row_ptr, const int32_t *col, const float *val, int64_t n,
+               double log_z, void *ws, const Layout &L, hipStream_t st);
 // the tree's records as {com, count, threshold} and documented meta words (both nullable)
 void launch_tree_unpack(int64_t n, void *ws, const Layout &L, float *summary, uint32_t *meta, hipStream_t st);
 void launch_repulsive(int64_t n, void *ws, const Layout &L, hipStream_t st);

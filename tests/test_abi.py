@@ -100,6 +100,23 @@ def test_gradient_rejects_bad_arguments(case):
     assert _grad(lib, P, **kw) == bh.BHTSNE_EINVAL
 
 
+def test_evaluation_calls_reject_bad_arguments():
+    lib = bh.load_library()
+    z = C.c_double(0.0)
+    ws = C.c_void_p(FAKE)
+    assert lib.bhtsne_z_exact(None, 10, C.byref(z), ws, 1 << 40, None) == bh.BHTSNE_EINVAL
+    assert lib.bhtsne_z_exact(C.c_void_p(FAKE), 1, C.byref(z), ws, 1 << 40, None) == bh.BHTSNE_EINVAL
+    assert lib.bhtsne_z_exact(C.c_void_p(FAKE), 10, None, ws, 1 << 40, None) == bh.BHTSNE_EINVAL
+    assert lib.bhtsne_z_exact(C.c_void_p(FAKE), 10, C.byref(z), None, 1 << 40, None) == bh.BHTSNE_EWORKSPACE
+    assert lib.bhtsne_z_exact(C.c_void_p(FAKE), 10, C.byref(z), ws, 16, None) == bh.BHTSNE_EWORKSPACE
+    P = bh._binding._Csr(10, 20, C.c_void_p(FAKE), C.c_void_p(FAKE), C.c_void_p(FAKE))
+    for bad_z in (0.0, -1.0, float("nan"), float("inf")):
+        assert lib.bhtsne_kl(C.c_void_p(FAKE), C.byref(P), bad_z, C.byref(z), ws, 1 << 40, None) == bh.BHTSNE_EINVAL
+    assert lib.bhtsne_kl(C.c_void_p(FAKE), None, 1.0, C.byref(z), ws, 1 << 40, None) == bh.BHTSNE_EINVAL
+    assert lib.bhtsne_kl(None, C.byref(P), 1.0, C.byref(z), ws, 1 << 40, None) == bh.BHTSNE_EINVAL
+    assert lib.bhtsne_kl(C.c_void_p(FAKE), C.byref(P), 1.0, None, ws, 1 << 40, None) == bh.BHTSNE_EINVAL
+
+
 def test_timing_phase_mask():
     lib = bh.load_library()
     assert lib.bhtsne_timing_phases(1 << len(bh.PHASES)) == bh.BHTSNE_EINVAL
