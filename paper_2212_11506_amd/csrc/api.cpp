@@ -246,7 +246,7 @@ int run(float *Y, const bhtsne_csr *P, float theta, const StepArgs &a, float *up
     build_tree(Y, n, theta, nullptr, ws, L, TreeDebug{}, st);
     {
         PhaseTimer pt(BHTSNE_PHASE_REPULSIVE, st);
-        launch_repulsive(n, ws, L, st);
+        launch_repulsive(n, repulsive_self_test(theta), ws, L, st);
     }
     {
         PhaseTimer pt(BHTSNE_PHASE_ATTRACTIVE, st);
@@ -331,7 +331,7 @@ int run_layout(float *Y, const bhtsne_layout *lay, float theta, const StepArgs &
     }
     {
         PhaseTimer pt(BHTSNE_PHASE_REPULSIVE, st);
-        launch_repulsive(n, ws, L, st);
+        launch_repulsive(n, repulsive_self_test(theta), ws, L, st);
     }
     if (side && hipStreamWaitEvent(st, side->join, 0) != hipSuccess) return BHTSNE_EDEVICE;
     if (lk.owns_lock()) lk.unlock();

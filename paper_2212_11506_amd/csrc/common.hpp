@@ -32,16 +32,16 @@ constexpr int kEvalMaxBlocks = 2048;
 // repulsive walk: 16 waves of consecutive points per block share one CU, so
 // their walks, which overlap in most nodes, share the scalar cache's lines
 constexpr int kRepBlock = 1024;
-// meta word of a node (the fourth word of its record):
-//   cell (internal or bucket): level << kMetaLevelShift | skip index
-//   single point:              kMetaSingle | sorted position
-constexpr int kMetaLevelShift = 25;
-constexpr uint32_t kMetaSkipMask = (1u << kMetaLevelShift) - 1u;
-constexpr uint32_t kMetaSingle = 0xFE000000u; // level field all ones, sign bit set
-constexpr uint32_t kLeafBit = 0x80000000u;    // single points only
-constexpr int kThrTable = 128;                // thresholds by the meta word's top 7 bits
-constexpr uint32_t kIndexMask = 0x3fffffffu; // meta: begin of a leaf
-// the 2n - 1 node records keep their skip index in 25 bits of the meta word
+// A node of the pre-order tree: one 24-byte record
+//   {com.x, com.y, count, thr, next, self}
+// thr: the acceptance threshold as float bits (a cell of level L is summarised
+//      for a point at squared distance d2 > thr = side(L)^2 / theta^2, +inf
+//      when theta == 0; -1 for a single point, which is always taken);
+// next: byte offset of the first record after the node's subtree;
+// self: the sorted position of a single point, kNodeCell for a cell.
+constexpr int kNodeBytes = 24;
+constexpr uint32_t kNodeCell = 0xFFFFFFFFu;
+// the 2n - 1 records end below 2^32 bytes
 constexpr int64_t kMaxPoints = (int64_t(1) << 24) - 1;
 constexpr int64_t kYPad = 16384 + 2;                   // padding points after the private copy of Y
 // tiled attractive step: rows in blocks of kTileRows, columns in segments of
@@ -87,16 +87,10 @@ struct Header {
     double eval;           // result of the last evaluation call
 };
 
-// A node of the pre-order tree: one 16-byte record
-//   {com.x, com.y, count (float), meta word (bits)}.
-// A cell of level L is summarised for a point at squared distance d2 iff
-// d2 > thr(L) = side(L)^2 / theta^2 (+inf when theta == 0); single points are
-// always taken exactly (thr = -1).  thr_table[m >> kMetaLevelShift] holds
-// these thresholds as float bits (levels 0..32, then -1 for single points).
 struct Layout {
     int64_t n, nnz, sort_tiles, scan_tiles, rep_blocks;
     size_t header, hist, bbox_part, codes0, codes1, idx0, idx1, status, ycopy, ys, levelmask,
-        split_b, split_e, base, psum, scan_cnt, scan_sum, nodes, thr_table, frep, fattr, partial, zpart, ipart, eval_part, total;
+        split_b, split_e, base, psum, scan_cnt, scan_sum, nodes, frep, fattr, partial, zpart, ipart, eval_part, total;
 };
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -139,8 +133,8 @@ inline Layout make_layout(int64_t n, int64_t nnz)
     L.psum = take(16 * size_t(n + 1));
     L.scan_cnt = take(4 * size_t(L.scan_tiles + 1));
     L.scan_sum = take(16 * size_t(L.scan_tiles + 1));
-    L.nodes = take(16 * size_t(2 * n));
-    L.thr_table = take(4 * size_t(kThrTable));
+    // + 8 bytes: the walk loads 32 bytes at a record's offset
+    L.nodes = take(kNodeBytes * size_t(2 * n) + 8);
     L.frep = take(8 * size_t(n));
     L.fattr = take(8 * size_t(n));
     // partial attractive sums, one per (tile, sorted row slot): up to

@@ -8,7 +8,7 @@
 //
 // GPU design: points are processed in Morton order, one lane per point, and a
 // wavefront walks the pre-order node array together.  The current node index
-// is wave-uniform (scalar loads of the 20-byte node record); a lane that
+// is wave-uniform (scalar loads of the 24-byte node record); a lane that
 // summarises a cell parks itself until the walk reaches the cell's skip
 // index, so its own interaction list is exactly the depth-first one, while the
 // wave only descends where some lane needs it.  No stack is needed.
@@ -25,86 +25,80 @@ __device__ inline float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
 
 // Lane masks straight from the vector compares (one instruction each, no
 // conversion through a boolean per lane): predicates as in LLVM's icmp/fcmp.
-constexpr int kCmpUge = 35, kCmpNe = 33, kCmpSgt = 38;
+constexpr int kCmpUge = 35, kCmpNe = 33, kCmpOgt = 2;
 __device__ inline uint64_t mask_uge(uint32_t a, uint32_t b) { return __builtin_amdgcn_uicmp(a, b, kCmpUge); }
 __device__ inline uint64_t mask_ne(uint32_t a, uint32_t b) { return __builtin_amdgcn_uicmp(a, b, kCmpNe); }
-// the predicate, not the operand type, decides signedness
-__device__ inline uint64_t mask_sgt(int32_t a, int32_t b)
+__device__ inline uint64_t mask_ogt(float a, float b) { return __builtin_amdgcn_fcmpf(a, b, kCmpOgt); }
+
+// The interaction with one node in the lanes of `take` only: EXEC is narrowed
+// to the mask for the block and restored after it, so lanes outside keep their
+// sums and resume offsets and no per-lane select is needed.  The instruction
+// between the reciprocal and its first use gives the one wait state that a
+// transcendental result needs before another VALU reads it on gfx950.
+__device__ inline void take_node(uint64_t take, float d2, float dx, float dy, float cnt, uint32_t next, float &z,
+                                 float &fx, float &fy, uint32_t &resume)
 {
-    return __builtin_amdgcn_uicmp(uint32_t(a), uint32_t(b), kCmpSgt);
-}
-// x in the lanes whose bit of m is set, else 0 (one v_cndmask on the mask)
-__device__ inline float keep_lanes(uint64_t m, float x)
-{
-    float r;
-    asm("v_cndmask_b32_e64 %0, 0, %1, %2" : "=v"(r) : "v"(x), "s"(m));
-    return r;
-}
-// x in the lanes whose bit of m is set, else y
-__device__ inline uint32_t pick_lanes_u(uint64_t m, uint32_t x, uint32_t y)
-{
-    uint32_t r;
-    asm("v_cndmask_b32_e64 %0, %1, %2, %3" : "=v"(r) : "v"(y), "v"(x), "s"(m));
-    return r;
+    float w, t;
+    uint64_t saved;
+    asm volatile("s_and_saveexec_b64 %[sv], %[take]\n\t"
+                 "v_add_f32 %[w], 1.0, %[d2]\n\t"
+                 "v_rcp_f32 %[w], %[w]\n\t"
+                 "v_mov_b32 %[res], %[next]\n\t"
+                 "v_mul_f32 %[t], %[cnt], %[w]\n\t"
+                 "v_fmac_f32 %[z], %[cnt], %[w]\n\t"
+                 "v_mul_f32 %[t], %[t], %[w]\n\t"
+                 "v_fmac_f32 %[fx], %[t], %[dx]\n\t"
+                 "v_fmac_f32 %[fy], %[t], %[dy]\n\t"
+                 "s_mov_b64 exec, %[sv]"
+                 : [z] "+v"(z), [fx] "+v"(fx), [fy] "+v"(fy), [res] "+v"(resume), [w] "=&v"(w), [t] "=&v"(t),
+                   [sv] "=&s"(saved)
+                 : [take] "s"(take), [d2] "v"(d2), [cnt] "s"(cnt), [dx] "v"(dx), [dy] "v"(dy), [next] "s"(next)
+                 : "scc");
 }
 
-// One lane per point.  Every visit runs the same straight-line code: a single
-// point is a cell that is always accepted (its threshold is -1) unless it is
-// the lane's own point (its meta word then equals the lane's self code), and
-// a bucket of identical points is a cell whose children are its points.  The
-// acceptance test yields a lane mask, the weight is zeroed outside it, the
-// interaction count is its population, and the next node is a scalar select
-// (the skip index when no lane descends into the cell).  One 16-byte record per
-// node (the meta word in its fourth component) is one scalar load per visit.
+// One lane per point.  Every visit runs the same code on a 24-byte record read
+// with one scalar load: a single point is a node whose threshold (-1) every
+// lane passes, and a bucket of identical points is a cell whose children are
+// its points.  The acceptance test gives the lanes that take the node; the
+// interaction terms are accumulated in those lanes only, which also park until
+// the walk reaches the node's next offset.  The next node is the first child
+// when some active lane descends, else the node's next offset.
 //
-// The threshold of a cell of level L is side(L)^2 / theta^2 = thr(0) * 4^-L,
-// so unless it leaves the normal range its float bits are those of thr(0)
-// minus L << 24; the walk forms them from the meta word's level field in
-// scalar code.  A single point's field is all ones, which takes the bits below
-// zero as an integer, and for squared distances (never negative) the integer
-// order of the bits is the float order, so one signed compare accepts every
-// single point and tests every cell.  When the shortcut does not reproduce the
-// thresholds (theta = 0, or a domain so small or large that thr leaves the
-// normal range) the walk reads each threshold from the table instead.
-template <bool kShift>
-__device__ inline void repulsive_walk(const char *nbase, const uint32_t *__restrict__ thr_table, uint32_t thr0,
-                                      uint32_t total, float2 yi, uint32_t self, uint32_t &resume, float &fx,
-                                      float &fy, float &z, uint32_t &inter)
+// The lane's own point: with theta^2 <= 0.49 no point accepts a cell that
+// contains it (the centre of mass lies in the cell's square, so the squared
+// distance is at most 2 side^2, below side^2 / theta^2), so every lane reaches
+// its own leaf and takes it once with d2 = 0: a weight of exactly 1 in z and
+// nothing in the force, removed after the walk.  Larger theta compares the
+// leaf's position with the lane's.
+template <bool kSelf>
+__device__ inline void repulsive_walk(const char *nbase, uint32_t end, float2 yi, uint32_t si, uint32_t &resume,
+                                      float &fx, float &fy, float &z, uint32_t &inter)
 {
-    uint32_t cur = 0;
-    while (cur < total) {
-        const float4 r = *reinterpret_cast<const float4 *>(nbase + (cur << 4));
-        const uint32_t m = __float_as_uint(r.w);
-        const uint32_t lv = m >> kMetaLevelShift;
-        const uint32_t thr = kShift ? thr0 - (lv << 24) : thr_table[lv];
-        const float dx = yi.x - r.x, dy = yi.y - r.y;
+    uint32_t cur = 0; // byte offset of the current record
+    while (cur < end) {
+        // the record and 8 bytes beyond it: one 32-byte scalar load
+        typedef uint32_t u32x8 __attribute__((ext_vector_type(8)));
+        const u32x8 r = *reinterpret_cast<const u32x8 *>(nbase + cur);
+        const float cx = __uint_as_float(r[0]), cy = __uint_as_float(r[1]);
+        const float cnt = __uint_as_float(r[2]), thr = __uint_as_float(r[3]);
+        const uint32_t next = r[4];
+        const float dx = yi.x - cx, dy = yi.y - cy;
         const float d2 = fmaf(dx, dx, dy * dy);
         const uint64_t act = mask_uge(cur, resume);
-        const uint64_t take = act & mask_sgt(__float_as_int(d2), int32_t(thr)) & mask_ne(m, self);
-        const float wgt = fast_rcp(1.0f + d2);
-        const float nw = keep_lanes(take, r.z * wgt);
-        z += nw;
-        const float nw2 = nw * wgt;
-        fx = fmaf(nw2, dx, fx);
-        fy = fmaf(nw2, dy, fy);
-        inter += uint32_t(__builtin_popcountll(take));
+        uint64_t take = act & mask_ogt(d2, thr);
+        if (kSelf) take &= mask_ne(r[5], si);
         const uint64_t rej = act & ~take;
-        // the skip index of a cell, 0 for a single point (negative meta word)
-        const uint32_t skip = uint32_t(max(int32_t(m), 0)) & kMetaSkipMask;
-        // accepting lanes park until the walk leaves a cell.  A lane that
-        // takes a node is active, so its old resume index is at most cur and
-        // the new one (skip, or 0 after a single point) keeps every later node
-        // that the old one allowed: no max is needed
-        resume = pick_lanes_u(take, skip, resume);
-        // a skip index lies beyond its cell: skip when no lane descends
-        cur = rej ? cur + 1 : max(cur + 1, skip);
+        inter += uint32_t(__builtin_popcountll(take));
+        take_node(take, d2, dx, dy, cnt, next, z, fx, fy, resume);
+        // the first child follows its cell; no lane descends: jump past the subtree
+        cur = rej ? cur + kNodeBytes : next;
     }
 }
 
 __global__ __launch_bounds__(kRepBlock) void repulsive_kernel(
-    const float4 *__restrict__ nodes, const uint32_t *__restrict__ thr_table, const float2 *__restrict__ ys,
-    const uint32_t *__restrict__ perm, Header *__restrict__ hdr, int64_t n, float2 *__restrict__ frep,
-    double *__restrict__ zpart, unsigned long long *__restrict__ ipart)
+    const char *__restrict__ nodes, const float2 *__restrict__ ys, const uint32_t *__restrict__ perm,
+    Header *__restrict__ hdr, int64_t n, int self_test, float2 *__restrict__ frep, double *__restrict__ zpart,
+    unsigned long long *__restrict__ ipart)
 {
     const uint32_t nb = gridDim.x;
     const uint32_t lb = xcd_contiguous(blockIdx.x, nb);
@@ -112,28 +106,23 @@ __global__ __launch_bounds__(kRepBlock) void repulsive_kernel(
     const int64_t s64 = int64_t(lb) * kRepBlock + threadIdx.x;
     const bool valid = s64 < n;
     const uint32_t si = uint32_t(s64);
-    const uint32_t self = kMetaSingle | si; // meta word of this lane's own single-point node
     const float2 yi = valid ? ys[s64] : make_float2(0.0f, 0.0f);
     uint32_t resume = valid ? 0u : 0xffffffffu;
     float fx = 0.0f, fy = 0.0f, z = 0.0f;
     uint32_t total = uniform(hdr->nodes);
-    const uint32_t cap = uint32_t(2 * n);
+    const uint32_t cap = uint32_t(2 * n - 1);
     total = total < cap ? total : cap;
-    // does thr(0) - (L << 24) reproduce the thresholds of levels 0..32, and
-    // stay above the bits of every single point's field?
-    const uint32_t thr0 = uniform(thr_table[0]);
-    const int lane = lane_id();
-    const uint32_t tl = thr_table[lane < 33 ? lane : 0];
-    const bool shift_ok = lane >= 33 || tl == thr0 - (uint32_t(lane) << 24);
-    const bool shift = ballot(shift_ok) == ~0ull && thr0 < 0x7F000000u;
-    // node records by 32-bit byte offset (fewer than 2^27 nodes)
-    const char *nbase = reinterpret_cast<const char *>(nodes);
+    const uint32_t end = total * uint32_t(kNodeBytes);
 
     uint32_t inter = 0; // this wave's interactions (a launch has fewer than 2^32 per wave)
-    if (shift)
-        repulsive_walk<true>(nbase, thr_table, thr0, total, yi, self, resume, fx, fy, z, inter);
-    else
-        repulsive_walk<false>(nbase, thr_table, thr0, total, yi, self, resume, fx, fy, z, inter);
+    if (self_test) {
+        repulsive_walk<true>(nodes, end, yi, si, resume, fx, fy, z, inter);
+    } else {
+        repulsive_walk<false>(nodes, end, yi, si, resume, fx, fy, z, inter);
+        // each valid lane took its own leaf once, with weight 1
+        if (valid) z -= 1.0f;
+        inter -= uint32_t(__builtin_popcountll(ballot(valid)));
+    }
 
     if (valid) {
         const uint32_t p = perm[si];
@@ -257,11 +246,11 @@ __global__ __launch_bounds__(256) void attract_kernel(
 }
 
 // ------------------------------------------------------------------ launchers
-void launch_repulsive(int64_t n, void *ws, const Layout &L, hipStream_t st)
+void launch_repulsive(int64_t n, bool self_test, void *ws, const Layout &L, hipStream_t st)
 {
     repulsive_kernel<<<unsigned(L.rep_blocks), kRepBlock, 0, st>>>(
-        at<float4>(ws, L.nodes), at<uint32_t>(ws, L.thr_table), at<float2>(ws, L.ys), at<uint32_t>(ws, L.idx0),
-        at<Header>(ws, L.header), n, at<float2>(ws, L.frep), at<double>(ws, L.zpart),
+        at<char>(ws, L.nodes), at<float2>(ws, L.ys), at<uint32_t>(ws, L.idx0), at<Header>(ws, L.header), n,
+        self_test ? 1 : 0, at<float2>(ws, L.frep), at<double>(ws, L.zpart),
         at<unsigned long long>(ws, L.ipart));
 }
 

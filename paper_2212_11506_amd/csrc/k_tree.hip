@@ -387,8 +387,15 @@ __device__ inline float accept_threshold(double rspan, int L, double theta2)
     return float(side * side / theta2);
 }
 
-// meta word of a cell of level L whose subtree ends before node skip
-__device__ inline uint32_t cell_meta(int L, uint32_t skip) { return (uint32_t(L) << kMetaLevelShift) | skip; }
+// one node record, as three 8-byte stores (records are 8-byte aligned)
+__device__ inline void store_node(char *__restrict__ nodes, int64_t pre, float2 com, float count, float thr,
+                                  uint32_t next, uint32_t self)
+{
+    uint2 *r = reinterpret_cast<uint2 *>(nodes + pre * kNodeBytes);
+    r[0] = make_uint2(__float_as_uint(com.x), __float_as_uint(com.y));
+    r[1] = make_uint2(__float_as_uint(count), __float_as_uint(thr));
+    r[2] = make_uint2(next, self);
+}
 
 // Centre of mass of the sorted points [b, e).  Small cells sum their points
 // directly (fp64, relative to the first point, so nothing cancels); larger
@@ -418,22 +425,23 @@ __global__ __launch_bounds__(256) void tree_nodes_kernel(
     const uint64_t *__restrict__ codes, int64_t n, const uint32_t *__restrict__ levelmask,
     const uint32_t *__restrict__ split_b, const uint32_t *__restrict__ split_e,
     const uint32_t *__restrict__ base, const double2 *__restrict__ psum, const float2 *__restrict__ ys,
-    Header *__restrict__ hdr, float theta, float4 *__restrict__ nodes, uint32_t *__restrict__ thr_table,
-    TreeDebug dbg)
+    Header *__restrict__ hdr, float theta, char *__restrict__ nodes, TreeDebug dbg)
 {
     int64_t x = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
     const double c0 = hdr->cent[0], c1 = hdr->cent[1], rspan = hdr->rspan;
-    const double theta2 = double(theta) * double(theta);
-    // thresholds by the meta word's top 7 bits: levels 0..32, then single points
-    // (the grid has at least one block of 256 threads, whatever n is)
-    if (x < kThrTable) thr_table[x] = __float_as_uint(x <= 32 ? accept_threshold(rspan, int(x), theta2) : -1.0f);
+    // acceptance thresholds of the cell levels 0..32 (32: buckets)
+    __shared__ float s_thr[33];
+    if (threadIdx.x < 33) s_thr[threadIdx.x] = accept_threshold(rspan, int(threadIdx.x), double(theta) * double(theta));
+    __syncthreads();
     if (x >= n) return;
-    auto emit = [&](int64_t pre, float2 com, int64_t b, int64_t e, int L, uint32_t m, int kind) {
-        if (pre >= 2 * n) { // only reachable from a corrupted sort
+    auto emit = [&](int64_t pre, float2 com, int64_t b, int64_t e, int L, int64_t next, int kind) {
+        if (pre >= 2 * n || next > 2 * n) { // only reachable from a corrupted sort
             atomicOr(&hdr->flags, kErrRange);
             return;
         }
-        nodes[pre] = make_float4(com.x, com.y, float(e - b), __uint_as_float(m));
+        const bool single = kind == 2;
+        store_node(nodes, pre, com, float(e - b), single ? -1.0f : s_thr[L], uint32_t(next * kNodeBytes),
+                   single ? uint32_t(b) : kNodeCell);
         if (dbg.level) {
             dbg.level[pre] = uint8_t(L);
             dbg.kind[pre] = uint8_t(kind);
@@ -446,14 +454,13 @@ __global__ __launch_bounds__(256) void tree_nodes_kernel(
         int64_t b = split_b[x], e = split_e[x];
         int L = split_level(codes[x], codes[x + 1]);
         int64_t pre = base[b] + __popc(levelmask[b] & ((1u << L) - 1u));
-        emit(pre, centre_of_mass(psum, ys, b, e, c0, c1), b, e, L, cell_meta(L, base[e]), 0);
+        emit(pre, centre_of_mass(psum, ys, b, e, c0, c1), b, e, L, base[e], 0);
     }
     // (b) the root, when no split lies at level 0 (all points in one quadrant)
     if (x == 0 && quad_digit(codes[0], 0) == quad_digit(codes[n - 1], 0))
-        emit(0, centre_of_mass(psum, ys, 0, n, c0, c1), 0, n, 0, cell_meta(0, base[n]), 0);
+        emit(0, centre_of_mass(psum, ys, 0, n, c0, c1), 0, n, 0, base[n], 0);
     // (c) the leaf of point x, preceded by its bucket when a run of identical
     // codes starts at x (bucket members are leaves at level 33)
-    const uint32_t single = kMetaSingle | uint32_t(x);
     if (x == 0 || codes[x - 1] != codes[x]) {
         int64_t e = run_end(codes, x, n);
         int64_t pre = base[x] + __popc(levelmask[x]);
@@ -464,32 +471,31 @@ __global__ __launch_bounds__(256) void tree_nodes_kernel(
                 int r = split_level(codes[x], codes[x + 1]);
                 lv = r > lv ? r : lv;
             }
-            emit(pre, ys[x], x, e, lv + 1, single, 2);
+            emit(pre, ys[x], x, e, lv + 1, pre + 1, 2);
         } else {
-            emit(pre, centre_of_mass(psum, ys, x, e, c0, c1), x, e, 32, cell_meta(32, base[e]), 1);
-            emit(pre + 1, ys[x], x, x + 1, 33, single, 2);
+            emit(pre, centre_of_mass(psum, ys, x, e, c0, c1), x, e, 32, base[e], 1);
+            emit(pre + 1, ys[x], x, x + 1, 33, pre + 2, 2);
         }
     } else {
-        emit(base[x], ys[x], x, x + 1, 33, single, 2); // a later member of a bucket
+        emit(base[x], ys[x], x, x + 1, 33, int64_t(base[x]) + 1, 2); // a later member of a bucket
     }
 }
 
 // ------------------------------------------------------------------ debug export
 // Records in the documented form: {com, count, threshold} and the meta word as
 // the skip index of a cell or begin | 0xC0000000 for a single point.
-__global__ __launch_bounds__(256) void tree_unpack_kernel(const float4 *__restrict__ nodes,
-                                                          const uint32_t *__restrict__ thr_table,
+__global__ __launch_bounds__(256) void tree_unpack_kernel(const char *__restrict__ nodes,
                                                           const Header *__restrict__ hdr, int64_t cap,
                                                           float4 *__restrict__ summary, uint32_t *__restrict__ meta)
 {
     const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
     const int64_t count = hdr->nodes < cap ? int64_t(hdr->nodes) : cap;
     if (i >= count) return;
-    const float4 r = nodes[i];
-    const uint32_t m = __float_as_uint(r.w);
-    const bool single = (m & kLeafBit) != 0;
-    if (summary) summary[i] = make_float4(r.x, r.y, r.z, __uint_as_float(thr_table[m >> kMetaLevelShift]));
-    if (meta) meta[i] = single ? ((m & kMetaSkipMask) | 0xC0000000u) : (m & kMetaSkipMask);
+    const uint2 *r = reinterpret_cast<const uint2 *>(nodes + i * kNodeBytes);
+    const uint2 a = r[0], b = r[1], c = r[2];
+    if (summary)
+        summary[i] = make_float4(__uint_as_float(a.x), __uint_as_float(a.y), __uint_as_float(b.x), __uint_as_float(b.y));
+    if (meta) meta[i] = c.y != kNodeCell ? (c.y | 0xC0000000u) : c.x / uint32_t(kNodeBytes);
 }
 
 // ------------------------------------------------------------------ launchers
@@ -509,14 +515,14 @@ void launch_tree(int64_t n, float theta, void *ws, const Layout &L, const TreeDe
     scan_reduce_kernel<<<unsigned(L.scan_tiles), kScanBlock, 0, st>>>(codes, lm, ys, hdr, n, tc, ts);
     scan_top_kernel<<<1, kScanBlock, 0, st>>>(tc, ts, L.scan_tiles, n, base, psum, hdr);
     scan_down_kernel<<<unsigned(L.scan_tiles), kScanBlock, 0, st>>>(codes, lm, ys, hdr, n, tc, ts, base, psum);
-    tree_nodes_kernel<<<gn, 256, 0, st>>>(codes, n, lm, sb, se, base, psum, ys, hdr, theta,
-                                          at<float4>(ws, L.nodes), at<uint32_t>(ws, L.thr_table), dbg);
+    tree_nodes_kernel<<<gn, 256, 0, st>>>(codes, n, lm, sb, se, base, psum, ys, hdr, theta, at<char>(ws, L.nodes),
+                                          dbg);
 }
 
 void launch_tree_unpack(int64_t n, void *ws, const Layout &L, float *summary, uint32_t *meta, hipStream_t st)
 {
     tree_unpack_kernel<<<unsigned((2 * n + 255) / 256), 256, 0, st>>>(
-        at<float4>(ws, L.nodes), at<uint32_t>(ws, L.thr_table), at<Header>(ws, L.header), 2 * n,
+        at<char>(ws, L.nodes), at<Header>(ws, L.header), 2 * n,
         reinterpret_cast<float4 *>(summary), meta);
 }
 

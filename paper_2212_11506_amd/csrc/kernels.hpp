@@ -71,7 +71,10 @@ void launch_kl(const float *Y, const int64_t *row_ptr, const int32_t *col, const
                double log_z, void *ws, const Layout &L, hipStream_t st);
 // the tree's records as {com, count, threshold} and documented meta words (both nullable)
 void launch_tree_unpack(int64_t n, void *ws, const Layout &L, float *summary, uint32_t *meta, hipStream_t st);
-void launch_repulsive(int64_t n, void *ws, const Layout &L, hipStream_t st);
+// theta^2 <= 0.49: no point accepts a cell containing it, so the walk needs no
+// comparison with the lane's own leaf
+inline bool repulsive_self_test(float theta) { return double(theta) * double(theta) > 0.49; }
+void launch_repulsive(int64_t n, bool self_test, void *ws, const Layout &L, hipStream_t st);
 void launch_attract(const int64_t *row_ptr, const int32_t *col, const float *val, int64_t n, int64_t nnz,
                     const StepArgs &a, float *Y, float *upd, float *gains, float *grad, void *ws, const Layout &L,
                     hipStream_t st);
