@@ -260,6 +260,48 @@ def make_inputs(cid: int, n: Optional[int] = None, progress=None, k: int = K_NEI
     return Inputs(w, n, Y, row_ptr, col, val, labels, time.time() - t0)
 
 
+@dataclasses.dataclass
+class Knn:
+    """Neighbour lists as a k-nearest-neighbour search returns them."""
+    n: int
+    k: int
+    idx: np.ndarray        # (n, k) int32, each row's neighbours by increasing distance
+    dist: np.ndarray       # (n, k) float32, ascending within each row
+    labels: np.ndarray     # (n,) int32 cluster id
+    gen_seconds: float = 0.0
+
+
+def make_knn(cid: int, n: Optional[int] = None, k: int = K_NEIGHBOURS, progress=None) -> Knn:
+    """Neighbour lists of workload ``cid``: the same clusters and neighbour
+    draw as its P (row i takes k distinct members of its own cluster), with
+    distances d ~ U(0, 3) sorted ascending per row.  Every cluster must have
+    more than k members."""
+    t0 = time.time()
+    w = WORKLOADS[cid]
+    n = w.n if n is None else int(n)
+    rng_sz, rng_lab, rng_nb, rng_w, _ = _streams(cid)
+    sizes = cluster_sizes(w, n, rng_sz)
+    if sizes.min() <= k:
+        raise ValueError(f"a cluster of {sizes.min()} points cannot give {k} neighbours")
+    perm = rng_lab.permutation(n)
+    labels = np.empty(n, np.int32)
+    idx = np.empty((n, k), np.int32)
+    off = 0
+    for c in range(sizes.size):
+        members = perm[off:off + sizes[c]]
+        off += sizes[c]
+        labels[members] = c
+        _, cols = _neighbours_for_cluster(members, k, rng_nb)
+        idx[members] = cols.reshape(members.size, k)
+        if progress and c % 10 == 9:
+            progress(f"[synth] knn {cid}: cluster {c + 1}/{sizes.size}")
+    dist = rng_w.uniform(0.0, 3.0, size=(n, k)).astype(np.float32)
+    order = np.argsort(dist, axis=1, kind="stable")
+    dist = np.take_along_axis(dist, order, axis=1)
+    idx = np.take_along_axis(idx, order, axis=1)
+    return Knn(n, k, idx, dist, labels, time.time() - t0)
+
+
 def random_y(n: int, seed: int, scale: float = 1.0, dups: int = 0) -> np.ndarray:
     """Small free-form embeddings for edge-case tests (float32, n x 2)."""
     rng = Generator(PCG64(SeedSequence(seed)))
