@@ -50,7 +50,9 @@ typedef enum {
     BHTSNE_EINVAL = -1,     /* an argument failed a host-side check */
     BHTSNE_EWORKSPACE = -2, /* workspace missing, misaligned or too small */
     BHTSNE_ENONFINITE = -3, /* Y held a NaN or an infinity */
-    BHTSNE_EDEVICE = -4     /* a HIP call failed or the GPU flagged an internal error */
+    BHTSNE_EDEVICE = -4,    /* a HIP call failed or the GPU flagged an internal error */
+    BHTSNE_EINPUT = -5,     /* the GPU found invalid input data (bhtsne_affinities) */
+    BHTSNE_ECAPACITY = -6   /* output arrays too small; the required size is returned */
 } bhtsne_status;
 
 /* Sparse symmetric P in CSR form (0-based columns).  Expected, not checked:
@@ -248,6 +250,43 @@ int bhtsne_debug_sort(const float *Y, int64_t n, uint64_t *codes, uint64_t *sort
 int bhtsne_debug_tree(const float *Y, int64_t n, float theta, int64_t *n_nodes, uint8_t *level, uint8_t *kind,
                       uint32_t *begin, uint32_t *end, float *summary, uint32_t *meta, void *workspace,
                       size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Input similarities (Background, "Input similarity computation": the sparse
+ * approximation of p_{j|i} over the k nearest neighbours and the
+ * symmetrisation p_ij = (p_{j|i} + p_{i|j}) / (2N); Binary Search
+ * Perplexity).  For every point i, sigma_i^2 is found by bisection (the middle
+ * point of the current interval each step, run to machine precision in fp64)
+ * so that the perplexity exp(H) of
+ *     p_{j|i} = exp(-d_ij^2 / 2 sigma_i^2) / sum_l exp(-d_il^2 / 2 sigma_i^2)
+ * equals `perplexity`; then P is symmetrised over the union of the neighbour
+ * relations in both directions.  With perplexity > k the row ends uniform
+ * (sigma^2 = +inf); at or below the number of ties at the minimum distance it
+ * ends uniform over those ties.
+ *
+ * knn_idx   [n * k] int32, device: row i lists k distinct neighbours of i (any
+ *           order, none equal to i, all in [0, n)).
+ * knn_dist  [n * k] float32, device: the matching distances (not squared),
+ *           finite and >= 0.
+ * row_ptr   [n + 1] int64, device, written: the CSR row pointers of P.
+ * col, val  [capacity] device, written: columns (sorted within each row) and
+ *           fp32 values of P; nullable when capacity == 0.
+ * nnz       host out: the entry count of P (between n k and 2 n k), also
+ *           when the call fails with BHTSNE_ECAPACITY, so the caller can size
+ *           col and val and call again.
+ * sigma2    [n] fp64, device, nullable: sigma_i^2.
+ * Limits: 1 <= k <= 256, k < n <= 16777215; a row of P holds at most 4096
+ * entries (k plus the number of points that list i and that i does not list).
+ * The call synchronises `stream` twice (to learn nnz, then to report).
+ * Errors: BHTSNE_EINVAL (arguments), BHTSNE_EWORKSPACE, BHTSNE_ENONFINITE (a
+ * NaN, infinite or negative distance), BHTSNE_EINPUT (a neighbour index out of
+ * range, equal to its row or repeated within a row, or a row over 4096
+ * entries; col and val then hold no usable result), BHTSNE_ECAPACITY,
+ * BHTSNE_EDEVICE.  The library allocates nothing. */
+size_t bhtsne_affinities_workspace_size(int64_t n, int32_t k);
+int bhtsne_affinities(const int32_t *knn_idx, const float *knn_dist, int64_t n, int32_t k, double perplexity,
+                      int64_t *row_ptr, int32_t *col, float *val, int64_t capacity, int64_t *nnz, double *sigma2,
+                      void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 #ifdef __cplusplus
 }

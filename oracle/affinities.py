@@ -47,7 +47,8 @@ def _entropy(dp: np.ndarray, s2: np.ndarray) -> np.ndarray:
         a = np.where(np.isinf(s2)[:, None], 0.0, a)
         w = np.exp(-a)
         s = w.sum(axis=1)
-        return np.log(s) + (a * w).sum(axis=1) / s
+        # a e^-a -> 0 where the weight underflows (a = inf)
+        return np.log(s) + np.where(w > 0.0, a * w, 0.0).sum(axis=1) / s
 
 
 def sigma2(dist: np.ndarray, u: float) -> np.ndarray:

@@ -1,4 +1,4 @@
-"""MI355X (gfx950) Barnes-Hut t-SNE gradient step.
+"""MI355X (gfx950) Barnes-Hut t-SNE gradient step and input similarities.
 
 A thin ctypes binding over ``lib/libbhtsne.so`` (C ABI in ``include/bhtsne.h``).
 PyTorch only provides device memory and the current stream; every step of
@@ -6,7 +6,9 @@ the computation runs in the library's HIP kernels.  The functions keep the C
 names without the ``bhtsne_`` prefix.
 """
 from ._binding import (  # noqa: F401
+    BHTSNE_ECAPACITY,
     BHTSNE_EDEVICE,
+    BHTSNE_EINPUT,
     BHTSNE_EINVAL,
     BHTSNE_ENONFINITE,
     BHTSNE_EWORKSPACE,
@@ -15,6 +17,8 @@ from ._binding import (  # noqa: F401
     BhtsneError,
     Csr,
     Layout,
+    affinities,
+    affinities_workspace_size,
     debug_sort,
     debug_tree,
     get_stats,

@@ -17,6 +17,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB = os.path.join(_HERE, "lib", "libbhtsne.so")
 
 BHTSNE_OK, BHTSNE_EINVAL, BHTSNE_EWORKSPACE, BHTSNE_ENONFINITE, BHTSNE_EDEVICE = 0, -1, -2, -3, -4
+BHTSNE_EINPUT, BHTSNE_ECAPACITY = -5, -6
 PHASES = ("bbox_morton", "sort", "tree", "repulsive", "attractive", "update")
 
 
@@ -79,6 +80,9 @@ def load_library():
         "bhtsne_z_exact": (C.c_int, [vp, i64, C.POINTER(C.c_double), vp, C.c_size_t, vp]),
         "bhtsne_kl": (C.c_int, [vp, C.POINTER(_Csr), C.c_double, C.POINTER(C.c_double), vp, C.c_size_t, vp]),
         "bhtsne_timing_read": (C.c_int, [C.POINTER(_Timing), C.c_int]),
+        "bhtsne_affinities_workspace_size": (C.c_size_t, [i64, C.c_int32]),
+        "bhtsne_affinities": (C.c_int, [vp, vp, i64, C.c_int32, C.c_double, vp, vp, vp, i64,
+                                        C.POINTER(C.c_int64), vp, vp, C.c_size_t, vp]),
         "bhtsne_debug_sort": (C.c_int, [vp, i64, vp, vp, vp, f64p, vp, C.c_size_t, vp]),
         "bhtsne_debug_tree": (C.c_int, [vp, i64, f32, C.POINTER(C.c_int64), vp, vp, vp, vp, vp, vp, vp,
                                         C.c_size_t, vp]),
@@ -226,6 +230,44 @@ def kl(Y: torch.Tensor, P: "Csr", Z: float, workspace: Optional[torch.Tensor] = 
     _check(lib.bhtsne_kl(_ptr(Y, torch.float32, "Y"), P.struct, float(Z), C.byref(out),
                          _ptr(ws, None, "workspace"), ws.numel(), _stream()), "bhtsne_kl")
     return out.value
+
+
+def affinities_workspace_size(n: int, k: int) -> int:
+    return int(load_library().bhtsne_affinities_workspace_size(int(n), int(k)))
+
+
+def affinities(knn_idx: torch.Tensor, knn_dist: torch.Tensor, perplexity: float,
+               workspace: Optional[torch.Tensor] = None, capacity: Optional[int] = None,
+               sigma2: bool = False):
+    """bhtsne_affinities: the symmetric P of k-nearest-neighbour lists
+    (knn_idx int32 [n, k], knn_dist float32 [n, k]) at the given perplexity.
+    Returns (Csr, sigma^2 fp64 [n] or None).  Output arrays hold `capacity`
+    entries (default 2 n k, the most P can have) and are trimmed to nnz."""
+    lib = load_library()
+    n, k = int(knn_idx.shape[0]), int(knn_idx.shape[1])
+    if tuple(knn_dist.shape) != (n, k):
+        raise ValueError("knn_idx and knn_dist must have the same shape")
+    need = affinities_workspace_size(n, k)
+    if need == 0:
+        raise BhtsneError(BHTSNE_EINVAL, "bhtsne_affinities_workspace_size")
+    ws = workspace if workspace is not None else torch.empty(need, dtype=torch.uint8, device=knn_idx.device)
+    cap = 2 * n * k if capacity is None else int(capacity)
+    dev = knn_idx.device
+    row_ptr = torch.empty(n + 1, dtype=torch.int64, device=dev)
+    col = torch.empty(max(cap, 1), dtype=torch.int32, device=dev)
+    val = torch.empty(max(cap, 1), dtype=torch.float32, device=dev)
+    s2 = torch.empty(n, dtype=torch.float64, device=dev) if sigma2 else None
+    nnz = C.c_int64(0)
+    rc = lib.bhtsne_affinities(_ptr(knn_idx, torch.int32, "knn_idx"), _ptr(knn_dist, torch.float32, "knn_dist"),
+                               n, k, float(perplexity), _ptr(row_ptr, torch.int64, "row_ptr"),
+                               _ptr(col, torch.int32, "col"), _ptr(val, torch.float32, "val"), cap,
+                               C.byref(nnz), _ptr(s2, torch.float64, "sigma2"), _ptr(ws, None, "workspace"),
+                               ws.numel(), _stream())
+    if rc == BHTSNE_ECAPACITY:
+        raise BhtsneError(rc, f"bhtsne_affinities (needs {nnz.value} entries)")
+    _check(rc, "bhtsne_affinities")
+    m = nnz.value
+    return Csr(row_ptr, col[:m], val[:m]), s2
 
 
 def step(Y: torch.Tensor, P, theta: float, exaggeration: float, learning_rate: float,

@@ -19,7 +19,7 @@ BUILD_DIR = os.path.join(ROOT, "_build")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["k_sort.hip", "k_tree.hip", "k_forces.hip", "k_layout.hip", "k_eval.hip", "api.cpp"]
+SOURCES = ["k_sort.hip", "k_tree.hip", "k_forces.hip", "k_layout.hip", "k_eval.hip", "k_affinity.hip", "api.cpp"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", CSRC, "-I", INCLUDE,
           "-Wall", "-Wno-unused-function",

@@ -476,6 +476,44 @@ int bhtsne_get_stats(const void *workspace, bhtsne_stats *out, hipStream_t strea
     return flags_status(h.flags);
 }
 
+size_t bhtsne_affinities_workspace_size(int64_t n, int32_t k)
+{
+    if (n < 2 || n > kMaxPoints || k < 1 || k > kAffMaxK || int64_t(k) >= n) return 0;
+    return make_aff_layout(n, k).total;
+}
+
+int bhtsne_affinities(const int32_t *knn_idx, const float *knn_dist, int64_t n, int32_t k, double perplexity,
+                      int64_t *row_ptr, int32_t *col, float *val, int64_t capacity, int64_t *nnz, double *sigma2,
+                      void *workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    if (!knn_idx || !knn_dist || !row_ptr || !nnz || capacity < 0) return BHTSNE_EINVAL;
+    if (capacity > 0 && (!col || !val)) return BHTSNE_EINVAL;
+    if (!std::isfinite(perplexity) || !(perplexity > 0.0)) return BHTSNE_EINVAL;
+    const size_t need = bhtsne_affinities_workspace_size(n, k);
+    if (need == 0) return BHTSNE_EINVAL;
+    if (!workspace || !aligned(workspace) || workspace_bytes < need) return BHTSNE_EWORKSPACE;
+    const AffLayout A = make_aff_layout(n, k);
+    launch_aff_front(knn_idx, knn_dist, n, k, perplexity, row_ptr, sigma2, workspace, A, stream);
+    if (hipGetLastError() != hipSuccess) return BHTSNE_EDEVICE;
+    Header h;
+    int64_t total = 0;
+    if (hipMemcpyAsync(&total, row_ptr + n, sizeof(total), hipMemcpyDeviceToHost, stream) != hipSuccess)
+        return BHTSNE_EDEVICE;
+    int rc = read_header(static_cast<char *>(workspace) + A.header, &h, stream);
+    if (rc != BHTSNE_OK) return rc;
+    if (h.flags & kErrNonFinite) return BHTSNE_ENONFINITE;
+    if (h.flags & kErrRange) return BHTSNE_EINPUT;
+    if (h.flags) return BHTSNE_EDEVICE;
+    *nnz = total;
+    if (total > capacity) return BHTSNE_ECAPACITY;
+    launch_aff_back(n, k, row_ptr, col, val, workspace, A, stream);
+    if (hipGetLastError() != hipSuccess) return BHTSNE_EDEVICE;
+    rc = read_header(static_cast<char *>(workspace) + A.header, &h, stream);
+    if (rc != BHTSNE_OK) return rc;
+    if (h.flags & kErrRange) return BHTSNE_EINPUT;
+    return h.flags ? BHTSNE_EDEVICE : BHTSNE_OK;
+}
+
 const char *bhtsne_status_string(int status)
 {
     switch (status) {
@@ -484,6 +522,8 @@ const char *bhtsne_status_string(int status)
     case BHTSNE_EWORKSPACE: return "workspace missing, misaligned or too small";
     case BHTSNE_ENONFINITE: return "non-finite coordinate in Y";
     case BHTSNE_EDEVICE: return "HIP error or device-side consistency failure";
+    case BHTSNE_EINPUT: return "invalid neighbour lists (index out of range, repeated or the point itself) or a row over the size limit";
+    case BHTSNE_ECAPACITY: return "output arrays too small (the required entry count is returned)";
     default: return "unknown status";
     }
 }

@@ -92,4 +92,12 @@ void launch_attract_layout(const LayoutView &lv, int64_t n, int64_t nnz, int til
 void launch_update(const LayoutView &lv, int64_t n, const StepArgs &a, float *Y, float *upd, float *gains,
                    float *grad, void *ws, const Layout &L, hipStream_t st);
 
+// input similarities from neighbour lists: search, own-row sort, pairs and
+// row pointers (row_ptr[n] = nnz); then, once the caller's arrays are known to
+// hold nnz entries, fill and the row sorts
+void launch_aff_front(const int32_t *idx, const float *dist, int64_t n, int k, double perplexity,
+                      int64_t *row_ptr, double *sigma2, void *ws, const AffLayout &A, hipStream_t st);
+void launch_aff_back(int64_t n, int k, const int64_t *row_ptr, int32_t *col, float *val, void *ws,
+                     const AffLayout &A, hipStream_t st);
+
 } // namespace bht

@@ -52,7 +52,7 @@ def test_workspace_size():
 
 def test_status_strings():
     for s in (bh.BHTSNE_OK, bh.BHTSNE_EINVAL, bh.BHTSNE_EWORKSPACE, bh.BHTSNE_ENONFINITE,
-              bh.BHTSNE_EDEVICE):
+              bh.BHTSNE_EDEVICE, bh.BHTSNE_EINPUT, bh.BHTSNE_ECAPACITY):
         assert bh.status_string(s) and bh.status_string(s) != "unknown status"
     assert bh.status_string(12345) == "unknown status"
 
@@ -172,3 +172,41 @@ def test_binding_refuses_cpu_tensors():
     with pytest.raises(ValueError):
         bh.Csr(torch.zeros(3, dtype=torch.int64), torch.zeros(2, dtype=torch.int32),
                torch.zeros(2, dtype=torch.float32))
+
+
+def test_affinities_workspace_size():
+    ws = bh.affinities_workspace_size
+    assert ws(1, 1) == 0 and ws(10, 0) == 0 and ws(10, 10) == 0  # k < n, k >= 1
+    assert ws(1000, 257) == 0 and ws(1000, 256) > 0             # at most 256 neighbours
+    assert ws(1 << 24, 90) == 0 and ws((1 << 24) - 1, 90) > 0
+    a, b = ws(1000, 30), ws(1000, 60)
+    assert 0 < a < b and a % 256 == 0
+    # p (8 B), columns (4 B) and partner positions (2 B) per neighbour
+    assert 14 * 1_300_000 * 90 < ws(1_300_000, 90) < 16 * 1_300_000 * 90
+
+
+def test_affinities_rejects_bad_arguments():
+    lib = bh.load_library()
+    nnz = C.c_int64(-1)
+    f = C.c_void_p(FAKE)
+    ws = C.c_void_p(FAKE)
+    big = 1 << 40
+
+    def call(idx=f, dist=f, n=100, k=10, u=5.0, rp=f, col=f, val=f, cap=2000, out=True, w=ws, wb=big):
+        return lib.bhtsne_affinities(idx, dist, n, k, u, rp, col, val, cap, C.byref(nnz) if out else None, None,
+                                     w, wb, None)
+
+    assert call(idx=None) == bh.BHTSNE_EINVAL
+    assert call(dist=None) == bh.BHTSNE_EINVAL
+    assert call(rp=None) == bh.BHTSNE_EINVAL
+    assert call(out=False) == bh.BHTSNE_EINVAL
+    assert call(cap=-1) == bh.BHTSNE_EINVAL
+    assert call(col=None) == bh.BHTSNE_EINVAL
+    for u in (0.0, -1.0, float("nan"), float("inf")):
+        assert call(u=u) == bh.BHTSNE_EINVAL
+    assert call(k=0) == bh.BHTSNE_EINVAL and call(k=257, n=1000) == bh.BHTSNE_EINVAL
+    assert call(k=100, n=100) == bh.BHTSNE_EINVAL and call(n=1) == bh.BHTSNE_EINVAL
+    assert call(w=None) == bh.BHTSNE_EWORKSPACE
+    assert call(w=C.c_void_p(FAKE + 8)) == bh.BHTSNE_EWORKSPACE
+    assert call(wb=lib.bhtsne_affinities_workspace_size(100, 10) - 1) == bh.BHTSNE_EWORKSPACE
+    assert nnz.value == -1  # nothing reached the device

@@ -1,0 +1,187 @@
+"""Parity of bhtsne_affinities with the fp64 similarity oracle (Background:
+the sparse approximation of p_{j|i} and p_ij = (p_{j|i} + p_{i|j}) / 2N;
+Binary Search Perplexity).
+
+Both sides run the bisection of sigma_i^2 to machine precision in fp64, so
+sigma_i^2 agrees to 1e-12 relative; the pattern of P (row pointers and
+sorted columns) must be identical, and each fp32 value within one unit in the
+last place of the oracle's fp64 value rounded to fp32 (the two fp64 sums
+round separately).
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2212_11506_amd as bh
+import synth
+from oracle import affinities as A
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def _gpu(idx, dist, u, **kw):
+    ti = torch.from_numpy(np.ascontiguousarray(idx, np.int32)).to(DEV)
+    td = torch.from_numpy(np.ascontiguousarray(dist, np.float32)).to(DEV)
+    P, s2 = bh.affinities(ti, td, u, sigma2=True, **kw)
+    return (P.row_ptr.cpu().numpy(), P.col.cpu().numpy(), P.val.cpu().numpy(), s2.cpu().numpy())
+
+
+def _ulps(a32, b64):
+    b32 = b64.astype(np.float32)
+    return np.abs(a32.view(np.int32).astype(np.int64) - b32.view(np.int32).astype(np.int64))
+
+
+def _compare(idx, dist, u, tag):
+    rp, col, val, s2 = _gpu(idx, dist, u)
+    orp, ocol, oval, os2 = A.affinities(idx, dist, u)
+    fin = np.isfinite(os2)
+    assert np.array_equal(np.isfinite(s2), fin)
+    rel = np.abs(s2[fin] - os2[fin]) / os2[fin]
+    assert rel.max() <= 1e-12, rel.max()
+    assert np.array_equal(rp, orp), tag
+    assert np.array_equal(col, ocol), tag
+    u_ = _ulps(val, oval)
+    say(f"[aff] {tag}: nnz {rp[-1]}, sigma2 rel {rel.max():.1e}, values off by 1 ulp: {(u_ == 1).sum()}")
+    assert u_.max() <= 1
+    return rp, col, val
+
+
+def _random_knn(n, k, seed, hub=None, hub_share=0.0):
+    rng = np.random.default_rng(seed)
+    idx = np.empty((n, k), np.int32)
+    for i in range(n):
+        c = rng.choice(n - 1, size=k, replace=False)
+        idx[i] = c + (c >= i)
+    if hub is not None:  # many rows list `hub` (replacing a neighbour that is not already hub)
+        rows = np.nonzero(rng.random(n) < hub_share)[0]
+        rows = rows[rows != hub]
+        for i in rows:
+            if hub not in idx[i]:
+                idx[i, 0] = hub
+    dist = np.sort(rng.uniform(0.0, 3.0, size=(n, k)), axis=1).astype(np.float32)
+    return idx, dist
+
+
+def test_workload_0_2k():
+    kn = synth.make_knn(0)
+    rp, col, val = _compare(kn.idx, kn.dist, 30.0, "workload 0")
+    assert abs(val.astype(np.float64).sum() - 1.0) < 1e-5
+
+
+def test_workload_1_70k():
+    kn = synth.make_knn(1)
+    _compare(kn.idx, kn.dist, 30.0, "workload 1")
+
+
+@pytest.mark.parametrize("k,u", [(1, 1.0), (2, 1.5), (5, 3.0), (63, 20.0), (64, 21.0), (65, 22.0),
+                                 (128, 40.0), (200, 66.0), (256, 85.0)])
+def test_neighbour_counts(k, u):
+    idx, dist = _random_knn(700, k, seed=k)
+    _compare(idx, dist, u, f"k={k}")
+
+
+def test_degenerate_rows():
+    idx, dist = _random_knn(500, 12, seed=5)
+    dist[0] = 1.25                    # flat row
+    dist[1, :4] = dist[1, 0]          # four ties at the minimum, u below them
+    dist[2] = np.sort(dist[2] * 1e-3)  # tiny distances
+    dist[3] = np.sort(dist[3] * 1e3)   # large distances
+    _compare(idx, dist, 3.0, "ties and scales")
+    _compare(idx, dist, 13.0, "u > k: uniform rows")
+
+
+def test_long_rows():
+    # point 7 is listed by about 900 rows: its row of P goes through the
+    # block sort; the others through the wave sort
+    idx, dist = _random_knn(3000, 30, seed=9, hub=7, hub_share=0.3)
+    rp, col, val = _compare(idx, dist, 10.0, "hub row")
+    assert np.diff(rp).max() > 256
+
+
+def test_row_over_limit_is_rejected():
+    idx, dist = _random_knn(5000, 8, seed=11, hub=3, hub_share=0.9)
+    with pytest.raises(bh.BhtsneError) as e:
+        _gpu(idx, dist, 4.0)
+    assert e.value.status == bh.BHTSNE_EINPUT
+
+
+@pytest.mark.parametrize("case", ["out_of_range", "self", "repeat", "negative"])
+def test_invalid_lists_are_rejected(case):
+    idx, dist = _random_knn(300, 10, seed=2)
+    if case == "out_of_range":
+        idx[17, 3] = 300
+    elif case == "self":
+        idx[17, 3] = 17
+    elif case == "repeat":
+        idx[17, 3] = idx[17, 4]
+    else:
+        idx[17, 3] = -2
+    with pytest.raises(bh.BhtsneError) as e:
+        _gpu(idx, dist, 4.0)
+    assert e.value.status == bh.BHTSNE_EINPUT
+
+
+def test_nonfinite_distance():
+    idx, dist = _random_knn(300, 10, seed=3)
+    dist[5, 2] = np.nan
+    with pytest.raises(bh.BhtsneError) as e:
+        _gpu(idx, dist, 4.0)
+    assert e.value.status == bh.BHTSNE_ENONFINITE
+
+
+def test_capacity_reports_nnz():
+    idx, dist = _random_knn(400, 10, seed=4)
+    orp, _, _, _ = A.affinities(idx, dist, 4.0)
+    with pytest.raises(bh.BhtsneError) as e:
+        _gpu(idx, dist, 4.0, capacity=int(orp[-1]) - 1)
+    assert e.value.status == bh.BHTSNE_ECAPACITY and f"needs {orp[-1]} entries" in str(e.value)
+    rp, col, val, _ = _gpu(idx, dist, 4.0, capacity=int(orp[-1]))
+    assert rp[-1] == orp[-1]
+
+
+def test_deterministic():
+    kn = synth.make_knn(0)
+    a = _gpu(kn.idx, kn.dist, 30.0)
+    b = _gpu(kn.idx, kn.dist, 30.0)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+
+
+def test_full_size_1p3m_sampled():
+    """Workload 2 (1.3M points, k = 90): sampled rows of P against the oracle,
+    built from the conditional rows of those points and of every point that
+    lists them."""
+    kn = synth.make_knn(2, progress=say)
+    n = kn.n
+    say(f"[aff] workload 2: n={n}, lists drawn in {kn.gen_seconds:.0f}s")
+    rp, col, val, s2 = _gpu(kn.idx, kn.dist, 30.0)
+    assert abs(val.astype(np.float64).sum() - 1.0) < 1e-4
+    rng = np.random.default_rng(12)
+    rows = np.sort(rng.choice(n, 400, replace=False))
+    rr, ee = np.nonzero(np.isin(kn.idx, rows))  # row rr lists a sampled point at position ee
+    need = np.unique(np.concatenate([rows, rr]))
+    os2, pc = A.conditional(kn.dist[need], 30.0)
+    pos = {int(r): t for t, r in enumerate(need)}
+    rel = np.abs(s2[need] - os2) / os2
+    assert rel.max() <= 1e-12
+    expect = {int(i): {} for i in rows}
+    for i in rows:
+        for e, j in enumerate(kn.idx[i]):
+            expect[int(i)][int(j)] = pc[pos[int(i)], e]
+    for r, e in zip(rr, ee):
+        i = int(kn.idx[r, e])
+        expect[i][int(r)] = expect[i].get(int(r), 0.0) + pc[pos[int(r)], e]
+    checked = 0
+    for i in rows:
+        cols = col[rp[i]:rp[i + 1]]
+        want = expect[int(i)]
+        assert np.array_equal(cols, np.array(sorted(want), np.int32))
+        ref = np.array([want[int(j)] for j in cols]) / (2.0 * n)
+        assert _ulps(val[rp[i]:rp[i + 1]], ref).max() <= 1
+        checked += cols.size
+    say(f"[aff] workload 2: {checked} sampled entries match, sigma2 rel {rel.max():.1e}")
