@@ -48,6 +48,8 @@ def parse():
     ap.add_argument("--cpu-iters", type=int, default=16, help="oracle iterations for the CPU baseline")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-count", action="store_true", help="skip the interaction-counting replay")
+    ap.add_argument("--no-affinities", action="store_true", help="skip the input-similarity measurement")
+    ap.add_argument("--affinities-only", action="store_true", help="measure only the input similarities")
     ap.add_argument("--plain", action="store_true",
                     help="attractive step straight from the CSR arrays (no locality layout)")
     ap.add_argument("--no-overlap", action="store_true",
@@ -99,6 +101,54 @@ def measured_traffic(kernel, sources):
     return None
 
 
+def bench_affinities(args, cpu_rows=20000):
+    """bhtsne_affinities on the workload's neighbour lists (k = 90, u = 30):
+    the input similarities, computed once before the iterations.  Inputs are
+    resident on the GPU when timing starts; each call synchronises twice (it
+    returns nnz), so the time is host wall-clock per call."""
+    import numpy as np
+    import torch
+
+    import paper_2212_11506_amd as bh
+    import synth
+
+    kn = synth.make_knn(args.workload, n=args.n)
+    n, k, u = kn.n, kn.k, 30.0
+    log(f"[bench] affinities: n={n} k={k}, lists drawn in {kn.gen_seconds:.1f}s")
+    idx = torch.from_numpy(kn.idx).cuda()
+    dist = torch.from_numpy(kn.dist).cuda()
+    ws = torch.empty(bh.affinities_workspace_size(n, k), dtype=torch.uint8, device="cuda")
+    P, _ = bh.affinities(idx, dist, u, workspace=ws)  # warm-up
+    torch.cuda.synchronize()
+    calls = 5
+    t0 = time.perf_counter()
+    for _ in range(calls):
+        P, _ = bh.affinities(idx, dist, u, workspace=ws)
+    torch.cuda.synchronize()
+    ms = 1e3 * (time.perf_counter() - t0) / calls
+    nnz = P.nnz
+    out = {"workload": f"neighbour lists of workload {args.workload}: k = {k} per point within its cluster, "
+                       f"d ~ U(0, 3) sorted per row; perplexity {u}",
+           "n": n, "k": k, "perplexity": u, "nnz": nnz, "calls": calls, "ms_per_call": ms,
+           "points_per_s": n / (ms * 1e-3),
+           # bytes the step must move: the lists in (8 B per neighbour), P out
+           # (8 B per entry + 8 B per row pointer)
+           "algorithmic_gbs": (8.0 * n * k + 8.0 * nnz + 8.0 * (n + 1)) / (ms * 1e-3) / 1e9}
+    del P, ws, idx, dist
+    torch.cuda.empty_cache()
+    if not args.no_cpu and cpu_rows > 0:
+        from oracle import affinities as A
+
+        rows = np.random.default_rng(5).choice(n, min(cpu_rows, n), replace=False)
+        tc = time.perf_counter()
+        A.conditional(kn.dist[rows], u)
+        dt = time.perf_counter() - tc
+        out["cpu_oracle"] = {"value": rows.size / dt, "unit": "points/s", "kind": "oracle",
+                             "sample": f"sigma search and p_(j|i) of {rows.size} random rows (numpy fp64, "
+                                       f"{dt:.1f}s); the symmetrisation is not in this figure"}
+    return out
+
+
 def main():
     args = parse()
     if args.no_overlap:
@@ -119,6 +169,9 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     bh.load_library()
+    if args.affinities_only:
+        print(json.dumps({"affinities": bench_affinities(args)}), flush=True)
+        return
     w = synth.WORKLOADS[args.workload]
     t0 = time.time()
     inp = synth.make_inputs(args.workload, n=args.n, progress=log)
@@ -325,6 +378,7 @@ def main():
         "kernels": kernels,
         "roofline": roof,
         "cpu_baseline": cpu,
+        "affinities": None if args.no_affinities else bench_affinities(args),
     }
     print(json.dumps(out), flush=True)
 

@@ -26,7 +26,6 @@
 
 namespace bht {
 
-constexpr int kAffPer = kAffMaxK / kWave; // neighbours per lane in the search
 constexpr int kAffSearchBlock = 256;      // four rows per block
 constexpr int kAffMaxSteps = 2200;        // halvings across the whole fp64 range
 constexpr int kAffShortCap = 256;         // row sorts by one wave
@@ -69,20 +68,21 @@ __global__ void aff_clear_kernel(Header *__restrict__ hdr, uint32_t *__restrict_
     }
 }
 
+// a = d'^2 / (2 sigma^2) from the reciprocal of 2 sigma^2: a tie (d' = 0) gives
+// 0 also where the reciprocal overflows (the smallest sigma^2)
+__device__ inline double scaled(double dp, double inv) { return dp > 0.0 ? dp * inv : 0.0; }
+
 // Entropy (nats) of the Gaussian weights at sigma^2 = s2 over this lane's
 // shifted squared distances (an infinite s2 gives log k).  a e^-a is taken as
 // 0 where the weight underflows.  The result is lane 0's, in every lane.
-__device__ inline double row_entropy(const double (&dp)[kAffPer], int k, double s2)
+template <int kPer> __device__ inline double row_entropy(const double (&dp)[kPer], int k, double s2)
 {
-    // a division, not a reciprocal: 1 / (2 s2) overflows for the smallest s2,
-    // where a tie (dp = 0) must still give a = 0
-    const bool inf = isinf(s2);
-    const double den = 2.0 * s2;
+    const double inv = isinf(s2) ? 0.0 : 1.0 / (2.0 * s2);
     double s = 0.0, t = 0.0;
 #pragma unroll
-    for (int q = 0; q < kAffPer; ++q) {
-        if (q * kWave + lane_id() < k) {
-            const double a = inf ? 0.0 : dp[q] / den;
+    for (int q = 0; q < kPer; ++q) {
+        if (q < kPer - 1 || (kPer - 1) * kWave + lane_id() < k) {
+            const double a = scaled(dp[q], inv);
             const double w = exp(-a);
             s += w;
             t += w > 0.0 ? a * w : 0.0;
@@ -93,7 +93,9 @@ __device__ inline double row_entropy(const double (&dp)[kAffPer], int k, double 
     return log(s) + t / s;
 }
 
-// 1. the search; writes p_{j|i} in the neighbour order and sigma_i^2
+// 1. the search; writes p_{j|i} in the neighbour order and sigma_i^2.  kPer
+// = ceil(k / 64) distances per lane.
+template <int kPer>
 __global__ __launch_bounds__(kAffSearchBlock) void aff_search_kernel(const float *__restrict__ dist, int64_t n, int k,
                                                                      double log_u, double *__restrict__ p,
                                                                      double *__restrict__ sigma2,
@@ -102,11 +104,11 @@ __global__ __launch_bounds__(kAffSearchBlock) void aff_search_kernel(const float
     const int64_t i = int64_t(blockIdx.x) * (kAffSearchBlock / kWave) + threadIdx.x / kWave;
     if (i >= n) return; // whole waves
     const int lane = lane_id();
-    double dp[kAffPer];
+    double dp[kPer];
     double mn = INFINITY, mx = 0.0;
     bool bad = false;
 #pragma unroll
-    for (int q = 0; q < kAffPer; ++q) {
+    for (int q = 0; q < kPer; ++q) {
         const int e = q * kWave + lane;
         dp[q] = 0.0;
         if (e < k) {
@@ -120,7 +122,7 @@ __global__ __launch_bounds__(kAffSearchBlock) void aff_search_kernel(const float
     if (ballot(bad) && lane == 0) atomicOr(&hdr->flags, kErrNonFinite);
     mn = uniform_d(wave_min_d(mn));
 #pragma unroll
-    for (int q = 0; q < kAffPer; ++q) {
+    for (int q = 0; q < kPer; ++q) {
         dp[q] = q * kWave + lane < k ? dp[q] - mn : 0.0;
         mx = fmax(mx, dp[q]);
     }
@@ -128,12 +130,12 @@ __global__ __launch_bounds__(kAffSearchBlock) void aff_search_kernel(const float
     double lo = 0.0, hi = mx > 0.0 ? mx : 1.0;
     if (mx > 0.0) {
         // grow the top of the interval until the perplexity there reaches u
-        while (!isinf(hi) && row_entropy(dp, k, hi) < log_u) hi *= 2.0;
+        while (!isinf(hi) && row_entropy<kPer>(dp, k, hi) < log_u) hi *= 2.0;
         if (!isinf(hi)) {
             for (int s = 0; s < kAffMaxSteps; ++s) {
                 const double mid = 0.5 * (lo + hi);
                 if (mid <= lo || mid >= hi) break;
-                if (row_entropy(dp, k, mid) < log_u)
+                if (row_entropy<kPer>(dp, k, mid) < log_u)
                     lo = mid;
                 else
                     hi = mid;
@@ -141,20 +143,19 @@ __global__ __launch_bounds__(kAffSearchBlock) void aff_search_kernel(const float
         }
     }
     // p_{j|i} at sigma^2 = hi
-    const bool inf = isinf(hi);
-    const double den = 2.0 * hi;
-    double w[kAffPer], s = 0.0;
+    const double inv = isinf(hi) ? 0.0 : 1.0 / (2.0 * hi);
+    double w[kPer], s = 0.0;
 #pragma unroll
-    for (int q = 0; q < kAffPer; ++q) {
+    for (int q = 0; q < kPer; ++q) {
         w[q] = 0.0;
         if (q * kWave + lane < k) {
-            w[q] = exp(-(inf ? 0.0 : dp[q] / den));
+            w[q] = exp(-scaled(dp[q], inv));
             s += w[q];
         }
     }
     s = uniform_d(wave_sum(s));
 #pragma unroll
-    for (int q = 0; q < kAffPer; ++q) {
+    for (int q = 0; q < kPer; ++q) {
         const int e = q * kWave + lane;
         if (e < k) p[i * k + e] = w[q] / s;
     }
@@ -421,8 +422,15 @@ void launch_aff_front(const int32_t *idx, const float *dist, int64_t n, int k, d
     double *sp = at<double>(ws, A.sp);
     int32_t *scol = at<int32_t>(ws, A.scol);
     aff_clear_kernel<<<unsigned((n + 255) / 256), 256, 0, st>>>(hdr, extra, fill, counters, n);
-    aff_search_kernel<<<unsigned((n + 3) / 4), kAffSearchBlock, 0, st>>>(dist, n, k, log(perplexity), sp, sigma2,
-                                                                         hdr);
+    const unsigned sb = unsigned((n + 3) / 4);
+    const double lu = log(perplexity);
+    switch ((k + kWave - 1) / kWave) {
+    case 1: aff_search_kernel<1><<<sb, kAffSearchBlock, 0, st>>>(dist, n, k, lu, sp, sigma2, hdr); break;
+    case 2: aff_search_kernel<2><<<sb, kAffSearchBlock, 0, st>>>(dist, n, k, lu, sp, sigma2, hdr); break;
+    case 3: aff_search_kernel<3><<<sb, kAffSearchBlock, 0, st>>>(dist, n, k, lu, sp, sigma2, hdr); break;
+    default: aff_search_kernel<4><<<sb, kAffSearchBlock, 0, st>>>(dist, n, k, lu, sp, sigma2, hdr); break;
+    }
+    static_assert(kAffMaxK <= 4 * kWave, "four distances per lane at most");
     aff_own_sort_kernel<<<unsigned(n), kWave, 0, st>>>(idx, n, k, scol, sp, hdr);
     const int64_t entries = n * k;
     aff_pairs_kernel<<<unsigned((entries + 255) / 256), 256, 0, st>>>(scol, n, k, at<int16_t>(ws, A.mpos), extra);
