@@ -148,41 +148,6 @@ inline Layout make_layout(int64_t n, int64_t nnz)
     return L;
 }
 
-// ---------------------------------------------------------------- similarities
-constexpr int kAffMaxK = 256;      // neighbours per point, at most
-constexpr int kAffLongCap = 4096;  // entries of one row of the symmetric P, at most
-constexpr int kAffScanTileRows = 1024;
-
-struct AffLayout {
-    int64_t n, k, scan_tiles;
-    size_t header, sp, scol, mpos, extra, fill, part, longrows, counters, total;
-};
-
-inline AffLayout make_aff_layout(int64_t n, int64_t k)
-{
-    AffLayout A{};
-    A.n = n;
-    A.k = k;
-    A.scan_tiles = (n + kAffScanTileRows - 1) / kAffScanTileRows;
-    size_t off = 0;
-    auto take = [&](size_t bytes) {
-        size_t o = off;
-        off = align_up(off + bytes, 256);
-        return o;
-    };
-    A.header = take(sizeof(Header));
-    A.sp = take(8 * size_t(n) * size_t(k));   // p_{j|i}, then in column order
-    A.scol = take(4 * size_t(n) * size_t(k)); // neighbours in column order
-    A.mpos = take(2 * size_t(n) * size_t(k)); // partner position in the other row, or -1
-    A.extra = take(4 * size_t(n));
-    A.fill = take(4 * size_t(n));
-    A.part = take(8 * size_t(A.scan_tiles + 1));
-    A.longrows = take(4 * size_t(n));
-    A.counters = take(16);
-    A.total = off;
-    return A;
-}
-
 template <typename T> __host__ __device__ inline T *at(void *ws, size_t off)
 {
     return reinterpret_cast<T *>(static_cast<char *>(ws) + off);

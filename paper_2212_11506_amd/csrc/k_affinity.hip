@@ -162,6 +162,93 @@ __global__ __launch_bounds__(kAffSearchBlock) void aff_search_kernel(const float
     if (sigma2 && lane == 0) sigma2[i] = hi;
 }
 
+// 1'. the search with one point per lane (k <= kAffLaneMaxK).  The distances
+// are first transposed (dT[e n + i]) so that the lanes of a wave read
+// neighbour e of their 64 points as one contiguous 256-byte load; each lane
+// then runs its own bisection with sums over its own row and no cross-lane
+// work.  Same steps and readings as the wave kernel; d^2 - min d^2 is one
+// fp64 fma, exact up to its single rounding (the square of an fp32 value is
+// exact in fp64).
+constexpr int kAffTransRows = 64;
+
+__global__ __launch_bounds__(256) void aff_transpose_kernel(const float *__restrict__ dist, int64_t n, int k,
+                                                            float *__restrict__ dT)
+{
+    __shared__ float tile[kAffTransRows][kAffLaneMaxK + 1];
+    const int64_t r0 = int64_t(blockIdx.x) * kAffTransRows;
+    const int rows = int(n - r0 < kAffTransRows ? n - r0 : kAffTransRows);
+    for (int x = threadIdx.x; x < rows * k; x += blockDim.x) tile[x / k][x % k] = dist[r0 * k + x];
+    __syncthreads();
+    for (int x = threadIdx.x; x < kAffTransRows * k; x += blockDim.x) {
+        const int e = x / kAffTransRows, r = x % kAffTransRows;
+        if (r < rows) dT[int64_t(e) * n + r0 + r] = tile[r][e];
+    }
+}
+
+__global__ __launch_bounds__(256) void aff_search_lane_kernel(const float *__restrict__ dT, int64_t n, int k,
+                                                              double log_u, double *__restrict__ p,
+                                                              double *__restrict__ sigma2, Header *__restrict__ hdr)
+{
+    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const float *col = dT + i;
+    double mn = INFINITY;
+    bool bad = false;
+    for (int e = 0; e < k; ++e) {
+        const float x = col[int64_t(e) * n];
+        if (!(x >= 0.0f) || isinf(x)) bad = true; // NaN, negative or infinite
+        mn = fmin(mn, double(x) * double(x));
+    }
+    if (bad) {
+        atomicOr(&hdr->flags, kErrNonFinite);
+        return;
+    }
+    double mx = 0.0;
+    for (int e = 0; e < k; ++e) {
+        const double x = col[int64_t(e) * n];
+        mx = fmax(mx, fma(x, x, -mn));
+    }
+    // entropy (nats) at sigma^2 = s2 over this lane's row
+    auto entropy = [&](double s2) {
+        const double inv = isinf(s2) ? 0.0 : 1.0 / (2.0 * s2);
+        double sw = 0.0, tw = 0.0;
+#pragma unroll 4
+        for (int e = 0; e < k; ++e) {
+            const double x = col[int64_t(e) * n];
+            const double a = scaled(fma(x, x, -mn), inv);
+            const double w = exp(-a);
+            sw += w;
+            tw += w > 0.0 ? a * w : 0.0;
+        }
+        return log(sw) + tw / sw;
+    };
+    double lo = 0.0, hi = mx > 0.0 ? mx : 1.0;
+    if (mx > 0.0) {
+        while (!isinf(hi) && entropy(hi) < log_u) hi *= 2.0;
+        if (!isinf(hi)) {
+            for (int s = 0; s < kAffMaxSteps; ++s) {
+                const double mid = 0.5 * (lo + hi);
+                if (mid <= lo || mid >= hi) break;
+                if (entropy(mid) < log_u)
+                    lo = mid;
+                else
+                    hi = mid;
+            }
+        }
+    }
+    const double inv = isinf(hi) ? 0.0 : 1.0 / (2.0 * hi);
+    double sw = 0.0;
+    for (int e = 0; e < k; ++e) {
+        const double x = col[int64_t(e) * n];
+        sw += exp(-scaled(fma(x, x, -mn), inv));
+    }
+    for (int e = 0; e < k; ++e) {
+        const double x = col[int64_t(e) * n];
+        p[i * k + e] = exp(-scaled(fma(x, x, -mn), inv)) / sw;
+    }
+    if (sigma2) sigma2[i] = hi;
+}
+
 // Ascending sort of len (key, value) pairs held in LDS by the block, padded
 // with all-ones keys to the next power of two (the arrays hold that many).
 __device__ inline void lds_bitonic(uint32_t *key, uint32_t *val, int len)
@@ -424,7 +511,12 @@ void launch_aff_front(const int32_t *idx, const float *dist, int64_t n, int k, d
     aff_clear_kernel<<<unsigned((n + 255) / 256), 256, 0, st>>>(hdr, extra, fill, counters, n);
     const unsigned sb = unsigned((n + 3) / 4);
     const double lu = log(perplexity);
-    switch ((k + kWave - 1) / kWave) {
+    if (k <= kAffLaneMaxK) {
+        float *dT = at<float>(ws, A.dT);
+        aff_transpose_kernel<<<unsigned((n + kAffTransRows - 1) / kAffTransRows), 256, 0, st>>>(dist, n, k, dT);
+        aff_search_lane_kernel<<<unsigned((n + 255) / 256), 256, 0, st>>>(dT, n, k, lu, sp, sigma2, hdr);
+    }
+    else switch ((k + kWave - 1) / kWave) {
     case 1: aff_search_kernel<1><<<sb, kAffSearchBlock, 0, st>>>(dist, n, k, lu, sp, sigma2, hdr); break;
     case 2: aff_search_kernel<2><<<sb, kAffSearchBlock, 0, st>>>(dist, n, k, lu, sp, sigma2, hdr); break;
     case 3: aff_search_kernel<3><<<sb, kAffSearchBlock, 0, st>>>(dist, n, k, lu, sp, sigma2, hdr); break;

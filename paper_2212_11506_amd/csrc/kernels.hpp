@@ -2,6 +2,7 @@
 #pragma once
 
 #include "common.hpp"
+#include "affinity.hpp"
 
 namespace bht {
 
