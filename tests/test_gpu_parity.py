@@ -210,11 +210,17 @@ def test_gradient_parity(case, theta):
     assert abs(Z - Zo) <= 1e-5 * Zo, (Z, Zo)
 
 
-@pytest.mark.parametrize("theta", [0.2, 0.8])
-def test_gradient_parity_other_angles(theta):
-    y = _case("late")
+# 0.7 is the largest angle at which the walk drops the comparison with a
+# point's own leaf (theta^2 <= 0.49: no point can accept a cell containing it,
+# so each takes its own leaf once and its weight of 1 is removed afterwards);
+# 0.71 and above compare positions instead.  "reps40" puts every point in a
+# bucket of 40 identical points, so the own leaf sits among equal neighbours.
+@pytest.mark.parametrize("case,theta", [("late", 0.2), ("late", 0.7), ("late", 0.71), ("late", 0.8), ("late", 1.2),
+                                        ("reps40", 0.7), ("reps40", 0.71), ("dups", 1.0)])
+def test_gradient_parity_other_angles(case, theta):
+    y = _case(case)
     rp, col, val = _p_for(y, seed=5)
-    say(f"[grad-angle] theta={theta}")
+    say(f"[grad-angle] case={case} theta={theta}")
     ws = torch.empty(bh.workspace_size(y.shape[0], col.size), dtype=torch.uint8, device="cuda")
     g, Z = bh.gradient(dev_y(y), dev_p(rp, col, val), theta, 1.0, workspace=ws)
     stats = bh.get_stats(ws)
