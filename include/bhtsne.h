@@ -275,13 +275,13 @@ int bhtsne_debug_tree(const float *Y, int64_t n, float theta, int64_t *n_nodes, 
  *           when the call fails with BHTSNE_ECAPACITY, so the caller can size
  *           col and val and call again.
  * sigma2    [n] fp64, device, nullable: sigma_i^2.
- * Limits: 1 <= k <= 256, k < n <= 16777215; a row of P holds at most 4096
- * entries (k plus the number of points that list i and that i does not list).
+ * Limits: 1 <= k <= 256, k < n <= 16777215; at most 4096 points may list
+ * the same point.
  * The call synchronises `stream` twice (to learn nnz, then to report).
  * Errors: BHTSNE_EINVAL (arguments), BHTSNE_EWORKSPACE, BHTSNE_ENONFINITE (a
  * NaN, infinite or negative distance), BHTSNE_EINPUT (a neighbour index out of
- * range, equal to its row or repeated within a row, or a row over 4096
- * entries; col and val then hold no usable result), BHTSNE_ECAPACITY,
+ * range, equal to its row or repeated within a row, or a point listed by
+ * more than 4096 others; col and val then hold no usable result), BHTSNE_ECAPACITY,
  * BHTSNE_EDEVICE.  The library allocates nothing. */
 size_t bhtsne_affinities_workspace_size(int64_t n, int32_t k);
 int bhtsne_affinities(const int32_t *knn_idx, const float *knn_dist, int64_t n, int32_t k, double perplexity,

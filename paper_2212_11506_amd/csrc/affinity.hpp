@@ -11,7 +11,7 @@ constexpr int kAffLaneMaxK = 128;  // up to this many neighbours, one point per 
 
 struct AffLayout {
     int64_t n, k, scan_tiles;
-    size_t header, sp, scol, mpos, extra, fill, part, longrows, counters, dT, total;
+    size_t header, sp, scol, indeg, cursor, ib, in_col, in_p, inonly, part, longrows, counters, dT, total;
 };
 
 inline AffLayout make_aff_layout(int64_t n, int64_t k)
@@ -27,11 +27,14 @@ inline AffLayout make_aff_layout(int64_t n, int64_t k)
         return o;
     };
     A.header = take(sizeof(Header));
-    A.sp = take(8 * size_t(n) * size_t(k));   // p_{j|i}, then in column order
-    A.scol = take(4 * size_t(n) * size_t(k)); // neighbours in column order
-    A.mpos = take(2 * size_t(n) * size_t(k)); // partner position in the other row, or -1
-    A.extra = take(4 * size_t(n));
-    A.fill = take(4 * size_t(n));
+    A.sp = take(8 * size_t(n) * size_t(k));      // p_{j|i}, then in column order
+    A.scol = take(4 * size_t(n) * size_t(k));    // neighbours in column order
+    A.indeg = take(4 * size_t(n));               // entries of each point's inbox
+    A.cursor = take(4 * size_t(n));
+    A.ib = take(8 * size_t(n + 1));              // inbox offsets
+    A.in_col = take(4 * size_t(n) * size_t(k));  // inboxes: listing point, p
+    A.in_p = take(8 * size_t(n) * size_t(k));
+    A.inonly = take(4 * size_t(n));              // inbox entries not in the own list
     A.part = take(8 * size_t(A.scan_tiles + 1));
     A.longrows = take(4 * size_t(n));
     A.counters = take(16);

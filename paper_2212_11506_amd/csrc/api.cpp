@@ -522,7 +522,7 @@ const char *bhtsne_status_string(int status)
     case BHTSNE_EWORKSPACE: return "workspace missing, misaligned or too small";
     case BHTSNE_ENONFINITE: return "non-finite coordinate in Y";
     case BHTSNE_EDEVICE: return "HIP error or device-side consistency failure";
-    case BHTSNE_EINPUT: return "invalid neighbour lists (index out of range, repeated or the point itself) or a row over the size limit";
+    case BHTSNE_EINPUT: return "invalid neighbour lists (index out of range, repeated or the point itself) or a point listed by more than 4096 others";
     case BHTSNE_ECAPACITY: return "output arrays too small (the required entry count is returned)";
     default: return "unknown status";
     }

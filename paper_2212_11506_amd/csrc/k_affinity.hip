@@ -8,19 +8,19 @@
 // current interval each step) until the perplexity exp(H) of p_{.|i} equals u.
 //
 // GPU design, one call:
-//   1. search: one wave per row, the k squared distances spread over the
-//      lanes in fp64; every step is two wave sums (sum w, sum a w).  The
+//   1. search: for k <= 128 one point per lane over a transposed copy of the
+//      distances (one coalesced load per neighbour for the wave's 64 points);
+//      for larger k one wave per point with two wave sums per step.  The
 //      search runs to machine precision: it stops when the midpoint equals an
 //      end of the interval and keeps the upper end;
 //   2. own rows: each row's neighbours sorted by column in LDS, carrying p;
-//   3. pairs: for every entry (i, j) a binary search of i in row j marks the
-//      pair mutual (both rows hold it) or counts a reverse entry for row j;
-//   4. row pointers: an exclusive scan of k + reverse entries per row;
-//   5. fill: each row's own entries first, in column order, with the mutual
-//      partner's p added; the reverse entries go to slots taken with an
-//      atomic counter per row;
-//   6. a final sort of every output row by column makes the result canonical.
-// Rows whose union holds more than kAffLongCap entries are rejected.
+//   3. inboxes: every entry (i, j) is scattered into row j's inbox (column i,
+//      p_{j|i}) at offsets from a scan of the in-degrees;
+//   4. per row: the inbox sorted in LDS, the own entries found in it counted
+//      (P's row holds k plus the inbox-only entries), row pointers scanned;
+//   5. per row: the union of the own list and the inbox written in column
+//      order, a pair in both lists once with the sum of its two p.
+// At most kAffLongCap points may list the same point.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -28,7 +28,7 @@ namespace bht {
 
 constexpr int kAffSearchBlock = 256;      // four rows per block
 constexpr int kAffMaxSteps = 2200;        // halvings across the whole fp64 range
-constexpr int kAffShortCap = 256;         // row sorts by one wave
+constexpr int kAffShortCap = 256;         // inboxes handled by one wave
 constexpr int kAffLongThreads = 256;
 
 // every lane takes lane 0's value, so branches on it stay wave-uniform
@@ -54,13 +54,13 @@ __device__ inline double wave_max_d(double v)
     return v;
 }
 
-__global__ void aff_clear_kernel(Header *__restrict__ hdr, uint32_t *__restrict__ extra, uint32_t *__restrict__ fill,
-                                 uint32_t *__restrict__ counters, int64_t n)
+__global__ void aff_clear_kernel(Header *__restrict__ hdr, uint32_t *__restrict__ indeg,
+                                 uint32_t *__restrict__ cursor, uint32_t *__restrict__ counters, int64_t n)
 {
     const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
     if (i < n) {
-        extra[i] = 0;
-        fill[i] = 0;
+        indeg[i] = 0;
+        cursor[i] = 0;
     }
     if (i == 0) {
         hdr->flags = 0;
@@ -306,37 +306,19 @@ __global__ __launch_bounds__(kWave) void aff_own_sort_kernel(const int32_t *__re
     if (ballot(bad) && threadIdx.x == 0) atomicOr(&hdr->flags, kErrRange);
 }
 
-// 3. mutual pairs and reverse counts; mpos holds the partner's position in
-// row j, or -1
-__global__ __launch_bounds__(256) void aff_pairs_kernel(const int32_t *__restrict__ scol, int64_t n, int k,
-                                                        int16_t *__restrict__ mpos, uint32_t *__restrict__ extra)
+// 3. inboxes: an entry (i, j) of i's list is also an entry of row j of P;
+// row j's inbox collects them (column i, value p_{j|i}).  Counts first.
+__global__ __launch_bounds__(256) void aff_indeg_kernel(const int32_t *__restrict__ scol, int64_t n, int k,
+                                                        uint32_t *__restrict__ indeg)
 {
     const int64_t x = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
     if (x >= n * k) return;
     const int64_t i = x / k;
     const uint32_t j = uint32_t(scol[x]);
-    if (j >= uint32_t(n) || int64_t(j) == i) { // flagged by the sort
-        mpos[x] = -1;
-        return;
-    }
-    const int32_t *row = scol + int64_t(j) * k;
-    int a = 0, b = k; // first position in row j whose column is >= i
-    while (a < b) {
-        const int m = (a + b) >> 1;
-        if (int64_t(row[m]) < i)
-            a = m + 1;
-        else
-            b = m;
-    }
-    if (a < k && int64_t(row[a]) == i) {
-        mpos[x] = int16_t(a);
-    } else {
-        mpos[x] = -1;
-        atomicAdd(&extra[j], 1u);
-    }
+    if (j < uint32_t(n) && int64_t(j) != i) atomicAdd(&indeg[j], 1u); // others are flagged
 }
 
-// 4. row pointers: exclusive scan of k + extra over tiles of 1024 rows
+// exclusive scan of base + cnt[i] over tiles of 1024 rows, into out[0..n]
 constexpr int kAffScanBlock = 256, kAffScanItems = 4, kAffScanTile = kAffScanBlock * kAffScanItems;
 static_assert(kAffScanTile == kAffScanTileRows, "one scan tile per partial");
 
@@ -363,22 +345,22 @@ __device__ inline unsigned long long block_scan_excl(unsigned long long v, unsig
     return off + x - v;
 }
 
-__global__ __launch_bounds__(kAffScanBlock) void aff_scan_part_kernel(const uint32_t *__restrict__ extra, int64_t n,
-                                                                      int k, unsigned long long *__restrict__ part)
+__global__ __launch_bounds__(kAffScanBlock) void aff_scan_part_kernel(const uint32_t *__restrict__ cnt, int64_t n,
+                                                                      int base, unsigned long long *__restrict__ part)
 {
     __shared__ unsigned long long s_w[kAffScanBlock / kWave];
-    const int64_t base = int64_t(blockIdx.x) * kAffScanTile + int64_t(threadIdx.x) * kAffScanItems;
+    const int64_t b0 = int64_t(blockIdx.x) * kAffScanTile + int64_t(threadIdx.x) * kAffScanItems;
     unsigned long long v = 0;
 #pragma unroll
     for (int q = 0; q < kAffScanItems; ++q)
-        if (base + q < n) v += uint64_t(k) + extra[base + q];
+        if (b0 + q < n) v += uint64_t(base) + cnt[b0 + q];
     unsigned long long tot;
     block_scan_excl(v, s_w, &tot);
     if (threadIdx.x == 0) part[blockIdx.x] = tot;
 }
 
 __global__ __launch_bounds__(kAffScanBlock) void aff_scan_top_kernel(unsigned long long *__restrict__ part,
-                                                                     int64_t tiles, int64_t *__restrict__ row_ptr,
+                                                                     int64_t tiles, int64_t *__restrict__ out,
                                                                      int64_t n)
 {
     __shared__ unsigned long long s_w[kAffScanBlock / kWave];
@@ -391,111 +373,209 @@ __global__ __launch_bounds__(kAffScanBlock) void aff_scan_top_kernel(unsigned lo
         if (t < tiles) part[t] = carry + ex;
         carry += tot;
     }
-    if (threadIdx.x == 0) row_ptr[n] = int64_t(carry);
+    if (threadIdx.x == 0) out[n] = int64_t(carry);
 }
 
-__global__ __launch_bounds__(kAffScanBlock) void aff_scan_down_kernel(const uint32_t *__restrict__ extra, int64_t n,
-                                                                      int k,
+__global__ __launch_bounds__(kAffScanBlock) void aff_scan_down_kernel(const uint32_t *__restrict__ cnt, int64_t n,
+                                                                      int base,
                                                                       const unsigned long long *__restrict__ part,
-                                                                      int64_t *__restrict__ row_ptr)
+                                                                      int64_t *__restrict__ out)
 {
     __shared__ unsigned long long s_w[kAffScanBlock / kWave];
-    const int64_t base = int64_t(blockIdx.x) * kAffScanTile + int64_t(threadIdx.x) * kAffScanItems;
+    const int64_t b0 = int64_t(blockIdx.x) * kAffScanTile + int64_t(threadIdx.x) * kAffScanItems;
     unsigned long long len[kAffScanItems], v = 0;
 #pragma unroll
     for (int q = 0; q < kAffScanItems; ++q) {
-        len[q] = base + q < n ? uint64_t(k) + extra[base + q] : 0ull;
+        len[q] = b0 + q < n ? uint64_t(base) + cnt[b0 + q] : 0ull;
         v += len[q];
     }
     unsigned long long tot;
     unsigned long long off = part[blockIdx.x] + block_scan_excl(v, s_w, &tot);
 #pragma unroll
     for (int q = 0; q < kAffScanItems; ++q) {
-        if (base + q < n) row_ptr[base + q] = int64_t(off);
+        if (b0 + q < n) out[b0 + q] = int64_t(off);
         off += len[q];
     }
 }
 
-// 5. fill the output rows
-__global__ __launch_bounds__(256) void aff_fill_kernel(const int32_t *__restrict__ scol,
-                                                       const double *__restrict__ sp,
-                                                       const int16_t *__restrict__ mpos, int64_t n, int k,
-                                                       const int64_t *__restrict__ row_ptr,
-                                                       uint32_t *__restrict__ fill, int32_t *__restrict__ col,
-                                                       float *__restrict__ val)
+// the entries into the inboxes, at slots taken with a counter per row (their
+// order is sorted away below)
+__global__ __launch_bounds__(256) void aff_scatter_kernel(const int32_t *__restrict__ scol,
+                                                          const double *__restrict__ sp, int64_t n, int k,
+                                                          const int64_t *__restrict__ ib,
+                                                          uint32_t *__restrict__ cursor,
+                                                          int32_t *__restrict__ in_col, double *__restrict__ in_p)
 {
     const int64_t x = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
     if (x >= n * k) return;
     const int64_t i = x / k;
-    const int e = int(x - i * k);
     const uint32_t j = uint32_t(scol[x]);
-    if (j >= uint32_t(n) || int64_t(j) == i) return; // flagged
-    const double pji = sp[x];
-    const int m = mpos[x];
-    const double inv2n = 1.0 / (2.0 * double(n));
-    const double own = m >= 0 ? pji + sp[int64_t(j) * k + m] : pji;
-    col[row_ptr[i] + e] = int32_t(j);
-    val[row_ptr[i] + e] = float(own * inv2n);
-    if (m < 0) {
-        const int64_t slot = row_ptr[j] + k + atomicAdd(&fill[j], 1u);
-        col[slot] = int32_t(i);
-        val[slot] = float(pji * inv2n);
-    }
+    if (j >= uint32_t(n) || int64_t(j) == i) return;
+    const int64_t slot = ib[j] + atomicAdd(&cursor[j], 1u);
+    in_col[slot] = int32_t(i);
+    in_p[slot] = sp[x];
 }
 
-// 6. output rows by column: rows of up to kAffShortCap entries by one wave
-// each; longer rows are listed for the block kernel below
-__global__ __launch_bounds__(kWave) void aff_row_sort_kernel(const int64_t *__restrict__ row_ptr, int64_t n,
-                                                             int32_t *__restrict__ col, float *__restrict__ val,
-                                                             uint32_t *__restrict__ longrows,
-                                                             uint32_t *__restrict__ counters)
+// first position in the sorted a[0..len) whose value is >= key
+__device__ inline int lower_bound_u32(const uint32_t *a, int len, uint32_t key)
 {
-    __shared__ uint32_t s_key[kAffShortCap];
-    __shared__ uint32_t s_val[kAffShortCap];
-    const int64_t i = blockIdx.x;
-    const int64_t b = row_ptr[i], len = row_ptr[i + 1] - b;
-    if (len > kAffShortCap) {
-        if (threadIdx.x == 0) longrows[atomicAdd(&counters[0], 1u)] = uint32_t(i);
+    int lo = 0, hi = len;
+    while (lo < hi) {
+        const int m = (lo + hi) >> 1;
+        if (a[m] < key)
+            lo = m + 1;
+        else
+            hi = m;
+    }
+    return lo;
+}
+
+// Exclusive prefix counts MO[0..k] of the flags f[0..k) (k <= 256) into LDS,
+// by the whole block; returns the total in every thread.
+__device__ inline uint32_t block_flag_scan(const uint8_t *f, int k, uint32_t *MO, uint32_t *s_w)
+{
+    const int per = (k + int(blockDim.x) - 1) / int(blockDim.x);
+    const int e0 = int(threadIdx.x) * per;
+    uint32_t c = 0;
+    for (int e = e0; e < e0 + per && e < k; ++e) c += f[e];
+    const int lane = lane_id(), w = threadIdx.x / kWave;
+    uint32_t x = c;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const uint32_t y = __shfl_up(x, o, kWave);
+        if (lane >= o) x += y;
+    }
+    if (lane == kWave - 1) s_w[w] = x;
+    __syncthreads();
+    uint32_t off = 0, tot = 0;
+    for (int q = 0; q < int(blockDim.x) / kWave; ++q) {
+        off += q < w ? s_w[q] : 0u;
+        tot += s_w[q];
+    }
+    uint32_t run = off + x - c;
+    for (int e = e0; e < e0 + per && e < k; ++e) {
+        MO[e] = run;
+        run += f[e];
+    }
+    if (threadIdx.x == 0) MO[k] = tot;
+    __syncthreads();
+    return tot;
+}
+
+// 4./5. one row j of P from its own list (k columns in order, with p_{c|j})
+// and its inbox (m columns, with p_{j|c}).  kWrite = false: sort the inbox in
+// place and count the inbox entries that are not in the own list (P's row
+// has k plus that many entries); kWrite = true: write the row in column
+// order.  With MO[e] the number of own entries before e that are also in the
+// inbox, own entry e goes to e + t - MO[e] (t: inbox entries below its
+// column) and an inbox-only entry at inbox position t to e' + t - MO[e'] (e':
+// own entries below its column).  A pair in both lists is written once, with
+// (p_{c|j} + p_{j|c}) / 2N: the same fp64 sum in both rows, so P is exactly
+// symmetric.
+template <int kCap, bool kWrite> struct AffRowLds {
+    uint32_t own[kAffMaxK];
+    double ownp[kAffMaxK];
+    uint32_t in[kCap];
+    uint32_t pos[kWrite ? 1 : kCap];
+    double inp[kCap];
+    uint8_t fl[kAffMaxK];
+    uint32_t mo[kAffMaxK + 1];
+    uint32_t w[kAffLongThreads / kWave];
+};
+
+template <int kCap, bool kWrite>
+__device__ inline void aff_row(int64_t j, int k, int64_t n, const int32_t *__restrict__ scol,
+                               const double *__restrict__ sp, const int64_t *__restrict__ ib,
+                               int32_t *__restrict__ in_col, double *__restrict__ in_p,
+                               uint32_t *__restrict__ inonly, const int64_t *__restrict__ row_ptr,
+                               int32_t *__restrict__ col, float *__restrict__ val, AffRowLds<kCap, kWrite> &L)
+{
+    const int64_t b = ib[j];
+    const int m = int(ib[j + 1] - b);
+    for (int e = threadIdx.x; e < k; e += blockDim.x) {
+        L.own[e] = uint32_t(scol[j * k + e]);
+        L.ownp[e] = sp[j * k + e];
+    }
+    for (int t = threadIdx.x; t < m; t += blockDim.x) {
+        L.in[t] = uint32_t(in_col[b + t]);
+        L.inp[t] = in_p[b + t];
+        if (!kWrite) L.pos[t] = uint32_t(t);
+    }
+    if (!kWrite) lds_bitonic(L.in, L.pos, m); // ends with a barrier
+    __syncthreads();
+    for (int e = threadIdx.x; e < k; e += blockDim.x) {
+        const int t = lower_bound_u32(L.in, m, L.own[e]);
+        L.fl[e] = t < m && L.in[t] == L.own[e];
+    }
+    __syncthreads();
+    const uint32_t both = block_flag_scan(L.fl, k, L.mo, L.w);
+    if (!kWrite) {
+        for (int t = threadIdx.x; t < m; t += blockDim.x) {
+            in_col[b + t] = int32_t(L.in[t]);
+            in_p[b + t] = L.inp[L.pos[t]];
+        }
+        if (threadIdx.x == 0) inonly[j] = uint32_t(m) - both;
         return;
     }
-    for (int e = threadIdx.x; e < len; e += kWave) {
-        s_key[e] = uint32_t(col[b + e]);
-        s_val[e] = __float_as_uint(val[b + e]);
+    const int64_t o = row_ptr[j];
+    const double inv2n = 1.0 / (2.0 * double(n));
+    for (int e = threadIdx.x; e < k; e += blockDim.x) {
+        const int t = lower_bound_u32(L.in, m, L.own[e]);
+        const int64_t q = o + e + t - L.mo[e];
+        col[q] = int32_t(L.own[e]);
+        val[q] = float((L.fl[e] ? L.ownp[e] + L.inp[t] : L.ownp[e]) * inv2n);
     }
-    lds_bitonic(s_key, s_val, int(len));
-    for (int e = threadIdx.x; e < len; e += kWave) {
-        col[b + e] = int32_t(s_key[e]);
-        val[b + e] = __uint_as_float(s_val[e]);
+    for (int t = threadIdx.x; t < m; t += blockDim.x) {
+        const int e = lower_bound_u32(L.own, k, L.in[t]);
+        if (e < k && L.own[e] == L.in[t]) continue; // written with the own entry
+        const int64_t q = o + e + t - L.mo[e];
+        col[q] = int32_t(L.in[t]);
+        val[q] = float(L.inp[t] * inv2n);
     }
 }
 
-__global__ __launch_bounds__(kAffLongThreads) void aff_long_sort_kernel(const int64_t *__restrict__ row_ptr,
-                                                                        int32_t *__restrict__ col,
-                                                                        float *__restrict__ val,
-                                                                        const uint32_t *__restrict__ longrows,
-                                                                        const uint32_t *__restrict__ counters,
-                                                                        Header *__restrict__ hdr)
+// rows whose inbox fits kAffShortCap: one wave each; longer ones are listed
+// (by the counting pass) for the block kernel
+template <bool kWrite>
+__global__ __launch_bounds__(kWave) void aff_row_kernel(int64_t n, int k, const int32_t *__restrict__ scol,
+                                                        const double *__restrict__ sp,
+                                                        const int64_t *__restrict__ ib, int32_t *__restrict__ in_col,
+                                                        double *__restrict__ in_p, uint32_t *__restrict__ inonly,
+                                                        const int64_t *__restrict__ row_ptr,
+                                                        int32_t *__restrict__ col, float *__restrict__ val,
+                                                        uint32_t *__restrict__ longrows,
+                                                        uint32_t *__restrict__ counters)
 {
-    __shared__ uint32_t s_key[kAffLongCap];
-    __shared__ uint32_t s_val[kAffLongCap];
+    __shared__ AffRowLds<kAffShortCap, kWrite> L;
+    const int64_t j = blockIdx.x;
+    if (ib[j + 1] - ib[j] > kAffShortCap) {
+        if (!kWrite && threadIdx.x == 0) longrows[atomicAdd(&counters[0], 1u)] = uint32_t(j);
+        return;
+    }
+    aff_row<kAffShortCap, kWrite>(j, k, n, scol, sp, ib, in_col, in_p, inonly, row_ptr, col, val, L);
+}
+
+template <bool kWrite>
+__global__ __launch_bounds__(kAffLongThreads) void aff_long_row_kernel(
+    int64_t n, int k, const int32_t *__restrict__ scol, const double *__restrict__ sp,
+    const int64_t *__restrict__ ib, int32_t *__restrict__ in_col, double *__restrict__ in_p,
+    uint32_t *__restrict__ inonly, const int64_t *__restrict__ row_ptr, int32_t *__restrict__ col,
+    float *__restrict__ val, const uint32_t *__restrict__ longrows, const uint32_t *__restrict__ counters,
+    Header *__restrict__ hdr)
+{
+    __shared__ AffRowLds<kAffLongCap, kWrite> L;
     const uint32_t count = counters[0];
     for (uint32_t r = blockIdx.x; r < count; r += gridDim.x) {
-        const int64_t i = longrows[r];
-        const int64_t b = row_ptr[i], len = row_ptr[i + 1] - b;
-        if (len > kAffLongCap) { // over the documented limit: left unsorted
-            if (threadIdx.x == 0) atomicOr(&hdr->flags, kErrRange);
+        const int64_t j = longrows[r];
+        if (ib[j + 1] - ib[j] > kAffLongCap) { // over the documented limit
+            if (!kWrite && threadIdx.x == 0) {
+                atomicOr(&hdr->flags, kErrRange);
+                inonly[j] = 0;
+            }
             continue;
         }
         __syncthreads();
-        for (int e = threadIdx.x; e < len; e += kAffLongThreads) {
-            s_key[e] = uint32_t(col[b + e]);
-            s_val[e] = __float_as_uint(val[b + e]);
-        }
-        lds_bitonic(s_key, s_val, int(len));
-        for (int e = threadIdx.x; e < len; e += kAffLongThreads) {
-            col[b + e] = int32_t(s_key[e]);
-            val[b + e] = __uint_as_float(s_val[e]);
-        }
+        aff_row<kAffLongCap, kWrite>(j, k, n, scol, sp, ib, in_col, in_p, inonly, row_ptr, col, val, L);
     }
 }
 
@@ -504,45 +584,60 @@ void launch_aff_front(const int32_t *idx, const float *dist, int64_t n, int k, d
                       int64_t *row_ptr, double *sigma2, void *ws, const AffLayout &A, hipStream_t st)
 {
     Header *hdr = at<Header>(ws, A.header);
-    uint32_t *extra = at<uint32_t>(ws, A.extra), *fill = at<uint32_t>(ws, A.fill);
-    uint32_t *counters = at<uint32_t>(ws, A.counters);
+    uint32_t *indeg = at<uint32_t>(ws, A.indeg), *cursor = at<uint32_t>(ws, A.cursor);
+    uint32_t *inonly = at<uint32_t>(ws, A.inonly), *counters = at<uint32_t>(ws, A.counters);
     double *sp = at<double>(ws, A.sp);
     int32_t *scol = at<int32_t>(ws, A.scol);
-    aff_clear_kernel<<<unsigned((n + 255) / 256), 256, 0, st>>>(hdr, extra, fill, counters, n);
-    const unsigned sb = unsigned((n + 3) / 4);
+    int64_t *ib = at<int64_t>(ws, A.ib);
+    int32_t *in_col = at<int32_t>(ws, A.in_col);
+    double *in_p = at<double>(ws, A.in_p);
+    uint32_t *longrows = at<uint32_t>(ws, A.longrows);
+    unsigned long long *part = at<unsigned long long>(ws, A.part);
+    aff_clear_kernel<<<unsigned((n + 255) / 256), 256, 0, st>>>(hdr, indeg, cursor, counters, n);
     const double lu = log(perplexity);
     if (k <= kAffLaneMaxK) {
         float *dT = at<float>(ws, A.dT);
         aff_transpose_kernel<<<unsigned((n + kAffTransRows - 1) / kAffTransRows), 256, 0, st>>>(dist, n, k, dT);
         aff_search_lane_kernel<<<unsigned((n + 255) / 256), 256, 0, st>>>(dT, n, k, lu, sp, sigma2, hdr);
+    } else {
+        const unsigned sb = unsigned((n + 3) / 4);
+        if ((k + kWave - 1) / kWave == 3)
+            aff_search_kernel<3><<<sb, kAffSearchBlock, 0, st>>>(dist, n, k, lu, sp, sigma2, hdr);
+        else
+            aff_search_kernel<4><<<sb, kAffSearchBlock, 0, st>>>(dist, n, k, lu, sp, sigma2, hdr);
     }
-    else switch ((k + kWave - 1) / kWave) {
-    case 1: aff_search_kernel<1><<<sb, kAffSearchBlock, 0, st>>>(dist, n, k, lu, sp, sigma2, hdr); break;
-    case 2: aff_search_kernel<2><<<sb, kAffSearchBlock, 0, st>>>(dist, n, k, lu, sp, sigma2, hdr); break;
-    case 3: aff_search_kernel<3><<<sb, kAffSearchBlock, 0, st>>>(dist, n, k, lu, sp, sigma2, hdr); break;
-    default: aff_search_kernel<4><<<sb, kAffSearchBlock, 0, st>>>(dist, n, k, lu, sp, sigma2, hdr); break;
-    }
-    static_assert(kAffMaxK <= 4 * kWave, "four distances per lane at most");
+    static_assert(kAffMaxK <= 4 * kWave && kAffLaneMaxK >= 2 * kWave, "three or four distances per lane");
     aff_own_sort_kernel<<<unsigned(n), kWave, 0, st>>>(idx, n, k, scol, sp, hdr);
-    const int64_t entries = n * k;
-    aff_pairs_kernel<<<unsigned((entries + 255) / 256), 256, 0, st>>>(scol, n, k, at<int16_t>(ws, A.mpos), extra);
-    unsigned long long *part = at<unsigned long long>(ws, A.part);
-    aff_scan_part_kernel<<<unsigned(A.scan_tiles), kAffScanBlock, 0, st>>>(extra, n, k, part);
+    const unsigned eb = unsigned((n * k + 255) / 256);
+    aff_indeg_kernel<<<eb, 256, 0, st>>>(scol, n, k, indeg);
+    aff_scan_part_kernel<<<unsigned(A.scan_tiles), kAffScanBlock, 0, st>>>(indeg, n, 0, part);
+    aff_scan_top_kernel<<<1, kAffScanBlock, 0, st>>>(part, A.scan_tiles, ib, n);
+    aff_scan_down_kernel<<<unsigned(A.scan_tiles), kAffScanBlock, 0, st>>>(indeg, n, 0, part, ib);
+    aff_scatter_kernel<<<eb, 256, 0, st>>>(scol, sp, n, k, ib, cursor, in_col, in_p);
+    aff_row_kernel<false><<<unsigned(n), kWave, 0, st>>>(n, k, scol, sp, ib, in_col, in_p, inonly, nullptr,
+                                                         nullptr, nullptr, longrows, counters);
+    aff_long_row_kernel<false><<<256, kAffLongThreads, 0, st>>>(n, k, scol, sp, ib, in_col, in_p, inonly, nullptr,
+                                                                nullptr, nullptr, longrows, counters, hdr);
+    aff_scan_part_kernel<<<unsigned(A.scan_tiles), kAffScanBlock, 0, st>>>(inonly, n, k, part);
     aff_scan_top_kernel<<<1, kAffScanBlock, 0, st>>>(part, A.scan_tiles, row_ptr, n);
-    aff_scan_down_kernel<<<unsigned(A.scan_tiles), kAffScanBlock, 0, st>>>(extra, n, k, part, row_ptr);
+    aff_scan_down_kernel<<<unsigned(A.scan_tiles), kAffScanBlock, 0, st>>>(inonly, n, k, part, row_ptr);
 }
 
 void launch_aff_back(int64_t n, int k, const int64_t *row_ptr, int32_t *col, float *val, void *ws,
                      const AffLayout &A, hipStream_t st)
 {
-    const int64_t entries = n * k;
-    uint32_t *counters = at<uint32_t>(ws, A.counters);
-    aff_fill_kernel<<<unsigned((entries + 255) / 256), 256, 0, st>>>(
-        at<int32_t>(ws, A.scol), at<double>(ws, A.sp), at<int16_t>(ws, A.mpos), n, k, row_ptr,
-        at<uint32_t>(ws, A.fill), col, val);
-    aff_row_sort_kernel<<<unsigned(n), kWave, 0, st>>>(row_ptr, n, col, val, at<uint32_t>(ws, A.longrows), counters);
-    aff_long_sort_kernel<<<256, kAffLongThreads, 0, st>>>(row_ptr, col, val, at<uint32_t>(ws, A.longrows), counters,
-                                                          at<Header>(ws, A.header));
+    const int32_t *scol = at<int32_t>(ws, A.scol);
+    const double *sp = at<double>(ws, A.sp);
+    const int64_t *ib = at<int64_t>(ws, A.ib);
+    int32_t *in_col = at<int32_t>(ws, A.in_col);
+    double *in_p = at<double>(ws, A.in_p);
+    uint32_t *inonly = at<uint32_t>(ws, A.inonly), *counters = at<uint32_t>(ws, A.counters);
+    uint32_t *longrows = at<uint32_t>(ws, A.longrows);
+    aff_row_kernel<true><<<unsigned(n), kWave, 0, st>>>(n, k, scol, sp, ib, in_col, in_p, inonly, row_ptr, col, val,
+                                                        longrows, counters);
+    aff_long_row_kernel<true><<<256, kAffLongThreads, 0, st>>>(n, k, scol, sp, ib, in_col, in_p, inonly, row_ptr,
+                                                               col, val, longrows, counters,
+                                                               at<Header>(ws, A.header));
 }
 
 } // namespace bht

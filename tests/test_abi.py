@@ -181,10 +181,10 @@ def test_affinities_workspace_size():
     assert ws(1 << 24, 90) == 0 and ws((1 << 24) - 1, 90) > 0
     a, b = ws(1000, 30), ws(1000, 60)
     assert 0 < a < b and a % 256 == 0
-    # p (8 B), columns (4 B), partner positions (2 B) and, for k <= 128, the
-    # transposed distances (4 B) per neighbour
-    assert 18 * 1_300_000 * 90 < ws(1_300_000, 90) < 20 * 1_300_000 * 90
-    assert 14 * 1000 * 200 < ws(1000, 200) < 16 * 1000 * 200
+    # per neighbour: p and its column (12 B), the inbox entry (12 B) and, for
+    # k <= 128, the transposed distance (4 B)
+    assert 28 * 1_300_000 * 90 < ws(1_300_000, 90) < 30 * 1_300_000 * 90
+    assert 24 * 1000 * 200 < ws(1000, 200) < 26 * 1000 * 200
 
 
 def test_affinities_rejects_bad_arguments():
