@@ -50,6 +50,8 @@ def parse():
     ap.add_argument("--no-count", action="store_true", help="skip the interaction-counting replay")
     ap.add_argument("--no-affinities", action="store_true", help="skip the input-similarity measurement")
     ap.add_argument("--affinities-only", action="store_true", help="measure only the input similarities")
+    ap.add_argument("--no-fp64", action="store_true", help="skip the fp64-variant measurement")
+    ap.add_argument("--fp64-only", action="store_true", help="measure only the fp64 variant")
     ap.add_argument("--plain", action="store_true",
                     help="attractive step straight from the CSR arrays (no locality layout)")
     ap.add_argument("--no-overlap", action="store_true",
@@ -149,6 +151,63 @@ def bench_affinities(args, cpu_rows=20000):
     return out
 
 
+def bench_fp64(args, inp, steps=200, warmup=5):
+    """The fp64 variant against the fp32 path on the same workload, both on
+    the plain CSR P (the variant has no locality layout): iterations/s over
+    the first `steps` iterations of the schedule, inputs resident, with the
+    per-phase event times of the fp64 run."""
+    import numpy as np
+    import torch
+
+    import paper_2212_11506_amd as bh
+
+    w = inp.workload
+    n, nnz = inp.n, inp.nnz
+    dev = torch.device("cuda:0")
+    out = {"workload": f"{w.description} (workload {w.cid}), plain CSR P, iterations 0..{steps - 1}",
+           "steps": steps}
+    for name, dt in (("fp64", torch.float64), ("fp32", torch.float32)):
+        if dt == torch.float64:
+            P = bh.CsrF64.from_numpy(inp.row_ptr, inp.col, inp.val.astype(np.float64), device=dev)
+            ws = torch.empty(bh.workspace_size_f64(n, nnz), dtype=torch.uint8, device=dev)
+            fn = bh.step_f64
+        else:
+            P = bh.Csr.from_numpy(inp.row_ptr, inp.col, inp.val, device=dev)
+            ws = torch.empty(bh.workspace_size(n, nnz), dtype=torch.uint8, device=dev)
+            fn = bh.step
+        Y0 = torch.from_numpy(inp.Y).to(dev).to(dt)
+        Y = Y0.clone()
+        u = torch.zeros_like(Y)
+        g = torch.ones_like(Y)
+
+        def run(k):
+            for it in range(k):
+                s = w.schedule(it)
+                fn(Y, P, args.theta, s["exaggeration"], s["learning_rate"], s["momentum"], 0.01, u, g, workspace=ws)
+
+        run(warmup)
+        torch.cuda.synchronize()
+        Y.copy_(Y0)
+        u.zero_()
+        g.fill_(1.0)
+        bh.timing_phases(None)
+        bh.timing_read(reset=True)
+        bh.timing_enable(True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        run(steps)
+        torch.cuda.synchronize()
+        dt_s = time.perf_counter() - t0
+        bh.timing_enable(False)
+        ph = bh.timing_read(reset=True)
+        out[name] = {"iterations_per_s": steps / dt_s, "ms_per_step": 1e3 * dt_s / steps,
+                     "phases_ms": {k: v[0] / v[1] for k, v in ph.items() if v[1]}}
+        del P, ws, Y0, Y, u, g
+        torch.cuda.empty_cache()
+    out["fp64_over_fp32_time"] = out["fp64"]["ms_per_step"] / out["fp32"]["ms_per_step"]
+    return out
+
+
 def main():
     args = parse()
     if args.no_overlap:
@@ -176,6 +235,9 @@ def main():
     t0 = time.time()
     inp = synth.make_inputs(args.workload, n=args.n, progress=log)
     log(f"[bench] inputs: n={inp.n} nnz={inp.nnz} generated in {time.time() - t0:.1f}s")
+    if args.fp64_only:
+        print(json.dumps({"fp64_variant": bench_fp64(args, inp)}), flush=True)
+        return
     n, nnz = inp.n, inp.nnz
     dev = torch.device("cuda:0")
     Y0 = torch.from_numpy(inp.Y).to(dev)
@@ -379,6 +441,7 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
         "affinities": None if args.no_affinities else bench_affinities(args),
+        "fp64_variant": None if args.no_fp64 else bench_fp64(args, inp),
     }
     print(json.dumps(out), flush=True)
 

@@ -288,6 +288,32 @@ int bhtsne_affinities(const int32_t *knn_idx, const float *knn_dist, int64_t n, 
                       int64_t *row_ptr, int32_t *col, float *val, int64_t capacity, int64_t *nnz, double *sigma2,
                       void *workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* ------------------------------------------------------------------------
+ * The fp64 variant of the gradient step (the paper's default precision; its
+ * supplementary fp32/fp64 comparison).  Same method, phases and readings as
+ * bhtsne_gradient / bhtsne_step on a plain CSR P, with fp64 coordinates,
+ * probabilities, tree centres and thresholds, forces, Z and optimiser state;
+ * the Morton codes quantise the fp64 coordinates.  Y, grad, update, gains are
+ * n x 2 row-major fp64 device arrays; P's values are fp64.  Its workspace
+ * size is bhtsne_workspace_size_f64 (larger than the fp32 one: fp64 copies
+ * of Y, 40-byte node records).  Same argument checks and errors as the fp32
+ * calls (theta, exaggeration, learning_rate, momentum and min_gain are
+ * doubles).  No locality layout for this variant. */
+typedef struct bhtsne_csr_f64 {
+    int64_t n;              /* points; 2 <= n <= 16777215 */
+    int64_t nnz;            /* stored entries, >= 0 */
+    const int64_t *row_ptr; /* device, n + 1 entries */
+    const int32_t *col;     /* device, nnz entries (may be NULL when nnz == 0) */
+    const double *val;      /* device, nnz entries (may be NULL when nnz == 0) */
+} bhtsne_csr_f64;
+
+size_t bhtsne_workspace_size_f64(int64_t n, int64_t nnz);
+int bhtsne_gradient_f64(const double *Y, const bhtsne_csr_f64 *P, double theta, double exaggeration, double *grad,
+                        double *Z, void *workspace, size_t workspace_bytes, hipStream_t stream);
+int bhtsne_step_f64(double *Y, const bhtsne_csr_f64 *P, double theta, double exaggeration, double learning_rate,
+                    double momentum, double min_gain, double *update, double *gains, double *grad, double *Z,
+                    void *workspace, size_t workspace_bytes, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

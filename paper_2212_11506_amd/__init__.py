@@ -16,6 +16,7 @@ from ._binding import (  # noqa: F401
     PHASES,
     BhtsneError,
     Csr,
+    CsrF64,
     Layout,
     affinities,
     affinities_workspace_size,
@@ -23,15 +24,18 @@ from ._binding import (  # noqa: F401
     debug_tree,
     get_stats,
     gradient,
+    gradient_f64,
     layout_size,
     library_path,
     load_library,
     status_string,
     step,
+    step_f64,
     timing_enable,
     timing_phases,
     timing_read,
     workspace_size,
+    workspace_size_f64,
     z_exact,
     kl,
 )

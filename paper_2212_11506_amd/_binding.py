@@ -81,6 +81,11 @@ def load_library():
         "bhtsne_kl": (C.c_int, [vp, C.POINTER(_Csr), C.c_double, C.POINTER(C.c_double), vp, C.c_size_t, vp]),
         "bhtsne_timing_read": (C.c_int, [C.POINTER(_Timing), C.c_int]),
         "bhtsne_affinities_workspace_size": (C.c_size_t, [i64, C.c_int32]),
+        "bhtsne_workspace_size_f64": (C.c_size_t, [i64, i64]),
+        "bhtsne_gradient_f64": (C.c_int, [vp, C.POINTER(_Csr), C.c_double, C.c_double, vp, f64p, vp, C.c_size_t,
+                                          vp]),
+        "bhtsne_step_f64": (C.c_int, [vp, C.POINTER(_Csr), C.c_double, C.c_double, C.c_double, C.c_double,
+                                      C.c_double, vp, vp, vp, f64p, vp, C.c_size_t, vp]),
         "bhtsne_affinities": (C.c_int, [vp, vp, i64, C.c_int32, C.c_double, vp, vp, vp, i64,
                                         C.POINTER(C.c_int64), vp, vp, C.c_size_t, vp]),
         "bhtsne_debug_sort": (C.c_int, [vp, i64, vp, vp, vp, f64p, vp, C.c_size_t, vp]),
@@ -140,6 +145,68 @@ class Csr:
     @property
     def struct(self):
         return C.byref(self._s)
+
+
+class CsrF64(Csr):
+    """Device CSR matrix P with fp64 values, for the fp64 variant (same
+    struct layout as Csr: bhtsne_csr_f64)."""
+
+    def __init__(self, row_ptr: torch.Tensor, col: torch.Tensor, val: torch.Tensor):
+        self.row_ptr, self.col, self.val = row_ptr, col, val
+        self.n = int(row_ptr.numel()) - 1
+        self.nnz = int(col.numel())
+        self._s = _Csr(self.n, self.nnz, _ptr(row_ptr, torch.int64, "row_ptr").value,
+                       _ptr(col, torch.int32, "col").value if self.nnz else None,
+                       _ptr(val, torch.float64, "val").value if self.nnz else None)
+
+    @classmethod
+    def from_numpy(cls, row_ptr, col, val, device="cuda"):
+        return cls(torch.as_tensor(row_ptr, dtype=torch.int64).to(device),
+                   torch.as_tensor(col, dtype=torch.int32).to(device),
+                   torch.as_tensor(val, dtype=torch.float64).to(device))
+
+
+def workspace_size_f64(n: int, nnz: int) -> int:
+    return int(load_library().bhtsne_workspace_size_f64(int(n), int(nnz)))
+
+
+def gradient_f64(Y: torch.Tensor, P: "CsrF64", theta: float, exaggeration: float = 1.0,
+                 grad: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                 return_z: bool = True):
+    """bhtsne_gradient_f64: returns (grad fp64, Z or None)."""
+    lib = load_library()
+    if not isinstance(P, CsrF64):
+        raise TypeError("gradient_f64 takes P as a CsrF64")
+    if grad is None:
+        grad = torch.empty_like(Y)
+    ws = workspace if workspace is not None else torch.empty(workspace_size_f64(P.n, P.nnz), dtype=torch.uint8,
+                                                             device=Y.device)
+    z = C.c_double(0.0)
+    rc = lib.bhtsne_gradient_f64(_ptr(Y, torch.float64, "Y"), P.struct, float(theta), float(exaggeration),
+                                 _ptr(grad, torch.float64, "grad"), C.byref(z) if return_z else None,
+                                 _ptr(ws, None, "workspace"), ws.numel(), _stream())
+    _check(rc, "bhtsne_gradient_f64")
+    return grad, (z.value if return_z else None)
+
+
+def step_f64(Y: torch.Tensor, P: "CsrF64", theta: float, exaggeration: float, learning_rate: float,
+             momentum: float, min_gain: float, update: torch.Tensor, gains: torch.Tensor,
+             grad: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+             return_z: bool = False):
+    """bhtsne_step_f64: one fp64 iteration in place on Y, update and gains."""
+    lib = load_library()
+    if not isinstance(P, CsrF64):
+        raise TypeError("step_f64 takes P as a CsrF64")
+    ws = workspace if workspace is not None else torch.empty(workspace_size_f64(P.n, P.nnz), dtype=torch.uint8,
+                                                             device=Y.device)
+    z = C.c_double(0.0)
+    rc = lib.bhtsne_step_f64(_ptr(Y, torch.float64, "Y"), P.struct, float(theta), float(exaggeration),
+                             float(learning_rate), float(momentum), float(min_gain),
+                             _ptr(update, torch.float64, "update"), _ptr(gains, torch.float64, "gains"),
+                             _ptr(grad, torch.float64, "grad"), C.byref(z) if return_z else None,
+                             _ptr(ws, None, "workspace"), ws.numel(), _stream())
+    _check(rc, "bhtsne_step_f64")
+    return z.value if return_z else None
 
 
 def workspace_size(n: int, nnz: int) -> int:

@@ -129,7 +129,7 @@ void build_sorted_tree(const float *Y, int64_t n, float theta, void *ws, const L
     }
     {
         PhaseTimer pt(BHTSNE_PHASE_TREE, st);
-        launch_tree(n, theta, ws, L, dbg, st);
+        launch_tree<float>(n, double(theta) * double(theta), ws, L, dbg, st);
     }
 }
 
@@ -246,7 +246,7 @@ int run(float *Y, const bhtsne_csr *P, float theta, const StepArgs &a, float *up
     build_tree(Y, n, theta, nullptr, ws, L, TreeDebug{}, st);
     {
         PhaseTimer pt(BHTSNE_PHASE_REPULSIVE, st);
-        launch_repulsive(n, repulsive_self_test(theta), ws, L, st);
+        launch_repulsive<float>(n, repulsive_self_test(theta), ws, L, st);
     }
     {
         PhaseTimer pt(BHTSNE_PHASE_ATTRACTIVE, st);
@@ -288,6 +288,37 @@ int check_layout(const bhtsne_layout *lay)
     return BHTSNE_OK;
 }
 
+// The fp64 variant (plain CSR): the same phases with fp64 coordinates,
+// centres, thresholds, forces and optimiser state.
+int run64(double *Y, const bhtsne_csr_f64 *P, double theta, const StepArgsT<double> &a, double *update,
+          double *gains, double *grad, double *Z, void *ws, hipStream_t st)
+{
+    const int64_t n = P->n;
+    const Layout L = make_layout(n, P->nnz, 8);
+    {
+        PhaseTimer pt(BHTSNE_PHASE_BBOX_MORTON, st);
+        launch_bbox(Y, n, ws, L, st);
+        launch_morton(Y, n, nullptr, ws, L, st);
+    }
+    {
+        PhaseTimer pt(BHTSNE_PHASE_SORT, st);
+        launch_sort(n, static_cast<const double *>(Y), ws, L, st);
+    }
+    {
+        PhaseTimer pt(BHTSNE_PHASE_TREE, st);
+        launch_tree<double>(n, theta * theta, ws, L, TreeDebug{}, st);
+    }
+    {
+        PhaseTimer pt(BHTSNE_PHASE_REPULSIVE, st);
+        launch_repulsive<double>(n, repulsive_self_test(theta), ws, L, st);
+    }
+    {
+        PhaseTimer pt(BHTSNE_PHASE_ATTRACTIVE, st);
+        launch_attract(P->row_ptr, P->col, P->val, n, P->nnz, a, Y, update, gains, grad, ws, L, st);
+    }
+    return finish(Z, ws, st);
+}
+
 int run_layout(float *Y, const bhtsne_layout *lay, float theta, const StepArgs &a, float *update, float *gains,
                float *grad, double *Z, void *ws, hipStream_t st)
 {
@@ -305,7 +336,7 @@ int run_layout(float *Y, const bhtsne_layout *lay, float theta, const StepArgs &
     }
     if (fork >= 2) {
         PhaseTimer pt(BHTSNE_PHASE_TREE, st);
-        launch_tree(n, theta, ws, L, TreeDebug{}, st);
+        launch_tree<float>(n, double(theta) * double(theta), ws, L, TreeDebug{}, st);
     }
     Side *side = overlap_enabled() ? side_stream() : nullptr;
     std::unique_lock<std::mutex> lk;
@@ -327,11 +358,11 @@ int run_layout(float *Y, const bhtsne_layout *lay, float theta, const StepArgs &
     }
     if (fork < 2) {
         PhaseTimer pt(BHTSNE_PHASE_TREE, st);
-        launch_tree(n, theta, ws, L, TreeDebug{}, st);
+        launch_tree<float>(n, double(theta) * double(theta), ws, L, TreeDebug{}, st);
     }
     {
         PhaseTimer pt(BHTSNE_PHASE_REPULSIVE, st);
-        launch_repulsive(n, repulsive_self_test(theta), ws, L, st);
+        launch_repulsive<float>(n, repulsive_self_test(theta), ws, L, st);
     }
     if (side && hipStreamWaitEvent(st, side->join, 0) != hipSuccess) return BHTSNE_EDEVICE;
     if (lk.owns_lock()) lk.unlock();
@@ -389,6 +420,62 @@ int bhtsne_step(float *Y, const bhtsne_csr *P, float theta, float exaggeration, 
     if (rc != BHTSNE_OK) return rc;
     StepArgs a{exaggeration, learning_rate, momentum, min_gain, 1};
     return run(Y, P, theta, a, update, gains, grad, Z, workspace, stream);
+}
+
+size_t bhtsne_workspace_size_f64(int64_t n, int64_t nnz)
+{
+    if (n < 2 || n > kMaxPoints || nnz < 0) return 0;
+    return make_layout(n, nnz, 8).total;
+}
+
+static int check_csr_f64(const bhtsne_csr_f64 *P)
+{
+    if (!P) return BHTSNE_EINVAL;
+    if (P->n < 2 || P->n > kMaxPoints) return BHTSNE_EINVAL;
+    if (P->nnz < 0 || !P->row_ptr) return BHTSNE_EINVAL;
+    if (P->nnz > 0 && (!P->col || !P->val)) return BHTSNE_EINVAL;
+    return BHTSNE_OK;
+}
+
+static int check_ws_f64(int64_t n, int64_t nnz, void *ws, size_t bytes)
+{
+    if (!ws || !aligned(ws)) return BHTSNE_EWORKSPACE;
+    size_t need = bhtsne_workspace_size_f64(n, nnz);
+    if (need == 0) return BHTSNE_EINVAL;
+    if (bytes < need) return BHTSNE_EWORKSPACE;
+    return BHTSNE_OK;
+}
+
+int bhtsne_gradient_f64(const double *Y, const bhtsne_csr_f64 *P, double theta, double exaggeration, double *grad,
+                        double *Z, void *workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    int rc = check_csr_f64(P);
+    if (rc != BHTSNE_OK) return rc;
+    if (!Y || !grad) return BHTSNE_EINVAL;
+    if (!std::isfinite(theta) || theta < 0.0) return BHTSNE_EINVAL;
+    if (!std::isfinite(exaggeration) || !(exaggeration > 0.0)) return BHTSNE_EINVAL;
+    rc = check_ws_f64(P->n, P->nnz, workspace, workspace_bytes);
+    if (rc != BHTSNE_OK) return rc;
+    StepArgsT<double> a{exaggeration, 0.0, 0.0, 0.0, 0};
+    return run64(const_cast<double *>(Y), P, theta, a, nullptr, nullptr, grad, Z, workspace, stream);
+}
+
+int bhtsne_step_f64(double *Y, const bhtsne_csr_f64 *P, double theta, double exaggeration, double learning_rate,
+                    double momentum, double min_gain, double *update, double *gains, double *grad, double *Z,
+                    void *workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    int rc = check_csr_f64(P);
+    if (rc != BHTSNE_OK) return rc;
+    if (!Y || !update || !gains) return BHTSNE_EINVAL;
+    if (!std::isfinite(theta) || theta < 0.0) return BHTSNE_EINVAL;
+    if (!std::isfinite(exaggeration) || !(exaggeration > 0.0)) return BHTSNE_EINVAL;
+    if (!std::isfinite(learning_rate) || !(learning_rate > 0.0)) return BHTSNE_EINVAL;
+    if (!std::isfinite(momentum) || momentum < 0.0 || !(momentum < 1.0)) return BHTSNE_EINVAL;
+    if (!std::isfinite(min_gain) || min_gain < 0.0) return BHTSNE_EINVAL;
+    rc = check_ws_f64(P->n, P->nnz, workspace, workspace_bytes);
+    if (rc != BHTSNE_OK) return rc;
+    StepArgsT<double> a{exaggeration, learning_rate, momentum, min_gain, 1};
+    return run64(Y, P, theta, a, update, gains, grad, Z, workspace, stream);
 }
 
 size_t bhtsne_layout_size(int64_t n, int64_t nnz)

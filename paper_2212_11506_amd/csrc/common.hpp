@@ -40,6 +40,9 @@ constexpr int kRepBlock = 1024;
 // next: byte offset of the first record after the node's subtree;
 // self: the sorted position of a single point, kNodeCell for a cell.
 constexpr int kNodeBytes = 24;
+// The fp64 variant's record: {com.x, com.y, thr (fp64), count (fp32), next,
+// self, padding}, 40 bytes.
+constexpr int kNodeBytes64 = 40;
 constexpr uint32_t kNodeCell = 0xFFFFFFFFu;
 // the 2n - 1 records end below 2^32 bytes
 constexpr int64_t kMaxPoints = (int64_t(1) << 24) - 1;
@@ -101,7 +104,9 @@ inline int64_t rep_blocks_for(int64_t n)
     return (b + 7) / 8 * 8; // multiple of 8 for the XCD-contiguous remap
 }
 
-inline Layout make_layout(int64_t n, int64_t nnz)
+// `fbytes` is the size of a coordinate: 4 (fp32 path) or 8 (fp64 variant,
+// which sizes the copies of Y, the node records and F_rep for fp64)
+inline Layout make_layout(int64_t n, int64_t nnz, int fbytes = 4)
 {
     Layout L{};
     L.n = n;
@@ -117,15 +122,15 @@ inline Layout make_layout(int64_t n, int64_t nnz)
     };
     L.header = take(sizeof(Header));
     L.hist = take(sizeof(uint32_t) * kHistCopies * kHistWords);
-    L.bbox_part = take(32 * kBBoxBlocks); // {min x, max x, min y, max y, non-finite flag}
+    L.bbox_part = take(64 * kBBoxBlocks); // {min x, max x, min y, max y, non-finite flag}, fp32 or fp64
     L.codes0 = take(8 * size_t(n));
     L.codes1 = take(8 * size_t(n));
     L.idx0 = take(4 * size_t(n));
     L.idx1 = take(4 * size_t(n));
     L.status = take(4 * size_t(kSortPasses) * kRadix * size_t(L.sort_tiles));
     // + one LDS segment of padding: segment loads past the last point stay inside the buffer
-    L.ycopy = take(8 * size_t(n + kYPad));
-    L.ys = take(8 * size_t(n));
+    L.ycopy = take(2 * size_t(fbytes) * size_t(n + kYPad));
+    L.ys = take(2 * size_t(fbytes) * size_t(n));
     L.levelmask = take(4 * size_t(n));
     L.split_b = take(4 * size_t(n));
     L.split_e = take(4 * size_t(n));
@@ -134,8 +139,8 @@ inline Layout make_layout(int64_t n, int64_t nnz)
     L.scan_cnt = take(4 * size_t(L.scan_tiles + 1));
     L.scan_sum = take(16 * size_t(L.scan_tiles + 1));
     // + 8 bytes: the walk loads 32 bytes at a record's offset
-    L.nodes = take(kNodeBytes * size_t(2 * n) + 8);
-    L.frep = take(8 * size_t(n));
+    L.nodes = take((fbytes == 8 ? kNodeBytes64 : kNodeBytes) * size_t(2 * n) + 8);
+    L.frep = take(2 * size_t(fbytes) * size_t(n));
     L.fattr = take(8 * size_t(n));
     // partial attractive sums, one per (tile, sorted row slot): up to
     // kTileMaxSeg tiles of kTileRows rows per row block
@@ -180,6 +185,33 @@ __device__ inline float wave_max(float v)
     for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
     return v;
 }
+
+__device__ inline double wave_min(double v)
+{
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmin(v, __shfl_xor(v, o, kWave));
+    return v;
+}
+
+__device__ inline double wave_max(double v)
+{
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o, kWave));
+    return v;
+}
+
+__device__ inline float vmin(float a, float b) { return fminf(a, b); }
+__device__ inline float vmax(float a, float b) { return fmaxf(a, b); }
+__device__ inline double vmin(double a, double b) { return fmin(a, b); }
+__device__ inline double vmax(double a, double b) { return fmax(a, b); }
+
+// two coordinates of the fp32 path or of the fp64 variant
+template <typename T> struct Vec2;
+template <> struct Vec2<float> { using type = float2; };
+template <> struct Vec2<double> { using type = double2; };
+template <typename T> using vec2_t = typename Vec2<T>::type;
+__host__ __device__ inline float2 make_vec2(float x, float y) { return make_float2(x, y); }
+__host__ __device__ inline double2 make_vec2(double x, double y) { return make_double2(x, y); }
 
 // Logical block index such that each of the 8 XCDs (blocks are dealt to XCDs
 // round-robin) receives one contiguous range of logical blocks.  `nblocks`

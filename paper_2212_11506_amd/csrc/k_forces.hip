@@ -95,9 +95,46 @@ __device__ inline void repulsive_walk(const char *nbase, uint32_t end, float2 yi
     }
 }
 
+// The fp64 variant of the walk: the same visit order and acceptance test on
+// 40-byte records with fp64 centres and thresholds; the lanes that take a
+// node accumulate under the compiler's own EXEC mask.
+template <bool kSelf>
+__device__ inline void repulsive_walk64(const char *nbase, uint32_t end, double2 yi, uint32_t si, uint32_t &resume,
+                                        double &fx, double &fy, double &z, uint32_t &inter)
+{
+    uint32_t cur = 0; // byte offset of the current record
+    while (cur < end) {
+        const double *d = reinterpret_cast<const double *>(nbase + cur);
+        const double cx = d[0], cy = d[1], thr = d[2];
+        const uint32_t *u = reinterpret_cast<const uint32_t *>(d + 3);
+        const double cnt = double(__uint_as_float(u[0]));
+        const uint32_t next = u[1], self = u[2];
+        const double dx = yi.x - cx, dy = yi.y - cy;
+        const double d2 = fma(dx, dx, dy * dy);
+        const bool act = cur >= resume;
+        bool tk = act & (d2 > thr);
+        if (kSelf) tk &= self != si;
+        const uint64_t take = ballot(tk);
+        const uint64_t rej = ballot(act & !tk);
+        inter += uint32_t(__builtin_popcountll(take));
+        if (tk) {
+            const double wgt = 1.0 / (1.0 + d2);
+            const double nw = cnt * wgt;
+            z += nw;
+            const double nw2 = nw * wgt;
+            fx = fma(nw2, dx, fx);
+            fy = fma(nw2, dy, fy);
+            resume = next;
+        }
+        cur = rej ? cur + kNodeBytes64 : next;
+    }
+}
+
+// T = float: the path (24-byte records); T = double: the fp64 variant.
+template <typename T>
 __global__ __launch_bounds__(kRepBlock) void repulsive_kernel(
-    const char *__restrict__ nodes, const float2 *__restrict__ ys, const uint32_t *__restrict__ perm,
-    Header *__restrict__ hdr, int64_t n, int self_test, float2 *__restrict__ frep, double *__restrict__ zpart,
+    const char *__restrict__ nodes, const vec2_t<T> *__restrict__ ys, const uint32_t *__restrict__ perm,
+    Header *__restrict__ hdr, int64_t n, int self_test, vec2_t<T> *__restrict__ frep, double *__restrict__ zpart,
     unsigned long long *__restrict__ ipart)
 {
     const uint32_t nb = gridDim.x;
@@ -106,27 +143,35 @@ __global__ __launch_bounds__(kRepBlock) void repulsive_kernel(
     const int64_t s64 = int64_t(lb) * kRepBlock + threadIdx.x;
     const bool valid = s64 < n;
     const uint32_t si = uint32_t(s64);
-    const float2 yi = valid ? ys[s64] : make_float2(0.0f, 0.0f);
+    const vec2_t<T> yi = valid ? ys[s64] : make_vec2(T(0), T(0));
     uint32_t resume = valid ? 0u : 0xffffffffu;
-    float fx = 0.0f, fy = 0.0f, z = 0.0f;
+    T fx = 0, fy = 0, z = 0;
     uint32_t total = uniform(hdr->nodes);
     const uint32_t cap = uint32_t(2 * n - 1);
     total = total < cap ? total : cap;
-    const uint32_t end = total * uint32_t(kNodeBytes);
+    const uint32_t end = total * uint32_t(sizeof(T) == 8 ? kNodeBytes64 : kNodeBytes);
 
     uint32_t inter = 0; // this wave's interactions (a launch has fewer than 2^32 per wave)
-    if (self_test) {
-        repulsive_walk<true>(nodes, end, yi, si, resume, fx, fy, z, inter);
+    if constexpr (sizeof(T) == 8) {
+        if (self_test)
+            repulsive_walk64<true>(nodes, end, yi, si, resume, fx, fy, z, inter);
+        else
+            repulsive_walk64<false>(nodes, end, yi, si, resume, fx, fy, z, inter);
     } else {
-        repulsive_walk<false>(nodes, end, yi, si, resume, fx, fy, z, inter);
+        if (self_test)
+            repulsive_walk<true>(nodes, end, yi, si, resume, fx, fy, z, inter);
+        else
+            repulsive_walk<false>(nodes, end, yi, si, resume, fx, fy, z, inter);
+    }
+    if (!self_test) {
         // each valid lane took its own leaf once, with weight 1
-        if (valid) z -= 1.0f;
+        if (valid) z -= T(1);
         inter -= uint32_t(__builtin_popcountll(ballot(valid)));
     }
 
     if (valid) {
         const uint32_t p = perm[si];
-        if (p < uint32_t(n)) frep[p] = make_float2(fx, fy);
+        if (p < uint32_t(n)) frep[p] = make_vec2(fx, fy);
     }
     // deterministic Z: wave -> block partial -> fixed-order sum in the last block
     double zw = wave_sum(double(z));
@@ -181,21 +226,25 @@ __global__ __launch_bounds__(kRepBlock) void repulsive_kernel(
     }
 }
 
-template <int G, bool kUpdate>
+__device__ inline float recip(float x) { return fast_rcp(x); }
+__device__ inline double recip(double x) { return 1.0 / x; }
+
+// T = float: the path's plain-CSR attraction; T = double: the fp64 variant
+template <int G, bool kUpdate, typename T>
 __global__ __launch_bounds__(256) void attract_kernel(
-    const int64_t *__restrict__ row_ptr, const int32_t *__restrict__ col, const float *__restrict__ val,
-    const float2 *__restrict__ ycopy, const float2 *__restrict__ frep, Header *__restrict__ hdr,
-    int64_t n, int64_t nnz, StepArgs a, float2 *__restrict__ Y, float2 *__restrict__ upd, float2 *__restrict__ gains,
-    float2 *__restrict__ grad)
+    const int64_t *__restrict__ row_ptr, const int32_t *__restrict__ col, const T *__restrict__ val,
+    const vec2_t<T> *__restrict__ ycopy, const vec2_t<T> *__restrict__ frep, Header *__restrict__ hdr,
+    int64_t n, int64_t nnz, StepArgsT<T> a, vec2_t<T> *__restrict__ Y, vec2_t<T> *__restrict__ upd,
+    vec2_t<T> *__restrict__ gains, vec2_t<T> *__restrict__ grad)
 {
     const int sub = lane_id() % G;
     constexpr int kRows = 256 / G;
-    const float inv_z = float(1.0 / hdr->Z);
+    const T inv_z = T(1.0 / hdr->Z);
     for (int64_t row0 = int64_t(blockIdx.x) * kRows; row0 < n; row0 += int64_t(gridDim.x) * kRows) {
         const int64_t i = row0 + threadIdx.x / G;
         const bool valid = i < n;
-        float fx = 0.0f, fy = 0.0f;
-        float2 yi = make_float2(0.0f, 0.0f);
+        T fx = 0, fy = 0;
+        vec2_t<T> yi = make_vec2(T(0), T(0));
         if (valid) {
             yi = ycopy[i];
             int64_t s = row_ptr[i], e = row_ptr[i + 1];
@@ -211,12 +260,12 @@ __global__ __launch_bounds__(256) void attract_kernel(
                     atomicOr(&hdr->flags, kErrRange);
                     continue;
                 }
-                const float p = __builtin_nontemporal_load(val + k);
-                const float2 yj = ycopy[j];
-                const float dx = yi.x - yj.x, dy = yi.y - yj.y;
-                const float pw = p * fast_rcp(1.0f + fmaf(dx, dx, dy * dy));
-                fx = fmaf(pw, dx, fx);
-                fy = fmaf(pw, dy, fy);
+                const T p = __builtin_nontemporal_load(val + k);
+                const vec2_t<T> yj = ycopy[j];
+                const T dx = yi.x - yj.x, dy = yi.y - yj.y;
+                const T pw = p * recip(T(1) + fma(dx, dx, dy * dy));
+                fx = fma(pw, dx, fx);
+                fy = fma(pw, dy, fy);
             }
         }
 #pragma unroll
@@ -225,19 +274,19 @@ __global__ __launch_bounds__(256) void attract_kernel(
             fy += __shfl_xor(fy, o, kWave);
         }
         if (valid && sub == 0) {
-            const float2 fr = frep[i];
-            const float gx = 4.0f * (a.alpha * fx - fr.x * inv_z);
-            const float gy = 4.0f * (a.alpha * fy - fr.y * inv_z);
-            if (grad) grad[i] = make_float2(gx, gy);
+            const vec2_t<T> fr = frep[i];
+            const T gx = T(4) * (a.alpha * fx - fr.x * inv_z);
+            const T gy = T(4) * (a.alpha * fy - fr.y * inv_z);
+            if (grad) grad[i] = make_vec2(gx, gy);
             if (kUpdate) {
-                float2 u = upd[i], gn = gains[i];
-                gn.x = (u.x * gx < 0.0f) ? gn.x + 0.2f : gn.x * 0.8f;
-                gn.y = (u.y * gy < 0.0f) ? gn.y + 0.2f : gn.y * 0.8f;
-                gn.x = fmaxf(gn.x, a.min_gain);
-                gn.y = fmaxf(gn.y, a.min_gain);
+                vec2_t<T> u = upd[i], gn = gains[i];
+                gn.x = (u.x * gx < T(0)) ? gn.x + T(0.2) : gn.x * T(0.8);
+                gn.y = (u.y * gy < T(0)) ? gn.y + T(0.2) : gn.y * T(0.8);
+                gn.x = vmax(gn.x, a.min_gain);
+                gn.y = vmax(gn.y, a.min_gain);
                 u.x = a.momentum * u.x - a.learning_rate * gn.x * gx;
                 u.y = a.momentum * u.y - a.learning_rate * gn.y * gy;
-                Y[i] = make_float2(yi.x + u.x, yi.y + u.y);
+                Y[i] = make_vec2(yi.x + u.x, yi.y + u.y);
                 upd[i] = u;
                 gains[i] = gn;
             }
@@ -246,32 +295,40 @@ __global__ __launch_bounds__(256) void attract_kernel(
 }
 
 // ------------------------------------------------------------------ launchers
-void launch_repulsive(int64_t n, bool self_test, void *ws, const Layout &L, hipStream_t st)
+template <typename T> void launch_repulsive(int64_t n, bool self_test, void *ws, const Layout &L, hipStream_t st)
 {
-    repulsive_kernel<<<unsigned(L.rep_blocks), kRepBlock, 0, st>>>(
-        at<char>(ws, L.nodes), at<float2>(ws, L.ys), at<uint32_t>(ws, L.idx0), at<Header>(ws, L.header), n,
-        self_test ? 1 : 0, at<float2>(ws, L.frep), at<double>(ws, L.zpart),
-        at<unsigned long long>(ws, L.ipart));
+    repulsive_kernel<T><<<unsigned(L.rep_blocks), kRepBlock, 0, st>>>(
+        at<char>(ws, L.nodes), at<vec2_t<T>>(ws, L.ys), at<uint32_t>(ws, L.idx0), at<Header>(ws, L.header), n,
+        self_test ? 1 : 0, at<vec2_t<T>>(ws, L.frep), at<double>(ws, L.zpart), at<unsigned long long>(ws, L.ipart));
 }
+template void launch_repulsive<float>(int64_t, bool, void *, const Layout &, hipStream_t);
+template void launch_repulsive<double>(int64_t, bool, void *, const Layout &, hipStream_t);
 
-void launch_attract(const int64_t *row_ptr, const int32_t *col, const float *val, int64_t n, int64_t nnz,
-                    const StepArgs &a, float *Y, float *upd, float *gains, float *grad, void *ws, const Layout &L,
-                    hipStream_t st)
+template <typename T>
+void launch_attract(const int64_t *row_ptr, const int32_t *col, const T *val, int64_t n, int64_t nnz,
+                    const StepArgsT<T> &a, T *Y, T *upd, T *gains, T *grad, void *ws, const Layout &L, hipStream_t st)
 {
     constexpr int G = 64; // one wave per row: rows hold ~100-200 entries
     int64_t blocks = (n + (256 / G) - 1) / (256 / G);
     if (blocks > 65535 * 8) blocks = 65535 * 8;
-    const float2 *yc = at<float2>(ws, L.ycopy);
-    const float2 *fr = at<float2>(ws, L.frep);
+    using V = vec2_t<T>;
+    const V *yc = at<V>(ws, L.ycopy);
+    const V *fr = at<V>(ws, L.frep);
     Header *hdr = at<Header>(ws, L.header);
     if (a.update)
-        attract_kernel<G, true><<<unsigned(blocks), 256, 0, st>>>(
-            row_ptr, col, val, yc, fr, hdr, n, nnz, a, reinterpret_cast<float2 *>(Y), reinterpret_cast<float2 *>(upd),
-            reinterpret_cast<float2 *>(gains), reinterpret_cast<float2 *>(grad));
+        attract_kernel<G, true, T><<<unsigned(blocks), 256, 0, st>>>(
+            row_ptr, col, val, yc, fr, hdr, n, nnz, a, reinterpret_cast<V *>(Y), reinterpret_cast<V *>(upd),
+            reinterpret_cast<V *>(gains), reinterpret_cast<V *>(grad));
     else
-        attract_kernel<G, false><<<unsigned(blocks), 256, 0, st>>>(row_ptr, col, val, yc, fr, hdr, n, nnz, a, nullptr,
-                                                                 nullptr, nullptr,
-                                                                 reinterpret_cast<float2 *>(grad));
+        attract_kernel<G, false, T><<<unsigned(blocks), 256, 0, st>>>(row_ptr, col, val, yc, fr, hdr, n, nnz, a,
+                                                                    nullptr, nullptr, nullptr,
+                                                                    reinterpret_cast<V *>(grad));
 }
+template void launch_attract<float>(const int64_t *, const int32_t *, const float *, int64_t, int64_t,
+                                    const StepArgsT<float> &, float *, float *, float *, float *, void *,
+                                    const Layout &, hipStream_t);
+template void launch_attract<double>(const int64_t *, const int32_t *, const double *, int64_t, int64_t,
+                                     const StepArgsT<double> &, double *, double *, double *, double *, void *,
+                                     const Layout &, hipStream_t);
 
 } // namespace bht

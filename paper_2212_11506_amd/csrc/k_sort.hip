@@ -18,26 +18,29 @@
 namespace bht {
 
 // ------------------------------------------------------------------ bbox
-__global__ __launch_bounds__(256) void bbox_partial_kernel(const float2 *__restrict__ Y, int64_t n,
-                                                           float *__restrict__ part)
+// T: float (the path) or double (the fp64 variant); each block writes
+// {min x, max x, min y, max y, non-finite flag} as 8 T.
+template <typename T>
+__global__ __launch_bounds__(256) void bbox_partial_kernel(const vec2_t<T> *__restrict__ Y, int64_t n,
+                                                           T *__restrict__ part)
 {
-    float mnx = INFINITY, mny = INFINITY, mxx = -INFINITY, mxy = -INFINITY;
+    T mnx = INFINITY, mny = INFINITY, mxx = -INFINITY, mxy = -INFINITY;
     uint32_t bad = 0;
     for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n;
          i += int64_t(gridDim.x) * blockDim.x) {
-        float2 y = Y[i];
+        const vec2_t<T> y = Y[i];
         bad |= !(isfinite(y.x) && isfinite(y.y));
-        mnx = fminf(mnx, y.x);
-        mxx = fmaxf(mxx, y.x);
-        mny = fminf(mny, y.y);
-        mxy = fmaxf(mxy, y.y);
+        mnx = vmin(mnx, y.x);
+        mxx = vmax(mxx, y.x);
+        mny = vmin(mny, y.y);
+        mxy = vmax(mxy, y.y);
     }
     mnx = wave_min(mnx);
     mny = wave_min(mny);
     mxx = wave_max(mxx);
     mxy = wave_max(mxy);
     bool anybad = ballot(bad != 0) != 0;
-    __shared__ float s[4][4];
+    __shared__ T s[4][4];
     __shared__ uint32_t sb[4];
     int w = threadIdx.x / kWave;
     if (lane_id() == 0) {
@@ -49,46 +52,47 @@ __global__ __launch_bounds__(256) void bbox_partial_kernel(const float2 *__restr
     }
     __syncthreads();
     if (threadIdx.x == 0) {
-        float r[4] = {s[0][0], s[0][1], s[0][2], s[0][3]};
+        T r[4] = {s[0][0], s[0][1], s[0][2], s[0][3]};
         uint32_t b = sb[0];
         for (int k = 1; k < 4; ++k) {
-            r[0] = fminf(r[0], s[k][0]);
-            r[1] = fmaxf(r[1], s[k][1]);
-            r[2] = fminf(r[2], s[k][2]);
-            r[3] = fmaxf(r[3], s[k][3]);
+            r[0] = vmin(r[0], s[k][0]);
+            r[1] = vmax(r[1], s[k][1]);
+            r[2] = vmin(r[2], s[k][2]);
+            r[3] = vmax(r[3], s[k][3]);
             b |= sb[k];
         }
-        float *o = part + 8 * blockIdx.x;
+        T *o = part + 8 * blockIdx.x;
         o[0] = r[0];
         o[1] = r[1];
         o[2] = r[2];
         o[3] = r[3];
-        reinterpret_cast<uint32_t *>(o)[4] = b;
+        reinterpret_cast<uint32_t *>(o + 4)[0] = b;
     }
 }
 
 // One block: finish the box, derive the quantisation parameters in fp64 and
 // reset the per-call counters and histograms.
-__global__ __launch_bounds__(256) void bbox_final_kernel(const float *__restrict__ part, int nparts,
+template <typename T>
+__global__ __launch_bounds__(256) void bbox_final_kernel(const T *__restrict__ part, int nparts,
                                                          Header *__restrict__ hdr,
                                                          uint32_t *__restrict__ hist)
 {
-    float mnx = INFINITY, mny = INFINITY, mxx = -INFINITY, mxy = -INFINITY;
+    T mnx = INFINITY, mny = INFINITY, mxx = -INFINITY, mxy = -INFINITY;
     uint32_t bad = 0;
     for (int k = threadIdx.x; k < nparts; k += blockDim.x) {
-        const float *p = part + 8 * k;
-        mnx = fminf(mnx, p[0]);
-        mxx = fmaxf(mxx, p[1]);
-        mny = fminf(mny, p[2]);
-        mxy = fmaxf(mxy, p[3]);
-        bad |= reinterpret_cast<const uint32_t *>(p)[4];
+        const T *p = part + 8 * k;
+        mnx = vmin(mnx, p[0]);
+        mxx = vmax(mxx, p[1]);
+        mny = vmin(mny, p[2]);
+        mxy = vmax(mxy, p[3]);
+        bad |= reinterpret_cast<const uint32_t *>(p + 4)[0];
     }
     mnx = wave_min(mnx);
     mny = wave_min(mny);
     mxx = wave_max(mxx);
     mxy = wave_max(mxy);
     bool anybad = ballot(bad != 0) != 0;
-    __shared__ float s[4][4];
+    __shared__ T s[4][4];
     __shared__ uint32_t sb[4];
     int w = threadIdx.x / kWave;
     if (lane_id() == 0) {
@@ -101,19 +105,19 @@ __global__ __launch_bounds__(256) void bbox_final_kernel(const float *__restrict
     for (int k = threadIdx.x; k < kHistCopies * kHistWords; k += blockDim.x) hist[k] = 0;
     __syncthreads();
     if (threadIdx.x == 0) {
-        float r[4] = {s[0][0], s[0][1], s[0][2], s[0][3]};
+        T r[4] = {s[0][0], s[0][1], s[0][2], s[0][3]};
         uint32_t b = sb[0];
         for (int k = 1; k < 4; ++k) {
-            r[0] = fminf(r[0], s[k][0]);
-            r[1] = fmaxf(r[1], s[k][1]);
-            r[2] = fminf(r[2], s[k][2]);
-            r[3] = fmaxf(r[3], s[k][3]);
+            r[0] = vmin(r[0], s[k][0]);
+            r[1] = vmax(r[1], s[k][1]);
+            r[2] = vmin(r[2], s[k][2]);
+            r[3] = vmax(r[3], s[k][3]);
             b |= sb[k];
         }
-        hdr->bmin[0] = r[0];
-        hdr->bmax[0] = r[1];
-        hdr->bmin[1] = r[2];
-        hdr->bmax[1] = r[3];
+        hdr->bmin[0] = float(r[0]);
+        hdr->bmax[0] = float(r[1]);
+        hdr->bmin[1] = float(r[2]);
+        hdr->bmax[1] = float(r[3]);
         // fp64, fixed operation order: the codes depend on these bits
         double c0 = (double(r[0]) + double(r[1])) * 0.5;
         double c1 = (double(r[2]) + double(r[3])) * 0.5;
@@ -137,7 +141,7 @@ __global__ __launch_bounds__(256) void bbox_final_kernel(const float *__restrict
 }
 
 // ------------------------------------------------------------------ Morton
-__device__ inline uint32_t quantise(float y, double yroot, double scale)
+template <typename T> __device__ inline uint32_t quantise(T y, double yroot, double scale)
 {
     double q = (double(y) - yroot) * scale;
     if (!(q > 0.0)) return 0u; // also catches NaN
@@ -160,9 +164,10 @@ __device__ inline uint64_t spread_even(uint32_t v)
 // Codes of one tile of points, the private copy of Y (in the caller's order,
 // or in a layout order when `rank` is given), the 8 global digit histograms; also clears the per-position tree masks and this tile's
 // look-back status words of every pass.
+template <typename T>
 __global__ __launch_bounds__(kSortBlock) void morton_kernel(
-    const float2 *__restrict__ Y, int64_t n, const Header *__restrict__ hdr,
-    uint64_t *__restrict__ codes, float2 *__restrict__ ycopy, const uint32_t *__restrict__ rank,
+    const vec2_t<T> *__restrict__ Y, int64_t n, const Header *__restrict__ hdr,
+    uint64_t *__restrict__ codes, vec2_t<T> *__restrict__ ycopy, const uint32_t *__restrict__ rank,
     uint32_t *__restrict__ hist, uint32_t *__restrict__ levelmask, uint32_t *__restrict__ status, int64_t tiles)
 {
     __shared__ uint32_t sh[kSortPasses * kRadix];
@@ -179,7 +184,7 @@ __global__ __launch_bounds__(kSortBlock) void morton_kernel(
     for (int r = 0; r < kSortItems; ++r) {
         int64_t i = base + r * kSortBlock + threadIdx.x;
         if (i < n) {
-            float2 y = Y[i];
+            const vec2_t<T> y = Y[i];
             if (rank) {
                 const uint32_t r = rank[i];
                 if (r < uint32_t(n)) ycopy[r] = y;
@@ -238,12 +243,12 @@ __device__ inline uint32_t peek(const uint32_t *p)
 
 static_assert(kSortBlock == kRadix, "thread t owns digit t in the scans and the look-back");
 
-template <bool kFirst, bool kLast>
+template <bool kFirst, bool kLast, typename T = float>
 __global__ __launch_bounds__(kSortBlock) void onesweep_kernel(
     const uint64_t *__restrict__ keys_in, const uint32_t *__restrict__ idx_in,
     uint64_t *__restrict__ keys_out, uint32_t *__restrict__ idx_out,
     uint32_t *__restrict__ status, const uint32_t *__restrict__ hist, Header *__restrict__ hdr,
-    int pass, int64_t n, const float2 *__restrict__ ysrc, float2 *__restrict__ ys)
+    int pass, int64_t n, const vec2_t<T> *__restrict__ ysrc, vec2_t<T> *__restrict__ ys)
 {
     constexpr int kWaves = kSortBlock / kWave;
     constexpr int kSeg = kWave * kSortItems; // keys per wave segment
@@ -372,7 +377,7 @@ __global__ __launch_bounds__(kSortBlock) void onesweep_kernel(
             keys_out[out] = k;
             uint32_t ix = s_idx[j];
             idx_out[out] = ix;
-            if (kLast) ys[out] = ix < uint32_t(n) ? ysrc[ix] : make_float2(0.0f, 0.0f);
+            if (kLast) ys[out] = ix < uint32_t(n) ? ysrc[ix] : make_vec2(T(0), T(0));
         } else {
             atomicOr(&hdr->flags, kErrRange);
         }
@@ -380,46 +385,55 @@ __global__ __launch_bounds__(kSortBlock) void onesweep_kernel(
 }
 
 // ------------------------------------------------------------------ launchers
-void launch_bbox(const float *Y, int64_t n, void *ws, const Layout &L, hipStream_t st)
+template <typename T> void launch_bbox(const T *Y, int64_t n, void *ws, const Layout &L, hipStream_t st)
 {
     int blocks = int((n + 255) / 256);
     if (blocks > kBBoxBlocks) blocks = kBBoxBlocks;
-    bbox_partial_kernel<<<blocks, 256, 0, st>>>(reinterpret_cast<const float2 *>(Y), n,
-                                                at<float>(ws, L.bbox_part));
-    bbox_final_kernel<<<1, 256, 0, st>>>(at<float>(ws, L.bbox_part), blocks,
-                                         at<Header>(ws, L.header), at<uint32_t>(ws, L.hist));
+    bbox_partial_kernel<T><<<blocks, 256, 0, st>>>(reinterpret_cast<const vec2_t<T> *>(Y), n,
+                                                   at<T>(ws, L.bbox_part));
+    bbox_final_kernel<T><<<1, 256, 0, st>>>(at<T>(ws, L.bbox_part), blocks, at<Header>(ws, L.header),
+                                            at<uint32_t>(ws, L.hist));
 }
+template void launch_bbox<float>(const float *, int64_t, void *, const Layout &, hipStream_t);
+template void launch_bbox<double>(const double *, int64_t, void *, const Layout &, hipStream_t);
 
-void launch_morton(const float *Y, int64_t n, const uint32_t *rank, void *ws, const Layout &L, hipStream_t st)
+template <typename T>
+void launch_morton(const T *Y, int64_t n, const uint32_t *rank, void *ws, const Layout &L, hipStream_t st)
 {
-    morton_kernel<<<unsigned(L.sort_tiles), kSortBlock, 0, st>>>(
-        reinterpret_cast<const float2 *>(Y), n, at<Header>(ws, L.header),
-        at<uint64_t>(ws, L.codes0), at<float2>(ws, L.ycopy), rank, at<uint32_t>(ws, L.hist),
-        at<uint32_t>(ws, L.levelmask), at<uint32_t>(ws, L.status), L.sort_tiles);
+    morton_kernel<T><<<unsigned(L.sort_tiles), kSortBlock, 0, st>>>(
+        reinterpret_cast<const vec2_t<T> *>(Y), n, at<Header>(ws, L.header), at<uint64_t>(ws, L.codes0),
+        at<vec2_t<T>>(ws, L.ycopy), rank, at<uint32_t>(ws, L.hist), at<uint32_t>(ws, L.levelmask),
+        at<uint32_t>(ws, L.status), L.sort_tiles);
 }
+template void launch_morton<float>(const float *, int64_t, const uint32_t *, void *, const Layout &, hipStream_t);
+template void launch_morton<double>(const double *, int64_t, const uint32_t *, void *, const Layout &,
+                                    hipStream_t);
 
-void launch_sort(int64_t n, const float *ysrc, void *ws, const Layout &L, hipStream_t st)
+// the last pass also gathers Y in sorted order (from `ysrc`, the private copy)
+template <typename T> void launch_sort(int64_t n, const T *ysrc, void *ws, const Layout &L, hipStream_t st)
 {
     uint64_t *k[2] = {at<uint64_t>(ws, L.codes0), at<uint64_t>(ws, L.codes1)};
     uint32_t *x[2] = {at<uint32_t>(ws, L.idx0), at<uint32_t>(ws, L.idx1)};
     Header *hdr = at<Header>(ws, L.header);
     const uint32_t *hist = at<uint32_t>(ws, L.hist);
-    const float2 *yc = reinterpret_cast<const float2 *>(ysrc);
-    float2 *ys = at<float2>(ws, L.ys);
+    const vec2_t<T> *yc = reinterpret_cast<const vec2_t<T> *>(ysrc);
+    vec2_t<T> *ys = at<vec2_t<T>>(ws, L.ys);
     for (int p = 0; p < kSortPasses; ++p) {
         uint32_t *status = at<uint32_t>(ws, L.status) + int64_t(p) * L.sort_tiles * kRadix;
         int src = p & 1, dst = src ^ 1;
         dim3 g(unsigned(L.sort_tiles));
         if (p == 0)
-            onesweep_kernel<true, false><<<g, kSortBlock, 0, st>>>(k[src], nullptr, k[dst], x[dst],
-                                                                  status, hist, hdr, p, n, yc, ys);
+            onesweep_kernel<true, false><<<g, kSortBlock, 0, st>>>(k[src], nullptr, k[dst], x[dst], status, hist,
+                                                                  hdr, p, n, nullptr, nullptr);
         else if (p == kSortPasses - 1)
-            onesweep_kernel<false, true><<<g, kSortBlock, 0, st>>>(k[src], x[src], k[dst], x[dst],
-                                                                  status, hist, hdr, p, n, yc, ys);
+            onesweep_kernel<false, true, T><<<g, kSortBlock, 0, st>>>(k[src], x[src], k[dst], x[dst], status,
+                                                                     hist, hdr, p, n, yc, ys);
         else
-            onesweep_kernel<false, false><<<g, kSortBlock, 0, st>>>(k[src], x[src], k[dst], x[dst],
-                                                                   status, hist, hdr, p, n, yc, ys);
+            onesweep_kernel<false, false><<<g, kSortBlock, 0, st>>>(k[src], x[src], k[dst], x[dst], status,
+                                                                   hist, hdr, p, n, nullptr, nullptr);
     }
 }
+template void launch_sort<float>(int64_t, const float *, void *, const Layout &, hipStream_t);
+template void launch_sort<double>(int64_t, const double *, void *, const Layout &, hipStream_t);
 
 } // namespace bht

@@ -255,12 +255,13 @@ struct ScanVal {
 
 __device__ inline ScanVal scan_add(ScanVal a, ScanVal b) { return {a.c + b.c, a.x + b.x, a.y + b.y}; }
 
+template <typename T>
 __device__ inline ScanVal element(const uint64_t *__restrict__ codes, const uint32_t *__restrict__ levelmask,
-                                  const float2 *__restrict__ ys, int64_t x, int64_t n, double c0, double c1)
+                                  const vec2_t<T> *__restrict__ ys, int64_t x, int64_t n, double c0, double c1)
 {
     const uint64_t k = codes[x];
     const uint32_t bucket = (x == 0 || codes[x - 1] != k) && x + 1 < n && codes[x + 1] == k ? 1u : 0u;
-    float2 y = ys[x];
+    const vec2_t<T> y = ys[x];
     return {1u + bucket + uint32_t(__popc(levelmask[x])), double(y.x) - c0, double(y.y) - c1};
 }
 
@@ -289,9 +290,10 @@ __device__ inline ScanVal block_scan_excl(ScanVal v, ScanVal *s_wave /*[4]*/, Sc
     return scan_add(off, prev);
 }
 
+template <typename T>
 __global__ __launch_bounds__(kScanBlock) void scan_reduce_kernel(
     const uint64_t *__restrict__ codes, const uint32_t *__restrict__ levelmask,
-    const float2 *__restrict__ ys, const Header *__restrict__ hdr, int64_t n,
+    const vec2_t<T> *__restrict__ ys, const Header *__restrict__ hdr, int64_t n,
     uint32_t *__restrict__ tile_cnt, double2 *__restrict__ tile_sum)
 {
     __shared__ ScanVal s_wave[4];
@@ -300,7 +302,7 @@ __global__ __launch_bounds__(kScanBlock) void scan_reduce_kernel(
     ScanVal acc{0, 0.0, 0.0};
     for (int k = 0; k < kScanItems; ++k) {
         int64_t x = first + k;
-        if (x < n) acc = scan_add(acc, element(codes, levelmask, ys, x, n, c0, c1));
+        if (x < n) acc = scan_add(acc, element<T>(codes, levelmask, ys, x, n, c0, c1));
     }
     ScanVal tot;
     block_scan_excl(acc, s_wave, &tot);
@@ -347,9 +349,10 @@ __global__ __launch_bounds__(kScanBlock) void scan_top_kernel(uint32_t *__restri
     }
 }
 
+template <typename T>
 __global__ __launch_bounds__(kScanBlock) void scan_down_kernel(
     const uint64_t *__restrict__ codes, const uint32_t *__restrict__ levelmask,
-    const float2 *__restrict__ ys, const Header *__restrict__ hdr, int64_t n,
+    const vec2_t<T> *__restrict__ ys, const Header *__restrict__ hdr, int64_t n,
     const uint32_t *__restrict__ tile_cnt, const double2 *__restrict__ tile_sum,
     uint32_t *__restrict__ base, double2 *__restrict__ psum)
 {
@@ -361,7 +364,7 @@ __global__ __launch_bounds__(kScanBlock) void scan_down_kernel(
 #pragma unroll
     for (int k = 0; k < kScanItems; ++k) {
         int64_t x = first + k;
-        loc[k] = (x < n) ? element(codes, levelmask, ys, x, n, c0, c1) : ScanVal{0, 0.0, 0.0};
+        loc[k] = (x < n) ? element<T>(codes, levelmask, ys, x, n, c0, c1) : ScanVal{0, 0.0, 0.0};
         acc = scan_add(acc, loc[k]);
     }
     ScanVal tot;
@@ -380,11 +383,11 @@ __global__ __launch_bounds__(kScanBlock) void scan_down_kernel(
 }
 
 // ------------------------------------------------------------------ 3. nodes
-__device__ inline float accept_threshold(double rspan, int L, double theta2)
+__device__ inline double accept_threshold(double rspan, int L, double theta2)
 {
     if (!(theta2 > 0.0)) return INFINITY;
     double side = ldexp(2.0 * rspan, -L);
-    return float(side * side / theta2);
+    return side * side / theta2;
 }
 
 // one node record, as three 8-byte stores (records are 8-byte aligned)
@@ -397,50 +400,70 @@ __device__ inline void store_node(char *__restrict__ nodes, int64_t pre, float2 
     r[2] = make_uint2(next, self);
 }
 
+// the fp64 variant's record: {com.x, com.y, thr, count, next, self}
+__device__ inline void store_node(char *__restrict__ nodes, int64_t pre, double2 com, float count, double thr,
+                                  uint32_t next, uint32_t self)
+{
+    double *d = reinterpret_cast<double *>(nodes + pre * kNodeBytes64);
+    d[0] = com.x;
+    d[1] = com.y;
+    d[2] = thr;
+    uint2 *r = reinterpret_cast<uint2 *>(d + 3);
+    r[0] = make_uint2(__float_as_uint(count), next);
+    r[1] = make_uint2(self, 0u);
+}
+
 // Centre of mass of the sorted points [b, e).  Small cells sum their points
 // directly (fp64, relative to the first point, so nothing cancels); larger
 // cells take the difference of the fp64 prefix sums, whose rounding error
 // divided by the count stays far below fp32 resolution.
 constexpr int64_t kDirectSum = 32;
 
-__device__ inline float2 centre_of_mass(const double2 *__restrict__ psum, const float2 *__restrict__ ys,
-                                        int64_t b, int64_t e, double c0, double c1)
+template <typename T>
+__device__ inline vec2_t<T> centre_of_mass(const double2 *__restrict__ psum, const vec2_t<T> *__restrict__ ys,
+                                           int64_t b, int64_t e, double c0, double c1)
 {
     const double inv = 1.0 / double(e - b);
     if (e - b <= kDirectSum) {
-        const float2 y0 = ys[b];
+        const vec2_t<T> y0 = ys[b];
         double sx = 0.0, sy = 0.0;
         for (int64_t s = b + 1; s < e; ++s) {
-            const float2 y = ys[s];
+            const vec2_t<T> y = ys[s];
             sx += double(y.x) - double(y0.x);
             sy += double(y.y) - double(y0.y);
         }
-        return make_float2(float(double(y0.x) + sx * inv), float(double(y0.y) + sy * inv));
+        return make_vec2(T(double(y0.x) + sx * inv), T(double(y0.y) + sy * inv));
     }
     double2 hi = psum[e], lo = psum[b];
-    return make_float2(float(c0 + (hi.x - lo.x) * inv), float(c1 + (hi.y - lo.y) * inv));
+    return make_vec2(T(c0 + (hi.x - lo.x) * inv), T(c1 + (hi.y - lo.y) * inv));
 }
 
+// T = float: 24-byte records with fp32 centres and thresholds; T = double
+// (the fp64 variant): 40-byte records with fp64 centres and thresholds.
+// theta2 is theta^2 in fp64 (from the float theta of the path, or the double
+// theta of the variant).
+template <typename T>
 __global__ __launch_bounds__(256) void tree_nodes_kernel(
     const uint64_t *__restrict__ codes, int64_t n, const uint32_t *__restrict__ levelmask,
     const uint32_t *__restrict__ split_b, const uint32_t *__restrict__ split_e,
-    const uint32_t *__restrict__ base, const double2 *__restrict__ psum, const float2 *__restrict__ ys,
-    Header *__restrict__ hdr, float theta, char *__restrict__ nodes, TreeDebug dbg)
+    const uint32_t *__restrict__ base, const double2 *__restrict__ psum, const vec2_t<T> *__restrict__ ys,
+    Header *__restrict__ hdr, double theta2, char *__restrict__ nodes, TreeDebug dbg)
 {
+    constexpr int kBytes = sizeof(T) == 8 ? kNodeBytes64 : kNodeBytes;
     int64_t x = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
     const double c0 = hdr->cent[0], c1 = hdr->cent[1], rspan = hdr->rspan;
     // acceptance thresholds of the cell levels 0..32 (32: buckets)
-    __shared__ float s_thr[33];
-    if (threadIdx.x < 33) s_thr[threadIdx.x] = accept_threshold(rspan, int(threadIdx.x), double(theta) * double(theta));
+    __shared__ T s_thr[33];
+    if (threadIdx.x < 33) s_thr[threadIdx.x] = T(accept_threshold(rspan, int(threadIdx.x), theta2));
     __syncthreads();
     if (x >= n) return;
-    auto emit = [&](int64_t pre, float2 com, int64_t b, int64_t e, int L, int64_t next, int kind) {
+    auto emit = [&](int64_t pre, vec2_t<T> com, int64_t b, int64_t e, int L, int64_t next, int kind) {
         if (pre >= 2 * n || next > 2 * n) { // only reachable from a corrupted sort
             atomicOr(&hdr->flags, kErrRange);
             return;
         }
         const bool single = kind == 2;
-        store_node(nodes, pre, com, float(e - b), single ? -1.0f : s_thr[L], uint32_t(next * kNodeBytes),
+        store_node(nodes, pre, com, float(e - b), single ? T(-1) : s_thr[L], uint32_t(next * kBytes),
                    single ? uint32_t(b) : kNodeCell);
         if (dbg.level) {
             dbg.level[pre] = uint8_t(L);
@@ -454,11 +477,11 @@ __global__ __launch_bounds__(256) void tree_nodes_kernel(
         int64_t b = split_b[x], e = split_e[x];
         int L = split_level(codes[x], codes[x + 1]);
         int64_t pre = base[b] + __popc(levelmask[b] & ((1u << L) - 1u));
-        emit(pre, centre_of_mass(psum, ys, b, e, c0, c1), b, e, L, base[e], 0);
+        emit(pre, centre_of_mass<T>(psum, ys, b, e, c0, c1), b, e, L, base[e], 0);
     }
     // (b) the root, when no split lies at level 0 (all points in one quadrant)
     if (x == 0 && quad_digit(codes[0], 0) == quad_digit(codes[n - 1], 0))
-        emit(0, centre_of_mass(psum, ys, 0, n, c0, c1), 0, n, 0, base[n], 0);
+        emit(0, centre_of_mass<T>(psum, ys, 0, n, c0, c1), 0, n, 0, base[n], 0);
     // (c) the leaf of point x, preceded by its bucket when a run of identical
     // codes starts at x (bucket members are leaves at level 33)
     if (x == 0 || codes[x - 1] != codes[x]) {
@@ -473,7 +496,7 @@ __global__ __launch_bounds__(256) void tree_nodes_kernel(
             }
             emit(pre, ys[x], x, e, lv + 1, pre + 1, 2);
         } else {
-            emit(pre, centre_of_mass(psum, ys, x, e, c0, c1), x, e, 32, base[e], 1);
+            emit(pre, centre_of_mass<T>(psum, ys, x, e, c0, c1), x, e, 32, base[e], 1);
             emit(pre + 1, ys[x], x, x + 1, 33, pre + 2, 2);
         }
     } else {
@@ -499,12 +522,13 @@ __global__ __launch_bounds__(256) void tree_unpack_kernel(const char *__restrict
 }
 
 // ------------------------------------------------------------------ launchers
-void launch_tree(int64_t n, float theta, void *ws, const Layout &L, const TreeDebug &dbg, hipStream_t st)
+template <typename T>
+void launch_tree(int64_t n, double theta2, void *ws, const Layout &L, const TreeDebug &dbg, hipStream_t st)
 {
     const uint64_t *codes = at<uint64_t>(ws, L.codes0);
     uint32_t *lm = at<uint32_t>(ws, L.levelmask);
     uint32_t *sb = at<uint32_t>(ws, L.split_b), *se = at<uint32_t>(ws, L.split_e);
-    const float2 *ys = at<float2>(ws, L.ys);
+    const vec2_t<T> *ys = at<vec2_t<T>>(ws, L.ys);
     Header *hdr = at<Header>(ws, L.header);
     uint32_t *base = at<uint32_t>(ws, L.base);
     double2 *psum = at<double2>(ws, L.psum);
@@ -512,12 +536,14 @@ void launch_tree(int64_t n, float theta, void *ws, const Layout &L, const TreeDe
     double2 *ts = at<double2>(ws, L.scan_sum);
     unsigned gn = unsigned((n + 255) / 256);
     tree_splits_kernel<<<gn, 256, 0, st>>>(codes, n, lm, sb, se);
-    scan_reduce_kernel<<<unsigned(L.scan_tiles), kScanBlock, 0, st>>>(codes, lm, ys, hdr, n, tc, ts);
+    scan_reduce_kernel<T><<<unsigned(L.scan_tiles), kScanBlock, 0, st>>>(codes, lm, ys, hdr, n, tc, ts);
     scan_top_kernel<<<1, kScanBlock, 0, st>>>(tc, ts, L.scan_tiles, n, base, psum, hdr);
-    scan_down_kernel<<<unsigned(L.scan_tiles), kScanBlock, 0, st>>>(codes, lm, ys, hdr, n, tc, ts, base, psum);
-    tree_nodes_kernel<<<gn, 256, 0, st>>>(codes, n, lm, sb, se, base, psum, ys, hdr, theta, at<char>(ws, L.nodes),
-                                          dbg);
+    scan_down_kernel<T><<<unsigned(L.scan_tiles), kScanBlock, 0, st>>>(codes, lm, ys, hdr, n, tc, ts, base, psum);
+    tree_nodes_kernel<T><<<gn, 256, 0, st>>>(codes, n, lm, sb, se, base, psum, ys, hdr, theta2,
+                                             at<char>(ws, L.nodes), dbg);
 }
+template void launch_tree<float>(int64_t, double, void *, const Layout &, const TreeDebug &, hipStream_t);
+template void launch_tree<double>(int64_t, double, void *, const Layout &, const TreeDebug &, hipStream_t);
 
 void launch_tree_unpack(int64_t n, void *ws, const Layout &L, float *summary, uint32_t *meta, hipStream_t st)
 {

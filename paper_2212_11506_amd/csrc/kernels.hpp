@@ -6,13 +6,14 @@
 
 namespace bht {
 
-struct StepArgs {
-    float alpha;         // exaggeration of the attractive term
-    float learning_rate; // eta
-    float momentum;      // mu
-    float min_gain;
-    int update;          // 0: gradient only
+template <typename T> struct StepArgsT {
+    T alpha;         // exaggeration of the attractive term
+    T learning_rate; // eta
+    T momentum;      // mu
+    T min_gain;
+    int update;      // 0: gradient only
 };
+using StepArgs = StepArgsT<float>;
 
 // Optional per-node exports of the tree (device arrays of at least 2n entries).
 struct TreeDebug {
@@ -60,12 +61,15 @@ struct TilePlan {
     int64_t entries = 0;
 };
 
-void launch_bbox(const float *Y, int64_t n, void *ws, const Layout &L, hipStream_t st);
+template <typename T> void launch_bbox(const T *Y, int64_t n, void *ws, const Layout &L, hipStream_t st);
 // rank (nullable): write the private copy of Y in that order instead of the caller's
-void launch_morton(const float *Y, int64_t n, const uint32_t *rank, void *ws, const Layout &L, hipStream_t st);
+template <typename T>
+void launch_morton(const T *Y, int64_t n, const uint32_t *rank, void *ws, const Layout &L, hipStream_t st);
 // ysrc: Y in the original order, gathered into Morton order by the last pass
-void launch_sort(int64_t n, const float *ysrc, void *ws, const Layout &L, hipStream_t st);
-void launch_tree(int64_t n, float theta, void *ws, const Layout &L, const TreeDebug &dbg, hipStream_t st);
+template <typename T> void launch_sort(int64_t n, const T *ysrc, void *ws, const Layout &L, hipStream_t st);
+// theta2 = theta^2 in fp64; T = float (the path) or double (the fp64 variant)
+template <typename T>
+void launch_tree(int64_t n, double theta2, void *ws, const Layout &L, const TreeDebug &dbg, hipStream_t st);
 // evaluation: exact Z and KL, results in the header's eval field
 void launch_z_exact(const float *Y, int64_t n, void *ws, const Layout &L, hipStream_t st);
 void launch_kl(const float *Y, const int64_t *row_ptr, const int32_t *col, const float *val, int64_t n,
@@ -75,10 +79,11 @@ void launch_tree_unpack(int64_t n, void *ws, const Layout &L, float *summary, ui
 // theta^2 <= 0.49: no point accepts a cell containing it, so the walk needs no
 // comparison with the lane's own leaf
 inline bool repulsive_self_test(float theta) { return double(theta) * double(theta) > 0.49; }
-void launch_repulsive(int64_t n, bool self_test, void *ws, const Layout &L, hipStream_t st);
-void launch_attract(const int64_t *row_ptr, const int32_t *col, const float *val, int64_t n, int64_t nnz,
-                    const StepArgs &a, float *Y, float *upd, float *gains, float *grad, void *ws, const Layout &L,
-                    hipStream_t st);
+inline bool repulsive_self_test(double theta) { return theta * theta > 0.49; }
+template <typename T> void launch_repulsive(int64_t n, bool self_test, void *ws, const Layout &L, hipStream_t st);
+template <typename T>
+void launch_attract(const int64_t *row_ptr, const int32_t *col, const T *val, int64_t n, int64_t nnz,
+                    const StepArgsT<T> &a, T *Y, T *upd, T *gains, T *grad, void *ws, const Layout &L, hipStream_t st);
 
 LayoutView layout_view(void *mem, int64_t n, int64_t nnz);
 // Builds the layout (synchronises the stream); fills *plan with the tile tables' sizes.
