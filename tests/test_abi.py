@@ -212,3 +212,33 @@ def test_affinities_rejects_bad_arguments():
     assert call(w=C.c_void_p(FAKE + 8)) == bh.BHTSNE_EWORKSPACE
     assert call(wb=lib.bhtsne_affinities_workspace_size(100, 10) - 1) == bh.BHTSNE_EWORKSPACE
     assert nnz.value == -1  # nothing reached the device
+
+
+def test_f64_workspace_size():
+    assert bh.workspace_size_f64(1, 0) == 0 and bh.workspace_size_f64(2, -1) == 0
+    assert bh.workspace_size_f64(1 << 24, 0) == 0 and bh.workspace_size_f64((1 << 24) - 1, 0) > 0
+    # fp64 copies of Y, F_rep and 40-byte node records: larger than the fp32 layout
+    a, b = bh.workspace_size(100000, 10**6), bh.workspace_size_f64(100000, 10**6)
+    assert a < b < a + 200 * 100000 and b % 256 == 0
+
+
+def test_f64_entry_points_reject_bad_arguments():
+    lib = bh.load_library()
+    P = bh._binding._Csr(100, 10, FAKE, FAKE, FAKE)
+    ws = C.c_void_p(FAKE)
+    f = C.c_void_p(FAKE)
+    z = C.c_double(0.0)
+    assert lib.bhtsne_gradient_f64(None, C.byref(P), 0.5, 1.0, f, None, ws, 1 << 40, None) == bh.BHTSNE_EINVAL
+    assert lib.bhtsne_gradient_f64(f, None, 0.5, 1.0, f, None, ws, 1 << 40, None) == bh.BHTSNE_EINVAL
+    for theta, alpha in [(-1.0, 1.0), (float("nan"), 1.0), (0.5, 0.0), (0.5, float("inf"))]:
+        assert lib.bhtsne_gradient_f64(f, C.byref(P), theta, alpha, f, C.byref(z), ws, 1 << 40,
+                                       None) == bh.BHTSNE_EINVAL
+    assert lib.bhtsne_gradient_f64(f, C.byref(P), 0.5, 1.0, f, None, None, 1 << 40, None) == bh.BHTSNE_EWORKSPACE
+    assert lib.bhtsne_gradient_f64(f, C.byref(P), 0.5, 1.0, f, None, ws, 16, None) == bh.BHTSNE_EWORKSPACE
+    for lr, mu, mg in [(0.0, 0.5, 0.01), (200.0, 1.0, 0.01), (200.0, -0.1, 0.01), (200.0, 0.5, -1.0)]:
+        assert lib.bhtsne_step_f64(f, C.byref(P), 0.5, 12.0, lr, mu, mg, f, f, None, None, ws, 1 << 40,
+                                   None) == bh.BHTSNE_EINVAL
+    assert lib.bhtsne_step_f64(f, C.byref(P), 0.5, 12.0, 200.0, 0.5, 0.01, None, f, None, None, ws, 1 << 40,
+                               None) == bh.BHTSNE_EINVAL
+    bad = bh._binding._Csr(1, 10, FAKE, FAKE, FAKE)
+    assert lib.bhtsne_gradient_f64(f, C.byref(bad), 0.5, 1.0, f, None, ws, 1 << 40, None) == bh.BHTSNE_EINVAL
