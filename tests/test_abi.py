@@ -242,3 +242,13 @@ def test_f64_entry_points_reject_bad_arguments():
                                None) == bh.BHTSNE_EINVAL
     bad = bh._binding._Csr(1, 10, FAKE, FAKE, FAKE)
     assert lib.bhtsne_gradient_f64(f, C.byref(bad), 0.5, 1.0, f, None, ws, 1 << 40, None) == bh.BHTSNE_EINVAL
+
+
+def test_bench_refuses_more_than_one_gpu():
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120, cwd=root)
+    assert r.returncode == 2 and "one GPU" in r.stderr
