@@ -329,3 +329,60 @@ def random_p(n: int, seed: int, k: int = 8) -> tuple:
     sym.sort_indices()
     return (sym.indptr.astype(np.int64), sym.indices.astype(np.int32),
             (sym.data / (2.0 * n)).astype(np.float32))
+
+
+def _ring_offsets(n: int, m: int, rng: Generator) -> np.ndarray:
+    """m distinct offsets in [1, n/2) (so i + o and i - o never meet mod n)."""
+    half = (n - 1) // 2
+    if m > half:
+        raise ValueError(f"{n} points cannot give {m} distinct ring offsets")
+    return np.sort(rng.choice(np.arange(1, half + 1, dtype=np.int64), size=m, replace=False)) \
+        if half < 1 << 20 else _distinct_draw(rng, 1, half + 1, m)
+
+
+def _distinct_draw(rng: Generator, lo: int, hi: int, m: int) -> np.ndarray:
+    out = np.empty(0, np.int64)
+    while out.size < m:
+        out = np.unique(np.concatenate([out, rng.integers(lo, hi, size=m)]))
+    return np.sort(rng.permutation(out)[:m])
+
+
+def ring_p(n: int, seed: int, m: int = 2) -> tuple:
+    """Symmetric CSR P for very large n, drawn in O(n m): row i lists the 2m
+    points i +- o_j (mod n) for m random distinct offsets, with
+    p_{i,i+o_j} = p_{i+o_j,i} = v_j and sum(P) = 1.  Index order and positions
+    are unrelated, as in a real dataset."""
+    rng = Generator(PCG64(SeedSequence(seed + 11)))
+    off = _ring_offsets(n, m, rng)
+    u = rng.uniform(0.1, 1.0, size=m)
+    v = u / (2.0 * n * u.sum())
+    d = np.concatenate([off, n - off])            # i + d (mod n) lists i +- o_j
+    dv = np.concatenate([v, v])
+    o = np.argsort(d)
+    d, dv = d[o], dv[o]
+    # row i in column order: the entries that wrap (d >= n - i) come first
+    i = np.arange(n, dtype=np.int32)               # n < 2^30: int32 sums stay exact
+    r = np.zeros(n, np.int32)
+    for dd in d:
+        r += i < n - dd
+    j = np.arange(2 * m, dtype=np.int32)[None, :] + r[:, None]
+    j[j >= 2 * m] -= 2 * m
+    cols = i[:, None] + d.astype(np.int32)[j]
+    cols[cols >= n] -= n
+    vals = dv.astype(np.float32)[j]
+    row_ptr = np.arange(0, 2 * m * n + 1, 2 * m, dtype=np.int64)
+    return row_ptr, cols.ravel(), vals.ravel()
+
+
+def ring_knn(n: int, k: int, seed: int) -> Knn:
+    """Neighbour lists for very large n, drawn in O(n k): row i lists the
+    points i + o_e (mod n) for k random distinct offsets in [1, n), so every
+    point is listed by exactly k rows; distances d ~ U(0, 3), ascending."""
+    t0 = time.time()
+    rng = Generator(PCG64(SeedSequence(seed + 13)))
+    off = rng.permutation(_distinct_draw(rng, 1, n, k))
+    idx = np.arange(n, dtype=np.int32)[:, None] + off.astype(np.int32)
+    idx[idx >= n] -= n
+    dist = rng.random((n, k), dtype=np.float32) * np.float32(3.0)
+    dist.sort(axis=1)
+    return Knn(n, k, idx, dist, np.zeros(n, np.int32), time.time() - t0)

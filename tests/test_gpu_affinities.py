@@ -152,20 +152,17 @@ def test_deterministic():
         assert np.array_equal(x, y)
 
 
-def test_full_size_1p3m_sampled():
-    """Workload 2 (1.3M points, k = 90): sampled rows of P against the oracle,
-    built from the conditional rows of those points and of every point that
-    lists them."""
-    kn = synth.make_knn(2, progress=say)
+def _check_sampled(kn, u, seed, tag):
+    """Sampled rows of P against the oracle, built from the conditional rows
+    of those points and of every point that lists them."""
     n = kn.n
-    say(f"[aff] workload 2: n={n}, lists drawn in {kn.gen_seconds:.0f}s")
-    rp, col, val, s2 = _gpu(kn.idx, kn.dist, 30.0)
+    rp, col, val, s2 = _gpu(kn.idx, kn.dist, u)
     assert abs(val.astype(np.float64).sum() - 1.0) < 1e-4
-    rng = np.random.default_rng(12)
+    rng = np.random.default_rng(seed)
     rows = np.sort(rng.choice(n, 400, replace=False))
     rr, ee = np.nonzero(np.isin(kn.idx, rows))  # row rr lists a sampled point at position ee
     need = np.unique(np.concatenate([rows, rr]))
-    os2, pc = A.conditional(kn.dist[need], 30.0)
+    os2, pc = A.conditional(kn.dist[need], u)
     pos = {int(r): t for t, r in enumerate(need)}
     rel = np.abs(s2[need] - os2) / os2
     assert rel.max() <= 1e-12
@@ -184,4 +181,21 @@ def test_full_size_1p3m_sampled():
         ref = np.array([want[int(j)] for j in cols]) / (2.0 * n)
         assert _ulps(val[rp[i]:rp[i + 1]], ref).max() <= 1
         checked += cols.size
-    say(f"[aff] workload 2: {checked} sampled entries match, sigma2 rel {rel.max():.1e}")
+    say(f"[aff] {tag}: {checked} sampled entries match, sigma2 rel {rel.max():.1e}")
+    return rp
+
+
+def test_full_size_1p3m_sampled():
+    """Workload 2 (1.3M points, k = 90), sampled rows."""
+    kn = synth.make_knn(2, progress=say)
+    say(f"[aff] workload 2: n={kn.n}, lists drawn in {kn.gen_seconds:.0f}s")
+    _check_sampled(kn, 30.0, 12, "workload 2")
+
+
+def test_maximum_size_sampled():
+    """n = 2^24 - 1, the largest point count the library accepts, with ring
+    neighbour lists (k = 8, every point listed by eight rows), sampled rows."""
+    kn = synth.ring_knn((1 << 24) - 1, 8, 21)
+    say(f"[aff] n={kn.n}: lists drawn in {kn.gen_seconds:.0f}s")
+    rp = _check_sampled(kn, 2.5, 22, "largest n")
+    assert rp[-1] <= 2 * 8 * kn.n

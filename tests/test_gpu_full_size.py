@@ -127,3 +127,71 @@ def test_full_run_kl_workload_1():
     say(f"[kl] workload 1: gpu {klg:.6f} oracle {klo:.6f} start {kl0:.6f}")
     assert klg < kl0 and klo < kl0
     assert abs(klg - klo) <= 0.01 * klo
+
+
+MAX_N = (1 << 24) - 1
+
+
+def _sample_estimate(vals, n):
+    """n * mean of a simple random sample, and its standard error (with the
+    finite-population correction)."""
+    m = vals.size
+    return n * vals.mean(), n * vals.std(ddof=1) / np.sqrt(m) * np.sqrt(1.0 - m / n)
+
+
+def test_maximum_size():
+    """n = 2^24 - 1, the largest point count the library accepts: N(0, 1)
+    positions and a ring P with four entries per row.  The layout path (the
+    bench's configuration), the plain CSR path and the fp64 variant each give
+    sampled gradients against the oracle's traversal of those points and the
+    exact node count.  The oracle's full pass at this size takes minutes, so
+    Z and the interaction total are checked against the estimate from a
+    traversal of 1M sampled points: within six standard errors."""
+    n = MAX_N
+    say(f"[max] n={n}: drawing Y and P")
+    Y32 = synth.random_y(n, 41)
+    rp, col, val = synth.ring_p(n, 41, m=2)
+    alpha = 12.0
+    sample = np.sort(np.random.default_rng(43).choice(n, size=SAMPLE, replace=False))
+    est = np.sort(np.random.default_rng(44).choice(n, size=1 << 20, replace=False))
+    dev = torch.device("cuda:0")
+    results = {}
+    Y = torch.from_numpy(Y32).to(dev)
+    P = bh.Csr.from_numpy(rp, col, val, device=dev)
+    ws = torch.empty(bh.workspace_size(n, col.size), dtype=torch.uint8, device=dev)
+    g, Z = bh.gradient(Y, P, 0.5, alpha, workspace=ws)
+    results["plain"] = (g.cpu().numpy()[sample].astype(np.float64), Z, bh.get_stats(ws))
+    lay = bh.Layout(P, Y, workspace=ws)
+    g, Z = bh.gradient(Y, lay, 0.5, alpha, workspace=ws)
+    results["layout"] = (g.cpu().numpy()[sample].astype(np.float64), Z, bh.get_stats(ws))
+    del lay, P, ws, g
+    gc.collect()
+    torch.cuda.empty_cache()
+    Y64 = Y.double()
+    P64 = bh.CsrF64.from_numpy(rp, col, val.astype(np.float64), device=dev)
+    ws = torch.empty(bh.workspace_size_f64(n, col.size), dtype=torch.uint8, device=dev)
+    g, Z = bh.gradient_f64(Y64, P64, 0.5, alpha, workspace=ws)
+    results["fp64"] = (g.cpu().numpy()[sample], Z, bh.get_stats(ws))
+    del Y, Y64, P64, ws, g
+    gc.collect()
+    torch.cuda.empty_cache()
+    say(f"[max] GPU gradients done; oracle tree and sampled traversals")
+    fattr = oracle.attractive(Y32, rp, col, val, rows=sample)
+    with oracle.State(Y32) as s:
+        t = s.tree()
+        bucket = t.kind == oracle.BUCKET
+        nodes_o = t.nodes + int((t.end[bucket].astype(np.int64) - t.begin[bucket]).sum())
+        del t
+        frep, _, _ = s.repulsive(0.5, points=sample)
+        _, zi, inter = s.repulsive(0.5, points=est)
+    z_est, z_se = _sample_estimate(zi, n)
+    i_est, i_se = _sample_estimate(inter.astype(np.float64), n)
+    for path, tol in [("layout", 1e-3), ("plain", 1e-3), ("fp64", 1e-9)]:
+        g, Z, stats = results[path]
+        err = rel_l2(g, 4.0 * (alpha * fattr - frep / Z))
+        say(f"[max] {path}: rel-L2 {err:.2e}, Z {Z:.6e} vs estimate {z_est:.6e} +- {z_se:.1e}, "
+            f"interactions {stats['interactions']} vs {i_est:.6e} +- {i_se:.1e}, nodes {stats['nodes']} vs {nodes_o}")
+        assert err <= tol, (path, err)
+        assert abs(Z - z_est) <= 6.0 * z_se, (path, Z, z_est, z_se)
+        assert abs(stats["interactions"] - i_est) <= 6.0 * i_se
+        assert stats["nodes"] == nodes_o
