@@ -1,6 +1,6 @@
 """GPU parity: the HIP path against the fp64 oracle on identical seeded inputs.
 
-Bars (per the method's definition and the tolerances of this build):
+Bars (from the method's definition and the tolerances the library promises):
   * bounding box, quantisation parameters, Morton codes, sorted order and the
     tree topology: bit-exact;
   * cell summaries: fp32 rounding of the oracle's fp64 centre of mass;
