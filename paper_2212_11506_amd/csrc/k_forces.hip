@@ -95,6 +95,19 @@ __device__ inline void repulsive_walk(const char *nbase, uint32_t end, float2 yi
     }
 }
 
+// 1/x in fp64 for x >= 1: the hardware's approximate reciprocal refined by
+// two Newton-Raphson steps r <- r + r (1 - x r), each of which squares the
+// relative error, so the result is within about an ulp of the quotient (the
+// IEEE division sequence costs twice the instructions); 1/inf stays 0.
+__device__ inline double recip(double x)
+{
+    double r = __builtin_amdgcn_rcp(x);
+    r = fma(r, fma(-x, r, 1.0), r);
+    r = fma(r, fma(-x, r, 1.0), r);
+    return x != __builtin_huge_val() ? r : 0.0;
+}
+__device__ inline float recip(float x) { return fast_rcp(x); }
+
 // The fp64 variant of the walk: the same visit order and acceptance test on
 // 40-byte records with fp64 centres and thresholds; the lanes that take a
 // node accumulate under the compiler's own EXEC mask.
@@ -118,7 +131,7 @@ __device__ inline void repulsive_walk64(const char *nbase, uint32_t end, double2
         const uint64_t rej = ballot(act & !tk);
         inter += uint32_t(__builtin_popcountll(take));
         if (tk) {
-            const double wgt = 1.0 / (1.0 + d2);
+            const double wgt = recip(1.0 + d2);
             const double nw = cnt * wgt;
             z += nw;
             const double nw2 = nw * wgt;
@@ -226,8 +239,6 @@ __global__ __launch_bounds__(kRepBlock) void repulsive_kernel(
     }
 }
 
-__device__ inline float recip(float x) { return fast_rcp(x); }
-__device__ inline double recip(double x) { return 1.0 / x; }
 
 // T = float: the path's plain-CSR attraction; T = double: the fp64 variant
 template <int G, bool kUpdate, typename T>
