@@ -28,6 +28,11 @@
  *    unless it must return a host value (Z or a node count), in which case it
  *    synchronises the stream first.  Calls that share a workspace must be
  *    ordered (same stream); distinct workspaces may run concurrently.
+ *  - The gradient and step calls (plain and layout forms, fp32 and fp64)
+ *    can be captured in a HIP graph when they return no host value: they
+ *    allocate nothing, enqueue no memset (counters are cleared by kernels),
+ *    and the layout forms' second stream joins the capture through the
+ *    fork and join events.  Each replay recomputes the whole step.
  *  - Every call returns a bhtsne_status code and never throws.  Arguments are
  *    checked on the host before anything is enqueued; nothing is enqueued when
  *    a check fails.  Conditions found on the GPU (a non-finite coordinate, a
