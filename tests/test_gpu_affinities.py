@@ -42,11 +42,11 @@ def _compare(idx, dist, u, tag):
     fin = np.isfinite(os2)
     assert np.array_equal(np.isfinite(s2), fin)
     rel = np.abs(s2[fin] - os2[fin]) / os2[fin]
-    assert rel.max() <= 1e-12, rel.max()
+    assert rel.max(initial=0.0) <= 1e-12, rel.max()
     assert np.array_equal(rp, orp), tag
     assert np.array_equal(col, ocol), tag
     u_ = _ulps(val, oval)
-    say(f"[aff] {tag}: nnz {rp[-1]}, sigma2 rel {rel.max():.1e}, values off by 1 ulp: {(u_ == 1).sum()}")
+    say(f"[aff] {tag}: nnz {rp[-1]}, sigma2 rel {rel.max(initial=0.0):.1e}, values off by 1 ulp: {(u_ == 1).sum()}")
     assert u_.max() <= 1
     return rp, col, val
 
@@ -83,6 +83,16 @@ def test_workload_1_70k():
 def test_neighbour_counts(k, u):
     idx, dist = _random_knn(700, k, seed=k)
     _compare(idx, dist, u, f"k={k}")
+
+
+@pytest.mark.parametrize("n,k,u", [(2, 1, 1.0), (2, 1, 2.0), (3, 2, 1.5), (5, 4, 3.0), (5, 4, 7.0)])
+def test_smallest_inputs(n, k, u):
+    """The fewest points the call accepts, and rows that list every other
+    point (k = n - 1); u >= k asks for more neighbours than a row has."""
+    kn = synth.ring_knn(n, k, 30 + n)
+    rp, col, val = _compare(kn.idx, kn.dist, u, f"n={n} k={k} u={u}")
+    assert rp[-1] == n * k  # every pair is listed both ways
+    assert abs(val.astype(np.float64).sum() - 1.0) < 1e-6
 
 
 def test_degenerate_rows():
