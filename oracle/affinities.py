@@ -65,7 +65,8 @@ def sigma2(dist: np.ndarray, u: float) -> np.ndarray:
     # grow the top of the interval until the perplexity there reaches u
     grow = ~flat & (_entropy(dp, hi) < target)
     while grow.any():
-        hi[grow] *= 2.0
+        with np.errstate(over="ignore"):  # hi = inf ends the row (u above reach)
+            hi[grow] *= 2.0
         grow &= np.isfinite(hi)
         idx = np.nonzero(grow)[0]
         if idx.size:
@@ -92,7 +93,7 @@ def conditional(dist: np.ndarray, u: float):
     s2 = sigma2(d, u)
     dd = d * d
     dp = dd - dd.min(axis=1, keepdims=True)
-    with np.errstate(divide="ignore", invalid="ignore"):
+    with np.errstate(divide="ignore", invalid="ignore", over="ignore"):  # a = inf gives w = 0
         a = np.where(np.isinf(s2)[:, None], 0.0, dp / (2.0 * s2[:, None]))
     w = np.exp(-a)
     return s2, w / w.sum(axis=1, keepdims=True)
