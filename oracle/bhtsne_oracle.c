@@ -15,7 +15,8 @@
  *   - centre of mass and count per cell      (Parallel Summarization) as direct sums
  *   - depth-first repulsive traversal with the acceptance test and the
  *     normaliser Z                           (Repulsive Force Computation; q_ij and Z)
- *   - CSR attractive forces                  (Attractive Force Computation; Algorithm 2)
+ *   - attractive forces over P's stored      (Gradient Descent, first sum of the split
+ *     entries                                 gradient; Attractive Force Computation)
  *   - gradient assembly                      (Gradient Descent, split-gradient equation)
  *   - gains / momentum update                (not specified by the paper; the standard
  *                                              t-SNE optimiser the experiments' defaults use)
@@ -405,25 +406,29 @@ void orc_state_repulsive(const orc_state *s, double theta, const int64_t *pts, i
 }
 
 /* ------------------------------------------------------------------ */
-/* Attractive Force Computation (CSR rows, 0-based columns).          */
-/* F_attr,i = sum_k val_k (1 + |y_i - y_col_k|^2)^-1 (y_i - y_col_k)  */
+/* Attractive forces: the first sum of the split gradient (Gradient    */
+/* Descent), F_attr,i = sum_{j != i} p_ij q_ij Z (y_i - y_j), where    */
+/* q_ij Z = (1 + |y_i - y_j|^2)^-1 is the Student-t kernel w_ij.  P is  */
+/* zero outside its stored entries, so only the stored entries of row  */
+/* i (0-based columns) contribute (Attractive Force Computation).      */
 /* ------------------------------------------------------------------ */
+static double orc_kernel_w(double dx, double dy) { return 1.0 / (1.0 + dx * dx + dy * dy); }
+
 void orc_attractive(const double *Y, const int64_t *row_ptr, const int32_t *col, const float *val,
                     const int64_t *rows, int64_t nrows, double *fattr)
 {
 #pragma omp parallel for schedule(dynamic, 256)
     for (int64_t k = 0; k < nrows; ++k) {
         int64_t i = rows ? rows[k] : k;
-        double yi0 = Y[2 * i], yi1 = Y[2 * i + 1], ax = 0.0, ay = 0.0;
+        double f[2] = {0.0, 0.0};
         for (int64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) {
             int64_t j = col[e];
-            double dx = yi0 - Y[2 * j], dy = yi1 - Y[2 * j + 1];
-            double pq = (double)val[e] / (1.0 + dx * dx + dy * dy);
-            ax += pq * dx;
-            ay += pq * dy;
+            double diff[2] = {Y[2 * i] - Y[2 * j], Y[2 * i + 1] - Y[2 * j + 1]};
+            double pw = (double)val[e] * orc_kernel_w(diff[0], diff[1]); /* p_ij q_ij Z */
+            for (int d = 0; d < 2; ++d) f[d] += pw * diff[d];
         }
-        fattr[2 * k] = ax;
-        fattr[2 * k + 1] = ay;
+        fattr[2 * k] = f[0];
+        fattr[2 * k + 1] = f[1];
     }
 }
 
@@ -490,18 +495,37 @@ void orc_step(double *y, int64_t n, const int64_t *row_ptr, const int32_t *col, 
 /* ------------------------------------------------------------------ */
 /* KL divergence (Gradient Descent, KL cost) with an exact Z.         */
 /* ------------------------------------------------------------------ */
+/* Z = sum over ordered pairs i != j of (1 + |y_i - y_j|^2)^-1 (the q_ij
+ * normaliser).  Each point's partial sum runs over j in index order; eight
+ * points are swept together, each with its own accumulator, which changes no
+ * rounding (the self pair adds an exact 0) and lets the compiler use vector
+ * divisions.  The partials are then summed in index order. */
+#define ORC_ZROWS 8
 double orc_z_exact(const double *Y, int64_t n)
 {
     double *part = (double *)calloc((size_t)n, 8);
-#pragma omp parallel for schedule(dynamic, 64)
-    for (int64_t i = 0; i < n; ++i) {
-        double yi0 = Y[2 * i], yi1 = Y[2 * i + 1], z = 0.0;
-        for (int64_t j = 0; j < n; ++j) {
-            if (j == i) continue;
-            double dx = yi0 - Y[2 * j], dy = yi1 - Y[2 * j + 1];
-            z += 1.0 / (1.0 + dx * dx + dy * dy);
+    const int64_t blocks = (n + ORC_ZROWS - 1) / ORC_ZROWS;
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t b = 0; b < blocks; ++b) {
+        double xi[ORC_ZROWS], yi[ORC_ZROWS], z[ORC_ZROWS];
+        int64_t id[ORC_ZROWS];
+        for (int r = 0; r < ORC_ZROWS; ++r) {
+            int64_t i = b * ORC_ZROWS + r;
+            id[r] = i < n ? i : -1; /* rows past the end compute and discard */
+            xi[r] = Y[2 * (i < n ? i : n - 1)];
+            yi[r] = Y[2 * (i < n ? i : n - 1) + 1];
+            z[r] = 0.0;
         }
-        part[i] = z;
+        for (int64_t j = 0; j < n; ++j) {
+            const double xj = Y[2 * j], yj = Y[2 * j + 1];
+            for (int r = 0; r < ORC_ZROWS; ++r) {
+                double dx = xi[r] - xj, dy = yi[r] - yj;
+                double w = 1.0 / (1.0 + dx * dx + dy * dy);
+                z[r] += (j == id[r]) ? 0.0 : w;
+            }
+        }
+        for (int r = 0; r < ORC_ZROWS; ++r)
+            if (id[r] >= 0) part[id[r]] = z[r];
     }
     double Z = orc_sum(part, n);
     free(part);
