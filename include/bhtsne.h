@@ -56,7 +56,7 @@ typedef enum {
     BHTSNE_EWORKSPACE = -2, /* workspace missing, misaligned or too small */
     BHTSNE_ENONFINITE = -3, /* Y held a NaN or an infinity */
     BHTSNE_EDEVICE = -4,    /* a HIP call failed or the GPU flagged an internal error */
-    BHTSNE_EINPUT = -5,     /* the GPU found invalid input data (bhtsne_affinities) */
+    BHTSNE_EINPUT = -5,     /* the GPU found invalid input data (bhtsne_affinities, bhtsne_layout_build) */
     BHTSNE_ECAPACITY = -6   /* output arrays too small; the required size is returned */
 } bhtsne_status;
 
@@ -95,6 +95,9 @@ typedef struct bhtsne_stats {
     double bbox[4];       /* min x, max x, min y, max y */
     double r_span;        /* half side of the square domain */
     uint32_t device_flags;/* 1 non-finite input, 2 look-back timeout, 4 index out of range */
+    int32_t max_depth;    /* deepest leaf of the quadtree: the level of the deepest single-point
+                             leaf, or 32 when identical points form a bucket (Quadtree Building:
+                             a cell at level L has side 2 r_span 2^-L) */
 } bhtsne_stats;
 
 /* Kernel phases timed by bhtsne_timing_*. */
@@ -172,7 +175,11 @@ size_t bhtsne_layout_size(int64_t n, int64_t nnz);
  *   out    host handle, filled on success.
  *   workspace  as for bhtsne_gradient (its contents are overwritten).
  * Synchronises the stream (the component search iterates until no label
- * changes).  Errors: BHTSNE_EINVAL, BHTSNE_EWORKSPACE, BHTSNE_EDEVICE. */
+ * changes).  P's row pointers are checked on the GPU before any entry is read
+ * (row_ptr[0] = 0, non-decreasing, row_ptr[n] = nnz); a violation returns
+ * BHTSNE_EINPUT and builds nothing.  Columns outside [0, n) are kept out of
+ * the copy.  Errors: BHTSNE_EINVAL, BHTSNE_EWORKSPACE, BHTSNE_EINPUT,
+ * BHTSNE_EDEVICE. */
 int bhtsne_layout_build(const bhtsne_csr *P, const float *Y, void *layout_mem, size_t layout_bytes,
                         bhtsne_layout *out, void *workspace, size_t workspace_bytes, hipStream_t stream);
 
@@ -226,8 +233,8 @@ int bhtsne_timing_read(bhtsne_timing *out, int reset);
  * bhtsne_kl: KL(P || Q) = sum over the stored entries with p_ij > 0 of
  * p_ij log(p_ij / q_ij), q_ij = (1 + |y_i - y_j|^2)^-1 / Z, for a given
  * Z > 0 (the exact one, or a step's Barnes-Hut estimate), in fp64 from the
- * fp32 inputs.  A column outside [0, n) is skipped and reported as
- * BHTSNE_EDEVICE. */
+ * fp32 inputs.  A column outside [0, n), or a row whose pointers reach outside
+ * [0, nnz), is skipped (clamped) and reported as BHTSNE_EDEVICE. */
 int bhtsne_z_exact(const float *Y, int64_t n, double *Z, void *workspace, size_t workspace_bytes,
                    hipStream_t stream);
 int bhtsne_kl(const float *Y, const bhtsne_csr *P, double Z, double *kl, void *workspace, size_t workspace_bytes,

@@ -39,7 +39,8 @@ class _Layout(C.Structure):
 
 class _Stats(C.Structure):
     _fields_ = [("Z", C.c_double), ("interactions", C.c_int64), ("nodes", C.c_int64),
-                ("bbox", C.c_double * 4), ("r_span", C.c_double), ("device_flags", C.c_uint32)]
+                ("bbox", C.c_double * 4), ("r_span", C.c_double), ("device_flags", C.c_uint32),
+                ("max_depth", C.c_int32)]
 
 
 class _Timing(C.Structure):
@@ -363,7 +364,7 @@ def get_stats(workspace: torch.Tensor, check: bool = True) -> dict:
     if check:
         _check(rc, "bhtsne_get_stats")
     return {"Z": s.Z, "interactions": s.interactions, "nodes": s.nodes, "bbox": list(s.bbox),
-            "r_span": s.r_span, "device_flags": s.device_flags, "status": rc}
+            "r_span": s.r_span, "device_flags": s.device_flags, "max_depth": s.max_depth, "status": rc}
 
 
 def timing_enable(on: bool = True):

@@ -498,8 +498,9 @@ int bhtsne_layout_build(const bhtsne_csr *P, const float *Y, void *layout_mem, s
     const Layout L = make_layout(P->n, P->nnz);
     const LayoutView lv = layout_view(layout_mem, P->n, P->nnz);
     TilePlan plan;
-    if (launch_layout_build(P->row_ptr, P->col, P->val, P->n, P->nnz, Y, lv, &plan, workspace, L, stream) != 0)
-        return BHTSNE_EDEVICE;
+    const int built = launch_layout_build(P->row_ptr, P->col, P->val, P->n, P->nnz, Y, lv, &plan, workspace, L, stream);
+    if (built == 1) return BHTSNE_EINPUT;
+    if (built != 0) return BHTSNE_EDEVICE;
     Header h;
     rc = read_header(workspace, &h, stream);
     if (rc != BHTSNE_OK) return rc;
@@ -560,6 +561,7 @@ int bhtsne_get_stats(const void *workspace, bhtsne_stats *out, hipStream_t strea
     out->bbox[3] = h.bmax[1];
     out->r_span = h.rspan;
     out->device_flags = h.flags;
+    out->max_depth = int32_t(h.max_depth);
     return flags_status(h.flags);
 }
 
@@ -609,7 +611,7 @@ const char *bhtsne_status_string(int status)
     case BHTSNE_EWORKSPACE: return "workspace missing, misaligned or too small";
     case BHTSNE_ENONFINITE: return "non-finite coordinate in Y";
     case BHTSNE_EDEVICE: return "HIP error or device-side consistency failure";
-    case BHTSNE_EINPUT: return "invalid neighbour lists (index out of range, repeated or the point itself) or a point listed by more than 4096 others";
+    case BHTSNE_EINPUT: return "invalid input data found on the GPU (malformed CSR row pointers, or neighbour lists with an index out of range, repeated or the point itself, or a point listed by more than 4096 others)";
     case BHTSNE_ECAPACITY: return "output arrays too small (the required entry count is returned)";
     default: return "unknown status";
     }
@@ -717,7 +719,7 @@ int bhtsne_kl(const float *Y, const bhtsne_csr *P, double Z, double *kl, void *w
     rc = check_ws(P->n, 0, workspace, workspace_bytes);
     if (rc != BHTSNE_OK) return rc;
     const Layout L = make_layout(P->n, 0);
-    launch_kl(Y, P->row_ptr, P->col, P->val, P->n, std::log(Z), workspace, L, stream);
+    launch_kl(Y, P->row_ptr, P->col, P->val, P->n, P->nnz, std::log(Z), workspace, L, stream);
     if (hipGetLastError() != hipSuccess) return BHTSNE_EDEVICE;
     Header h;
     rc = read_header(workspace, &h, stream);

@@ -86,7 +86,8 @@ struct Header {
     uint32_t ticket_rep;
     uint32_t attract_next; // next item of the persistent attractive kernel
     uint32_t ticket_eval;  // blocks done of an evaluation kernel (exact Z, KL)
-    uint32_t pad[4];
+    uint32_t max_depth;    // deepest leaf level of the last tree (32: a bucket of identical codes)
+    uint32_t pad[3];
     double eval;           // result of the last evaluation call
 };
 

@@ -119,15 +119,21 @@ constexpr int kKlLanes = 8;
 __global__ __launch_bounds__(kEvalBlock) void kl_kernel(const float2 *__restrict__ Y,
                                                        const int64_t *__restrict__ row_ptr,
                                                        const int32_t *__restrict__ col,
-                                                       const float *__restrict__ val, int64_t n, double log_z,
-                                                       double *__restrict__ part, Header *__restrict__ hdr)
+                                                       const float *__restrict__ val, int64_t n, int64_t nnz,
+                                                       double log_z, double *__restrict__ part,
+                                                       Header *__restrict__ hdr)
 {
     const int j = threadIdx.x % kKlLanes;
     const int64_t groups = int64_t(gridDim.x) * (kEvalBlock / kKlLanes);
     double mine = 0.0;
     for (int64_t i = int64_t(blockIdx.x) * (kEvalBlock / kKlLanes) + threadIdx.x / kKlLanes; i < n; i += groups) {
         const float2 yi = Y[i];
-        const int64_t e0 = row_ptr[i], e1 = row_ptr[i + 1];
+        int64_t e0 = row_ptr[i], e1 = row_ptr[i + 1];
+        if (e0 < 0 || e1 > nnz) { // malformed row: skip what lies outside the arrays
+            if (j == 0) atomicOr(&hdr->flags, kErrRange);
+            e0 = e0 < 0 ? 0 : e0;
+            e1 = e1 > nnz ? nnz : e1;
+        }
         double r = 0.0;
         for (int64_t e = e0 + j; e < e1; e += kKlLanes) {
             const double p = double(val[e]);
@@ -161,13 +167,13 @@ void launch_z_exact(const float *Y, int64_t n, void *ws, const Layout &L, hipStr
 }
 
 void launch_kl(const float *Y, const int64_t *row_ptr, const int32_t *col, const float *val, int64_t n,
-               double log_z, void *ws, const Layout &L, hipStream_t st)
+               int64_t nnz, double log_z, void *ws, const Layout &L, hipStream_t st)
 {
     Header *hdr = at<Header>(ws, L.header);
     eval_reset_kernel<<<1, 1, 0, st>>>(hdr);
     const int64_t want = (n + kEvalBlock / kKlLanes - 1) / (kEvalBlock / kKlLanes);
     const unsigned blocks = unsigned(want < kEvalMaxBlocks ? want : kEvalMaxBlocks);
-    kl_kernel<<<blocks, kEvalBlock, 0, st>>>(reinterpret_cast<const float2 *>(Y), row_ptr, col, val, n, log_z,
+    kl_kernel<<<blocks, kEvalBlock, 0, st>>>(reinterpret_cast<const float2 *>(Y), row_ptr, col, val, n, nnz, log_z,
                                              at<double>(ws, L.eval_part), hdr);
 }
 

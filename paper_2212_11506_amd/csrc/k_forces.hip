@@ -162,6 +162,10 @@ __global__ __launch_bounds__(kRepBlock) void repulsive_kernel(
     uint32_t total = uniform(hdr->nodes);
     const uint32_t cap = uint32_t(2 * n - 1);
     total = total < cap ? total : cap;
+    // Every record's next offset lies past the record (the tree kernel checks
+    // it and flags the call otherwise), so each visit advances and the walk
+    // ends after at most `total` visits.  A flagged tree is not walked.
+    if (uniform(hdr->flags) & (kErrLookback | kErrRange)) total = 0;
     const uint32_t end = total * uint32_t(sizeof(T) == 8 ? kNodeBytes64 : kNodeBytes);
 
     uint32_t inter = 0; // this wave's interactions (a launch has fewer than 2^32 per wave)

@@ -83,6 +83,22 @@ __global__ __launch_bounds__(256) void cc_compress_kernel(uint32_t *__restrict__
 
 __global__ void flag_clear_kernel(uint32_t *__restrict__ flag) { *flag = 0u; }
 
+// The row pointers alone, before any column or value is read: row_ptr[0] = 0,
+// non-decreasing, row_ptr[n] = nnz.  A violation latches kErrRange, and the
+// build stops before it reads P's entries.
+__global__ __launch_bounds__(256) void csr_check_kernel(const int64_t *__restrict__ row_ptr, int64_t n, int64_t nnz,
+                                                        Header *__restrict__ hdr)
+{
+    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i > n) return;
+    const int64_t a = row_ptr[i];
+    bool bad = a < 0 || a > nnz;
+    if (i == 0) bad |= a != 0;
+    if (i == n) bad |= a != nnz;
+    else bad |= row_ptr[i + 1] < a;
+    if (bad) atomicOr(&hdr->flags, kErrRange);
+}
+
 // ------------------------------------------------------------------ sort keys
 // key = component (26 bits) | top 38 bits of the Morton code (or the index).
 __global__ __launch_bounds__(256) void layout_keys_kernel(uint64_t *__restrict__ keys, const uint32_t *__restrict__ comp,
@@ -1071,6 +1087,13 @@ int launch_layout_build(const int64_t *row_ptr, const int32_t *col, const float 
     uint32_t *changed = at<uint32_t>(ws, L.split_e);
     const unsigned gn = unsigned((n + 255) / 256);
     const unsigned gw = unsigned((n + 3) / 4 < 65535 * 4 ? (n + 3) / 4 : 65535 * 4);
+    // validate the row pointers first: every later kernel indexes P's entries by them
+    flag_clear_kernel<<<1, 1, 0, st>>>(&hdr->flags);
+    csr_check_kernel<<<unsigned((n + 1 + 255) / 256), 256, 0, st>>>(row_ptr, n, nnz, hdr);
+    uint32_t flags = 0;
+    if (hipMemcpyAsync(&flags, &hdr->flags, 4, hipMemcpyDeviceToHost, st) != hipSuccess) return -1;
+    if (hipStreamSynchronize(st) != hipSuccess) return -1;
+    if (flags & kErrRange) return 1;
     cc_init_kernel<<<gn, 256, 0, st>>>(parent, n);
     for (int it = 0; it < 64; ++it) {
         flag_clear_kernel<<<1, 1, 0, st>>>(changed);

@@ -137,6 +137,7 @@ __global__ __launch_bounds__(256) void bbox_final_kernel(const T *__restrict__ p
         hdr->ticket_bbox = 0;
         hdr->ticket_rep = 0;
         hdr->attract_next = 0;
+        hdr->max_depth = 0;
     }
 }
 
@@ -149,16 +150,23 @@ template <typename T> __device__ inline uint32_t quantise(T y, double yroot, dou
     return uint32_t(q); // truncation toward zero
 }
 
-// Spread the 32 bits of v to the even positions of a 64-bit word.
-__device__ inline uint64_t spread_even(uint32_t v)
+// Interleaving by its definition: bit k of a grid coordinate goes to bit 2k
+// of its spread word, and dimension d is then shifted to bit 2k + d.  The
+// spread is taken a byte at a time: entry b of a 256-entry table holds byte b
+// with each bit k moved to bit 2k (built from that rule, one entry per
+// thread), and byte j of the coordinate lands at bit 16 j of the word.
+__device__ inline uint32_t spread_byte_rule(uint32_t b)
 {
-    uint64_t x = v;
-    x = (x | (x << 16)) & 0x0000ffff0000ffffull;
-    x = (x | (x << 8)) & 0x00ff00ff00ff00ffull;
-    x = (x | (x << 4)) & 0x0f0f0f0f0f0f0f0full;
-    x = (x | (x << 2)) & 0x3333333333333333ull;
-    x = (x | (x << 1)) & 0x5555555555555555ull;
-    return x;
+    uint32_t s = 0;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) s |= ((b >> k) & 1u) << (2 * k);
+    return s;
+}
+
+__device__ inline uint64_t spread_by_bytes(const uint16_t *__restrict__ tab, uint32_t v)
+{
+    return uint64_t(tab[v & 0xffu]) | (uint64_t(tab[(v >> 8) & 0xffu]) << 16) |
+           (uint64_t(tab[(v >> 16) & 0xffu]) << 32) | (uint64_t(tab[v >> 24]) << 48);
 }
 
 // Codes of one tile of points, the private copy of Y (in the caller's order,
@@ -171,6 +179,9 @@ __global__ __launch_bounds__(kSortBlock) void morton_kernel(
     uint32_t *__restrict__ hist, uint32_t *__restrict__ levelmask, uint32_t *__restrict__ status, int64_t tiles)
 {
     __shared__ uint32_t sh[kSortPasses * kRadix];
+    __shared__ uint16_t s_spread[256];
+    static_assert(kSortBlock == 256, "one spread-table entry per thread");
+    s_spread[threadIdx.x] = uint16_t(spread_byte_rule(threadIdx.x));
     for (int k = threadIdx.x; k < kSortPasses * kRadix; k += kSortBlock) sh[k] = 0;
     // clear this tile's look-back words of every pass
     for (int k = threadIdx.x; k < kSortPasses * kRadix; k += kSortBlock) {
@@ -191,8 +202,8 @@ __global__ __launch_bounds__(kSortBlock) void morton_kernel(
             } else {
                 ycopy[i] = y;
             }
-            uint64_t code = spread_even(quantise(y.x, yr0, sc)) |
-                            (spread_even(quantise(y.y, yr1, sc)) << 1);
+            uint64_t code = spread_by_bytes(s_spread, quantise(y.x, yr0, sc)) |
+                            (spread_by_bytes(s_spread, quantise(y.y, yr1, sc)) << 1);
             codes[i] = code;
             levelmask[i] = 0;
 #pragma unroll

@@ -454,11 +454,19 @@ __global__ __launch_bounds__(256) void tree_nodes_kernel(
     const double c0 = hdr->cent[0], c1 = hdr->cent[1], rspan = hdr->rspan;
     // acceptance thresholds of the cell levels 0..32 (32: buckets)
     __shared__ T s_thr[33];
+    // deepest leaf level of the block (a single point's level, 32 for a bucket)
+    __shared__ uint32_t s_depth;
     if (threadIdx.x < 33) s_thr[threadIdx.x] = T(accept_threshold(rspan, int(threadIdx.x), theta2));
+    if (threadIdx.x == 0) s_depth = 0;
     __syncthreads();
-    if (x >= n) return;
+    uint32_t depth = 0;
+    // A record's next offset must lie past the record itself: the repulsive
+    // walk advances to it, so this is what makes every walk end.  Records
+    // that break it (or fall outside the array) are only reachable from a
+    // corrupted sort; they are not written and the call is flagged, and the
+    // walk then does not start.
     auto emit = [&](int64_t pre, vec2_t<T> com, int64_t b, int64_t e, int L, int64_t next, int kind) {
-        if (pre >= 2 * n || next > 2 * n) { // only reachable from a corrupted sort
+        if (pre >= 2 * n || next > 2 * n || next <= pre) {
             atomicOr(&hdr->flags, kErrRange);
             return;
         }
@@ -472,36 +480,52 @@ __global__ __launch_bounds__(256) void tree_nodes_kernel(
             dbg.end[pre] = uint32_t(e);
         }
     };
-    // (a) the internal node owned by split x
-    if (x < n - 1 && split_e[x] != 0) {
-        int64_t b = split_b[x], e = split_e[x];
-        int L = split_level(codes[x], codes[x + 1]);
-        int64_t pre = base[b] + __popc(levelmask[b] & ((1u << L) - 1u));
-        emit(pre, centre_of_mass<T>(psum, ys, b, e, c0, c1), b, e, L, base[e], 0);
-    }
-    // (b) the root, when no split lies at level 0 (all points in one quadrant)
-    if (x == 0 && quad_digit(codes[0], 0) == quad_digit(codes[n - 1], 0))
-        emit(0, centre_of_mass<T>(psum, ys, 0, n, c0, c1), 0, n, 0, base[n], 0);
-    // (c) the leaf of point x, preceded by its bucket when a run of identical
-    // codes starts at x (bucket members are leaves at level 33)
-    if (x == 0 || codes[x - 1] != codes[x]) {
-        int64_t e = run_end(codes, x, n);
-        int64_t pre = base[x] + __popc(levelmask[x]);
-        if (e == x + 1) {
-            int lv = -1;
-            if (x > 0) lv = split_level(codes[x - 1], codes[x]);
-            if (x + 1 < n) {
-                int r = split_level(codes[x], codes[x + 1]);
-                lv = r > lv ? r : lv;
-            }
-            emit(pre, ys[x], x, e, lv + 1, pre + 1, 2);
-        } else {
-            emit(pre, centre_of_mass<T>(psum, ys, x, e, c0, c1), x, e, 32, base[e], 1);
-            emit(pre + 1, ys[x], x, x + 1, 33, pre + 2, 2);
+    if (x < n) {
+        // (a) the internal node owned by split x
+        if (x < n - 1 && split_e[x] != 0) {
+            int64_t b = split_b[x], e = split_e[x];
+            int L = split_level(codes[x], codes[x + 1]);
+            int64_t pre = base[b] + __popc(levelmask[b] & ((1u << L) - 1u));
+            emit(pre, centre_of_mass<T>(psum, ys, b, e, c0, c1), b, e, L, base[e], 0);
         }
-    } else {
-        emit(base[x], ys[x], x, x + 1, 33, int64_t(base[x]) + 1, 2); // a later member of a bucket
+        // (b) the root, when no split lies at level 0 (all points in one quadrant)
+        if (x == 0 && quad_digit(codes[0], 0) == quad_digit(codes[n - 1], 0))
+            emit(0, centre_of_mass<T>(psum, ys, 0, n, c0, c1), 0, n, 0, base[n], 0);
+        // (c) the leaf of point x, preceded by its bucket when a run of identical
+        // codes starts at x (bucket members are leaves at level 33)
+        if (x == 0 || codes[x - 1] != codes[x]) {
+            int64_t e = run_end(codes, x, n);
+            int64_t pre = base[x] + __popc(levelmask[x]);
+            if (e == x + 1) {
+                int lv = -1;
+                if (x > 0) lv = split_level(codes[x - 1], codes[x]);
+                if (x + 1 < n) {
+                    int r = split_level(codes[x], codes[x + 1]);
+                    lv = r > lv ? r : lv;
+                }
+                emit(pre, ys[x], x, e, lv + 1, pre + 1, 2);
+                depth = uint32_t(lv + 1);
+            } else {
+                emit(pre, centre_of_mass<T>(psum, ys, x, e, c0, c1), x, e, 32, base[e], 1);
+                emit(pre + 1, ys[x], x, x + 1, 33, pre + 2, 2);
+                depth = 32;
+            }
+        } else {
+            emit(base[x], ys[x], x, x + 1, 33, int64_t(base[x]) + 1, 2); // a later member of a bucket
+        }
     }
+    // the block's deepest leaf; the global maximum only takes the atomic when
+    // the block beats the value it reads (the value only grows, so a stale
+    // read costs at most an extra atomic), which keeps thousands of blocks
+    // from queueing on one address
+    for (int o = kWave / 2; o > 0; o >>= 1) {
+        const uint32_t v = uint32_t(__shfl_xor(int(depth), o, kWave));
+        depth = v > depth ? v : depth;
+    }
+    if (lane_id() == 0 && depth) atomicMax(&s_depth, depth);
+    __syncthreads();
+    if (threadIdx.x == 0 && s_depth > __hip_atomic_load(&hdr->max_depth, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+        atomicMax(&hdr->max_depth, s_depth);
 }
 
 // ------------------------------------------------------------------ debug export

@@ -73,7 +73,7 @@ void launch_tree(int64_t n, double theta2, void *ws, const Layout &L, const Tree
 // evaluation: exact Z and KL, results in the header's eval field
 void launch_z_exact(const float *Y, int64_t n, void *ws, const Layout &L, hipStream_t st);
 void launch_kl(const float *Y, const int64_t *row_ptr, const int32_t *col, const float *val, int64_t n,
-               double log_z, void *ws, const Layout &L, hipStream_t st);
+               int64_t nnz, double log_z, void *ws, const Layout &L, hipStream_t st);
 // the tree's records as {com, count, threshold} and documented meta words (both nullable)
 void launch_tree_unpack(int64_t n, void *ws, const Layout &L, float *summary, uint32_t *meta, hipStream_t st);
 // theta^2 <= 0.49: no point accepts a cell containing it, so the walk needs no
@@ -87,6 +87,7 @@ void launch_attract(const int64_t *row_ptr, const int32_t *col, const T *val, in
 
 LayoutView layout_view(void *mem, int64_t n, int64_t nnz);
 // Builds the layout (synchronises the stream); fills *plan with the tile tables' sizes.
+// Returns 0, 1 when P's row pointers are malformed (nothing else was read), or -1 on a HIP error.
 int launch_layout_build(const int64_t *row_ptr, const int32_t *col, const float *val, int64_t n, int64_t nnz,
                         const float *Y, const LayoutView &lv, TilePlan *plan, void *ws, const Layout &L,
                         hipStream_t st);

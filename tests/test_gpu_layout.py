@@ -141,9 +141,7 @@ def test_gradient_through_layout(case, theta):
     elif case == "hubs":
         y = synth.random_y(6000, seed=4, scale=2.0)
         rp, col, val = _hub_p(6000, seed=4)
-    else:
-        if theta == 0.0:
-            pytest.skip("exact O(n^2) oracle limited to small n")
+    else:  # late phase with 5% duplicates; at theta = 0 every pair is exact (4e8 pairs)
         inp = synth.make_inputs(4, n=20000)
         y, rp, col, val = inp.Y, inp.row_ptr, inp.col, inp.val
     say(f"[layout-grad] case={case} theta={theta} max row={np.diff(rp).max()}")
@@ -202,6 +200,41 @@ def test_layout_rejects_bad_handles():
     with pytest.raises(bh.BhtsneError) as e:
         bh.gradient(Y, lay, 0.5, 1.0)
     assert e.value.status == bh.BHTSNE_EINVAL
+
+
+@pytest.mark.parametrize("fault", ["first", "decreasing", "past_end", "short_end"])
+def test_layout_rejects_malformed_row_pointers(fault):
+    """The build checks P's row pointers on the GPU before it reads any entry
+    (row_ptr[0] = 0, non-decreasing, row_ptr[n] = nnz) and returns
+    BHTSNE_EINPUT; the KL evaluation clamps such rows to the arrays and reports
+    BHTSNE_EDEVICE."""
+    inp = synth.make_inputs(0)
+    rp = inp.row_ptr.copy()
+    n, nnz = inp.n, inp.nnz
+    if fault == "first":
+        rp[0] = 1
+    elif fault == "decreasing":
+        rp[n // 2] = rp[n // 2 + 1] + 7
+    elif fault == "past_end":
+        rp[n - 1] = nnz + 1000
+        rp[n] = nnz + 1000
+    else:
+        rp[n] = nnz - 5
+    say(f"[malformed] {fault}")
+    Y = torch.from_numpy(inp.Y).cuda()
+    P = bh.Csr.from_numpy(rp, inp.col, inp.val)
+    with pytest.raises(bh.BhtsneError) as e:
+        bh.Layout(P, Y)
+    assert e.value.status == bh.BHTSNE_EINPUT
+    if fault == "past_end":
+        with pytest.raises(bh.BhtsneError) as e:
+            bh.kl(Y, P, 1.0)
+        assert e.value.status == bh.BHTSNE_EDEVICE
+    # a well-formed P still builds and runs on the same workspace afterwards
+    ws = torch.empty(bh.workspace_size(n, nnz), dtype=torch.uint8, device="cuda")
+    good = bh.Layout(bh.Csr.from_numpy(inp.row_ptr, inp.col, inp.val), Y, workspace=ws)
+    g, Z = bh.gradient(Y, good, 0.5, 12.0, workspace=ws)
+    assert torch.isfinite(g).all() and Z > 0
 
 
 def test_tiled_copy_reproduces_p():

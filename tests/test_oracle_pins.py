@@ -62,6 +62,18 @@ def test_quantisation_extremes():
     assert abs(mid - 2**31) < 2**31 * 1e-6 + 2
 
 
+def test_quantisation_truncates_hand_worked_case(golden_dir):
+    """Reading R2 fixed by a hand-worked case whose truncated and rounded grid
+    values differ (tests/golden/quantisation_truncation.txt)."""
+    rows = [line.split() for line in _rows(os.path.join(golden_dir, "quantisation_truncation.txt"))]
+    y = np.array([[float(r[0]), float(r[1])] for r in rows], np.float32)
+    codes, grid, yrs = oracle.morton(y)
+    for k, r in enumerate(rows):
+        assert int(grid[k, 0]) == int(r[2], 16) and int(grid[k, 1]) == int(r[3], 16), k
+        assert int(codes[k]) == int(r[4], 16), k
+    assert yrs[0] == 0.0 and yrs[1] == 0.0
+
+
 def test_all_points_identical_gives_zero_codes():
     y = np.full((9, 2), 1.25, np.float32)
     codes, grid, yrs = oracle.morton(y)
