@@ -492,6 +492,98 @@ void orc_step(double *y, int64_t n, const int64_t *row_ptr, const int32_t *col, 
     if (!grad_out) free(g);
 }
 
+/* The same iteration as orc_step, with the wall time of each step of the
+ * paper's per-step tables (Evaluating performance improvements of
+ * individual steps): ms = {tree building (box, codes, sort, tree),
+ * summarization, attractive, repulsive (with Z), gradient and update}.
+ * stats (nullable) = {Z, interactions, nodes}. */
+void orc_step_timed(double *y, int64_t n, const int64_t *row_ptr, const int32_t *col, const float *val,
+                    double theta, double alpha, double eta, double mu, double min_gain, double *u, double *gains,
+                    double *stats, double *ms)
+{
+#ifdef _OPENMP
+#define ORC_NOW() omp_get_wtime()
+#else
+#define ORC_NOW() 0.0
+#endif
+    double t0 = ORC_NOW();
+    orc_state *s = (orc_state *)calloc(1, sizeof(orc_state));
+    s->n = n;
+    s->codes = (uint64_t *)malloc(8 * (size_t)n);
+    s->sorted = (uint64_t *)malloc(8 * (size_t)n);
+    s->perm = (uint32_t *)malloc(4 * (size_t)n);
+    s->inv = (uint32_t *)malloc(4 * (size_t)n);
+    orc_bbox(y, n, s->box);
+    orc_morton(y, n, s->codes, NULL, s->yrs);
+    orc_sort(s->codes, n, s->sorted, s->perm);
+    for (int64_t i = 0; i < n; ++i) s->inv[s->perm[i]] = (uint32_t)i;
+    int64_t cap = 2 * n;
+    s->level = (uint8_t *)malloc((size_t)cap);
+    s->kind = (uint8_t *)malloc((size_t)cap);
+    s->begin = (uint32_t *)malloc(4 * (size_t)cap);
+    s->end = (uint32_t *)malloc(4 * (size_t)cap);
+    s->parent = (int32_t *)malloc(4 * (size_t)cap);
+    s->nn = orc_tree(s->sorted, n, s->level, s->kind, s->begin, s->end, s->parent);
+    s->child_ptr = (int64_t *)calloc((size_t)s->nn + 1, 8);
+    s->child = (int32_t *)malloc(4 * (size_t)(s->nn > 1 ? s->nn - 1 : 1));
+    for (int64_t v = 1; v < s->nn; ++v) s->child_ptr[s->parent[v] + 1]++;
+    for (int64_t v = 0; v < s->nn; ++v) s->child_ptr[v + 1] += s->child_ptr[v];
+    int64_t *fill = (int64_t *)malloc(8 * (size_t)s->nn);
+    memcpy(fill, s->child_ptr, 8 * (size_t)s->nn);
+    for (int64_t v = 1; v < s->nn; ++v) s->child[fill[s->parent[v]]++] = (int32_t)v;
+    free(fill);
+    s->ys = (double *)malloc(16 * (size_t)n);
+    for (int64_t i = 0; i < n; ++i) {
+        s->ys[2 * i] = y[2 * (int64_t)s->perm[i]];
+        s->ys[2 * i + 1] = y[2 * (int64_t)s->perm[i] + 1];
+    }
+    double t1 = ORC_NOW();
+    s->count = (uint32_t *)malloc(4 * (size_t)s->nn);
+    s->com = (double *)malloc(16 * (size_t)s->nn);
+    orc_summaries(y, s->perm, s->nn, s->begin, s->end, s->com, s->count);
+    double t2 = ORC_NOW();
+    double *fattr = (double *)malloc(16 * (size_t)n);
+    orc_attractive(y, row_ptr, col, val, NULL, n, fattr);
+    double t3 = ORC_NOW();
+    double *frep = (double *)malloc(16 * (size_t)n);
+    double *zi = (double *)malloc(8 * (size_t)n);
+    int64_t *inter = (int64_t *)malloc(8 * (size_t)n);
+    orc_state_repulsive(s, theta, NULL, n, frep, zi, inter);
+    double Z = orc_sum(zi, n);
+    double t4 = ORC_NOW();
+    double *g = (double *)malloc(16 * (size_t)n);
+    for (int64_t i = 0; i < 2 * n; ++i) g[i] = 4.0 * (alpha * fattr[i] - frep[i] / Z);
+    orc_update(y, u, gains, g, 2 * n, eta, mu, min_gain);
+    double t5 = ORC_NOW();
+    if (stats) {
+        int64_t tot = 0;
+        for (int64_t i = 0; i < n; ++i) tot += inter[i];
+        stats[0] = Z;
+        stats[1] = (double)tot;
+        stats[2] = (double)s->nn;
+    }
+    if (ms) {
+        ms[0] = 1e3 * (t1 - t0);
+        ms[1] = 1e3 * (t2 - t1);
+        ms[2] = 1e3 * (t3 - t2);
+        ms[3] = 1e3 * (t4 - t3);
+        ms[4] = 1e3 * (t5 - t4);
+    }
+    free(g); free(frep); free(zi); free(inter); free(fattr);
+    orc_state_free(s);
+#undef ORC_NOW
+}
+
+/* Threads of the OpenMP loops (the results do not depend on it). */
+void orc_set_threads(int t)
+{
+#ifdef _OPENMP
+    if (t > 0) omp_set_num_threads(t);
+#else
+    (void)t;
+#endif
+}
+
 /* ------------------------------------------------------------------ */
 /* KL divergence (Gradient Descent, KL cost) with an exact Z.         */
 /* ------------------------------------------------------------------ */

@@ -216,6 +216,37 @@ def make_y(w: Workload, n: int, labels_perm: np.ndarray, sizes: np.ndarray,
     return y
 
 
+def make_y3(w: Workload, n: int, labels_perm: np.ndarray, sizes: np.ndarray,
+            rng: Generator) -> np.ndarray:
+    """A 3-D embedding with the workload's recipe: N(0, 1e-4 I) (early phase)
+    or clustered centres ~ U(-50, 50)^3 with spread sigma ~ U(0.1, 2) per
+    cluster (late phase), and the same share of duplicated points."""
+    if w.y_kind == "gauss":
+        return (rng.standard_normal((n, 3)) * 1e-2).astype(np.float32)
+    y = np.empty((n, 3), np.float64)
+    centres = rng.uniform(-50.0, 50.0, size=(sizes.size, 3))
+    sig = rng.uniform(0.1, 2.0, size=sizes.size)
+    off = 0
+    for c in range(sizes.size):
+        members = labels_perm[off:off + sizes[c]]
+        off += sizes[c]
+        y[members] = centres[c] + sig[c] * rng.standard_normal((members.size, 3))
+    y = y.astype(np.float32)
+    if w.dup_frac > 0.0:
+        ndup = int(round(w.dup_frac * n))
+        copier = rng.choice(n, size=ndup, replace=False)
+        mask = np.zeros(n, bool)
+        mask[copier] = True
+        off = 0
+        for c in range(sizes.size):
+            members = labels_perm[off:off + sizes[c]]
+            off += sizes[c]
+            cop, src = members[mask[members]], members[~mask[members]]
+            if cop.size and src.size:
+                y[cop] = y[src[rng.integers(0, src.size, size=cop.size)]]
+    return y
+
+
 @dataclasses.dataclass
 class Inputs:
     workload: Workload
@@ -237,9 +268,11 @@ class Inputs:
                                 ("col", self.col), ("val", self.val))}
 
 
-def make_inputs(cid: int, n: Optional[int] = None, progress=None, k: int = K_NEIGHBOURS) -> Inputs:
-    """Generate workload ``cid``; ``n`` overrides the size (cluster shares are kept)
-    and ``k`` the neighbours per row of the conditional matrix."""
+def make_inputs(cid: int, n: Optional[int] = None, progress=None, k: int = K_NEIGHBOURS,
+                dim: int = 2) -> Inputs:
+    """Generate workload ``cid``; ``n`` overrides the size (cluster shares are kept),
+    ``k`` the neighbours per row of the conditional matrix and ``dim`` (2 or 3)
+    the embedding's dimension (P does not depend on it)."""
     t0 = time.time()
     w = WORKLOADS[cid]
     n = w.n if n is None else int(n)
@@ -256,7 +289,7 @@ def make_inputs(cid: int, n: Optional[int] = None, progress=None, k: int = K_NEI
     row_ptr, col, val = make_p(w, n, perm, sizes, rng_nb, rng_w, k=k)
     if progress:
         progress(f"[synth] workload {cid}: nnz={col.size}, drawing Y")
-    Y = make_y(w, n, perm, sizes, rng_y)
+    Y = make_y(w, n, perm, sizes, rng_y) if dim == 2 else make_y3(w, n, perm, sizes, rng_y)
     return Inputs(w, n, Y, row_ptr, col, val, labels, time.time() - t0)
 
 
@@ -306,6 +339,16 @@ def random_y(n: int, seed: int, scale: float = 1.0, dups: int = 0) -> np.ndarray
     """Small free-form embeddings for edge-case tests (float32, n x 2)."""
     rng = Generator(PCG64(SeedSequence(seed)))
     y = (rng.standard_normal((n, 2)) * scale).astype(np.float32)
+    for _ in range(dups):
+        a, b = rng.integers(0, n, size=2)
+        y[a] = y[b]
+    return y
+
+
+def random_y3(n: int, seed: int, scale: float = 1.0, dups: int = 0) -> np.ndarray:
+    """Small free-form 3-D embeddings for edge-case tests (float32, n x 3)."""
+    rng = Generator(PCG64(SeedSequence(seed + 3)))
+    y = (rng.standard_normal((n, 3)) * scale).astype(np.float32)
     for _ in range(dups):
         a, b = rng.integers(0, n, size=2)
         y[a] = y[b]
