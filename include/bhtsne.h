@@ -326,6 +326,44 @@ int bhtsne_step_f64(double *Y, const bhtsne_csr_f64 *P, double theta, double exa
                     double momentum, double min_gain, double *update, double *gains, double *grad, double *Z,
                     void *workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* ------------------------------------------------------------------------
+ * Three-dimensional embeddings (the problem statement allows a two- or
+ * three-dimensional embedding; the paper works the method out in 2-D).  The
+ * same method, readings and phases as bhtsne_gradient / bhtsne_step on a
+ * plain CSR P, carried to three dimensions:
+ *  - the domain is the cube centred on the bounding box whose half side
+ *    r_span is the widest half extent;
+ *  - each coordinate is quantised to 21 bits, trunc((y - y_root) 2^20 /
+ *    r_span) clamped to [0, 2^21 - 1] (fp64), and bit k of dimension d goes
+ *    to bit 3k + d of a 63-bit Morton code;
+ *  - the compressed octree has cells at levels 0..21 of side 2 r_span 2^-L
+ *    (identical codes form a bucket at level 21, whose points follow it one
+ *    level below), and a cell stands in for its points when
+ *    side^2 < theta^2 |y_i - c|^2;
+ *  - Y, grad, update and gains are n x 3 float32, row-major (x, y, z).
+ * The workspace is bhtsne_workspace_size_3d bytes.  There is no locality
+ * layout for 3-D.  Arguments, checks, synchronisation and errors as the 2-D
+ * calls; bhtsne_get_stats reports Z, the interaction and node counts and
+ * max_depth (bbox and r_span hold x, y and the cube's r_span). */
+size_t bhtsne_workspace_size_3d(int64_t n, int64_t nnz);
+int bhtsne_gradient_3d(const float *Y, const bhtsne_csr *P, float theta, float exaggeration, float *grad,
+                       double *Z, void *workspace, size_t workspace_bytes, hipStream_t stream);
+int bhtsne_step_3d(float *Y, const bhtsne_csr *P, float theta, float exaggeration, float learning_rate,
+                   float momentum, float min_gain, float *update, float *gains, float *grad, double *Z,
+                   void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Test exports for 3-D embeddings, as bhtsne_debug_sort / bhtsne_debug_tree:
+ * params is a host array of 14 doubles {min x, max x, min y, max y, min z,
+ * max z, cent x, cent y, cent z, r_span, y_root x, y_root y, y_root z,
+ * scale}; summary is 2n x 4 floats {com x, com y, com z, count}, threshold
+ * 2n floats (-1 for single points, else side^2 / theta^2), meta as for
+ * bhtsne_debug_tree; bucket members sit at level 22. */
+int bhtsne_debug_sort_3d(const float *Y, int64_t n, uint64_t *codes, uint64_t *sorted_codes, uint32_t *perm,
+                         double *params, void *workspace, size_t workspace_bytes, hipStream_t stream);
+int bhtsne_debug_tree_3d(const float *Y, int64_t n, float theta, int64_t *n_nodes, uint8_t *level, uint8_t *kind,
+                         uint32_t *begin, uint32_t *end, float *summary, float *threshold, uint32_t *meta,
+                         void *workspace, size_t workspace_bytes, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

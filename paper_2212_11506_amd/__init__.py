@@ -21,20 +21,25 @@ from ._binding import (  # noqa: F401
     affinities,
     affinities_workspace_size,
     debug_sort,
+    debug_sort_3d,
     debug_tree,
+    debug_tree_3d,
     get_stats,
     gradient,
+    gradient_3d,
     gradient_f64,
     layout_size,
     library_path,
     load_library,
     status_string,
     step,
+    step_3d,
     step_f64,
     timing_enable,
     timing_phases,
     timing_read,
     workspace_size,
+    workspace_size_3d,
     workspace_size_f64,
     z_exact,
     kl,

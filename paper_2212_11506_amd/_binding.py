@@ -89,6 +89,13 @@ def load_library():
                                       C.c_double, vp, vp, vp, f64p, vp, C.c_size_t, vp]),
         "bhtsne_affinities": (C.c_int, [vp, vp, i64, C.c_int32, C.c_double, vp, vp, vp, i64,
                                         C.POINTER(C.c_int64), vp, vp, C.c_size_t, vp]),
+        "bhtsne_workspace_size_3d": (C.c_size_t, [i64, i64]),
+        "bhtsne_gradient_3d": (C.c_int, [vp, C.POINTER(_Csr), f32, f32, vp, f64p, vp, C.c_size_t, vp]),
+        "bhtsne_step_3d": (C.c_int, [vp, C.POINTER(_Csr), f32, f32, f32, f32, f32, vp, vp, vp, f64p, vp,
+                                     C.c_size_t, vp]),
+        "bhtsne_debug_sort_3d": (C.c_int, [vp, i64, vp, vp, vp, f64p, vp, C.c_size_t, vp]),
+        "bhtsne_debug_tree_3d": (C.c_int, [vp, i64, f32, C.POINTER(C.c_int64), vp, vp, vp, vp, vp, vp, vp, vp,
+                                           C.c_size_t, vp]),
         "bhtsne_debug_sort": (C.c_int, [vp, i64, vp, vp, vp, f64p, vp, C.c_size_t, vp]),
         "bhtsne_debug_tree": (C.c_int, [vp, i64, f32, C.POINTER(C.c_int64), vp, vp, vp, vp, vp, vp, vp,
                                         C.c_size_t, vp]),
@@ -418,3 +425,97 @@ def debug_tree(Y: torch.Tensor, theta: float = 0.5, workspace: Optional[torch.Te
     k = nn.value
     return {"nodes": k, "level": level[:k], "kind": kind[:k], "begin": begin[:k], "end": end[:k],
             "summary": summ[:k], "meta": meta[:k]}
+
+
+# ---------------------------------------------------------------- 3-D embeddings
+def workspace_size_3d(n: int, nnz: int) -> int:
+    return int(load_library().bhtsne_workspace_size_3d(int(n), int(nnz)))
+
+
+def _workspace_3d(n, nnz, ws):
+    need = workspace_size_3d(n, nnz)
+    if need == 0:
+        raise BhtsneError(BHTSNE_EINVAL, "workspace_size_3d")
+    if ws is None:
+        ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    return ws
+
+
+def _check_3d(Y):
+    if Y.dim() != 2 or Y.shape[1] != 3:
+        raise ValueError("a 3-D embedding is an n x 3 tensor")
+
+
+def gradient_3d(Y: torch.Tensor, P: "Csr", theta: float, exaggeration: float = 1.0,
+                grad: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                return_z: bool = True):
+    """bhtsne_gradient_3d: returns (grad n x 3, Z or None)."""
+    lib = load_library()
+    _check_3d(Y)
+    if grad is None:
+        grad = torch.empty_like(Y)
+    ws = _workspace_3d(P.n, P.nnz, workspace)
+    z = C.c_double(0.0)
+    rc = lib.bhtsne_gradient_3d(_ptr(Y, torch.float32, "Y"), P.struct, float(theta), float(exaggeration),
+                                _ptr(grad, torch.float32, "grad"), C.byref(z) if return_z else None,
+                                _ptr(ws, None, "workspace"), ws.numel(), _stream())
+    _check(rc, "bhtsne_gradient_3d")
+    return grad, (z.value if return_z else None)
+
+
+def step_3d(Y: torch.Tensor, P: "Csr", theta: float, exaggeration: float, learning_rate: float,
+            momentum: float, min_gain: float, update: torch.Tensor, gains: torch.Tensor,
+            grad: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+            return_z: bool = False):
+    """bhtsne_step_3d: one iteration in place on Y, update and gains (n x 3)."""
+    lib = load_library()
+    _check_3d(Y)
+    ws = _workspace_3d(P.n, P.nnz, workspace)
+    z = C.c_double(0.0)
+    rc = lib.bhtsne_step_3d(_ptr(Y, torch.float32, "Y"), P.struct, float(theta), float(exaggeration),
+                            float(learning_rate), float(momentum), float(min_gain),
+                            _ptr(update, torch.float32, "update"), _ptr(gains, torch.float32, "gains"),
+                            _ptr(grad, torch.float32, "grad"), C.byref(z) if return_z else None,
+                            _ptr(ws, None, "workspace"), ws.numel(), _stream())
+    _check(rc, "bhtsne_step_3d")
+    return z.value if return_z else None
+
+
+def debug_sort_3d(Y: torch.Tensor, workspace: Optional[torch.Tensor] = None):
+    """(codes, sorted_codes, perm, params[14]) of a 3-D embedding."""
+    lib = load_library()
+    _check_3d(Y)
+    n = Y.shape[0]
+    ws = _workspace_3d(n, 0, workspace)
+    codes = torch.empty(n, dtype=torch.int64, device=Y.device)
+    scodes = torch.empty(n, dtype=torch.int64, device=Y.device)
+    perm = torch.empty(n, dtype=torch.int32, device=Y.device)
+    params = (C.c_double * 14)()
+    rc = lib.bhtsne_debug_sort_3d(_ptr(Y, torch.float32, "Y"), n, _ptr(codes), _ptr(scodes), _ptr(perm),
+                                  params, _ptr(ws), ws.numel(), _stream())
+    _check(rc, "bhtsne_debug_sort_3d")
+    return codes, scodes, perm, list(params)
+
+
+def debug_tree_3d(Y: torch.Tensor, theta: float = 0.5, workspace: Optional[torch.Tensor] = None) -> dict:
+    """Octree arrays (pre-order) truncated to the node count, on the device."""
+    lib = load_library()
+    _check_3d(Y)
+    n = Y.shape[0]
+    ws = _workspace_3d(n, 0, workspace)
+    dev = Y.device
+    level = torch.empty(2 * n, dtype=torch.uint8, device=dev)
+    kind = torch.empty(2 * n, dtype=torch.uint8, device=dev)
+    begin = torch.empty(2 * n, dtype=torch.int32, device=dev)
+    end = torch.empty(2 * n, dtype=torch.int32, device=dev)
+    summ = torch.empty((2 * n, 4), dtype=torch.float32, device=dev)
+    thr = torch.empty(2 * n, dtype=torch.float32, device=dev)
+    meta = torch.empty(2 * n, dtype=torch.int32, device=dev)
+    nn = C.c_int64(0)
+    rc = lib.bhtsne_debug_tree_3d(_ptr(Y, torch.float32, "Y"), n, float(theta), C.byref(nn), _ptr(level),
+                                  _ptr(kind), _ptr(begin), _ptr(end), _ptr(summ), _ptr(thr), _ptr(meta),
+                                  _ptr(ws), ws.numel(), _stream())
+    _check(rc, "bhtsne_debug_tree_3d")
+    k = nn.value
+    return {"nodes": k, "level": level[:k], "kind": kind[:k], "begin": begin[:k], "end": end[:k],
+            "summary": summ[:k], "threshold": thr[:k], "meta": meta[:k]}

@@ -129,7 +129,7 @@ void build_sorted_tree(const float *Y, int64_t n, float theta, void *ws, const L
     }
     {
         PhaseTimer pt(BHTSNE_PHASE_TREE, st);
-        launch_tree<float>(n, double(theta) * double(theta), ws, L, dbg, st);
+        launch_tree<2, float>(n, double(theta) * double(theta), ws, L, dbg, st);
     }
 }
 
@@ -246,11 +246,11 @@ int run(float *Y, const bhtsne_csr *P, float theta, const StepArgs &a, float *up
     build_tree(Y, n, theta, nullptr, ws, L, TreeDebug{}, st);
     {
         PhaseTimer pt(BHTSNE_PHASE_REPULSIVE, st);
-        launch_repulsive<float>(n, repulsive_self_test(theta), ws, L, st);
+        launch_repulsive<2, float>(n, repulsive_self_test(theta), ws, L, st);
     }
     {
         PhaseTimer pt(BHTSNE_PHASE_ATTRACTIVE, st);
-        launch_attract(P->row_ptr, P->col, P->val, n, P->nnz, a, Y, update, gains, grad, ws, L, st);
+        launch_attract<2>(P->row_ptr, P->col, P->val, n, P->nnz, a, Y, update, gains, grad, ws, L, st);
     }
     return finish(Z, ws, st);
 }
@@ -306,15 +306,15 @@ int run64(double *Y, const bhtsne_csr_f64 *P, double theta, const StepArgsT<doub
     }
     {
         PhaseTimer pt(BHTSNE_PHASE_TREE, st);
-        launch_tree<double>(n, theta * theta, ws, L, TreeDebug{}, st);
+        launch_tree<2, double>(n, theta * theta, ws, L, TreeDebug{}, st);
     }
     {
         PhaseTimer pt(BHTSNE_PHASE_REPULSIVE, st);
-        launch_repulsive<double>(n, repulsive_self_test(theta), ws, L, st);
+        launch_repulsive<2, double>(n, repulsive_self_test(theta), ws, L, st);
     }
     {
         PhaseTimer pt(BHTSNE_PHASE_ATTRACTIVE, st);
-        launch_attract(P->row_ptr, P->col, P->val, n, P->nnz, a, Y, update, gains, grad, ws, L, st);
+        launch_attract<2>(P->row_ptr, P->col, P->val, n, P->nnz, a, Y, update, gains, grad, ws, L, st);
     }
     return finish(Z, ws, st);
 }
@@ -336,7 +336,7 @@ int run_layout(float *Y, const bhtsne_layout *lay, float theta, const StepArgs &
     }
     if (fork >= 2) {
         PhaseTimer pt(BHTSNE_PHASE_TREE, st);
-        launch_tree<float>(n, double(theta) * double(theta), ws, L, TreeDebug{}, st);
+        launch_tree<2, float>(n, double(theta) * double(theta), ws, L, TreeDebug{}, st);
     }
     Side *side = overlap_enabled() ? side_stream() : nullptr;
     std::unique_lock<std::mutex> lk;
@@ -358,17 +358,47 @@ int run_layout(float *Y, const bhtsne_layout *lay, float theta, const StepArgs &
     }
     if (fork < 2) {
         PhaseTimer pt(BHTSNE_PHASE_TREE, st);
-        launch_tree<float>(n, double(theta) * double(theta), ws, L, TreeDebug{}, st);
+        launch_tree<2, float>(n, double(theta) * double(theta), ws, L, TreeDebug{}, st);
     }
     {
         PhaseTimer pt(BHTSNE_PHASE_REPULSIVE, st);
-        launch_repulsive<float>(n, repulsive_self_test(theta), ws, L, st);
+        launch_repulsive<2, float>(n, repulsive_self_test(theta), ws, L, st);
     }
     if (side && hipStreamWaitEvent(st, side->join, 0) != hipSuccess) return BHTSNE_EDEVICE;
     if (lk.owns_lock()) lk.unlock();
     {
         PhaseTimer pt(BHTSNE_PHASE_UPDATE, st);
         launch_update(lv, n, a, Y, update, gains, grad, ws, L, st);
+    }
+    return finish(Z, ws, st);
+}
+
+// A 3-D embedding (plain CSR P): the same phases on a cube, 63-bit codes, an
+// octree with 32-byte records and three-component forces.
+int run3(float *Y, const bhtsne_csr *P, float theta, const StepArgs &a, float *update, float *gains, float *grad,
+         double *Z, void *ws, hipStream_t st)
+{
+    const int64_t n = P->n;
+    const Layout L = make_layout(n, P->nnz, 4, 3);
+    {
+        PhaseTimer pt(BHTSNE_PHASE_BBOX_MORTON, st);
+        launch_bbox_morton3(Y, n, ws, L, st);
+    }
+    {
+        PhaseTimer pt(BHTSNE_PHASE_SORT, st);
+        launch_sort_points(n, reinterpret_cast<const float3 *>(Y), ws, L, st);
+    }
+    {
+        PhaseTimer pt(BHTSNE_PHASE_TREE, st);
+        launch_tree<3, float>(n, double(theta) * double(theta), ws, L, TreeDebug{}, st);
+    }
+    {
+        PhaseTimer pt(BHTSNE_PHASE_REPULSIVE, st);
+        launch_repulsive<3, float>(n, repulsive_self_test3(theta), ws, L, st);
+    }
+    {
+        PhaseTimer pt(BHTSNE_PHASE_ATTRACTIVE, st);
+        launch_attract<3>(P->row_ptr, P->col, P->val, n, P->nnz, a, Y, update, gains, grad, ws, L, st);
     }
     return finish(Z, ws, st);
 }
@@ -476,6 +506,108 @@ int bhtsne_step_f64(double *Y, const bhtsne_csr_f64 *P, double theta, double exa
     if (rc != BHTSNE_OK) return rc;
     StepArgsT<double> a{exaggeration, learning_rate, momentum, min_gain, 1};
     return run64(Y, P, theta, a, update, gains, grad, Z, workspace, stream);
+}
+
+size_t bhtsne_workspace_size_3d(int64_t n, int64_t nnz)
+{
+    if (n < 2 || n > kMaxPoints || nnz < 0) return 0;
+    return make_layout(n, nnz, 4, 3).total;
+}
+
+static int check_ws_3d(int64_t n, int64_t nnz, void *ws, size_t bytes)
+{
+    if (!ws || !aligned(ws)) return BHTSNE_EWORKSPACE;
+    const size_t need = bhtsne_workspace_size_3d(n, nnz);
+    if (need == 0) return BHTSNE_EINVAL;
+    if (bytes < need) return BHTSNE_EWORKSPACE;
+    return BHTSNE_OK;
+}
+
+int bhtsne_gradient_3d(const float *Y, const bhtsne_csr *P, float theta, float exaggeration, float *grad, double *Z,
+                       void *workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    int rc = check_csr(P);
+    if (rc != BHTSNE_OK) return rc;
+    if (!Y || !grad) return BHTSNE_EINVAL;
+    if (!finite_f(theta) || theta < 0.0f) return BHTSNE_EINVAL;
+    if (!finite_f(exaggeration) || !(exaggeration > 0.0f)) return BHTSNE_EINVAL;
+    rc = check_ws_3d(P->n, P->nnz, workspace, workspace_bytes);
+    if (rc != BHTSNE_OK) return rc;
+    StepArgs a{exaggeration, 0.0f, 0.0f, 0.0f, 0};
+    return run3(const_cast<float *>(Y), P, theta, a, nullptr, nullptr, grad, Z, workspace, stream);
+}
+
+int bhtsne_step_3d(float *Y, const bhtsne_csr *P, float theta, float exaggeration, float learning_rate,
+                   float momentum, float min_gain, float *update, float *gains, float *grad, double *Z,
+                   void *workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    int rc = check_csr(P);
+    if (rc != BHTSNE_OK) return rc;
+    if (!Y || !update || !gains) return BHTSNE_EINVAL;
+    rc = check_step_args(theta, exaggeration, learning_rate, momentum, min_gain);
+    if (rc != BHTSNE_OK) return rc;
+    rc = check_ws_3d(P->n, P->nnz, workspace, workspace_bytes);
+    if (rc != BHTSNE_OK) return rc;
+    StepArgs a{exaggeration, learning_rate, momentum, min_gain, 1};
+    return run3(Y, P, theta, a, update, gains, grad, Z, workspace, stream);
+}
+
+int bhtsne_debug_sort_3d(const float *Y, int64_t n, uint64_t *codes, uint64_t *sorted_codes, uint32_t *perm,
+                         double *params, void *workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    if (!Y || n < 2 || n > kMaxPoints) return BHTSNE_EINVAL;
+    int rc = check_ws_3d(n, 0, workspace, workspace_bytes);
+    if (rc != BHTSNE_OK) return rc;
+    const Layout L = make_layout(n, 0, 4, 3);
+    launch_bbox_morton3(Y, n, workspace, L, stream);
+    if (codes && hipMemcpyAsync(codes, at<void>(workspace, L.codes0), 8 * size_t(n), hipMemcpyDeviceToDevice,
+                                stream) != hipSuccess)
+        return BHTSNE_EDEVICE;
+    launch_sort_points(n, reinterpret_cast<const float3 *>(Y), workspace, L, stream);
+    if (sorted_codes && hipMemcpyAsync(sorted_codes, at<void>(workspace, L.codes0), 8 * size_t(n),
+                                       hipMemcpyDeviceToDevice, stream) != hipSuccess)
+        return BHTSNE_EDEVICE;
+    if (perm && hipMemcpyAsync(perm, at<void>(workspace, L.idx0), 4 * size_t(n), hipMemcpyDeviceToDevice,
+                               stream) != hipSuccess)
+        return BHTSNE_EDEVICE;
+    if (hipGetLastError() != hipSuccess) return BHTSNE_EDEVICE;
+    if (params) {
+        Header h;
+        rc = read_header(workspace, &h, stream);
+        if (rc != BHTSNE_OK) return rc;
+        const double p[14] = {h.bmin[0], h.bmax[0], h.bmin[1],  h.bmax[1],  h.bmin[2],  h.bmax[2],  h.cent[0],
+                              h.cent[1], h.cent[2], h.rspan,    h.yroot[0], h.yroot[1], h.yroot[2], h.scale};
+        std::memcpy(params, p, sizeof(p));
+        return flags_status(h.flags);
+    }
+    return BHTSNE_OK;
+}
+
+int bhtsne_debug_tree_3d(const float *Y, int64_t n, float theta, int64_t *n_nodes, uint8_t *level, uint8_t *kind,
+                         uint32_t *begin, uint32_t *end, float *summary, float *threshold, uint32_t *meta,
+                         void *workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    if (!Y || !n_nodes || n < 2 || n > kMaxPoints) return BHTSNE_EINVAL;
+    if (!finite_f(theta) || theta < 0.0f) return BHTSNE_EINVAL;
+    if ((level || kind || begin || end) && !(level && kind && begin && end)) return BHTSNE_EINVAL;
+    int rc = check_ws_3d(n, 0, workspace, workspace_bytes);
+    if (rc != BHTSNE_OK) return rc;
+    const Layout L = make_layout(n, 0, 4, 3);
+    TreeDebug dbg;
+    dbg.level = level;
+    dbg.kind = kind;
+    dbg.begin = begin;
+    dbg.end = end;
+    launch_bbox_morton3(Y, n, workspace, L, stream);
+    launch_sort_points(n, reinterpret_cast<const float3 *>(Y), workspace, L, stream);
+    launch_tree<3, float>(n, double(theta) * double(theta), workspace, L, dbg, stream);
+    if (summary || threshold || meta) launch_tree_unpack3(n, workspace, L, summary, threshold, meta, stream);
+    if (hipGetLastError() != hipSuccess) return BHTSNE_EDEVICE;
+    Header h;
+    rc = read_header(workspace, &h, stream);
+    if (rc != BHTSNE_OK) return rc;
+    *n_nodes = int64_t(h.nodes);
+    return flags_status(h.flags);
 }
 
 size_t bhtsne_layout_size(int64_t n, int64_t nnz)

@@ -43,6 +43,10 @@ constexpr int kNodeBytes = 24;
 // The fp64 variant's record: {com.x, com.y, thr (fp64), count (fp32), next,
 // self, padding}, 40 bytes.
 constexpr int kNodeBytes64 = 40;
+// A 3-D embedding's record: {com.x, com.y, com.z, count, thr, next, self,
+// padding}, 32 bytes: one scalar load of eight dwords.
+constexpr int kNodeBytes3 = 32;
+template <int D, typename T> constexpr int node_bytes() { return D == 3 ? kNodeBytes3 : (sizeof(T) == 8 ? kNodeBytes64 : kNodeBytes); }
 constexpr uint32_t kNodeCell = 0xFFFFFFFFu;
 // the 2n - 1 records end below 2^32 bytes
 constexpr int64_t kMaxPoints = (int64_t(1) << 24) - 1;
@@ -72,11 +76,11 @@ constexpr uint32_t kErrRange = 4u;
 
 // Per-call scalars, written by the kernels, read back by the host on demand.
 struct Header {
-    float bmin[2], bmax[2];   // bounding box (exact fp32 min/max)
-    double cent[2];           // box centre
+    float bmin[3], bmax[3];   // bounding box (exact fp32 min/max; z only for 3-D embeddings)
+    double cent[3];           // box centre
     double rspan;             // half of the widest extent
-    double yroot[2];          // lower-left corner of the square domain
-    double scale;             // 2^31 / r_span (0 when r_span == 0)
+    double yroot[3];          // lower corner of the square (cube) domain
+    double scale;             // 2^31 / r_span (2-D) or 2^20 / r_span (3-D); 0 when r_span == 0
     double Z;                 // normaliser of the last call
     unsigned long long interactions;
     uint32_t nodes;           // node count of the last tree
@@ -106,8 +110,9 @@ inline int64_t rep_blocks_for(int64_t n)
 }
 
 // `fbytes` is the size of a coordinate: 4 (fp32 path) or 8 (fp64 variant,
-// which sizes the copies of Y, the node records and F_rep for fp64)
-inline Layout make_layout(int64_t n, int64_t nnz, int fbytes = 4)
+// which sizes the copies of Y, the node records and F_rep for fp64); `dim`
+// the embedding's dimension (2, or 3 for the 3-D calls, fp32 only)
+inline Layout make_layout(int64_t n, int64_t nnz, int fbytes = 4, int dim = 2)
 {
     Layout L{};
     L.n = n;
@@ -130,22 +135,22 @@ inline Layout make_layout(int64_t n, int64_t nnz, int fbytes = 4)
     L.idx1 = take(4 * size_t(n));
     L.status = take(4 * size_t(kSortPasses) * kRadix * size_t(L.sort_tiles));
     // + one LDS segment of padding: segment loads past the last point stay inside the buffer
-    L.ycopy = take(2 * size_t(fbytes) * size_t(n + kYPad));
-    L.ys = take(2 * size_t(fbytes) * size_t(n));
+    L.ycopy = take(size_t(dim) * size_t(fbytes) * size_t(n + kYPad));
+    L.ys = take(size_t(dim) * size_t(fbytes) * size_t(n));
     L.levelmask = take(4 * size_t(n));
     L.split_b = take(4 * size_t(n));
     L.split_e = take(4 * size_t(n));
     L.base = take(4 * size_t(n + 1));
-    L.psum = take(16 * size_t(n + 1));
+    L.psum = take(8 * size_t(dim) * size_t(n + 1));
     L.scan_cnt = take(4 * size_t(L.scan_tiles + 1));
-    L.scan_sum = take(16 * size_t(L.scan_tiles + 1));
-    // + 8 bytes: the walk loads 32 bytes at a record's offset
-    L.nodes = take((fbytes == 8 ? kNodeBytes64 : kNodeBytes) * size_t(2 * n) + 8);
-    L.frep = take(2 * size_t(fbytes) * size_t(n));
+    L.scan_sum = take(8 * size_t(dim) * size_t(L.scan_tiles + 1));
+    // + 8 bytes: the 2-D walk loads 32 bytes at a record's offset
+    L.nodes = take((dim == 3 ? kNodeBytes3 : (fbytes == 8 ? kNodeBytes64 : kNodeBytes)) * size_t(2 * n) + 8);
+    L.frep = take(size_t(dim) * size_t(fbytes) * size_t(n));
     L.fattr = take(8 * size_t(n));
     // partial attractive sums, one per (tile, sorted row slot): up to
     // kTileMaxSeg tiles of kTileRows rows per row block
-    L.partial = take(8 * size_t((n + kTileRows - 1) / kTileRows) * kTileRows * kTileMaxSeg);
+    L.partial = dim == 3 ? take(0) : take(8 * size_t((n + kTileRows - 1) / kTileRows) * kTileRows * kTileMaxSeg);
     L.zpart = take(8 * size_t(L.rep_blocks));
     const int64_t zb = (n + kZEvalPoints - 1) / kZEvalPoints;
     L.eval_part = take(8 * size_t(zb > kEvalMaxBlocks ? zb : kEvalMaxBlocks));
@@ -206,6 +211,25 @@ __device__ inline float vmax(float a, float b) { return fmaxf(a, b); }
 __device__ inline double vmin(double a, double b) { return fmin(a, b); }
 __device__ inline double vmax(double a, double b) { return fmax(a, b); }
 
+// Geometry of the Morton tree of a D-dimensional embedding: a cell at level L
+// holds the codes that share their top bits above cell_shift(L); its 2^D
+// children are told apart by the D-bit digit of level L + 1.  2-D: 32 bits
+// per axis interleaved into 64-bit codes, 32 levels.  3-D: 21 bits per axis
+// interleaved into the low 63 bits (the top bit stays 0), 21 levels.
+template <int D> struct Geom;
+template <> struct Geom<2> {
+    static constexpr int kBucketLevel = 32; // identical codes: a bucket cell at the last level
+    __device__ static int split_level(uint64_t a, uint64_t b) { return __clzll((long long)(a ^ b)) >> 1; }
+    __device__ static uint32_t digit(uint64_t code, int L) { return uint32_t(code >> (62 - 2 * L)) & 3u; }
+    __device__ static int cell_shift(int L) { return 64 - 2 * L; }
+};
+template <> struct Geom<3> {
+    static constexpr int kBucketLevel = 21;
+    __device__ static int split_level(uint64_t a, uint64_t b) { return (__clzll((long long)(a ^ b)) - 1) / 3; }
+    __device__ static uint32_t digit(uint64_t code, int L) { return uint32_t(code >> (60 - 3 * L)) & 7u; }
+    __device__ static int cell_shift(int L) { return 63 - 3 * L; }
+};
+
 // two coordinates of the fp32 path or of the fp64 variant
 template <typename T> struct Vec2;
 template <> struct Vec2<float> { using type = float2; };
@@ -213,6 +237,19 @@ template <> struct Vec2<double> { using type = double2; };
 template <typename T> using vec2_t = typename Vec2<T>::type;
 __host__ __device__ inline float2 make_vec2(float x, float y) { return make_float2(x, y); }
 __host__ __device__ inline double2 make_vec2(double x, double y) { return make_double2(x, y); }
+
+// a point of a D-dimensional embedding with coordinates of type T
+template <int D, typename T> struct PointOf;
+template <> struct PointOf<2, float> { using type = float2; };
+template <> struct PointOf<2, double> { using type = double2; };
+template <> struct PointOf<3, float> { using type = float3; };
+template <int D, typename T> using point_t = typename PointOf<D, T>::type;
+__host__ __device__ inline float coord(const float2 &v, int k) { return k == 0 ? v.x : v.y; }
+__host__ __device__ inline double coord(const double2 &v, int k) { return k == 0 ? v.x : v.y; }
+__host__ __device__ inline float coord(const float3 &v, int k) { return k == 0 ? v.x : (k == 1 ? v.y : v.z); }
+__host__ __device__ inline float2 make_point(const float *c, float2 *) { return make_float2(c[0], c[1]); }
+__host__ __device__ inline double2 make_point(const double *c, double2 *) { return make_double2(c[0], c[1]); }
+__host__ __device__ inline float3 make_point(const float *c, float3 *) { return make_float3(c[0], c[1], c[2]); }
 
 // Logical block index such that each of the 8 XCDs (blocks are dealt to XCDs
 // round-robin) receives one contiguous range of logical blocks.  `nblocks`

@@ -95,6 +95,59 @@ __device__ inline void repulsive_walk(const char *nbase, uint32_t end, float2 yi
     }
 }
 
+// The 3-D interaction with one node in the lanes of `take` (see take_node).
+__device__ inline void take_node3(uint64_t take, float d2, float dx, float dy, float dz, float cnt, uint32_t next,
+                                  float &z, float &fx, float &fy, float &fz, uint32_t &resume)
+{
+    float w, t;
+    uint64_t saved;
+    asm volatile("s_and_saveexec_b64 %[sv], %[take]\n\t"
+                 "v_add_f32 %[w], 1.0, %[d2]\n\t"
+                 "v_rcp_f32 %[w], %[w]\n\t"
+                 "v_mov_b32 %[res], %[next]\n\t"
+                 "v_mul_f32 %[t], %[cnt], %[w]\n\t"
+                 "v_fmac_f32 %[z], %[cnt], %[w]\n\t"
+                 "v_mul_f32 %[t], %[t], %[w]\n\t"
+                 "v_fmac_f32 %[fx], %[t], %[dx]\n\t"
+                 "v_fmac_f32 %[fy], %[t], %[dy]\n\t"
+                 "v_fmac_f32 %[fz], %[t], %[dz]\n\t"
+                 "s_mov_b64 exec, %[sv]"
+                 : [z] "+v"(z), [fx] "+v"(fx), [fy] "+v"(fy), [fz] "+v"(fz), [res] "+v"(resume), [w] "=&v"(w),
+                   [t] "=&v"(t), [sv] "=&s"(saved)
+                 : [take] "s"(take), [d2] "v"(d2), [cnt] "s"(cnt), [dx] "v"(dx), [dy] "v"(dy), [dz] "v"(dz),
+                   [next] "s"(next)
+                 : "scc");
+}
+
+// The walk over a 3-D embedding's octree: the same visit order and lane
+// masks on 32-byte records {com.x, com.y, com.z, count, thr, next, self, 0},
+// each exactly one 32-byte scalar load.  With theta^2 <= 0.33 no point
+// accepts a cell containing it (the centre of mass lies in the cell's cube,
+// so the squared distance is at most 3 side^2, below side^2 / theta^2), and
+// the lane's own leaf is taken once with weight 1 as in 2-D.
+template <bool kSelf>
+__device__ inline void repulsive_walk3(const char *nbase, uint32_t end, float3 yi, uint32_t si, uint32_t &resume,
+                                       float &fx, float &fy, float &fz, float &z, uint32_t &inter)
+{
+    uint32_t cur = 0;
+    while (cur < end) {
+        typedef uint32_t u32x8 __attribute__((ext_vector_type(8)));
+        const u32x8 r = *reinterpret_cast<const u32x8 *>(nbase + cur);
+        const float dx = yi.x - __uint_as_float(r[0]), dy = yi.y - __uint_as_float(r[1]);
+        const float dz = yi.z - __uint_as_float(r[2]);
+        const float cnt = __uint_as_float(r[3]), thr = __uint_as_float(r[4]);
+        const uint32_t next = r[5];
+        const float d2 = fmaf(dx, dx, fmaf(dy, dy, dz * dz));
+        const uint64_t act = mask_uge(cur, resume);
+        uint64_t take = act & mask_ogt(d2, thr);
+        if (kSelf) take &= mask_ne(r[6], si);
+        const uint64_t rej = act & ~take;
+        inter += uint32_t(__builtin_popcountll(take));
+        take_node3(take, d2, dx, dy, dz, cnt, next, z, fx, fy, fz, resume);
+        cur = rej ? cur + kNodeBytes3 : next;
+    }
+}
+
 // 1/x in fp64 for x >= 1: the hardware's approximate reciprocal refined by
 // two Newton-Raphson steps r <- r + r (1 - x r), each of which squares the
 // relative error, so the result is within about an ulp of the quotient (the
@@ -143,22 +196,24 @@ __device__ inline void repulsive_walk64(const char *nbase, uint32_t end, double2
     }
 }
 
-// T = float: the path (24-byte records); T = double: the fp64 variant.
-template <typename T>
+// D = 2, T = float: the path (24-byte records); T = double: the fp64
+// variant; D = 3: 3-D embeddings (32-byte records).
+template <int D, typename T>
 __global__ __launch_bounds__(kRepBlock) void repulsive_kernel(
-    const char *__restrict__ nodes, const vec2_t<T> *__restrict__ ys, const uint32_t *__restrict__ perm,
-    Header *__restrict__ hdr, int64_t n, int self_test, vec2_t<T> *__restrict__ frep, double *__restrict__ zpart,
+    const char *__restrict__ nodes, const point_t<D, T> *__restrict__ ys, const uint32_t *__restrict__ perm,
+    Header *__restrict__ hdr, int64_t n, int self_test, point_t<D, T> *__restrict__ frep, double *__restrict__ zpart,
     unsigned long long *__restrict__ ipart)
 {
+    using V = point_t<D, T>;
     const uint32_t nb = gridDim.x;
     const uint32_t lb = xcd_contiguous(blockIdx.x, nb);
     const int w = threadIdx.x / kWave;
     const int64_t s64 = int64_t(lb) * kRepBlock + threadIdx.x;
     const bool valid = s64 < n;
     const uint32_t si = uint32_t(s64);
-    const vec2_t<T> yi = valid ? ys[s64] : make_vec2(T(0), T(0));
+    const V yi = valid ? ys[s64] : V{};
     uint32_t resume = valid ? 0u : 0xffffffffu;
-    T fx = 0, fy = 0, z = 0;
+    T fx = 0, fy = 0, fz = 0, z = 0;
     uint32_t total = uniform(hdr->nodes);
     const uint32_t cap = uint32_t(2 * n - 1);
     total = total < cap ? total : cap;
@@ -166,10 +221,15 @@ __global__ __launch_bounds__(kRepBlock) void repulsive_kernel(
     // it and flags the call otherwise), so each visit advances and the walk
     // ends after at most `total` visits.  A flagged tree is not walked.
     if (uniform(hdr->flags) & (kErrLookback | kErrRange)) total = 0;
-    const uint32_t end = total * uint32_t(sizeof(T) == 8 ? kNodeBytes64 : kNodeBytes);
+    const uint32_t end = total * uint32_t(node_bytes<D, T>());
 
     uint32_t inter = 0; // this wave's interactions (a launch has fewer than 2^32 per wave)
-    if constexpr (sizeof(T) == 8) {
+    if constexpr (D == 3) {
+        if (self_test)
+            repulsive_walk3<true>(nodes, end, yi, si, resume, fx, fy, fz, z, inter);
+        else
+            repulsive_walk3<false>(nodes, end, yi, si, resume, fx, fy, fz, z, inter);
+    } else if constexpr (sizeof(T) == 8) {
         if (self_test)
             repulsive_walk64<true>(nodes, end, yi, si, resume, fx, fy, z, inter);
         else
@@ -188,7 +248,8 @@ __global__ __launch_bounds__(kRepBlock) void repulsive_kernel(
 
     if (valid) {
         const uint32_t p = perm[si];
-        if (p < uint32_t(n)) frep[p] = make_vec2(fx, fy);
+        const T f[3] = {fx, fy, fz};
+        if (p < uint32_t(n)) frep[p] = make_point(f, static_cast<V *>(nullptr));
     }
     // deterministic Z: wave -> block partial -> fixed-order sum in the last block
     double zw = wave_sum(double(z));
@@ -244,22 +305,27 @@ __global__ __launch_bounds__(kRepBlock) void repulsive_kernel(
 }
 
 
-// T = float: the path's plain-CSR attraction; T = double: the fp64 variant
-template <int G, bool kUpdate, typename T>
+// D = 2, T = float: the path's plain-CSR attraction; T = double: the fp64
+// variant; D = 3: 3-D embeddings.  Coordinates are handled component by
+// component (unrolled).
+template <int G, bool kUpdate, int D, typename T>
 __global__ __launch_bounds__(256) void attract_kernel(
     const int64_t *__restrict__ row_ptr, const int32_t *__restrict__ col, const T *__restrict__ val,
-    const vec2_t<T> *__restrict__ ycopy, const vec2_t<T> *__restrict__ frep, Header *__restrict__ hdr,
-    int64_t n, int64_t nnz, StepArgsT<T> a, vec2_t<T> *__restrict__ Y, vec2_t<T> *__restrict__ upd,
-    vec2_t<T> *__restrict__ gains, vec2_t<T> *__restrict__ grad)
+    const point_t<D, T> *__restrict__ ycopy, const point_t<D, T> *__restrict__ frep, Header *__restrict__ hdr,
+    int64_t n, int64_t nnz, StepArgsT<T> a, point_t<D, T> *__restrict__ Y, point_t<D, T> *__restrict__ upd,
+    point_t<D, T> *__restrict__ gains, point_t<D, T> *__restrict__ grad)
 {
+    using V = point_t<D, T>;
     const int sub = lane_id() % G;
     constexpr int kRows = 256 / G;
     const T inv_z = T(1.0 / hdr->Z);
     for (int64_t row0 = int64_t(blockIdx.x) * kRows; row0 < n; row0 += int64_t(gridDim.x) * kRows) {
         const int64_t i = row0 + threadIdx.x / G;
         const bool valid = i < n;
-        T fx = 0, fy = 0;
-        vec2_t<T> yi = make_vec2(T(0), T(0));
+        T f[D];
+#pragma unroll
+        for (int d = 0; d < D; ++d) f[d] = T(0);
+        V yi{};
         if (valid) {
             yi = ycopy[i];
             int64_t s = row_ptr[i], e = row_ptr[i + 1];
@@ -276,74 +342,90 @@ __global__ __launch_bounds__(256) void attract_kernel(
                     continue;
                 }
                 const T p = __builtin_nontemporal_load(val + k);
-                const vec2_t<T> yj = ycopy[j];
-                const T dx = yi.x - yj.x, dy = yi.y - yj.y;
-                const T pw = p * recip(T(1) + fma(dx, dx, dy * dy));
-                fx = fma(pw, dx, fx);
-                fy = fma(pw, dy, fy);
+                const V yj = ycopy[j];
+                T dv[D];
+#pragma unroll
+                for (int d = 0; d < D; ++d) dv[d] = coord(yi, d) - coord(yj, d);
+                T d2 = dv[D - 1] * dv[D - 1];
+#pragma unroll
+                for (int d = D - 2; d >= 0; --d) d2 = fma(dv[d], dv[d], d2);
+                const T pw = p * recip(T(1) + d2);
+#pragma unroll
+                for (int d = 0; d < D; ++d) f[d] = fma(pw, dv[d], f[d]);
             }
         }
 #pragma unroll
         for (int o = G / 2; o > 0; o >>= 1) {
-            fx += __shfl_xor(fx, o, kWave);
-            fy += __shfl_xor(fy, o, kWave);
+#pragma unroll
+            for (int d = 0; d < D; ++d) f[d] += __shfl_xor(f[d], o, kWave);
         }
         if (valid && sub == 0) {
-            const vec2_t<T> fr = frep[i];
-            const T gx = T(4) * (a.alpha * fx - fr.x * inv_z);
-            const T gy = T(4) * (a.alpha * fy - fr.y * inv_z);
-            if (grad) grad[i] = make_vec2(gx, gy);
+            const V fr = frep[i];
+            T g[D];
+#pragma unroll
+            for (int d = 0; d < D; ++d) g[d] = T(4) * (a.alpha * f[d] - coord(fr, d) * inv_z);
+            if (grad) grad[i] = make_point(g, static_cast<V *>(nullptr));
             if (kUpdate) {
-                vec2_t<T> u = upd[i], gn = gains[i];
-                gn.x = (u.x * gx < T(0)) ? gn.x + T(0.2) : gn.x * T(0.8);
-                gn.y = (u.y * gy < T(0)) ? gn.y + T(0.2) : gn.y * T(0.8);
-                gn.x = vmax(gn.x, a.min_gain);
-                gn.y = vmax(gn.y, a.min_gain);
-                u.x = a.momentum * u.x - a.learning_rate * gn.x * gx;
-                u.y = a.momentum * u.y - a.learning_rate * gn.y * gy;
-                Y[i] = make_vec2(yi.x + u.x, yi.y + u.y);
-                upd[i] = u;
-                gains[i] = gn;
+                const V u0 = upd[i], g0 = gains[i];
+                T u[D], gn[D], y[D];
+#pragma unroll
+                for (int d = 0; d < D; ++d) {
+                    const T ud = coord(u0, d);
+                    T gd = (ud * g[d] < T(0)) ? coord(g0, d) + T(0.2) : coord(g0, d) * T(0.8);
+                    gd = vmax(gd, a.min_gain);
+                    u[d] = a.momentum * ud - a.learning_rate * gd * g[d];
+                    gn[d] = gd;
+                    y[d] = coord(yi, d) + u[d];
+                }
+                Y[i] = make_point(y, static_cast<V *>(nullptr));
+                upd[i] = make_point(u, static_cast<V *>(nullptr));
+                gains[i] = make_point(gn, static_cast<V *>(nullptr));
             }
         }
     }
 }
 
 // ------------------------------------------------------------------ launchers
-template <typename T> void launch_repulsive(int64_t n, bool self_test, void *ws, const Layout &L, hipStream_t st)
+template <int D, typename T>
+void launch_repulsive(int64_t n, bool self_test, void *ws, const Layout &L, hipStream_t st)
 {
-    repulsive_kernel<T><<<unsigned(L.rep_blocks), kRepBlock, 0, st>>>(
-        at<char>(ws, L.nodes), at<vec2_t<T>>(ws, L.ys), at<uint32_t>(ws, L.idx0), at<Header>(ws, L.header), n,
-        self_test ? 1 : 0, at<vec2_t<T>>(ws, L.frep), at<double>(ws, L.zpart), at<unsigned long long>(ws, L.ipart));
+    using V = point_t<D, T>;
+    repulsive_kernel<D, T><<<unsigned(L.rep_blocks), kRepBlock, 0, st>>>(
+        at<char>(ws, L.nodes), at<V>(ws, L.ys), at<uint32_t>(ws, L.idx0), at<Header>(ws, L.header), n,
+        self_test ? 1 : 0, at<V>(ws, L.frep), at<double>(ws, L.zpart), at<unsigned long long>(ws, L.ipart));
 }
-template void launch_repulsive<float>(int64_t, bool, void *, const Layout &, hipStream_t);
-template void launch_repulsive<double>(int64_t, bool, void *, const Layout &, hipStream_t);
+template void launch_repulsive<2, float>(int64_t, bool, void *, const Layout &, hipStream_t);
+template void launch_repulsive<2, double>(int64_t, bool, void *, const Layout &, hipStream_t);
+template void launch_repulsive<3, float>(int64_t, bool, void *, const Layout &, hipStream_t);
 
-template <typename T>
+template <int D, typename T>
 void launch_attract(const int64_t *row_ptr, const int32_t *col, const T *val, int64_t n, int64_t nnz,
                     const StepArgsT<T> &a, T *Y, T *upd, T *gains, T *grad, void *ws, const Layout &L, hipStream_t st)
 {
     constexpr int G = 64; // one wave per row: rows hold ~100-200 entries
     int64_t blocks = (n + (256 / G) - 1) / (256 / G);
     if (blocks > 65535 * 8) blocks = 65535 * 8;
-    using V = vec2_t<T>;
+    using V = point_t<D, T>;
     const V *yc = at<V>(ws, L.ycopy);
     const V *fr = at<V>(ws, L.frep);
     Header *hdr = at<Header>(ws, L.header);
     if (a.update)
-        attract_kernel<G, true, T><<<unsigned(blocks), 256, 0, st>>>(
+        attract_kernel<G, true, D, T><<<unsigned(blocks), 256, 0, st>>>(
             row_ptr, col, val, yc, fr, hdr, n, nnz, a, reinterpret_cast<V *>(Y), reinterpret_cast<V *>(upd),
             reinterpret_cast<V *>(gains), reinterpret_cast<V *>(grad));
     else
-        attract_kernel<G, false, T><<<unsigned(blocks), 256, 0, st>>>(row_ptr, col, val, yc, fr, hdr, n, nnz, a,
-                                                                    nullptr, nullptr, nullptr,
-                                                                    reinterpret_cast<V *>(grad));
+        attract_kernel<G, false, D, T><<<unsigned(blocks), 256, 0, st>>>(row_ptr, col, val, yc, fr, hdr, n, nnz, a,
+                                                                       nullptr, nullptr, nullptr,
+                                                                       reinterpret_cast<V *>(grad));
 }
-template void launch_attract<float>(const int64_t *, const int32_t *, const float *, int64_t, int64_t,
-                                    const StepArgsT<float> &, float *, float *, float *, float *, void *,
-                                    const Layout &, hipStream_t);
-template void launch_attract<double>(const int64_t *, const int32_t *, const double *, int64_t, int64_t,
-                                     const StepArgsT<double> &, double *, double *, double *, double *, void *,
-                                     const Layout &, hipStream_t);
+template void launch_attract<2, float>(const int64_t *, const int32_t *, const float *, int64_t, int64_t,
+                                       const StepArgsT<float> &, float *, float *, float *, float *, void *,
+                                       const Layout &, hipStream_t);
+template void launch_attract<2, double>(const int64_t *, const int32_t *, const double *, int64_t, int64_t,
+                                        const StepArgsT<double> &, double *, double *, double *, double *, void *,
+                                        const Layout &, hipStream_t);
+template void launch_attract<3, float>(const int64_t *, const int32_t *, const float *, int64_t, int64_t,
+                                       const StepArgsT<float> &, float *, float *, float *, float *, void *,
+                                       const Layout &, hipStream_t);
 
 } // namespace bht

@@ -70,6 +70,19 @@ __global__ __launch_bounds__(256) void bbox_partial_kernel(const vec2_t<T> *__re
     }
 }
 
+// The per-call scalars and counters, reset by the box kernel that starts a call.
+__device__ inline void reset_call_state(Header *hdr, uint32_t nonfinite)
+{
+    hdr->flags = nonfinite ? kErrNonFinite : 0u;
+    hdr->Z = 0.0;
+    hdr->interactions = 0;
+    for (int k = 0; k < kSortPasses; ++k) hdr->tile_counter[k] = 0;
+    hdr->ticket_bbox = 0;
+    hdr->ticket_rep = 0;
+    hdr->attract_next = 0;
+    hdr->max_depth = 0;
+}
+
 // One block: finish the box, derive the quantisation parameters in fp64 and
 // reset the per-call counters and histograms.
 template <typename T>
@@ -130,14 +143,7 @@ __global__ __launch_bounds__(256) void bbox_final_kernel(const T *__restrict__ p
         hdr->yroot[0] = c0 - rs;
         hdr->yroot[1] = c1 - rs;
         hdr->scale = rs > 0.0 ? 2147483648.0 / rs : 0.0;
-        hdr->flags = b ? kErrNonFinite : 0u;
-        hdr->Z = 0.0;
-        hdr->interactions = 0;
-        for (int k = 0; k < kSortPasses; ++k) hdr->tile_counter[k] = 0;
-        hdr->ticket_bbox = 0;
-        hdr->ticket_rep = 0;
-        hdr->attract_next = 0;
-        hdr->max_depth = 0;
+        reset_call_state(hdr, b);
     }
 }
 
@@ -217,6 +223,185 @@ __global__ __launch_bounds__(kSortBlock) void morton_kernel(
         if (sh[k]) atomicAdd(&hc[k], sh[k]);
 }
 
+// ------------------------------------------------------------------ 3-D box and codes
+// A 3-D embedding: the domain is the cube centred on the box with half-side
+// r_span (the widest half extent); each coordinate is quantised to 21 bits,
+// trunc((y - y_root) * 2^20 / r_span) clamped to [0, 2^21 - 1], in fp64 in
+// a fixed order, and bit k of dimension d goes to bit 3k + d of the code
+// (63 bits; the top bit stays 0).
+__global__ __launch_bounds__(256) void bbox3_partial_kernel(const float3 *__restrict__ Y, int64_t n,
+                                                            float *__restrict__ part)
+{
+    float mn[3] = {INFINITY, INFINITY, INFINITY}, mx[3] = {-INFINITY, -INFINITY, -INFINITY};
+    uint32_t bad = 0;
+    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x) {
+        const float3 y = Y[i];
+        bad |= !(isfinite(y.x) && isfinite(y.y) && isfinite(y.z));
+#pragma unroll
+        for (int d = 0; d < 3; ++d) {
+            mn[d] = fminf(mn[d], coord(y, d));
+            mx[d] = fmaxf(mx[d], coord(y, d));
+        }
+    }
+#pragma unroll
+    for (int d = 0; d < 3; ++d) {
+        mn[d] = wave_min(mn[d]);
+        mx[d] = wave_max(mx[d]);
+    }
+    const bool anybad = ballot(bad != 0) != 0;
+    __shared__ float s[4][6];
+    __shared__ uint32_t sb[4];
+    const int w = threadIdx.x / kWave;
+    if (lane_id() == 0) {
+#pragma unroll
+        for (int d = 0; d < 3; ++d) {
+            s[w][2 * d] = mn[d];
+            s[w][2 * d + 1] = mx[d];
+        }
+        sb[w] = anybad;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float *o = part + 8 * blockIdx.x; // {min x, max x, min y, max y, min z, max z, flag}
+        uint32_t b = 0;
+        for (int d = 0; d < 3; ++d) {
+            float lo = s[0][2 * d], hi = s[0][2 * d + 1];
+            for (int k = 1; k < 4; ++k) {
+                lo = fminf(lo, s[k][2 * d]);
+                hi = fmaxf(hi, s[k][2 * d + 1]);
+            }
+            o[2 * d] = lo;
+            o[2 * d + 1] = hi;
+        }
+        for (int k = 0; k < 4; ++k) b |= sb[k];
+        reinterpret_cast<uint32_t *>(o + 6)[0] = b;
+    }
+}
+
+__global__ __launch_bounds__(256) void bbox3_final_kernel(const float *__restrict__ part, int nparts,
+                                                          Header *__restrict__ hdr, uint32_t *__restrict__ hist)
+{
+    float mn[3] = {INFINITY, INFINITY, INFINITY}, mx[3] = {-INFINITY, -INFINITY, -INFINITY};
+    uint32_t bad = 0;
+    for (int k = threadIdx.x; k < nparts; k += blockDim.x) {
+        const float *p = part + 8 * k;
+#pragma unroll
+        for (int d = 0; d < 3; ++d) {
+            mn[d] = fminf(mn[d], p[2 * d]);
+            mx[d] = fmaxf(mx[d], p[2 * d + 1]);
+        }
+        bad |= reinterpret_cast<const uint32_t *>(p + 6)[0];
+    }
+#pragma unroll
+    for (int d = 0; d < 3; ++d) {
+        mn[d] = wave_min(mn[d]);
+        mx[d] = wave_max(mx[d]);
+    }
+    const bool anybad = ballot(bad != 0) != 0;
+    __shared__ float s[4][6];
+    __shared__ uint32_t sb[4];
+    const int w = threadIdx.x / kWave;
+    if (lane_id() == 0) {
+#pragma unroll
+        for (int d = 0; d < 3; ++d) {
+            s[w][2 * d] = mn[d];
+            s[w][2 * d + 1] = mx[d];
+        }
+        sb[w] = anybad;
+    }
+    for (int k = threadIdx.x; k < kHistCopies * kHistWords; k += blockDim.x) hist[k] = 0;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t b = 0;
+        for (int k = 0; k < 4; ++k) b |= sb[k];
+        double c[3], widest = 0.0;
+        for (int d = 0; d < 3; ++d) {
+            float lo = s[0][2 * d], hi = s[0][2 * d + 1];
+            for (int k = 1; k < 4; ++k) {
+                lo = fminf(lo, s[k][2 * d]);
+                hi = fmaxf(hi, s[k][2 * d + 1]);
+            }
+            hdr->bmin[d] = lo;
+            hdr->bmax[d] = hi;
+            // fp64, fixed operation order: the codes depend on these bits
+            c[d] = (double(lo) + double(hi)) * 0.5;
+            const double ext = double(hi) - double(lo);
+            widest = ext > widest ? ext : widest;
+        }
+        const double rs = 0.5 * widest;
+        for (int d = 0; d < 3; ++d) {
+            hdr->cent[d] = c[d];
+            hdr->yroot[d] = c[d] - rs;
+        }
+        hdr->rspan = rs;
+        hdr->scale = rs > 0.0 ? 1048576.0 / rs : 0.0;
+        reset_call_state(hdr, b);
+    }
+}
+
+__device__ inline uint32_t quantise21(float y, double yroot, double scale)
+{
+    double q = (double(y) - yroot) * scale;
+    if (!(q > 0.0)) return 0u; // also catches NaN
+    if (q >= 2097151.0) return 2097151u;
+    return uint32_t(q); // truncation toward zero
+}
+
+// Three-way spread by the interleaving rule: entry b of the table holds byte
+// b with each bit k moved to bit 3k; byte j of a 21-bit coordinate lands at
+// bit 24 j of the word.
+__device__ inline uint32_t spread3_byte_rule(uint32_t b)
+{
+    uint32_t s = 0;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) s |= ((b >> k) & 1u) << (3 * k);
+    return s;
+}
+
+__device__ inline uint64_t spread3_by_bytes(const uint32_t *__restrict__ tab, uint32_t v)
+{
+    return uint64_t(tab[v & 0xffu]) | (uint64_t(tab[(v >> 8) & 0xffu]) << 24) | (uint64_t(tab[v >> 16]) << 48);
+}
+
+__global__ __launch_bounds__(kSortBlock) void morton3_kernel(
+    const float3 *__restrict__ Y, int64_t n, const Header *__restrict__ hdr, uint64_t *__restrict__ codes,
+    float3 *__restrict__ ycopy, uint32_t *__restrict__ hist, uint32_t *__restrict__ levelmask,
+    uint32_t *__restrict__ status, int64_t tiles)
+{
+    __shared__ uint32_t sh[kSortPasses * kRadix];
+    __shared__ uint32_t s_spread[256];
+    static_assert(kSortBlock == 256, "one spread-table entry per thread");
+    s_spread[threadIdx.x] = spread3_byte_rule(threadIdx.x);
+    for (int k = threadIdx.x; k < kSortPasses * kRadix; k += kSortBlock) sh[k] = 0;
+    for (int k = threadIdx.x; k < kSortPasses * kRadix; k += kSortBlock) {
+        const int pass = k / kRadix, d = k % kRadix;
+        status[(int64_t(pass) * tiles + blockIdx.x) * kRadix + d] = 0;
+    }
+    __syncthreads();
+    const double yr0 = hdr->yroot[0], yr1 = hdr->yroot[1], yr2 = hdr->yroot[2], sc = hdr->scale;
+    const int64_t base = int64_t(blockIdx.x) * kSortTile;
+#pragma unroll
+    for (int r = 0; r < kSortItems; ++r) {
+        const int64_t i = base + r * kSortBlock + threadIdx.x;
+        if (i < n) {
+            const float3 y = Y[i];
+            ycopy[i] = y;
+            const uint64_t code = spread3_by_bytes(s_spread, quantise21(y.x, yr0, sc)) |
+                                  (spread3_by_bytes(s_spread, quantise21(y.y, yr1, sc)) << 1) |
+                                  (spread3_by_bytes(s_spread, quantise21(y.z, yr2, sc)) << 2);
+            codes[i] = code;
+            levelmask[i] = 0;
+#pragma unroll
+            for (int p = 0; p < kSortPasses; ++p)
+                atomicAdd(&sh[p * kRadix + int((code >> (p * kRadixBits)) & (kRadix - 1))], 1u);
+        }
+    }
+    __syncthreads();
+    uint32_t *hc = hist + (blockIdx.x % kHistCopies) * kHistWords;
+    for (int k = threadIdx.x; k < kSortPasses * kRadix; k += kSortBlock)
+        if (sh[k]) atomicAdd(&hc[k], sh[k]);
+}
+
 // ------------------------------------------------------------------ onesweep pass
 // Block-wide exclusive scan of one value per thread (256 threads).
 __device__ inline uint32_t block_exclusive_scan256(uint32_t v, uint32_t *s_wave /*[4]*/,
@@ -254,12 +439,13 @@ __device__ inline uint32_t peek(const uint32_t *p)
 
 static_assert(kSortBlock == kRadix, "thread t owns digit t in the scans and the look-back");
 
-template <bool kFirst, bool kLast, typename T = float>
+// V: the point type gathered by the last pass (float2, double2 or float3)
+template <bool kFirst, bool kLast, typename V = float2>
 __global__ __launch_bounds__(kSortBlock) void onesweep_kernel(
     const uint64_t *__restrict__ keys_in, const uint32_t *__restrict__ idx_in,
     uint64_t *__restrict__ keys_out, uint32_t *__restrict__ idx_out,
     uint32_t *__restrict__ status, const uint32_t *__restrict__ hist, Header *__restrict__ hdr,
-    int pass, int64_t n, const vec2_t<T> *__restrict__ ysrc, vec2_t<T> *__restrict__ ys)
+    int pass, int64_t n, const V *__restrict__ ysrc, V *__restrict__ ys)
 {
     constexpr int kWaves = kSortBlock / kWave;
     constexpr int kSeg = kWave * kSortItems; // keys per wave segment
@@ -388,7 +574,7 @@ __global__ __launch_bounds__(kSortBlock) void onesweep_kernel(
             keys_out[out] = k;
             uint32_t ix = s_idx[j];
             idx_out[out] = ix;
-            if (kLast) ys[out] = ix < uint32_t(n) ? ysrc[ix] : make_vec2(T(0), T(0));
+            if (kLast) ys[out] = ix < uint32_t(n) ? ysrc[ix] : V{};
         } else {
             atomicOr(&hdr->flags, kErrRange);
         }
@@ -408,6 +594,19 @@ template <typename T> void launch_bbox(const T *Y, int64_t n, void *ws, const La
 template void launch_bbox<float>(const float *, int64_t, void *, const Layout &, hipStream_t);
 template void launch_bbox<double>(const double *, int64_t, void *, const Layout &, hipStream_t);
 
+void launch_bbox_morton3(const float *Y, int64_t n, void *ws, const Layout &L, hipStream_t st)
+{
+    int blocks = int((n + 255) / 256);
+    if (blocks > kBBoxBlocks) blocks = kBBoxBlocks;
+    const float3 *y3 = reinterpret_cast<const float3 *>(Y);
+    bbox3_partial_kernel<<<blocks, 256, 0, st>>>(y3, n, at<float>(ws, L.bbox_part));
+    bbox3_final_kernel<<<1, 256, 0, st>>>(at<float>(ws, L.bbox_part), blocks, at<Header>(ws, L.header),
+                                          at<uint32_t>(ws, L.hist));
+    morton3_kernel<<<unsigned(L.sort_tiles), kSortBlock, 0, st>>>(
+        y3, n, at<Header>(ws, L.header), at<uint64_t>(ws, L.codes0), at<float3>(ws, L.ycopy),
+        at<uint32_t>(ws, L.hist), at<uint32_t>(ws, L.levelmask), at<uint32_t>(ws, L.status), L.sort_tiles);
+}
+
 template <typename T>
 void launch_morton(const T *Y, int64_t n, const uint32_t *rank, void *ws, const Layout &L, hipStream_t st)
 {
@@ -420,29 +619,35 @@ template void launch_morton<float>(const float *, int64_t, const uint32_t *, voi
 template void launch_morton<double>(const double *, int64_t, const uint32_t *, void *, const Layout &,
                                     hipStream_t);
 
-// the last pass also gathers Y in sorted order (from `ysrc`, the private copy)
-template <typename T> void launch_sort(int64_t n, const T *ysrc, void *ws, const Layout &L, hipStream_t st)
+// the last pass also gathers the points in sorted order (from `ysrc`, in the
+// order the codes were made)
+template <typename V> void launch_sort_points(int64_t n, const V *ysrc, void *ws, const Layout &L, hipStream_t st)
 {
     uint64_t *k[2] = {at<uint64_t>(ws, L.codes0), at<uint64_t>(ws, L.codes1)};
     uint32_t *x[2] = {at<uint32_t>(ws, L.idx0), at<uint32_t>(ws, L.idx1)};
     Header *hdr = at<Header>(ws, L.header);
     const uint32_t *hist = at<uint32_t>(ws, L.hist);
-    const vec2_t<T> *yc = reinterpret_cast<const vec2_t<T> *>(ysrc);
-    vec2_t<T> *ys = at<vec2_t<T>>(ws, L.ys);
+    V *ys = at<V>(ws, L.ys);
     for (int p = 0; p < kSortPasses; ++p) {
         uint32_t *status = at<uint32_t>(ws, L.status) + int64_t(p) * L.sort_tiles * kRadix;
         int src = p & 1, dst = src ^ 1;
         dim3 g(unsigned(L.sort_tiles));
         if (p == 0)
-            onesweep_kernel<true, false><<<g, kSortBlock, 0, st>>>(k[src], nullptr, k[dst], x[dst], status, hist,
-                                                                  hdr, p, n, nullptr, nullptr);
+            onesweep_kernel<true, false, V><<<g, kSortBlock, 0, st>>>(k[src], nullptr, k[dst], x[dst], status, hist,
+                                                                     hdr, p, n, nullptr, nullptr);
         else if (p == kSortPasses - 1)
-            onesweep_kernel<false, true, T><<<g, kSortBlock, 0, st>>>(k[src], x[src], k[dst], x[dst], status,
-                                                                     hist, hdr, p, n, yc, ys);
+            onesweep_kernel<false, true, V><<<g, kSortBlock, 0, st>>>(k[src], x[src], k[dst], x[dst], status,
+                                                                     hist, hdr, p, n, ysrc, ys);
         else
-            onesweep_kernel<false, false><<<g, kSortBlock, 0, st>>>(k[src], x[src], k[dst], x[dst], status,
-                                                                   hist, hdr, p, n, nullptr, nullptr);
+            onesweep_kernel<false, false, V><<<g, kSortBlock, 0, st>>>(k[src], x[src], k[dst], x[dst], status,
+                                                                      hist, hdr, p, n, nullptr, nullptr);
     }
+}
+template void launch_sort_points<float3>(int64_t, const float3 *, void *, const Layout &, hipStream_t);
+
+template <typename T> void launch_sort(int64_t n, const T *ysrc, void *ws, const Layout &L, hipStream_t st)
+{
+    launch_sort_points(n, reinterpret_cast<const vec2_t<T> *>(ysrc), ws, L, st);
 }
 template void launch_sort<float>(int64_t, const float *, void *, const Layout &, hipStream_t);
 template void launch_sort<double>(int64_t, const double *, void *, const Layout &, hipStream_t);

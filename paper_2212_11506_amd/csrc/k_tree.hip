@@ -23,14 +23,14 @@
 //      sorted coordinates: com = (S[e] - S[b]) / (e - b), so no bottom-up
 //      level sweep is needed (cells of up to 32 points sum their points
 //      directly instead).
+//
+// The same kernels build the octree of a 3-D embedding: D = 3 reads 3-bit
+// digits from 63-bit codes (Geom<3>), keeps three prefix sums and writes
+// 32-byte records; D = 2 with T = double is the fp64 variant.
 #include "common.hpp"
 #include "kernels.hpp"
 
 namespace bht {
-
-__device__ inline int split_level(uint64_t a, uint64_t b) { return __clzll((long long)(a ^ b)) >> 1; }
-
-__device__ inline uint32_t quad_digit(uint64_t code, int L) { return uint32_t(code >> (62 - 2 * L)) & 3u; }
 
 // first index in [0, s] whose code shares the top (64 - sh) bits of key
 __device__ inline int64_t gallop_left(const uint64_t *__restrict__ codes, int64_t s, uint64_t key, int sh)
@@ -171,11 +171,13 @@ __device__ inline int64_t wave_first_other(const uint64_t *__restrict__ codes, i
     return hi;
 }
 
+template <int D>
 __global__ __launch_bounds__(kSplitBlock) void tree_splits_kernel(const uint64_t *__restrict__ codes, int64_t n,
                                                                   uint32_t *__restrict__ levelmask,
                                                                   uint32_t *__restrict__ split_b,
                                                                   uint32_t *__restrict__ split_e)
 {
+    using G = Geom<D>;
     __shared__ uint64_t s_c[kSplitBlock + 2 * kSplitWin + 1];
     __shared__ int64_t s_b[kSplitBlock], s_e[kSplitBlock];
     __shared__ uint16_t s_hard[2 * kSplitBlock];
@@ -197,11 +199,11 @@ __global__ __launch_bounds__(kSplitBlock) void tree_splits_kernel(const uint64_t
         ms = s_c[s - wlo];
         const uint64_t mn = s_c[s + 1 - wlo];
         split = ms != mn;
-        if (split) L = split_level(ms, mn);
+        if (split) L = G::split_level(ms, mn);
     }
     int64_t b = 0, e = n;
     if (split && L > 0) {
-        const int sh = 64 - 2 * L;
+        const int sh = G::cell_shift(L);
         // in window coordinates; the window holds s and s + 1
         const int64_t bl = gallop_left(s_c, s - wlo, ms, sh);
         const int64_t el = gallop_right(s_c, s + 1 - wlo, whi - wlo, ms, sh);
@@ -218,7 +220,7 @@ __global__ __launch_bounds__(kSplitBlock) void tree_splits_kernel(const uint64_t
     for (uint32_t h = uint32_t(t / kWave); h < nh; h += kSplitBlock / kWave) {
         const int owner = s_hard[h] >> 1, dir = s_hard[h] & 1;
         const uint64_t key = s_c[base + owner - wlo];
-        const int sh = 64 - 2 * split_level(key, s_c[base + owner + 1 - wlo]);
+        const int sh = G::cell_shift(G::split_level(key, s_c[base + owner + 1 - wlo]));
         if (dir == 0) {
             // codes[wlo] shares the cell; find its first index in [0, wlo]
             const int64_t r = wave_first_same(codes, -1, wlo, key, sh);
@@ -237,7 +239,7 @@ __global__ __launch_bounds__(kSplitBlock) void tree_splits_kernel(const uint64_t
     b = s_b[t];
     e = s_e[t];
     const uint64_t cb = b >= wlo ? s_c[b - wlo] : codes[b];
-    const bool owner = quad_digit(cb, L) == quad_digit(ms, L);
+    const bool owner = G::digit(cb, L) == G::digit(ms, L);
     if (owner) {
         atomicOr(&levelmask[b], 1u << L);
         split_b[s] = uint32_t(b);
@@ -248,36 +250,68 @@ __global__ __launch_bounds__(kSplitBlock) void tree_splits_kernel(const uint64_t
 }
 
 // ------------------------------------------------------------------ 2. scans
-struct ScanVal {
+// One element per sorted position: its node count and its coordinates
+// relative to the box centre (D of them), scanned together.
+template <int D> struct ScanVal {
     uint32_t c;
-    double x, y;
+    double s[D];
 };
 
-__device__ inline ScanVal scan_add(ScanVal a, ScanVal b) { return {a.c + b.c, a.x + b.x, a.y + b.y}; }
+template <int D> __device__ inline ScanVal<D> scan_add(const ScanVal<D> &a, const ScanVal<D> &b)
+{
+    ScanVal<D> r;
+    r.c = a.c + b.c;
+#pragma unroll
+    for (int k = 0; k < D; ++k) r.s[k] = a.s[k] + b.s[k];
+    return r;
+}
 
-template <typename T>
-__device__ inline ScanVal element(const uint64_t *__restrict__ codes, const uint32_t *__restrict__ levelmask,
-                                  const vec2_t<T> *__restrict__ ys, int64_t x, int64_t n, double c0, double c1)
+template <int D> __device__ inline ScanVal<D> scan_zero()
+{
+    ScanVal<D> r;
+    r.c = 0;
+#pragma unroll
+    for (int k = 0; k < D; ++k) r.s[k] = 0.0;
+    return r;
+}
+
+template <int D> __device__ inline ScanVal<D> shfl_up(const ScanVal<D> &v, int o)
+{
+    ScanVal<D> r;
+    r.c = __shfl_up(v.c, o, kWave);
+#pragma unroll
+    for (int k = 0; k < D; ++k) r.s[k] = __shfl_up(v.s[k], o, kWave);
+    return r;
+}
+
+template <int D, typename T>
+__device__ inline ScanVal<D> element(const uint64_t *__restrict__ codes, const uint32_t *__restrict__ levelmask,
+                                     const point_t<D, T> *__restrict__ ys, int64_t x, int64_t n, const double *c)
 {
     const uint64_t k = codes[x];
     const uint32_t bucket = (x == 0 || codes[x - 1] != k) && x + 1 < n && codes[x + 1] == k ? 1u : 0u;
-    const vec2_t<T> y = ys[x];
-    return {1u + bucket + uint32_t(__popc(levelmask[x])), double(y.x) - c0, double(y.y) - c1};
+    const point_t<D, T> y = ys[x];
+    ScanVal<D> r;
+    r.c = 1u + bucket + uint32_t(__popc(levelmask[x]));
+#pragma unroll
+    for (int d = 0; d < D; ++d) r.s[d] = double(coord(y, d)) - c[d];
+    return r;
 }
 
 // exclusive block scan of one ScanVal per thread (256 threads); returns the block total
-__device__ inline ScanVal block_scan_excl(ScanVal v, ScanVal *s_wave /*[4]*/, ScanVal *out_total)
+template <int D>
+__device__ inline ScanVal<D> block_scan_excl(ScanVal<D> v, ScanVal<D> *s_wave /*[4]*/, ScanVal<D> *out_total)
 {
     int lane = lane_id(), w = threadIdx.x / kWave;
-    ScanVal x = v;
+    ScanVal<D> x = v;
 #pragma unroll
     for (int o = 1; o < kWave; o <<= 1) {
-        ScanVal y{__shfl_up(x.c, o, kWave), __shfl_up(x.x, o, kWave), __shfl_up(x.y, o, kWave)};
+        ScanVal<D> y = shfl_up(x, o);
         if (lane >= o) x = scan_add(y, x);
     }
     if (lane == kWave - 1) s_wave[w] = x;
     __syncthreads();
-    ScanVal off{0, 0.0, 0.0}, tot{0, 0.0, 0.0};
+    ScanVal<D> off = scan_zero<D>(), tot = scan_zero<D>();
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         if (k < w) off = scan_add(off, s_wave[k]);
@@ -285,98 +319,117 @@ __device__ inline ScanVal block_scan_excl(ScanVal v, ScanVal *s_wave /*[4]*/, Sc
     }
     *out_total = tot;
     // exclusive: total of earlier waves + inclusive-in-wave of the previous lane
-    ScanVal prev{__shfl_up(x.c, 1, kWave), __shfl_up(x.x, 1, kWave), __shfl_up(x.y, 1, kWave)};
-    if (lane == 0) prev = {0, 0.0, 0.0};
+    ScanVal<D> prev = shfl_up(x, 1);
+    if (lane == 0) prev = scan_zero<D>();
     return scan_add(off, prev);
 }
 
-template <typename T>
+template <int D> __device__ inline void load_centre(const Header *hdr, double *c)
+{
+#pragma unroll
+    for (int d = 0; d < D; ++d) c[d] = hdr->cent[d];
+}
+
+template <int D, typename T>
 __global__ __launch_bounds__(kScanBlock) void scan_reduce_kernel(
     const uint64_t *__restrict__ codes, const uint32_t *__restrict__ levelmask,
-    const vec2_t<T> *__restrict__ ys, const Header *__restrict__ hdr, int64_t n,
-    uint32_t *__restrict__ tile_cnt, double2 *__restrict__ tile_sum)
+    const point_t<D, T> *__restrict__ ys, const Header *__restrict__ hdr, int64_t n,
+    uint32_t *__restrict__ tile_cnt, double *__restrict__ tile_sum)
 {
-    __shared__ ScanVal s_wave[4];
-    const double c0 = hdr->cent[0], c1 = hdr->cent[1];
+    __shared__ ScanVal<D> s_wave[4];
+    double c[D];
+    load_centre<D>(hdr, c);
     int64_t first = int64_t(blockIdx.x) * kScanTile + int64_t(threadIdx.x) * kScanItems;
-    ScanVal acc{0, 0.0, 0.0};
+    ScanVal<D> acc = scan_zero<D>();
     for (int k = 0; k < kScanItems; ++k) {
         int64_t x = first + k;
-        if (x < n) acc = scan_add(acc, element<T>(codes, levelmask, ys, x, n, c0, c1));
+        if (x < n) acc = scan_add(acc, element<D, T>(codes, levelmask, ys, x, n, c));
     }
-    ScanVal tot;
+    ScanVal<D> tot;
     block_scan_excl(acc, s_wave, &tot);
     if (threadIdx.x == 0) {
         tile_cnt[blockIdx.x] = tot.c;
-        tile_sum[blockIdx.x] = make_double2(tot.x, tot.y);
+#pragma unroll
+        for (int d = 0; d < D; ++d) tile_sum[int64_t(blockIdx.x) * D + d] = tot.s[d];
     }
 }
 
 // one block: exclusive scan over the tile totals, in place; totals -> base[n], psum[n]
+template <int D>
 __global__ __launch_bounds__(kScanBlock) void scan_top_kernel(uint32_t *__restrict__ tile_cnt,
-                                                              double2 *__restrict__ tile_sum, int64_t tiles,
+                                                              double *__restrict__ tile_sum, int64_t tiles,
                                                               int64_t n, uint32_t *__restrict__ base,
-                                                              double2 *__restrict__ psum,
+                                                              double *__restrict__ psum,
                                                               Header *__restrict__ hdr)
 {
-    __shared__ ScanVal s_wave[4];
+    __shared__ ScanVal<D> s_wave[4];
     int64_t per = (tiles + kScanBlock - 1) / kScanBlock;
     int64_t first = int64_t(threadIdx.x) * per;
-    ScanVal acc{0, 0.0, 0.0};
+    auto load = [&](int64_t t) {
+        ScanVal<D> v;
+        v.c = tile_cnt[t];
+#pragma unroll
+        for (int d = 0; d < D; ++d) v.s[d] = tile_sum[t * D + d];
+        return v;
+    };
+    ScanVal<D> acc = scan_zero<D>();
     for (int64_t k = 0; k < per; ++k) {
         int64_t t = first + k;
-        if (t < tiles) {
-            double2 s = tile_sum[t];
-            acc = scan_add(acc, ScanVal{tile_cnt[t], s.x, s.y});
-        }
+        if (t < tiles) acc = scan_add(acc, load(t));
     }
-    ScanVal tot;
-    ScanVal run = block_scan_excl(acc, s_wave, &tot);
+    ScanVal<D> tot;
+    ScanVal<D> run = block_scan_excl(acc, s_wave, &tot);
     for (int64_t k = 0; k < per; ++k) {
         int64_t t = first + k;
         if (t < tiles) {
-            double2 s = tile_sum[t];
-            ScanVal v{tile_cnt[t], s.x, s.y};
+            const ScanVal<D> v = load(t);
             tile_cnt[t] = run.c;
-            tile_sum[t] = make_double2(run.x, run.y);
+#pragma unroll
+            for (int d = 0; d < D; ++d) tile_sum[t * D + d] = run.s[d];
             run = scan_add(run, v);
         }
     }
     if (threadIdx.x == 0) {
         base[n] = tot.c;
-        psum[n] = make_double2(tot.x, tot.y);
+#pragma unroll
+        for (int d = 0; d < D; ++d) psum[n * D + d] = tot.s[d];
         hdr->nodes = tot.c;
     }
 }
 
-template <typename T>
+template <int D, typename T>
 __global__ __launch_bounds__(kScanBlock) void scan_down_kernel(
     const uint64_t *__restrict__ codes, const uint32_t *__restrict__ levelmask,
-    const vec2_t<T> *__restrict__ ys, const Header *__restrict__ hdr, int64_t n,
-    const uint32_t *__restrict__ tile_cnt, const double2 *__restrict__ tile_sum,
-    uint32_t *__restrict__ base, double2 *__restrict__ psum)
+    const point_t<D, T> *__restrict__ ys, const Header *__restrict__ hdr, int64_t n,
+    const uint32_t *__restrict__ tile_cnt, const double *__restrict__ tile_sum,
+    uint32_t *__restrict__ base, double *__restrict__ psum)
 {
-    __shared__ ScanVal s_wave[4];
-    const double c0 = hdr->cent[0], c1 = hdr->cent[1];
+    __shared__ ScanVal<D> s_wave[4];
+    double c[D];
+    load_centre<D>(hdr, c);
     int64_t first = int64_t(blockIdx.x) * kScanTile + int64_t(threadIdx.x) * kScanItems;
-    ScanVal loc[kScanItems];
-    ScanVal acc{0, 0.0, 0.0};
+    ScanVal<D> loc[kScanItems];
+    ScanVal<D> acc = scan_zero<D>();
 #pragma unroll
     for (int k = 0; k < kScanItems; ++k) {
         int64_t x = first + k;
-        loc[k] = (x < n) ? element<T>(codes, levelmask, ys, x, n, c0, c1) : ScanVal{0, 0.0, 0.0};
+        loc[k] = (x < n) ? element<D, T>(codes, levelmask, ys, x, n, c) : scan_zero<D>();
         acc = scan_add(acc, loc[k]);
     }
-    ScanVal tot;
-    ScanVal run = block_scan_excl(acc, s_wave, &tot);
-    double2 ts = tile_sum[blockIdx.x];
-    run = scan_add(ScanVal{tile_cnt[blockIdx.x], ts.x, ts.y}, run);
+    ScanVal<D> tot;
+    ScanVal<D> run = block_scan_excl(acc, s_wave, &tot);
+    ScanVal<D> tile_off;
+    tile_off.c = tile_cnt[blockIdx.x];
+#pragma unroll
+    for (int d = 0; d < D; ++d) tile_off.s[d] = tile_sum[int64_t(blockIdx.x) * D + d];
+    run = scan_add(tile_off, run);
 #pragma unroll
     for (int k = 0; k < kScanItems; ++k) {
         int64_t x = first + k;
         if (x < n) {
             base[x] = run.c;
-            psum[x] = make_double2(run.x, run.y);
+#pragma unroll
+            for (int d = 0; d < D; ++d) psum[x * D + d] = run.s[d];
         }
         run = scan_add(run, loc[k]);
     }
@@ -413,50 +466,68 @@ __device__ inline void store_node(char *__restrict__ nodes, int64_t pre, double2
     r[1] = make_uint2(self, 0u);
 }
 
+// a 3-D record: {com.x, com.y, com.z, count, thr, next, self, 0}, two 16-byte stores
+__device__ inline void store_node(char *__restrict__ nodes, int64_t pre, float3 com, float count, float thr,
+                                  uint32_t next, uint32_t self)
+{
+    uint4 *r = reinterpret_cast<uint4 *>(nodes + pre * kNodeBytes3);
+    r[0] = make_uint4(__float_as_uint(com.x), __float_as_uint(com.y), __float_as_uint(com.z), __float_as_uint(count));
+    r[1] = make_uint4(__float_as_uint(thr), next, self, 0u);
+}
+
 // Centre of mass of the sorted points [b, e).  Small cells sum their points
 // directly (fp64, relative to the first point, so nothing cancels); larger
 // cells take the difference of the fp64 prefix sums, whose rounding error
 // divided by the count stays far below fp32 resolution.
 constexpr int64_t kDirectSum = 32;
 
-template <typename T>
-__device__ inline vec2_t<T> centre_of_mass(const double2 *__restrict__ psum, const vec2_t<T> *__restrict__ ys,
-                                           int64_t b, int64_t e, double c0, double c1)
+template <int D, typename T>
+__device__ inline point_t<D, T> centre_of_mass(const double *__restrict__ psum, const point_t<D, T> *__restrict__ ys,
+                                               int64_t b, int64_t e, const double *c)
 {
     const double inv = 1.0 / double(e - b);
+    T out[D];
     if (e - b <= kDirectSum) {
-        const vec2_t<T> y0 = ys[b];
-        double sx = 0.0, sy = 0.0;
+        const point_t<D, T> y0 = ys[b];
+        double acc[D];
+#pragma unroll
+        for (int d = 0; d < D; ++d) acc[d] = 0.0;
         for (int64_t s = b + 1; s < e; ++s) {
-            const vec2_t<T> y = ys[s];
-            sx += double(y.x) - double(y0.x);
-            sy += double(y.y) - double(y0.y);
+            const point_t<D, T> y = ys[s];
+#pragma unroll
+            for (int d = 0; d < D; ++d) acc[d] += double(coord(y, d)) - double(coord(y0, d));
         }
-        return make_vec2(T(double(y0.x) + sx * inv), T(double(y0.y) + sy * inv));
+#pragma unroll
+        for (int d = 0; d < D; ++d) out[d] = T(double(coord(y0, d)) + acc[d] * inv);
+    } else {
+#pragma unroll
+        for (int d = 0; d < D; ++d) out[d] = T(c[d] + (psum[e * D + d] - psum[b * D + d]) * inv);
     }
-    double2 hi = psum[e], lo = psum[b];
-    return make_vec2(T(c0 + (hi.x - lo.x) * inv), T(c1 + (hi.y - lo.y) * inv));
+    return make_point(out, static_cast<point_t<D, T> *>(nullptr));
 }
 
-// T = float: 24-byte records with fp32 centres and thresholds; T = double
-// (the fp64 variant): 40-byte records with fp64 centres and thresholds.
-// theta2 is theta^2 in fp64 (from the float theta of the path, or the double
-// theta of the variant).
-template <typename T>
+// D = 2, T = float: 24-byte records with fp32 centres and thresholds; T =
+// double (the fp64 variant): 40-byte records with fp64 centres and
+// thresholds; D = 3: 32-byte records.  theta2 is theta^2 in fp64.
+template <int D, typename T>
 __global__ __launch_bounds__(256) void tree_nodes_kernel(
     const uint64_t *__restrict__ codes, int64_t n, const uint32_t *__restrict__ levelmask,
     const uint32_t *__restrict__ split_b, const uint32_t *__restrict__ split_e,
-    const uint32_t *__restrict__ base, const double2 *__restrict__ psum, const vec2_t<T> *__restrict__ ys,
+    const uint32_t *__restrict__ base, const double *__restrict__ psum, const point_t<D, T> *__restrict__ ys,
     Header *__restrict__ hdr, double theta2, char *__restrict__ nodes, TreeDebug dbg)
 {
-    constexpr int kBytes = sizeof(T) == 8 ? kNodeBytes64 : kNodeBytes;
+    using G = Geom<D>;
+    constexpr int kBytes = node_bytes<D, T>();
+    constexpr int kLast = G::kBucketLevel; // bucket cells; their points sit one level below
     int64_t x = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-    const double c0 = hdr->cent[0], c1 = hdr->cent[1], rspan = hdr->rspan;
-    // acceptance thresholds of the cell levels 0..32 (32: buckets)
-    __shared__ T s_thr[33];
-    // deepest leaf level of the block (a single point's level, 32 for a bucket)
+    double c[D];
+    load_centre<D>(hdr, c);
+    const double rspan = hdr->rspan;
+    // acceptance thresholds of the cell levels 0..kLast
+    __shared__ T s_thr[kLast + 1];
+    // deepest leaf level of the block (a single point's level, kLast for a bucket)
     __shared__ uint32_t s_depth;
-    if (threadIdx.x < 33) s_thr[threadIdx.x] = T(accept_threshold(rspan, int(threadIdx.x), theta2));
+    if (threadIdx.x <= kLast) s_thr[threadIdx.x] = T(accept_threshold(rspan, int(threadIdx.x), theta2));
     if (threadIdx.x == 0) s_depth = 0;
     __syncthreads();
     uint32_t depth = 0;
@@ -465,7 +536,7 @@ __global__ __launch_bounds__(256) void tree_nodes_kernel(
     // that break it (or fall outside the array) are only reachable from a
     // corrupted sort; they are not written and the call is flagged, and the
     // walk then does not start.
-    auto emit = [&](int64_t pre, vec2_t<T> com, int64_t b, int64_t e, int L, int64_t next, int kind) {
+    auto emit = [&](int64_t pre, point_t<D, T> com, int64_t b, int64_t e, int L, int64_t next, int kind) {
         if (pre >= 2 * n || next > 2 * n || next <= pre) {
             atomicOr(&hdr->flags, kErrRange);
             return;
@@ -484,34 +555,34 @@ __global__ __launch_bounds__(256) void tree_nodes_kernel(
         // (a) the internal node owned by split x
         if (x < n - 1 && split_e[x] != 0) {
             int64_t b = split_b[x], e = split_e[x];
-            int L = split_level(codes[x], codes[x + 1]);
+            int L = G::split_level(codes[x], codes[x + 1]);
             int64_t pre = base[b] + __popc(levelmask[b] & ((1u << L) - 1u));
-            emit(pre, centre_of_mass<T>(psum, ys, b, e, c0, c1), b, e, L, base[e], 0);
+            emit(pre, centre_of_mass<D, T>(psum, ys, b, e, c), b, e, L, base[e], 0);
         }
-        // (b) the root, when no split lies at level 0 (all points in one quadrant)
-        if (x == 0 && quad_digit(codes[0], 0) == quad_digit(codes[n - 1], 0))
-            emit(0, centre_of_mass<T>(psum, ys, 0, n, c0, c1), 0, n, 0, base[n], 0);
+        // (b) the root, when no split lies at level 0 (all points in one child cell)
+        if (x == 0 && G::digit(codes[0], 0) == G::digit(codes[n - 1], 0))
+            emit(0, centre_of_mass<D, T>(psum, ys, 0, n, c), 0, n, 0, base[n], 0);
         // (c) the leaf of point x, preceded by its bucket when a run of identical
-        // codes starts at x (bucket members are leaves at level 33)
+        // codes starts at x (bucket members are leaves one level below the bucket)
         if (x == 0 || codes[x - 1] != codes[x]) {
             int64_t e = run_end(codes, x, n);
             int64_t pre = base[x] + __popc(levelmask[x]);
             if (e == x + 1) {
                 int lv = -1;
-                if (x > 0) lv = split_level(codes[x - 1], codes[x]);
+                if (x > 0) lv = G::split_level(codes[x - 1], codes[x]);
                 if (x + 1 < n) {
-                    int r = split_level(codes[x], codes[x + 1]);
+                    int r = G::split_level(codes[x], codes[x + 1]);
                     lv = r > lv ? r : lv;
                 }
                 emit(pre, ys[x], x, e, lv + 1, pre + 1, 2);
                 depth = uint32_t(lv + 1);
             } else {
-                emit(pre, centre_of_mass<T>(psum, ys, x, e, c0, c1), x, e, 32, base[e], 1);
-                emit(pre + 1, ys[x], x, x + 1, 33, pre + 2, 2);
-                depth = 32;
+                emit(pre, centre_of_mass<D, T>(psum, ys, x, e, c), x, e, kLast, base[e], 1);
+                emit(pre + 1, ys[x], x, x + 1, kLast + 1, pre + 2, 2);
+                depth = kLast;
             }
         } else {
-            emit(base[x], ys[x], x, x + 1, 33, int64_t(base[x]) + 1, 2); // a later member of a bucket
+            emit(base[x], ys[x], x, x + 1, kLast + 1, int64_t(base[x]) + 1, 2); // a later member of a bucket
         }
     }
     // the block's deepest leaf; the global maximum only takes the atomic when
@@ -545,35 +616,61 @@ __global__ __launch_bounds__(256) void tree_unpack_kernel(const char *__restrict
     if (meta) meta[i] = c.y != kNodeCell ? (c.y | 0xC0000000u) : c.x / uint32_t(kNodeBytes);
 }
 
+// The 3-D records in the same documented form: summary {com x, com y, com z,
+// count} and threshold, meta as above.
+__global__ __launch_bounds__(256) void tree_unpack3_kernel(const char *__restrict__ nodes,
+                                                           const Header *__restrict__ hdr, int64_t cap,
+                                                           float4 *__restrict__ summary, float *__restrict__ thr,
+                                                           uint32_t *__restrict__ meta)
+{
+    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    const int64_t count = hdr->nodes < cap ? int64_t(hdr->nodes) : cap;
+    if (i >= count) return;
+    const uint4 *r = reinterpret_cast<const uint4 *>(nodes + i * kNodeBytes3);
+    const uint4 a = r[0], b = r[1];
+    if (summary)
+        summary[i] = make_float4(__uint_as_float(a.x), __uint_as_float(a.y), __uint_as_float(a.z), __uint_as_float(a.w));
+    if (thr) thr[i] = __uint_as_float(b.x);
+    if (meta) meta[i] = b.z != kNodeCell ? (b.z | 0xC0000000u) : b.y / uint32_t(kNodeBytes3);
+}
+
 // ------------------------------------------------------------------ launchers
-template <typename T>
+template <int D, typename T>
 void launch_tree(int64_t n, double theta2, void *ws, const Layout &L, const TreeDebug &dbg, hipStream_t st)
 {
     const uint64_t *codes = at<uint64_t>(ws, L.codes0);
     uint32_t *lm = at<uint32_t>(ws, L.levelmask);
     uint32_t *sb = at<uint32_t>(ws, L.split_b), *se = at<uint32_t>(ws, L.split_e);
-    const vec2_t<T> *ys = at<vec2_t<T>>(ws, L.ys);
+    const point_t<D, T> *ys = at<point_t<D, T>>(ws, L.ys);
     Header *hdr = at<Header>(ws, L.header);
     uint32_t *base = at<uint32_t>(ws, L.base);
-    double2 *psum = at<double2>(ws, L.psum);
+    double *psum = at<double>(ws, L.psum);
     uint32_t *tc = at<uint32_t>(ws, L.scan_cnt);
-    double2 *ts = at<double2>(ws, L.scan_sum);
+    double *ts = at<double>(ws, L.scan_sum);
     unsigned gn = unsigned((n + 255) / 256);
-    tree_splits_kernel<<<gn, 256, 0, st>>>(codes, n, lm, sb, se);
-    scan_reduce_kernel<T><<<unsigned(L.scan_tiles), kScanBlock, 0, st>>>(codes, lm, ys, hdr, n, tc, ts);
-    scan_top_kernel<<<1, kScanBlock, 0, st>>>(tc, ts, L.scan_tiles, n, base, psum, hdr);
-    scan_down_kernel<T><<<unsigned(L.scan_tiles), kScanBlock, 0, st>>>(codes, lm, ys, hdr, n, tc, ts, base, psum);
-    tree_nodes_kernel<T><<<gn, 256, 0, st>>>(codes, n, lm, sb, se, base, psum, ys, hdr, theta2,
-                                             at<char>(ws, L.nodes), dbg);
+    tree_splits_kernel<D><<<gn, 256, 0, st>>>(codes, n, lm, sb, se);
+    scan_reduce_kernel<D, T><<<unsigned(L.scan_tiles), kScanBlock, 0, st>>>(codes, lm, ys, hdr, n, tc, ts);
+    scan_top_kernel<D><<<1, kScanBlock, 0, st>>>(tc, ts, L.scan_tiles, n, base, psum, hdr);
+    scan_down_kernel<D, T><<<unsigned(L.scan_tiles), kScanBlock, 0, st>>>(codes, lm, ys, hdr, n, tc, ts, base, psum);
+    tree_nodes_kernel<D, T><<<gn, 256, 0, st>>>(codes, n, lm, sb, se, base, psum, ys, hdr, theta2,
+                                                at<char>(ws, L.nodes), dbg);
 }
-template void launch_tree<float>(int64_t, double, void *, const Layout &, const TreeDebug &, hipStream_t);
-template void launch_tree<double>(int64_t, double, void *, const Layout &, const TreeDebug &, hipStream_t);
+template void launch_tree<2, float>(int64_t, double, void *, const Layout &, const TreeDebug &, hipStream_t);
+template void launch_tree<2, double>(int64_t, double, void *, const Layout &, const TreeDebug &, hipStream_t);
+template void launch_tree<3, float>(int64_t, double, void *, const Layout &, const TreeDebug &, hipStream_t);
 
 void launch_tree_unpack(int64_t n, void *ws, const Layout &L, float *summary, uint32_t *meta, hipStream_t st)
 {
     tree_unpack_kernel<<<unsigned((2 * n + 255) / 256), 256, 0, st>>>(
         at<char>(ws, L.nodes), at<Header>(ws, L.header), 2 * n,
         reinterpret_cast<float4 *>(summary), meta);
+}
+
+void launch_tree_unpack3(int64_t n, void *ws, const Layout &L, float *summary, float *thr, uint32_t *meta,
+                         hipStream_t st)
+{
+    tree_unpack3_kernel<<<unsigned((2 * n + 255) / 256), 256, 0, st>>>(
+        at<char>(ws, L.nodes), at<Header>(ws, L.header), 2 * n, reinterpret_cast<float4 *>(summary), thr, meta);
 }
 
 } // namespace bht

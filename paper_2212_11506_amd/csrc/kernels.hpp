@@ -65,10 +65,16 @@ template <typename T> void launch_bbox(const T *Y, int64_t n, void *ws, const La
 // rank (nullable): write the private copy of Y in that order instead of the caller's
 template <typename T>
 void launch_morton(const T *Y, int64_t n, const uint32_t *rank, void *ws, const Layout &L, hipStream_t st);
+// 3-D embeddings (Y n x 3 fp32): box, cube, 63-bit codes, digit histograms and
+// the private copy of Y in the caller's order
+void launch_bbox_morton3(const float *Y, int64_t n, void *ws, const Layout &L, hipStream_t st);
 // ysrc: Y in the original order, gathered into Morton order by the last pass
 template <typename T> void launch_sort(int64_t n, const T *ysrc, void *ws, const Layout &L, hipStream_t st);
-// theta2 = theta^2 in fp64; T = float (the path) or double (the fp64 variant)
-template <typename T>
+// the same with the points' type given (float3: 3-D embeddings)
+template <typename V> void launch_sort_points(int64_t n, const V *ysrc, void *ws, const Layout &L, hipStream_t st);
+// theta2 = theta^2 in fp64; D = 2 with T = float (the path) or double (the
+// fp64 variant), or D = 3 with T = float (3-D embeddings)
+template <int D, typename T>
 void launch_tree(int64_t n, double theta2, void *ws, const Layout &L, const TreeDebug &dbg, hipStream_t st);
 // evaluation: exact Z and KL, results in the header's eval field
 void launch_z_exact(const float *Y, int64_t n, void *ws, const Layout &L, hipStream_t st);
@@ -76,12 +82,17 @@ void launch_kl(const float *Y, const int64_t *row_ptr, const int32_t *col, const
                int64_t nnz, double log_z, void *ws, const Layout &L, hipStream_t st);
 // the tree's records as {com, count, threshold} and documented meta words (both nullable)
 void launch_tree_unpack(int64_t n, void *ws, const Layout &L, float *summary, uint32_t *meta, hipStream_t st);
+void launch_tree_unpack3(int64_t n, void *ws, const Layout &L, float *summary, float *thr, uint32_t *meta,
+                         hipStream_t st);
 // theta^2 <= 0.49: no point accepts a cell containing it, so the walk needs no
 // comparison with the lane's own leaf
 inline bool repulsive_self_test(float theta) { return double(theta) * double(theta) > 0.49; }
 inline bool repulsive_self_test(double theta) { return theta * theta > 0.49; }
-template <typename T> void launch_repulsive(int64_t n, bool self_test, void *ws, const Layout &L, hipStream_t st);
-template <typename T>
+// the same in 3-D: a cube's centre of mass lies within sqrt(3) sides of any of its points
+inline bool repulsive_self_test3(float theta) { return double(theta) * double(theta) > 0.33; }
+template <int D, typename T>
+void launch_repulsive(int64_t n, bool self_test, void *ws, const Layout &L, hipStream_t st);
+template <int D, typename T>
 void launch_attract(const int64_t *row_ptr, const int32_t *col, const T *val, int64_t n, int64_t nnz,
                     const StepArgsT<T> &a, T *Y, T *upd, T *gains, T *grad, void *ws, const Layout &L, hipStream_t st);
 

@@ -252,3 +252,28 @@ def test_bench_refuses_more_than_one_gpu():
     r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"], capture_output=True,
                        text=True, timeout=120, cwd=root)
     assert r.returncode == 2 and "one GPU" in r.stderr
+
+
+def test_3d_workspace_size_and_argument_checks():
+    lib = bh.load_library()
+    assert lib.bhtsne_workspace_size_3d(1, 0) == 0 and lib.bhtsne_workspace_size_3d(1 << 24, 0) == 0
+    n = 5000
+    assert lib.bhtsne_workspace_size_3d(n, 10) > lib.bhtsne_workspace_size(n, 10) // 2
+    P = _Csr(n, 10, FAKE, FAKE, FAKE)
+    ws = lib.bhtsne_workspace_size_3d(n, 10)
+    # bad theta, bad exaggeration, missing grad, small workspace: all refused on the host
+    assert lib.bhtsne_gradient_3d(C.c_void_p(FAKE), C.byref(P), -1.0, 1.0, C.c_void_p(FAKE), None,
+                                  C.c_void_p(FAKE), ws, None) == bh.BHTSNE_EINVAL
+    assert lib.bhtsne_gradient_3d(C.c_void_p(FAKE), C.byref(P), 0.5, 0.0, C.c_void_p(FAKE), None,
+                                  C.c_void_p(FAKE), ws, None) == bh.BHTSNE_EINVAL
+    assert lib.bhtsne_gradient_3d(C.c_void_p(FAKE), C.byref(P), 0.5, 1.0, None, None,
+                                  C.c_void_p(FAKE), ws, None) == bh.BHTSNE_EINVAL
+    assert lib.bhtsne_gradient_3d(C.c_void_p(FAKE), C.byref(P), 0.5, 1.0, C.c_void_p(FAKE), None,
+                                  C.c_void_p(FAKE), ws - 1, None) == bh.BHTSNE_EWORKSPACE
+    assert lib.bhtsne_step_3d(C.c_void_p(FAKE), C.byref(P), 0.5, 1.0, 200.0, 1.0, 0.01, C.c_void_p(FAKE),
+                              C.c_void_p(FAKE), None, None, C.c_void_p(FAKE), ws, None) == bh.BHTSNE_EINVAL
+    nn = C.c_int64(0)
+    assert lib.bhtsne_debug_tree_3d(C.c_void_p(FAKE), 1, 0.5, C.byref(nn), None, None, None, None, None, None,
+                                    None, C.c_void_p(FAKE), ws, None) == bh.BHTSNE_EINVAL
+    assert lib.bhtsne_debug_sort_3d(None, n, None, None, None, None, C.c_void_p(FAKE), ws,
+                                    None) == bh.BHTSNE_EINVAL

@@ -1,0 +1,312 @@
+"""GPU parity of the 3-D embedding path against the 3-D fp64 oracle.
+
+Same bars as in 2-D: the box, the quantisation parameters, the 63-bit Morton
+codes, the sorted order and the octree topology bit for bit; the centres of
+mass to fp32 rounding of the fp64 definition; gradients within rel-L2 1e-4
+at theta = 0 and 1e-3 at theta > 0 against the oracle's Barnes-Hut on the
+same Y; Z within 1e-5; the update rule element by element; the final KL of a
+full run within 1% of the oracle's own run.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    import paper_2212_11506_amd as bh
+
+BUCKET_LEVEL = 21
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def rel_l2(a, b):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
+
+
+def dev_y(y):
+    return torch.from_numpy(np.ascontiguousarray(y, np.float32)).cuda()
+
+
+def _case(name):
+    if name == "c0":
+        return synth.make_inputs(0, dim=3).Y
+    if name.startswith("rand"):
+        n = int(name[4:])
+        return synth.random_y3(n, seed=n, scale=1.0)
+    if name == "dups":
+        return synth.random_y3(3000, seed=9, scale=1.0, dups=600)
+    if name == "identical":
+        return np.full((1000, 3), 0.375, np.float32)
+    if name == "identical2":
+        return np.array([[1.0, 2.0, 3.0], [1.0, 2.0, 3.0]], np.float32)
+    if name == "huge":
+        return synth.random_y3(4000, seed=10, scale=1e35)
+    if name == "tiny":
+        return synth.random_y3(4000, seed=11, scale=1e-20)
+    if name == "outlier":
+        y = synth.random_y3(5000, seed=12, scale=1e-3)
+        y[17] = (1e4, -3e3, 5e2)
+        return y
+    if name == "line":
+        t = np.linspace(-1, 1, 3001, dtype=np.float32)
+        return np.stack([t, t, t], 1)
+    if name == "plane":  # a flat embedding: every point at z = 0
+        y = synth.random_y3(4000, seed=14, scale=1.0)
+        y[:, 2] = 0.0
+        return y
+    if name == "late":
+        return synth.make_inputs(4, n=20000, dim=3).Y
+    if name == "reps40":
+        y = np.repeat(synth.random_y3(3000, seed=13, scale=1.0), 40, axis=0)
+        return y[np.random.default_rng(13).permutation(y.shape[0])]
+    raise KeyError(name)
+
+
+SORT_CASES = ["c0", "rand2", "rand3", "rand63", "rand64", "rand65", "rand2049", "rand4097", "rand70001", "dups",
+              "identical", "identical2", "huge", "tiny", "outlier", "line", "plane", "late", "reps40"]
+
+
+@pytest.mark.parametrize("case", SORT_CASES)
+def test_morton3_and_sort_bit_exact(case):
+    y = _case(case)
+    say(f"[sort3] case={case} n={y.shape[0]}")
+    codes, scodes, perm, params = bh.debug_sort_3d(dev_y(y))
+    with oracle.State3(y) as s:
+        t = s.tree()
+    assert params[0:6] == list(t.box[0:6])
+    assert params[6:10] == list(t.box[6:10])
+    assert params[10:13] == list(t.yrs[0:3]) and params[13] == t.yrs[3]
+    assert np.array_equal(codes.cpu().numpy().view(np.uint64), t.codes)
+    assert np.array_equal(scodes.cpu().numpy().view(np.uint64), t.sorted_codes)
+    assert np.array_equal(perm.cpu().numpy().view(np.uint32), t.perm)
+
+
+def test_quantisation3_hand_worked_case(golden_dir):
+    import os
+    rows = [line.split() for line in open(os.path.join(golden_dir, "quantisation3_truncation.txt"))
+            if line.strip() and not line.startswith("#")]
+    y = np.array([[float(r[0]), float(r[1]), float(r[2])] for r in rows], np.float32)
+    codes, _, _, params = bh.debug_sort_3d(dev_y(y))
+    assert [int(c) for c in codes.cpu().numpy().view(np.uint64)] == [int(r[6], 16) for r in rows]
+    assert params[9] == 1.5 and params[10:13] == [0.0, 0.0, 0.0]
+
+
+def _with_members(t, y):
+    """The oracle's octree as the library stores it: each bucket followed by
+    its points as single-point nodes one level below the bucket level."""
+    from types import SimpleNamespace
+    lev, kind, beg, end, cnt, com = [], [], [], [], [], []
+    ys = y.astype(np.float64)[t.perm.astype(np.int64)]
+    for i in range(t.nodes):
+        lev.append(t.level[i]); kind.append(t.kind[i]); beg.append(t.begin[i]); end.append(t.end[i])
+        cnt.append(t.count[i]); com.append(t.com[i])
+        if t.kind[i] == oracle.BUCKET:
+            for j in range(int(t.begin[i]), int(t.end[i])):
+                lev.append(BUCKET_LEVEL + 1); kind.append(oracle.SINGLE); beg.append(j); end.append(j + 1)
+                cnt.append(1); com.append(ys[j])
+    u = SimpleNamespace(box=t.box)
+    u.nodes = len(lev)
+    u.level = np.array(lev, dtype=np.uint8)
+    u.kind = np.array(kind, dtype=np.uint8)
+    u.begin = np.array(beg, dtype=np.uint32)
+    u.end = np.array(end, dtype=np.uint32)
+    u.count = np.array(cnt, dtype=np.uint32)
+    u.com = np.array(com, dtype=np.float64).reshape(-1, 3)
+    return u
+
+
+@pytest.mark.parametrize("case", SORT_CASES)
+def test_octree_and_summaries(case):
+    y = _case(case)
+    theta = 0.5
+    say(f"[tree3] case={case} n={y.shape[0]}")
+    ws = torch.empty(bh.workspace_size_3d(y.shape[0], 0), dtype=torch.uint8, device="cuda")
+    g = bh.debug_tree_3d(dev_y(y), theta, workspace=ws)
+    with oracle.State3(y) as s:
+        raw = s.tree()
+    t = _with_members(raw, y)
+    assert g["nodes"] == t.nodes
+    assert np.array_equal(g["level"].cpu().numpy(), t.level)
+    assert np.array_equal(g["kind"].cpu().numpy(), t.kind)
+    assert np.array_equal(g["begin"].cpu().numpy().view(np.uint32), t.begin)
+    assert np.array_equal(g["end"].cpu().numpy().view(np.uint32), t.end)
+    summ = g["summary"].cpu().numpy().astype(np.float64)
+    assert np.array_equal(summ[:, 3], t.count.astype(np.float64))
+    # centres: fp32 rounding of the fp64 definition, plus (cells of more than 32
+    # points) the rounding of a difference of two fp64 prefix sums
+    err = np.abs(summ[:, :3] - t.com)
+    smax = np.abs(y.astype(np.float64) - t.box[6:9]).sum(0)
+    cnt = t.count.astype(np.float64)[:, None]
+    tol = 7e-8 * np.abs(t.com) + np.where(cnt > 32, 8 * 2.0 ** -52 * smax / cnt, 0.0) + 1e-38
+    assert np.all(err <= tol), float((err / tol).max())
+    thr = g["threshold"].cpu().numpy().astype(np.float64)
+    single = t.kind == oracle.SINGLE
+    assert np.all(thr[single] == -1.0)
+    side2 = (2 * t.box[9] * np.exp2(-t.level[~single].astype(np.float64))) ** 2 / theta ** 2
+    with np.errstate(over="ignore"):
+        side2_f32 = side2.astype(np.float32).astype(np.float64)
+    assert np.allclose(thr[~single], side2_f32, rtol=1e-6, atol=1e-45)
+    meta = g["meta"].cpu().numpy().view(np.uint32)
+    order_end = np.searchsorted(t.begin.astype(np.int64) * 64 + t.level, t.end.astype(np.int64) * 64, side="left")
+    assert np.array_equal(meta[~single], order_end[~single].astype(np.uint32))
+    assert np.array_equal(meta[single], t.begin[single] | np.uint32(0xC0000000))
+    leaf = (raw.kind == oracle.SINGLE) | (raw.kind == oracle.BUCKET)
+    assert bh.get_stats(ws)["max_depth"] == int(raw.level[leaf].max())
+
+
+def _p_for(y, seed=3, k=8):
+    return synth.random_p(y.shape[0], seed=seed, k=k)
+
+
+GRAD_CASES = ["c0", "rand2", "rand3", "rand65", "rand2049", "dups", "identical", "line", "plane", "late"]
+
+
+def _grad_check(y, rp, col, val, theta, alpha):
+    ws = torch.empty(bh.workspace_size_3d(y.shape[0], col.size), dtype=torch.uint8, device="cuda")
+    P = bh.Csr.from_numpy(rp, col, val)
+    g, Z = bh.gradient_3d(dev_y(y), P, theta, alpha, workspace=ws)
+    stats = bh.get_stats(ws)
+    go, Zo, inter_o, nodes_o = oracle.gradient3(y, rp, col, val, theta, alpha)
+    with oracle.State3(y) as s:
+        t = s.tree()
+    b = t.kind == oracle.BUCKET
+    assert stats["nodes"] == nodes_o + int((t.end[b].astype(np.int64) - t.begin[b]).sum())
+    if theta == 0.0:
+        assert stats["interactions"] == inter_o == y.shape[0] * (y.shape[0] - 1)
+    else:
+        assert abs(stats["interactions"] - inter_o) <= 1e-3 * inter_o + 2
+    tol = 1e-4 if theta == 0.0 else 1e-3
+    g = g.cpu().numpy()
+    if np.linalg.norm(go) == 0.0:
+        assert np.abs(g).max() <= 1e-6
+        err = 0.0
+    else:
+        err = rel_l2(g, go)
+        assert err <= tol, err
+    assert abs(Z - Zo) <= 1e-5 * Zo, (Z, Zo)
+    return err
+
+
+@pytest.mark.parametrize("case", GRAD_CASES)
+@pytest.mark.parametrize("theta", [0.0, 0.5])
+def test_gradient3_parity(case, theta):
+    if case == "c0":
+        inp = synth.make_inputs(0, dim=3)
+        y, rp, col, val = inp.Y, inp.row_ptr, inp.col, inp.val
+    else:
+        y = _case(case)
+        rp, col, val = _p_for(y)
+    say(f"[grad3] case={case} theta={theta} n={y.shape[0]}")
+    err = _grad_check(y, rp, col, val, theta, 12.0)
+    say(f"[grad3] case={case} theta={theta}: rel-L2 {err:.2e}")
+
+
+# 0.57 is below and 0.58 above the largest angle (theta^2 <= 0.33) at which the
+# 3-D walk drops the comparison with a point's own leaf
+@pytest.mark.parametrize("case,theta", [("late", 0.2), ("late", 0.57), ("late", 0.58), ("late", 0.8),
+                                        ("late", 1.2), ("reps40", 0.57), ("reps40", 0.58), ("dups", 1.0)])
+def test_gradient3_parity_other_angles(case, theta):
+    y = _case(case)
+    rp, col, val = _p_for(y, seed=5)
+    say(f"[grad3-angle] case={case} theta={theta}")
+    _grad_check(y, rp, col, val, theta, 1.0)
+
+
+def test_step3_matches_update_rule():
+    inp = synth.make_inputs(0, dim=3)
+    w = inp.workload
+    Y = dev_y(inp.Y)
+    P = bh.Csr.from_numpy(inp.row_ptr, inp.col, inp.val)
+    u, gains, grad = torch.zeros_like(Y), torch.ones_like(Y), torch.empty_like(Y)
+    y64 = inp.Y.astype(np.float64)
+    u64, g64 = np.zeros_like(y64), np.ones_like(y64)
+    for it in range(3):
+        s = w.schedule(it)
+        bh.step_3d(Y, P, 0.5, s["exaggeration"], s["learning_rate"], s["momentum"], 0.01, u, gains, grad=grad)
+        gd = grad.cpu().numpy().astype(np.float64)
+        oracle.update(y64, u64, g64, gd, s["learning_rate"], s["momentum"], 0.01)
+        assert np.allclose(gains.cpu().numpy(), g64, rtol=1e-6, atol=0)
+        assert np.allclose(u.cpu().numpy(), u64, rtol=2e-5, atol=1e-6 * np.abs(u64).max())
+        assert np.allclose(Y.cpu().numpy(), y64, rtol=2e-5, atol=1e-6 * np.abs(y64).max())
+        y64 = Y.cpu().numpy().astype(np.float64)
+        u64 = u.cpu().numpy().astype(np.float64)
+        g64 = gains.cpu().numpy().astype(np.float64)
+
+
+def test_full_run_kl3_small_workload():
+    """The 2k workload's 50 iterations with a 3-D embedding on the GPU and in the
+    oracle (fp64, its own trajectory): final KL (exact Z) within 1%."""
+    inp = synth.make_inputs(0, dim=3)
+    w = inp.workload
+    Y = dev_y(inp.Y)
+    P = bh.Csr.from_numpy(inp.row_ptr, inp.col, inp.val)
+    u, gains = torch.zeros_like(Y), torch.ones_like(Y)
+    ws = torch.empty(bh.workspace_size_3d(inp.n, inp.nnz), dtype=torch.uint8, device="cuda")
+    y = inp.Y.astype(np.float64)
+    uo, go = np.zeros_like(y), np.ones_like(y)
+    for it in range(w.iters):
+        s = w.schedule(it)
+        bh.step_3d(Y, P, 0.5, s["exaggeration"], s["learning_rate"], s["momentum"], 0.01, u, gains, workspace=ws)
+        oracle.step3(y, uo, go, inp.row_ptr, inp.col, inp.val, 0.5, s["exaggeration"], s["learning_rate"],
+                     s["momentum"], 0.01)
+    klg = oracle.kl3(Y.cpu().numpy(), inp.row_ptr, inp.col, inp.val)
+    klo = oracle.kl3(y, inp.row_ptr, inp.col, inp.val)
+    kl0 = oracle.kl3(inp.Y, inp.row_ptr, inp.col, inp.val)
+    say(f"[kl3] workload 0: gpu {klg:.6f} oracle {klo:.6f} start {kl0:.6f}")
+    assert klg < kl0 and klo < kl0
+    assert abs(klg - klo) <= 0.01 * klo
+
+
+@pytest.mark.parametrize("cid,theta", [(2, 0.5), (4, 0.5)])
+def test_gradient3_full_size_sampled(cid, theta):
+    """1.3M points with a 3-D embedding (early phase, and late phase with 5%
+    duplicates): 4000 sampled gradients against the oracle's traversal of
+    those points, Z and the interaction total from its full pass, the node
+    count exactly."""
+    inp = synth.make_inputs(cid, dim=3, progress=say)
+    n = inp.n
+    alpha = synth.WORKLOADS[cid].schedule(0)["exaggeration"]
+    P = bh.Csr.from_numpy(inp.row_ptr, inp.col, inp.val)
+    ws = torch.empty(bh.workspace_size_3d(n, inp.nnz), dtype=torch.uint8, device="cuda")
+    g, Z = bh.gradient_3d(dev_y(inp.Y), P, theta, alpha, workspace=ws)
+    stats = bh.get_stats(ws)
+    sample = np.sort(np.random.default_rng(3000 + cid).choice(n, size=4000, replace=False))
+    g = g.cpu().numpy()[sample].astype(np.float64)
+    del P, ws
+    torch.cuda.empty_cache()
+    fattr = oracle.attractive3(inp.Y, inp.row_ptr, inp.col, inp.val, rows=sample)
+    with oracle.State3(inp.Y) as s:
+        t = s.tree()
+        b = t.kind == oracle.BUCKET
+        nodes_o = t.nodes + int((t.end[b].astype(np.int64) - t.begin[b]).sum())
+        del t
+        frep, zi, inter = s.repulsive(theta)
+    Zo = oracle.ordered_sum(zi)
+    go = 4.0 * (alpha * fattr - frep[sample] / Zo)
+    err = rel_l2(g, go)
+    say(f"[full3] workload {cid}: rel-L2 {err:.2e}, Z {Z:.9e} vs {Zo:.9e}, interactions "
+        f"{stats['interactions']} vs {int(inter.sum())}, nodes {stats['nodes']} vs {nodes_o}")
+    assert err <= 1e-3
+    assert abs(Z - Zo) <= 1e-5 * Zo
+    assert abs(stats["interactions"] - int(inter.sum())) <= 1e-3 * int(inter.sum())
+    assert stats["nodes"] == nodes_o
+
+
+def test_nonfinite_input3_is_reported():
+    y = synth.random_y3(500, seed=7)
+    y[3, 2] = np.nan
+    rp, col, val = _p_for(y)
+    with pytest.raises(bh.BhtsneError) as e:
+        bh.gradient_3d(dev_y(y), bh.Csr.from_numpy(rp, col, val), 0.5, 1.0)
+    assert e.value.status == bh.BHTSNE_ENONFINITE
