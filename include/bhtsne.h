@@ -151,6 +151,23 @@ int bhtsne_step(float *Y, const bhtsne_csr *P, float theta, float exaggeration, 
                 float momentum, float min_gain, float *update, float *gains, float *grad, double *Z,
                 void *workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation):
+ * bhtsne_step with no workspace argument.  Its scratch space is a fixed
+ * array of bhtsne_noalloc_max_bytes() bytes (64 MiB) in the library's device
+ * image, one per GPU, reserved when the library is loaded and held until the
+ * process ends; the call allocates nothing.  Sizes whose
+ * bhtsne_workspace_size(n, nnz) exceeds it (n above about 249,000 points)
+ * are BHTSNE_EINVAL.  Every call on a GPU shares that GPU's array: calls
+ * that may overlap on one GPU (different streams or threads) race and must
+ * be serialised by the caller; the kernels clear every counter they need,
+ * so what a previous call left in the array does not matter.  Arguments,
+ * results and other errors as bhtsne_step (plain CSR P). */
+size_t bhtsne_noalloc_max_bytes(void);
+int bhtsne_step_noalloc(float *Y, const bhtsne_csr *P, float theta, float exaggeration, float learning_rate,
+                        float momentum, float min_gain, float *update, float *gains, float *grad, double *Z,
+                        hipStream_t stream);
+
 /* Bytes of device memory a layout of P needs (0 if n or nnz is out of range):
  * about 15.5 bytes per stored entry + 560 bytes per point (a row-sorted copy,
  * and room for a sliced copy with 16-bit column offsets and its tables). */

@@ -31,10 +31,12 @@ from ._binding import (  # noqa: F401
     layout_size,
     library_path,
     load_library,
+    noalloc_max_bytes,
     status_string,
     step,
     step_3d,
     step_f64,
+    step_noalloc,
     timing_enable,
     timing_phases,
     timing_read,

@@ -89,6 +89,8 @@ def load_library():
                                       C.c_double, vp, vp, vp, f64p, vp, C.c_size_t, vp]),
         "bhtsne_affinities": (C.c_int, [vp, vp, i64, C.c_int32, C.c_double, vp, vp, vp, i64,
                                         C.POINTER(C.c_int64), vp, vp, C.c_size_t, vp]),
+        "bhtsne_noalloc_max_bytes": (C.c_size_t, []),
+        "bhtsne_step_noalloc": (C.c_int, [vp, C.POINTER(_Csr), f32, f32, f32, f32, f32, vp, vp, vp, f64p, vp]),
         "bhtsne_workspace_size_3d": (C.c_size_t, [i64, i64]),
         "bhtsne_gradient_3d": (C.c_int, [vp, C.POINTER(_Csr), f32, f32, vp, f64p, vp, C.c_size_t, vp]),
         "bhtsne_step_3d": (C.c_int, [vp, C.POINTER(_Csr), f32, f32, f32, f32, f32, vp, vp, vp, f64p, vp,
@@ -361,6 +363,27 @@ def step(Y: torch.Tensor, P, theta: float, exaggeration: float, learning_rate: f
                          _ptr(grad, torch.float32, "grad"), C.byref(z) if return_z else None,
                          _ptr(ws, None, "workspace"), ws.numel(), _stream())
     _check(rc, fn.__name__)
+    return z.value if return_z else None
+
+
+def noalloc_max_bytes() -> int:
+    return int(load_library().bhtsne_noalloc_max_bytes())
+
+
+def step_noalloc(Y: torch.Tensor, P: "Csr", theta: float, exaggeration: float, learning_rate: float,
+                 momentum: float, min_gain: float, update: torch.Tensor, gains: torch.Tensor,
+                 grad: Optional[torch.Tensor] = None, return_z: bool = False):
+    """bhtsne_step_noalloc: bhtsne_step on the library's fixed scratch array
+    (no workspace, nothing allocated); Y, update and gains change in place."""
+    lib = load_library()
+    if not isinstance(P, Csr):
+        raise TypeError("step_noalloc takes P as a Csr")
+    z = C.c_double(0.0)
+    rc = lib.bhtsne_step_noalloc(_ptr(Y, torch.float32, "Y"), P.struct, float(theta), float(exaggeration),
+                                 float(learning_rate), float(momentum), float(min_gain),
+                                 _ptr(update, torch.float32, "update"), _ptr(gains, torch.float32, "gains"),
+                                 _ptr(grad, torch.float32, "grad"), C.byref(z) if return_z else None, _stream())
+    _check(rc, "bhtsne_step_noalloc")
     return z.value if return_z else None
 
 

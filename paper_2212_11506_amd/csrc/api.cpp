@@ -255,6 +255,30 @@ int run(float *Y, const bhtsne_csr *P, float theta, const StepArgs &a, float *up
     return finish(Z, ws, st);
 }
 
+// ------------------------------------------------------------------ fixed scratch
+// Workspace of bhtsne_step_noalloc: one array per device, allocated when the
+// code object is loaded and held until the process ends.  Host code never
+// uses the symbol itself (on the host it names a stand-in, not device
+// memory): the device address is looked up once per device, with that device
+// current, and every launch takes that address.
+constexpr size_t kStaticScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+void *static_scratch()
+{
+    static std::mutex mu;
+    static void *addr[kMaxDevices] = {};
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> g(mu);
+    if (!addr[dev]) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+        addr[dev] = p;
+    }
+    return addr[dev];
+}
+
 constexpr uint64_t kLayoutMagic = 0x62687473654c3031ull; // "bhtseL01"
 
 int stage_segments()
@@ -450,6 +474,25 @@ int bhtsne_step(float *Y, const bhtsne_csr *P, float theta, float exaggeration, 
     if (rc != BHTSNE_OK) return rc;
     StepArgs a{exaggeration, learning_rate, momentum, min_gain, 1};
     return run(Y, P, theta, a, update, gains, grad, Z, workspace, stream);
+}
+
+size_t bhtsne_noalloc_max_bytes(void) { return kStaticScratchBytes; }
+
+int bhtsne_step_noalloc(float *Y, const bhtsne_csr *P, float theta, float exaggeration, float learning_rate,
+                        float momentum, float min_gain, float *update, float *gains, float *grad, double *Z,
+                        hipStream_t stream)
+{
+    int rc = check_csr(P);
+    if (rc != BHTSNE_OK) return rc;
+    if (!Y || !update || !gains) return BHTSNE_EINVAL;
+    rc = check_step_args(theta, exaggeration, learning_rate, momentum, min_gain);
+    if (rc != BHTSNE_OK) return rc;
+    const size_t need = bhtsne_workspace_size(P->n, P->nnz);
+    if (need == 0 || need > kStaticScratchBytes) return BHTSNE_EINVAL;
+    void *ws = static_scratch();
+    if (!ws) return BHTSNE_EDEVICE;
+    StepArgs a{exaggeration, learning_rate, momentum, min_gain, 1};
+    return run(Y, P, theta, a, update, gains, grad, Z, ws, stream);
 }
 
 size_t bhtsne_workspace_size_f64(int64_t n, int64_t nnz)

@@ -254,6 +254,18 @@ def test_bench_refuses_more_than_one_gpu():
     assert r.returncode == 2 and "one GPU" in r.stderr
 
 
+def test_step_noalloc_rejects_bad_arguments_on_the_host():
+    lib = bh.load_library()
+    assert lib.bhtsne_noalloc_max_bytes() == 64 << 20
+    # a size whose workspace exceeds the fixed array, bad optimiser arguments, missing state
+    big = _Csr(300000, 10, FAKE, FAKE, FAKE)
+    small = _Csr(100, 10, FAKE, FAKE, FAKE)
+    for P, lr, upd in ((big, 200.0, FAKE), (small, 0.0, FAKE), (small, 200.0, None)):
+        rc = lib.bhtsne_step_noalloc(C.c_void_p(FAKE), C.byref(P), 0.5, 12.0, lr, 0.5, 0.01,
+                                     C.c_void_p(upd) if upd else None, C.c_void_p(FAKE), None, None, None)
+        assert rc == bh.BHTSNE_EINVAL
+
+
 def test_3d_workspace_size_and_argument_checks():
     lib = bh.load_library()
     assert lib.bhtsne_workspace_size_3d(1, 0) == 0 and lib.bhtsne_workspace_size_3d(1 << 24, 0) == 0
