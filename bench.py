@@ -24,9 +24,11 @@ if ROOT not in sys.path:
 
 METRIC = "BH t-SNE gradient iterations/s at N=1.3M, theta=0.5; repulsive interactions/s"
 HBM_PEAK_GBS = 8000.0
-# fp32 vector peak without packed math (the build disables packed fp32):
-# 256 CUs x 64 lanes x 2 flops (FMA) x 2.4 GHz
-ALU_PEAK_TFLOPS = 256 * 64 * 2 * 2.4e9 / 1e12
+# MI355X's published fp32 vector peak (it counts packed fp32: two lanes' worth
+# per instruction) and the rate without packed math, which this build
+# disables: 256 CUs x 64 lanes x 2 flops (FMA) x 2.4 GHz
+ALU_PEAK_TFLOPS = 157.3
+ALU_PEAK_NONPACKED_TFLOPS = 256 * 64 * 2 * 2.4e9 / 1e12
 # algorithmic flops of one interaction (summary or exact pair): dx, dy (2),
 # d^2 (3), 1 + d^2 (1), reciprocal (1), count x w and w^2 (2), Z (1), forces (4)
 FLOPS_PER_INTERACTION = 14
@@ -59,6 +61,10 @@ def parse():
                          "(for counter collection, which takes one dispatch at a time)")
     ap.add_argument("--copy-calibrate", action="store_true",
                     help="only run device-to-device copies of 1 GiB (for scaling HBM counters)")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the other workloads (0, 1, 3 and 4 at each theta) of the headline run")
+    ap.add_argument("--no-3d", action="store_true", help="skip the 3-D embedding measurement")
+    ap.add_argument("--configs-only", action="store_true", help="measure only the other workloads")
     return ap.parse_args()
 
 
@@ -101,6 +107,204 @@ def measured_traffic(kernel, sources):
                 return None
             return traffic if cells[3] == source_hash(*sources) else None
     return None
+
+
+def gpu_run(inp, theta, steps, warmup, schedule, layout=True):
+    """Iterations of `schedule` on the GPU through the locality layout (the
+    launch configuration of the headline run), inputs resident in HBM: the
+    rate over `steps` timed iterations after `warmup` untimed ones (from the
+    initial state again), the walk's and the attraction's event times, and
+    the interactions per iteration from a replay of the same (deterministic)
+    trajectory with a sync per step."""
+    import numpy as np
+    import torch
+
+    import paper_2212_11506_amd as bh
+
+    dev = torch.device("cuda:0")
+    n, nnz = inp.n, inp.nnz
+    Y0 = torch.from_numpy(inp.Y).to(dev)
+    P = bh.Csr.from_numpy(inp.row_ptr, inp.col, inp.val, device=dev)
+    ws = torch.empty(bh.workspace_size(n, nnz), dtype=torch.uint8, device=dev)
+    if layout:
+        P = bh.Layout(P, Y0, workspace=ws)
+    Y, u, g = Y0.clone(), torch.zeros_like(Y0), torch.ones_like(Y0)
+
+    def reset():
+        Y.copy_(Y0)
+        u.zero_()
+        g.fill_(1.0)
+
+    def run(k, per_step=None):
+        for it in range(k):
+            s = schedule(it)
+            bh.step(Y, P, theta, s["exaggeration"], s["learning_rate"], s["momentum"], 0.01, u, g, workspace=ws)
+            if per_step:
+                per_step(it)
+
+    run(warmup)
+    torch.cuda.synchronize()
+    reset()
+    bh.timing_read(reset=True)
+    bh.timing_phases(["repulsive", "attractive"])
+    bh.timing_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    run(steps)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    bh.timing_enable(False)
+    bh.timing_phases(None)
+    ph = bh.timing_read(reset=True)
+    y_final = Y.cpu().numpy()
+    reset()
+    counts = []
+    run(steps, per_step=lambda it: counts.append(bh.get_stats(ws)["interactions"]))
+    torch.cuda.synchronize()
+    same = bool(np.array_equal(Y.cpu().numpy(), y_final))
+    inter = float(np.mean(counts)) if same else None
+    rep_ms = ph["repulsive"][0] / max(ph["repulsive"][1], 1)
+    att_ms = ph["attractive"][0] / max(ph["attractive"][1], 1)
+    out = {"n": n, "nnz": nnz, "theta": theta, "steps": steps, "iterations_per_s": steps / dt,
+           "ms_per_step": 1e3 * dt / steps, "interactions_per_iteration": inter,
+           "interactions_per_s": inter * steps / dt if inter else None,
+           "repulsive_ms": rep_ms, "attractive_ms": att_ms,
+           "attractive_path": ("sliced tiles" if P.tiles > 0 else "row blocks") if layout else "plain CSR"}
+    if inter:
+        tf = FLOPS_PER_INTERACTION * inter / (rep_ms * 1e-3) / 1e12
+        out["repulsive_tflops"] = tf
+        out["repulsive_frac_alu"] = tf / ALU_PEAK_TFLOPS
+        out["repulsive_frac_alu_nonpacked"] = tf / ALU_PEAK_NONPACKED_TFLOPS
+    out["attractive_model_gbs"] = (8.0 * nnz + 32.0 * n) / (att_ms * 1e-3) / 1e9
+    out["attractive_model_frac_hbm"] = out["attractive_model_gbs"] / HBM_PEAK_GBS
+    del P, ws, Y0, Y, u, g
+    torch.cuda.empty_cache()
+    return out
+
+
+def oracle_sample(inp, theta, iters, schedule, threads=None):
+    """The fp64 oracle (as it stands) on the first `iters` iterations of the
+    same schedule, with the wall time of each of the paper's steps."""
+    import numpy as np
+
+    import oracle
+
+    all_threads = oracle.threads()
+    if threads:
+        oracle.set_threads(threads)
+    try:
+        y = inp.Y.astype(np.float64)
+        u, g = np.zeros_like(y), np.ones_like(y)
+        tot = dict.fromkeys(oracle.STEP_PHASES, 0.0)
+        t0 = time.perf_counter()
+        inter = 0
+        for it in range(iters):
+            s = schedule(it)
+            _, k, _, ms = oracle.step_timed(y, u, g, inp.row_ptr, inp.col, inp.val, theta, s["exaggeration"],
+                                            s["learning_rate"], s["momentum"], 0.01)
+            inter += k
+            for key in tot:
+                tot[key] += ms[key]
+        dt = time.perf_counter() - t0
+        cores = oracle.threads()
+    finally:
+        oracle.set_threads(all_threads)
+    return {"iterations_per_s": iters / dt, "cores": cores, "iterations": iters, "seconds": dt,
+            "interactions_per_s": inter / dt, "step_ms": {k: v / iters for k, v in tot.items()}}
+
+
+def bench_configs(args, log_every=None):
+    """Every workload besides the headline one, each with its own schedule:
+    iterations/s and interactions/s on the GPU, walk and attraction
+    fractions, and the oracle on the host (all cores, single thread for the
+    two small workloads) on a bounded sample of the same run."""
+    import gc
+
+    import synth
+
+    out = {}
+    plan = [(0, [0.5], 50, 10, 2), (1, [0.5], 1000, 3, 1), (4, [0.2, 0.5, 0.8], 100, 1, 0), (3, [0.5], 200, 1, 0)]
+    for cid, thetas, steps, cpu_iters, cpu_single in plan:
+        t0 = time.time()
+        inp = synth.make_inputs(cid, progress=log)
+        w = inp.workload
+        log(f"[bench] workload {cid}: n={inp.n} nnz={inp.nnz} generated in {time.time() - t0:.1f}s")
+        entry = {"workload": f"{w.description} (workload {cid})", "n": inp.n, "nnz": inp.nnz,
+                 "schedule": f"iterations 0..{steps - 1}", "by_theta": {}}
+        for theta in thetas:
+            r = gpu_run(inp, theta, steps, 5 if steps >= 50 else 1, w.schedule)
+            log(f"[bench] workload {cid} theta={theta}: {r['iterations_per_s']:.1f} it/s, "
+                f"{r['interactions_per_s'] or 0:.3e} interactions/s")
+            if not args.no_cpu and cpu_iters:
+                r["oracle"] = oracle_sample(inp, theta, cpu_iters, w.schedule)
+                if cpu_single:
+                    r["oracle_single_thread"] = oracle_sample(inp, theta, cpu_single, w.schedule, threads=1)
+                log(f"[bench] workload {cid} theta={theta}: oracle {r['oracle']['iterations_per_s']:.3f} it/s "
+                    f"on {r['oracle']['cores']} threads")
+            entry["by_theta"][str(theta)] = r
+        out[f"workload_{cid}"] = entry
+        del inp
+        gc.collect()
+    return out
+
+
+def bench_3d(args, steps=200, warmup=5):
+    """The 3-D embedding path on workload 2's P with a 3-D early-phase Y
+    (N(0, 1e-4 I3)): iterations/s over the first `steps` iterations of the
+    schedule on the plain CSR P, with the walk's event time."""
+    import numpy as np
+    import torch
+
+    import paper_2212_11506_amd as bh
+    import synth
+
+    inp = synth.make_inputs(2, dim=3)
+    w = inp.workload
+    n, nnz = inp.n, inp.nnz
+    dev = torch.device("cuda:0")
+    P = bh.Csr.from_numpy(inp.row_ptr, inp.col, inp.val, device=dev)
+    ws = torch.empty(bh.workspace_size_3d(n, nnz), dtype=torch.uint8, device=dev)
+    Y0 = torch.from_numpy(inp.Y).to(dev)
+    Y, u, g = Y0.clone(), torch.zeros_like(Y0), torch.ones_like(Y0)
+
+    def run(k, per_step=None):
+        for it in range(k):
+            s = w.schedule(it)
+            bh.step_3d(Y, P, args.theta, s["exaggeration"], s["learning_rate"], s["momentum"], 0.01, u, g,
+                       workspace=ws)
+            if per_step:
+                per_step(it)
+
+    run(warmup)
+    torch.cuda.synchronize()
+    Y.copy_(Y0)
+    u.zero_()
+    g.fill_(1.0)
+    bh.timing_read(reset=True)
+    bh.timing_phases(None)
+    bh.timing_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    run(steps)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    bh.timing_enable(False)
+    ph = bh.timing_read(reset=True)
+    Y.copy_(Y0)
+    u.zero_()
+    g.fill_(1.0)
+    counts = []
+    run(steps, per_step=lambda it: counts.append(bh.get_stats(ws)["interactions"]))
+    torch.cuda.synchronize()
+    inter = float(np.mean(counts))
+    out = {"workload": "workload 2's P (1.3M points) with a 3-D early-phase Y ~ N(0, 1e-4 I3), plain CSR P",
+           "n": n, "nnz": nnz, "theta": args.theta, "steps": steps, "iterations_per_s": steps / dt,
+           "ms_per_step": 1e3 * dt / steps, "interactions_per_iteration": inter,
+           "phases_ms": {k: v[0] / v[1] for k, v in ph.items() if v[1]}}
+    out["interactions_per_s_walk"] = inter / (out["phases_ms"]["repulsive"] * 1e-3)
+    del P, ws, Y0, Y, u, g
+    torch.cuda.empty_cache()
+    return out
 
 
 def bench_affinities(args, cpu_rows=20000):
@@ -230,6 +434,9 @@ def main():
     bh.load_library()
     if args.affinities_only:
         print(json.dumps({"affinities": bench_affinities(args)}), flush=True)
+        return
+    if args.configs_only:
+        print(json.dumps({"configs": bench_configs(args)}), flush=True)
         return
     w = synth.WORKLOADS[args.workload]
     t0 = time.time()
@@ -361,21 +568,36 @@ def main():
     rep_src = ("k_forces.hip", "k_tree.hip", "common.hpp")
     att_src = ("k_layout.hip", "common.hpp") if not args.plain else ("k_forces.hip", "common.hpp")
     rep = kernels["repulsive"]
+    rep_traffic = measured_traffic("repulsive_kernel", rep_src)
     if inter_total is not None:
         per_launch = inter_total / args.steps
         rep["interactions_per_s"] = per_launch / (rep_ms * 1e-3)
         rep["tflops"] = FLOPS_PER_INTERACTION * rep["interactions_per_s"] / 1e12
         rep["frac_alu"] = rep["tflops"] / ALU_PEAK_TFLOPS
+        rep["frac_alu_nonpacked"] = rep["tflops"] / ALU_PEAK_NONPACKED_TFLOPS
         # the per-interaction byte model (16 B per summary or point + 20 B per
-        # point): nodes come from caches, so this exceeds what HBM moves
+        # point) counts cache hits: the node records stay in the caches, so it
+        # exceeds what HBM can move and is no measure of HBM use
         rep["model16_gbs"] = (16.0 * per_launch + 20.0 * n) / (rep_ms * 1e-3) / 1e9
+    if rep_traffic:
+        # what the walk really moves through HBM (committed FETCH + WRITE counters)
+        rep["measured_gbs"] = rep_traffic / (rep_ms * 1e-3) / 1e9
+        rep["measured_frac_hbm"] = rep["measured_gbs"] / HBM_PEAK_GBS
     # attraction: 8 B per stored entry (column, value) and 32 B per point (row
     # pointers, y_i, output); with the plain CSR path the phase also holds the
     # gradient assembly and update, 72 B per point, which the layout path times
     # as its own phase
     att_bytes = 8.0 * nnz + (104.0 if args.plain else 32.0) * n
-    kernels["attractive"]["gbs"] = att_bytes / (att_ms * 1e-3) / 1e9
-    kernels["attractive"]["frac_hbm"] = kernels["attractive"]["gbs"] / HBM_PEAK_GBS
+    att = kernels["attractive"]
+    att["model_gbs"] = att_bytes / (att_ms * 1e-3) / 1e9
+    att["model_frac_hbm"] = att["model_gbs"] / HBM_PEAK_GBS
+    att_kernels = ("attract_sell_kernel", "attract_rows_kernel") if not args.plain else ("attract_kernel",)
+    att_traffic = [measured_traffic(k, att_src) for k in att_kernels]
+    att["traffic"] = sum(att_traffic) if all(t is not None for t in att_traffic) else None
+    if att["traffic"]:
+        # measured HBM bytes of the phase's kernels over the phase's time
+        att["measured_gbs"] = att["traffic"] / (att_ms * 1e-3) / 1e9
+        att["measured_frac_hbm"] = att["measured_gbs"] / HBM_PEAK_GBS
     if kernels.get("update", {}).get("launches"):
         upd = kernels["update"]
         upd["gbs"] = 72.0 * n / (upd["ms_per_launch"] * 1e-3) / 1e9
@@ -384,34 +606,31 @@ def main():
     dominant = max(("repulsive", "attractive"), key=lambda k: kernels[k]["ms_per_launch"])
     if dominant == "repulsive" and inter_total is not None:
         roof = {"kernel": "repulsive", "bound": "alu", "achieved": rep["tflops"], "peak": ALU_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": rep["frac_alu"],
-                "traffic": measured_traffic("repulsive_kernel", rep_src),
-                "model": f"{FLOPS_PER_INTERACTION} fp32 flops per interaction (summary or exact pair); peak "
-                         "without packed fp32: 256 CUs x 64 lanes x 2 x 2.4 GHz"}
+                "unit": "TFLOP/s", "frac": rep["frac_alu"], "traffic": rep_traffic,
+                "peak_nonpacked": ALU_PEAK_NONPACKED_TFLOPS, "frac_nonpacked": rep["frac_alu_nonpacked"],
+                "measured_frac_hbm": rep.get("measured_frac_hbm"),
+                "model": f"{FLOPS_PER_INTERACTION} fp32 flops per interaction (summary or exact pair); peak: the "
+                         "published fp32 vector rate (packed); peak_nonpacked: 256 CUs x 64 lanes x 2 x 2.4 GHz, "
+                         "the rate without packed fp32, which this build disables"}
     else:
-        roof = {"kernel": "attractive", "bound": "hbm", "achieved": kernels["attractive"]["gbs"],
-                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": kernels["attractive"]["frac_hbm"],
-                "traffic": measured_traffic("attract_sell_kernel" if not args.plain else "attract_kernel", att_src),
-                "model": "8 B per stored entry + %d B per point" % (104 if args.plain else 32)}
+        achieved = att.get("measured_gbs") or att["model_gbs"]
+        roof = {"kernel": "attractive", "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK_GBS, "traffic": att["traffic"],
+                "model": ("measured FETCH_SIZE + WRITE_SIZE bytes" if att.get("measured_gbs") else
+                          "8 B per stored entry + %d B per point" % (104 if args.plain else 32))}
 
     cpu = None
     if not args.no_cpu and args.cpu_iters > 0:
-        import oracle
-
-        y = inp.Y.astype(np.float64)
-        uo = np.zeros_like(y)
-        go = np.ones_like(y)
-        tc = time.perf_counter()
-        for it in range(args.cpu_iters):
-            s = w.schedule(it)
-            oracle.step(y, uo, go, inp.row_ptr, inp.col, inp.val, args.theta, s["exaggeration"],
-                        s["learning_rate"], s["momentum"], 0.01)
-            log(f"[bench] oracle iteration {it} done at {time.perf_counter() - tc:.1f}s")
-        dt = time.perf_counter() - tc
-        cpu = {"value": args.cpu_iters / dt, "unit": "iterations/s", "cores": oracle.threads(),
-               "kind": "oracle",
+        o = oracle_sample(inp, args.theta, args.cpu_iters, w.schedule)
+        log(f"[bench] oracle: {o['iterations_per_s']:.3f} it/s on {o['cores']} threads ({o['seconds']:.1f}s)")
+        cpu = {"value": o["iterations_per_s"], "unit": "iterations/s", "cores": o["cores"], "kind": "oracle",
                "sample": f"first {args.cpu_iters} iterations of the same workload and schedule, "
-                         f"fp64 oracle, {dt:.1f}s"}
+                         f"fp64 oracle, {o['seconds']:.1f}s",
+               "interactions_per_s": o["interactions_per_s"], "step_ms": o["step_ms"]}
+    layout_tiles = None if args.plain else P.tiles
+    layout_entries = None if args.plain else P.entries
+    del P, Pcsr, ws, Y0, Y, u, gains
+    torch.cuda.empty_cache()
 
     out = {
         "metric": METRIC,
@@ -435,13 +654,15 @@ def main():
         "nodes_last": stats_last["nodes"],
         "attractive_path": "plain CSR" if args.plain else "locality layout + LDS staging",
         "layout_build_s": layout_s,
-        "layout_tiles": None if args.plain else P.tiles,
-        "layout_entries": None if args.plain else P.entries,
+        "layout_tiles": layout_tiles,
+        "layout_entries": layout_entries,
         "kernels": kernels,
         "roofline": roof,
         "cpu_baseline": cpu,
         "affinities": None if args.no_affinities else bench_affinities(args),
         "fp64_variant": None if args.no_fp64 else bench_fp64(args, inp),
+        "embedding_3d": None if (args.no_3d or args.workload != 2 or args.n) else bench_3d(args),
+        "configs": None if (args.no_configs or args.workload != 2 or args.n) else bench_configs(args),
     }
     print(json.dumps(out), flush=True)
 
