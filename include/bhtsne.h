@@ -84,6 +84,8 @@ typedef struct bhtsne_layout {
     int64_t tiles;  /* tiles of the (row block x column segment) copy; 0 = row-block path */
     int64_t items;  /* work items of the tiled kernel (runs of tiles sharing a segment) */
     int64_t entries; /* entries of the sliced copy, padding included (0 without tiles) */
+    int64_t windows; /* column windows of the windowed row segments (0 = none; only without tiles) */
+    int64_t segments; /* (row, window) segments of that form */
     uint64_t magic;
 } bhtsne_layout;
 
@@ -183,7 +185,11 @@ size_t bhtsne_layout_size(int64_t n, int64_t nnz);
  * stored entry-major, so that one window of Y in LDS serves many tiles and
  * every load is contiguous (out->tiles > 0, out->items > 0).  The copy is
  * skipped when its padding would exceed a quarter of nnz plus one chunk per
- * slice.  The gradient does not depend on the order; only the speed of the
+ * slice.  Without that copy (rows whose neighbours spread over a large
+ * component), the build lists instead, for each column window of 2^18
+ * points, the (row, entry range) segments of the rows with entries there
+ * (out->windows > 0): the attraction then takes one pass per window, with
+ * that window of Y held in the L2 caches.  The gradient does not depend on the order; only the speed of the
  * attractive step does.
  *   P      the matrix (as for bhtsne_gradient; nnz < 2^31).
  *   Y      device, n x 2, nullable: without it points keep their index order
@@ -327,7 +333,7 @@ int bhtsne_affinities(const int32_t *knn_idx, const float *knn_dist, int64_t n, 
  * size is bhtsne_workspace_size_f64 (larger than the fp32 one: fp64 copies
  * of Y, 40-byte node records).  Same argument checks and errors as the fp32
  * calls (theta, exaggeration, learning_rate, momentum and min_gain are
- * doubles).  No locality layout for this variant. */
+ * doubles).  Its locality layout (bhtsne_layout_build_f64) follows below. */
 typedef struct bhtsne_csr_f64 {
     int64_t n;              /* points; 2 <= n <= 16777215 */
     int64_t nnz;            /* stored entries, >= 0 */
@@ -342,6 +348,33 @@ int bhtsne_gradient_f64(const double *Y, const bhtsne_csr_f64 *P, double theta, 
 int bhtsne_step_f64(double *Y, const bhtsne_csr_f64 *P, double theta, double exaggeration, double learning_rate,
                     double momentum, double min_gain, double *update, double *gains, double *grad, double *Z,
                     void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* A locality layout for the fp64 variant (Attractive Force Computation: the
+ * y_j reads of a row are what bound it).  bhtsne_layout_build_f64 renumbers
+ * the points as bhtsne_layout_build does (connected component, then Morton
+ * order of the fp64 Y when given), stores P's rows in that order with fp64
+ * values and sorted columns, and lists the (row, entry range) segments of
+ * each column window of 2^18 points (out->windows > 0, out->segments > 0);
+ * it builds no sliced copy (out->tiles = 0).  A row longer than 4096 entries
+ * keeps its order, and then no segments are built (out->windows = 0); such
+ * a layout is refused by the two calls below (BHTSNE_EINVAL): use the plain
+ * fp64 calls.  The workspace is bhtsne_workspace_size_f64; layout memory is
+ * bhtsne_layout_size_f64 bytes.  The handle is tagged as an fp64 layout: the
+ * fp32 layout calls refuse it, and these calls refuse an fp32 one.
+ * bhtsne_gradient_layout_f64 / bhtsne_step_layout_f64 are bhtsne_gradient_f64
+ * / bhtsne_step_f64 taking P through such a layout: the attraction runs one
+ * pass per column window on the library's second stream, beside the sort,
+ * tree and walk; results come back in the caller's order.  Errors as the
+ * plain fp64 calls, and BHTSNE_EINPUT from the build for malformed row
+ * pointers. */
+size_t bhtsne_layout_size_f64(int64_t n, int64_t nnz);
+int bhtsne_layout_build_f64(const bhtsne_csr_f64 *P, const double *Y, void *layout_mem, size_t layout_bytes,
+                            bhtsne_layout *out, void *workspace, size_t workspace_bytes, hipStream_t stream);
+int bhtsne_gradient_layout_f64(const double *Y, const bhtsne_layout *layout, double theta, double exaggeration,
+                               double *grad, double *Z, void *workspace, size_t workspace_bytes, hipStream_t stream);
+int bhtsne_step_layout_f64(double *Y, const bhtsne_layout *layout, double theta, double exaggeration,
+                           double learning_rate, double momentum, double min_gain, double *update, double *gains,
+                           double *grad, double *Z, void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * Three-dimensional embeddings (the problem statement allows a two- or

@@ -18,6 +18,7 @@ from ._binding import (  # noqa: F401
     Csr,
     CsrF64,
     Layout,
+    LayoutF64,
     affinities,
     affinities_workspace_size,
     debug_sort,

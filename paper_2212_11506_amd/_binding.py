@@ -34,7 +34,8 @@ class _Csr(C.Structure):
 
 class _Layout(C.Structure):
     _fields_ = [("n", C.c_int64), ("nnz", C.c_int64), ("mem", C.c_void_p), ("bytes", C.c_size_t),
-                ("tiles", C.c_int64), ("items", C.c_int64), ("entries", C.c_int64), ("magic", C.c_uint64)]
+                ("tiles", C.c_int64), ("items", C.c_int64), ("entries", C.c_int64), ("windows", C.c_int64),
+                ("segments", C.c_int64), ("magic", C.c_uint64)]
 
 
 class _Stats(C.Structure):
@@ -91,6 +92,13 @@ def load_library():
                                         C.POINTER(C.c_int64), vp, vp, C.c_size_t, vp]),
         "bhtsne_noalloc_max_bytes": (C.c_size_t, []),
         "bhtsne_step_noalloc": (C.c_int, [vp, C.POINTER(_Csr), f32, f32, f32, f32, f32, vp, vp, vp, f64p, vp]),
+        "bhtsne_layout_size_f64": (C.c_size_t, [i64, i64]),
+        "bhtsne_layout_build_f64": (C.c_int, [C.POINTER(_Csr), vp, vp, C.c_size_t, C.POINTER(_Layout), vp,
+                                              C.c_size_t, vp]),
+        "bhtsne_gradient_layout_f64": (C.c_int, [vp, C.POINTER(_Layout), C.c_double, C.c_double, vp, f64p, vp,
+                                                 C.c_size_t, vp]),
+        "bhtsne_step_layout_f64": (C.c_int, [vp, C.POINTER(_Layout), C.c_double, C.c_double, C.c_double,
+                                             C.c_double, C.c_double, vp, vp, vp, f64p, vp, C.c_size_t, vp]),
         "bhtsne_workspace_size_3d": (C.c_size_t, [i64, i64]),
         "bhtsne_gradient_3d": (C.c_int, [vp, C.POINTER(_Csr), f32, f32, vp, f64p, vp, C.c_size_t, vp]),
         "bhtsne_step_3d": (C.c_int, [vp, C.POINTER(_Csr), f32, f32, f32, f32, f32, vp, vp, vp, f64p, vp,
@@ -185,17 +193,18 @@ def gradient_f64(Y: torch.Tensor, P: "CsrF64", theta: float, exaggeration: float
                  return_z: bool = True):
     """bhtsne_gradient_f64: returns (grad fp64, Z or None)."""
     lib = load_library()
-    if not isinstance(P, CsrF64):
-        raise TypeError("gradient_f64 takes P as a CsrF64")
+    if not isinstance(P, (CsrF64, LayoutF64)):
+        raise TypeError("gradient_f64 takes P as a CsrF64 or a LayoutF64")
     if grad is None:
         grad = torch.empty_like(Y)
     ws = workspace if workspace is not None else torch.empty(workspace_size_f64(P.n, P.nnz), dtype=torch.uint8,
                                                              device=Y.device)
     z = C.c_double(0.0)
-    rc = lib.bhtsne_gradient_f64(_ptr(Y, torch.float64, "Y"), P.struct, float(theta), float(exaggeration),
-                                 _ptr(grad, torch.float64, "grad"), C.byref(z) if return_z else None,
-                                 _ptr(ws, None, "workspace"), ws.numel(), _stream())
-    _check(rc, "bhtsne_gradient_f64")
+    fn = lib.bhtsne_gradient_layout_f64 if isinstance(P, LayoutF64) else lib.bhtsne_gradient_f64
+    rc = fn(_ptr(Y, torch.float64, "Y"), P.struct, float(theta), float(exaggeration),
+            _ptr(grad, torch.float64, "grad"), C.byref(z) if return_z else None,
+            _ptr(ws, None, "workspace"), ws.numel(), _stream())
+    _check(rc, fn.__name__)
     return grad, (z.value if return_z else None)
 
 
@@ -205,17 +214,18 @@ def step_f64(Y: torch.Tensor, P: "CsrF64", theta: float, exaggeration: float, le
              return_z: bool = False):
     """bhtsne_step_f64: one fp64 iteration in place on Y, update and gains."""
     lib = load_library()
-    if not isinstance(P, CsrF64):
-        raise TypeError("step_f64 takes P as a CsrF64")
+    if not isinstance(P, (CsrF64, LayoutF64)):
+        raise TypeError("step_f64 takes P as a CsrF64 or a LayoutF64")
     ws = workspace if workspace is not None else torch.empty(workspace_size_f64(P.n, P.nnz), dtype=torch.uint8,
                                                              device=Y.device)
     z = C.c_double(0.0)
-    rc = lib.bhtsne_step_f64(_ptr(Y, torch.float64, "Y"), P.struct, float(theta), float(exaggeration),
-                             float(learning_rate), float(momentum), float(min_gain),
-                             _ptr(update, torch.float64, "update"), _ptr(gains, torch.float64, "gains"),
-                             _ptr(grad, torch.float64, "grad"), C.byref(z) if return_z else None,
-                             _ptr(ws, None, "workspace"), ws.numel(), _stream())
-    _check(rc, "bhtsne_step_f64")
+    fn = lib.bhtsne_step_layout_f64 if isinstance(P, LayoutF64) else lib.bhtsne_step_f64
+    rc = fn(_ptr(Y, torch.float64, "Y"), P.struct, float(theta), float(exaggeration),
+            float(learning_rate), float(momentum), float(min_gain),
+            _ptr(update, torch.float64, "update"), _ptr(gains, torch.float64, "gains"),
+            _ptr(grad, torch.float64, "grad"), C.byref(z) if return_z else None,
+            _ptr(ws, None, "workspace"), ws.numel(), _stream())
+    _check(rc, fn.__name__)
     return z.value if return_z else None
 
 
@@ -261,8 +271,37 @@ class Layout:
         return int(self._s.entries)
 
     @property
+    def windows(self) -> int:
+        return int(self._s.windows)
+
+    @property
+    def segments(self) -> int:
+        return int(self._s.segments)
+
+    @property
     def struct(self):
         return C.byref(self._s)
+
+
+class LayoutF64(Layout):
+    """A locality layout of an fp64 P (CsrF64) for the fp64 variant's calls:
+    relabelled rows with fp64 values and windowed segments, no sliced copy."""
+
+    def __init__(self, P: "CsrF64", Y: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None):
+        lib = load_library()
+        if not isinstance(P, CsrF64):
+            raise TypeError("LayoutF64 takes P as a CsrF64")
+        self.n, self.nnz = P.n, P.nnz
+        need = int(lib.bhtsne_layout_size_f64(P.n, P.nnz))
+        if need == 0:
+            raise BhtsneError(BHTSNE_EINVAL, "bhtsne_layout_size_f64")
+        self.mem = torch.empty(need, dtype=torch.uint8, device="cuda")
+        ws = workspace if workspace is not None else torch.empty(workspace_size_f64(P.n, P.nnz), dtype=torch.uint8,
+                                                                 device="cuda")
+        self._s = _Layout()
+        rc = lib.bhtsne_layout_build_f64(P.struct, _ptr(Y, torch.float64, "Y"), _ptr(self.mem), need,
+                                         C.byref(self._s), _ptr(ws), ws.numel(), _stream())
+        _check(rc, "bhtsne_layout_build_f64")
 
 
 def layout_size(n: int, nnz: int) -> int:

@@ -301,14 +301,33 @@ bool tile_path_enabled()
     return v;
 }
 
-int check_layout(const bhtsne_layout *lay)
+// BHTSNE_WINDOWS=0 keeps the row-block attractive kernel where windowed
+// segments would be built (for comparisons and tests)
+bool window_path_enabled()
 {
-    if (!lay || lay->magic != kLayoutMagic || !lay->mem || !aligned(lay->mem)) return BHTSNE_EINVAL;
+    static bool v = [] {
+        const char *e = std::getenv("BHTSNE_WINDOWS");
+        return !(e && std::atoi(e) == 0);
+    }();
+    return v;
+}
+
+constexpr uint64_t kLayoutMagic64 = 0x62687473654c3634ull; // "bhtseL64": an fp64 layout
+
+// vbytes: 4 for the fp32 calls' layouts, 8 for the fp64 variant's
+int check_layout(const bhtsne_layout *lay, int vbytes = 4)
+{
+    if (!lay || lay->magic != (vbytes == 8 ? kLayoutMagic64 : kLayoutMagic) || !lay->mem || !aligned(lay->mem))
+        return BHTSNE_EINVAL;
     if (lay->n < 2 || lay->n > kMaxPoints || lay->nnz < 0) return BHTSNE_EINVAL;
-    const LayoutView v = layout_view(nullptr, lay->n, lay->nnz);
+    const LayoutView v = layout_view(nullptr, lay->n, lay->nnz, vbytes);
+    if (vbytes == 8 && lay->tiles != 0) return BHTSNE_EINVAL;
     if (lay->bytes < v.bytes) return BHTSNE_EINVAL;
     if (lay->tiles < 0 || lay->tiles > v.max_tiles) return BHTSNE_EINVAL;
     if (lay->items < 0 || lay->items > lay->tiles || (lay->tiles > 0) != (lay->items > 0)) return BHTSNE_EINVAL;
+    if (lay->windows < 0 || lay->windows > kMaxWindows || (lay->windows > 0 && lay->tiles > 0)) return BHTSNE_EINVAL;
+    if (lay->segments < 0 || lay->segments > v.max_segments || (lay->windows > 0) != (lay->segments > 0))
+        return BHTSNE_EINVAL;
     return BHTSNE_OK;
 }
 
@@ -343,6 +362,54 @@ int run64(double *Y, const bhtsne_csr_f64 *P, double theta, const StepArgsT<doub
     return finish(Z, ws, st);
 }
 
+// The fp64 variant through a layout: the windowed-segment attraction (or the
+// plain one when the layout has no segments) on the second stream, forked
+// after the codes, beside the sort, tree and walk.
+int run_layout64(double *Y, const bhtsne_layout *lay, double theta, const StepArgsT<double> &a, double *update,
+                 double *gains, double *grad, double *Z, void *ws, hipStream_t st)
+{
+    const int64_t n = lay->n;
+    const Layout L = make_layout(n, lay->nnz, 8);
+    const LayoutView lv = layout_view(lay->mem, n, lay->nnz, 8);
+    {
+        PhaseTimer pt(BHTSNE_PHASE_BBOX_MORTON, st);
+        launch_bbox(Y, n, ws, L, st);
+        launch_morton(static_cast<const double *>(Y), n, lv.rank, ws, L, st);
+    }
+    Side *side = overlap_enabled() ? side_stream() : nullptr;
+    std::unique_lock<std::mutex> lk;
+    if (side) {
+        lk = std::unique_lock<std::mutex>(side->mu);
+        if (hipEventRecord(side->fork, st) != hipSuccess || hipStreamWaitEvent(side->st, side->fork, 0) != hipSuccess)
+            return BHTSNE_EDEVICE;
+    }
+    const hipStream_t sa = side ? side->st : st;
+    {
+        PhaseTimer pt(BHTSNE_PHASE_ATTRACTIVE, sa);
+        launch_attract_windows<double>(lv, n, attract_blocks(side != nullptr, 0), int(lay->windows), ws, L, sa);
+    }
+    if (side && hipEventRecord(side->join, sa) != hipSuccess) return BHTSNE_EDEVICE;
+    {
+        PhaseTimer pt(BHTSNE_PHASE_SORT, st);
+        launch_sort(n, static_cast<const double *>(Y), ws, L, st);
+    }
+    {
+        PhaseTimer pt(BHTSNE_PHASE_TREE, st);
+        launch_tree<2, double>(n, theta * theta, ws, L, TreeDebug{}, st);
+    }
+    {
+        PhaseTimer pt(BHTSNE_PHASE_REPULSIVE, st);
+        launch_repulsive<2, double>(n, repulsive_self_test(theta), ws, L, st);
+    }
+    if (side && hipStreamWaitEvent(st, side->join, 0) != hipSuccess) return BHTSNE_EDEVICE;
+    if (lk.owns_lock()) lk.unlock();
+    {
+        PhaseTimer pt(BHTSNE_PHASE_UPDATE, st);
+        launch_update(lv, n, a, Y, update, gains, grad, ws, L, st);
+    }
+    return finish(Z, ws, st);
+}
+
 int run_layout(float *Y, const bhtsne_layout *lay, float theta, const StepArgs &a, float *update, float *gains,
                float *grad, double *Z, void *ws, hipStream_t st)
 {
@@ -373,7 +440,7 @@ int run_layout(float *Y, const bhtsne_layout *lay, float theta, const StepArgs &
     {
         PhaseTimer pt(BHTSNE_PHASE_ATTRACTIVE, sa);
         launch_attract_layout(lv, n, lay->nnz, tiles, int(lay->items), attract_blocks(side != nullptr, int(lay->items)),
-                              stage_segments(), ws, L, sa);
+                              stage_segments(), int(lay->windows), ws, L, sa);
     }
     if (side && hipEventRecord(side->join, sa) != hipSuccess) return BHTSNE_EDEVICE;
     if (fork < 1) {
@@ -688,8 +755,85 @@ int bhtsne_layout_build(const bhtsne_csr *P, const float *Y, void *layout_mem, s
     out->tiles = tiled ? plan.tiles : 0;
     out->items = tiled ? plan.items : 0;
     out->entries = tiled ? plan.entries : 0;
+    const bool windowed = !tiled && plan.windows > 0 && window_path_enabled();
+    out->windows = windowed ? plan.windows : 0;
+    out->segments = windowed ? plan.segments : 0;
     out->magic = kLayoutMagic;
     return BHTSNE_OK;
+}
+
+size_t bhtsne_layout_size_f64(int64_t n, int64_t nnz)
+{
+    if (n < 2 || n > kMaxPoints || nnz < 0) return 0;
+    return layout_view(nullptr, n, nnz, 8).bytes;
+}
+
+int bhtsne_layout_build_f64(const bhtsne_csr_f64 *P, const double *Y, void *layout_mem, size_t layout_bytes,
+                            bhtsne_layout *out, void *workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    int rc = check_csr_f64(P);
+    if (rc != BHTSNE_OK) return rc;
+    if (!out || !layout_mem || !aligned(layout_mem)) return BHTSNE_EINVAL;
+    if (layout_bytes < bhtsne_layout_size_f64(P->n, P->nnz)) return BHTSNE_EINVAL;
+    if (P->nnz + 3 * P->n + 4 >= (int64_t(1) << 31)) return BHTSNE_EINVAL;
+    rc = check_ws_f64(P->n, P->nnz, workspace, workspace_bytes);
+    if (rc != BHTSNE_OK) return rc;
+    const Layout L = make_layout(P->n, P->nnz, 8);
+    const LayoutView lv = layout_view(layout_mem, P->n, P->nnz, 8);
+    TilePlan plan;
+    const int built = launch_layout_build(P->row_ptr, P->col, P->val, P->n, P->nnz, Y, lv, &plan, workspace, L, stream);
+    if (built == 1) return BHTSNE_EINPUT;
+    if (built != 0) return BHTSNE_EDEVICE;
+    Header h;
+    rc = read_header(workspace, &h, stream);
+    if (rc != BHTSNE_OK) return rc;
+    if (h.flags & (kErrLookback | kErrRange)) return BHTSNE_EDEVICE;
+    out->n = P->n;
+    out->nnz = P->nnz;
+    out->mem = layout_mem;
+    out->bytes = layout_bytes;
+    out->tiles = out->items = out->entries = 0;
+    const bool windowed = plan.windows > 0 && window_path_enabled();
+    out->windows = windowed ? plan.windows : 0;
+    out->segments = windowed ? plan.segments : 0;
+    out->magic = kLayoutMagic64;
+    return BHTSNE_OK;
+}
+
+static int check_layout64_step(const bhtsne_layout *layout, const double *Y, double theta, double exaggeration,
+                               void *workspace, size_t workspace_bytes)
+{
+    int rc = check_layout(layout, 8);
+    if (rc != BHTSNE_OK) return rc;
+    if (layout->windows == 0) return BHTSNE_EINVAL; // rows out of window order: use the plain fp64 calls
+    if (!Y) return BHTSNE_EINVAL;
+    if (!std::isfinite(theta) || theta < 0.0) return BHTSNE_EINVAL;
+    if (!std::isfinite(exaggeration) || !(exaggeration > 0.0)) return BHTSNE_EINVAL;
+    return check_ws_f64(layout->n, layout->nnz, workspace, workspace_bytes);
+}
+
+int bhtsne_gradient_layout_f64(const double *Y, const bhtsne_layout *layout, double theta, double exaggeration,
+                               double *grad, double *Z, void *workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    int rc = check_layout64_step(layout, Y, theta, exaggeration, workspace, workspace_bytes);
+    if (rc != BHTSNE_OK) return rc;
+    if (!grad) return BHTSNE_EINVAL;
+    StepArgsT<double> a{exaggeration, 0.0, 0.0, 0.0, 0};
+    return run_layout64(const_cast<double *>(Y), layout, theta, a, nullptr, nullptr, grad, Z, workspace, stream);
+}
+
+int bhtsne_step_layout_f64(double *Y, const bhtsne_layout *layout, double theta, double exaggeration,
+                           double learning_rate, double momentum, double min_gain, double *update, double *gains,
+                           double *grad, double *Z, void *workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    int rc = check_layout64_step(layout, Y, theta, exaggeration, workspace, workspace_bytes);
+    if (rc != BHTSNE_OK) return rc;
+    if (!update || !gains) return BHTSNE_EINVAL;
+    if (!std::isfinite(learning_rate) || !(learning_rate > 0.0)) return BHTSNE_EINVAL;
+    if (!std::isfinite(momentum) || momentum < 0.0 || !(momentum < 1.0)) return BHTSNE_EINVAL;
+    if (!std::isfinite(min_gain) || min_gain < 0.0) return BHTSNE_EINVAL;
+    StepArgsT<double> a{exaggeration, learning_rate, momentum, min_gain, 1};
+    return run_layout64(Y, layout, theta, a, update, gains, grad, Z, workspace, stream);
 }
 
 int bhtsne_gradient_layout(const float *Y, const bhtsne_layout *layout, float theta, float exaggeration, float *grad,

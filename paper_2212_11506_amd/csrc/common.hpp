@@ -62,6 +62,10 @@ constexpr int kItemMaxTiles = 128; // tiles of one segment handled by one block
 constexpr int kSellSlice = 64;
 constexpr int kSellChunk = 4 * kSellSlice;
 constexpr int kSlicesPerTile = kTileRows / kSellSlice;
+// windowed segments: column windows of 2^18 points (2 MB of Y, resident in
+// one XCD's 4 MB L2 beside the stream of P); n < 2^24 gives at most 64
+constexpr int kWinShift = 18;
+constexpr int kMaxWindows = 64;
 
 // Status words of the decoupled look-back: 2 flag bits + 30-bit count.
 constexpr uint32_t kFlagAggregate = 1u << 30;
@@ -91,7 +95,8 @@ struct Header {
     uint32_t attract_next; // next item of the persistent attractive kernel
     uint32_t ticket_eval;  // blocks done of an evaluation kernel (exact Z, KL)
     uint32_t max_depth;    // deepest leaf level of the last tree (32: a bucket of identical codes)
-    uint32_t pad[3];
+    uint32_t unsorted;     // layout build: some row's columns are not in window order
+    uint32_t pad[2];
     double eval;           // result of the last evaluation call
 };
 
@@ -147,7 +152,7 @@ inline Layout make_layout(int64_t n, int64_t nnz, int fbytes = 4, int dim = 2)
     // + 8 bytes: the 2-D walk loads 32 bytes at a record's offset
     L.nodes = take((dim == 3 ? kNodeBytes3 : (fbytes == 8 ? kNodeBytes64 : kNodeBytes)) * size_t(2 * n) + 8);
     L.frep = take(size_t(dim) * size_t(fbytes) * size_t(n));
-    L.fattr = take(8 * size_t(n));
+    L.fattr = take(2 * size_t(fbytes) * size_t(n));
     // partial attractive sums, one per (tile, sorted row slot): up to
     // kTileMaxSeg tiles of kTileRows rows per row block
     L.partial = dim == 3 ? take(0) : take(8 * size_t((n + kTileRows - 1) / kTileRows) * kTileRows * kTileMaxSeg);

@@ -305,6 +305,8 @@ __global__ __launch_bounds__(kRepBlock) void repulsive_kernel(
 }
 
 
+constexpr int kAttB = 4;
+
 // D = 2, T = float: the path's plain-CSR attraction; T = double: the fp64
 // variant; D = 3: 3-D embeddings.  Coordinates are handled component by
 // component (unrolled).
@@ -334,24 +336,38 @@ __global__ __launch_bounds__(256) void attract_kernel(
                 s = s < 0 ? 0 : s;
                 e = e > nnz ? nnz : e;
             }
-            for (int64_t k = s + sub; k < e; k += G) {
-                // P is streamed once per call: keep it out of the caches that hold Y
-                const int32_t j = __builtin_nontemporal_load(col + k);
-                if (uint32_t(j) >= uint32_t(n)) {
-                    atomicOr(&hdr->flags, kErrRange);
-                    continue;
+            // kAttB entries per lane at a time: their loads, then their gathers,
+            // are in flight together
+            for (int64_t k0 = s + sub; k0 < e; k0 += kAttB * G) {
+                int32_t j[kAttB];
+                T p[kAttB];
+#pragma unroll
+                for (int u = 0; u < kAttB; ++u) {
+                    const int64_t k = k0 + u * G;
+                    // P is streamed once per call: keep it out of the caches that hold Y
+                    j[u] = k < e ? __builtin_nontemporal_load(col + k) : 0;
+                    p[u] = k < e ? __builtin_nontemporal_load(val + k) : T(0);
+                    if (uint32_t(j[u]) >= uint32_t(n)) {
+                        atomicOr(&hdr->flags, kErrRange);
+                        j[u] = 0;
+                        p[u] = T(0);
+                    }
                 }
-                const T p = __builtin_nontemporal_load(val + k);
-                const V yj = ycopy[j];
-                T dv[D];
+                V yj[kAttB];
 #pragma unroll
-                for (int d = 0; d < D; ++d) dv[d] = coord(yi, d) - coord(yj, d);
-                T d2 = dv[D - 1] * dv[D - 1];
+                for (int u = 0; u < kAttB; ++u) yj[u] = ycopy[j[u]];
 #pragma unroll
-                for (int d = D - 2; d >= 0; --d) d2 = fma(dv[d], dv[d], d2);
-                const T pw = p * recip(T(1) + d2);
+                for (int u = 0; u < kAttB; ++u) {
+                    T dv[D];
 #pragma unroll
-                for (int d = 0; d < D; ++d) f[d] = fma(pw, dv[d], f[d]);
+                    for (int d = 0; d < D; ++d) dv[d] = coord(yi, d) - coord(yj[u], d);
+                    T d2 = dv[D - 1] * dv[D - 1];
+#pragma unroll
+                    for (int d = D - 2; d >= 0; --d) d2 = fma(dv[d], dv[d], d2);
+                    const T pw = p[u] * recip(T(1) + d2);
+#pragma unroll
+                    for (int d = 0; d < D; ++d) f[d] = fma(pw, dv[d], f[d]);
+                }
             }
         }
 #pragma unroll

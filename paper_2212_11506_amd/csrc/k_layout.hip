@@ -22,6 +22,13 @@
 //       and gathers y_j from LDS;
 //     - update_kernel combines F_attr, F_rep and Z in the caller's order.
 //
+// When the rows of a block reach too many column windows for the sliced
+// copy (no tile locality: a row's neighbours spread over a large component),
+// the build makes windowed row segments instead: for each column window of
+// 2^18 points (2 MB of Y, held in an XCD's L2), the list of (row, entry range)
+// of the rows with entries there.  The attraction then takes one launch per
+// window; the y_j it gathers stay in L2 while P streams through once.
+//
 // The order affects only speed: any permutation gives the same sums.
 #include "common.hpp"
 #include "kernels.hpp"
@@ -240,12 +247,14 @@ constexpr int32_t kNoColumn = 0x7fffffff;
 
 // One wave per new row: copy the old row with renumbered columns, padded to a
 // multiple of 4 entries.
+// V: the value type of P (float; double for the fp64 variant's layouts)
+template <typename V>
 __global__ __launch_bounds__(256) void layout_copy_kernel(const int64_t *__restrict__ row_ptr,
-                                                          const int32_t *__restrict__ col, const float *__restrict__ val,
+                                                          const int32_t *__restrict__ col, const V *__restrict__ val,
                                                           const uint32_t *__restrict__ perm,
                                                           const uint32_t *__restrict__ rank,
                                                           const int64_t *__restrict__ new_ptr, int64_t n, int64_t cap,
-                                                          int32_t *__restrict__ new_col, float *__restrict__ new_val)
+                                                          int32_t *__restrict__ new_col, V *__restrict__ new_val)
 {
     const int lane = lane_id();
     for (int64_t r = (int64_t(blockIdx.x) * blockDim.x + threadIdx.x) / kWave; r < n;
@@ -262,34 +271,41 @@ __global__ __launch_bounds__(256) void layout_copy_kernel(const int64_t *__restr
                 new_val[o] = val[s + t];
             } else { // padding entries sort to the end and contribute nothing
                 new_col[o] = kNoColumn;
-                new_val[o] = 0.0f;
+                new_val[o] = V(0);
             }
         }
     }
 }
 
+template <typename V>
 __global__ void layout_sentinel_kernel(const int64_t *__restrict__ new_ptr, int64_t n, int32_t *__restrict__ col,
-                                       float *__restrict__ val)
+                                       V *__restrict__ val)
 {
     const int64_t e = new_ptr[n];
     for (int t = 0; t < 4; ++t) {
         col[e + t] = kNoColumn;
-        val[e + t] = 0.0f;
+        val[e + t] = V(0);
     }
 }
 
 // One block per row: bitonic sort of the row's entries by (renumbered) column
 // in LDS.  Sorted rows let the staged kernel skip, wave by wave, the register
-// slots whose columns lie outside the LDS segment in hand.  Rows longer than
-// kSortRowMax keep their order (only speed depends on it).
-constexpr int kSortRowMax = 4096;
+// slots whose columns lie outside the LDS segment in hand, and give each
+// column window one contiguous range of the row (windowed segments).  Rows
+// longer than kSortRowMax keep their order: the staged kernel is as correct
+// on them, and the segment build then falls back to it.  With fp32 values,
+// 8192 covers every row the input-similarity step can produce (k + 4096);
+// fp64 values fit 4096 in the same 64 KB of LDS.
+template <typename V> constexpr int sort_row_max() { return sizeof(V) == 4 ? 8192 : 4096; }
 
+template <typename V>
 __global__ __launch_bounds__(256) void layout_sort_rows_kernel(const int64_t *__restrict__ row_ptr,
-                                                               int32_t *__restrict__ col, float *__restrict__ val,
+                                                               int32_t *__restrict__ col, V *__restrict__ val,
                                                                int64_t n)
 {
+    constexpr int kSortRowMax = sort_row_max<V>();
     __shared__ int32_t sk[kSortRowMax];
-    __shared__ float sv[kSortRowMax];
+    __shared__ V sv[kSortRowMax];
     for (int64_t r = blockIdx.x; r < n; r += gridDim.x) {
         const int64_t s = row_ptr[r], len = row_ptr[r + 1] - s;
         if (len < 2 || len > kSortRowMax) continue; // block-uniform
@@ -298,7 +314,7 @@ __global__ __launch_bounds__(256) void layout_sort_rows_kernel(const int64_t *__
         __syncthreads();
         for (int t = threadIdx.x; t < size; t += blockDim.x) {
             sk[t] = t < len ? col[s + t] : 0x7fffffff;
-            sv[t] = t < len ? val[s + t] : 0.0f;
+            sv[t] = t < len ? val[s + t] : V(0);
         }
         __syncthreads();
         for (int k = 2; k <= size; k <<= 1)
@@ -311,7 +327,7 @@ __global__ __launch_bounds__(256) void layout_sort_rows_kernel(const int64_t *__
                         if ((a > b) == up) {
                             sk[t] = b;
                             sk[u] = a;
-                            const float x = sv[t];
+                            const V x = sv[t];
                             sv[t] = sv[u];
                             sv[u] = x;
                         }
@@ -489,6 +505,180 @@ __global__ __launch_bounds__(256) void sell_copy_kernel(const int64_t *__restric
     }
 }
 
+// ------------------------------------------------------------------ windowed row segments
+constexpr int kSegBlock = 256; // rows per block of the segment build
+
+// Windows touched by each row (bit w: some real entry has its column in
+// window w), and per (window, row block) the number of rows touching it,
+// stored window-major: cnt[w * nblk + block].
+// A row whose real entries are not in window order (longer than the row
+// sort takes) sets *unsorted: its windows would not be contiguous ranges.
+__global__ __launch_bounds__(kSegBlock) void seg_mask_kernel(const int64_t *__restrict__ row_ptr,
+                                                             const int32_t *__restrict__ col, int64_t n, int nw,
+                                                             int64_t nblk, uint64_t *__restrict__ mask,
+                                                             int64_t *__restrict__ cnt, uint32_t *__restrict__ unsorted)
+{
+    __shared__ uint32_t s_cnt[kSegBlock / kWave][kMaxWindows];
+    const int64_t r = int64_t(blockIdx.x) * kSegBlock + threadIdx.x;
+    uint64_t m = 0;
+    bool ordered = true;
+    if (r < n) {
+        uint32_t last = 0;
+        for (int64_t k = row_ptr[r]; k < row_ptr[r + 1]; ++k) {
+            const int32_t c = col[k];
+            if (c != kNoColumn && uint32_t(c) < uint32_t(n)) {
+                const uint32_t win = uint32_t(c) >> kWinShift;
+                ordered &= win >= last;
+                last = win;
+                m |= 1ull << win;
+            }
+        }
+        mask[r] = m;
+    }
+    if (ballot(!ordered) && lane_id() == 0) atomicOr(unsorted, 1u);
+    const int w = threadIdx.x / kWave;
+    for (int k = 0; k < nw; ++k) {
+        const uint32_t c = uint32_t(__builtin_popcountll(ballot((m >> k) & 1u)));
+        if (lane_id() == 0) s_cnt[w][k] = c;
+    }
+    __syncthreads();
+    for (int k = threadIdx.x; k < nw; k += kSegBlock) {
+        uint32_t t = 0;
+        for (int q = 0; q < kSegBlock / kWave; ++q) t += s_cnt[q][k];
+        cnt[int64_t(k) * nblk + blockIdx.x] = t;
+    }
+}
+
+// Each row writes its segments at their window-major positions: the block's
+// offset for the window plus the row's rank among the block's rows that touch
+// it, so every window's segments are in row order.  The entry range of a
+// window within the (column-sorted) row is found by walking the row once.
+__global__ __launch_bounds__(kSegBlock) void seg_fill_kernel(const int64_t *__restrict__ row_ptr,
+                                                             const int32_t *__restrict__ col, int64_t n, int nw,
+                                                             int64_t nblk, const uint64_t *__restrict__ mask,
+                                                             const int64_t *__restrict__ off, int64_t cap,
+                                                             uint32_t *__restrict__ seg_row,
+                                                             uint32_t *__restrict__ seg_start,
+                                                             uint32_t *__restrict__ seg_len)
+{
+    __shared__ uint32_t s_cnt[kSegBlock / kWave][kMaxWindows];
+    const int64_t r = int64_t(blockIdx.x) * kSegBlock + threadIdx.x;
+    const uint64_t m = r < n ? mask[r] : 0ull;
+    const int w = threadIdx.x / kWave;
+    const uint64_t lt = (lane_id() == 0) ? 0ull : (~0ull >> (kWave - lane_id()));
+    for (int k = 0; k < nw; ++k) {
+        const uint32_t c = uint32_t(__builtin_popcountll(ballot((m >> k) & 1u)));
+        if (lane_id() == 0) s_cnt[w][k] = c;
+    }
+    __syncthreads();
+    int64_t e = 0, stop = 0;
+    if (r < n) {
+        e = row_ptr[r];
+        stop = row_ptr[r + 1];
+    }
+    for (int k = 0; k < nw; ++k) {
+        const bool has = (m >> k) & 1u;
+        const uint64_t b = ballot(has);
+        if (!has) continue;
+        uint32_t rank = uint32_t(__builtin_popcountll(b & lt));
+        for (int q = 0; q < w; ++q) rank += s_cnt[q][k];
+        // the row's entries in window k: skip those below it, take those in it
+        while (e < stop && (col[e] == kNoColumn || (uint32_t(col[e]) >> kWinShift) < uint32_t(k))) ++e;
+        const int64_t first = e;
+        while (e < stop && col[e] != kNoColumn && (uint32_t(col[e]) >> kWinShift) == uint32_t(k)) ++e;
+        const int64_t pos = off[int64_t(k) * nblk + blockIdx.x] + rank;
+        if (pos < cap) {
+            seg_row[pos] = uint32_t(r);
+            seg_start[pos] = uint32_t(first);
+            seg_len[pos] = uint32_t(e - first);
+        }
+    }
+}
+
+// window starts: wstart[w] = offset of (window w, block 0); wstart[nw] = total
+__global__ void seg_windows_kernel(const int64_t *__restrict__ off, int nw, int64_t nblk, const int64_t *__restrict__ total,
+                                   int64_t *__restrict__ wstart)
+{
+    const int k = threadIdx.x;
+    if (k < nw) wstart[k] = off[int64_t(k) * nblk];
+    if (k == nw) wstart[k] = *total;
+}
+
+template <typename T> __global__ __launch_bounds__(256) void zero_vec2_kernel(vec2_t<T> *__restrict__ f, int64_t n)
+{
+    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x)
+        f[i] = make_vec2(T(0), T(0));
+}
+
+__device__ inline float wrecip(float x) { return __builtin_amdgcn_rcpf(x); }
+// 1/x in fp64 for x >= 1: the approximate reciprocal and two Newton-Raphson
+// steps, within about an ulp of the quotient
+__device__ inline double wrecip(double x)
+{
+    double r = __builtin_amdgcn_rcp(x);
+    r = fma(r, fma(-x, r, 1.0), r);
+    r = fma(r, fma(-x, r, 1.0), r);
+    return x != __builtin_huge_val() ? r : 0.0;
+}
+
+// One window: kWinG lanes per segment sum p_ij w_ij (y_i - y_j) over the
+// segment's entries (strided, then a fixed butterfly) and add it to F_attr of
+// the row.  Segments of one window belong to distinct rows, so the add needs
+// no atomic; windows run in order, one launch each.
+constexpr int kWinG = 16;
+constexpr int kWinB = 4;
+
+template <typename T>
+__global__ __launch_bounds__(256) void attract_window_kernel(
+    const int64_t *__restrict__ wstart, int w, const uint32_t *__restrict__ seg_row,
+    const uint32_t *__restrict__ seg_start, const uint32_t *__restrict__ seg_len, const int32_t *__restrict__ col,
+    const T *__restrict__ val, const vec2_t<T> *__restrict__ ycopy, int64_t n, vec2_t<T> *__restrict__ fattr)
+{
+    const int64_t s0 = wstart[w], s1 = wstart[w + 1];
+    const int sub = lane_id() % kWinG;
+    const int64_t per = int64_t(gridDim.x) * (256 / kWinG);
+    for (int64_t s = s0 + (int64_t(blockIdx.x) * 256 + threadIdx.x) / kWinG; s < s1; s += per) {
+        const uint32_t r = seg_row[s];
+        const int64_t a = seg_start[s], e = a + seg_len[s];
+        const vec2_t<T> yi = ycopy[r < uint32_t(n) ? r : 0];
+        T fx = T(0), fy = T(0);
+        // kWinB entries per lane at a time: their loads, then their gathers, are
+        // in flight together (a segment's entries are few per lane, so one at a
+        // time would leave the lane waiting out every latency in turn)
+        for (int64_t k0 = a + sub; k0 < e; k0 += kWinB * kWinG) {
+            int32_t j[kWinB];
+            T p[kWinB];
+#pragma unroll
+            for (int u = 0; u < kWinB; ++u) {
+                const int64_t k = k0 + u * kWinG;
+                j[u] = k < e ? __builtin_nontemporal_load(col + k) : 0;
+                p[u] = k < e ? __builtin_nontemporal_load(val + k) : T(0);
+            }
+            vec2_t<T> yj[kWinB];
+#pragma unroll
+            for (int u = 0; u < kWinB; ++u) yj[u] = ycopy[uint32_t(j[u]) < uint32_t(n) ? j[u] : 0];
+#pragma unroll
+            for (int u = 0; u < kWinB; ++u) {
+                const T dx = yi.x - yj[u].x, dy = yi.y - yj[u].y;
+                const T pw = p[u] * wrecip(T(1) + fma(dx, dx, dy * dy));
+                fx = fma(pw, dx, fx);
+                fy = fma(pw, dy, fy);
+            }
+        }
+#pragma unroll
+        for (int o = kWinG / 2; o > 0; o >>= 1) {
+            fx += __shfl_xor(fx, o, kWinG);
+            fy += __shfl_xor(fy, o, kWinG);
+        }
+        if (sub == 0 && r < uint32_t(n)) {
+            vec2_t<T> f = fattr[r];
+            f.x += fx;
+            f.y += fy;
+            fattr[r] = f;
+        }
+    }
+}
+
 // ------------------------------------------------------------------ staged attraction
 constexpr int kAttG = 16; // lanes per row
 constexpr int kAttV = 4;  // entries per 16-byte vector slot
@@ -548,7 +738,7 @@ __global__ __launch_bounds__(kAttBlock) void attract_staged_kernel(
     int32_t ve[kAttRG], ov[kAttRG];
 #pragma unroll
     for (int r = 0; r < kAttRG; ++r) {
-        const bool sorted = re[r] - rs[r] <= kSortRowMax;
+        const bool sorted = re[r] - rs[r] <= sort_row_max<float>();
         ve[r] = sorted ? re[r] : rs[r];
         ov[r] = sorted ? rs[r] + kSpan : rs[r];
     }
@@ -831,39 +1021,41 @@ __global__ __launch_bounds__(256) void attract_rows_kernel(const float2 *__restr
 // In the caller's order: g = 4 (alpha F_attr - F_rep / Z), then the gains /
 // momentum update of the optimiser (when a.update).  F_attr of a point is
 // that of its row in layout order.
-__global__ __launch_bounds__(256) void update_kernel(const float2 *__restrict__ fattr_lay,
+template <typename T>
+__global__ __launch_bounds__(256) void update_kernel(const vec2_t<T> *__restrict__ fattr_lay,
                                                      const uint32_t *__restrict__ rank,
-                                                     const float2 *__restrict__ frep, const Header *__restrict__ hdr,
-                                                     int64_t n, StepArgs a, float2 *__restrict__ Y,
-                                                     float2 *__restrict__ upd, float2 *__restrict__ gains,
-                                                     float2 *__restrict__ grad)
+                                                     const vec2_t<T> *__restrict__ frep, const Header *__restrict__ hdr,
+                                                     int64_t n, StepArgsT<T> a, vec2_t<T> *__restrict__ Y,
+                                                     vec2_t<T> *__restrict__ upd, vec2_t<T> *__restrict__ gains,
+                                                     vec2_t<T> *__restrict__ grad)
 {
+    using V = vec2_t<T>;
     const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
     if (i >= n) return;
-    const float inv_z = float(1.0 / hdr->Z);
+    const T inv_z = T(1.0 / hdr->Z);
     const uint32_t r = rank[i];
-    const float2 fa = r < uint32_t(n) ? fattr_lay[r] : make_float2(0.0f, 0.0f);
-    const float2 fr = frep[i];
-    const float gx = 4.0f * (a.alpha * fa.x - fr.x * inv_z);
-    const float gy = 4.0f * (a.alpha * fa.y - fr.y * inv_z);
-    if (grad) grad[i] = make_float2(gx, gy);
+    const V fa = r < uint32_t(n) ? fattr_lay[r] : make_vec2(T(0), T(0));
+    const V fr = frep[i];
+    const T gx = T(4) * (a.alpha * fa.x - fr.x * inv_z);
+    const T gy = T(4) * (a.alpha * fa.y - fr.y * inv_z);
+    if (grad) grad[i] = make_vec2(gx, gy);
     if (a.update) {
-        float2 u = upd[i], gn = gains[i];
-        const float2 y = Y[i];
-        gn.x = (u.x * gx < 0.0f) ? gn.x + 0.2f : gn.x * 0.8f;
-        gn.y = (u.y * gy < 0.0f) ? gn.y + 0.2f : gn.y * 0.8f;
-        gn.x = fmaxf(gn.x, a.min_gain);
-        gn.y = fmaxf(gn.y, a.min_gain);
+        V u = upd[i], gn = gains[i];
+        const V y = Y[i];
+        gn.x = (u.x * gx < T(0)) ? gn.x + T(0.2) : gn.x * T(0.8);
+        gn.y = (u.y * gy < T(0)) ? gn.y + T(0.2) : gn.y * T(0.8);
+        gn.x = gn.x > a.min_gain ? gn.x : a.min_gain;
+        gn.y = gn.y > a.min_gain ? gn.y : a.min_gain;
         u.x = a.momentum * u.x - a.learning_rate * gn.x * gx;
         u.y = a.momentum * u.y - a.learning_rate * gn.y * gy;
-        Y[i] = make_float2(y.x + u.x, y.y + u.y);
+        Y[i] = make_vec2(y.x + u.x, y.y + u.y);
         upd[i] = u;
         gains[i] = gn;
     }
 }
 
 // ------------------------------------------------------------------ launchers
-LayoutView layout_view(void *mem, int64_t n, int64_t nnz)
+LayoutView layout_view(void *mem, int64_t n, int64_t nnz, int vbytes)
 {
     LayoutView v;
     size_t off = 0;
@@ -875,7 +1067,7 @@ LayoutView layout_view(void *mem, int64_t n, int64_t nnz)
     size_t o_perm = take(4 * size_t(n)), o_rank = take(4 * size_t(n)), o_ptr = take(8 * size_t(n + 1));
     // rows are padded to multiples of 4 entries, plus one 4-entry sentinel vector at the end
     const size_t cap = size_t(nnz) + 3 * size_t(n) + 4;
-    size_t o_col = take(4 * cap), o_val = take(4 * cap);
+    size_t o_col = take(4 * cap), o_val = take(size_t(vbytes) * cap);
     // tiled copy: at most kTileMaxSeg tiles per row block, sliced
     const int64_t blocks = (n + kTileRows - 1) / kTileRows;
     v.max_tiles = blocks * kTileMaxSeg;
@@ -894,12 +1086,16 @@ LayoutView layout_view(void *mem, int64_t n, int64_t nnz)
            o_wu = take(16 * size_t(v.max_tiles) * (kTileRows / kWave)), o_tc = take(2 * size_t(v.max_entries)),
            o_tv = take(4 * size_t(v.max_entries));
     v.bytes = off;
+    // windowed segments reuse the sliced copy's memory (tcol, then tval)
+    const size_t seg_bytes = v.bytes - o_tc;
+    v.max_segments = int64_t((seg_bytes - 8 * (kMaxWindows + 1) - 4 * 256) / 12);
     if (mem) {
         v.perm = at<uint32_t>(mem, o_perm);
         v.rank = at<uint32_t>(mem, o_rank);
         v.row_ptr = at<int64_t>(mem, o_ptr);
         v.col = at<int32_t>(mem, o_col);
         v.val = at<float>(mem, o_val);
+        v.val64 = at<double>(mem, o_val);
         v.blk_seg_lo = at<int32_t>(mem, o_lo);
         v.blk_nseg = at<int32_t>(mem, o_ns);
         v.blk_tiles = at<int32_t>(mem, o_bt);
@@ -918,6 +1114,14 @@ LayoutView layout_view(void *mem, int64_t n, int64_t nnz)
         v.wave_units = at<int4>(mem, o_wu);
         v.tcol = at<uint16_t>(mem, o_tc);
         v.tval = at<float>(mem, o_tv);
+        size_t o = o_tc;
+        v.wstart = at<int64_t>(mem, o);
+        o = align_up(o + 8 * (kMaxWindows + 1), 256);
+        v.seg_row = at<uint32_t>(mem, o);
+        o = align_up(o + 4 * size_t(v.max_segments), 256);
+        v.seg_start = at<uint32_t>(mem, o);
+        o = align_up(o + 4 * size_t(v.max_segments), 256);
+        v.seg_len = at<uint32_t>(mem, o);
     }
     return v;
 }
@@ -1078,10 +1282,50 @@ static int build_tiles(const LayoutView &lv, int64_t n, TilePlan *plan, void *ws
     return 0;
 }
 
-int launch_layout_build(const int64_t *row_ptr, const int32_t *col, const float *val, int64_t n, int64_t nnz,
-                        const float *Y, const LayoutView &lv, TilePlan *plan, void *ws, const Layout &L,
+// Windowed row segments of a built (sorted, padded) layout, for rows without
+// tile locality; plan->windows stays 0 when they do not fit the memory.
+static int build_windows(const LayoutView &lv, int64_t n, TilePlan *plan, void *ws, const Layout &L, hipStream_t st)
+{
+    plan->windows = 0;
+    plan->segments = 0;
+    const int nw = int((n + (int64_t(1) << kWinShift) - 1) >> kWinShift);
+    if (nw < 1 || nw > kMaxWindows) return 0;
+    const int64_t nblk = (n + kSegBlock - 1) / kSegBlock;
+    uint64_t *mask = at<uint64_t>(ws, L.codes0);   // n words
+    int64_t *cnt = at<int64_t>(ws, L.codes1);      // nw * nblk <= n / 4 words
+    int64_t *off = reinterpret_cast<int64_t *>(at<double>(ws, L.psum)); // nw * nblk + 1 words
+    int64_t *tsum = at<int64_t>(ws, L.scan_sum);
+    const int64_t m = int64_t(nw) * nblk;
+    Header *hdr = at<Header>(ws, L.header);
+    flag_clear_kernel<<<1, 1, 0, st>>>(&hdr->unsorted);
+    seg_mask_kernel<<<unsigned(nblk), kSegBlock, 0, st>>>(lv.row_ptr, lv.col, n, nw, nblk, mask, cnt, &hdr->unsorted);
+    const int64_t tiles = (m + kI64Tile - 1) / kI64Tile;
+    i64_reduce_kernel<<<unsigned(tiles), 256, 0, st>>>(cnt, m, tsum);
+    i64_top_kernel<<<1, 256, 0, st>>>(tsum, tiles, off + m);
+    i64_down_kernel<<<unsigned(tiles), 256, 0, st>>>(cnt, m, tsum, off);
+    int64_t total = 0;
+    uint32_t unsorted = 0;
+    if (hipMemcpyAsync(&total, off + m, 8, hipMemcpyDeviceToHost, st) != hipSuccess) return -1;
+    if (hipMemcpyAsync(&unsorted, &hdr->unsorted, 4, hipMemcpyDeviceToHost, st) != hipSuccess) return -1;
+    if (hipStreamSynchronize(st) != hipSuccess) return -1;
+    // rows out of window order, or more segments than the memory holds: keep the row-block kernel
+    if (unsorted || total > lv.max_segments || total >= (int64_t(1) << 32)) return 0;
+    seg_fill_kernel<<<unsigned(nblk), kSegBlock, 0, st>>>(lv.row_ptr, lv.col, n, nw, nblk, mask, off, lv.max_segments,
+                                                          lv.seg_row, lv.seg_start, lv.seg_len);
+    seg_windows_kernel<<<1, kMaxWindows + 1, 0, st>>>(off, nw, nblk, off + m, lv.wstart);
+    if (hipStreamSynchronize(st) != hipSuccess) return -1;
+    if (hipGetLastError() != hipSuccess) return -1;
+    plan->windows = nw;
+    plan->segments = total;
+    return 0;
+}
+
+template <typename V>
+int launch_layout_build(const int64_t *row_ptr, const int32_t *col, const V *val, int64_t n, int64_t nnz,
+                        const V *Y, const LayoutView &lv, TilePlan *plan, void *ws, const Layout &L,
                         hipStream_t st)
 {
+    V *lval = sizeof(V) == 4 ? reinterpret_cast<V *>(lv.val) : reinterpret_cast<V *>(lv.val64);
     Header *hdr = at<Header>(ws, L.header);
     uint32_t *parent = at<uint32_t>(ws, L.split_b);
     uint32_t *changed = at<uint32_t>(ws, L.split_e);
@@ -1116,7 +1360,7 @@ int launch_layout_build(const int64_t *row_ptr, const int32_t *col, const float 
     sort_reset_kernel<<<1, 256, 0, st>>>(hdr, at<uint32_t>(ws, L.hist));
     keys_hist_kernel<<<unsigned(L.sort_tiles), kSortBlock, 0, st>>>(keys, n, at<uint32_t>(ws, L.hist),
                                                                     at<uint32_t>(ws, L.status), L.sort_tiles);
-    launch_sort(n, Y ? Y : reinterpret_cast<const float *>(at<float2>(ws, L.ycopy)), ws, L, st);
+    launch_sort(n, Y ? Y : reinterpret_cast<const V *>(at<char>(ws, L.ycopy)), ws, L, st);
     // new order -> rank, row lengths, row pointers, relabelled rows
     const uint32_t *perm_ws = at<uint32_t>(ws, L.idx0);
     if (hipMemcpyAsync(lv.perm, perm_ws, 4 * size_t(n), hipMemcpyDeviceToDevice, st) != hipSuccess) return -1;
@@ -1128,12 +1372,43 @@ int launch_layout_build(const int64_t *row_ptr, const int32_t *col, const float 
     i64_top_kernel<<<1, 256, 0, st>>>(tsum, tiles, lv.row_ptr + n);
     i64_down_kernel<<<unsigned(tiles), 256, 0, st>>>(len, n, tsum, lv.row_ptr);
     const int64_t cap = nnz + 3 * n + 4;
-    layout_copy_kernel<<<gw, 256, 0, st>>>(row_ptr, col, val, lv.perm, lv.rank, lv.row_ptr, n, cap, lv.col, lv.val);
-    layout_sentinel_kernel<<<1, 1, 0, st>>>(lv.row_ptr, n, lv.col, lv.val);
-    layout_sort_rows_kernel<<<unsigned(n < 65535 * 16 ? n : 65535 * 16), 256, 0, st>>>(lv.row_ptr, lv.col, lv.val, n);
+    layout_copy_kernel<V><<<gw, 256, 0, st>>>(row_ptr, col, val, lv.perm, lv.rank, lv.row_ptr, n, cap, lv.col, lval);
+    layout_sentinel_kernel<V><<<1, 1, 0, st>>>(lv.row_ptr, n, lv.col, lval);
+    layout_sort_rows_kernel<V><<<unsigned(n < 65535 * 16 ? n : 65535 * 16), 256, 0, st>>>(lv.row_ptr, lv.col, lval, n);
     if (hipGetLastError() != hipSuccess) return -1;
-    return build_tiles(lv, n, plan, ws, L, st);
+    if (sizeof(V) == 4) { // the sliced copy holds fp32 values
+        const int rc = build_tiles(lv, n, plan, ws, L, st);
+        if (rc != 0 || plan->tiled) return rc;
+    } else {
+        *plan = TilePlan{};
+    }
+    return build_windows(lv, n, plan, ws, L, st);
 }
+template int launch_layout_build<float>(const int64_t *, const int32_t *, const float *, int64_t, int64_t,
+                                        const float *, const LayoutView &, TilePlan *, void *, const Layout &,
+                                        hipStream_t);
+template int launch_layout_build<double>(const int64_t *, const int32_t *, const double *, int64_t, int64_t,
+                                         const double *, const LayoutView &, TilePlan *, void *, const Layout &,
+                                         hipStream_t);
+
+// One launch per column window, after F_attr is cleared (layout order).
+template <typename T>
+void launch_attract_windows(const LayoutView &lv, int64_t n, int blocks, int windows, void *ws, const Layout &L,
+                            hipStream_t st)
+{
+    vec2_t<T> *fattr = at<vec2_t<T>>(ws, L.fattr);
+    const T *val = sizeof(T) == 4 ? reinterpret_cast<const T *>(lv.val) : reinterpret_cast<const T *>(lv.val64);
+    zero_vec2_kernel<T><<<unsigned(std::min<int64_t>((n + 255) / 256, 4096)), 256, 0, st>>>(fattr, n);
+    // a grid that fills the chip; blocks stride over the window's segments
+    const unsigned grid = unsigned(std::max(1, blocks) * 8);
+    for (int w = 0; w < windows; ++w)
+        attract_window_kernel<T><<<grid, 256, 0, st>>>(lv.wstart, w, lv.seg_row, lv.seg_start, lv.seg_len, lv.col, val,
+                                                       at<vec2_t<T>>(ws, L.ycopy), n, fattr);
+}
+template void launch_attract_windows<float>(const LayoutView &, int64_t, int, int, void *, const Layout &,
+                                            hipStream_t);
+template void launch_attract_windows<double>(const LayoutView &, int64_t, int, int, void *, const Layout &,
+                                             hipStream_t);
 
 template <int B, int S, int RG>
 static void launch_staged(const LayoutView &lv, int64_t n, int64_t nnz, int max_segs, void *ws, const Layout &L,
@@ -1146,8 +1421,12 @@ static void launch_staged(const LayoutView &lv, int64_t n, int64_t nnz, int max_
 }
 
 void launch_attract_layout(const LayoutView &lv, int64_t n, int64_t nnz, int tiles, int items, int blocks,
-                           int max_segs, void *ws, const Layout &L, hipStream_t st)
+                           int max_segs, int windows, void *ws, const Layout &L, hipStream_t st)
 {
+    if (tiles == 0 && windows > 0) {
+        launch_attract_windows<float>(lv, n, blocks, windows, ws, L, st);
+        return;
+    }
     if (tiles > 0) {
         const unsigned grid = unsigned(blocks < items ? blocks : items);
         attract_sell_kernel<<<grid, kTileBlock, 0, st>>>(lv.item_tiles, lv.item_units, lv.wave_units, lv.tile_blk,
@@ -1162,15 +1441,19 @@ void launch_attract_layout(const LayoutView &lv, int64_t n, int64_t nnz, int til
     launch_staged<1024, 16384, 2>(lv, n, nnz, max_segs, ws, L, st);
 }
 
-void launch_update(const LayoutView &lv, int64_t n, const StepArgs &a, float *Y, float *upd, float *gains,
-                   float *grad, void *ws, const Layout &L, hipStream_t st)
+template <typename T>
+void launch_update(const LayoutView &lv, int64_t n, const StepArgsT<T> &a, T *Y, T *upd, T *gains, T *grad,
+                   void *ws, const Layout &L, hipStream_t st)
 {
-    // both attractive kernels leave F_attr per row in layout order
-    update_kernel<<<unsigned((n + 255) / 256), 256, 0, st>>>(
-        at<float2>(ws, L.fattr), lv.rank, at<float2>(ws, L.frep),
-        at<Header>(ws, L.header), n, a,
-        reinterpret_cast<float2 *>(Y), reinterpret_cast<float2 *>(upd), reinterpret_cast<float2 *>(gains),
-        reinterpret_cast<float2 *>(grad));
+    // every attractive kernel of a layout leaves F_attr per row in layout order
+    using V = vec2_t<T>;
+    update_kernel<T><<<unsigned((n + 255) / 256), 256, 0, st>>>(
+        at<V>(ws, L.fattr), lv.rank, at<V>(ws, L.frep), at<Header>(ws, L.header), n, a, reinterpret_cast<V *>(Y),
+        reinterpret_cast<V *>(upd), reinterpret_cast<V *>(gains), reinterpret_cast<V *>(grad));
 }
+template void launch_update<float>(const LayoutView &, int64_t, const StepArgsT<float> &, float *, float *, float *,
+                                   float *, void *, const Layout &, hipStream_t);
+template void launch_update<double>(const LayoutView &, int64_t, const StepArgsT<double> &, double *, double *,
+                                    double *, double *, void *, const Layout &, hipStream_t);
 
 } // namespace bht

@@ -29,7 +29,8 @@ struct LayoutView {
     uint32_t *rank = nullptr; // original index -> new position
     int64_t *row_ptr = nullptr;
     int32_t *col = nullptr;
-    float *val = nullptr;
+    float *val = nullptr;           // fp32 values (fp32 layouts)
+    double *val64 = nullptr;        // the same region as fp64 values (the fp64 variant's layouts)
     // tiled copy: rows in blocks of kTileRows, columns in segments of kTileSeg
     // points; one tile = (row block, segment), sliced into units of 64 rows
     int32_t *blk_seg_lo = nullptr;  // [blocks] first segment of a row block
@@ -51,6 +52,13 @@ struct LayoutView {
     uint16_t *tcol = nullptr;       // [max entries] column offset in the segment
     float *tval = nullptr;          // [max entries]
     int64_t max_tiles = 0, max_entries = 0;
+    // windowed row segments (built instead of the sliced copy when rows have
+    // no tile locality), carved from the sliced copy's memory: per column
+    // window w, the segments [wstart[w], wstart[w + 1]) of the rows that have
+    // entries in it, each {row, first entry, entry count} of the relabelled CSR
+    int64_t *wstart = nullptr;      // [kMaxWindows + 1]
+    uint32_t *seg_row = nullptr, *seg_start = nullptr, *seg_len = nullptr;
+    int64_t max_segments = 0;
     size_t bytes = 0;
 };
 
@@ -59,6 +67,8 @@ struct TilePlan {
     bool tiled = false;
     int32_t blocks = 0, tiles = 0, items = 0;
     int64_t entries = 0;
+    int32_t windows = 0;   // column windows of the windowed segments (0: none)
+    int64_t segments = 0;
 };
 
 template <typename T> void launch_bbox(const T *Y, int64_t n, void *ws, const Layout &L, hipStream_t st);
@@ -96,19 +106,27 @@ template <int D, typename T>
 void launch_attract(const int64_t *row_ptr, const int32_t *col, const T *val, int64_t n, int64_t nnz,
                     const StepArgsT<T> &a, T *Y, T *upd, T *gains, T *grad, void *ws, const Layout &L, hipStream_t st);
 
-LayoutView layout_view(void *mem, int64_t n, int64_t nnz);
+// vbytes: 4 (fp32 values) or 8 (the fp64 variant's layouts)
+LayoutView layout_view(void *mem, int64_t n, int64_t nnz, int vbytes = 4);
 // Builds the layout (synchronises the stream); fills *plan with the tile tables' sizes.
 // Returns 0, 1 when P's row pointers are malformed (nothing else was read), or -1 on a HIP error.
-int launch_layout_build(const int64_t *row_ptr, const int32_t *col, const float *val, int64_t n, int64_t nnz,
-                        const float *Y, const LayoutView &lv, TilePlan *plan, void *ws, const Layout &L,
+// V = double builds no sliced copy (only the relabelled rows and windowed segments).
+template <typename V>
+int launch_layout_build(const int64_t *row_ptr, const int32_t *col, const V *val, int64_t n, int64_t nnz,
+                        const V *Y, const LayoutView &lv, TilePlan *plan, void *ws, const Layout &L,
                         hipStream_t st);
+// attraction through windowed segments: F_attr in layout order (ws fattr)
+template <typename T>
+void launch_attract_windows(const LayoutView &lv, int64_t n, int blocks, int windows, void *ws, const Layout &L,
+                            hipStream_t st);
 // Attractive forces through a layout: the streaming tile kernel when the
 // layout has tiles (tiles > 0, items > 0), else the row-block kernel.
 // `blocks`: grid of the persistent sliced kernel (items are taken from a counter)
 void launch_attract_layout(const LayoutView &lv, int64_t n, int64_t nnz, int tiles, int items, int blocks,
-                           int max_segs, void *ws, const Layout &L, hipStream_t st);
-void launch_update(const LayoutView &lv, int64_t n, const StepArgs &a, float *Y, float *upd, float *gains,
-                   float *grad, void *ws, const Layout &L, hipStream_t st);
+                           int max_segs, int windows, void *ws, const Layout &L, hipStream_t st);
+template <typename T>
+void launch_update(const LayoutView &lv, int64_t n, const StepArgsT<T> &a, T *Y, T *upd, T *gains, T *grad,
+                   void *ws, const Layout &L, hipStream_t st);
 
 // input similarities from neighbour lists: search, own-row sort, pairs and
 // row pointers (row_ptr[n] = nnz); then, once the caller's arrays are known to

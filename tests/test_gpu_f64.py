@@ -135,3 +135,103 @@ def test_f64_rejects_bad_arguments():
     with pytest.raises(bh.BhtsneError) as e:
         bh.gradient_f64(bad, P, 0.5, 1.0)
     assert e.value.status == bh.BHTSNE_ENONFINITE
+
+
+# ------------------------------------------------------------------ the fp64 layout
+def _ring64(n, seed, m=3):
+    rp, col, val = synth.ring_p(n, seed, m=m)
+    return rp, col, val
+
+
+@pytest.mark.parametrize("case", ["c0", "late20k", "ring300k"])
+def test_gradient_through_f64_layout(case):
+    """The fp64 variant through its locality layout (relabelled rows with fp64
+    values, windowed segments): the same 1e-9 / 1e-12 bars against the oracle,
+    and the same Z as the plain fp64 call (same tree and walk).  ring300k: a
+    ring P over a random Y, two column windows."""
+    if case == "c0":
+        inp = synth.make_inputs(0)
+        y, (rp, col, val) = _y64(inp.Y, 11), (inp.row_ptr, inp.col, inp.val)
+    elif case == "late20k":
+        y = CASES["late20k"]()
+        rp, col, val = _p_for(y.shape[0])
+    else:
+        y = _y64(synth.random_y(300_000, seed=12, scale=2.0), 12)
+        rp, col, val = _ring64(300_000, 12)
+    n = y.shape[0]
+    P = _p64(rp, col, val)
+    Y = torch.from_numpy(y).to(DEV)
+    ws = torch.empty(bh.workspace_size_f64(n, col.size), dtype=torch.uint8, device=DEV)
+    lay = bh.LayoutF64(P, Y, workspace=ws)
+    assert lay.tiles == 0 and lay.windows == (n + (1 << 18) - 1) >> 18 and lay.segments > 0
+    g, Z = bh.gradient_f64(Y, lay, 0.5, 12.0, workspace=ws)
+    gp, Zp = bh.gradient_f64(Y, P, 0.5, 12.0, workspace=ws)
+    go, Zo, _, _ = oracle.gradient(y, rp, col, val, 0.5, 12.0)
+    err = rel_l2(g.cpu().numpy(), go)
+    say(f"[f64 layout] {case}: {lay.windows} windows, {lay.segments} segments, rel-L2 {err:.2e}, "
+        f"Z rel {abs(Z - Zo) / Zo:.2e}")
+    assert err <= 1e-9 and abs(Z - Zo) <= 1e-12 * Zo
+    assert Z == Zp and rel_l2(g.cpu().numpy(), gp.cpu().numpy()) <= 1e-12
+
+
+def test_f64_layout_steps_track_plain_steps():
+    inp = synth.make_inputs(0)
+    w = inp.workload
+    y = _y64(inp.Y, 13)
+    P = _p64(inp.row_ptr, inp.col, inp.val)
+    Ya, Yb = torch.from_numpy(y).to(DEV), torch.from_numpy(y).to(DEV)
+    lay = bh.LayoutF64(P, Ya)
+    ua, ub = torch.zeros_like(Ya), torch.zeros_like(Ya)
+    ga, gb = torch.ones_like(Ya), torch.ones_like(Ya)
+    for it in range(10):
+        s = w.schedule(it)
+        bh.step_f64(Ya, lay, 0.5, s["exaggeration"], s["learning_rate"], s["momentum"], 0.01, ua, ga)
+        bh.step_f64(Yb, P, 0.5, s["exaggeration"], s["learning_rate"], s["momentum"], 0.01, ub, gb)
+    err = rel_l2(Ya.cpu().numpy() - y, Yb.cpu().numpy() - y)
+    say(f"[f64 layout] 10 steps against the plain calls: displacement rel-L2 {err:.2e}")
+    assert err <= 1e-10
+
+
+def test_f64_and_fp32_layouts_are_not_interchangeable():
+    inp = synth.make_inputs(0)
+    P64 = _p64(inp.row_ptr, inp.col, inp.val)
+    Y64 = torch.from_numpy(_y64(inp.Y, 14)).to(DEV)
+    P32 = bh.Csr.from_numpy(inp.row_ptr, inp.col, inp.val)
+    Y32 = torch.from_numpy(inp.Y).to(DEV)
+    lay64 = bh.LayoutF64(P64, Y64)
+    lay32 = bh.Layout(P32, Y32)
+    lay32.__class__ = bh.LayoutF64  # the fp64 calls with an fp32 handle
+    with pytest.raises(bh.BhtsneError) as e:
+        bh.gradient_f64(Y64, lay32, 0.5, 1.0)
+    assert e.value.status == bh.BHTSNE_EINVAL
+    lay64.__class__ = bh.Layout  # the fp32 calls with an fp64 handle
+    with pytest.raises(bh.BhtsneError) as e:
+        bh.gradient(Y32, lay64, 0.5, 1.0)
+    assert e.value.status == bh.BHTSNE_EINVAL
+
+
+def test_f64_layout_with_a_row_too_long_to_sort_is_refused():
+    """A row of 5000 entries is longer than the fp64 row sort takes (4096):
+    no segments, and the layout calls refuse the handle; the plain calls
+    still serve such a P."""
+    n = 300_000
+    rp, col, val = synth.ring_p(n, 15, m=3)
+    import scipy.sparse as sp
+    P = sp.csr_matrix((val.astype(np.float64), col, rp), shape=(n, n))
+    others = np.random.default_rng(15).choice(np.arange(1, n), size=5000, replace=False)
+    H = sp.csr_matrix((np.full(10000, 1e-7), (np.r_[np.zeros(5000, int), others], np.r_[others, np.zeros(5000, int)])),
+                      shape=(n, n))
+    P = (P + H).tocsr()
+    P.sum_duplicates()
+    P.sort_indices()
+    P.data /= P.data.sum()
+    y = _y64(synth.random_y(n, seed=15), 15)
+    Pd = bh.CsrF64.from_numpy(P.indptr.astype(np.int64), P.indices.astype(np.int32), P.data, device=DEV)
+    Y = torch.from_numpy(y).to(DEV)
+    lay = bh.LayoutF64(Pd, Y)
+    assert lay.windows == 0
+    with pytest.raises(bh.BhtsneError) as e:
+        bh.gradient_f64(Y, lay, 0.5, 1.0)
+    assert e.value.status == bh.BHTSNE_EINVAL
+    g, Z = bh.gradient_f64(Y, Pd, 0.5, 1.0)
+    assert torch.isfinite(g).all() and Z > 0

@@ -80,6 +80,42 @@ def _layout_arrays(lay, tiles=False):
 NO_COLUMN = 0x7FFFFFFF
 
 
+def _tcol_offset(n, nnz):
+    """Byte offset of the sliced copy's column array in the layout memory (the
+    windowed segments reuse that region), and the end of the layout."""
+    off = 0
+
+    def take(nbytes):
+        nonlocal off
+        o = off
+        off = (off + nbytes + 255) // 256 * 256
+        return o
+
+    cap = nnz + 3 * n + 4
+    for nbytes in (4 * n, 4 * n, 8 * (n + 1), 4 * cap, 4 * cap):
+        take(nbytes)
+    blocks = (n + TILE_ROWS - 1) // TILE_ROWS
+    max_tiles = blocks * TILE_MAX_SEG
+    max_units = max_tiles * SLICES
+    max_entries = nnz + nnz // 4 + CHUNK * SLICES * max_tiles + CHUNK
+    for nbytes in (4 * blocks, 4 * blocks, 4 * blocks * TILE_MAX_SEG, 4 * max_tiles, 4 * max_tiles, 4 * max_tiles,
+                   8 * max_tiles, 4 * max_tiles * TILE_ROWS, 2 * max_tiles * TILE_ROWS, 2 * max_tiles * TILE_ROWS,
+                   4 * max_units, 4 * max_units, 4 * max_units, 4 * max_units, 16 * max_tiles, 16 * max_tiles * 16):
+        take(nbytes)
+    o_tc = take(2 * max_entries)
+    take(4 * max_entries)
+    return o_tc, off
+
+
+def _window_region_offset(lay):
+    return _tcol_offset(lay.n, lay.nnz)[0]
+
+
+def _max_segments(lay):
+    o_tc, end = _tcol_offset(lay.n, lay.nnz)
+    return (end - o_tc - 8 * 65 - 4 * 256) // 12
+
+
 def _hub_p(n, seed, sizes=(300, 450, 5000)):
     """Symmetric P whose first rows hold many more entries than the register slots
     (and one more than the in-LDS row sort takes)."""
@@ -330,12 +366,12 @@ def _subprocess_gradient(env_extra, n=None, wide=False):
         "else:\n"
         "    inp = synth.make_inputs(1, n=%r); y, rp, col, val = inp.Y, inp.row_ptr, inp.col, inp.val\n"
         "Y = torch.from_numpy(y).cuda(); P = bh.Csr.from_numpy(rp, col, val)\n"
-        "lay = bh.Layout(P, Y); print('tiles', lay.tiles)\n"
+        "lay = bh.Layout(P, Y); print('tiles', lay.tiles, 'windows', lay.windows, 'segments', lay.segments)\n"
         "g, Z = bh.gradient(Y, lay, 0.5, 12.0)\n"
         "go, Zo, _, _ = oracle.gradient(y, rp, col, val, 0.5, 12.0)\n"
         "e = np.linalg.norm(g.cpu().numpy() - go) / np.linalg.norm(go)\n"
         "print('relL2', e); assert e <= 1e-3 and abs(Z - Zo) <= 1e-5 * Zo\n"
-        "sys.exit(3 if lay.tiles > 0 else 4)\n" % (ROOT, wide, n))
+        "sys.exit(3 if lay.tiles > 0 else (5 if lay.windows > 0 else 4))\n" % (ROOT, wide, n))
     env = dict(os.environ, **env_extra)
     r = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True, timeout=300)
     say(r.stdout, r.stderr[-2000:])
@@ -346,6 +382,106 @@ def test_row_block_path_when_tiles_disabled():
     assert _subprocess_gradient({"BHTSNE_TILES": "0"}, n=40000) == 4
 
 
-def test_wide_row_blocks_fall_back_from_tiles():
-    # random columns: every block of 1024 rows spans all ~19 windows of 16384 points
-    assert _subprocess_gradient({}, wide=True) == 4
+def test_wide_row_blocks_take_windowed_segments():
+    # random columns: every block of 1024 rows spans all ~19 windows of 16384
+    # points, so no sliced copy; the rows are cut into segments of the two
+    # column windows of 2^18 points instead
+    assert _subprocess_gradient({}, wide=True) == 5
+
+
+def test_wide_row_blocks_fall_back_to_row_blocks_without_windows():
+    assert _subprocess_gradient({"BHTSNE_WINDOWS": "0"}, wide=True) == 4
+
+
+def test_rows_longer_than_the_row_sort_keep_the_row_block_kernel():
+    """A row of 9000 entries is longer than the layout's in-LDS row sort takes,
+    so its columns stay out of window order: no segments are built, the
+    row-block kernel runs, and the gradient still matches the oracle."""
+    n = 400_000
+    y = synth.random_y(n, seed=34, scale=2.0)
+    rp, col, val = _ring_hubs(n, seed=34, sizes=(9000,))
+    say(f"[windows] long row: n={n} nnz={col.size} longest={np.diff(rp).max()}")
+    Y = torch.from_numpy(np.ascontiguousarray(y)).cuda()
+    lay = bh.Layout(bh.Csr.from_numpy(rp, col, val), Y)
+    assert lay.tiles == 0 and lay.windows == 0
+    g, Z = bh.gradient(Y, lay, 0.5, 12.0)
+    go, Zo, _, _ = oracle.gradient(y, rp, col, val, 0.5, 12.0)
+    assert rel_l2(g.cpu().numpy(), go) <= 1e-3 and abs(Z - Zo) <= 1e-5 * Zo
+
+
+def _ring_hubs(n, seed, sizes=(300, 450, 5000)):
+    """A ring P (6 entries per row) plus hub rows longer than any register budget."""
+    rp, col, val = synth.ring_p(n, seed, m=3)
+    P = sp.csr_matrix((val.astype(np.float64), col, rp), shape=(n, n))
+    rng = np.random.default_rng(seed)
+    r, c = [], []
+    for h, size in enumerate(sizes):
+        others = rng.choice(np.arange(len(sizes), n), size=size, replace=False)
+        r += [h] * size + list(others)
+        c += list(others) + [h] * size
+    H = sp.csr_matrix((np.full(len(r), 1e-7), (r, c)), shape=(n, n))
+    P = (P + H).tocsr()
+    P.sum_duplicates()
+    P.sort_indices()
+    P.data /= P.data.sum()
+    return P.indptr.astype(np.int64), P.indices.astype(np.int32), P.data.astype(np.float32)
+
+
+@pytest.mark.parametrize("case", ["ring6", "ring40", "hubs"])
+def test_windowed_segments_are_p_and_match_the_oracle(case):
+    """Layouts without tile locality at several column windows: the segments
+    cover every real entry of the relabelled copy exactly once, in window order
+    within each row and in row order within each window, and the gradient
+    matches the oracle.  Ring P over a random Y: after the relabelling by the
+    Morton code of Y, a row's columns spread over the whole range (one
+    component).  ring6: 700k points, 6 entries per row (3 windows); ring40:
+    600k points, 40 per row; hubs: 540k points plus rows of 300, 450 and 5000
+    entries."""
+    if case == "ring6":
+        n = 700_000
+        y = synth.random_y(n, seed=31, scale=3.0)
+        rp, col, val = synth.ring_p(n, 31, m=3)
+    elif case == "ring40":
+        n = 600_000
+        y = synth.random_y(n, seed=32, scale=4.0)
+        rp, col, val = synth.ring_p(n, 32, m=20)
+    else:
+        n = 540_000
+        y = synth.random_y(n, seed=33, scale=2.0)
+        rp, col, val = _ring_hubs(n, seed=33)
+    say(f"[windows] {case}: n={n} nnz={col.size}")
+    Y = torch.from_numpy(np.ascontiguousarray(y)).cuda()
+    P = bh.Csr.from_numpy(rp, col, val)
+    lay = bh.Layout(P, Y)
+    assert lay.tiles == 0 and lay.windows == (n + (1 << 18) - 1) >> 18 and lay.segments > 0
+    (perm, rank, lrp, lcol, lval) = _layout_arrays(lay)
+    mem = lay.mem.cpu().numpy()
+    base = _window_region_offset(lay)
+    wstart = mem[base:base + 8 * 65].view(np.int64)
+    S = lay.segments
+    o = base + ((8 * 65 + 255) // 256) * 256
+    cap = _max_segments(lay)
+    seg_row = mem[o:o + 4 * cap].view(np.uint32)[:S]
+    o += ((4 * cap + 255) // 256) * 256
+    seg_start = mem[o:o + 4 * cap].view(np.uint32)[:S]
+    o += ((4 * cap + 255) // 256) * 256
+    seg_len = mem[o:o + 4 * cap].view(np.uint32)[:S]
+    assert wstart[0] == 0 and wstart[lay.windows] == S and np.all(np.diff(wstart[:lay.windows + 1]) >= 0)
+    win = np.repeat(np.arange(lay.windows), np.diff(wstart[:lay.windows + 1]))
+    rows = seg_row.astype(np.int64)
+    st = seg_start.astype(np.int64)
+    ln = seg_len.astype(np.int64)
+    for w in range(lay.windows):  # row order, one segment per row and window
+        assert np.all(np.diff(rows[wstart[w]:wstart[w + 1]]) > 0)
+    assert np.all(ln > 0) and np.all(lrp[rows] <= st) and np.all(st + ln <= lrp[rows + 1])
+    idx = np.repeat(st, ln) + (np.arange(ln.sum()) - np.repeat(np.cumsum(ln) - ln, ln))
+    assert np.all((lcol[idx] >> 18) == np.repeat(win, ln))
+    covered = np.bincount(idx, minlength=lcol.size)
+    real = lcol != NO_COLUMN
+    real[lrp[-1]:] = False
+    assert np.all(covered[real] == 1) and np.all(covered[~real] == 0)
+    g, Z = bh.gradient(Y, lay, 0.5, 12.0)
+    go, Zo, _, _ = oracle.gradient(y, rp, col, val, 0.5, 12.0)
+    err = rel_l2(g.cpu().numpy(), go)
+    say(f"[windows] {case}: {lay.windows} windows, {S} segments, rel-L2 {err:.2e}")
+    assert err <= 1e-3 and abs(Z - Zo) <= 1e-5 * Zo
