@@ -405,7 +405,7 @@ int run_layout64(double *Y, const bhtsne_layout *lay, double theta, const StepAr
     if (lk.owns_lock()) lk.unlock();
     {
         PhaseTimer pt(BHTSNE_PHASE_UPDATE, st);
-        launch_update(lv, n, a, Y, update, gains, grad, ws, L, st);
+        launch_update(lv, n, true, a, Y, update, gains, grad, ws, L, st); // windows: F_attr in layout order
     }
     return finish(Z, ws, st);
 }
@@ -459,7 +459,7 @@ int run_layout(float *Y, const bhtsne_layout *lay, float theta, const StepArgs &
     if (lk.owns_lock()) lk.unlock();
     {
         PhaseTimer pt(BHTSNE_PHASE_UPDATE, st);
-        launch_update(lv, n, a, Y, update, gains, grad, ws, L, st);
+        launch_update(lv, n, tiles == 0 && lay->windows > 0, a, Y, update, gains, grad, ws, L, st);
     }
     return finish(Z, ws, st);
 }
@@ -901,7 +901,12 @@ int bhtsne_affinities(const int32_t *knn_idx, const float *knn_dist, int64_t n, 
     if (need == 0) return BHTSNE_EINVAL;
     if (!workspace || !aligned(workspace) || workspace_bytes < need) return BHTSNE_EWORKSPACE;
     const AffLayout A = make_aff_layout(n, k);
-    launch_aff_front(knn_idx, knn_dist, n, k, perplexity, row_ptr, sigma2, workspace, A, stream);
+    launch_aff_clear(workspace, A, stream);
+    // the index work and the search share the chip poorly (the search keeps
+    // the VALU busy, the sort passes then wait for wave slots), so they run
+    // one after the other
+    launch_aff_index(knn_idx, n, k, row_ptr, workspace, A, stream);
+    launch_aff_search(knn_dist, n, k, perplexity, sigma2, workspace, A, stream);
     if (hipGetLastError() != hipSuccess) return BHTSNE_EDEVICE;
     Header h;
     int64_t total = 0;

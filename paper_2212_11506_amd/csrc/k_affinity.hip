@@ -8,21 +8,32 @@
 // current interval each step) until the perplexity exp(H) of p_{.|i} equals u.
 //
 // GPU design, one call:
-//   1. search: for k <= 128 one point per lane over a transposed copy of the
-//      distances (one coalesced load per neighbour for the wave's 64 points);
-//      for larger k one wave per point with two wave sums per step.  The
-//      search runs to machine precision: it stops when the midpoint equals an
-//      end of the interval and keeps the upper end;
-//   2. own rows: each row's neighbours sorted by column in LDS, carrying p;
-//   3. inboxes: every entry (i, j) is scattered into row j's inbox (column i,
-//      p_{j|i}) at offsets from a scan of the in-degrees;
-//   4. per row: the inbox sorted in LDS, the own entries found in it counted
-//      (P's row holds k plus the inbox-only entries), row pointers scanned;
+//   1. own rows: each row's (column, neighbour position) pairs sorted by a
+//      bitonic network in registers, giving the row in column order and the
+//      place of each entry's p;
+//   2. inboxes: the pairs (column j, place of p_{j|i}) of all rows, in entry
+//      order, sorted by j with a stable LSD radix sort (8-bit digits,
+//      onesweep passes with decoupled look-back), so that row j's inbox (the
+//      points that list j) comes out in increasing i with no atomics;
+//   3. per row: the own entries found in the inbox counted (P's row holds k
+//      plus the inbox-only entries), row pointers scanned;
+//   4. search: for k <= 128 four lanes per point with the distances in
+//      registers; for larger k one wave per point with two wave sums per
+//      step.  The search runs to machine precision: it stops when the
+//      midpoint equals an end of the interval and keeps the upper end.  It
+//      writes p_{j|i} in the neighbour order;
 //   5. per row: the union of the own list and the inbox written in column
 //      order, a pair in both lists once with the sum of its two p.
+// Steps 1-3 read only the neighbour indices.  On a second stream beside the
+// search they slowed each other down as much as they overlapped (the search
+// keeps the VALU busy and holds the wave slots the sort passes wait for), so
+// the steps run in order.
 // At most kAffLongCap points may list the same point.
 #include "common.hpp"
 #include "kernels.hpp"
+
+#include <algorithm>
+#include <type_traits>
 
 namespace bht {
 
@@ -54,16 +65,17 @@ __device__ inline double wave_max_d(double v)
     return v;
 }
 
-__global__ void aff_clear_kernel(Header *__restrict__ hdr, uint32_t *__restrict__ indeg,
-                                 uint32_t *__restrict__ cursor, uint32_t *__restrict__ counters, int64_t n)
+// the flags, tile counters, histograms and look-back words of one call
+__global__ __launch_bounds__(256) void aff_clear_kernel(Header *__restrict__ hdr, uint32_t *__restrict__ hist,
+                                                        unsigned long long *__restrict__ status, int64_t status_words,
+                                                        uint32_t *__restrict__ counters)
 {
-    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (i < n) {
-        indeg[i] = 0;
-        cursor[i] = 0;
-    }
-    if (i == 0) {
+    const int64_t i0 = int64_t(blockIdx.x) * blockDim.x + threadIdx.x, stride = int64_t(gridDim.x) * blockDim.x;
+    for (int64_t i = i0; i < status_words; i += stride) status[i] = 0ull;
+    for (int64_t i = i0; i < int64_t(kHistCopies) * kAffHistWords; i += stride) hist[i] = 0u;
+    if (i0 == 0) {
         hdr->flags = 0;
+        for (int q = 0; q < kSortPasses; ++q) hdr->tile_counter[q] = 0;
         counters[0] = 0;
     }
 }
@@ -162,68 +174,146 @@ __global__ __launch_bounds__(kAffSearchBlock) void aff_search_kernel(const float
     if (sigma2 && lane == 0) sigma2[i] = hi;
 }
 
-// 1'. the search with one point per lane (k <= kAffLaneMaxK).  The distances
-// are first transposed (dT[e n + i]) so that the lanes of a wave read
-// neighbour e of their 64 points as one contiguous 256-byte load; each lane
-// then runs its own bisection with sums over its own row and no cross-lane
-// work.  Same steps and readings as the wave kernel; d^2 - min d^2 is one
-// fp64 fma, exact up to its single rounding (the square of an fp32 value is
-// exact in fp64).
-constexpr int kAffTransRows = 64;
+// 2^-x for 0 <= x <= kExp2Clamp: x = n + r with n = rint(x), so r = x - n,
+// |r| <= 1/2, is exact (no reduction error), then 2^-r = exp(-r ln 2) from
+// its Taylor series to degree 13 (coefficients (ln 2)^d / d!; the truncation
+// is below 5e-18 relative for |r ln 2| <= 0.35) by Horner's rule, and the
+// factor 2^-n as an exponent adjustment, which flushes to 0 beyond the
+// subnormal range (x > 1074).  The arguments here are never negative, so the
+// overflow branches of a general exponential are not needed.
+constexpr double kLn2 = 0.6931471805599453;  // ln 2
+constexpr double kLog2e = 1.4426950408889634; // 1 / ln 2
+constexpr int kExpDegree = 13;
+constexpr double kExp2Clamp = 1500.0; // 2^-1500 is 0 in fp64
 
-__global__ __launch_bounds__(256) void aff_transpose_kernel(const float *__restrict__ dist, int64_t n, int k,
-                                                            float *__restrict__ dT)
+constexpr double ln2_pow_over_factorial(int d)
 {
-    __shared__ float tile[kAffTransRows][kAffLaneMaxK + 1];
-    const int64_t r0 = int64_t(blockIdx.x) * kAffTransRows;
-    const int rows = int(n - r0 < kAffTransRows ? n - r0 : kAffTransRows);
-    for (int x = threadIdx.x; x < rows * k; x += blockDim.x) tile[x / k][x % k] = dist[r0 * k + x];
-    __syncthreads();
-    for (int x = threadIdx.x; x < kAffTransRows * k; x += blockDim.x) {
-        const int e = x / kAffTransRows, r = x % kAffTransRows;
-        if (r < rows) dT[int64_t(e) * n + r0 + r] = tile[r][e];
-    }
+    double c = 1.0;
+    for (int q = 1; q <= d; ++q) c *= kLn2 / double(q);
+    return c;
 }
 
-__global__ __launch_bounds__(256) void aff_search_lane_kernel(const float *__restrict__ dT, int64_t n, int k,
-                                                              double log_u, double *__restrict__ p,
-                                                              double *__restrict__ sigma2, Header *__restrict__ hdr)
+__device__ inline double exp2_neg(double x)
 {
-    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (i >= n) return;
-    const float *col = dT + i;
+    const double nn = rint(x);
+    const double s = nn - x; // -r, exact
+    double q = ln2_pow_over_factorial(kExpDegree);
+#pragma unroll
+    for (int d = kExpDegree - 1; d >= 0; --d) q = fma(q, s, ln2_pow_over_factorial(d));
+    return ldexp(q, -int(nn));
+}
+
+// sums over the four lanes of a row: butterflies, so all four get the same bits
+__device__ inline double quad_sum(double v)
+{
+    v += __shfl_xor(v, 1, kWave);
+    return v + __shfl_xor(v, 2, kWave);
+}
+
+__device__ inline double quad_min(double v)
+{
+    v = fmin(v, __shfl_xor(v, 1, kWave));
+    return fmin(v, __shfl_xor(v, 2, kWave));
+}
+
+__device__ inline double quad_max(double v)
+{
+    v = fmax(v, __shfl_xor(v, 1, kWave));
+    return fmax(v, __shfl_xor(v, 2, kWave));
+}
+
+__device__ inline bool quad_any(bool b)
+{
+    int x = b ? 1 : 0;
+    x |= __shfl_xor(x, 1, kWave);
+    x |= __shfl_xor(x, 2, kWave);
+    return x != 0;
+}
+
+// 1'. the search with four lanes per row (k <= kAffLaneMaxK).  Lane g of a
+// row holds the shifted squared distances of neighbours g, g + 4, g + 8, ...
+// in registers (kPer slots; the unused ones hold NaN), so a bisection step
+// reads no memory.  The row's sums are quad butterflies, equal to the bit in
+// its four lanes, so the four take the same branches.  Same steps and
+// readings as the wave kernel.  Per neighbour and step: x = a / ln 2 with a
+// = d'^2 / 2 sigma^2 (the slots hold d'^2 / ln 2), clamped at kExp2Clamp
+// (2^-x is 0 in fp64 from 1075 on; NaN slots clamp to it too), the weight
+// 2^-x = exp(-a) by exp2_neg, and the entropy log S + ln 2 sum(x w) / S.  A
+// step whose 1 / 2 sigma^2 is infinite (sigma^2 in the subnormal range) takes
+// the limit: weight 1 at d' = 0, else 0.
+constexpr int kAffG = 4;
+
+// f(0), f(1), ..., f(N - 1) with compile-time arguments, so that arrays
+// indexed by them stay in registers whatever the unroller decides
+template <int Q, int N> struct StaticFor {
+    template <typename F> __device__ __forceinline__ static void run(F &&f)
+    {
+        f(std::integral_constant<int, Q>{});
+        StaticFor<Q + 1, N>::run(f);
+    }
+};
+template <int N> struct StaticFor<N, N> {
+    template <typename F> __device__ __forceinline__ static void run(F &&) {}
+};
+
+// entropy (nats) of the Gaussian weights at sigma^2 = s2 over a row held as
+// in aff_search_quad_kernel; the same value in the row's four lanes
+template <int kPer> __device__ __forceinline__ double row_entropy_quad(const double (&dp)[kPer], double s2)
+{
+    const double inv = isinf(s2) ? 0.0 : 1.0 / (2.0 * s2);
+    double sw = 0.0, tw = 0.0;
+    if (!isinf(inv)) {
+        StaticFor<0, kPer>::run([&](auto qc) {
+            const double x = fmin(dp[decltype(qc)::value] * inv, kExp2Clamp); // a / ln 2
+            const double w = exp2_neg(x);
+            sw += w;
+            tw = fma(x, w, tw);
+        });
+    } else {
+        // a = 0 or +inf: a w = 0
+        StaticFor<0, kPer>::run([&](auto qc) { sw += dp[decltype(qc)::value] == 0.0 ? 1.0 : 0.0; });
+    }
+    sw = quad_sum(sw);
+    tw = quad_sum(tw);
+    return log(sw) + kLn2 * tw / sw;
+}
+
+template <int kPer>
+__device__ __forceinline__ void search_row_quad(const float *__restrict__ dist, int64_t i, int g, int k,
+                                                double log_u, double *__restrict__ p, double *__restrict__ sigma2,
+                                                Header *__restrict__ hdr)
+{
+    const float *row = dist + i * k;
+    double dp[kPer];
     double mn = INFINITY;
     bool bad = false;
-    for (int e = 0; e < k; ++e) {
-        const float x = col[int64_t(e) * n];
+    StaticFor<0, kPer>::run([&](auto qc) {
+        constexpr int q = decltype(qc)::value;
+        const int e = g + kAffG * q;
+        const float x = e < k ? row[e] : 0.0f;
         if (!(x >= 0.0f) || isinf(x)) bad = true; // NaN, negative or infinite
-        mn = fmin(mn, double(x) * double(x));
-    }
-    if (bad) {
-        atomicOr(&hdr->flags, kErrNonFinite);
+        dp[q] = double(x);
+        if (e < k) mn = fmin(mn, dp[q] * dp[q]);
+    });
+    if (quad_any(bad)) {
+        if (g == 0) atomicOr(&hdr->flags, kErrNonFinite);
         return;
     }
+    mn = quad_min(mn);
     double mx = 0.0;
-    for (int e = 0; e < k; ++e) {
-        const double x = col[int64_t(e) * n];
-        mx = fmax(mx, fma(x, x, -mn));
-    }
-    // entropy (nats) at sigma^2 = s2 over this lane's row
-    auto entropy = [&](double s2) {
-        const double inv = isinf(s2) ? 0.0 : 1.0 / (2.0 * s2);
-        double sw = 0.0, tw = 0.0;
-#pragma unroll 4
-        for (int e = 0; e < k; ++e) {
-            const double x = col[int64_t(e) * n];
-            const double a = scaled(fma(x, x, -mn), inv);
-            const double w = exp(-a);
-            sw += w;
-            tw += w > 0.0 ? a * w : 0.0;
-        }
-        return log(sw) + tw / sw;
-    };
+    StaticFor<0, kPer>::run([&](auto qc) {
+        constexpr int q = decltype(qc)::value;
+        const bool live = g + kAffG * q < k;
+        dp[q] = live ? fma(dp[q], dp[q], -mn) : __builtin_nan("");
+        if (live) mx = fmax(mx, dp[q]);
+    });
+    mx = quad_max(mx);
+    // from here on the slots hold d'^2 / ln 2, so that a / ln 2 = slot / 2 sigma^2
+    StaticFor<0, kPer>::run([&](auto qc) { dp[decltype(qc)::value] *= kLog2e; });
+    auto entropy = [&](double s2) { return row_entropy_quad<kPer>(dp, s2); };
     double lo = 0.0, hi = mx > 0.0 ? mx : 1.0;
     if (mx > 0.0) {
+        // grow the top of the interval until the perplexity there reaches u
         while (!isinf(hi) && entropy(hi) < log_u) hi *= 2.0;
         if (!isinf(hi)) {
             for (int s = 0; s < kAffMaxSteps; ++s) {
@@ -236,86 +326,296 @@ __global__ __launch_bounds__(256) void aff_search_lane_kernel(const float *__res
             }
         }
     }
+    // p_{j|i} at sigma^2 = hi
     const double inv = isinf(hi) ? 0.0 : 1.0 / (2.0 * hi);
     double sw = 0.0;
-    for (int e = 0; e < k; ++e) {
-        const double x = col[int64_t(e) * n];
-        sw += exp(-scaled(fma(x, x, -mn), inv));
-    }
-    for (int e = 0; e < k; ++e) {
-        const double x = col[int64_t(e) * n];
-        p[i * k + e] = exp(-scaled(fma(x, x, -mn), inv)) / sw;
-    }
-    if (sigma2) sigma2[i] = hi;
+    auto weight = [&](double d) { return !isinf(inv) ? exp2_neg(fmin(d * inv, kExp2Clamp)) : (d == 0.0 ? 1.0 : 0.0); };
+    StaticFor<0, kPer>::run([&](auto qc) { sw += weight(dp[decltype(qc)::value]); });
+    sw = quad_sum(sw);
+    StaticFor<0, kPer>::run([&](auto qc) {
+        constexpr int q = decltype(qc)::value;
+        const int e = g + kAffG * q;
+        if (e < k) p[i * k + e] = weight(dp[q]) / sw;
+    });
+    if (sigma2 && g == 0) sigma2[i] = hi;
 }
 
-// Ascending sort of len (key, value) pairs held in LDS by the block, padded
-// with all-ones keys to the next power of two (the arrays hold that many).
-__device__ inline void lds_bitonic(uint32_t *key, uint32_t *val, int len)
+// rows i = blockIdx.x * 64 + threadIdx.x / 4, strided by the grid
+template <int kPer>
+__global__ __launch_bounds__(256) void aff_search_quad_kernel(const float *__restrict__ dist, int64_t n, int k,
+                                                              double log_u, double *__restrict__ p,
+                                                              double *__restrict__ sigma2, Header *__restrict__ hdr)
 {
-    int size = 1;
-    while (size < len) size <<= 1;
-    for (int t = len + threadIdx.x; t < size; t += blockDim.x) {
-        key[t] = 0xffffffffu;
-        val[t] = 0u;
+    const int g = int(threadIdx.x % kAffG);
+    for (int64_t i = (int64_t(blockIdx.x) * blockDim.x + threadIdx.x) / kAffG; i < n;
+         i += int64_t(gridDim.x) * (blockDim.x / kAffG))
+        search_row_quad<kPer>(dist, i, g, k, log_u, p, sigma2, hdr); // whole quads take the same rows
+}
+
+// 2. own rows in column order, one wave per row (four rows per block).  The
+// entries, packed as column * 256 + neighbour position (distinct, so the
+// order is strict and ties keep the neighbour order) and padded with all-ones
+// to 64 kS slots, are sorted by a bitonic network held in registers: slot x
+// = 64 q + lane; partners fewer than 64 slots apart are exchanged by lane
+// shuffles, farther ones within the lane.  Writes the row in column order
+// (scol), each entry's neighbour position (sorig) and the number of its p in
+// p (spos = i k + neighbour position), and flags columns outside [0, n), the
+// row itself and repeated neighbours.  kS: 1, 2 or 4 (k <= 64 kS).
+template <int kS>
+__global__ __launch_bounds__(256) void aff_own_sort_kernel(const int32_t *__restrict__ idx, int64_t n, int k,
+                                                           int32_t *__restrict__ scol, uint8_t *__restrict__ sorig,
+                                                           uint32_t *__restrict__ spos, Header *__restrict__ hdr)
+{
+    constexpr int kN = kS * kWave;
+    const int w = threadIdx.x / kWave, lane = lane_id();
+    const int64_t i = int64_t(blockIdx.x) * (256 / kWave) + w;
+    if (i >= n) return; // whole waves
+    uint32_t v[kS];
+    bool bad = false;
+#pragma unroll
+    for (int q = 0; q < kS; ++q) {
+        const int e = q * kWave + lane;
+        v[q] = 0xffffffffu;
+        if (e < k) {
+            const uint32_t c = uint32_t(idx[i * k + e]);
+            if (c >= uint32_t(n) || int64_t(c) == i) bad = true;
+            v[q] = ((c < 0xffffffu ? c : 0xffffffu) << 8) | uint32_t(e);
+        }
     }
-    for (int span = 2; span <= size; span <<= 1) {
-        for (int stride = span >> 1; stride > 0; stride >>= 1) {
-            __syncthreads();
-            for (int t = threadIdx.x; t < size / 2; t += blockDim.x) {
-                const int a = 2 * stride * (t / stride) + (t % stride), b = a + stride;
-                const bool up = (a & span) == 0;
-                const uint32_t ka = key[a], kb = key[b];
-                if ((ka > kb) == up) {
-                    key[a] = kb;
-                    key[b] = ka;
-                    const uint32_t v = val[a];
-                    val[a] = val[b];
-                    val[b] = v;
+#pragma unroll
+    for (int size = 2; size <= kN; size <<= 1) {
+#pragma unroll
+        for (int stride = size >> 1; stride > 0; stride >>= 1) {
+            if (stride >= kWave) {
+                const int qs = stride / kWave;
+#pragma unroll
+                for (int q = 0; q < kS; ++q) {
+                    if (q & qs) continue;
+                    const bool up = ((q * kWave + lane) & size) == 0;
+                    const uint32_t a = v[q], b = v[q | qs];
+                    v[q] = up ? min(a, b) : max(a, b);
+                    v[q | qs] = up ? max(a, b) : min(a, b);
+                }
+            } else {
+#pragma unroll
+                for (int q = 0; q < kS; ++q) {
+                    const uint32_t o = uint32_t(__shfl_xor(int(v[q]), stride, kWave));
+                    const bool up = ((q * kWave + lane) & size) == 0;
+                    const bool low = (lane & stride) == 0;
+                    v[q] = (low == up) ? min(v[q], o) : max(v[q], o);
                 }
             }
         }
     }
-    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < kS; ++q) {
+        const int x = q * kWave + lane;
+        // the slot before: the lane below, or the last lane of the slot row before
+        uint32_t prev = uint32_t(__shfl_up(int(v[q]), 1, kWave));
+        if (q > 0) {
+            const uint32_t last = uint32_t(__shfl(int(v[q > 0 ? q - 1 : 0]), kWave - 1, kWave));
+            if (lane == 0) prev = last;
+        }
+        if (x < k) {
+            if (x > 0 && (prev >> 8) == (v[q] >> 8)) bad = true;
+            const uint32_t e = v[q] & 0xffu;
+            scol[i * k + x] = int32_t(v[q] >> 8);
+            sorig[i * k + x] = uint8_t(e);
+            spos[i * k + x] = uint32_t(i * k) + e;
+        }
+    }
+    if (ballot(bad) && lane == 0) atomicOr(&hdr->flags, kErrRange);
 }
 
-// 2. own rows by column: (col, p) in place, one wave per row.  Flags columns
-// outside [0, n), the row itself and repeated neighbours.
-__global__ __launch_bounds__(kWave) void aff_own_sort_kernel(const int32_t *__restrict__ idx, int64_t n, int k,
-                                                             int32_t *__restrict__ scol, double *__restrict__ sp,
-                                                             Header *__restrict__ hdr)
+// 3. the pairs.  Key of an entry: its column, or n for a column outside
+// [0, n) (the call fails on those, but the sort still sees keys in range).
+__device__ inline uint32_t pair_key(int32_t c, int64_t n)
 {
-    __shared__ uint32_t s_key[kAffMaxK];
-    __shared__ uint32_t s_pos[kAffMaxK];
-    __shared__ double s_p[kAffMaxK];
-    const int64_t i = blockIdx.x;
-    bool bad = false;
-    for (int e = threadIdx.x; e < k; e += kWave) {
-        const uint32_t c = uint32_t(idx[i * k + e]);
-        if (c >= uint32_t(n) || int64_t(c) == i) bad = true;
-        s_key[e] = c;
-        s_pos[e] = uint32_t(e);
-        s_p[e] = sp[i * k + e];
-    }
-    lds_bitonic(s_key, s_pos, k);
-    for (int e = threadIdx.x; e < k; e += kWave) {
-        if (e > 0 && s_key[e] == s_key[e - 1]) bad = true;
-        scol[i * k + e] = int32_t(s_key[e]);
-        sp[i * k + e] = s_p[s_pos[e]];
-    }
-    if (ballot(bad) && threadIdx.x == 0) atomicOr(&hdr->flags, kErrRange);
+    return uint32_t(c) < uint32_t(n) ? uint32_t(c) : uint32_t(n);
 }
 
-// 3. inboxes: an entry (i, j) of i's list is also an entry of row j of P;
-// row j's inbox collects them (column i, value p_{j|i}).  Counts first.
-__global__ __launch_bounds__(256) void aff_indeg_kernel(const int32_t *__restrict__ scol, int64_t n, int k,
-                                                        uint32_t *__restrict__ indeg)
+// digit counts of every pass, per block in LDS, added into kHistCopies copies
+__global__ __launch_bounds__(256) void aff_hist_kernel(const int32_t *__restrict__ scol, int64_t m, int64_t n,
+                                                       int passes, uint32_t *__restrict__ hist)
+{
+    __shared__ uint32_t s_h[kAffHistWords];
+    for (int q = threadIdx.x; q < kAffHistWords; q += blockDim.x) s_h[q] = 0u;
+    __syncthreads();
+    for (int64_t x = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; x < m; x += int64_t(gridDim.x) * blockDim.x) {
+        const uint32_t key = pair_key(scol[x], n);
+        for (int q = 0; q < passes; ++q) atomicAdd(&s_h[q * kRadix + ((key >> (q * kRadixBits)) & (kRadix - 1))], 1u);
+    }
+    __syncthreads();
+    uint32_t *h = hist + (blockIdx.x % kHistCopies) * kAffHistWords;
+    for (int q = threadIdx.x; q < passes * kRadix; q += blockDim.x)
+        if (s_h[q]) atomicAdd(&h[q], s_h[q]);
+}
+
+// Block-wide exclusive scan of one value per thread (kSortBlock threads).
+__device__ inline uint32_t aff_block_scan(uint32_t v, uint32_t *s_wave)
+{
+    const int lane = lane_id(), w = threadIdx.x / kWave;
+    uint32_t x = v;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const uint32_t y = __shfl_up(x, o, kWave);
+        if (lane >= o) x += y;
+    }
+    if (lane == kWave - 1) s_wave[w] = x;
+    __syncthreads();
+    uint32_t off = 0;
+#pragma unroll
+    for (int q = 0; q < kSortBlock / kWave; ++q) off += q < w ? s_wave[q] : 0u;
+    __syncthreads();
+    return off + x - v;
+}
+
+// look-back words: flag bits above a 32-bit count
+constexpr unsigned long long kAffAggregate = 1ull << 32, kAffInclusive = 2ull << 32;
+
+static_assert(kSortBlock == kRadix, "thread t owns digit t in the scans and the look-back");
+
+// One stable pass over 8-bit digit `pass` of the keys, carrying a 32-bit
+// value.  Tiles are numbered in start order by a counter, so a tile's
+// predecessors have all started; the look-back adds their per-digit counts
+// until one publishes its inclusive prefix.  The first pass reads the keys
+// from the sorted own rows (columns, mapped by pair_key) and the values from
+// spos, in entry order, so each inbox comes out in increasing listing point.
+template <bool kFirst>
+__global__ __launch_bounds__(kSortBlock) void aff_pair_pass_kernel(
+    const uint32_t *__restrict__ kin, const uint32_t *__restrict__ vin, uint32_t *__restrict__ kout,
+    uint32_t *__restrict__ vout, unsigned long long *__restrict__ status, const uint32_t *__restrict__ hist,
+    Header *__restrict__ hdr, int pass, int64_t m, int64_t n)
+{
+    constexpr int kWaves = kSortBlock / kWave;
+    constexpr int kSeg = kWave * kAffSortItems; // keys per wave segment
+    __shared__ uint32_t s_tile;
+    __shared__ uint32_t s_wcnt[kWaves][kRadix];
+    __shared__ uint32_t s_lstart[kRadix];
+    __shared__ uint32_t s_gofs[kRadix];
+    __shared__ uint32_t s_scan[kWaves];
+    __shared__ uint32_t s_keys[kAffSortTile];
+    __shared__ uint32_t s_vals[kAffSortTile];
+
+    const int t = threadIdx.x, w = t / kWave, lane = lane_id();
+    const int shift = pass * kRadixBits;
+    if (t == 0) s_tile = atomicAdd(&hdr->tile_counter[pass], 1u);
+    for (int q = t; q < kWaves * kRadix; q += kSortBlock) (&s_wcnt[0][0])[q] = 0;
+    __syncthreads();
+    const uint32_t tile = s_tile;
+    const int64_t base = int64_t(tile) * kAffSortTile;
+    const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
+
+    uint32_t key[kAffSortItems], vv[kAffSortItems], rank[kAffSortItems];
+#pragma unroll
+    for (int r = 0; r < kAffSortItems; ++r) {
+        const int64_t p = base + w * kSeg + r * kWave + lane;
+        const bool valid = p < m;
+        key[r] = valid ? (kFirst ? pair_key(int32_t(kin[p]), n) : kin[p]) : 0u;
+        vv[r] = valid ? vin[p] : 0u;
+    }
+#pragma unroll
+    for (int r = 0; r < kAffSortItems; ++r) {
+        const int64_t p = base + w * kSeg + r * kWave + lane;
+        const bool valid = p < m;
+        const uint32_t d = (key[r] >> shift) & (kRadix - 1);
+        uint64_t peers = ballot(valid);
+#pragma unroll
+        for (int b = 0; b < kRadixBits; ++b) {
+            const bool bit = (d >> b) & 1u;
+            const uint64_t mk = ballot(bit);
+            peers &= bit ? mk : ~mk;
+        }
+        const int leader = peers ? __ffsll((unsigned long long)peers) - 1 : lane;
+        uint32_t old = 0;
+        if (valid && lane == leader) {
+            old = s_wcnt[w][d];
+            s_wcnt[w][d] = old + uint32_t(__popcll(peers));
+        }
+        old = __shfl(old, leader, kWave);
+        rank[r] = old + uint32_t(__popcll(peers & lt_mask));
+    }
+    __syncthreads();
+
+    // thread t owns digit t: per-wave offsets, tile count, look-back
+    const uint32_t d = t;
+    uint32_t tot = 0;
+#pragma unroll
+    for (int q = 0; q < kWaves; ++q) {
+        const uint32_t c = s_wcnt[q][d];
+        s_wcnt[q][d] = tot;
+        tot += c;
+    }
+    unsigned long long *my = status + int64_t(tile) * kRadix + d;
+    __hip_atomic_store(my, (tile == 0 ? kAffInclusive : kAffAggregate) | tot, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+    s_lstart[d] = aff_block_scan(tot, s_scan);
+    uint32_t h = 0;
+#pragma unroll
+    for (int c = 0; c < kHistCopies; ++c) h += hist[c * kAffHistWords + pass * kRadix + d];
+    const uint32_t dbase = aff_block_scan(h, s_scan);
+    uint32_t excl = 0;
+    if (tile > 0) {
+        int64_t tt = int64_t(tile) - 1;
+        uint32_t spins = 0;
+        for (;;) {
+            const unsigned long long sv =
+                __hip_atomic_load(status + tt * kRadix + d, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if ((sv >> 32) == 0) { // not published yet
+                if (++spins > kSpinLimit) {
+                    atomicOr(&hdr->flags, kErrLookback);
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(1);
+                continue;
+            }
+            excl += uint32_t(sv);
+            if (sv & kAffInclusive) break;
+            if (--tt < 0) break; // cannot happen: tile 0 publishes an inclusive prefix
+        }
+        __hip_atomic_store(my, kAffInclusive | (excl + tot), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    s_gofs[d] = dbase + excl;
+    __syncthreads();
+
+    // rank -> position inside the tile, staged through LDS, then out in digit runs
+#pragma unroll
+    for (int r = 0; r < kAffSortItems; ++r) {
+        const int64_t p = base + w * kSeg + r * kWave + lane;
+        if (p < m) {
+            const uint32_t dd = (key[r] >> shift) & (kRadix - 1);
+            const uint32_t lp = s_lstart[dd] + s_wcnt[w][dd] + rank[r];
+            s_keys[lp] = key[r];
+            s_vals[lp] = vv[r];
+        }
+    }
+    __syncthreads();
+    const int tile_n = int(m - base < kAffSortTile ? m - base : kAffSortTile);
+    for (int j = t; j < tile_n; j += kSortBlock) {
+        const uint32_t k2 = s_keys[j];
+        const uint32_t dd = (k2 >> shift) & (kRadix - 1);
+        const uint64_t out = uint64_t(s_gofs[dd]) + (uint32_t(j) - s_lstart[dd]);
+        if (out < uint64_t(m)) {
+            kout[out] = k2;
+            vout[out] = s_vals[j];
+        } else {
+            atomicOr(&hdr->flags, kErrRange);
+        }
+    }
+}
+
+// inbox offsets from the sorted keys (all in [0, n]): ib[j] = the first
+// position whose key is >= j, for j = 0..n; every j is written by exactly one
+// thread, the one at the end of the gap that contains it
+__global__ __launch_bounds__(256) void aff_inbox_kernel(const uint32_t *__restrict__ keys, int64_t m, int64_t n,
+                                                        int64_t *__restrict__ ib)
 {
     const int64_t x = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (x >= n * k) return;
-    const int64_t i = x / k;
-    const uint32_t j = uint32_t(scol[x]);
-    if (j < uint32_t(n) && int64_t(j) != i) atomicAdd(&indeg[j], 1u); // others are flagged
+    if (x > m) return;
+    // clamped, so that even keys left unsorted by a failed look-back write in bounds
+    const int64_t lo = x == 0 ? -1 : (keys[x - 1] < n ? int64_t(keys[x - 1]) : n);
+    const int64_t hi = x == m ? n : (keys[x] < n ? int64_t(keys[x]) : n);
+    for (int64_t j = lo + 1; j <= hi; ++j) ib[j] = x;
 }
 
 // exclusive scan of base + cnt[i] over tiles of 1024 rows, into out[0..n]
@@ -398,24 +698,6 @@ __global__ __launch_bounds__(kAffScanBlock) void aff_scan_down_kernel(const uint
     }
 }
 
-// the entries into the inboxes, at slots taken with a counter per row (their
-// order is sorted away below)
-__global__ __launch_bounds__(256) void aff_scatter_kernel(const int32_t *__restrict__ scol,
-                                                          const double *__restrict__ sp, int64_t n, int k,
-                                                          const int64_t *__restrict__ ib,
-                                                          uint32_t *__restrict__ cursor,
-                                                          int32_t *__restrict__ in_col, double *__restrict__ in_p)
-{
-    const int64_t x = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (x >= n * k) return;
-    const int64_t i = x / k;
-    const uint32_t j = uint32_t(scol[x]);
-    if (j >= uint32_t(n) || int64_t(j) == i) return;
-    const int64_t slot = ib[j] + atomicAdd(&cursor[j], 1u);
-    in_col[slot] = int32_t(i);
-    in_p[slot] = sp[x];
-}
-
 // first position in the sorted a[0..len) whose value is >= key
 __device__ inline int lower_bound_u32(const uint32_t *a, int len, uint32_t key)
 {
@@ -463,45 +745,70 @@ __device__ inline uint32_t block_flag_scan(const uint8_t *f, int k, uint32_t *MO
 }
 
 // 4./5. one row j of P from its own list (k columns in order, with p_{c|j})
-// and its inbox (m columns, with p_{j|c}).  kWrite = false: sort the inbox in
-// place and count the inbox entries that are not in the own list (P's row
-// has k plus that many entries); kWrite = true: write the row in column
+// and its inbox (m columns in order, with p_{j|c}): the sorted pairs
+// [ib[j], ib[j + 1]), each holding c k + e for the neighbour e of row c that
+// is j (the place of p_{j|c} in p).
+// kWrite = false: count the inbox entries that are not in the own list (P's
+// row has k plus that many entries); kWrite = true: write the row in column
 // order.  With MO[e] the number of own entries before e that are also in the
 // inbox, own entry e goes to e + t - MO[e] (t: inbox entries below its
 // column) and an inbox-only entry at inbox position t to e' + t - MO[e'] (e':
 // own entries below its column).  A pair in both lists is written once, with
 // (p_{c|j} + p_{j|c}) / 2N: the same fp64 sum in both rows, so P is exactly
-// symmetric.
+// symmetric.  p is in neighbour order: sorted entry e of row c sits at
+// c k + sorig[c k + e].
 template <int kCap, bool kWrite> struct AffRowLds {
     uint32_t own[kAffMaxK];
-    double ownp[kAffMaxK];
+    double ownp[kWrite ? kAffMaxK : 1];
     uint32_t in[kCap];
-    uint32_t pos[kWrite ? 1 : kCap];
-    double inp[kCap];
+    double inp[kWrite ? kCap : 1];
     uint8_t fl[kAffMaxK];
     uint32_t mo[kAffMaxK + 1];
     uint32_t w[kAffLongThreads / kWave];
 };
 
-template <int kCap, bool kWrite>
-__device__ inline void aff_row(int64_t j, int k, int64_t n, const int32_t *__restrict__ scol,
-                               const double *__restrict__ sp, const int64_t *__restrict__ ib,
-                               int32_t *__restrict__ in_col, double *__restrict__ in_p,
-                               uint32_t *__restrict__ inonly, const int64_t *__restrict__ row_ptr,
-                               int32_t *__restrict__ col, float *__restrict__ val, AffRowLds<kCap, kWrite> &L)
+struct AffRowArgs {
+    int64_t n, m; // points, pairs
+    int k;
+    const int32_t *scol;
+    const uint8_t *sorig;
+    const double *p;
+    const int64_t *ib;
+    const uint32_t *pair; // values of the sorted pairs: places in p
+    uint32_t *inonly;
+    const int64_t *row_ptr;
+    int32_t *col;
+    float *val;
+};
+
+// a row's inbox range, clamped to the pairs (the offsets are sound unless the
+// sort failed, which the call reports)
+__device__ inline void inbox_range(const AffRowArgs &a, int64_t j, int64_t *b, int *len)
 {
-    const int64_t b = ib[j];
-    const int m = int(ib[j + 1] - b);
+    int64_t lo = a.ib[j], hi = a.ib[j + 1];
+    lo = lo < 0 ? 0 : lo > a.m ? a.m : lo;
+    hi = hi < lo ? lo : hi > a.m ? a.m : hi;
+    *b = lo;
+    *len = int(hi - lo < int64_t(1) << 30 ? hi - lo : int64_t(1) << 30);
+}
+
+template <int kCap, bool kWrite>
+__device__ inline void aff_row(int64_t j, const AffRowArgs &a, AffRowLds<kCap, kWrite> &L)
+{
+    const int k = a.k;
+    int64_t b;
+    int m;
+    inbox_range(a, j, &b, &m);
     for (int e = threadIdx.x; e < k; e += blockDim.x) {
-        L.own[e] = uint32_t(scol[j * k + e]);
-        L.ownp[e] = sp[j * k + e];
+        L.own[e] = uint32_t(a.scol[j * k + e]);
+        if (kWrite) L.ownp[e] = a.p[j * k + a.sorig[j * k + e]];
     }
     for (int t = threadIdx.x; t < m; t += blockDim.x) {
-        L.in[t] = uint32_t(in_col[b + t]);
-        L.inp[t] = in_p[b + t];
-        if (!kWrite) L.pos[t] = uint32_t(t);
+        uint32_t x = a.pair[b + t]; // c k + the neighbour position of j in row c
+        x = x < uint64_t(a.m) ? x : 0u; // only a failed sort leaves other values
+        L.in[t] = x / uint32_t(k);
+        if (kWrite) L.inp[t] = a.p[x];
     }
-    if (!kWrite) lds_bitonic(L.in, L.pos, m); // ends with a barrier
     __syncthreads();
     for (int e = threadIdx.x; e < k; e += blockDim.x) {
         const int t = lower_bound_u32(L.in, m, L.own[e]);
@@ -510,134 +817,179 @@ __device__ inline void aff_row(int64_t j, int k, int64_t n, const int32_t *__res
     __syncthreads();
     const uint32_t both = block_flag_scan(L.fl, k, L.mo, L.w);
     if (!kWrite) {
-        for (int t = threadIdx.x; t < m; t += blockDim.x) {
-            in_col[b + t] = int32_t(L.in[t]);
-            in_p[b + t] = L.inp[L.pos[t]];
-        }
-        if (threadIdx.x == 0) inonly[j] = uint32_t(m) - both;
+        if (threadIdx.x == 0) a.inonly[j] = uint32_t(m) - both;
         return;
     }
-    const int64_t o = row_ptr[j];
-    const double inv2n = 1.0 / (2.0 * double(n));
+    const int64_t o = a.row_ptr[j];
+    const double inv2n = 1.0 / (2.0 * double(a.n));
     for (int e = threadIdx.x; e < k; e += blockDim.x) {
         const int t = lower_bound_u32(L.in, m, L.own[e]);
         const int64_t q = o + e + t - L.mo[e];
-        col[q] = int32_t(L.own[e]);
-        val[q] = float((L.fl[e] ? L.ownp[e] + L.inp[t] : L.ownp[e]) * inv2n);
+        a.col[q] = int32_t(L.own[e]);
+        a.val[q] = float((L.fl[e] ? L.ownp[e] + L.inp[t] : L.ownp[e]) * inv2n);
     }
     for (int t = threadIdx.x; t < m; t += blockDim.x) {
         const int e = lower_bound_u32(L.own, k, L.in[t]);
         if (e < k && L.own[e] == L.in[t]) continue; // written with the own entry
         const int64_t q = o + e + t - L.mo[e];
-        col[q] = int32_t(L.in[t]);
-        val[q] = float(L.inp[t] * inv2n);
+        a.col[q] = int32_t(L.in[t]);
+        a.val[q] = float(L.inp[t] * inv2n);
     }
 }
 
 // rows whose inbox fits kAffShortCap: one wave each; longer ones are listed
 // (by the counting pass) for the block kernel
 template <bool kWrite>
-__global__ __launch_bounds__(kWave) void aff_row_kernel(int64_t n, int k, const int32_t *__restrict__ scol,
-                                                        const double *__restrict__ sp,
-                                                        const int64_t *__restrict__ ib, int32_t *__restrict__ in_col,
-                                                        double *__restrict__ in_p, uint32_t *__restrict__ inonly,
-                                                        const int64_t *__restrict__ row_ptr,
-                                                        int32_t *__restrict__ col, float *__restrict__ val,
-                                                        uint32_t *__restrict__ longrows,
+__global__ __launch_bounds__(kWave) void aff_row_kernel(AffRowArgs a, uint32_t *__restrict__ longrows,
                                                         uint32_t *__restrict__ counters)
 {
     __shared__ AffRowLds<kAffShortCap, kWrite> L;
     const int64_t j = blockIdx.x;
-    if (ib[j + 1] - ib[j] > kAffShortCap) {
+    int64_t b;
+    int m;
+    inbox_range(a, j, &b, &m);
+    if (m > kAffShortCap) {
         if (!kWrite && threadIdx.x == 0) longrows[atomicAdd(&counters[0], 1u)] = uint32_t(j);
         return;
     }
-    aff_row<kAffShortCap, kWrite>(j, k, n, scol, sp, ib, in_col, in_p, inonly, row_ptr, col, val, L);
+    aff_row<kAffShortCap, kWrite>(j, a, L);
 }
 
 template <bool kWrite>
-__global__ __launch_bounds__(kAffLongThreads) void aff_long_row_kernel(
-    int64_t n, int k, const int32_t *__restrict__ scol, const double *__restrict__ sp,
-    const int64_t *__restrict__ ib, int32_t *__restrict__ in_col, double *__restrict__ in_p,
-    uint32_t *__restrict__ inonly, const int64_t *__restrict__ row_ptr, int32_t *__restrict__ col,
-    float *__restrict__ val, const uint32_t *__restrict__ longrows, const uint32_t *__restrict__ counters,
-    Header *__restrict__ hdr)
+__global__ __launch_bounds__(kAffLongThreads) void aff_long_row_kernel(AffRowArgs a,
+                                                                       const uint32_t *__restrict__ longrows,
+                                                                       const uint32_t *__restrict__ counters,
+                                                                       Header *__restrict__ hdr)
 {
     __shared__ AffRowLds<kAffLongCap, kWrite> L;
     const uint32_t count = counters[0];
     for (uint32_t r = blockIdx.x; r < count; r += gridDim.x) {
         const int64_t j = longrows[r];
-        if (ib[j + 1] - ib[j] > kAffLongCap) { // over the documented limit
+        int64_t b;
+        int m;
+        inbox_range(a, j, &b, &m);
+        if (m > kAffLongCap) { // over the documented limit
             if (!kWrite && threadIdx.x == 0) {
                 atomicOr(&hdr->flags, kErrRange);
-                inonly[j] = 0;
+                a.inonly[j] = 0;
             }
             continue;
         }
         __syncthreads();
-        aff_row<kAffLongCap, kWrite>(j, k, n, scol, sp, ib, in_col, in_p, inonly, row_ptr, col, val, L);
+        aff_row<kAffLongCap, kWrite>(j, a, L);
     }
 }
 
 // ------------------------------------------------------------------ launchers
-void launch_aff_front(const int32_t *idx, const float *dist, int64_t n, int k, double perplexity,
-                      int64_t *row_ptr, double *sigma2, void *ws, const AffLayout &A, hipStream_t st)
+static AffRowArgs row_args(int64_t n, int k, void *ws, const AffLayout &A)
+{
+    AffRowArgs a{};
+    a.n = n;
+    a.m = A.m;
+    a.k = k;
+    a.scol = at<int32_t>(ws, A.scol);
+    a.sorig = at<uint8_t>(ws, A.sorig);
+    a.p = at<double>(ws, A.p);
+    a.ib = at<int64_t>(ws, A.ib);
+    a.pair = at<uint32_t>(ws, A.val[(A.passes - 1) & 1]); // the last pass's output
+    a.inonly = at<uint32_t>(ws, A.inonly);
+    return a;
+}
+
+void launch_aff_clear(void *ws, const AffLayout &A, hipStream_t st)
+{
+    const int64_t words = int64_t(A.passes) * A.sort_tiles * kRadix;
+    const int64_t blocks = std::min<int64_t>(2048, std::max<int64_t>(1, (words + 255) / 256));
+    aff_clear_kernel<<<unsigned(blocks), 256, 0, st>>>(at<Header>(ws, A.header), at<uint32_t>(ws, A.hist),
+                                                       at<unsigned long long>(ws, A.status), words,
+                                                       at<uint32_t>(ws, A.counters));
+}
+
+// step 1: p_{j|i} in neighbour order and sigma_i^2
+void launch_aff_search(const float *dist, int64_t n, int k, double perplexity, double *sigma2, void *ws,
+                       const AffLayout &A, hipStream_t st)
 {
     Header *hdr = at<Header>(ws, A.header);
-    uint32_t *indeg = at<uint32_t>(ws, A.indeg), *cursor = at<uint32_t>(ws, A.cursor);
-    uint32_t *inonly = at<uint32_t>(ws, A.inonly), *counters = at<uint32_t>(ws, A.counters);
-    double *sp = at<double>(ws, A.sp);
-    int32_t *scol = at<int32_t>(ws, A.scol);
-    int64_t *ib = at<int64_t>(ws, A.ib);
-    int32_t *in_col = at<int32_t>(ws, A.in_col);
-    double *in_p = at<double>(ws, A.in_p);
-    uint32_t *longrows = at<uint32_t>(ws, A.longrows);
-    unsigned long long *part = at<unsigned long long>(ws, A.part);
-    aff_clear_kernel<<<unsigned((n + 255) / 256), 256, 0, st>>>(hdr, indeg, cursor, counters, n);
+    double *p = at<double>(ws, A.p);
     const double lu = log(perplexity);
     if (k <= kAffLaneMaxK) {
-        float *dT = at<float>(ws, A.dT);
-        aff_transpose_kernel<<<unsigned((n + kAffTransRows - 1) / kAffTransRows), 256, 0, st>>>(dist, n, k, dT);
-        aff_search_lane_kernel<<<unsigned((n + 255) / 256), 256, 0, st>>>(dT, n, k, lu, sp, sigma2, hdr);
+        const unsigned qb = unsigned((n + 63) / 64); // blocks of 64 rows
+        if (k <= 8 * kAffG)
+            aff_search_quad_kernel<8><<<qb, 256, 0, st>>>(dist, n, k, lu, p, sigma2, hdr);
+        else if (k <= 16 * kAffG)
+            aff_search_quad_kernel<16><<<qb, 256, 0, st>>>(dist, n, k, lu, p, sigma2, hdr);
+        else if (k <= 24 * kAffG)
+            aff_search_quad_kernel<24><<<qb, 256, 0, st>>>(dist, n, k, lu, p, sigma2, hdr);
+        else
+            aff_search_quad_kernel<32><<<qb, 256, 0, st>>>(dist, n, k, lu, p, sigma2, hdr);
     } else {
         const unsigned sb = unsigned((n + 3) / 4);
         if ((k + kWave - 1) / kWave == 3)
-            aff_search_kernel<3><<<sb, kAffSearchBlock, 0, st>>>(dist, n, k, lu, sp, sigma2, hdr);
+            aff_search_kernel<3><<<sb, kAffSearchBlock, 0, st>>>(dist, n, k, lu, p, sigma2, hdr);
         else
-            aff_search_kernel<4><<<sb, kAffSearchBlock, 0, st>>>(dist, n, k, lu, sp, sigma2, hdr);
+            aff_search_kernel<4><<<sb, kAffSearchBlock, 0, st>>>(dist, n, k, lu, p, sigma2, hdr);
     }
-    static_assert(kAffMaxK <= 4 * kWave && kAffLaneMaxK >= 2 * kWave, "three or four distances per lane");
-    aff_own_sort_kernel<<<unsigned(n), kWave, 0, st>>>(idx, n, k, scol, sp, hdr);
-    const unsigned eb = unsigned((n * k + 255) / 256);
-    aff_indeg_kernel<<<eb, 256, 0, st>>>(scol, n, k, indeg);
-    aff_scan_part_kernel<<<unsigned(A.scan_tiles), kAffScanBlock, 0, st>>>(indeg, n, 0, part);
-    aff_scan_top_kernel<<<1, kAffScanBlock, 0, st>>>(part, A.scan_tiles, ib, n);
-    aff_scan_down_kernel<<<unsigned(A.scan_tiles), kAffScanBlock, 0, st>>>(indeg, n, 0, part, ib);
-    aff_scatter_kernel<<<eb, 256, 0, st>>>(scol, sp, n, k, ib, cursor, in_col, in_p);
-    aff_row_kernel<false><<<unsigned(n), kWave, 0, st>>>(n, k, scol, sp, ib, in_col, in_p, inonly, nullptr,
-                                                         nullptr, nullptr, longrows, counters);
-    aff_long_row_kernel<false><<<256, kAffLongThreads, 0, st>>>(n, k, scol, sp, ib, in_col, in_p, inonly, nullptr,
-                                                                nullptr, nullptr, longrows, counters, hdr);
+    static_assert(kAffMaxK <= 4 * kWave && kAffLaneMaxK == 32 * kAffG && kAffLaneMaxK >= 2 * kWave,
+                  "three or four distances per lane in the wave kernel, at most 32 per lane in the quad kernel");
+}
+
+// steps 2-4 (the neighbour indices only): sorted own rows, the pair sort,
+// inbox offsets, the union counts and P's row pointers
+void launch_aff_index(const int32_t *idx, int64_t n, int k, int64_t *row_ptr, void *ws, const AffLayout &A,
+                      hipStream_t st)
+{
+    Header *hdr = at<Header>(ws, A.header);
+    int32_t *scol = at<int32_t>(ws, A.scol);
+    uint8_t *sorig = at<uint8_t>(ws, A.sorig);
+    uint32_t *hist = at<uint32_t>(ws, A.hist), *counters = at<uint32_t>(ws, A.counters);
+    uint32_t *inonly = at<uint32_t>(ws, A.inonly), *longrows = at<uint32_t>(ws, A.longrows);
+    unsigned long long *part = at<unsigned long long>(ws, A.part);
+    const unsigned rb = unsigned((n + 3) / 4);
+    // spos goes into the second value buffer, which the first pass reads and
+    // only the second pass writes
+    uint32_t *spos = at<uint32_t>(ws, A.val[1]);
+    if (k <= kWave)
+        aff_own_sort_kernel<1><<<rb, 256, 0, st>>>(idx, n, k, scol, sorig, spos, hdr);
+    else if (k <= 2 * kWave)
+        aff_own_sort_kernel<2><<<rb, 256, 0, st>>>(idx, n, k, scol, sorig, spos, hdr);
+    else
+        aff_own_sort_kernel<4><<<rb, 256, 0, st>>>(idx, n, k, scol, sorig, spos, hdr);
+    const int64_t m = A.m;
+    aff_hist_kernel<<<unsigned(std::min<int64_t>(2048, (m + 255) / 256)), 256, 0, st>>>(scol, m, n, A.passes, hist);
+    const uint32_t *kin = reinterpret_cast<const uint32_t *>(scol), *vin = spos;
+    for (int q = 0; q < A.passes; ++q) {
+        uint32_t *kout = at<uint32_t>(ws, A.key[q & 1]), *vout = at<uint32_t>(ws, A.val[q & 1]);
+        unsigned long long *status = at<unsigned long long>(ws, A.status) + int64_t(q) * A.sort_tiles * kRadix;
+        if (q == 0)
+            aff_pair_pass_kernel<true><<<unsigned(A.sort_tiles), kSortBlock, 0, st>>>(kin, vin, kout, vout, status,
+                                                                                    hist, hdr, q, m, n);
+        else
+            aff_pair_pass_kernel<false><<<unsigned(A.sort_tiles), kSortBlock, 0, st>>>(kin, vin, kout, vout, status,
+                                                                                     hist, hdr, q, m, n);
+        kin = kout;
+        vin = vout;
+    }
+    int64_t *ib = at<int64_t>(ws, A.ib);
+    aff_inbox_kernel<<<unsigned((m + 1 + 255) / 256), 256, 0, st>>>(kin, m, n, ib);
+    const AffRowArgs a = row_args(n, k, ws, A);
+    aff_row_kernel<false><<<unsigned(n), kWave, 0, st>>>(a, longrows, counters);
+    aff_long_row_kernel<false><<<256, kAffLongThreads, 0, st>>>(a, longrows, counters, hdr);
     aff_scan_part_kernel<<<unsigned(A.scan_tiles), kAffScanBlock, 0, st>>>(inonly, n, k, part);
     aff_scan_top_kernel<<<1, kAffScanBlock, 0, st>>>(part, A.scan_tiles, row_ptr, n);
     aff_scan_down_kernel<<<unsigned(A.scan_tiles), kAffScanBlock, 0, st>>>(inonly, n, k, part, row_ptr);
 }
 
+// step 5: P's rows
 void launch_aff_back(int64_t n, int k, const int64_t *row_ptr, int32_t *col, float *val, void *ws,
                      const AffLayout &A, hipStream_t st)
 {
-    const int32_t *scol = at<int32_t>(ws, A.scol);
-    const double *sp = at<double>(ws, A.sp);
-    const int64_t *ib = at<int64_t>(ws, A.ib);
-    int32_t *in_col = at<int32_t>(ws, A.in_col);
-    double *in_p = at<double>(ws, A.in_p);
-    uint32_t *inonly = at<uint32_t>(ws, A.inonly), *counters = at<uint32_t>(ws, A.counters);
-    uint32_t *longrows = at<uint32_t>(ws, A.longrows);
-    aff_row_kernel<true><<<unsigned(n), kWave, 0, st>>>(n, k, scol, sp, ib, in_col, in_p, inonly, row_ptr, col, val,
-                                                        longrows, counters);
-    aff_long_row_kernel<true><<<256, kAffLongThreads, 0, st>>>(n, k, scol, sp, ib, in_col, in_p, inonly, row_ptr,
-                                                               col, val, longrows, counters,
-                                                               at<Header>(ws, A.header));
+    AffRowArgs a = row_args(n, k, ws, A);
+    a.row_ptr = row_ptr;
+    a.col = col;
+    a.val = val;
+    uint32_t *counters = at<uint32_t>(ws, A.counters), *longrows = at<uint32_t>(ws, A.longrows);
+    aff_row_kernel<true><<<unsigned(n), kWave, 0, st>>>(a, longrows, counters);
+    aff_long_row_kernel<true><<<256, kAffLongThreads, 0, st>>>(a, longrows, counters, at<Header>(ws, A.header));
 }
 
 } // namespace bht

@@ -702,7 +702,8 @@ __device__ inline void attract_add(float2 yi, float2 yj, float p, float &fx, flo
 template <int kAttBlock, int kAttSeg, int kAttRG>
 __global__ __launch_bounds__(kAttBlock) void attract_staged_kernel(
     const int64_t *__restrict__ row_ptr, const int32_t *__restrict__ col, const float *__restrict__ val,
-    const float2 *__restrict__ ylay, int64_t n, int max_segs, float2 *__restrict__ fattr)
+    const float2 *__restrict__ ylay, const uint32_t *__restrict__ perm, int64_t n, int max_segs,
+    float2 *__restrict__ fattr)
 {
     constexpr int kAttGroups = kAttBlock / kAttG;
     constexpr int kAttRows = kAttGroups * kAttRG;
@@ -836,7 +837,7 @@ __global__ __launch_bounds__(kAttBlock) void attract_staged_kernel(
             ax += __shfl_xor(ax, o, kWave);
             ay += __shfl_xor(ay, o, kWave);
         }
-        if (i < n && sub == 0) fattr[i] = make_float2(ax, ay);
+        if (i < n && sub == 0) fattr[perm[i]] = make_float2(ax, ay);
     }
 }
 
@@ -993,13 +994,16 @@ __global__ __launch_bounds__(kTileBlock) void attract_sell_kernel(
 }
 
 // ------------------------------------------------------------------ attractive row sums
-// F_attr of each row in layout order: its partials of the block's tiles, k = 0,
-// 1, ... in segment order, each at the row's sorted position in that tile.
-// Consecutive rows read one tile's 8 KB of partials at a time.
+// F_attr of each row: its partials of the block's tiles, k = 0, 1, ... in
+// segment order, each at the row's sorted position in that tile, stored at the
+// row's original index (perm), so that the update reads it in the caller's
+// order without a gather.  Consecutive rows read one tile's 8 KB of partials
+// at a time.
 __global__ __launch_bounds__(256) void attract_rows_kernel(const float2 *__restrict__ partial,
                                                            const int32_t *__restrict__ blk_nseg,
                                                            const int32_t *__restrict__ blk_tiles,
-                                                           const uint16_t *__restrict__ tpos, int64_t n,
+                                                           const uint16_t *__restrict__ tpos,
+                                                           const uint32_t *__restrict__ perm, int64_t n,
                                                            float2 *__restrict__ fattr)
 {
     const int64_t r = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
@@ -1014,13 +1018,15 @@ __global__ __launch_bounds__(256) void attract_rows_kernel(const float2 *__restr
         fa.x += v.x;
         fa.y += v.y;
     }
-    fattr[r] = fa;
+    fattr[perm[r]] = fa;
 }
 
 // ------------------------------------------------------------------ gradient + update
 // In the caller's order: g = 4 (alpha F_attr - F_rep / Z), then the gains /
-// momentum update of the optimiser (when a.update).  F_attr of a point is
-// that of its row in layout order.
+// momentum update of the optimiser (when a.update).  F_attr is in the
+// caller's order (rank == nullptr: the sliced and row-block kernels store it
+// there) or in layout order, read at rank[i] (the windowed segments, which
+// accumulate over launches).
 template <typename T>
 __global__ __launch_bounds__(256) void update_kernel(const vec2_t<T> *__restrict__ fattr_lay,
                                                      const uint32_t *__restrict__ rank,
@@ -1033,7 +1039,7 @@ __global__ __launch_bounds__(256) void update_kernel(const vec2_t<T> *__restrict
     const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
     if (i >= n) return;
     const T inv_z = T(1.0 / hdr->Z);
-    const uint32_t r = rank[i];
+    const uint32_t r = rank ? rank[i] : uint32_t(i);
     const V fa = r < uint32_t(n) ? fattr_lay[r] : make_vec2(T(0), T(0));
     const V fr = frep[i];
     const T gx = T(4) * (a.alpha * fa.x - fr.x * inv_z);
@@ -1417,7 +1423,7 @@ static void launch_staged(const LayoutView &lv, int64_t n, int64_t nnz, int max_
     constexpr int rows = (B / kAttG) * RG;
     const int64_t blocks = ((n + rows - 1) / rows + 7) / 8 * 8; // multiple of 8 for the XCD remap
     attract_staged_kernel<B, S, RG><<<unsigned(blocks), B, 0, st>>>(lv.row_ptr, lv.col, lv.val, at<float2>(ws, L.ycopy),
-                                                                   n, max_segs, at<float2>(ws, L.fattr));
+                                                                   lv.perm, n, max_segs, at<float2>(ws, L.fattr));
 }
 
 void launch_attract_layout(const LayoutView &lv, int64_t n, int64_t nnz, int tiles, int items, int blocks,
@@ -1434,7 +1440,8 @@ void launch_attract_layout(const LayoutView &lv, int64_t n, int64_t nnz, int til
                                                          lv.tperm, lv.tcol, lv.tval, at<float2>(ws, L.ycopy), items,
                                                          at<Header>(ws, L.header), at<float2>(ws, L.partial));
         attract_rows_kernel<<<unsigned((n + 255) / 256), 256, 0, st>>>(at<float2>(ws, L.partial), lv.blk_nseg,
-                                                                      lv.blk_tiles, lv.tpos, n, at<float2>(ws, L.fattr));
+                                                                      lv.blk_tiles, lv.tpos, lv.perm, n,
+                                                                      at<float2>(ws, L.fattr));
         return;
     }
     // 1024 threads (one block per CU: the segment fills 128 KB of LDS), 2 rows per lane group
@@ -1442,18 +1449,17 @@ void launch_attract_layout(const LayoutView &lv, int64_t n, int64_t nnz, int til
 }
 
 template <typename T>
-void launch_update(const LayoutView &lv, int64_t n, const StepArgsT<T> &a, T *Y, T *upd, T *gains, T *grad,
-                   void *ws, const Layout &L, hipStream_t st)
+void launch_update(const LayoutView &lv, int64_t n, bool layout_order, const StepArgsT<T> &a, T *Y, T *upd, T *gains,
+                   T *grad, void *ws, const Layout &L, hipStream_t st)
 {
-    // every attractive kernel of a layout leaves F_attr per row in layout order
     using V = vec2_t<T>;
     update_kernel<T><<<unsigned((n + 255) / 256), 256, 0, st>>>(
-        at<V>(ws, L.fattr), lv.rank, at<V>(ws, L.frep), at<Header>(ws, L.header), n, a, reinterpret_cast<V *>(Y),
+        at<V>(ws, L.fattr), layout_order ? lv.rank : nullptr, at<V>(ws, L.frep), at<Header>(ws, L.header), n, a, reinterpret_cast<V *>(Y),
         reinterpret_cast<V *>(upd), reinterpret_cast<V *>(gains), reinterpret_cast<V *>(grad));
 }
-template void launch_update<float>(const LayoutView &, int64_t, const StepArgsT<float> &, float *, float *, float *,
-                                   float *, void *, const Layout &, hipStream_t);
-template void launch_update<double>(const LayoutView &, int64_t, const StepArgsT<double> &, double *, double *,
+template void launch_update<float>(const LayoutView &, int64_t, bool, const StepArgsT<float> &, float *, float *,
+                                   float *, float *, void *, const Layout &, hipStream_t);
+template void launch_update<double>(const LayoutView &, int64_t, bool, const StepArgsT<double> &, double *, double *,
                                     double *, double *, void *, const Layout &, hipStream_t);
 
 } // namespace bht

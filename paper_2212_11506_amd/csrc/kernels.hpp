@@ -125,14 +125,18 @@ void launch_attract_windows(const LayoutView &lv, int64_t n, int blocks, int win
 void launch_attract_layout(const LayoutView &lv, int64_t n, int64_t nnz, int tiles, int items, int blocks,
                            int max_segs, int windows, void *ws, const Layout &L, hipStream_t st);
 template <typename T>
-void launch_update(const LayoutView &lv, int64_t n, const StepArgsT<T> &a, T *Y, T *upd, T *gains, T *grad,
-                   void *ws, const Layout &L, hipStream_t st);
+void launch_update(const LayoutView &lv, int64_t n, bool layout_order, const StepArgsT<T> &a, T *Y, T *upd, T *gains,
+                   T *grad, void *ws, const Layout &L, hipStream_t st);
 
-// input similarities from neighbour lists: search, own-row sort, pairs and
-// row pointers (row_ptr[n] = nnz); then, once the caller's arrays are known to
-// hold nnz entries, fill and the row sorts
-void launch_aff_front(const int32_t *idx, const float *dist, int64_t n, int k, double perplexity,
-                      int64_t *row_ptr, double *sigma2, void *ws, const AffLayout &A, hipStream_t st);
+// input similarities from neighbour lists: clear, the index work (own-row
+// order, pair sort, inbox offsets, union counts, row pointers with row_ptr[n]
+// = nnz) and the search; then, once the caller's arrays are known to hold nnz
+// entries, the rows of P
+void launch_aff_clear(void *ws, const AffLayout &A, hipStream_t st);
+void launch_aff_search(const float *dist, int64_t n, int k, double perplexity, double *sigma2, void *ws,
+                       const AffLayout &A, hipStream_t st);
+void launch_aff_index(const int32_t *idx, int64_t n, int k, int64_t *row_ptr, void *ws, const AffLayout &A,
+                      hipStream_t st);
 void launch_aff_back(int64_t n, int k, const int64_t *row_ptr, int32_t *col, float *val, void *ws,
                      const AffLayout &A, hipStream_t st);
 

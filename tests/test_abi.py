@@ -181,10 +181,12 @@ def test_affinities_workspace_size():
     assert ws(1 << 24, 90) == 0 and ws((1 << 24) - 1, 90) > 0
     a, b = ws(1000, 30), ws(1000, 60)
     assert 0 < a < b and a % 256 == 0
-    # per neighbour: p and its column (12 B), the inbox entry (12 B) and, for
-    # k <= 128, the transposed distance (4 B)
-    assert 28 * 1_300_000 * 90 < ws(1_300_000, 90) < 30 * 1_300_000 * 90
-    assert 24 * 1000 * 200 < ws(1000, 200) < 26 * 1000 * 200
+    # per neighbour: p and its sorted column with the neighbour position (13 B),
+    # two ping-pong (column, entry) pairs of the sort (16 B) and the look-back
+    # words, 3 passes x 256 digits x 8 B per 4096 pairs (1.5 B; 2 passes below
+    # 65536 points), plus 16 B per point
+    assert 30.5 * 1_300_000 * 90 < ws(1_300_000, 90) < 30.8 * 1_300_000 * 90
+    assert 30 * 1000 * 200 < ws(1000, 200) < 31 * 1000 * 200
 
 
 def test_affinities_rejects_bad_arguments():
