@@ -65,6 +65,13 @@ def parse():
                     help="skip the other workloads (0, 1, 3 and 4 at each theta) of the headline run")
     ap.add_argument("--no-3d", action="store_true", help="skip the 3-D embedding measurement")
     ap.add_argument("--configs-only", action="store_true", help="measure only the other workloads")
+    ap.add_argument("--save-y", default=None,
+                    help="run --save-after iterations of the schedule, save Y there (.npy) and stop")
+    ap.add_argument("--save-after", type=int, default=900)
+    ap.add_argument("--load-y", default=None,
+                    help="start from a Y saved by --save-y (layout built from it), at schedule iteration "
+                         "--iter0, with zero momentum and unit gains (for counters on late iterations)")
+    ap.add_argument("--iter0", type=int, default=900)
     return ap.parse_args()
 
 
@@ -107,6 +114,13 @@ def measured_traffic(kernel, sources):
                 return None
             return traffic if cells[3] == source_hash(*sources) else None
     return None
+
+
+def attractive_path(lay):
+    """Which attractive kernel a layout takes."""
+    if lay.tiles > 0:
+        return "sliced tiles"
+    return "windowed segments" if lay.windows > 0 else "row blocks"
 
 
 def gpu_run(inp, theta, steps, warmup, schedule, layout=True):
@@ -169,7 +183,7 @@ def gpu_run(inp, theta, steps, warmup, schedule, layout=True):
            "ms_per_step": 1e3 * dt / steps, "interactions_per_iteration": inter,
            "interactions_per_s": inter * steps / dt if inter else None,
            "repulsive_ms": rep_ms, "attractive_ms": att_ms,
-           "attractive_path": ("sliced tiles" if P.tiles > 0 else "row blocks") if layout else "plain CSR"}
+           "attractive_path": attractive_path(P) if layout else "plain CSR"}
     if inter:
         tf = FLOPS_PER_INTERACTION * inter / (rep_ms * 1e-3) / 1e12
         out["repulsive_tflops"] = tf
@@ -448,6 +462,18 @@ def main():
     if args.fp64_only:
         print(json.dumps({"fp64_variant": bench_fp64(args, inp)}), flush=True)
         return
+    iter0 = 0
+    if args.load_y:
+        y = np.load(args.load_y)
+        if y.shape != inp.Y.shape or y.dtype != np.float32:
+            raise SystemExit(f"{args.load_y}: expected float32 {inp.Y.shape}, found {y.dtype} {y.shape}")
+        inp.Y = y
+        iter0 = args.iter0
+        log(f"[bench] starting from {args.load_y} at schedule iteration {iter0}")
+
+    def sched(it):
+        return w.schedule(it + iter0)
+
     n, nnz = inp.n, inp.nnz
     dev = torch.device("cuda:0")
     Y0 = torch.from_numpy(inp.Y).to(dev)
@@ -475,11 +501,17 @@ def main():
 
     def run(k, per_step=None):
         for it in range(k):
-            s = w.schedule(it)
+            s = sched(it)
             bh.step(Y, P, args.theta, s["exaggeration"], s["learning_rate"], s["momentum"], 0.01, u,
                     gains, workspace=ws)
             if per_step:
                 per_step(it)
+
+    if args.save_y:
+        run(args.save_after)
+        np.save(args.save_y, Y.cpu().numpy())
+        print(json.dumps({"saved_y": args.save_y, "iterations": args.save_after}), flush=True)
+        return
 
     # warm-up (code-object loading, caches), then back to the initial state
     run(args.warmup)
@@ -603,7 +635,11 @@ def main():
         att["measured_frac_hbm"] = att["measured_gbs"] / HBM_PEAK_GBS
     if kernels.get("update", {}).get("launches"):
         upd = kernels["update"]
-        upd["gbs"] = 72.0 * n / (upd["ms_per_launch"] * 1e-3) / 1e9
+        # reads F_attr, F_rep, Y, update and gains (8 B each), writes the last
+        # three; the windowed segments leave F_attr in layout order and add the
+        # 4-byte rank read
+        upd_bytes = (68.0 if not args.plain and attractive_path(P) == "windowed segments" else 64.0) * n
+        upd["gbs"] = upd_bytes / (upd["ms_per_launch"] * 1e-3) / 1e9
         upd["frac_hbm"] = upd["gbs"] / HBM_PEAK_GBS
         upd["traffic"] = measured_traffic("update_kernel", att_src)
     dominant = max(("repulsive", "attractive"), key=lambda k: kernels[k]["ms_per_launch"])
@@ -632,6 +668,7 @@ def main():
                "interactions_per_s": o["interactions_per_s"], "step_ms": o["step_ms"]}
     layout_tiles = None if args.plain else P.tiles
     layout_entries = None if args.plain else P.entries
+    path = "plain CSR" if args.plain else attractive_path(P)
     del P, Pcsr, ws, Y0, Y, u, gains
     torch.cuda.empty_cache()
 
@@ -655,7 +692,7 @@ def main():
         "interactions_per_s": (inter_total / elapsed) if inter_total is not None else None,
         "interactions_per_iteration": (inter_total / args.steps) if inter_total is not None else None,
         "nodes_last": stats_last["nodes"],
-        "attractive_path": "plain CSR" if args.plain else "locality layout + LDS staging",
+        "attractive_path": path,
         "layout_build_s": layout_s,
         "layout_tiles": layout_tiles,
         "layout_entries": layout_entries,
