@@ -358,13 +358,13 @@ __global__ __launch_bounds__(256) void aff_search_quad_kernel(const float *__res
 // to 64 kS slots, are sorted by a bitonic network held in registers: slot x
 // = 64 q + lane; partners fewer than 64 slots apart are exchanged by lane
 // shuffles, farther ones within the lane.  Writes the row in column order
-// (scol), each entry's neighbour position (sorig) and the number of its p in
-// p (spos = i k + neighbour position), and flags columns outside [0, n), the
-// row itself and repeated neighbours.  kS: 1, 2 or 4 (k <= 64 kS).
+// (scol) and each entry's neighbour position (sorig), and flags columns
+// outside [0, n), the row itself and repeated neighbours.  kS: 1, 2 or 4 (k
+// <= 64 kS).
 template <int kS>
 __global__ __launch_bounds__(256) void aff_own_sort_kernel(const int32_t *__restrict__ idx, int64_t n, int k,
                                                            int32_t *__restrict__ scol, uint8_t *__restrict__ sorig,
-                                                           uint32_t *__restrict__ spos, Header *__restrict__ hdr)
+                                                           Header *__restrict__ hdr)
 {
     constexpr int kN = kS * kWave;
     const int w = threadIdx.x / kWave, lane = lane_id();
@@ -421,7 +421,6 @@ __global__ __launch_bounds__(256) void aff_own_sort_kernel(const int32_t *__rest
             const uint32_t e = v[q] & 0xffu;
             scol[i * k + x] = int32_t(v[q] >> 8);
             sorig[i * k + x] = uint8_t(e);
-            spos[i * k + x] = uint32_t(i * k) + e;
         }
     }
     if (ballot(bad) && lane == 0) atomicOr(&hdr->flags, kErrRange);
@@ -479,13 +478,15 @@ static_assert(kSortBlock == kRadix, "thread t owns digit t in the scans and the 
 // value.  Tiles are numbered in start order by a counter, so a tile's
 // predecessors have all started; the look-back adds their per-digit counts
 // until one publishes its inclusive prefix.  The first pass reads the keys
-// from the sorted own rows (columns, mapped by pair_key) and the values from
-// spos, in entry order, so each inbox comes out in increasing listing point.
+// from the sorted own rows (columns, mapped by pair_key) in entry order and
+// makes the values, the places of the entries' p in p: entry x of row i = x
+// / k takes i k + sorig[x].  So each inbox comes out in increasing listing
+// point.
 template <bool kFirst>
 __global__ __launch_bounds__(kSortBlock) void aff_pair_pass_kernel(
-    const uint32_t *__restrict__ kin, const uint32_t *__restrict__ vin, uint32_t *__restrict__ kout,
-    uint32_t *__restrict__ vout, unsigned long long *__restrict__ status, const uint32_t *__restrict__ hist,
-    Header *__restrict__ hdr, int pass, int64_t m, int64_t n)
+    const uint32_t *__restrict__ kin, const uint32_t *__restrict__ vin, const uint8_t *__restrict__ sorig,
+    uint32_t *__restrict__ kout, uint32_t *__restrict__ vout, unsigned long long *__restrict__ status,
+    const uint32_t *__restrict__ hist, Header *__restrict__ hdr, int pass, int64_t m, int64_t n, int k)
 {
     constexpr int kWaves = kSortBlock / kWave;
     constexpr int kSeg = kWave * kAffSortItems; // keys per wave segment
@@ -512,7 +513,12 @@ __global__ __launch_bounds__(kSortBlock) void aff_pair_pass_kernel(
         const int64_t p = base + w * kSeg + r * kWave + lane;
         const bool valid = p < m;
         key[r] = valid ? (kFirst ? pair_key(int32_t(kin[p]), n) : kin[p]) : 0u;
-        vv[r] = valid ? vin[p] : 0u;
+        if (kFirst) {
+            const uint32_t x = uint32_t(p), row = x / uint32_t(k);
+            vv[r] = valid ? row * uint32_t(k) + sorig[p] : 0u;
+        } else {
+            vv[r] = valid ? vin[p] : 0u;
+        }
     }
 #pragma unroll
     for (int r = 0; r < kAffSortItems; ++r) {
@@ -945,27 +951,24 @@ void launch_aff_index(const int32_t *idx, int64_t n, int k, int64_t *row_ptr, vo
     uint32_t *inonly = at<uint32_t>(ws, A.inonly), *longrows = at<uint32_t>(ws, A.longrows);
     unsigned long long *part = at<unsigned long long>(ws, A.part);
     const unsigned rb = unsigned((n + 3) / 4);
-    // spos goes into the second value buffer, which the first pass reads and
-    // only the second pass writes
-    uint32_t *spos = at<uint32_t>(ws, A.val[1]);
     if (k <= kWave)
-        aff_own_sort_kernel<1><<<rb, 256, 0, st>>>(idx, n, k, scol, sorig, spos, hdr);
+        aff_own_sort_kernel<1><<<rb, 256, 0, st>>>(idx, n, k, scol, sorig, hdr);
     else if (k <= 2 * kWave)
-        aff_own_sort_kernel<2><<<rb, 256, 0, st>>>(idx, n, k, scol, sorig, spos, hdr);
+        aff_own_sort_kernel<2><<<rb, 256, 0, st>>>(idx, n, k, scol, sorig, hdr);
     else
-        aff_own_sort_kernel<4><<<rb, 256, 0, st>>>(idx, n, k, scol, sorig, spos, hdr);
+        aff_own_sort_kernel<4><<<rb, 256, 0, st>>>(idx, n, k, scol, sorig, hdr);
     const int64_t m = A.m;
     aff_hist_kernel<<<unsigned(std::min<int64_t>(2048, (m + 255) / 256)), 256, 0, st>>>(scol, m, n, A.passes, hist);
-    const uint32_t *kin = reinterpret_cast<const uint32_t *>(scol), *vin = spos;
+    const uint32_t *kin = reinterpret_cast<const uint32_t *>(scol), *vin = nullptr;
     for (int q = 0; q < A.passes; ++q) {
         uint32_t *kout = at<uint32_t>(ws, A.key[q & 1]), *vout = at<uint32_t>(ws, A.val[q & 1]);
         unsigned long long *status = at<unsigned long long>(ws, A.status) + int64_t(q) * A.sort_tiles * kRadix;
         if (q == 0)
-            aff_pair_pass_kernel<true><<<unsigned(A.sort_tiles), kSortBlock, 0, st>>>(kin, vin, kout, vout, status,
-                                                                                    hist, hdr, q, m, n);
+            aff_pair_pass_kernel<true><<<unsigned(A.sort_tiles), kSortBlock, 0, st>>>(
+                kin, vin, sorig, kout, vout, status, hist, hdr, q, m, n, k);
         else
-            aff_pair_pass_kernel<false><<<unsigned(A.sort_tiles), kSortBlock, 0, st>>>(kin, vin, kout, vout, status,
-                                                                                     hist, hdr, q, m, n);
+            aff_pair_pass_kernel<false><<<unsigned(A.sort_tiles), kSortBlock, 0, st>>>(
+                kin, vin, sorig, kout, vout, status, hist, hdr, q, m, n, k);
         kin = kout;
         vin = vout;
     }
