@@ -64,6 +64,9 @@ def parse():
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the other workloads (0, 1, 3 and 4 at each theta) of the headline run")
     ap.add_argument("--no-3d", action="store_true", help="skip the 3-D embedding measurement")
+    ap.add_argument("--no-locality", action="store_true",
+                    help="skip the layout-order measurement on a geometric P with a random Y")
+    ap.add_argument("--locality-only", action="store_true", help="measure only the layout orders")
     ap.add_argument("--configs-only", action="store_true", help="measure only the other workloads")
     ap.add_argument("--save-y", default=None,
                     help="run --save-after iterations of the schedule, save Y there (.npy) and stop")
@@ -123,7 +126,7 @@ def attractive_path(lay):
     return "windowed segments" if lay.windows > 0 else "row blocks"
 
 
-def gpu_run(inp, theta, steps, warmup, schedule, layout=True):
+def gpu_run(inp, theta, steps, warmup, schedule, layout=True, order=None):
     """Iterations of `schedule` on the GPU through the locality layout (the
     launch configuration of the headline run), inputs resident in HBM: the
     rate over `steps` timed iterations after `warmup` untimed ones (from the
@@ -140,8 +143,13 @@ def gpu_run(inp, theta, steps, warmup, schedule, layout=True):
     Y0 = torch.from_numpy(inp.Y).to(dev)
     P = bh.Csr.from_numpy(inp.row_ptr, inp.col, inp.val, device=dev)
     ws = torch.empty(bh.workspace_size(n, nnz), dtype=torch.uint8, device=dev)
+    build_s = None
     if layout:
-        P = bh.Layout(P, Y0, workspace=ws)
+        torch.cuda.synchronize()
+        tb = time.perf_counter()
+        P = bh.Layout(P, Y0, workspace=ws, order=order)
+        torch.cuda.synchronize()
+        build_s = time.perf_counter() - tb
     Y, u, g = Y0.clone(), torch.zeros_like(Y0), torch.ones_like(Y0)
 
     def reset():
@@ -184,6 +192,9 @@ def gpu_run(inp, theta, steps, warmup, schedule, layout=True):
            "interactions_per_s": inter * steps / dt if inter else None,
            "repulsive_ms": rep_ms, "attractive_ms": att_ms,
            "attractive_path": attractive_path(P) if layout else "plain CSR"}
+    if layout:
+        out["layout_order"] = "bfs levels" if P.order == bh.ORDER_BFS else "morton"
+        out["layout_build_s"] = build_s
     if inter:
         tf = FLOPS_PER_INTERACTION * inter / (rep_ms * 1e-3) / 1e12
         out["repulsive_tflops"] = tf
@@ -225,6 +236,35 @@ def oracle_sample(inp, theta, iters, schedule, threads=None):
         oracle.set_threads(all_threads)
     return {"iterations_per_s": iters / dt, "cores": cores, "iterations": iters, "seconds": dt,
             "interactions_per_s": inter / dt, "step_ms": {k: v / iters for k, v in tot.items()}}
+
+
+def bench_locality(args, n=1_300_000, k=90, steps=100, seed=2212):
+    """A P whose locality lies in P alone: the 90 nearest neighbours of 1.3M
+    points uniform in the unit square (one connected component), from a
+    random initial Y (N(0, 1e-4 I)), iterations 0..99 of the headline
+    schedule.  The layout's automatic order (the breadth-first levels of P's
+    graph, which tile) against the Morton order of Y (no tiles: windowed
+    segments)."""
+    import types
+
+    import synth
+
+    t0 = time.time()
+    rp, col, val = synth.geometric_p(n, seed, k=k)
+    y = synth.random_y(n, seed=seed, scale=1e-2)
+    log(f"[bench] locality: geometric P, n={n} nnz={col.size} drawn in {time.time() - t0:.0f}s")
+    inp = types.SimpleNamespace(n=n, nnz=int(col.size), Y=y, row_ptr=rp, col=col, val=val)
+    w = synth.WORKLOADS[2]
+    out = {"workload": f"kNN graph (k = {k}) of {n} points uniform in the unit square, one component, "
+                       f"random initial Y, iterations 0..{steps - 1} of the workload-2 schedule",
+           "n": n, "nnz": int(col.size)}
+    import paper_2212_11506_amd as bh
+    for tag, order in (("auto", bh.ORDER_AUTO), ("morton", bh.ORDER_MORTON)):
+        r = gpu_run(inp, args.theta, steps, 5, w.schedule, order=order)
+        log(f"[bench] locality {tag}: {r['iterations_per_s']:.1f} it/s, {r['attractive_path']} "
+            f"({r['layout_order']}), attraction {r['attractive_ms']:.3f} ms")
+        out[tag] = r
+    return out
 
 
 def bench_configs(args, log_every=None):
@@ -454,6 +494,9 @@ def main():
         return
     if args.configs_only:
         print(json.dumps({"configs": bench_configs(args)}), flush=True)
+        return
+    if args.locality_only:
+        print(json.dumps({"locality": bench_locality(args)}), flush=True)
         return
     w = synth.WORKLOADS[args.workload]
     t0 = time.time()
@@ -703,6 +746,7 @@ def main():
         "fp64_variant": None if args.no_fp64 else bench_fp64(args, inp),
         "embedding_3d": None if (args.no_3d or args.workload != 2 or args.n) else bench_3d(args),
         "configs": None if (args.no_configs or args.workload != 2 or args.n) else bench_configs(args),
+        "locality": None if (args.no_locality or args.workload != 2 or args.n) else bench_locality(args),
     }
     print(json.dumps(out), flush=True)
 

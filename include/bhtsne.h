@@ -86,8 +86,18 @@ typedef struct bhtsne_layout {
     int64_t entries; /* entries of the sliced copy, padding included (0 without tiles) */
     int64_t windows; /* column windows of the windowed row segments (0 = none; only without tiles) */
     int64_t segments; /* (row, window) segments of that form */
+    int64_t order;   /* point order of the copy: BHTSNE_ORDER_MORTON or BHTSNE_ORDER_BFS */
     uint64_t magic;
 } bhtsne_layout;
+
+/* Point orders of a layout, within each connected component of P's graph
+ * (bhtsne_layout_build_ordered). */
+enum {
+    BHTSNE_ORDER_MORTON = 0, /* Morton code of Y (index order when Y is NULL) */
+    BHTSNE_ORDER_BFS = 1,    /* breadth-first level from the component's root (its smallest point),
+                                then index */
+    BHTSNE_ORDER_AUTO = 2    /* Morton; the BFS levels when Morton gives no tiles and they do */
+};
 
 /* Scalars of the last call on a workspace (bhtsne_get_stats). */
 typedef struct bhtsne_stats {
@@ -177,7 +187,9 @@ size_t bhtsne_layout_size(int64_t n, int64_t nnz);
 
 /* Build a locality layout of P (once per matrix; may be rebuilt as Y evolves).
  * Points are renumbered by (connected component of P's graph, Morton code of
- * Y); the copy stores P's rows in that order with renumbered columns, so the
+ * Y), or by the component's breadth-first levels when those give tiles and
+ * the Morton order does not (bhtsne_layout_build_ordered, BHTSNE_ORDER_AUTO);
+ * the copy stores P's rows in that order with renumbered columns, so the
  * columns of consecutive rows fall into compact index windows.  When every
  * block of 1024 rows spans at most 16 windows of 16384 columns, a second,
  * sliced copy is built: for each (row block, window) tile the rows are sorted
@@ -205,6 +217,23 @@ size_t bhtsne_layout_size(int64_t n, int64_t nnz);
  * BHTSNE_EDEVICE. */
 int bhtsne_layout_build(const bhtsne_csr *P, const float *Y, void *layout_mem, size_t layout_bytes,
                         bhtsne_layout *out, void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* bhtsne_layout_build with the point order chosen by the caller; the plain
+ * call is this one with BHTSNE_ORDER_AUTO.  The Morton order brings a row's
+ * columns together when Y already reflects P (after the first iterations);
+ * the breadth-first levels do when P itself has locality, whatever Y is (a
+ * kNN graph of points on a low-dimensional set, from a random initial Y):
+ * the neighbours of a point at level l lie at levels l - 1 to l + 1.  The
+ * search runs from every component's root at once, one host synchronisation
+ * per level; it gives up, and the Morton order is used, when a level holds
+ * more than 65536 points or some point lies more than 16383 levels deep.
+ * BHTSNE_ORDER_AUTO builds the Morton order first and, when that gives no
+ * tiles, tries the levels, keeping whichever tiles (the Morton order if
+ * neither does).  out->order reports the order taken.  Errors as
+ * bhtsne_layout_build, and BHTSNE_EINVAL for another order code. */
+int bhtsne_layout_build_ordered(const bhtsne_csr *P, const float *Y, int order, void *layout_mem,
+                                size_t layout_bytes, bhtsne_layout *out, void *workspace, size_t workspace_bytes,
+                                hipStream_t stream);
 
 /* bhtsne_gradient / bhtsne_step taking P through a layout built by
  * bhtsne_layout_build (the original CSR arrays are not read).  Arguments,

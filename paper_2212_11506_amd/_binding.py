@@ -18,6 +18,7 @@ _LIB = os.path.join(_HERE, "lib", "libbhtsne.so")
 
 BHTSNE_OK, BHTSNE_EINVAL, BHTSNE_EWORKSPACE, BHTSNE_ENONFINITE, BHTSNE_EDEVICE = 0, -1, -2, -3, -4
 BHTSNE_EINPUT, BHTSNE_ECAPACITY = -5, -6
+ORDER_MORTON, ORDER_BFS, ORDER_AUTO = 0, 1, 2  # point orders of a layout (bhtsne_layout_build_ordered)
 PHASES = ("bbox_morton", "sort", "tree", "repulsive", "attractive", "update")
 
 
@@ -35,7 +36,7 @@ class _Csr(C.Structure):
 class _Layout(C.Structure):
     _fields_ = [("n", C.c_int64), ("nnz", C.c_int64), ("mem", C.c_void_p), ("bytes", C.c_size_t),
                 ("tiles", C.c_int64), ("items", C.c_int64), ("entries", C.c_int64), ("windows", C.c_int64),
-                ("segments", C.c_int64), ("magic", C.c_uint64)]
+                ("segments", C.c_int64), ("order", C.c_int64), ("magic", C.c_uint64)]
 
 
 class _Stats(C.Structure):
@@ -73,6 +74,8 @@ def load_library():
         "bhtsne_layout_size": (C.c_size_t, [i64, i64]),
         "bhtsne_layout_build": (C.c_int, [C.POINTER(_Csr), vp, vp, C.c_size_t, C.POINTER(_Layout), vp,
                                           C.c_size_t, vp]),
+        "bhtsne_layout_build_ordered": (C.c_int, [C.POINTER(_Csr), vp, C.c_int, vp, C.c_size_t, C.POINTER(_Layout),
+                                                  vp, C.c_size_t, vp]),
         "bhtsne_gradient_layout": (C.c_int, [vp, C.POINTER(_Layout), f32, f32, vp, f64p, vp, C.c_size_t, vp]),
         "bhtsne_step_layout": (C.c_int, [vp, C.POINTER(_Layout), f32, f32, f32, f32, f32, vp, vp, vp, f64p, vp,
                                          C.c_size_t, vp]),
@@ -243,9 +246,12 @@ def _workspace(n, nnz, ws):
 
 
 class Layout:
-    """A locality layout of P (relabelled copy in device memory) for the *_layout calls."""
+    """A locality layout of P (relabelled copy in device memory) for the *_layout calls.
+    order: None (bhtsne_layout_build, the automatic choice) or one of
+    ORDER_MORTON, ORDER_BFS, ORDER_AUTO (bhtsne_layout_build_ordered)."""
 
-    def __init__(self, P: Csr, Y: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None):
+    def __init__(self, P: Csr, Y: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                 order: Optional[int] = None):
         lib = load_library()
         self.n, self.nnz = P.n, P.nnz
         need = int(lib.bhtsne_layout_size(P.n, P.nnz))
@@ -254,9 +260,19 @@ class Layout:
         self.mem = torch.empty(need, dtype=torch.uint8, device="cuda")
         ws, _ = _workspace(P.n, P.nnz, workspace)
         self._s = _Layout()
-        rc = lib.bhtsne_layout_build(P.struct, _ptr(Y, torch.float32, "Y"), _ptr(self.mem), need,
-                                     C.byref(self._s), _ptr(ws), ws.numel(), _stream())
-        _check(rc, "bhtsne_layout_build")
+        if order is None:
+            rc = lib.bhtsne_layout_build(P.struct, _ptr(Y, torch.float32, "Y"), _ptr(self.mem), need,
+                                         C.byref(self._s), _ptr(ws), ws.numel(), _stream())
+            _check(rc, "bhtsne_layout_build")
+        else:
+            rc = lib.bhtsne_layout_build_ordered(P.struct, _ptr(Y, torch.float32, "Y"), int(order), _ptr(self.mem),
+                                                 need, C.byref(self._s), _ptr(ws), ws.numel(), _stream())
+            _check(rc, "bhtsne_layout_build_ordered")
+
+    @property
+    def order(self) -> int:
+        """ORDER_MORTON or ORDER_BFS: the point order the copy was built in."""
+        return int(self._s.order)
 
     @property
     def tiles(self) -> int:

@@ -328,6 +328,7 @@ int check_layout(const bhtsne_layout *lay, int vbytes = 4)
     if (lay->windows < 0 || lay->windows > kMaxWindows || (lay->windows > 0 && lay->tiles > 0)) return BHTSNE_EINVAL;
     if (lay->segments < 0 || lay->segments > v.max_segments || (lay->windows > 0) != (lay->segments > 0))
         return BHTSNE_EINVAL;
+    if (lay->order != BHTSNE_ORDER_MORTON && lay->order != BHTSNE_ORDER_BFS) return BHTSNE_EINVAL;
     return BHTSNE_OK;
 }
 
@@ -729,6 +730,19 @@ size_t bhtsne_layout_size(int64_t n, int64_t nnz)
 int bhtsne_layout_build(const bhtsne_csr *P, const float *Y, void *layout_mem, size_t layout_bytes,
                         bhtsne_layout *out, void *workspace, size_t workspace_bytes, hipStream_t stream)
 {
+    return bhtsne_layout_build_ordered(P, Y, BHTSNE_ORDER_AUTO, layout_mem, layout_bytes, out, workspace,
+                                       workspace_bytes, stream);
+}
+
+int bhtsne_layout_build_ordered(const bhtsne_csr *P, const float *Y, int order, void *layout_mem,
+                                size_t layout_bytes, bhtsne_layout *out, void *workspace, size_t workspace_bytes,
+                                hipStream_t stream)
+{
+    static_assert(BHTSNE_ORDER_MORTON == kOrderMorton && BHTSNE_ORDER_BFS == kOrderBfs &&
+                      BHTSNE_ORDER_AUTO == kOrderAuto,
+                  "the public order codes are the build's");
+    if (order != BHTSNE_ORDER_MORTON && order != BHTSNE_ORDER_BFS && order != BHTSNE_ORDER_AUTO)
+        return BHTSNE_EINVAL;
     int rc = check_csr(P);
     if (rc != BHTSNE_OK) return rc;
     if (!out || !layout_mem || !aligned(layout_mem)) return BHTSNE_EINVAL;
@@ -740,7 +754,8 @@ int bhtsne_layout_build(const bhtsne_csr *P, const float *Y, void *layout_mem, s
     const Layout L = make_layout(P->n, P->nnz);
     const LayoutView lv = layout_view(layout_mem, P->n, P->nnz);
     TilePlan plan;
-    const int built = launch_layout_build(P->row_ptr, P->col, P->val, P->n, P->nnz, Y, lv, &plan, workspace, L, stream);
+    const int built =
+        launch_layout_build(P->row_ptr, P->col, P->val, P->n, P->nnz, Y, order, lv, &plan, workspace, L, stream);
     if (built == 1) return BHTSNE_EINPUT;
     if (built != 0) return BHTSNE_EDEVICE;
     Header h;
@@ -751,6 +766,7 @@ int bhtsne_layout_build(const bhtsne_csr *P, const float *Y, void *layout_mem, s
     out->nnz = P->nnz;
     out->mem = layout_mem;
     out->bytes = layout_bytes;
+    out->order = plan.order;
     const bool tiled = plan.tiled && tile_path_enabled();
     out->tiles = tiled ? plan.tiles : 0;
     out->items = tiled ? plan.items : 0;
@@ -781,7 +797,8 @@ int bhtsne_layout_build_f64(const bhtsne_csr_f64 *P, const double *Y, void *layo
     const Layout L = make_layout(P->n, P->nnz, 8);
     const LayoutView lv = layout_view(layout_mem, P->n, P->nnz, 8);
     TilePlan plan;
-    const int built = launch_layout_build(P->row_ptr, P->col, P->val, P->n, P->nnz, Y, lv, &plan, workspace, L, stream);
+    const int built = launch_layout_build(P->row_ptr, P->col, P->val, P->n, P->nnz, Y, kOrderMorton, lv, &plan,
+                                          workspace, L, stream);
     if (built == 1) return BHTSNE_EINPUT;
     if (built != 0) return BHTSNE_EDEVICE;
     Header h;
@@ -792,6 +809,7 @@ int bhtsne_layout_build_f64(const bhtsne_csr_f64 *P, const double *Y, void *layo
     out->nnz = P->nnz;
     out->mem = layout_mem;
     out->bytes = layout_bytes;
+    out->order = plan.order;
     out->tiles = out->items = out->entries = 0;
     const bool windowed = plan.windows > 0 && window_path_enabled();
     out->windows = windowed ? plan.windows : 0;

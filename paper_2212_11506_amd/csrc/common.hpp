@@ -96,7 +96,7 @@ struct Header {
     uint32_t ticket_eval;  // blocks done of an evaluation kernel (exact Z, KL)
     uint32_t max_depth;    // deepest leaf level of the last tree (32: a bucket of identical codes)
     uint32_t unsorted;     // layout build: some row's columns are not in window order
-    uint32_t pad[2];
+    uint32_t bfs_count[2]; // layout build: frontier sizes of the breadth-first search
     double eval;           // result of the last evaluation call
 };
 

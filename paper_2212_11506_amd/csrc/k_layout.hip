@@ -117,6 +117,58 @@ __global__ __launch_bounds__(256) void layout_keys_kernel(uint64_t *__restrict__
     keys[i] = (uint64_t(comp[i]) << 38) | low;
 }
 
+// Breadth-first levels from every component's root (the point whose label
+// is itself), all components at once: dist[v] is the number of edges on a
+// shortest path from v's root along P's rows.  The frontier of a level is a
+// list built by appending; its order varies between runs, the levels do not.
+constexpr uint32_t kBfsUnseen = 0xffffffffu;
+constexpr int kBfsMaxLevels = 16383; // the level field of the key holds 14 bits
+
+__global__ __launch_bounds__(256) void bfs_init_kernel(const uint32_t *__restrict__ comp, int64_t n,
+                                                       uint32_t *__restrict__ dist, uint32_t *__restrict__ frontier,
+                                                       uint32_t *__restrict__ count)
+{
+    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const bool root = comp[i] == uint32_t(i);
+    dist[i] = root ? 0u : kBfsUnseen;
+    if (root) frontier[atomicAdd(count, 1u)] = uint32_t(i);
+}
+
+// one level: a wave per frontier point labels its unseen neighbours `level +
+// 1` (the compare-and-swap lets exactly one finder append each of them)
+__global__ __launch_bounds__(256) void bfs_expand_kernel(const int64_t *__restrict__ row_ptr,
+                                                         const int32_t *__restrict__ col, int64_t n, int64_t nnz,
+                                                         const uint32_t *__restrict__ frontier, uint32_t size,
+                                                         uint32_t level, uint32_t *__restrict__ dist,
+                                                         uint32_t *__restrict__ next, uint32_t *__restrict__ count)
+{
+    const int lane = lane_id();
+    for (int64_t f = (int64_t(blockIdx.x) * blockDim.x + threadIdx.x) / kWave; f < int64_t(size);
+         f += int64_t(gridDim.x) * (blockDim.x / kWave)) {
+        const uint32_t u = frontier[f];
+        int64_t s = row_ptr[u], e = row_ptr[u + 1];
+        s = s < 0 ? 0 : s;
+        e = e > nnz ? nnz : e;
+        for (int64_t k = s + lane; k < e; k += kWave) {
+            const uint32_t w = uint32_t(col[k]);
+            if (w >= uint32_t(n) || dist[w] != kBfsUnseen) continue;
+            if (atomicCAS(&dist[w], kBfsUnseen, level + 1) == kBfsUnseen) next[atomicAdd(count, 1u)] = w;
+        }
+    }
+}
+
+// key = component (26 bits) | BFS level (14 bits; unreached points last) | index (24 bits)
+__global__ __launch_bounds__(256) void layout_keys_bfs_kernel(uint64_t *__restrict__ keys,
+                                                              const uint32_t *__restrict__ comp,
+                                                              const uint32_t *__restrict__ dist, int64_t n)
+{
+    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const uint64_t lev = dist[i] < uint32_t(kBfsMaxLevels) ? dist[i] : uint32_t(kBfsMaxLevels);
+    keys[i] = (uint64_t(comp[i]) << 38) | (lev << 24) | uint64_t(i);
+}
+
 // Global digit histograms of existing keys and the clearing of the look-back
 // words (the Morton kernel does both for the codes it makes).
 __global__ __launch_bounds__(kSortBlock) void keys_hist_kernel(const uint64_t *__restrict__ keys, int64_t n,
@@ -1326,15 +1378,92 @@ static int build_windows(const LayoutView &lv, int64_t n, TilePlan *plan, void *
     return 0;
 }
 
+// Breadth-first levels into dist.  Returns 1 when every point was reached
+// within kBfsMaxLevels levels and no level (past the roots) held more than
+// kBfsMaxFront points, 0 when abandoned (the order would not bring columns
+// together), -1 on a HIP error.  One host synchronisation per level.
+constexpr uint32_t kBfsMaxFront = 4 * kTileSeg;
+
+static int bfs_levels(const int64_t *row_ptr, const int32_t *col, int64_t n, int64_t nnz, const uint32_t *comp,
+                      uint32_t *dist, void *ws, const Layout &L, hipStream_t st)
+{
+    Header *hdr = at<Header>(ws, L.header);
+    uint32_t *fr[2] = {at<uint32_t>(ws, L.idx0), at<uint32_t>(ws, L.idx1)};
+    uint32_t *cnt = hdr->bfs_count;
+    flag_clear_kernel<<<1, 1, 0, st>>>(&cnt[0]);
+    bfs_init_kernel<<<unsigned((n + 255) / 256), 256, 0, st>>>(comp, n, dist, fr[0], &cnt[0]);
+    uint32_t size = 0, reached = 0;
+    if (hipMemcpyAsync(&size, &cnt[0], 4, hipMemcpyDeviceToHost, st) != hipSuccess) return -1;
+    if (hipStreamSynchronize(st) != hipSuccess) return -1;
+    for (int level = 0; size > 0; ++level) {
+        reached += size;
+        if (level >= kBfsMaxLevels) return 0;
+        uint32_t *next_cnt = &cnt[(level + 1) & 1];
+        flag_clear_kernel<<<1, 1, 0, st>>>(next_cnt);
+        const int64_t blocks = std::min<int64_t>((int64_t(size) + 3) / 4, 65535 * 4); // a wave per point
+        bfs_expand_kernel<<<unsigned(blocks), 256, 0, st>>>(row_ptr, col, n, nnz, fr[level & 1], size,
+                                                             uint32_t(level), dist, fr[(level + 1) & 1], next_cnt);
+        if (hipMemcpyAsync(&size, next_cnt, 4, hipMemcpyDeviceToHost, st) != hipSuccess) return -1;
+        if (hipStreamSynchronize(st) != hipSuccess) return -1;
+        if (size > kBfsMaxFront) return 0;
+    }
+    return reached == uint32_t(n) ? 1 : 0;
+}
+
+// Renumbers the points by the keys of `order` and writes the relabelled rows:
+// perm, rank, row pointers, columns and values, each row sorted.
 template <typename V>
-int launch_layout_build(const int64_t *row_ptr, const int32_t *col, const V *val, int64_t n, int64_t nnz,
-                        const V *Y, const LayoutView &lv, TilePlan *plan, void *ws, const Layout &L,
-                        hipStream_t st)
+static int relabel(const int64_t *row_ptr, const int32_t *col, const V *val, int64_t n, int64_t nnz, const V *Y,
+                   int order, const LayoutView &lv, void *ws, const Layout &L, hipStream_t st)
 {
     V *lval = sizeof(V) == 4 ? reinterpret_cast<V *>(lv.val) : reinterpret_cast<V *>(lv.val64);
     Header *hdr = at<Header>(ws, L.header);
+    const uint32_t *comp = at<uint32_t>(ws, L.split_b);
+    const unsigned gn = unsigned((n + 255) / 256);
+    const unsigned gw = unsigned((n + 3) / 4 < 65535 * 4 ? (n + 3) / 4 : 65535 * 4);
+    uint64_t *keys = at<uint64_t>(ws, L.codes0);
+    if (order == kOrderBfs) {
+        layout_keys_bfs_kernel<<<gn, 256, 0, st>>>(keys, comp, at<uint32_t>(ws, L.base), n);
+    } else {
+        // keys: component, then Morton order of Y when given
+        if (Y) {
+            launch_bbox(Y, n, ws, L, st);
+            launch_morton(Y, n, nullptr, ws, L, st);
+        } else {
+            sort_reset_kernel<<<1, 256, 0, st>>>(hdr, at<uint32_t>(ws, L.hist));
+        }
+        layout_keys_kernel<<<gn, 256, 0, st>>>(keys, comp, n, Y ? 1 : 0);
+    }
+    sort_reset_kernel<<<1, 256, 0, st>>>(hdr, at<uint32_t>(ws, L.hist));
+    keys_hist_kernel<<<unsigned(L.sort_tiles), kSortBlock, 0, st>>>(keys, n, at<uint32_t>(ws, L.hist),
+                                                                    at<uint32_t>(ws, L.status), L.sort_tiles);
+    launch_sort(n, Y ? Y : reinterpret_cast<const V *>(at<char>(ws, L.ycopy)), ws, L, st);
+    // new order -> rank, row lengths, row pointers, relabelled rows
+    const uint32_t *perm_ws = at<uint32_t>(ws, L.idx0);
+    if (hipMemcpyAsync(lv.perm, perm_ws, 4 * size_t(n), hipMemcpyDeviceToDevice, st) != hipSuccess) return -1;
+    int64_t *len = at<int64_t>(ws, L.codes1); // scratch, n entries
+    layout_rank_kernel<<<gn, 256, 0, st>>>(lv.perm, lv.rank, row_ptr, len, n);
+    const int64_t tiles = (n + kI64Tile - 1) / kI64Tile;
+    int64_t *tsum = at<int64_t>(ws, L.scan_sum); // >= tiles + 1 entries of 16 bytes
+    i64_reduce_kernel<<<unsigned(tiles), 256, 0, st>>>(len, n, tsum);
+    i64_top_kernel<<<1, 256, 0, st>>>(tsum, tiles, lv.row_ptr + n);
+    i64_down_kernel<<<unsigned(tiles), 256, 0, st>>>(len, n, tsum, lv.row_ptr);
+    const int64_t cap = nnz + 3 * n + 4;
+    layout_copy_kernel<V><<<gw, 256, 0, st>>>(row_ptr, col, val, lv.perm, lv.rank, lv.row_ptr, n, cap, lv.col, lval);
+    layout_sentinel_kernel<V><<<1, 1, 0, st>>>(lv.row_ptr, n, lv.col, lval);
+    layout_sort_rows_kernel<V><<<unsigned(n < 65535 * 16 ? n : 65535 * 16), 256, 0, st>>>(lv.row_ptr, lv.col, lval, n);
+    return hipGetLastError() != hipSuccess ? -1 : 0;
+}
+
+template <typename V>
+int launch_layout_build(const int64_t *row_ptr, const int32_t *col, const V *val, int64_t n, int64_t nnz,
+                        const V *Y, int order, const LayoutView &lv, TilePlan *plan, void *ws, const Layout &L,
+                        hipStream_t st)
+{
+    Header *hdr = at<Header>(ws, L.header);
     uint32_t *parent = at<uint32_t>(ws, L.split_b);
     uint32_t *changed = at<uint32_t>(ws, L.split_e);
+    uint32_t *dist = at<uint32_t>(ws, L.base);
     const unsigned gn = unsigned((n + 255) / 256);
     const unsigned gw = unsigned((n + 3) / 4 < 65535 * 4 ? (n + 3) / 4 : 65535 * 4);
     // validate the row pointers first: every later kernel indexes P's entries by them
@@ -1354,48 +1483,51 @@ int launch_layout_build(const int64_t *row_ptr, const int32_t *col, const V *val
         if (hipStreamSynchronize(st) != hipSuccess) return -1;
         if (h == 0) break;
     }
-    // keys: component, then Morton order of Y when given
-    if (Y) {
-        launch_bbox(Y, n, ws, L, st);
-        launch_morton(Y, n, nullptr, ws, L, st);
-    } else {
-        sort_reset_kernel<<<1, 256, 0, st>>>(hdr, at<uint32_t>(ws, L.hist));
+    // the first order: BFS levels when asked for (Morton if the search gives
+    // up), else Morton
+    int chosen = kOrderMorton;
+    if (order == kOrderBfs) {
+        const int rc = bfs_levels(row_ptr, col, n, nnz, parent, dist, ws, L, st);
+        if (rc < 0) return -1;
+        if (rc == 1) chosen = kOrderBfs;
     }
-    uint64_t *keys = at<uint64_t>(ws, L.codes0);
-    layout_keys_kernel<<<gn, 256, 0, st>>>(keys, parent, n, Y ? 1 : 0);
-    sort_reset_kernel<<<1, 256, 0, st>>>(hdr, at<uint32_t>(ws, L.hist));
-    keys_hist_kernel<<<unsigned(L.sort_tiles), kSortBlock, 0, st>>>(keys, n, at<uint32_t>(ws, L.hist),
-                                                                    at<uint32_t>(ws, L.status), L.sort_tiles);
-    launch_sort(n, Y ? Y : reinterpret_cast<const V *>(at<char>(ws, L.ycopy)), ws, L, st);
-    // new order -> rank, row lengths, row pointers, relabelled rows
-    const uint32_t *perm_ws = at<uint32_t>(ws, L.idx0);
-    if (hipMemcpyAsync(lv.perm, perm_ws, 4 * size_t(n), hipMemcpyDeviceToDevice, st) != hipSuccess) return -1;
-    int64_t *len = at<int64_t>(ws, L.codes1); // scratch, n entries
-    layout_rank_kernel<<<gn, 256, 0, st>>>(lv.perm, lv.rank, row_ptr, len, n);
-    const int64_t tiles = (n + kI64Tile - 1) / kI64Tile;
-    int64_t *tsum = at<int64_t>(ws, L.scan_sum); // >= tiles + 1 entries of 16 bytes
-    i64_reduce_kernel<<<unsigned(tiles), 256, 0, st>>>(len, n, tsum);
-    i64_top_kernel<<<1, 256, 0, st>>>(tsum, tiles, lv.row_ptr + n);
-    i64_down_kernel<<<unsigned(tiles), 256, 0, st>>>(len, n, tsum, lv.row_ptr);
-    const int64_t cap = nnz + 3 * n + 4;
-    layout_copy_kernel<V><<<gw, 256, 0, st>>>(row_ptr, col, val, lv.perm, lv.rank, lv.row_ptr, n, cap, lv.col, lval);
-    layout_sentinel_kernel<V><<<1, 1, 0, st>>>(lv.row_ptr, n, lv.col, lval);
-    layout_sort_rows_kernel<V><<<unsigned(n < 65535 * 16 ? n : 65535 * 16), 256, 0, st>>>(lv.row_ptr, lv.col, lval, n);
-    if (hipGetLastError() != hipSuccess) return -1;
+    if (relabel(row_ptr, col, val, n, nnz, Y, chosen, lv, ws, L, st) != 0) return -1;
+    *plan = TilePlan{};
     if (sizeof(V) == 4) { // the sliced copy holds fp32 values
-        const int rc = build_tiles(lv, n, plan, ws, L, st);
-        if (rc != 0 || plan->tiled) return rc;
-    } else {
-        *plan = TilePlan{};
+        int rc = build_tiles(lv, n, plan, ws, L, st);
+        if (rc != 0) return rc;
+        if (plan->tiled) {
+            plan->order = chosen;
+            return 0;
+        }
+        if (order == kOrderAuto) {
+            // Morton order gave no tiles: try the BFS levels, which bring a
+            // row's columns together when P itself has locality (a kNN graph
+            // of points on a low-dimensional set) whatever Y looks like
+            rc = bfs_levels(row_ptr, col, n, nnz, parent, dist, ws, L, st);
+            if (rc < 0) return -1;
+            if (rc == 1) {
+                if (relabel(row_ptr, col, val, n, nnz, Y, kOrderBfs, lv, ws, L, st) != 0) return -1;
+                rc = build_tiles(lv, n, plan, ws, L, st);
+                if (rc != 0) return rc;
+                if (plan->tiled) {
+                    plan->order = kOrderBfs;
+                    return 0;
+                }
+                if (relabel(row_ptr, col, val, n, nnz, Y, kOrderMorton, lv, ws, L, st) != 0) return -1;
+            }
+            *plan = TilePlan{};
+        }
     }
+    plan->order = chosen;
     return build_windows(lv, n, plan, ws, L, st);
 }
 template int launch_layout_build<float>(const int64_t *, const int32_t *, const float *, int64_t, int64_t,
-                                        const float *, const LayoutView &, TilePlan *, void *, const Layout &,
+                                        const float *, int, const LayoutView &, TilePlan *, void *, const Layout &,
                                         hipStream_t);
 template int launch_layout_build<double>(const int64_t *, const int32_t *, const double *, int64_t, int64_t,
-                                         const double *, const LayoutView &, TilePlan *, void *, const Layout &,
-                                         hipStream_t);
+                                         const double *, int, const LayoutView &, TilePlan *, void *,
+                                         const Layout &, hipStream_t);
 
 // One launch per column window, after F_attr is cleared (layout order).
 template <typename T>

@@ -69,7 +69,13 @@ struct TilePlan {
     int64_t entries = 0;
     int32_t windows = 0;   // column windows of the windowed segments (0: none)
     int64_t segments = 0;
+    int32_t order = 0;     // point order of the copy: kOrderMorton or kOrderBfs
 };
+
+// point orders of a layout (within each connected component of P's graph)
+constexpr int kOrderMorton = 0; // Morton code of Y (index order without Y)
+constexpr int kOrderBfs = 1;    // breadth-first level from the component's root, then index
+constexpr int kOrderAuto = 2;   // Morton; BFS levels when Morton gives no tiles and BFS does
 
 template <typename T> void launch_bbox(const T *Y, int64_t n, void *ws, const Layout &L, hipStream_t st);
 // rank (nullable): write the private copy of Y in that order instead of the caller's
@@ -113,7 +119,7 @@ LayoutView layout_view(void *mem, int64_t n, int64_t nnz, int vbytes = 4);
 // V = double builds no sliced copy (only the relabelled rows and windowed segments).
 template <typename V>
 int launch_layout_build(const int64_t *row_ptr, const int32_t *col, const V *val, int64_t n, int64_t nnz,
-                        const V *Y, const LayoutView &lv, TilePlan *plan, void *ws, const Layout &L,
+                        const V *Y, int order, const LayoutView &lv, TilePlan *plan, void *ws, const Layout &L,
                         hipStream_t st);
 // attraction through windowed segments: F_attr in layout order (ws fattr)
 template <typename T>

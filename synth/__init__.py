@@ -374,6 +374,35 @@ def random_p(n: int, seed: int, k: int = 8) -> tuple:
             (sym.data / (2.0 * n)).astype(np.float32))
 
 
+def geometric_p(n: int, seed: int, k: int = K_NEIGHBOURS, blobs: int = 1) -> tuple:
+    """Symmetric CSR P from the exact k nearest neighbours of n points drawn
+    uniformly in the unit square (``blobs`` > 1: in that many disjoint squares
+    side by side, one connected component each): the kNN graph of data on a
+    low-dimensional set, whose locality lies in P itself and not in any
+    embedding.  Weights exp(-(d / d_k)^2) with d_k the row's k-th neighbour
+    distance, row-normalised in fp64, P = (P + P^T) / (2N).  The drawn order
+    is the index order, so as in a real dataset it carries no locality."""
+    from scipy.spatial import cKDTree
+    rng = Generator(PCG64(SeedSequence(seed + 13)))
+    x = rng.uniform(0.0, 1.0, size=(n, 2))
+    if blobs > 1:
+        x[:, 0] += 2.0 * rng.integers(0, blobs, size=n)   # gaps wider than any neighbour distance
+    d, nb = cKDTree(x).query(x, k=k + 1, workers=-1)
+    d, nb = d[:, 1:], nb[:, 1:]                         # column 0 is the point itself
+    dk = np.maximum(d[:, -1:], 1e-300)
+    wts = np.exp(-(d / dk) ** 2).ravel()
+    rows = np.repeat(np.arange(n), k)
+    cond = sp.csr_matrix((wts, (rows, nb.ravel())), shape=(n, n), dtype=np.float64)
+    rs = np.asarray(cond.sum(axis=1)).ravel()
+    rs[rs == 0] = 1.0
+    cond = sp.diags(1.0 / rs) @ cond
+    sym = (cond + cond.T.tocsr()).tocsr()
+    sym.sum_duplicates()
+    sym.sort_indices()
+    return (sym.indptr.astype(np.int64), sym.indices.astype(np.int32),
+            (sym.data / (2.0 * n)).astype(np.float32))
+
+
 def _ring_offsets(n: int, m: int, rng: Generator) -> np.ndarray:
     """m distinct offsets in [1, n/2) (so i + o and i - o never meet mod n)."""
     half = (n - 1) // 2

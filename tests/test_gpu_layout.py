@@ -432,8 +432,9 @@ def test_windowed_segments_are_p_and_match_the_oracle(case):
     """Layouts without tile locality at several column windows: the segments
     cover every real entry of the relabelled copy exactly once, in window order
     within each row and in row order within each window, and the gradient
-    matches the oracle.  Ring P over a random Y: after the relabelling by the
-    Morton code of Y, a row's columns spread over the whole range (one
+    matches the oracle.  Ring P over a random Y, relabelled by the Morton code
+    of Y (asked for: a ring with few offsets is a lattice whose breadth-first
+    levels would tile it): a row's columns spread over the whole range (one
     component).  ring6: 700k points, 6 entries per row (3 windows); ring40:
     600k points, 40 per row; hubs: 540k points plus rows of 300, 450 and 5000
     entries."""
@@ -452,7 +453,7 @@ def test_windowed_segments_are_p_and_match_the_oracle(case):
     say(f"[windows] {case}: n={n} nnz={col.size}")
     Y = torch.from_numpy(np.ascontiguousarray(y)).cuda()
     P = bh.Csr.from_numpy(rp, col, val)
-    lay = bh.Layout(P, Y)
+    lay = bh.Layout(P, Y, order=bh.ORDER_MORTON)
     assert lay.tiles == 0 and lay.windows == (n + (1 << 18) - 1) >> 18 and lay.segments > 0
     (perm, rank, lrp, lcol, lval) = _layout_arrays(lay)
     mem = lay.mem.cpu().numpy()
@@ -485,3 +486,92 @@ def test_windowed_segments_are_p_and_match_the_oracle(case):
     err = rel_l2(g.cpu().numpy(), go)
     say(f"[windows] {case}: {lay.windows} windows, {S} segments, rel-L2 {err:.2e}")
     assert err <= 1e-3 and abs(Z - Zo) <= 1e-5 * Zo
+
+
+# ------------------------------------------------------------------ point orders
+def _bfs_perm(rp, col, n):
+    """The order (component, breadth-first level from the component's smallest
+    point along P's rows, index), from scipy's graph routines."""
+    import scipy.sparse.csgraph as cg
+    A = sp.csr_matrix((np.ones(col.size), col, rp), shape=(n, n))
+    nc, lab = cg.connected_components(A, directed=False)
+    root = np.full(nc, n, np.int64)
+    np.minimum.at(root, lab, np.arange(n))
+    level = np.full(n, -1, np.int64)
+    for r in root:
+        order, pred = cg.breadth_first_order(A, int(r), directed=True, return_predecessors=True)
+        level[r] = 0
+        for v in order[1:]:  # breadth-first: a predecessor's level is set before its children's
+            level[v] = level[pred[v]] + 1
+    assert np.all(level >= 0)
+    return np.lexsort((np.arange(n), level, root[lab])).astype(np.uint32)
+
+
+@pytest.mark.parametrize("blobs", [1, 2])
+def test_bfs_order_tiles_a_geometric_p_from_a_random_y(blobs):
+    """P from the 30 nearest neighbours of 400,000 points uniform in the unit
+    square (one component; two squares apart: two), Y a random initial
+    embedding.  Morton order of Y brings nothing together (a block of 1024
+    rows then reaches all 25 column windows, more than the 16 a tile row
+    allows), so the automatic build takes the breadth-first levels of P's
+    graph (250 or 180 levels of at most 3,700 points: a row block reaches two
+    windows): the sliced tiles engage.  The copy's order is exactly
+    (component, level, index), and both layouts give the oracle's
+    gradient."""
+    n = 400_000
+    rp, col, val = synth.geometric_p(n, 41 + blobs, k=30, blobs=blobs)
+    y = synth.random_y(n, seed=41 + blobs, scale=1e-2)
+    Y = torch.from_numpy(np.ascontiguousarray(y)).cuda()
+    P = bh.Csr.from_numpy(rp, col, val)
+    lay = bh.Layout(P, Y)
+    say(f"[order] geometric blobs={blobs}: order {lay.order}, tiles {lay.tiles}, windows {lay.windows}")
+    assert lay.order == bh.ORDER_BFS and lay.tiles > 0
+    perm = _layout_arrays(lay)[0]
+    assert np.array_equal(perm, _bfs_perm(rp, col, n))
+    morton = bh.Layout(P, Y, order=bh.ORDER_MORTON)
+    assert morton.order == bh.ORDER_MORTON and morton.tiles == 0
+    go, Zo, _, _ = oracle.gradient(y, rp, col, val, 0.5, 12.0)
+    for lt in (lay, morton):
+        g, Z = bh.gradient(Y, lt, 0.5, 12.0)
+        err = rel_l2(g.cpu().numpy(), go)
+        say(f"[order] order {lt.order}: rel-L2 {err:.2e}")
+        assert err <= 1e-3 and abs(Z - Zo) <= 1e-5 * Zo
+
+
+def test_bfs_order_gives_up_without_locality():
+    """A ring P with 40 random offsets per row over 700,000 points: the
+    breadth-first levels grow fortyfold and pass 65,536 points at the fourth,
+    so an explicit request for them, like the automatic build, falls back to
+    the Morton order (and the windowed segments), and the gradient is
+    unchanged."""
+    n = 700_000
+    rp, col, val = synth.ring_p(n, 43, m=20)
+    y = synth.random_y(n, seed=43, scale=3.0)
+    Y = torch.from_numpy(np.ascontiguousarray(y)).cuda()
+    P = bh.Csr.from_numpy(rp, col, val)
+    gp, _ = bh.gradient(Y, P, 0.5, 12.0)
+    for order in (bh.ORDER_BFS, bh.ORDER_AUTO):
+        lay = bh.Layout(P, Y, order=order)
+        assert lay.order == bh.ORDER_MORTON and lay.tiles == 0 and lay.windows > 0
+        g, _ = bh.gradient(Y, lay, 0.5, 12.0)
+        assert rel_l2(g.cpu().numpy(), gp.cpu().numpy().astype(np.float64)) <= 1e-5
+
+
+def test_explicit_orders_on_a_clustered_p():
+    """Workload 0 (2k points, 10 clusters): the automatic build keeps the Morton
+    order, which tiles; the breadth-first order is exact and tiles too; an
+    unknown order code is rejected."""
+    inp = synth.make_inputs(0)
+    P = bh.Csr.from_numpy(inp.row_ptr, inp.col, inp.val)
+    Y = torch.from_numpy(inp.Y).cuda()
+    auto = bh.Layout(P, Y)
+    assert auto.order == bh.ORDER_MORTON and auto.tiles > 0
+    bfs = bh.Layout(P, Y, order=bh.ORDER_BFS)
+    assert bfs.order == bh.ORDER_BFS and bfs.tiles > 0
+    assert np.array_equal(_layout_arrays(bfs)[0], _bfs_perm(inp.row_ptr, inp.col, inp.n))
+    ga, _ = bh.gradient(Y, auto, 0.5, 12.0)
+    gb, _ = bh.gradient(Y, bfs, 0.5, 12.0)
+    assert rel_l2(gb.cpu().numpy(), ga.cpu().numpy().astype(np.float64)) <= 1e-5
+    with pytest.raises(bh.BhtsneError) as e:
+        bh.Layout(P, Y, order=7)
+    assert e.value.status == bh.BHTSNE_EINVAL
