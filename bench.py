@@ -413,8 +413,9 @@ def bench_fp64(args, inp, steps=200, warmup=5):
     """The fp64 variant against the fp32 path on the same workload:
     iterations/s over the first `steps` iterations of the schedule, inputs
     resident, with the per-phase event times.  fp64: through its locality
-    layout (relabelled rows, windowed segments); fp64_plain and fp32: both on
-    the plain CSR P, for the like-for-like precision ratio."""
+    layout (the sliced copy over 8192-point windows, or windowed segments);
+    fp64_plain and fp32: both on the plain CSR P, for the like-for-like
+    precision ratio."""
     import numpy as np
     import torch
 
@@ -462,7 +463,10 @@ def bench_fp64(args, inp, steps=200, warmup=5):
         bh.timing_enable(False)
         ph = bh.timing_read(reset=True)
         out[name] = {"iterations_per_s": steps / dt_s, "ms_per_step": 1e3 * dt_s / steps,
-                     "phases_ms": {k: v[0] / v[1] for k, v in ph.items() if v[1]}}
+                     "phases_ms": {k: v[0] / v[1] for k, v in ph.items() if v[1]},
+                     "attractive_path": attractive_path(P) if name == "fp64" else "plain CSR"}
+        if name == "fp64":
+            out[name].update(layout_tiles=P.tiles, layout_entries=P.entries, layout_windows=P.windows)
         del P, ws, Y0, Y, u, g
         torch.cuda.empty_cache()
     out["fp64_over_fp32_time"] = out["fp64_plain"]["ms_per_step"] / out["fp32"]["ms_per_step"]

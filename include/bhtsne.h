@@ -380,22 +380,25 @@ int bhtsne_step_f64(double *Y, const bhtsne_csr_f64 *P, double theta, double exa
 
 /* A locality layout for the fp64 variant (Attractive Force Computation: the
  * y_j reads of a row are what bound it).  bhtsne_layout_build_f64 renumbers
- * the points as bhtsne_layout_build does (connected component, then Morton
- * order of the fp64 Y when given), stores P's rows in that order with fp64
- * values and sorted columns, and lists the (row, entry range) segments of
- * each column window of 2^18 points (out->windows > 0, out->segments > 0);
- * it builds no sliced copy (out->tiles = 0).  A row longer than 4096 entries
- * keeps its order, and then no segments are built (out->windows = 0); such
+ * the points as bhtsne_layout_build does (BHTSNE_ORDER_AUTO: connected
+ * component, then Morton order of the fp64 Y when given, or the breadth-first
+ * levels when only those tile) and stores P's rows in that order with fp64
+ * values and sorted columns.  It then builds the sliced copy as the fp32 build
+ * does, with fp64 values over column windows of 8192 points (128 KB of fp64 Y
+ * in LDS) and at most 32 tiles per block of 1024 rows (out->tiles > 0);
+ * without it, the (row, entry range) segments of each column window of 2^18
+ * points (out->windows > 0, out->segments > 0).  A row longer than 4096
+ * entries keeps its order, which rules out the sliced copy and, with more
+ * than one column window, the segments (out->tiles = out->windows = 0); such
  * a layout is refused by the two calls below (BHTSNE_EINVAL): use the plain
  * fp64 calls.  The workspace is bhtsne_workspace_size_f64; layout memory is
  * bhtsne_layout_size_f64 bytes.  The handle is tagged as an fp64 layout: the
  * fp32 layout calls refuse it, and these calls refuse an fp32 one.
  * bhtsne_gradient_layout_f64 / bhtsne_step_layout_f64 are bhtsne_gradient_f64
- * / bhtsne_step_f64 taking P through such a layout: the attraction runs one
- * pass per column window on the library's second stream, beside the sort,
- * tree and walk; results come back in the caller's order.  Errors as the
- * plain fp64 calls, and BHTSNE_EINPUT from the build for malformed row
- * pointers. */
+ * / bhtsne_step_f64 taking P through such a layout: the attraction runs on
+ * the library's second stream, beside the sort, tree and walk; results come
+ * back in the caller's order.  Errors as the plain fp64 calls, and
+ * BHTSNE_EINPUT from the build for malformed row pointers. */
 size_t bhtsne_layout_size_f64(int64_t n, int64_t nnz);
 int bhtsne_layout_build_f64(const bhtsne_csr_f64 *P, const double *Y, void *layout_mem, size_t layout_bytes,
                             bhtsne_layout *out, void *workspace, size_t workspace_bytes, hipStream_t stream);

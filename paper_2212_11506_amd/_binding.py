@@ -301,7 +301,8 @@ class Layout:
 
 class LayoutF64(Layout):
     """A locality layout of an fp64 P (CsrF64) for the fp64 variant's calls:
-    relabelled rows with fp64 values and windowed segments, no sliced copy."""
+    relabelled rows with fp64 values, then the sliced copy over 8192-point
+    windows or, without tile locality, windowed segments."""
 
     def __init__(self, P: "CsrF64", Y: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None):
         lib = load_library()

@@ -321,7 +321,6 @@ int check_layout(const bhtsne_layout *lay, int vbytes = 4)
         return BHTSNE_EINVAL;
     if (lay->n < 2 || lay->n > kMaxPoints || lay->nnz < 0) return BHTSNE_EINVAL;
     const LayoutView v = layout_view(nullptr, lay->n, lay->nnz, vbytes);
-    if (vbytes == 8 && lay->tiles != 0) return BHTSNE_EINVAL;
     if (lay->bytes < v.bytes) return BHTSNE_EINVAL;
     if (lay->tiles < 0 || lay->tiles > v.max_tiles) return BHTSNE_EINVAL;
     if (lay->items < 0 || lay->items > lay->tiles || (lay->tiles > 0) != (lay->items > 0)) return BHTSNE_EINVAL;
@@ -387,7 +386,9 @@ int run_layout64(double *Y, const bhtsne_layout *lay, double theta, const StepAr
     const hipStream_t sa = side ? side->st : st;
     {
         PhaseTimer pt(BHTSNE_PHASE_ATTRACTIVE, sa);
-        launch_attract_windows<double>(lv, n, attract_blocks(side != nullptr, 0), int(lay->windows), ws, L, sa);
+        launch_attract_layout<double>(lv, n, lay->nnz, int(lay->tiles), int(lay->items),
+                                      attract_blocks(side != nullptr, int(lay->items)), stage_segments(),
+                                      int(lay->windows), ws, L, sa);
     }
     if (side && hipEventRecord(side->join, sa) != hipSuccess) return BHTSNE_EDEVICE;
     {
@@ -406,7 +407,7 @@ int run_layout64(double *Y, const bhtsne_layout *lay, double theta, const StepAr
     if (lk.owns_lock()) lk.unlock();
     {
         PhaseTimer pt(BHTSNE_PHASE_UPDATE, st);
-        launch_update(lv, n, true, a, Y, update, gains, grad, ws, L, st); // windows: F_attr in layout order
+        launch_update(lv, n, lay->tiles == 0 && lay->windows > 0, a, Y, update, gains, grad, ws, L, st);
     }
     return finish(Z, ws, st);
 }
@@ -440,8 +441,9 @@ int run_layout(float *Y, const bhtsne_layout *lay, float theta, const StepArgs &
     const hipStream_t sa = side ? side->st : st;
     {
         PhaseTimer pt(BHTSNE_PHASE_ATTRACTIVE, sa);
-        launch_attract_layout(lv, n, lay->nnz, tiles, int(lay->items), attract_blocks(side != nullptr, int(lay->items)),
-                              stage_segments(), int(lay->windows), ws, L, sa);
+        launch_attract_layout<float>(lv, n, lay->nnz, tiles, int(lay->items),
+                                     attract_blocks(side != nullptr, int(lay->items)), stage_segments(),
+                                     int(lay->windows), ws, L, sa);
     }
     if (side && hipEventRecord(side->join, sa) != hipSuccess) return BHTSNE_EDEVICE;
     if (fork < 1) {
@@ -797,7 +799,7 @@ int bhtsne_layout_build_f64(const bhtsne_csr_f64 *P, const double *Y, void *layo
     const Layout L = make_layout(P->n, P->nnz, 8);
     const LayoutView lv = layout_view(layout_mem, P->n, P->nnz, 8);
     TilePlan plan;
-    const int built = launch_layout_build(P->row_ptr, P->col, P->val, P->n, P->nnz, Y, kOrderMorton, lv, &plan,
+    const int built = launch_layout_build(P->row_ptr, P->col, P->val, P->n, P->nnz, Y, kOrderAuto, lv, &plan,
                                           workspace, L, stream);
     if (built == 1) return BHTSNE_EINPUT;
     if (built != 0) return BHTSNE_EDEVICE;
@@ -810,8 +812,11 @@ int bhtsne_layout_build_f64(const bhtsne_csr_f64 *P, const double *Y, void *layo
     out->mem = layout_mem;
     out->bytes = layout_bytes;
     out->order = plan.order;
-    out->tiles = out->items = out->entries = 0;
-    const bool windowed = plan.windows > 0 && window_path_enabled();
+    const bool tiled = plan.tiled && tile_path_enabled();
+    out->tiles = tiled ? plan.tiles : 0;
+    out->items = tiled ? plan.items : 0;
+    out->entries = tiled ? plan.entries : 0;
+    const bool windowed = !tiled && plan.windows > 0 && window_path_enabled();
     out->windows = windowed ? plan.windows : 0;
     out->segments = windowed ? plan.segments : 0;
     out->magic = kLayoutMagic64;
@@ -823,7 +828,8 @@ static int check_layout64_step(const bhtsne_layout *layout, const double *Y, dou
 {
     int rc = check_layout(layout, 8);
     if (rc != BHTSNE_OK) return rc;
-    if (layout->windows == 0) return BHTSNE_EINVAL; // rows out of window order: use the plain fp64 calls
+    // neither form (rows out of window order): use the plain fp64 calls
+    if (layout->windows == 0 && layout->tiles == 0) return BHTSNE_EINVAL;
     if (!Y) return BHTSNE_EINVAL;
     if (!std::isfinite(theta) || theta < 0.0) return BHTSNE_EINVAL;
     if (!std::isfinite(exaggeration) || !(exaggeration > 0.0)) return BHTSNE_EINVAL;

@@ -57,6 +57,9 @@ constexpr int64_t kYPad = 16384 + 2;                   // padding points after t
 constexpr int kTileRows = 1024;
 constexpr int kTileSeg = 16384; // 128 KB of Y in LDS
 constexpr int kTileMaxSeg = 16;
+// tiles per row block for values of `vbytes` bytes: windows of fp64 points
+// are half as wide, so twice as many cover the same column span
+constexpr int max_tiles_per_block(int vbytes) { return kTileMaxSeg * (vbytes / 4); }
 constexpr int kItemMaxTiles = 128; // tiles of one segment handled by one block
 // sliced copy of a tile: 64 rows per slice (one per lane), chunks of 4 entries per lane
 constexpr int kSellSlice = 64;
@@ -155,7 +158,9 @@ inline Layout make_layout(int64_t n, int64_t nnz, int fbytes = 4, int dim = 2)
     L.fattr = take(2 * size_t(fbytes) * size_t(n));
     // partial attractive sums, one per (tile, sorted row slot): up to
     // kTileMaxSeg tiles of kTileRows rows per row block
-    L.partial = dim == 3 ? take(0) : take(8 * size_t((n + kTileRows - 1) / kTileRows) * kTileRows * kTileMaxSeg);
+    L.partial = dim == 3 ? take(0)
+                         : take(2 * size_t(fbytes) * size_t((n + kTileRows - 1) / kTileRows) * kTileRows *
+                                size_t(max_tiles_per_block(fbytes)));
     L.zpart = take(8 * size_t(L.rep_blocks));
     const int64_t zb = (n + kZEvalPoints - 1) / kZEvalPoints;
     L.eval_part = take(8 * size_t(zb > kEvalMaxBlocks ? zb : kEvalMaxBlocks));

@@ -395,7 +395,21 @@ __global__ __launch_bounds__(256) void layout_sort_rows_kernel(const int64_t *__
 }
 
 // ------------------------------------------------------------------ tiled copy
+// Column windows of the sliced copy: 128 KB of Y in LDS, 16384 fp32 points or
+// 8192 fp64 points.
+template <typename T> constexpr int window_points() { return sizeof(T) == 4 ? kTileSeg : kTileSeg / 2; }
+
+// Rows longer than the in-LDS row sort stay unsorted; the sliced copy finds a
+// row's runs by binary search, so one such row rules it out.
+__global__ __launch_bounds__(256) void long_rows_kernel(const int64_t *__restrict__ row_ptr, int64_t n,
+                                                        int64_t max_len, uint32_t *__restrict__ flag)
+{
+    const int64_t r = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (r < n && row_ptr[r + 1] - row_ptr[r] > max_len) *flag = 1u;
+}
+
 // Segment range of each row block (its real entries' smallest and largest column).
+template <int kSeg>
 __global__ __launch_bounds__(256) void tile_block_range_kernel(const int64_t *__restrict__ row_ptr,
                                                                const int32_t *__restrict__ col, int64_t n,
                                                                int32_t *__restrict__ seg_lo, int32_t *__restrict__ nseg)
@@ -428,8 +442,8 @@ __global__ __launch_bounds__(256) void tile_block_range_kernel(const int64_t *__
         }
         lo = min(lo, s_lo[0]);
         hi = max(hi, s_hi[0]);
-        seg_lo[b] = hi >= 0 ? lo / kTileSeg : 0;
-        nseg[b] = hi >= 0 ? hi / kTileSeg - lo / kTileSeg + 1 : 0;
+        seg_lo[b] = hi >= 0 ? lo / kSeg : 0;
+        nseg[b] = hi >= 0 ? hi / kSeg - lo / kSeg + 1 : 0;
     }
 }
 
@@ -449,6 +463,7 @@ __device__ inline int64_t row_lower_bound(const int32_t *__restrict__ col, int64
 // Run length (entries in the tile's segment) of every (row, tile) of the tiled
 // row blocks; one wave per row, one lane per segment of the row's block.
 // Rows past n get empty runs.
+template <int kSeg, int kMaxSeg>
 __global__ __launch_bounds__(256) void tile_run_len_kernel(const int64_t *__restrict__ row_ptr,
                                                            const int32_t *__restrict__ col, int64_t n, int64_t rows,
                                                            const int32_t *__restrict__ seg_lo,
@@ -465,10 +480,10 @@ __global__ __launch_bounds__(256) void tile_run_len_kernel(const int64_t *__rest
         int32_t len = 0;
         if (r < n) {
             const int64_t a = row_ptr[r], e = row_ptr[r + 1];
-            const int32_t s0 = (seg_lo[b] + lane) * kTileSeg;
-            len = int32_t(row_lower_bound(col, a, e, s0 + kTileSeg) - row_lower_bound(col, a, e, s0));
+            const int32_t s0 = (seg_lo[b] + lane) * kSeg;
+            len = int32_t(row_lower_bound(col, a, e, s0 + kSeg) - row_lower_bound(col, a, e, s0));
         }
-        run_len[int64_t(blk_tiles[b * kTileMaxSeg + lane]) * kTileRows + rl] = len;
+        run_len[int64_t(blk_tiles[b * kMaxSeg + lane]) * kTileRows + rl] = len;
     }
 }
 
@@ -510,12 +525,12 @@ __global__ __launch_bounds__(kTileRows) void tile_sort_kernel(const int32_t *__r
     }
 }
 
-__global__ __launch_bounds__(256) void fill_zero_kernel(uint16_t *__restrict__ tcol, float *__restrict__ tval,
-                                                        int64_t m)
+template <typename T>
+__global__ __launch_bounds__(256) void fill_zero_kernel(uint16_t *__restrict__ tcol, T *__restrict__ tval, int64_t m)
 {
     for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < m; i += int64_t(gridDim.x) * blockDim.x) {
         tcol[i] = 0;
-        tval[i] = 0.0f;
+        tval[i] = T(0);
     }
 }
 
@@ -523,16 +538,19 @@ __global__ __launch_bounds__(256) void fill_zero_kernel(uint16_t *__restrict__ t
 // (sorted position % 64) of unit (tile, sorted position / 64); its e-th entry
 // in the segment goes to chunk e / 4, element e % 4 of that lane.  Everything
 // else was zeroed (padding carries p = 0).
+template <typename T>
 __global__ __launch_bounds__(256) void sell_copy_kernel(const int64_t *__restrict__ row_ptr,
-                                                        const int32_t *__restrict__ col, const float *__restrict__ val,
+                                                        const int32_t *__restrict__ col, const T *__restrict__ val,
                                                         int64_t n, const int32_t *__restrict__ seg_lo,
                                                         const int32_t *__restrict__ nseg,
                                                         const int32_t *__restrict__ blk_tiles,
                                                         const uint16_t *__restrict__ tpos,
                                                         const int32_t *__restrict__ unit_of,
                                                         const int32_t *__restrict__ unit_chunk0, int64_t max_entries,
-                                                        uint16_t *__restrict__ tcol, float *__restrict__ tval)
+                                                        uint16_t *__restrict__ tcol, T *__restrict__ tval)
 {
+    constexpr int kSeg = window_points<T>();
+    constexpr int kMaxSeg = max_tiles_per_block(sizeof(T));
     const int lane = lane_id();
     for (int64_t r = (int64_t(blockIdx.x) * blockDim.x + threadIdx.x) / kWave; r < n;
          r += int64_t(gridDim.x) * (blockDim.x / kWave)) {
@@ -543,15 +561,15 @@ __global__ __launch_bounds__(256) void sell_copy_kernel(const int64_t *__restric
         for (int64_t j = a + lane; j < e; j += kWave) {
             const int32_t c = col[j];
             if (c == kNoColumn) continue;
-            const int32_t sg = c / kTileSeg, k = sg - lo;
+            const int32_t sg = c / kSeg, k = sg - lo;
             if (k < 0 || k >= ns) continue;
-            const int64_t t = blk_tiles[b * kTileMaxSeg + k];
+            const int64_t t = blk_tiles[b * kMaxSeg + k];
             const int32_t pos = tpos[t * kTileRows + rl];
             const int32_t u = unit_of[t * kSlicesPerTile + pos / kSellSlice];
-            const int64_t ei = j - row_lower_bound(col, a, e, sg * kTileSeg);
+            const int64_t ei = j - row_lower_bound(col, a, e, sg * kSeg);
             const int64_t d = (int64_t(unit_chunk0[u]) + ei / 4) * kSellChunk + (pos % kSellSlice) * 4 + ei % 4;
             if (d < 0 || d >= max_entries) continue;
-            tcol[d] = uint16_t(c - sg * kTileSeg);
+            tcol[d] = uint16_t(c - sg * kSeg);
             tval[d] = val[j];
         }
     }
@@ -747,6 +765,13 @@ __device__ inline void attract_add(float2 yi, float2 yj, float p, float &fx, flo
     fx = fmaf(pw, dx, fx);
     fy = fmaf(pw, dy, fy);
 }
+__device__ inline void attract_add(double2 yi, double2 yj, double p, double &fx, double &fy)
+{
+    const double dx = yi.x - yj.x, dy = yi.y - yj.y;
+    const double pw = p * wrecip(1.0 + fma(dx, dx, dy * dy));
+    fx = fma(pw, dx, fx);
+    fy = fma(pw, dy, fy);
+}
 
 // kAttBlock threads, kAttSeg points of Y per LDS segment, kAttRG rows per lane group.
 // Rows of the layout are sorted, padded to whole vectors and 16-byte aligned;
@@ -919,14 +944,25 @@ constexpr int kSellWaves = kTileBlock / kWave;
 constexpr int kItemMaxUnits = kItemMaxTiles * kSlicesPerTile;
 
 typedef uint16_t v4u16 __attribute__((ext_vector_type(4)));
+typedef double v4d __attribute__((ext_vector_type(4)));
+template <typename T> struct Vec4Of;
+template <> struct Vec4Of<float> { using type = v4f; };
+template <> struct Vec4Of<double> { using type = v4d; };
 
+// T = float: fp32 values and centres, 16384-point windows; T = double: the
+// fp64 variant, 8192-point windows.  Either way a window is 128 KB of LDS.
+template <typename T>
 __global__ __launch_bounds__(kTileBlock) void attract_sell_kernel(
     const int2 *__restrict__ item_tiles, const int4 *__restrict__ item_units, const int4 *__restrict__ wave_units,
     const int32_t *__restrict__ tile_blk, const int32_t *__restrict__ tile_seg,
     const int32_t *__restrict__ unit_chunks, const int32_t *__restrict__ unit_tj, const uint16_t *__restrict__ tperm,
-    const uint16_t *__restrict__ tcol, const float *__restrict__ tval, const float2 *__restrict__ ylay,
-    int32_t nitems, Header *__restrict__ hdr, float2 *__restrict__ partial)
+    const uint16_t *__restrict__ tcol, const T *__restrict__ tval, const vec2_t<T> *__restrict__ ylay,
+    int32_t nitems, Header *__restrict__ hdr, vec2_t<T> *__restrict__ partial)
 {
+    using V = vec2_t<T>;
+    using V4 = typename Vec4Of<T>::type;
+    constexpr int kSeg = window_points<T>();
+    static_assert(kSeg * sizeof(V) == kTileSeg * sizeof(float2), "a window is 128 KB of LDS");
     __shared__ v4f sy4[kTileSeg / 2];
     __shared__ int32_t s_row0[kItemMaxTiles];
     // per stored unit of the item: chunks (a run holds at most kTileSeg entries)
@@ -934,7 +970,7 @@ __global__ __launch_bounds__(kTileBlock) void attract_sell_kernel(
     static_assert(kTileSeg / 4 < 65536 && kItemMaxUnits <= 65536, "unit tables are 16-bit");
     __shared__ uint16_t s_K[kItemMaxUnits], s_tj[kItemMaxUnits];
     __shared__ uint32_t s_item;
-    const float2 *sy = reinterpret_cast<const float2 *>(sy4);
+    const V *sy = reinterpret_cast<const V *>(sy4);
     // a fixed grid takes the items (stored largest first) from a counter; the
     // barrier at the top also keeps the LDS of one item until every wave is done
     for (;;) {
@@ -952,15 +988,15 @@ __global__ __launch_bounds__(kTileBlock) void attract_sell_kernel(
 
         // this wave's chunk g (clamped: loads past the end are issued and unused)
         const uint16_t *tc = tcol + int64_t(wu.z) * kSellChunk + 4 * lane;
-        const float *tv = tval + int64_t(wu.z) * kSellChunk + 4 * lane;
+        const T *tv = tval + int64_t(wu.z) * kSellChunk + 4 * lane;
         v4u16 c[kSellRing];
-        v4f p[kSellRing];
+        V4 p[kSellRing];
         auto issue = [&](int x, int32_t g) {
             const int64_t at = int64_t(g < G ? g : (G > 0 ? G - 1 : 0)) * kSellChunk;
             // read once per iteration: streamed past the caches' retained lines, which
             // the sort and tree running beside this kernel keep using
             c[x] = __builtin_nontemporal_load(reinterpret_cast<const v4u16 *>(tc + at));
-            p[x] = __builtin_nontemporal_load(reinterpret_cast<const v4f *>(tv + at));
+            p[x] = __builtin_nontemporal_load(reinterpret_cast<const V4 *>(tv + at));
         };
         // the segment of Y (8 independent 16-byte loads per thread) and the first
         // chunks are in flight together
@@ -996,7 +1032,7 @@ __global__ __launch_bounds__(kTileBlock) void attract_sell_kernel(
         auto unit_row0 = [&](int32_t u) { return uni(s_row0[uni(s_tj[u - iu.x]) / kSlicesPerTile]); };
 
         // units without entries in their tile's segment: their rows' partials are 0
-        for (int32_t u = iu.y + w; u < iu.z; u += kSellWaves) partial[unit_at(u)] = make_float2(0.0f, 0.0f);
+        for (int32_t u = iu.y + w; u < iu.z; u += kSellWaves) partial[unit_at(u)] = make_vec2(T(0), T(0));
         if (wu.x < wu.y) { // this wave has units
         const int32_t ulast = wu.y - 1;
         int32_t u = wu.x;             // unit being summed (wave-uniform)
@@ -1007,27 +1043,27 @@ __global__ __launch_bounds__(kTileBlock) void attract_sell_kernel(
         int32_t rowA = unit_row0(u) + unit_rl(u);
         int32_t rowB = unit_row0(clampu(u + 1)) + unit_rl(clampu(u + 1));
         int32_t rlC = unit_rl(clampu(u + 2));
-        float2 yA = ylay[rowA], yB = ylay[rowB];
+        V yA = ylay[rowA], yB = ylay[rowB];
         // Wait here once for y of the first two units (the last loads issued):
         // otherwise the loop head, where this entry path meets the back edge,
         // would wait for them on every trip.  The empty statement only uses the
         // registers, which makes the compiler complete their loads before it.
         asm volatile("" ::"v"(yA.x), "v"(yA.y), "v"(yB.x), "v"(yB.y));
-        float fx = 0.0f, fy = 0.0f;
+        T fx = T(0), fy = T(0);
 
         // one wave step: sum chunk g from ring slot x, refill the slot with chunk
         // g + kSellRing, and close the unit when g was its last chunk
         auto step = [&](int x, int32_t g) {
             const bool live = g < G; // wave-uniform; dead steps only occur after the last chunk
-            float cx = 0.0f, cy = 0.0f;
+            T cx = T(0), cy = T(0);
 #pragma unroll
-            for (int v = 0; v < 4; ++v) attract_add(yA, sy[c[x][v] & (kTileSeg - 1)], p[x][v], cx, cy);
-            fx += live ? cx : 0.0f;
-            fy += live ? cy : 0.0f;
+            for (int v = 0; v < 4; ++v) attract_add(yA, sy[c[x][v] & (kSeg - 1)], T(p[x][v]), cx, cy);
+            fx += live ? cx : T(0);
+            fy += live ? cy : T(0);
             issue(x, g + kSellRing);
             if (live && g + 1 == uend) {
-                partial[unit_at(u)] = make_float2(fx, fy);
-                fx = fy = 0.0f;
+                partial[unit_at(u)] = make_vec2(fx, fy);
+                fx = fy = T(0);
                 ++u;
                 if (u <= ulast) uend += uni(s_K[u - iu.x]);
                 rowA = rowB;
@@ -1051,22 +1087,23 @@ __global__ __launch_bounds__(kTileBlock) void attract_sell_kernel(
 // row's original index (perm), so that the update reads it in the caller's
 // order without a gather.  Consecutive rows read one tile's 8 KB of partials
 // at a time.
-__global__ __launch_bounds__(256) void attract_rows_kernel(const float2 *__restrict__ partial,
+template <typename T>
+__global__ __launch_bounds__(256) void attract_rows_kernel(const vec2_t<T> *__restrict__ partial,
                                                            const int32_t *__restrict__ blk_nseg,
                                                            const int32_t *__restrict__ blk_tiles,
                                                            const uint16_t *__restrict__ tpos,
                                                            const uint32_t *__restrict__ perm, int64_t n,
-                                                           float2 *__restrict__ fattr)
+                                                           vec2_t<T> *__restrict__ fattr)
 {
     const int64_t r = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
     if (r >= n) return;
     const int64_t b = r / kTileRows;
     const int rr = int(r % kTileRows);
     const int ns = blk_nseg[b];
-    float2 fa = make_float2(0.0f, 0.0f);
+    vec2_t<T> fa = make_vec2(T(0), T(0));
     for (int k = 0; k < ns; ++k) {
-        const int64_t t = blk_tiles[b * kTileMaxSeg + k];
-        const float2 v = partial[t * kTileRows + tpos[t * kTileRows + rr]];
+        const int64_t t = blk_tiles[b * max_tiles_per_block(sizeof(T)) + k];
+        const vec2_t<T> v = partial[t * kTileRows + tpos[t * kTileRows + rr]];
         fa.x += v.x;
         fa.y += v.y;
     }
@@ -1126,23 +1163,24 @@ LayoutView layout_view(void *mem, int64_t n, int64_t nnz, int vbytes)
     // rows are padded to multiples of 4 entries, plus one 4-entry sentinel vector at the end
     const size_t cap = size_t(nnz) + 3 * size_t(n) + 4;
     size_t o_col = take(4 * cap), o_val = take(size_t(vbytes) * cap);
-    // tiled copy: at most kTileMaxSeg tiles per row block, sliced
+    // tiled copy: at most max_tiles_per_block tiles per row block, sliced
     const int64_t blocks = (n + kTileRows - 1) / kTileRows;
-    v.max_tiles = blocks * kTileMaxSeg;
+    const int max_seg = max_tiles_per_block(vbytes);
+    v.max_tiles = blocks * max_seg;
     // the sliced copy pads every run to its slice's longest run, rounded up to
     // whole chunks; it is built only when that fits in a quarter of nnz plus
     // one chunk per slice (else the row-block kernel is used)
     v.max_entries = nnz + nnz / 4 + int64_t(kSellChunk) * kSlicesPerTile * v.max_tiles + kSellChunk;
     const int64_t max_units = v.max_tiles * kSlicesPerTile;
     size_t o_lo = take(4 * size_t(blocks)), o_ns = take(4 * size_t(blocks)),
-           o_bt = take(4 * size_t(blocks) * kTileMaxSeg), o_tb = take(4 * size_t(v.max_tiles)),
+           o_bt = take(4 * size_t(blocks) * max_seg), o_tb = take(4 * size_t(v.max_tiles)),
            o_ts = take(4 * size_t(v.max_tiles)), o_tk = take(4 * size_t(v.max_tiles)),
            o_it = take(8 * size_t(v.max_tiles)), o_rl = take(4 * size_t(v.max_tiles) * kTileRows),
            o_tp = take(2 * size_t(v.max_tiles) * kTileRows), o_tq = take(2 * size_t(v.max_tiles) * kTileRows),
            o_uo = take(4 * size_t(max_units)), o_uk = take(4 * size_t(max_units)), o_uj = take(4 * size_t(max_units)),
            o_uc = take(4 * size_t(max_units)), o_iu = take(16 * size_t(v.max_tiles)),
            o_wu = take(16 * size_t(v.max_tiles) * (kTileRows / kWave)), o_tc = take(2 * size_t(v.max_entries)),
-           o_tv = take(4 * size_t(v.max_entries));
+           o_tv = take(size_t(vbytes) * size_t(v.max_entries));
     v.bytes = off;
     // windowed segments reuse the sliced copy's memory (tcol, then tval)
     const size_t seg_bytes = v.bytes - o_tc;
@@ -1172,6 +1210,7 @@ LayoutView layout_view(void *mem, int64_t n, int64_t nnz, int vbytes)
         v.wave_units = at<int4>(mem, o_wu);
         v.tcol = at<uint16_t>(mem, o_tc);
         v.tval = at<float>(mem, o_tv);
+        v.tval64 = at<double>(mem, o_tv);
         size_t o = o_tc;
         v.wstart = at<int64_t>(mem, o);
         o = align_up(o + 8 * (kMaxWindows + 1), 256);
@@ -1185,33 +1224,44 @@ LayoutView layout_view(void *mem, int64_t n, int64_t nnz, int vbytes)
 }
 
 // The tiled copy of a built (sorted, padded) layout; plan->tiled stays false when
-// some row block spans more than kTileMaxSeg segments.
+// some row block spans more than max_tiles_per_block segments.
+template <typename T>
 static int build_tiles(const LayoutView &lv, int64_t n, TilePlan *plan, void *ws, const Layout &L, hipStream_t st)
 {
+    constexpr int kSeg = window_points<T>();
+    constexpr int kMaxSeg = max_tiles_per_block(sizeof(T));
+    T *tval = sizeof(T) == 4 ? reinterpret_cast<T *>(lv.tval) : reinterpret_cast<T *>(lv.tval64);
+    const T *val = sizeof(T) == 4 ? reinterpret_cast<const T *>(lv.val) : reinterpret_cast<const T *>(lv.val64);
     *plan = TilePlan{};
     const int64_t blocks = (n + kTileRows - 1) / kTileRows;
     plan->blocks = int32_t(blocks);
-    tile_block_range_kernel<<<unsigned(blocks), 256, 0, st>>>(lv.row_ptr, lv.col, n, lv.blk_seg_lo, lv.blk_nseg);
+    Header *hdr = at<Header>(ws, L.header);
+    flag_clear_kernel<<<1, 1, 0, st>>>(&hdr->unsorted);
+    long_rows_kernel<<<unsigned((n + 255) / 256), 256, 0, st>>>(lv.row_ptr, n, sort_row_max<T>(), &hdr->unsorted);
+    uint32_t unsorted = 0;
+    if (hipMemcpyAsync(&unsorted, &hdr->unsorted, 4, hipMemcpyDeviceToHost, st) != hipSuccess) return -1;
+    tile_block_range_kernel<kSeg><<<unsigned(blocks), 256, 0, st>>>(lv.row_ptr, lv.col, n, lv.blk_seg_lo, lv.blk_nseg);
     std::vector<int32_t> lo(blocks), ns(blocks);
     if (hipMemcpyAsync(lo.data(), lv.blk_seg_lo, 4 * blocks, hipMemcpyDeviceToHost, st) != hipSuccess) return -1;
     if (hipMemcpyAsync(ns.data(), lv.blk_nseg, 4 * blocks, hipMemcpyDeviceToHost, st) != hipSuccess) return -1;
     if (hipStreamSynchronize(st) != hipSuccess) return -1;
+    if (unsorted) return 0; // a row too long to sort: keep the row-block kernel
     // tiles in segment-major order, (block, k) -> tile, then items of up to
     // `per` tiles that never straddle a segment (a few items per CU)
     std::vector<std::pair<int32_t, int32_t>> order; // (segment, block)
     for (int64_t b = 0; b < blocks; ++b) {
-        if (ns[b] > kTileMaxSeg) return 0; // too wide: keep the row-block kernel
+        if (ns[b] > kMaxSeg) return 0; // too wide: keep the row-block kernel
         for (int k = 0; k < ns[b]; ++k) order.emplace_back(lo[b] + k, int32_t(b));
     }
     const int64_t tiles = int64_t(order.size());
     if (tiles == 0 || tiles > lv.max_tiles) return 0;
     std::sort(order.begin(), order.end());
-    std::vector<int32_t> bt(size_t(blocks) * kTileMaxSeg, -1), tb(tiles), ts(tiles), tk(tiles);
+    std::vector<int32_t> bt(size_t(blocks) * kMaxSeg, -1), tb(tiles), ts(tiles), tk(tiles);
     for (int64_t t = 0; t < tiles; ++t) {
         ts[t] = order[t].first;
         tb[t] = order[t].second;
         tk[t] = ts[t] - lo[tb[t]];
-        bt[size_t(tb[t]) * kTileMaxSeg + tk[t]] = int32_t(t);
+        bt[size_t(tb[t]) * kMaxSeg + tk[t]] = int32_t(t);
     }
     if (hipMemcpyAsync(lv.blk_tiles, bt.data(), 4 * bt.size(), hipMemcpyHostToDevice, st) != hipSuccess) return -1;
     if (hipMemcpyAsync(lv.tile_blk, tb.data(), 4 * tiles, hipMemcpyHostToDevice, st) != hipSuccess) return -1;
@@ -1220,7 +1270,7 @@ static int build_tiles(const LayoutView &lv, int64_t n, TilePlan *plan, void *ws
     // run lengths, rows sorted by run length in every tile, chunks per slice
     const int64_t rows = blocks * kTileRows;
     const unsigned gw = unsigned((rows + 3) / 4 < 65535 * 4 ? (rows + 3) / 4 : 65535 * 4);
-    tile_run_len_kernel<<<gw, 256, 0, st>>>(lv.row_ptr, lv.col, n, rows, lv.blk_seg_lo, lv.blk_nseg, lv.blk_tiles,
+    tile_run_len_kernel<kSeg, kMaxSeg><<<gw, 256, 0, st>>>(lv.row_ptr, lv.col, n, rows, lv.blk_seg_lo, lv.blk_nseg, lv.blk_tiles,
                                             lv.run_len);
     tile_sort_kernel<<<unsigned(tiles), kTileRows, 0, st>>>(lv.run_len, lv.tperm, lv.tpos, lv.unit_chunks);
     const int64_t units = tiles * kSlicesPerTile;
@@ -1325,11 +1375,11 @@ static int build_tiles(const LayoutView &lv, int64_t n, TilePlan *plan, void *ws
     if (hipMemcpyAsync(lv.wave_units, wu.data(), 16 * wu.size(), hipMemcpyHostToDevice, st) != hipSuccess) return -1;
     // zeros everywhere (chunk 0 included, which lanes without work read), then the entries
     const int64_t zero = entries > kSellChunk ? entries : kSellChunk;
-    fill_zero_kernel<<<unsigned(std::min<int64_t>((zero + 255) / 256, 65535 * 4)), 256, 0, st>>>(lv.tcol, lv.tval,
-                                                                                                 zero);
-    sell_copy_kernel<<<unsigned(n < 65535 * 4 ? (n + 3) / 4 : 65535 * 4), 256, 0, st>>>(
-        lv.row_ptr, lv.col, lv.val, n, lv.blk_seg_lo, lv.blk_nseg, lv.blk_tiles, lv.tpos, lv.unit_of, lv.unit_chunk0,
-        lv.max_entries, lv.tcol, lv.tval);
+    fill_zero_kernel<T><<<unsigned(std::min<int64_t>((zero + 255) / 256, 65535 * 4)), 256, 0, st>>>(lv.tcol, tval,
+                                                                                                    zero);
+    sell_copy_kernel<T><<<unsigned(n < 65535 * 4 ? (n + 3) / 4 : 65535 * 4), 256, 0, st>>>(
+        lv.row_ptr, lv.col, val, n, lv.blk_seg_lo, lv.blk_nseg, lv.blk_tiles, lv.tpos, lv.unit_of, lv.unit_chunk0,
+        lv.max_entries, lv.tcol, tval);
     // the tables above must stay alive until the copies have been read
     if (hipStreamSynchronize(st) != hipSuccess) return -1;
     if (hipGetLastError() != hipSuccess) return -1;
@@ -1493,8 +1543,8 @@ int launch_layout_build(const int64_t *row_ptr, const int32_t *col, const V *val
     }
     if (relabel(row_ptr, col, val, n, nnz, Y, chosen, lv, ws, L, st) != 0) return -1;
     *plan = TilePlan{};
-    if (sizeof(V) == 4) { // the sliced copy holds fp32 values
-        int rc = build_tiles(lv, n, plan, ws, L, st);
+    {
+        int rc = build_tiles<V>(lv, n, plan, ws, L, st);
         if (rc != 0) return rc;
         if (plan->tiled) {
             plan->order = chosen;
@@ -1508,7 +1558,7 @@ int launch_layout_build(const int64_t *row_ptr, const int32_t *col, const V *val
             if (rc < 0) return -1;
             if (rc == 1) {
                 if (relabel(row_ptr, col, val, n, nnz, Y, kOrderBfs, lv, ws, L, st) != 0) return -1;
-                rc = build_tiles(lv, n, plan, ws, L, st);
+                rc = build_tiles<V>(lv, n, plan, ws, L, st);
                 if (rc != 0) return rc;
                 if (plan->tiled) {
                     plan->order = kOrderBfs;
@@ -1558,27 +1608,34 @@ static void launch_staged(const LayoutView &lv, int64_t n, int64_t nnz, int max_
                                                                    lv.perm, n, max_segs, at<float2>(ws, L.fattr));
 }
 
+template <typename T>
 void launch_attract_layout(const LayoutView &lv, int64_t n, int64_t nnz, int tiles, int items, int blocks,
                            int max_segs, int windows, void *ws, const Layout &L, hipStream_t st)
 {
+    using V = vec2_t<T>;
     if (tiles == 0 && windows > 0) {
-        launch_attract_windows<float>(lv, n, blocks, windows, ws, L, st);
+        launch_attract_windows<T>(lv, n, blocks, windows, ws, L, st);
         return;
     }
     if (tiles > 0) {
+        const T *tval = sizeof(T) == 4 ? reinterpret_cast<const T *>(lv.tval) : reinterpret_cast<const T *>(lv.tval64);
         const unsigned grid = unsigned(blocks < items ? blocks : items);
-        attract_sell_kernel<<<grid, kTileBlock, 0, st>>>(lv.item_tiles, lv.item_units, lv.wave_units, lv.tile_blk,
-                                                         lv.tile_seg, lv.unit_chunks, lv.unit_tj,
-                                                         lv.tperm, lv.tcol, lv.tval, at<float2>(ws, L.ycopy), items,
-                                                         at<Header>(ws, L.header), at<float2>(ws, L.partial));
-        attract_rows_kernel<<<unsigned((n + 255) / 256), 256, 0, st>>>(at<float2>(ws, L.partial), lv.blk_nseg,
-                                                                      lv.blk_tiles, lv.tpos, lv.perm, n,
-                                                                      at<float2>(ws, L.fattr));
+        attract_sell_kernel<T><<<grid, kTileBlock, 0, st>>>(lv.item_tiles, lv.item_units, lv.wave_units, lv.tile_blk,
+                                                            lv.tile_seg, lv.unit_chunks, lv.unit_tj, lv.tperm, lv.tcol,
+                                                            tval, at<V>(ws, L.ycopy), items, at<Header>(ws, L.header),
+                                                            at<V>(ws, L.partial));
+        attract_rows_kernel<T><<<unsigned((n + 255) / 256), 256, 0, st>>>(at<V>(ws, L.partial), lv.blk_nseg,
+                                                                         lv.blk_tiles, lv.tpos, lv.perm, n,
+                                                                         at<V>(ws, L.fattr));
         return;
     }
     // 1024 threads (one block per CU: the segment fills 128 KB of LDS), 2 rows per lane group
-    launch_staged<1024, 16384, 2>(lv, n, nnz, max_segs, ws, L, st);
+    if constexpr (sizeof(T) == 4) launch_staged<1024, 16384, 2>(lv, n, nnz, max_segs, ws, L, st);
 }
+template void launch_attract_layout<float>(const LayoutView &, int64_t, int64_t, int, int, int, int, int, void *,
+                                           const Layout &, hipStream_t);
+template void launch_attract_layout<double>(const LayoutView &, int64_t, int64_t, int, int, int, int, int, void *,
+                                            const Layout &, hipStream_t);
 
 template <typename T>
 void launch_update(const LayoutView &lv, int64_t n, bool layout_order, const StepArgsT<T> &a, T *Y, T *upd, T *gains,

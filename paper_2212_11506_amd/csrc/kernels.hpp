@@ -31,11 +31,12 @@ struct LayoutView {
     int32_t *col = nullptr;
     float *val = nullptr;           // fp32 values (fp32 layouts)
     double *val64 = nullptr;        // the same region as fp64 values (the fp64 variant's layouts)
-    // tiled copy: rows in blocks of kTileRows, columns in segments of kTileSeg
-    // points; one tile = (row block, segment), sliced into units of 64 rows
+    // tiled copy: rows in blocks of kTileRows, columns in segments of 128 KB of
+    // Y (kTileSeg fp32 points, kTileSeg / 2 fp64 points); one tile = (row
+    // block, segment), sliced into units of 64 rows
     int32_t *blk_seg_lo = nullptr;  // [blocks] first segment of a row block
     int32_t *blk_nseg = nullptr;    // [blocks] segments of a row block (0: none)
-    int32_t *blk_tiles = nullptr;   // [blocks * kTileMaxSeg] tile of (row block, k-th segment)
+    int32_t *blk_tiles = nullptr;   // [blocks * max_tiles_per_block] tile of (row block, k-th segment)
     int32_t *tile_blk = nullptr;    // [max tiles] row block of a tile; tiles are segment-major
     int32_t *tile_seg = nullptr;    // [max tiles] segment of a tile
     int32_t *tile_k = nullptr;      // [max tiles] segment of a tile counted from its block's first
@@ -51,6 +52,7 @@ struct LayoutView {
     int4 *wave_units = nullptr;     // [items * 16] units [x, y) and chunks [z, z + w) of a wave
     uint16_t *tcol = nullptr;       // [max entries] column offset in the segment
     float *tval = nullptr;          // [max entries]
+    double *tval64 = nullptr;       // the same region as fp64 values (the fp64 variant's layouts)
     int64_t max_tiles = 0, max_entries = 0;
     // windowed row segments (built instead of the sliced copy when rows have
     // no tile locality), carved from the sliced copy's memory: per column
@@ -114,9 +116,10 @@ void launch_attract(const int64_t *row_ptr, const int32_t *col, const T *val, in
 
 // vbytes: 4 (fp32 values) or 8 (the fp64 variant's layouts)
 LayoutView layout_view(void *mem, int64_t n, int64_t nnz, int vbytes = 4);
-// Builds the layout (synchronises the stream); fills *plan with the tile tables' sizes.
+// Builds the layout in the point order `order` (kOrder*; synchronises the
+// stream); fills *plan with the tile tables' sizes and the order taken.
 // Returns 0, 1 when P's row pointers are malformed (nothing else was read), or -1 on a HIP error.
-// V = double builds no sliced copy (only the relabelled rows and windowed segments).
+// V = double: fp64 values, the sliced copy over 8192-point windows (up to 32 per row block).
 template <typename V>
 int launch_layout_build(const int64_t *row_ptr, const int32_t *col, const V *val, int64_t n, int64_t nnz,
                         const V *Y, int order, const LayoutView &lv, TilePlan *plan, void *ws, const Layout &L,
@@ -128,6 +131,7 @@ void launch_attract_windows(const LayoutView &lv, int64_t n, int blocks, int win
 // Attractive forces through a layout: the streaming tile kernel when the
 // layout has tiles (tiles > 0, items > 0), else the row-block kernel.
 // `blocks`: grid of the persistent sliced kernel (items are taken from a counter)
+template <typename T>
 void launch_attract_layout(const LayoutView &lv, int64_t n, int64_t nnz, int tiles, int items, int blocks,
                            int max_segs, int windows, void *ws, const Layout &L, hipStream_t st);
 template <typename T>

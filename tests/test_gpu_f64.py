@@ -143,32 +143,42 @@ def _ring64(n, seed, m=3):
     return rp, col, val
 
 
-@pytest.mark.parametrize("case", ["c0", "late20k", "ring300k"])
+@pytest.mark.parametrize("case", ["c0", "late20k", "ring300k", "ring40_300k"])
 def test_gradient_through_f64_layout(case):
     """The fp64 variant through its locality layout (relabelled rows with fp64
-    values, windowed segments): the same 1e-9 / 1e-12 bars against the oracle,
-    and the same Z as the plain fp64 call (same tree and walk).  ring300k: a
-    ring P over a random Y, two column windows."""
+    values; the sliced copy over windows of 8192 points, or windowed
+    segments): the same 1e-9 / 1e-12 bars against the oracle, and the same Z
+    as the plain fp64 call (same tree and walk).  c0, late20k: clustered P,
+    Morton order, sliced copy.  ring300k: a ring P with 3 offsets over a
+    random Y, a lattice whose breadth-first levels tile.  ring40_300k: 20
+    offsets, whose levels explode: windowed segments (two column windows)."""
     if case == "c0":
         inp = synth.make_inputs(0)
         y, (rp, col, val) = _y64(inp.Y, 11), (inp.row_ptr, inp.col, inp.val)
     elif case == "late20k":
         y = CASES["late20k"]()
         rp, col, val = _p_for(y.shape[0])
-    else:
+    elif case == "ring300k":
         y = _y64(synth.random_y(300_000, seed=12, scale=2.0), 12)
         rp, col, val = _ring64(300_000, 12)
+    else:
+        y = _y64(synth.random_y(300_000, seed=16, scale=2.0), 16)
+        rp, col, val = _ring64(300_000, 16, m=20)
     n = y.shape[0]
     P = _p64(rp, col, val)
     Y = torch.from_numpy(y).to(DEV)
     ws = torch.empty(bh.workspace_size_f64(n, col.size), dtype=torch.uint8, device=DEV)
     lay = bh.LayoutF64(P, Y, workspace=ws)
-    assert lay.tiles == 0 and lay.windows == (n + (1 << 18) - 1) >> 18 and lay.segments > 0
+    if case == "ring40_300k":
+        assert lay.tiles == 0 and lay.windows == (n + (1 << 18) - 1) >> 18 and lay.segments > 0
+    else:
+        assert lay.tiles > 0 and lay.windows == 0
+        assert lay.order == (bh.ORDER_BFS if case == "ring300k" else bh.ORDER_MORTON)
     g, Z = bh.gradient_f64(Y, lay, 0.5, 12.0, workspace=ws)
     gp, Zp = bh.gradient_f64(Y, P, 0.5, 12.0, workspace=ws)
     go, Zo, _, _ = oracle.gradient(y, rp, col, val, 0.5, 12.0)
     err = rel_l2(g.cpu().numpy(), go)
-    say(f"[f64 layout] {case}: {lay.windows} windows, {lay.segments} segments, rel-L2 {err:.2e}, "
+    say(f"[f64 layout] {case}: {lay.tiles} tiles, {lay.windows} windows, {lay.segments} segments, rel-L2 {err:.2e}, "
         f"Z rel {abs(Z - Zo) / Zo:.2e}")
     assert err <= 1e-9 and abs(Z - Zo) <= 1e-12 * Zo
     assert Z == Zp and rel_l2(g.cpu().numpy(), gp.cpu().numpy()) <= 1e-12
@@ -210,12 +220,15 @@ def test_f64_and_fp32_layouts_are_not_interchangeable():
     assert e.value.status == bh.BHTSNE_EINVAL
 
 
-def test_f64_layout_with_a_row_too_long_to_sort_is_refused():
+@pytest.mark.parametrize("ring_m", [3, 20])
+def test_f64_layout_with_a_row_too_long_to_sort_is_refused(ring_m):
     """A row of 5000 entries is longer than the fp64 row sort takes (4096):
-    no segments, and the layout calls refuse the handle; the plain calls
-    still serve such a P."""
+    neither the sliced copy (which finds runs by binary search) nor segments,
+    and the layout calls refuse the handle; the plain calls still serve such
+    a P.  With 3 ring offsets the rest of P would tile (its breadth-first
+    levels), with 20 it would take windowed segments."""
     n = 300_000
-    rp, col, val = synth.ring_p(n, 15, m=3)
+    rp, col, val = synth.ring_p(n, 15, m=ring_m)
     import scipy.sparse as sp
     P = sp.csr_matrix((val.astype(np.float64), col, rp), shape=(n, n))
     others = np.random.default_rng(15).choice(np.arange(1, n), size=5000, replace=False)
@@ -229,7 +242,7 @@ def test_f64_layout_with_a_row_too_long_to_sort_is_refused():
     Pd = bh.CsrF64.from_numpy(P.indptr.astype(np.int64), P.indices.astype(np.int32), P.data, device=DEV)
     Y = torch.from_numpy(y).to(DEV)
     lay = bh.LayoutF64(Pd, Y)
-    assert lay.windows == 0
+    assert lay.windows == 0 and lay.tiles == 0
     with pytest.raises(bh.BhtsneError) as e:
         bh.gradient_f64(Y, lay, 0.5, 1.0)
     assert e.value.status == bh.BHTSNE_EINVAL

@@ -575,3 +575,32 @@ def test_explicit_orders_on_a_clustered_p():
     with pytest.raises(bh.BhtsneError) as e:
         bh.Layout(P, Y, order=7)
     assert e.value.status == bh.BHTSNE_EINVAL
+
+
+def test_a_row_too_long_to_sort_rules_out_the_sliced_copy():
+    """40,000 points of workload 1's clusters (which tile) plus one point
+    linked to 9,000 others: that row is longer than the in-LDS row sort
+    (8192) and stays unsorted, so the sliced copy, which finds a row's runs
+    by binary search, is not built.  With one column window of 2^18 points a
+    row is a single segment, whose order does not matter, so the windowed
+    segments serve the layout; the gradient matches the oracle."""
+    inp = synth.make_inputs(1, n=40000)
+    n = inp.n
+    P = sp.csr_matrix((inp.val.astype(np.float64), inp.col, inp.row_ptr), shape=(n, n))
+    others = np.random.default_rng(17).choice(np.arange(1, n), size=9000, replace=False)
+    H = sp.csr_matrix((np.full(18000, 1e-7), (np.r_[np.zeros(9000, int), others], np.r_[others, np.zeros(9000, int)])),
+                      shape=(n, n))
+    P = (P + H).tocsr()
+    P.sum_duplicates()
+    P.sort_indices()
+    P.data /= P.data.sum()
+    rp, col, val = P.indptr.astype(np.int64), P.indices.astype(np.int32), P.data.astype(np.float32)
+    assert np.diff(rp).max() > 8192
+    Y = torch.from_numpy(inp.Y).cuda()
+    lay = bh.Layout(bh.Csr.from_numpy(rp, col, val), Y)
+    assert lay.tiles == 0 and lay.windows == 1
+    g, Z = bh.gradient(Y, lay, 0.5, 12.0)
+    go, Zo, _, _ = oracle.gradient(inp.Y, rp, col, val, 0.5, 12.0)
+    assert rel_l2(g.cpu().numpy(), go) <= 1e-3 and abs(Z - Zo) <= 1e-5 * Zo
+    # without the long row the same P tiles
+    assert bh.Layout(bh.Csr.from_numpy(inp.row_ptr, inp.col, inp.val), Y).tiles > 0
