@@ -126,7 +126,7 @@ def attractive_path(lay):
     return "windowed segments" if lay.windows > 0 else "row blocks"
 
 
-def gpu_run(inp, theta, steps, warmup, schedule, layout=True, order=None):
+def gpu_run(inp, theta, steps, warmup, schedule, layout=True, order=None, graph=False):
     """Iterations of `schedule` on the GPU through the locality layout (the
     launch configuration of the headline run), inputs resident in HBM: the
     rate over `steps` timed iterations after `warmup` untimed ones (from the
@@ -185,6 +185,32 @@ def gpu_run(inp, theta, steps, warmup, schedule, layout=True, order=None):
     torch.cuda.synchronize()
     same = bool(np.array_equal(Y.cpu().numpy(), y_final))
     inter = float(np.mean(counts)) if same else None
+    graph_rate = graph_same = None
+    if graph:
+        # the same iterations replayed from HIP graphs, one per set of the
+        # schedule's parameters (a step never synchronises without Z)
+        graphs = {}
+        keys = [tuple(schedule(it)[k] for k in ("exaggeration", "learning_rate", "momentum")) for it in range(steps)]
+        reset()
+        torch.cuda.synchronize()
+        for key in dict.fromkeys(keys):
+            gr = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gr):
+                bh.step(Y, P, theta, key[0], key[1], key[2], 0.01, u, g, workspace=ws)
+            graphs[key] = gr
+        torch.cuda.synchronize()
+        for gr in graphs.values():  # warm replays, then the initial state again
+            gr.replay()
+        torch.cuda.synchronize()
+        reset()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for key in keys:
+            graphs[key].replay()
+        torch.cuda.synchronize()
+        graph_rate = steps / (time.perf_counter() - t0)
+        graph_same = bool(np.array_equal(Y.cpu().numpy(), y_final))
+        del graphs
     rep_ms = ph["repulsive"][0] / max(ph["repulsive"][1], 1)
     att_ms = ph["attractive"][0] / max(ph["attractive"][1], 1)
     out = {"n": n, "nnz": nnz, "theta": theta, "steps": steps, "iterations_per_s": steps / dt,
@@ -195,6 +221,9 @@ def gpu_run(inp, theta, steps, warmup, schedule, layout=True, order=None):
     if layout:
         out["layout_order"] = "bfs levels" if P.order == bh.ORDER_BFS else "morton"
         out["layout_build_s"] = build_s
+    if graph:
+        out["graph_iterations_per_s"] = graph_rate
+        out["graph_matches_eager"] = graph_same
     if inter:
         tf = FLOPS_PER_INTERACTION * inter / (rep_ms * 1e-3) / 1e12
         out["repulsive_tflops"] = tf
@@ -286,7 +315,8 @@ def bench_configs(args, log_every=None):
         entry = {"workload": f"{w.description} (workload {cid})", "n": inp.n, "nnz": inp.nnz,
                  "schedule": f"iterations 0..{steps - 1}", "by_theta": {}}
         for theta in thetas:
-            r = gpu_run(inp, theta, steps, 5 if steps >= 50 else 1, w.schedule)
+            # the small workloads are launch-bound: also replayed from HIP graphs
+            r = gpu_run(inp, theta, steps, 5 if steps >= 50 else 1, w.schedule, graph=cid in (0, 1))
             log(f"[bench] workload {cid} theta={theta}: {r['iterations_per_s']:.1f} it/s, "
                 f"{r['interactions_per_s'] or 0:.3e} interactions/s")
             if not args.no_cpu and cpu_iters:
