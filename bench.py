@@ -64,6 +64,7 @@ def parse():
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the other workloads (0, 1, 3 and 4 at each theta) of the headline run")
     ap.add_argument("--no-3d", action="store_true", help="skip the 3-D embedding measurement")
+    ap.add_argument("--3d-only", dest="only_3d", action="store_true", help="measure only the 3-D embedding path")
     ap.add_argument("--no-locality", action="store_true",
                     help="skip the layout-order measurement on a geometric P with a random Y")
     ap.add_argument("--locality-only", action="store_true", help="measure only the layout orders")
@@ -335,7 +336,9 @@ def bench_configs(args, log_every=None):
 def bench_3d(args, steps=200, warmup=5):
     """The 3-D embedding path on workload 2's P with a 3-D early-phase Y
     (N(0, 1e-4 I3)): iterations/s over the first `steps` iterations of the
-    schedule on the plain CSR P, with the walk's event time."""
+    schedule with P through the 3-D locality layout (the sliced attraction
+    beside the sort, tree and walk), then on the plain CSR P; each with the
+    phases' event times."""
     import numpy as np
     import torch
 
@@ -350,43 +353,59 @@ def bench_3d(args, steps=200, warmup=5):
     ws = torch.empty(bh.workspace_size_3d(n, nnz), dtype=torch.uint8, device=dev)
     Y0 = torch.from_numpy(inp.Y).to(dev)
     Y, u, g = Y0.clone(), torch.zeros_like(Y0), torch.ones_like(Y0)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    lay = bh.Layout3(P, Y0, workspace=ws)
+    torch.cuda.synchronize()
+    build_s = time.perf_counter() - t0
 
-    def run(k, per_step=None):
+    def reset():
+        Y.copy_(Y0)
+        u.zero_()
+        g.fill_(1.0)
+
+    def run(PP, k, per_step=None):
         for it in range(k):
             s = w.schedule(it)
-            bh.step_3d(Y, P, args.theta, s["exaggeration"], s["learning_rate"], s["momentum"], 0.01, u, g,
+            bh.step_3d(Y, PP, args.theta, s["exaggeration"], s["learning_rate"], s["momentum"], 0.01, u, g,
                        workspace=ws)
             if per_step:
                 per_step(it)
 
-    run(warmup)
-    torch.cuda.synchronize()
-    Y.copy_(Y0)
-    u.zero_()
-    g.fill_(1.0)
-    bh.timing_read(reset=True)
-    bh.timing_phases(None)
-    bh.timing_enable(True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    run(steps)
-    torch.cuda.synchronize()
-    dt = time.perf_counter() - t0
-    bh.timing_enable(False)
-    ph = bh.timing_read(reset=True)
-    Y.copy_(Y0)
-    u.zero_()
-    g.fill_(1.0)
+    def measure(PP):
+        run(PP, warmup)
+        torch.cuda.synchronize()
+        reset()
+        bh.timing_read(reset=True)
+        bh.timing_phases(None)
+        bh.timing_enable(True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        run(PP, steps)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        bh.timing_enable(False)
+        ph = bh.timing_read(reset=True)
+        reset()
+        return {"iterations_per_s": steps / dt, "ms_per_step": 1e3 * dt / steps,
+                "phases_ms": {k: v[0] / v[1] for k, v in ph.items() if v[1]}}
+
+    tiled = lay.tiles > 0
+    out = {"workload": "workload 2's P (1.3M points) with a 3-D early-phase Y ~ N(0, 1e-4 I3)",
+           "n": n, "nnz": nnz, "theta": args.theta, "steps": steps,
+           "attractive_path": "sliced tiles" if tiled else "plain CSR (the layout has no tiles)",
+           "layout_tiles": lay.tiles, "layout_entries": lay.entries,
+           "layout_order": "bfs levels" if lay.order == bh.ORDER_BFS else "morton", "layout_build_s": build_s}
+    out.update(measure(lay if tiled else P))
+    out["plain_csr"] = measure(P)
     counts = []
-    run(steps, per_step=lambda it: counts.append(bh.get_stats(ws)["interactions"]))
+    run(P, steps, per_step=lambda it: counts.append(bh.get_stats(ws)["interactions"]))
     torch.cuda.synchronize()
+    reset()
     inter = float(np.mean(counts))
-    out = {"workload": "workload 2's P (1.3M points) with a 3-D early-phase Y ~ N(0, 1e-4 I3), plain CSR P",
-           "n": n, "nnz": nnz, "theta": args.theta, "steps": steps, "iterations_per_s": steps / dt,
-           "ms_per_step": 1e3 * dt / steps, "interactions_per_iteration": inter,
-           "phases_ms": {k: v[0] / v[1] for k, v in ph.items() if v[1]}}
+    out["interactions_per_iteration"] = inter
     out["interactions_per_s_walk"] = inter / (out["phases_ms"]["repulsive"] * 1e-3)
-    del P, ws, Y0, Y, u, g
+    del P, ws, Y0, Y, u, g, lay
     torch.cuda.empty_cache()
     return out
 
@@ -531,6 +550,9 @@ def main():
         return
     if args.locality_only:
         print(json.dumps({"locality": bench_locality(args)}), flush=True)
+        return
+    if args.only_3d:
+        print(json.dumps({"embedding_3d": bench_3d(args)}), flush=True)
         return
     w = synth.WORKLOADS[args.workload]
     t0 = time.time()

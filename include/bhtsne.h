@@ -423,16 +423,42 @@ int bhtsne_step_layout_f64(double *Y, const bhtsne_layout *layout, double theta,
  *    level below), and a cell stands in for its points when
  *    side^2 < theta^2 |y_i - c|^2;
  *  - Y, grad, update and gains are n x 3 float32, row-major (x, y, z).
- * The workspace is bhtsne_workspace_size_3d bytes.  There is no locality
- * layout for 3-D.  Arguments, checks, synchronisation and errors as the 2-D
- * calls; bhtsne_get_stats reports Z, the interaction and node counts and
- * max_depth (bbox and r_span hold x, y and the cube's r_span). */
+ * The workspace is bhtsne_workspace_size_3d bytes.  Arguments, checks,
+ * synchronisation and errors as the 2-D calls; bhtsne_get_stats reports Z,
+ * the interaction and node counts and max_depth (bbox and r_span hold x, y
+ * and the cube's r_span). */
 size_t bhtsne_workspace_size_3d(int64_t n, int64_t nnz);
 int bhtsne_gradient_3d(const float *Y, const bhtsne_csr *P, float theta, float exaggeration, float *grad,
                        double *Z, void *workspace, size_t workspace_bytes, hipStream_t stream);
 int bhtsne_step_3d(float *Y, const bhtsne_csr *P, float theta, float exaggeration, float learning_rate,
                    float momentum, float min_gain, float *update, float *gains, float *grad, double *Z,
                    void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Locality layout for 3-D embeddings: the relabelled copy of P and its sliced
+ * copy, as bhtsne_layout_build with the automatic order (Morton order of the
+ * n x 3 Y when given, else the breadth-first order when Morton order gives no
+ * tiles), over column windows of 8192 points (96 KB of LDS) and up to 32
+ * tiles per row block.  There are no windowed segments: when no order gives
+ * tiles (or a row is too long to sort) the build succeeds with tiles == 0 and
+ * the 3-D layout calls refuse the handle with BHTSNE_EINVAL; the plain 3-D
+ * calls serve such a P.  layout_mem holds bhtsne_layout_size_3d bytes (256-byte
+ * aligned, owned by the caller and kept alive and unchanged while the handle
+ * is used); the workspace is bhtsne_workspace_size_3d bytes.  The handle is
+ * tagged as a 3-D layout: the 2-D layout calls refuse it and these calls
+ * refuse a 2-D one.  bhtsne_gradient_layout_3d / bhtsne_step_layout_3d are
+ * bhtsne_gradient_3d / bhtsne_step_3d taking P through such a layout: the
+ * attractive forces run on the library's second stream beside the sort,
+ * tree and walk; results come back in the caller's order.  Errors as the
+ * plain 3-D calls, and BHTSNE_EINPUT from the build for malformed row
+ * pointers. */
+size_t bhtsne_layout_size_3d(int64_t n, int64_t nnz);
+int bhtsne_layout_build_3d(const bhtsne_csr *P, const float *Y, void *layout_mem, size_t layout_bytes,
+                           bhtsne_layout *out, void *workspace, size_t workspace_bytes, hipStream_t stream);
+int bhtsne_gradient_layout_3d(const float *Y, const bhtsne_layout *layout, float theta, float exaggeration,
+                              float *grad, double *Z, void *workspace, size_t workspace_bytes, hipStream_t stream);
+int bhtsne_step_layout_3d(float *Y, const bhtsne_layout *layout, float theta, float exaggeration,
+                          float learning_rate, float momentum, float min_gain, float *update, float *gains,
+                          float *grad, double *Z, void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Test exports for 3-D embeddings, as bhtsne_debug_sort / bhtsne_debug_tree:
  * params is a host array of 14 doubles {min x, max x, min y, max y, min z,

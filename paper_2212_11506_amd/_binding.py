@@ -106,6 +106,12 @@ def load_library():
         "bhtsne_gradient_3d": (C.c_int, [vp, C.POINTER(_Csr), f32, f32, vp, f64p, vp, C.c_size_t, vp]),
         "bhtsne_step_3d": (C.c_int, [vp, C.POINTER(_Csr), f32, f32, f32, f32, f32, vp, vp, vp, f64p, vp,
                                      C.c_size_t, vp]),
+        "bhtsne_layout_size_3d": (C.c_size_t, [i64, i64]),
+        "bhtsne_layout_build_3d": (C.c_int, [C.POINTER(_Csr), vp, vp, C.c_size_t, C.POINTER(_Layout), vp,
+                                             C.c_size_t, vp]),
+        "bhtsne_gradient_layout_3d": (C.c_int, [vp, C.POINTER(_Layout), f32, f32, vp, f64p, vp, C.c_size_t, vp]),
+        "bhtsne_step_layout_3d": (C.c_int, [vp, C.POINTER(_Layout), f32, f32, f32, f32, f32, vp, vp, vp, f64p, vp,
+                                            C.c_size_t, vp]),
         "bhtsne_debug_sort_3d": (C.c_int, [vp, i64, vp, vp, vp, f64p, vp, C.c_size_t, vp]),
         "bhtsne_debug_tree_3d": (C.c_int, [vp, i64, f32, C.POINTER(C.c_int64), vp, vp, vp, vp, vp, vp, vp, vp,
                                            C.c_size_t, vp]),
@@ -525,20 +531,50 @@ def _check_3d(Y):
         raise ValueError("a 3-D embedding is an n x 3 tensor")
 
 
+class Layout3(Layout):
+    """A locality layout of P for 3-D embeddings (bhtsne_layout_build_3d): the
+    relabelled rows and their sliced copy over 8192-point windows of 3-D
+    points.  With tiles == 0 (no tile locality) the 3-D calls refuse it and
+    the plain Csr serves."""
+
+    def __init__(self, P: Csr, Y: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None):
+        lib = load_library()
+        if Y is not None:
+            _check_3d(Y)
+        self.n, self.nnz = P.n, P.nnz
+        need = int(lib.bhtsne_layout_size_3d(P.n, P.nnz))
+        if need == 0:
+            raise BhtsneError(BHTSNE_EINVAL, "bhtsne_layout_size_3d")
+        self.mem = torch.empty(need, dtype=torch.uint8, device="cuda")
+        ws = _workspace_3d(P.n, P.nnz, workspace)
+        self._s = _Layout()
+        rc = lib.bhtsne_layout_build_3d(P.struct, _ptr(Y, torch.float32, "Y"), _ptr(self.mem), need,
+                                        C.byref(self._s), _ptr(ws), ws.numel(), _stream())
+        _check(rc, "bhtsne_layout_build_3d")
+
+
+def layout_size_3d(n: int, nnz: int) -> int:
+    return int(load_library().bhtsne_layout_size_3d(int(n), int(nnz)))
+
+
 def gradient_3d(Y: torch.Tensor, P: "Csr", theta: float, exaggeration: float = 1.0,
                 grad: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
                 return_z: bool = True):
-    """bhtsne_gradient_3d: returns (grad n x 3, Z or None)."""
+    """bhtsne_gradient_3d (P a Csr) or bhtsne_gradient_layout_3d (P a Layout3):
+    returns (grad n x 3, Z or None)."""
     lib = load_library()
     _check_3d(Y)
+    if isinstance(P, Layout) and not isinstance(P, Layout3):
+        raise TypeError("gradient_3d takes P as a Csr or a Layout3")
     if grad is None:
         grad = torch.empty_like(Y)
     ws = _workspace_3d(P.n, P.nnz, workspace)
     z = C.c_double(0.0)
-    rc = lib.bhtsne_gradient_3d(_ptr(Y, torch.float32, "Y"), P.struct, float(theta), float(exaggeration),
-                                _ptr(grad, torch.float32, "grad"), C.byref(z) if return_z else None,
-                                _ptr(ws, None, "workspace"), ws.numel(), _stream())
-    _check(rc, "bhtsne_gradient_3d")
+    fn = lib.bhtsne_gradient_layout_3d if isinstance(P, Layout3) else lib.bhtsne_gradient_3d
+    rc = fn(_ptr(Y, torch.float32, "Y"), P.struct, float(theta), float(exaggeration),
+            _ptr(grad, torch.float32, "grad"), C.byref(z) if return_z else None,
+            _ptr(ws, None, "workspace"), ws.numel(), _stream())
+    _check(rc, fn.__name__)
     return grad, (z.value if return_z else None)
 
 
@@ -546,17 +582,21 @@ def step_3d(Y: torch.Tensor, P: "Csr", theta: float, exaggeration: float, learni
             momentum: float, min_gain: float, update: torch.Tensor, gains: torch.Tensor,
             grad: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
             return_z: bool = False):
-    """bhtsne_step_3d: one iteration in place on Y, update and gains (n x 3)."""
+    """bhtsne_step_3d (P a Csr) or bhtsne_step_layout_3d (P a Layout3): one
+    iteration in place on Y, update and gains (n x 3)."""
     lib = load_library()
     _check_3d(Y)
+    if isinstance(P, Layout) and not isinstance(P, Layout3):
+        raise TypeError("step_3d takes P as a Csr or a Layout3")
     ws = _workspace_3d(P.n, P.nnz, workspace)
     z = C.c_double(0.0)
-    rc = lib.bhtsne_step_3d(_ptr(Y, torch.float32, "Y"), P.struct, float(theta), float(exaggeration),
-                            float(learning_rate), float(momentum), float(min_gain),
-                            _ptr(update, torch.float32, "update"), _ptr(gains, torch.float32, "gains"),
-                            _ptr(grad, torch.float32, "grad"), C.byref(z) if return_z else None,
-                            _ptr(ws, None, "workspace"), ws.numel(), _stream())
-    _check(rc, "bhtsne_step_3d")
+    fn = lib.bhtsne_step_layout_3d if isinstance(P, Layout3) else lib.bhtsne_step_3d
+    rc = fn(_ptr(Y, torch.float32, "Y"), P.struct, float(theta), float(exaggeration),
+            float(learning_rate), float(momentum), float(min_gain),
+            _ptr(update, torch.float32, "update"), _ptr(gains, torch.float32, "gains"),
+            _ptr(grad, torch.float32, "grad"), C.byref(z) if return_z else None,
+            _ptr(ws, None, "workspace"), ws.numel(), _stream())
+    _check(rc, fn.__name__)
     return z.value if return_z else None
 
 

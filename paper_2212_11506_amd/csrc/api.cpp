@@ -313,14 +313,16 @@ bool window_path_enabled()
 }
 
 constexpr uint64_t kLayoutMagic64 = 0x62687473654c3634ull; // "bhtseL64": an fp64 layout
+constexpr uint64_t kLayoutMagic3 = 0x62687473654c3033ull;  // "bhtseL03": a 3-D layout
 
-// vbytes: 4 for the fp32 calls' layouts, 8 for the fp64 variant's
-int check_layout(const bhtsne_layout *lay, int vbytes = 4)
+// vbytes: 4 for the fp32 calls' layouts, 8 for the fp64 variant's; dim 3 for
+// the 3-D calls' layouts
+int check_layout(const bhtsne_layout *lay, int vbytes = 4, int dim = 2)
 {
-    if (!lay || lay->magic != (vbytes == 8 ? kLayoutMagic64 : kLayoutMagic) || !lay->mem || !aligned(lay->mem))
-        return BHTSNE_EINVAL;
+    const uint64_t magic = dim == 3 ? kLayoutMagic3 : (vbytes == 8 ? kLayoutMagic64 : kLayoutMagic);
+    if (!lay || lay->magic != magic || !lay->mem || !aligned(lay->mem)) return BHTSNE_EINVAL;
     if (lay->n < 2 || lay->n > kMaxPoints || lay->nnz < 0) return BHTSNE_EINVAL;
-    const LayoutView v = layout_view(nullptr, lay->n, lay->nnz, vbytes);
+    const LayoutView v = layout_view(nullptr, lay->n, lay->nnz, vbytes, dim);
     if (lay->bytes < v.bytes) return BHTSNE_EINVAL;
     if (lay->tiles < 0 || lay->tiles > v.max_tiles) return BHTSNE_EINVAL;
     if (lay->items < 0 || lay->items > lay->tiles || (lay->tiles > 0) != (lay->items > 0)) return BHTSNE_EINVAL;
@@ -476,7 +478,7 @@ int run3(float *Y, const bhtsne_csr *P, float theta, const StepArgs &a, float *u
     const Layout L = make_layout(n, P->nnz, 4, 3);
     {
         PhaseTimer pt(BHTSNE_PHASE_BBOX_MORTON, st);
-        launch_bbox_morton3(Y, n, ws, L, st);
+        launch_bbox_morton3(Y, n, nullptr, ws, L, st);
     }
     {
         PhaseTimer pt(BHTSNE_PHASE_SORT, st);
@@ -493,6 +495,54 @@ int run3(float *Y, const bhtsne_csr *P, float theta, const StepArgs &a, float *u
     {
         PhaseTimer pt(BHTSNE_PHASE_ATTRACTIVE, st);
         launch_attract<3>(P->row_ptr, P->col, P->val, n, P->nnz, a, Y, update, gains, grad, ws, L, st);
+    }
+    return finish(Z, ws, st);
+}
+
+// A 3-D embedding through a layout: the codes also write the layout-order copy
+// of Y, the sliced attraction runs on the second stream beside the sort, tree
+// and walk, and the update joins F_attr (caller's order) with F_rep.
+int run_layout3(float *Y, const bhtsne_layout *lay, float theta, const StepArgs &a, float *update, float *gains,
+                float *grad, double *Z, void *ws, hipStream_t st)
+{
+    const int64_t n = lay->n;
+    const Layout L = make_layout(n, lay->nnz, 4, 3);
+    const LayoutView lv = layout_view(lay->mem, n, lay->nnz, 4, 3);
+    {
+        PhaseTimer pt(BHTSNE_PHASE_BBOX_MORTON, st);
+        launch_bbox_morton3(Y, n, lv.rank, ws, L, st);
+    }
+    Side *side = overlap_enabled() ? side_stream() : nullptr;
+    std::unique_lock<std::mutex> lk;
+    if (side) {
+        lk = std::unique_lock<std::mutex>(side->mu);
+        if (hipEventRecord(side->fork, st) != hipSuccess || hipStreamWaitEvent(side->st, side->fork, 0) != hipSuccess)
+            return BHTSNE_EDEVICE;
+    }
+    const hipStream_t sa = side ? side->st : st;
+    {
+        PhaseTimer pt(BHTSNE_PHASE_ATTRACTIVE, sa);
+        launch_attract_layout3(lv, n, int(lay->tiles), int(lay->items), attract_blocks(side != nullptr, int(lay->items)),
+                               ws, L, sa);
+    }
+    if (side && hipEventRecord(side->join, sa) != hipSuccess) return BHTSNE_EDEVICE;
+    {
+        PhaseTimer pt(BHTSNE_PHASE_SORT, st);
+        launch_sort_points(n, reinterpret_cast<const float3 *>(Y), ws, L, st);
+    }
+    {
+        PhaseTimer pt(BHTSNE_PHASE_TREE, st);
+        launch_tree<3, float>(n, double(theta) * double(theta), ws, L, TreeDebug{}, st);
+    }
+    {
+        PhaseTimer pt(BHTSNE_PHASE_REPULSIVE, st);
+        launch_repulsive<3, float>(n, repulsive_self_test3(theta), ws, L, st);
+    }
+    if (side && hipStreamWaitEvent(st, side->join, 0) != hipSuccess) return BHTSNE_EDEVICE;
+    if (lk.owns_lock()) lk.unlock();
+    {
+        PhaseTimer pt(BHTSNE_PHASE_UPDATE, st);
+        launch_update3(n, a, Y, update, gains, grad, ws, L, st);
     }
     return finish(Z, ws, st);
 }
@@ -672,7 +722,7 @@ int bhtsne_debug_sort_3d(const float *Y, int64_t n, uint64_t *codes, uint64_t *s
     int rc = check_ws_3d(n, 0, workspace, workspace_bytes);
     if (rc != BHTSNE_OK) return rc;
     const Layout L = make_layout(n, 0, 4, 3);
-    launch_bbox_morton3(Y, n, workspace, L, stream);
+    launch_bbox_morton3(Y, n, nullptr, workspace, L, stream);
     if (codes && hipMemcpyAsync(codes, at<void>(workspace, L.codes0), 8 * size_t(n), hipMemcpyDeviceToDevice,
                                 stream) != hipSuccess)
         return BHTSNE_EDEVICE;
@@ -711,7 +761,7 @@ int bhtsne_debug_tree_3d(const float *Y, int64_t n, float theta, int64_t *n_node
     dbg.kind = kind;
     dbg.begin = begin;
     dbg.end = end;
-    launch_bbox_morton3(Y, n, workspace, L, stream);
+    launch_bbox_morton3(Y, n, nullptr, workspace, L, stream);
     launch_sort_points(n, reinterpret_cast<const float3 *>(Y), workspace, L, stream);
     launch_tree<3, float>(n, double(theta) * double(theta), workspace, L, dbg, stream);
     if (summary || threshold || meta) launch_tree_unpack3(n, workspace, L, summary, threshold, meta, stream);
@@ -721,6 +771,84 @@ int bhtsne_debug_tree_3d(const float *Y, int64_t n, float theta, int64_t *n_node
     if (rc != BHTSNE_OK) return rc;
     *n_nodes = int64_t(h.nodes);
     return flags_status(h.flags);
+}
+
+size_t bhtsne_layout_size_3d(int64_t n, int64_t nnz)
+{
+    if (n < 2 || n > kMaxPoints || nnz < 0) return 0;
+    return layout_view(nullptr, n, nnz, 4, 3).bytes;
+}
+
+int bhtsne_layout_build_3d(const bhtsne_csr *P, const float *Y, void *layout_mem, size_t layout_bytes,
+                           bhtsne_layout *out, void *workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    int rc = check_csr(P);
+    if (rc != BHTSNE_OK) return rc;
+    if (!out || !layout_mem || !aligned(layout_mem)) return BHTSNE_EINVAL;
+    if (layout_bytes < bhtsne_layout_size_3d(P->n, P->nnz)) return BHTSNE_EINVAL;
+    if (P->nnz + 3 * P->n + 4 >= (int64_t(1) << 31)) return BHTSNE_EINVAL;
+    rc = check_ws_3d(P->n, P->nnz, workspace, workspace_bytes);
+    if (rc != BHTSNE_OK) return rc;
+    const Layout L = make_layout(P->n, P->nnz, 4, 3);
+    const LayoutView lv = layout_view(layout_mem, P->n, P->nnz, 4, 3);
+    TilePlan plan;
+    const int built = launch_layout_build<float, 3>(P->row_ptr, P->col, P->val, P->n, P->nnz, Y, kOrderAuto, lv,
+                                                    &plan, workspace, L, stream);
+    if (built == 1) return BHTSNE_EINPUT;
+    if (built != 0) return BHTSNE_EDEVICE;
+    Header h;
+    rc = read_header(workspace, &h, stream);
+    if (rc != BHTSNE_OK) return rc;
+    if (h.flags & (kErrLookback | kErrRange)) return BHTSNE_EDEVICE;
+    out->n = P->n;
+    out->nnz = P->nnz;
+    out->mem = layout_mem;
+    out->bytes = layout_bytes;
+    out->order = plan.order;
+    const bool tiled = plan.tiled && tile_path_enabled();
+    out->tiles = tiled ? plan.tiles : 0;
+    out->items = tiled ? plan.items : 0;
+    out->entries = tiled ? plan.entries : 0;
+    out->windows = 0;
+    out->segments = 0;
+    out->magic = kLayoutMagic3;
+    return BHTSNE_OK;
+}
+
+static int check_layout3_step(const bhtsne_layout *layout, const float *Y, float theta, float exaggeration,
+                              void *workspace, size_t workspace_bytes)
+{
+    int rc = check_layout(layout, 4, 3);
+    if (rc != BHTSNE_OK) return rc;
+    // no sliced copy (no tile locality, or rows too long to sort): use the plain 3-D calls
+    if (layout->tiles == 0 || layout->windows != 0) return BHTSNE_EINVAL;
+    if (!Y) return BHTSNE_EINVAL;
+    if (!finite_f(theta) || theta < 0.0f) return BHTSNE_EINVAL;
+    if (!finite_f(exaggeration) || !(exaggeration > 0.0f)) return BHTSNE_EINVAL;
+    return check_ws_3d(layout->n, layout->nnz, workspace, workspace_bytes);
+}
+
+int bhtsne_gradient_layout_3d(const float *Y, const bhtsne_layout *layout, float theta, float exaggeration,
+                              float *grad, double *Z, void *workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    int rc = check_layout3_step(layout, Y, theta, exaggeration, workspace, workspace_bytes);
+    if (rc != BHTSNE_OK) return rc;
+    if (!grad) return BHTSNE_EINVAL;
+    StepArgs a{exaggeration, 0.0f, 0.0f, 0.0f, 0};
+    return run_layout3(const_cast<float *>(Y), layout, theta, a, nullptr, nullptr, grad, Z, workspace, stream);
+}
+
+int bhtsne_step_layout_3d(float *Y, const bhtsne_layout *layout, float theta, float exaggeration,
+                          float learning_rate, float momentum, float min_gain, float *update, float *gains,
+                          float *grad, double *Z, void *workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    int rc = check_layout3_step(layout, Y, theta, exaggeration, workspace, workspace_bytes);
+    if (rc != BHTSNE_OK) return rc;
+    if (!update || !gains) return BHTSNE_EINVAL;
+    rc = check_step_args(theta, exaggeration, learning_rate, momentum, min_gain);
+    if (rc != BHTSNE_OK) return rc;
+    StepArgs a{exaggeration, learning_rate, momentum, min_gain, 1};
+    return run_layout3(Y, layout, theta, a, update, gains, grad, Z, workspace, stream);
 }
 
 size_t bhtsne_layout_size(int64_t n, int64_t nnz)
@@ -756,8 +884,8 @@ int bhtsne_layout_build_ordered(const bhtsne_csr *P, const float *Y, int order, 
     const Layout L = make_layout(P->n, P->nnz);
     const LayoutView lv = layout_view(layout_mem, P->n, P->nnz);
     TilePlan plan;
-    const int built =
-        launch_layout_build(P->row_ptr, P->col, P->val, P->n, P->nnz, Y, order, lv, &plan, workspace, L, stream);
+    const int built = launch_layout_build<float, 2>(P->row_ptr, P->col, P->val, P->n, P->nnz, Y, order, lv, &plan,
+                                                    workspace, L, stream);
     if (built == 1) return BHTSNE_EINPUT;
     if (built != 0) return BHTSNE_EDEVICE;
     Header h;
@@ -799,8 +927,8 @@ int bhtsne_layout_build_f64(const bhtsne_csr_f64 *P, const double *Y, void *layo
     const Layout L = make_layout(P->n, P->nnz, 8);
     const LayoutView lv = layout_view(layout_mem, P->n, P->nnz, 8);
     TilePlan plan;
-    const int built = launch_layout_build(P->row_ptr, P->col, P->val, P->n, P->nnz, Y, kOrderAuto, lv, &plan,
-                                          workspace, L, stream);
+    const int built = launch_layout_build<double, 2>(P->row_ptr, P->col, P->val, P->n, P->nnz, Y, kOrderAuto, lv,
+                                                     &plan, workspace, L, stream);
     if (built == 1) return BHTSNE_EINPUT;
     if (built != 0) return BHTSNE_EDEVICE;
     Header h;

@@ -57,9 +57,15 @@ constexpr int64_t kYPad = 16384 + 2;                   // padding points after t
 constexpr int kTileRows = 1024;
 constexpr int kTileSeg = 16384; // 128 KB of Y in LDS
 constexpr int kTileMaxSeg = 16;
-// tiles per row block for values of `vbytes` bytes: windows of fp64 points
-// are half as wide, so twice as many cover the same column span
-constexpr int max_tiles_per_block(int vbytes) { return kTileMaxSeg * (vbytes / 4); }
+// Column windows of a sliced copy (points of Y held in LDS) and the tiles a
+// row block may span: 16384 fp32 2-D points (128 KB), 8192 fp64 2-D points
+// (128 KB) or 8192 3-D points (96 KB); the narrower windows take twice as many
+// tiles, so every form covers the same column span.
+constexpr int window_points_of(int vbytes, int dim) { return vbytes == 4 && dim == 2 ? kTileSeg : kTileSeg / 2; }
+constexpr int max_tiles_per_block(int vbytes, int dim = 2)
+{
+    return kTileMaxSeg * (kTileSeg / window_points_of(vbytes, dim));
+}
 constexpr int kItemMaxTiles = 128; // tiles of one segment handled by one block
 // sliced copy of a tile: 64 rows per slice (one per lane), chunks of 4 entries per lane
 constexpr int kSellSlice = 64;
@@ -155,12 +161,11 @@ inline Layout make_layout(int64_t n, int64_t nnz, int fbytes = 4, int dim = 2)
     // + 8 bytes: the 2-D walk loads 32 bytes at a record's offset
     L.nodes = take((dim == 3 ? kNodeBytes3 : (fbytes == 8 ? kNodeBytes64 : kNodeBytes)) * size_t(2 * n) + 8);
     L.frep = take(size_t(dim) * size_t(fbytes) * size_t(n));
-    L.fattr = take(2 * size_t(fbytes) * size_t(n));
+    L.fattr = take(size_t(dim) * size_t(fbytes) * size_t(n));
     // partial attractive sums, one per (tile, sorted row slot): up to
-    // kTileMaxSeg tiles of kTileRows rows per row block
-    L.partial = dim == 3 ? take(0)
-                         : take(2 * size_t(fbytes) * size_t((n + kTileRows - 1) / kTileRows) * kTileRows *
-                                size_t(max_tiles_per_block(fbytes)));
+    // max_tiles_per_block tiles of kTileRows rows per row block
+    L.partial = take(size_t(dim) * size_t(fbytes) * size_t((n + kTileRows - 1) / kTileRows) * kTileRows *
+                     size_t(max_tiles_per_block(fbytes, dim)));
     L.zpart = take(8 * size_t(L.rep_blocks));
     const int64_t zb = (n + kZEvalPoints - 1) / kZEvalPoints;
     L.eval_part = take(8 * size_t(zb > kEvalMaxBlocks ? zb : kEvalMaxBlocks));

@@ -395,9 +395,9 @@ __global__ __launch_bounds__(256) void layout_sort_rows_kernel(const int64_t *__
 }
 
 // ------------------------------------------------------------------ tiled copy
-// Column windows of the sliced copy: 128 KB of Y in LDS, 16384 fp32 points or
-// 8192 fp64 points.
-template <typename T> constexpr int window_points() { return sizeof(T) == 4 ? kTileSeg : kTileSeg / 2; }
+// Column windows of the sliced copy: 16384 fp32 or 8192 fp64 2-D points
+// (128 KB of LDS), or 8192 3-D points (96 KB).
+template <typename T, int D> constexpr int window_points() { return window_points_of(sizeof(T), D); }
 
 // Rows longer than the in-LDS row sort stay unsorted; the sliced copy finds a
 // row's runs by binary search, so one such row rules it out.
@@ -538,7 +538,7 @@ __global__ __launch_bounds__(256) void fill_zero_kernel(uint16_t *__restrict__ t
 // (sorted position % 64) of unit (tile, sorted position / 64); its e-th entry
 // in the segment goes to chunk e / 4, element e % 4 of that lane.  Everything
 // else was zeroed (padding carries p = 0).
-template <typename T>
+template <typename T, int D>
 __global__ __launch_bounds__(256) void sell_copy_kernel(const int64_t *__restrict__ row_ptr,
                                                         const int32_t *__restrict__ col, const T *__restrict__ val,
                                                         int64_t n, const int32_t *__restrict__ seg_lo,
@@ -549,8 +549,8 @@ __global__ __launch_bounds__(256) void sell_copy_kernel(const int64_t *__restric
                                                         const int32_t *__restrict__ unit_chunk0, int64_t max_entries,
                                                         uint16_t *__restrict__ tcol, T *__restrict__ tval)
 {
-    constexpr int kSeg = window_points<T>();
-    constexpr int kMaxSeg = max_tiles_per_block(sizeof(T));
+    constexpr int kSeg = window_points<T, D>();
+    constexpr int kMaxSeg = max_tiles_per_block(sizeof(T), D);
     const int lane = lane_id();
     for (int64_t r = (int64_t(blockIdx.x) * blockDim.x + threadIdx.x) / kWave; r < n;
          r += int64_t(gridDim.x) * (blockDim.x / kWave)) {
@@ -773,6 +773,32 @@ __device__ inline void attract_add(double2 yi, double2 yj, double p, double &fx,
     fy = fma(pw, dy, fy);
 }
 
+__device__ inline void attract_add(float3 yi, float3 yj, float p, float &fx, float &fy, float &fz)
+{
+    const float dx = yi.x - yj.x, dy = yi.y - yj.y, dz = yi.z - yj.z;
+    const float pw = p * __builtin_amdgcn_rcpf(1.0f + fmaf(dx, dx, fmaf(dy, dy, dz * dz)));
+    fx = fmaf(pw, dx, fx);
+    fy = fmaf(pw, dy, fy);
+    fz = fmaf(pw, dz, fz);
+}
+
+// the same on whole points: f += p_ij w_ij (y_i - y_j)
+__device__ inline void attract_acc(float2 yi, float2 yj, float p, float2 &f) { attract_add(yi, yj, p, f.x, f.y); }
+__device__ inline void attract_acc(double2 yi, double2 yj, double p, double2 &f) { attract_add(yi, yj, p, f.x, f.y); }
+__device__ inline void attract_acc(float3 yi, float3 yj, float p, float3 &f)
+{
+    attract_add(yi, yj, p, f.x, f.y, f.z);
+}
+// f += c where `live`, component by component
+template <typename P> __device__ inline void point_add(P &f, const P &c, bool live = true)
+{
+    using T = decltype(c.x);
+    f.x += live ? c.x : T(0);
+    f.y += live ? c.y : T(0);
+    if constexpr (sizeof(P) == 3 * sizeof(T)) f.z += live ? c.z : T(0);
+}
+static_assert(sizeof(float3) == 12, "3-D points are packed");
+
 // kAttBlock threads, kAttSeg points of Y per LDS segment, kAttRG rows per lane group.
 // Rows of the layout are sorted, padded to whole vectors and 16-byte aligned;
 // lane `sub` of a row's group holds the vectors sub, sub + 16, sub + 32, ...
@@ -949,21 +975,26 @@ template <typename T> struct Vec4Of;
 template <> struct Vec4Of<float> { using type = v4f; };
 template <> struct Vec4Of<double> { using type = v4d; };
 
-// T = float: fp32 values and centres, 16384-point windows; T = double: the
-// fp64 variant, 8192-point windows.  Either way a window is 128 KB of LDS.
-template <typename T>
+// (T, D) = (float, 2): fp32 values and centres, 16384-point windows; (double,
+// 2): the fp64 variant, 8192-point windows (either is 128 KB of LDS); (float,
+// 3): 3-D embeddings, 8192-point windows (96 KB).
+template <typename T, int D>
 __global__ __launch_bounds__(kTileBlock) void attract_sell_kernel(
     const int2 *__restrict__ item_tiles, const int4 *__restrict__ item_units, const int4 *__restrict__ wave_units,
     const int32_t *__restrict__ tile_blk, const int32_t *__restrict__ tile_seg,
     const int32_t *__restrict__ unit_chunks, const int32_t *__restrict__ unit_tj, const uint16_t *__restrict__ tperm,
-    const uint16_t *__restrict__ tcol, const T *__restrict__ tval, const vec2_t<T> *__restrict__ ylay,
-    int32_t nitems, Header *__restrict__ hdr, vec2_t<T> *__restrict__ partial)
+    const uint16_t *__restrict__ tcol, const T *__restrict__ tval, const point_t<D, T> *__restrict__ ylay,
+    int32_t nitems, Header *__restrict__ hdr, point_t<D, T> *__restrict__ partial)
 {
-    using V = vec2_t<T>;
+    using V = point_t<D, T>;
     using V4 = typename Vec4Of<T>::type;
-    constexpr int kSeg = window_points<T>();
-    static_assert(kSeg * sizeof(V) == kTileSeg * sizeof(float2), "a window is 128 KB of LDS");
-    __shared__ v4f sy4[kTileSeg / 2];
+    constexpr int kSeg = window_points<T, D>();
+    // a window of Y in 16-byte vectors, staged by every thread in equal shares
+    constexpr int kSegVec = int(kSeg * sizeof(V) / 16);
+    static_assert(kSegVec * 16 == int(kSeg * sizeof(V)) && kSegVec % kTileBlock == 0 &&
+                      kSegVec * 16 <= kTileSeg * int(sizeof(float2)),
+                  "a window is whole 16-byte vectors per thread, at most 128 KB of LDS");
+    __shared__ v4f sy4[kSegVec];
     __shared__ int32_t s_row0[kItemMaxTiles];
     // per stored unit of the item: chunks (a run holds at most kTileSeg entries)
     // and (tile - t0) * 16 + slice, both below 2^16
@@ -1000,11 +1031,11 @@ __global__ __launch_bounds__(kTileBlock) void attract_sell_kernel(
         };
         // the segment of Y (8 independent 16-byte loads per thread) and the first
         // chunks are in flight together
-        static_assert(kYPad >= kTileSeg + 2 && kYPad >= kTileRows, "padding must cover one segment and one block");
-        constexpr int kStage = kTileSeg / 2 / kTileBlock;
+        static_assert(kYPad >= kSeg + 2 && kYPad >= kTileRows, "padding must cover one segment and one block");
+        constexpr int kStage = kSegVec / kTileBlock;
         v4f stage[kStage];
         {
-            const v4f *src = reinterpret_cast<const v4f *>(ylay) + int64_t(sg) * (kTileSeg / 2) + threadIdx.x;
+            const v4f *src = reinterpret_cast<const v4f *>(ylay) + int64_t(sg) * kSegVec + threadIdx.x;
 #pragma unroll
             for (int q = 0; q < kStage; ++q) stage[q] = src[q * kTileBlock];
         }
@@ -1032,7 +1063,7 @@ __global__ __launch_bounds__(kTileBlock) void attract_sell_kernel(
         auto unit_row0 = [&](int32_t u) { return uni(s_row0[uni(s_tj[u - iu.x]) / kSlicesPerTile]); };
 
         // units without entries in their tile's segment: their rows' partials are 0
-        for (int32_t u = iu.y + w; u < iu.z; u += kSellWaves) partial[unit_at(u)] = make_vec2(T(0), T(0));
+        for (int32_t u = iu.y + w; u < iu.z; u += kSellWaves) partial[unit_at(u)] = V{};
         if (wu.x < wu.y) { // this wave has units
         const int32_t ulast = wu.y - 1;
         int32_t u = wu.x;             // unit being summed (wave-uniform)
@@ -1048,22 +1079,24 @@ __global__ __launch_bounds__(kTileBlock) void attract_sell_kernel(
         // otherwise the loop head, where this entry path meets the back edge,
         // would wait for them on every trip.  The empty statement only uses the
         // registers, which makes the compiler complete their loads before it.
-        asm volatile("" ::"v"(yA.x), "v"(yA.y), "v"(yB.x), "v"(yB.y));
-        T fx = T(0), fy = T(0);
+        if constexpr (D == 3)
+            asm volatile("" ::"v"(yA.x), "v"(yA.y), "v"(yA.z), "v"(yB.x), "v"(yB.y), "v"(yB.z));
+        else
+            asm volatile("" ::"v"(yA.x), "v"(yA.y), "v"(yB.x), "v"(yB.y));
+        V f{};
 
         // one wave step: sum chunk g from ring slot x, refill the slot with chunk
         // g + kSellRing, and close the unit when g was its last chunk
         auto step = [&](int x, int32_t g) {
             const bool live = g < G; // wave-uniform; dead steps only occur after the last chunk
-            T cx = T(0), cy = T(0);
+            V cs{};
 #pragma unroll
-            for (int v = 0; v < 4; ++v) attract_add(yA, sy[c[x][v] & (kSeg - 1)], T(p[x][v]), cx, cy);
-            fx += live ? cx : T(0);
-            fy += live ? cy : T(0);
+            for (int v = 0; v < 4; ++v) attract_acc(yA, sy[c[x][v] & (kSeg - 1)], T(p[x][v]), cs);
+            point_add(f, cs, live);
             issue(x, g + kSellRing);
             if (live && g + 1 == uend) {
-                partial[unit_at(u)] = make_vec2(fx, fy);
-                fx = fy = T(0);
+                partial[unit_at(u)] = f;
+                f = V{};
                 ++u;
                 if (u <= ulast) uend += uni(s_K[u - iu.x]);
                 rowA = rowB;
@@ -1087,25 +1120,23 @@ __global__ __launch_bounds__(kTileBlock) void attract_sell_kernel(
 // row's original index (perm), so that the update reads it in the caller's
 // order without a gather.  Consecutive rows read one tile's 8 KB of partials
 // at a time.
-template <typename T>
-__global__ __launch_bounds__(256) void attract_rows_kernel(const vec2_t<T> *__restrict__ partial,
+template <typename T, int D>
+__global__ __launch_bounds__(256) void attract_rows_kernel(const point_t<D, T> *__restrict__ partial,
                                                            const int32_t *__restrict__ blk_nseg,
                                                            const int32_t *__restrict__ blk_tiles,
                                                            const uint16_t *__restrict__ tpos,
                                                            const uint32_t *__restrict__ perm, int64_t n,
-                                                           vec2_t<T> *__restrict__ fattr)
+                                                           point_t<D, T> *__restrict__ fattr)
 {
     const int64_t r = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
     if (r >= n) return;
     const int64_t b = r / kTileRows;
     const int rr = int(r % kTileRows);
     const int ns = blk_nseg[b];
-    vec2_t<T> fa = make_vec2(T(0), T(0));
+    point_t<D, T> fa{};
     for (int k = 0; k < ns; ++k) {
-        const int64_t t = blk_tiles[b * max_tiles_per_block(sizeof(T)) + k];
-        const vec2_t<T> v = partial[t * kTileRows + tpos[t * kTileRows + rr]];
-        fa.x += v.x;
-        fa.y += v.y;
+        const int64_t t = blk_tiles[b * max_tiles_per_block(sizeof(T), D) + k];
+        point_add(fa, partial[t * kTileRows + tpos[t * kTileRows + rr]]);
     }
     fattr[perm[r]] = fa;
 }
@@ -1149,8 +1180,42 @@ __global__ __launch_bounds__(256) void update_kernel(const vec2_t<T> *__restrict
     }
 }
 
+// 3-D embeddings: the same gradient and update on three components, with
+// F_attr in the caller's order.
+__global__ __launch_bounds__(256) void update3_kernel(const float3 *__restrict__ fattr,
+                                                      const float3 *__restrict__ frep, const Header *__restrict__ hdr,
+                                                      int64_t n, StepArgsT<float> a, float3 *__restrict__ Y,
+                                                      float3 *__restrict__ upd, float3 *__restrict__ gains,
+                                                      float3 *__restrict__ grad)
+{
+    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const float inv_z = float(1.0 / hdr->Z);
+    const float3 fa = fattr[i], fr = frep[i];
+    float g[3];
+#pragma unroll
+    for (int d = 0; d < 3; ++d) g[d] = 4.0f * (a.alpha * coord(fa, d) - coord(fr, d) * inv_z);
+    if (grad) grad[i] = make_float3(g[0], g[1], g[2]);
+    if (a.update) {
+        const float3 u0 = upd[i], g0 = gains[i], y0 = Y[i];
+        float u[3], gn[3], y[3];
+#pragma unroll
+        for (int d = 0; d < 3; ++d) {
+            const float ud = coord(u0, d);
+            float gd = (ud * g[d] < 0.0f) ? coord(g0, d) + 0.2f : coord(g0, d) * 0.8f;
+            gd = gd > a.min_gain ? gd : a.min_gain;
+            u[d] = a.momentum * ud - a.learning_rate * gd * g[d];
+            gn[d] = gd;
+            y[d] = coord(y0, d) + u[d];
+        }
+        Y[i] = make_float3(y[0], y[1], y[2]);
+        upd[i] = make_float3(u[0], u[1], u[2]);
+        gains[i] = make_float3(gn[0], gn[1], gn[2]);
+    }
+}
+
 // ------------------------------------------------------------------ launchers
-LayoutView layout_view(void *mem, int64_t n, int64_t nnz, int vbytes)
+LayoutView layout_view(void *mem, int64_t n, int64_t nnz, int vbytes, int dim)
 {
     LayoutView v;
     size_t off = 0;
@@ -1165,7 +1230,7 @@ LayoutView layout_view(void *mem, int64_t n, int64_t nnz, int vbytes)
     size_t o_col = take(4 * cap), o_val = take(size_t(vbytes) * cap);
     // tiled copy: at most max_tiles_per_block tiles per row block, sliced
     const int64_t blocks = (n + kTileRows - 1) / kTileRows;
-    const int max_seg = max_tiles_per_block(vbytes);
+    const int max_seg = max_tiles_per_block(vbytes, dim);
     v.max_tiles = blocks * max_seg;
     // the sliced copy pads every run to its slice's longest run, rounded up to
     // whole chunks; it is built only when that fits in a quarter of nnz plus
@@ -1225,11 +1290,11 @@ LayoutView layout_view(void *mem, int64_t n, int64_t nnz, int vbytes)
 
 // The tiled copy of a built (sorted, padded) layout; plan->tiled stays false when
 // some row block spans more than max_tiles_per_block segments.
-template <typename T>
+template <typename T, int D>
 static int build_tiles(const LayoutView &lv, int64_t n, TilePlan *plan, void *ws, const Layout &L, hipStream_t st)
 {
-    constexpr int kSeg = window_points<T>();
-    constexpr int kMaxSeg = max_tiles_per_block(sizeof(T));
+    constexpr int kSeg = window_points<T, D>();
+    constexpr int kMaxSeg = max_tiles_per_block(sizeof(T), D);
     T *tval = sizeof(T) == 4 ? reinterpret_cast<T *>(lv.tval) : reinterpret_cast<T *>(lv.tval64);
     const T *val = sizeof(T) == 4 ? reinterpret_cast<const T *>(lv.val) : reinterpret_cast<const T *>(lv.val64);
     *plan = TilePlan{};
@@ -1377,7 +1442,7 @@ static int build_tiles(const LayoutView &lv, int64_t n, TilePlan *plan, void *ws
     const int64_t zero = entries > kSellChunk ? entries : kSellChunk;
     fill_zero_kernel<T><<<unsigned(std::min<int64_t>((zero + 255) / 256, 65535 * 4)), 256, 0, st>>>(lv.tcol, tval,
                                                                                                     zero);
-    sell_copy_kernel<T><<<unsigned(n < 65535 * 4 ? (n + 3) / 4 : 65535 * 4), 256, 0, st>>>(
+    sell_copy_kernel<T, D><<<unsigned(n < 65535 * 4 ? (n + 3) / 4 : 65535 * 4), 256, 0, st>>>(
         lv.row_ptr, lv.col, val, n, lv.blk_seg_lo, lv.blk_nseg, lv.blk_tiles, lv.tpos, lv.unit_of, lv.unit_chunk0,
         lv.max_entries, lv.tcol, tval);
     // the tables above must stay alive until the copies have been read
@@ -1462,7 +1527,7 @@ static int bfs_levels(const int64_t *row_ptr, const int32_t *col, int64_t n, int
 
 // Renumbers the points by the keys of `order` and writes the relabelled rows:
 // perm, rank, row pointers, columns and values, each row sorted.
-template <typename V>
+template <typename V, int D>
 static int relabel(const int64_t *row_ptr, const int32_t *col, const V *val, int64_t n, int64_t nnz, const V *Y,
                    int order, const LayoutView &lv, void *ws, const Layout &L, hipStream_t st)
 {
@@ -1477,8 +1542,12 @@ static int relabel(const int64_t *row_ptr, const int32_t *col, const V *val, int
     } else {
         // keys: component, then Morton order of Y when given
         if (Y) {
-            launch_bbox(Y, n, ws, L, st);
-            launch_morton(Y, n, nullptr, ws, L, st);
+            if constexpr (D == 3) {
+                launch_bbox_morton3(Y, n, nullptr, ws, L, st);
+            } else {
+                launch_bbox(Y, n, ws, L, st);
+                launch_morton(Y, n, nullptr, ws, L, st);
+            }
         } else {
             sort_reset_kernel<<<1, 256, 0, st>>>(hdr, at<uint32_t>(ws, L.hist));
         }
@@ -1487,7 +1556,12 @@ static int relabel(const int64_t *row_ptr, const int32_t *col, const V *val, int
     sort_reset_kernel<<<1, 256, 0, st>>>(hdr, at<uint32_t>(ws, L.hist));
     keys_hist_kernel<<<unsigned(L.sort_tiles), kSortBlock, 0, st>>>(keys, n, at<uint32_t>(ws, L.hist),
                                                                     at<uint32_t>(ws, L.status), L.sort_tiles);
-    launch_sort(n, Y ? Y : reinterpret_cast<const V *>(at<char>(ws, L.ycopy)), ws, L, st);
+    // (the sorted copy of the points this also makes is not used)
+    const V *ysrc = Y ? Y : reinterpret_cast<const V *>(at<char>(ws, L.ycopy));
+    if constexpr (D == 3)
+        launch_sort_points(n, reinterpret_cast<const float3 *>(ysrc), ws, L, st);
+    else
+        launch_sort(n, ysrc, ws, L, st);
     // new order -> rank, row lengths, row pointers, relabelled rows
     const uint32_t *perm_ws = at<uint32_t>(ws, L.idx0);
     if (hipMemcpyAsync(lv.perm, perm_ws, 4 * size_t(n), hipMemcpyDeviceToDevice, st) != hipSuccess) return -1;
@@ -1505,7 +1579,7 @@ static int relabel(const int64_t *row_ptr, const int32_t *col, const V *val, int
     return hipGetLastError() != hipSuccess ? -1 : 0;
 }
 
-template <typename V>
+template <typename V, int D>
 int launch_layout_build(const int64_t *row_ptr, const int32_t *col, const V *val, int64_t n, int64_t nnz,
                         const V *Y, int order, const LayoutView &lv, TilePlan *plan, void *ws, const Layout &L,
                         hipStream_t st)
@@ -1541,10 +1615,10 @@ int launch_layout_build(const int64_t *row_ptr, const int32_t *col, const V *val
         if (rc < 0) return -1;
         if (rc == 1) chosen = kOrderBfs;
     }
-    if (relabel(row_ptr, col, val, n, nnz, Y, chosen, lv, ws, L, st) != 0) return -1;
+    if (relabel<V, D>(row_ptr, col, val, n, nnz, Y, chosen, lv, ws, L, st) != 0) return -1;
     *plan = TilePlan{};
     {
-        int rc = build_tiles<V>(lv, n, plan, ws, L, st);
+        int rc = build_tiles<V, D>(lv, n, plan, ws, L, st);
         if (rc != 0) return rc;
         if (plan->tiled) {
             plan->order = chosen;
@@ -1557,27 +1631,32 @@ int launch_layout_build(const int64_t *row_ptr, const int32_t *col, const V *val
             rc = bfs_levels(row_ptr, col, n, nnz, parent, dist, ws, L, st);
             if (rc < 0) return -1;
             if (rc == 1) {
-                if (relabel(row_ptr, col, val, n, nnz, Y, kOrderBfs, lv, ws, L, st) != 0) return -1;
-                rc = build_tiles<V>(lv, n, plan, ws, L, st);
+                if (relabel<V, D>(row_ptr, col, val, n, nnz, Y, kOrderBfs, lv, ws, L, st) != 0) return -1;
+                rc = build_tiles<V, D>(lv, n, plan, ws, L, st);
                 if (rc != 0) return rc;
                 if (plan->tiled) {
                     plan->order = kOrderBfs;
                     return 0;
                 }
-                if (relabel(row_ptr, col, val, n, nnz, Y, kOrderMorton, lv, ws, L, st) != 0) return -1;
+                if (relabel<V, D>(row_ptr, col, val, n, nnz, Y, kOrderMorton, lv, ws, L, st) != 0) return -1;
             }
             *plan = TilePlan{};
         }
     }
     plan->order = chosen;
+    // 3-D layouts have the sliced copy only
+    if constexpr (D == 3) return 0;
     return build_windows(lv, n, plan, ws, L, st);
 }
-template int launch_layout_build<float>(const int64_t *, const int32_t *, const float *, int64_t, int64_t,
-                                        const float *, int, const LayoutView &, TilePlan *, void *, const Layout &,
-                                        hipStream_t);
-template int launch_layout_build<double>(const int64_t *, const int32_t *, const double *, int64_t, int64_t,
-                                         const double *, int, const LayoutView &, TilePlan *, void *,
-                                         const Layout &, hipStream_t);
+template int launch_layout_build<float, 2>(const int64_t *, const int32_t *, const float *, int64_t, int64_t,
+                                           const float *, int, const LayoutView &, TilePlan *, void *,
+                                           const Layout &, hipStream_t);
+template int launch_layout_build<double, 2>(const int64_t *, const int32_t *, const double *, int64_t, int64_t,
+                                            const double *, int, const LayoutView &, TilePlan *, void *,
+                                            const Layout &, hipStream_t);
+template int launch_layout_build<float, 3>(const int64_t *, const int32_t *, const float *, int64_t, int64_t,
+                                           const float *, int, const LayoutView &, TilePlan *, void *,
+                                           const Layout &, hipStream_t);
 
 // One launch per column window, after F_attr is cleared (layout order).
 template <typename T>
@@ -1620,11 +1699,11 @@ void launch_attract_layout(const LayoutView &lv, int64_t n, int64_t nnz, int til
     if (tiles > 0) {
         const T *tval = sizeof(T) == 4 ? reinterpret_cast<const T *>(lv.tval) : reinterpret_cast<const T *>(lv.tval64);
         const unsigned grid = unsigned(blocks < items ? blocks : items);
-        attract_sell_kernel<T><<<grid, kTileBlock, 0, st>>>(lv.item_tiles, lv.item_units, lv.wave_units, lv.tile_blk,
+        attract_sell_kernel<T, 2><<<grid, kTileBlock, 0, st>>>(lv.item_tiles, lv.item_units, lv.wave_units, lv.tile_blk,
                                                             lv.tile_seg, lv.unit_chunks, lv.unit_tj, lv.tperm, lv.tcol,
                                                             tval, at<V>(ws, L.ycopy), items, at<Header>(ws, L.header),
                                                             at<V>(ws, L.partial));
-        attract_rows_kernel<T><<<unsigned((n + 255) / 256), 256, 0, st>>>(at<V>(ws, L.partial), lv.blk_nseg,
+        attract_rows_kernel<T, 2><<<unsigned((n + 255) / 256), 256, 0, st>>>(at<V>(ws, L.partial), lv.blk_nseg,
                                                                          lv.blk_tiles, lv.tpos, lv.perm, n,
                                                                          at<V>(ws, L.fattr));
         return;
@@ -1650,5 +1729,25 @@ template void launch_update<float>(const LayoutView &, int64_t, bool, const Step
                                    float *, float *, void *, const Layout &, hipStream_t);
 template void launch_update<double>(const LayoutView &, int64_t, bool, const StepArgsT<double> &, double *, double *,
                                     double *, double *, void *, const Layout &, hipStream_t);
+
+void launch_attract_layout3(const LayoutView &lv, int64_t n, int tiles, int items, int blocks, void *ws,
+                            const Layout &L, hipStream_t st)
+{
+    if (tiles <= 0 || items <= 0) return;
+    const unsigned grid = unsigned(blocks < items ? blocks : items);
+    attract_sell_kernel<float, 3><<<grid, kTileBlock, 0, st>>>(
+        lv.item_tiles, lv.item_units, lv.wave_units, lv.tile_blk, lv.tile_seg, lv.unit_chunks, lv.unit_tj, lv.tperm,
+        lv.tcol, lv.tval, at<float3>(ws, L.ycopy), items, at<Header>(ws, L.header), at<float3>(ws, L.partial));
+    attract_rows_kernel<float, 3><<<unsigned((n + 255) / 256), 256, 0, st>>>(
+        at<float3>(ws, L.partial), lv.blk_nseg, lv.blk_tiles, lv.tpos, lv.perm, n, at<float3>(ws, L.fattr));
+}
+
+void launch_update3(int64_t n, const StepArgsT<float> &a, float *Y, float *upd, float *gains, float *grad, void *ws,
+                    const Layout &L, hipStream_t st)
+{
+    update3_kernel<<<unsigned((n + 255) / 256), 256, 0, st>>>(
+        at<float3>(ws, L.fattr), at<float3>(ws, L.frep), at<Header>(ws, L.header), n, a, reinterpret_cast<float3 *>(Y),
+        reinterpret_cast<float3 *>(upd), reinterpret_cast<float3 *>(gains), reinterpret_cast<float3 *>(grad));
+}
 
 } // namespace bht

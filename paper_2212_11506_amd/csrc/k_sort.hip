@@ -365,8 +365,8 @@ __device__ inline uint64_t spread3_by_bytes(const uint32_t *__restrict__ tab, ui
 
 __global__ __launch_bounds__(kSortBlock) void morton3_kernel(
     const float3 *__restrict__ Y, int64_t n, const Header *__restrict__ hdr, uint64_t *__restrict__ codes,
-    float3 *__restrict__ ycopy, uint32_t *__restrict__ hist, uint32_t *__restrict__ levelmask,
-    uint32_t *__restrict__ status, int64_t tiles)
+    float3 *__restrict__ ycopy, const uint32_t *__restrict__ rank, uint32_t *__restrict__ hist,
+    uint32_t *__restrict__ levelmask, uint32_t *__restrict__ status, int64_t tiles)
 {
     __shared__ uint32_t sh[kSortPasses * kRadix];
     __shared__ uint32_t s_spread[256];
@@ -385,7 +385,8 @@ __global__ __launch_bounds__(kSortBlock) void morton3_kernel(
         const int64_t i = base + r * kSortBlock + threadIdx.x;
         if (i < n) {
             const float3 y = Y[i];
-            ycopy[i] = y;
+            const uint32_t o = rank ? rank[i] : uint32_t(i); // a layout's order, or the caller's
+            ycopy[o < uint32_t(n) ? o : uint32_t(i)] = y;
             const uint64_t code = spread3_by_bytes(s_spread, quantise21(y.x, yr0, sc)) |
                                   (spread3_by_bytes(s_spread, quantise21(y.y, yr1, sc)) << 1) |
                                   (spread3_by_bytes(s_spread, quantise21(y.z, yr2, sc)) << 2);
@@ -594,7 +595,7 @@ template <typename T> void launch_bbox(const T *Y, int64_t n, void *ws, const La
 template void launch_bbox<float>(const float *, int64_t, void *, const Layout &, hipStream_t);
 template void launch_bbox<double>(const double *, int64_t, void *, const Layout &, hipStream_t);
 
-void launch_bbox_morton3(const float *Y, int64_t n, void *ws, const Layout &L, hipStream_t st)
+void launch_bbox_morton3(const float *Y, int64_t n, const uint32_t *rank, void *ws, const Layout &L, hipStream_t st)
 {
     int blocks = int((n + 255) / 256);
     if (blocks > kBBoxBlocks) blocks = kBBoxBlocks;
@@ -603,7 +604,7 @@ void launch_bbox_morton3(const float *Y, int64_t n, void *ws, const Layout &L, h
     bbox3_final_kernel<<<1, 256, 0, st>>>(at<float>(ws, L.bbox_part), blocks, at<Header>(ws, L.header),
                                           at<uint32_t>(ws, L.hist));
     morton3_kernel<<<unsigned(L.sort_tiles), kSortBlock, 0, st>>>(
-        y3, n, at<Header>(ws, L.header), at<uint64_t>(ws, L.codes0), at<float3>(ws, L.ycopy),
+        y3, n, at<Header>(ws, L.header), at<uint64_t>(ws, L.codes0), at<float3>(ws, L.ycopy), rank,
         at<uint32_t>(ws, L.hist), at<uint32_t>(ws, L.levelmask), at<uint32_t>(ws, L.status), L.sort_tiles);
 }
 

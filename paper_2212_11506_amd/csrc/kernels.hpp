@@ -84,8 +84,9 @@ template <typename T> void launch_bbox(const T *Y, int64_t n, void *ws, const La
 template <typename T>
 void launch_morton(const T *Y, int64_t n, const uint32_t *rank, void *ws, const Layout &L, hipStream_t st);
 // 3-D embeddings (Y n x 3 fp32): box, cube, 63-bit codes, digit histograms and
-// the private copy of Y in the caller's order
-void launch_bbox_morton3(const float *Y, int64_t n, void *ws, const Layout &L, hipStream_t st);
+// the private copy of Y in the caller's order, or in rank's (nullable) order
+void launch_bbox_morton3(const float *Y, int64_t n, const uint32_t *rank, void *ws, const Layout &L,
+                         hipStream_t st);
 // ysrc: Y in the original order, gathered into Morton order by the last pass
 template <typename T> void launch_sort(int64_t n, const T *ysrc, void *ws, const Layout &L, hipStream_t st);
 // the same with the points' type given (float3: 3-D embeddings)
@@ -114,13 +115,16 @@ template <int D, typename T>
 void launch_attract(const int64_t *row_ptr, const int32_t *col, const T *val, int64_t n, int64_t nnz,
                     const StepArgsT<T> &a, T *Y, T *upd, T *gains, T *grad, void *ws, const Layout &L, hipStream_t st);
 
-// vbytes: 4 (fp32 values) or 8 (the fp64 variant's layouts)
-LayoutView layout_view(void *mem, int64_t n, int64_t nnz, int vbytes = 4);
+// vbytes: 4 (fp32 values) or 8 (the fp64 variant's layouts); dim: 2, or 3
+// for 3-D embeddings (fp32)
+LayoutView layout_view(void *mem, int64_t n, int64_t nnz, int vbytes = 4, int dim = 2);
 // Builds the layout in the point order `order` (kOrder*; synchronises the
 // stream); fills *plan with the tile tables' sizes and the order taken.
 // Returns 0, 1 when P's row pointers are malformed (nothing else was read), or -1 on a HIP error.
 // V = double: fp64 values, the sliced copy over 8192-point windows (up to 32 per row block).
-template <typename V>
+// D = 3 (V = float, Y n x 3): the same over 8192-point windows of 3-D points;
+// no windowed segments (plan->windows stays 0).
+template <typename V, int D = 2>
 int launch_layout_build(const int64_t *row_ptr, const int32_t *col, const V *val, int64_t n, int64_t nnz,
                         const V *Y, int order, const LayoutView &lv, TilePlan *plan, void *ws, const Layout &L,
                         hipStream_t st);
@@ -137,6 +141,12 @@ void launch_attract_layout(const LayoutView &lv, int64_t n, int64_t nnz, int til
 template <typename T>
 void launch_update(const LayoutView &lv, int64_t n, bool layout_order, const StepArgsT<T> &a, T *Y, T *upd, T *gains,
                    T *grad, void *ws, const Layout &L, hipStream_t st);
+// 3-D layouts: the sliced tile kernel and the row sums (F_attr in the
+// caller's order), then the gradient and update from F_attr and F_rep
+void launch_attract_layout3(const LayoutView &lv, int64_t n, int tiles, int items, int blocks, void *ws,
+                            const Layout &L, hipStream_t st);
+void launch_update3(int64_t n, const StepArgsT<float> &a, float *Y, float *upd, float *gains, float *grad, void *ws,
+                    const Layout &L, hipStream_t st);
 
 // input similarities from neighbour lists: clear, the index work (own-row
 // order, pair sort, inbox offsets, union counts, row pointers with row_ptr[n]

@@ -293,3 +293,41 @@ def test_3d_workspace_size_and_argument_checks():
                                     None, C.c_void_p(FAKE), ws, None) == bh.BHTSNE_EINVAL
     assert lib.bhtsne_debug_sort_3d(None, n, None, None, None, None, C.c_void_p(FAKE), ws,
                                     None) == bh.BHTSNE_EINVAL
+
+
+def test_3d_layout_size_and_argument_checks():
+    from paper_2212_11506_amd._binding import _Layout
+    lib = bh.load_library()
+    assert lib.bhtsne_layout_size_3d(1, 0) == 0 and lib.bhtsne_layout_size_3d(1 << 24, 0) == 0
+    n, nnz = 100_000, 1_000_000
+    a2, a3 = lib.bhtsne_layout_size(n, nnz), lib.bhtsne_layout_size_3d(n, nnz)
+    # the same copies, with twice the tiles per row block (8192-point windows)
+    assert a2 < a3 < 2 * a2 and a3 % 256 == 0
+    P = _Csr(n, nnz, FAKE, FAKE, FAKE)
+    ws = lib.bhtsne_workspace_size_3d(n, nnz)
+    lay = _Layout()
+    f = C.c_void_p(FAKE)
+    assert lib.bhtsne_layout_build_3d(C.byref(P), None, f, a3, None, f, ws, None) == bh.BHTSNE_EINVAL
+    assert lib.bhtsne_layout_build_3d(C.byref(P), None, f, a3 - 1, C.byref(lay), f, ws, None) == bh.BHTSNE_EINVAL
+    assert lib.bhtsne_layout_build_3d(C.byref(P), None, f, a3, C.byref(lay), f, ws - 1,
+                                      None) == bh.BHTSNE_EWORKSPACE
+    assert lib.bhtsne_layout_build_3d(None, None, f, a3, C.byref(lay), f, ws, None) == bh.BHTSNE_EINVAL
+
+    def handle(magic, tiles):
+        return _Layout(n, nnz, FAKE, a3, tiles, 1 if tiles else 0, 4096 * tiles, 0, 0, 0, magic)
+
+    l3 = handle(0x62687473654c3033, 10)
+    for bad in (handle(0x62687473654c3031, 10), handle(0x62687473654c3634, 10), handle(0, 10),
+                handle(0x62687473654c3033, 0)):
+        # a 2-D, fp64 or unbuilt handle, or a 3-D one without tiles: refused on the host
+        assert lib.bhtsne_gradient_layout_3d(f, C.byref(bad), 0.5, 1.0, f, None, f, ws, None) == bh.BHTSNE_EINVAL
+        assert lib.bhtsne_step_layout_3d(f, C.byref(bad), 0.5, 1.0, 200.0, 0.5, 0.01, f, f, None, None, f, ws,
+                                         None) == bh.BHTSNE_EINVAL
+    # and the 2-D calls refuse a 3-D handle
+    assert lib.bhtsne_gradient_layout(f, C.byref(l3), 0.5, 1.0, f, None, f, 1 << 40, None) == bh.BHTSNE_EINVAL
+    assert lib.bhtsne_gradient_layout_3d(f, C.byref(l3), -1.0, 1.0, f, None, f, ws, None) == bh.BHTSNE_EINVAL
+    assert lib.bhtsne_gradient_layout_3d(f, C.byref(l3), 0.5, 1.0, None, None, f, ws, None) == bh.BHTSNE_EINVAL
+    assert lib.bhtsne_gradient_layout_3d(f, C.byref(l3), 0.5, 1.0, f, None, f, ws - 1,
+                                         None) == bh.BHTSNE_EWORKSPACE
+    assert lib.bhtsne_step_layout_3d(f, C.byref(l3), 0.5, 1.0, 200.0, 1.0, 0.01, f, f, None, None, f, ws,
+                                     None) == bh.BHTSNE_EINVAL

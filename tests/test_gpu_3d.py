@@ -303,6 +303,114 @@ def test_gradient3_full_size_sampled(cid, theta):
     assert stats["nodes"] == nodes_o
 
 
+# ---------------------------------------------------------------- locality layout
+LAYOUT_CASES = ["c0", "rand3", "rand2049", "dups", "identical", "line", "late"]
+
+
+def _layout_inputs(case):
+    if case == "c0":
+        inp = synth.make_inputs(0, dim=3)
+        return inp.Y, inp.row_ptr, inp.col, inp.val
+    y = _case(case)
+    return (y,) + tuple(_p_for(y))
+
+
+@pytest.mark.parametrize("case", LAYOUT_CASES)
+@pytest.mark.parametrize("theta", [0.0, 0.5])
+def test_gradient3_through_layout(case, theta):
+    """The 3-D gradient with P through the locality layout (sliced attraction
+    on the second stream): the oracle's bars, the plain path's Z bit for bit
+    (same tree, same walk) and its gradient to fp32 summation order."""
+    y, rp, col, val = _layout_inputs(case)
+    say(f"[layout3] case={case} theta={theta} n={y.shape[0]}")
+    Y = dev_y(y)
+    P = bh.Csr.from_numpy(rp, col, val)
+    ws = torch.empty(bh.workspace_size_3d(y.shape[0], col.size), dtype=torch.uint8, device="cuda")
+    lay = bh.Layout3(P, Y, workspace=ws)
+    # each of these spans at most 32 windows per row block
+    assert lay.tiles > 0 and lay.windows == 0
+    g, Z = bh.gradient_3d(Y, lay, theta, 12.0, workspace=ws)
+    go, Zo, _, _ = oracle.gradient3(y, rp, col, val, theta, 12.0)
+    g = g.cpu().numpy()
+    if np.linalg.norm(go) == 0.0:
+        assert np.abs(g).max() <= 1e-6
+    else:
+        assert rel_l2(g, go) <= (1e-4 if theta == 0.0 else 1e-3)
+    assert abs(Z - Zo) <= 1e-5 * Zo
+    gp, Zp = bh.gradient_3d(Y, P, theta, 12.0, workspace=ws)
+    assert Zp == Z
+    gp = gp.cpu().numpy()
+    if np.linalg.norm(gp) > 0.0:
+        assert rel_l2(g, gp) <= 1e-5
+    say(f"[layout3] case={case}: tiles {lay.tiles} items {lay.items} order {lay.order}")
+
+
+def test_layout3_sliced_copy_is_p():
+    """Several windows and row blocks (40k points, a ragged last block): the
+    tile tables and the sliced copy over 8192-point windows hold exactly P."""
+    from layout_tables import check_sliced_copy
+
+    inp = synth.make_inputs(1, n=40000, dim=3)
+    P = bh.Csr.from_numpy(inp.row_ptr, inp.col, inp.val)
+    lay = bh.Layout3(P, dev_y(inp.Y))
+    assert lay.tiles > 0
+    check_sliced_copy(lay, inp.row_ptr, inp.col, inp.val, seg=8192, max_seg=32)
+
+
+def test_layout3_steps_track_plain_steps():
+    inp = synth.make_inputs(0, dim=3)
+    w = inp.workload
+    P = bh.Csr.from_numpy(inp.row_ptr, inp.col, inp.val)
+    Ya = dev_y(inp.Y)
+    Yb = Ya.clone()
+    lay = bh.Layout3(P, Ya)
+    ua, ub = torch.zeros_like(Ya), torch.zeros_like(Ya)
+    ga, gb = torch.ones_like(Ya), torch.ones_like(Ya)
+    grad_b = torch.empty_like(Ya)
+    y64 = inp.Y.astype(np.float64)
+    u64, g64 = np.zeros_like(y64), np.ones_like(y64)
+    for it in range(5):
+        s = w.schedule(it)
+        bh.step_3d(Ya, P, 0.5, s["exaggeration"], s["learning_rate"], s["momentum"], 0.01, ua, ga)
+        bh.step_3d(Yb, lay, 0.5, s["exaggeration"], s["learning_rate"], s["momentum"], 0.01, ub, gb, grad=grad_b)
+        # the layout step's own update rule, element by element
+        oracle.update(y64, u64, g64, grad_b.cpu().numpy().astype(np.float64), s["learning_rate"], s["momentum"],
+                      0.01)
+        assert np.allclose(gb.cpu().numpy(), g64, rtol=1e-6, atol=0)
+        assert np.allclose(Yb.cpu().numpy(), y64, rtol=2e-5, atol=1e-6 * np.abs(y64).max())
+        y64 = Yb.cpu().numpy().astype(np.float64)
+        u64 = ub.cpu().numpy().astype(np.float64)
+        g64 = gb.cpu().numpy().astype(np.float64)
+    a, b = Ya.cpu().numpy(), Yb.cpu().numpy()
+    assert np.abs(a - b).max() <= 1e-4 * np.abs(a).max()
+
+
+def test_layout3_without_tiles_is_refused():
+    """Rows spread over more than 32 windows of one row block: the build
+    succeeds without a sliced copy and the layout calls refuse the handle."""
+    import scipy.sparse as sp
+
+    n = 300000
+    y = synth.random_y3(n, seed=8, scale=3.0)
+    # 6 random neighbours per row (no self pairs), symmetrised: no order brings
+    # a row block's columns within 32 windows
+    rng = np.random.default_rng(8)
+    rows = np.repeat(np.arange(n), 6)
+    cols = rng.integers(0, n - 1, size=rows.size)
+    cols += cols >= rows
+    c = sp.csr_matrix((rng.uniform(0.1, 1.0, rows.size), (rows, cols)), shape=(n, n))
+    Pm = (c + c.T).tocsr()
+    Pm.sum_duplicates()
+    Pm.sort_indices()
+    P = bh.Csr.from_numpy(Pm.indptr.astype(np.int64), Pm.indices.astype(np.int32),
+                          (Pm.data / Pm.data.sum()).astype(np.float32))
+    lay = bh.Layout3(P, dev_y(y))
+    assert lay.tiles == 0 and lay.windows == 0
+    with pytest.raises(bh.BhtsneError) as e:
+        bh.gradient_3d(dev_y(y), lay, 0.5, 1.0)
+    assert e.value.status == bh.BHTSNE_EINVAL
+
+
 def test_nonfinite_input3_is_reported():
     y = synth.random_y3(500, seed=7)
     y[3, 2] = np.nan
