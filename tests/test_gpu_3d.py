@@ -271,19 +271,26 @@ def test_full_run_kl3_small_workload():
 @pytest.mark.parametrize("cid,theta", [(2, 0.5), (4, 0.5)])
 def test_gradient3_full_size_sampled(cid, theta):
     """1.3M points with a 3-D embedding (early phase, and late phase with 5%
-    duplicates): 4000 sampled gradients against the oracle's traversal of
-    those points, Z and the interaction total from its full pass, the node
-    count exactly."""
+    duplicates): 4000 sampled gradients, with P plain and through the 3-D
+    layout, against the oracle's traversal of those points, Z and the
+    interaction total from its full pass, the node count exactly."""
     inp = synth.make_inputs(cid, dim=3, progress=say)
     n = inp.n
     alpha = synth.WORKLOADS[cid].schedule(0)["exaggeration"]
     P = bh.Csr.from_numpy(inp.row_ptr, inp.col, inp.val)
     ws = torch.empty(bh.workspace_size_3d(n, inp.nnz), dtype=torch.uint8, device="cuda")
-    g, Z = bh.gradient_3d(dev_y(inp.Y), P, theta, alpha, workspace=ws)
+    Y = dev_y(inp.Y)
+    g, Z = bh.gradient_3d(Y, P, theta, alpha, workspace=ws)
     stats = bh.get_stats(ws)
+    # the same gradient with P through the 3-D locality layout
+    lay = bh.Layout3(P, Y, workspace=ws)
+    assert lay.tiles > 0
+    gl, Zl = bh.gradient_3d(Y, lay, theta, alpha, workspace=ws)
+    assert Zl == Z
     sample = np.sort(np.random.default_rng(3000 + cid).choice(n, size=4000, replace=False))
     g = g.cpu().numpy()[sample].astype(np.float64)
-    del P, ws
+    gl = gl.cpu().numpy()[sample].astype(np.float64)
+    del P, ws, lay, Y
     torch.cuda.empty_cache()
     fattr = oracle.attractive3(inp.Y, inp.row_ptr, inp.col, inp.val, rows=sample)
     with oracle.State3(inp.Y) as s:
@@ -294,10 +301,10 @@ def test_gradient3_full_size_sampled(cid, theta):
         frep, zi, inter = s.repulsive(theta)
     Zo = oracle.ordered_sum(zi)
     go = 4.0 * (alpha * fattr - frep[sample] / Zo)
-    err = rel_l2(g, go)
-    say(f"[full3] workload {cid}: rel-L2 {err:.2e}, Z {Z:.9e} vs {Zo:.9e}, interactions "
+    err, errl = rel_l2(g, go), rel_l2(gl, go)
+    say(f"[full3] workload {cid}: rel-L2 {err:.2e} (layout {errl:.2e}), Z {Z:.9e} vs {Zo:.9e}, interactions "
         f"{stats['interactions']} vs {int(inter.sum())}, nodes {stats['nodes']} vs {nodes_o}")
-    assert err <= 1e-3
+    assert err <= 1e-3 and errl <= 1e-3
     assert abs(Z - Zo) <= 1e-5 * Zo
     assert abs(stats["interactions"] - int(inter.sum())) <= 1e-3 * int(inter.sum())
     assert stats["nodes"] == nodes_o
