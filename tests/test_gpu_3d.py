@@ -70,11 +70,22 @@ def _case(name):
     if name == "reps40":
         y = np.repeat(synth.random_y3(3000, seed=13, scale=1.0), 40, axis=0)
         return y[np.random.default_rng(13).permutation(y.shape[0])]
+    if name.startswith("jitter"):  # places of m points 1e-5 apart, shuffled: runs of equal top halves
+        places, m = {"jitter5": (1000, 5), "jitter100": (60, 100)}[name]
+        y = np.repeat(synth.random_y3(places, seed=15, scale=1.0), m, axis=0)
+        y = y + synth.random_y3(places * m, seed=16, scale=1e-5)
+        return y[np.random.default_rng(15).permutation(places * m)].astype(np.float32)
+    if name == "cloud6k":  # 6000 points within 1e-2 and one far away: a run of 6000 top halves
+        y = synth.random_y3(6000, seed=17, scale=1e-3)
+        y[4321] = (1e3, 1e3, 1e3)
+        return y
     raise KeyError(name)
 
 
 SORT_CASES = ["c0", "rand2", "rand3", "rand63", "rand64", "rand65", "rand2049", "rand4097", "rand70001", "dups",
-              "identical", "identical2", "huge", "tiny", "outlier", "line", "plane", "late", "reps40"]
+              "identical", "identical2", "huge", "tiny", "outlier", "line", "plane", "late", "reps40", "jitter5",
+              "jitter100", "cloud6k"]
+RUN_CASES = {"jitter5": (2, 32), "jitter100": (33, 4096), "cloud6k": (4097, 1 << 30)}
 
 
 @pytest.mark.parametrize("case", SORT_CASES)
@@ -90,6 +101,11 @@ def test_morton3_and_sort_bit_exact(case):
     assert np.array_equal(codes.cpu().numpy().view(np.uint64), t.codes)
     assert np.array_equal(scodes.cpu().numpy().view(np.uint64), t.sorted_codes)
     assert np.array_equal(perm.cpu().numpy().view(np.uint32), t.perm)
+    if case in RUN_CASES:
+        lo, hi = RUN_CASES[case]
+        top = t.sorted_codes.astype(np.uint64) >> np.uint64(32)
+        starts = np.flatnonzero(np.r_[True, top[1:] != top[:-1]])
+        assert lo <= int(np.diff(np.r_[starts, top.size]).max()) <= hi
 
 
 def test_quantisation3_hand_worked_case(golden_dir):

@@ -74,12 +74,31 @@ def _case(name):
         return y[np.random.default_rng(13).permutation(y.shape[0])]
     if name == "identical20k":  # one run of equal codes longer than a block sorts in LDS
         return np.full((20000, 2), -2.5, np.float32)
+    if name.startswith("jitter"):  # places of m points 1e-6 apart, shuffled: runs of equal top halves
+        places, m = {"jitter5": (1000, 5), "jitter100": (60, 100)}[name]
+        y = np.repeat(synth.random_y(places, seed=15, scale=1.0), m, axis=0)
+        y = y + synth.random_y(places * m, seed=16, scale=1e-6)
+        return y[np.random.default_rng(15).permutation(places * m)].astype(np.float32)
+    if name == "cloud6k":  # 6000 points within 1e-4 and one far away: a run of 6000 top halves
+        y = synth.random_y(6000, seed=17, scale=1e-5)
+        y[4321] = (1e3, 1e3)
+        return y
     raise KeyError(name)
 
 
 SORT_CASES = ["c0", "rand2", "rand3", "rand63", "rand64", "rand65", "rand2047", "rand2048",
               "rand2049", "rand4097", "rand70001", "dups", "identical", "identical2", "huge",
-              "tiny", "outlier", "line", "late", "reps40", "identical20k"]
+              "tiny", "outlier", "line", "late", "reps40", "identical20k", "jitter5", "jitter100", "cloud6k"]
+
+# the longest run of codes with equal top 32 bits these cases are made to have
+# (the sort's three ways of ordering such runs)
+RUN_CASES = {"jitter5": (2, 32), "jitter100": (33, 4096), "cloud6k": (4097, 1 << 30)}
+
+
+def longest_top_half_run(sorted_codes):
+    hi = np.asarray(sorted_codes, np.uint64) >> np.uint64(32)
+    starts = np.flatnonzero(np.r_[True, hi[1:] != hi[:-1]])
+    return int(np.diff(np.r_[starts, hi.size]).max())
 
 
 @pytest.mark.parametrize("case", SORT_CASES)
@@ -97,6 +116,9 @@ def test_morton_and_sort_bit_exact(case):
     assert np.array_equal(codes.cpu().numpy().view(np.uint64), t.codes)
     assert np.array_equal(scodes.cpu().numpy().view(np.uint64), t.sorted_codes)
     assert np.array_equal(perm.cpu().numpy().view(np.uint32), t.perm)
+    if case in RUN_CASES:
+        lo, hi = RUN_CASES[case]
+        assert lo <= longest_top_half_run(t.sorted_codes) <= hi
 
 
 def test_quantisation_truncates_like_the_hand_worked_case(golden_dir):
