@@ -1,6 +1,7 @@
 """A gradient step captured in a HIP graph (through torch.cuda.graph) and
 replayed: the layout step (with the attractive forces forked to the second
-stream and joined back by events), the plain CSR step and the fp64 step.
+stream and joined back by events), the plain CSR step, the fp64 step and
+the 3-D layout step.
 A step allocates nothing, never synchronises unless Z is requested and
 clears its counters with kernels, so each replay must give bit for bit the
 eager trajectory's Y, update and gains, with eager work on the same
@@ -22,11 +23,18 @@ def say(*a):
     print(*a, flush=True)
 
 
-@pytest.mark.parametrize("form", ["layout", "plain", "fp64"])
+@pytest.mark.parametrize("form", ["layout", "plain", "fp64", "layout3d"])
 def test_step_replays_in_a_graph(form):
-    inp = synth.make_inputs(1)
+    inp = synth.make_inputs(1, dim=3 if form == "layout3d" else 2)
     dev = torch.device(DEV)
-    if form == "fp64":
+    if form == "layout3d":
+        Y0 = torch.from_numpy(inp.Y).to(dev)
+        P = bh.Csr.from_numpy(inp.row_ptr, inp.col, inp.val, device=dev)
+        ws = torch.empty(bh.workspace_size_3d(inp.n, inp.nnz), dtype=torch.uint8, device=dev)
+        step, grad, other = bh.step_3d, bh.gradient_3d, P
+        P = bh.Layout3(P, Y0, workspace=ws)
+        assert P.tiles > 0
+    elif form == "fp64":
         Y0 = torch.from_numpy(inp.Y.astype(np.float64)).to(dev)
         P = bh.CsrF64.from_numpy(inp.row_ptr, inp.col, inp.val.astype(np.float64), device=dev)
         ws = torch.empty(bh.workspace_size_f64(inp.n, inp.nnz), dtype=torch.uint8, device=dev)
