@@ -129,3 +129,21 @@ def check_sliced_copy(lay, row_ptr, col_in, val_in, seg=TILE_SEG, max_seg=TILE_M
     Po = sp.csr_matrix((val_in, col_in, row_ptr), shape=(n, n))
     ref = Po[perm.astype(np.int64)][:, perm.astype(np.int64)]
     assert abs(Pt - ref).max() == 0.0 and Pt.nnz == len(col_in)
+
+
+def bfs_perm(rp, col, n):
+    """The order (component, breadth-first level from the component's smallest
+    point along P's rows, index), from scipy's graph routines."""
+    import scipy.sparse.csgraph as cg
+    A = sp.csr_matrix((np.ones(col.size), col, rp), shape=(n, n))
+    nc, lab = cg.connected_components(A, directed=False)
+    root = np.full(nc, n, np.int64)
+    np.minimum.at(root, lab, np.arange(n))
+    level = np.full(n, -1, np.int64)
+    for r in root:
+        order, pred = cg.breadth_first_order(A, int(r), directed=True, return_predecessors=True)
+        level[r] = 0
+        for v in order[1:]:  # breadth-first: a predecessor's level is set before its children's
+            level[v] = level[pred[v]] + 1
+    assert np.all(level >= 0)
+    return np.lexsort((np.arange(n), level, root[lab])).astype(np.uint32)

@@ -380,6 +380,31 @@ def test_layout3_sliced_copy_is_p():
     check_sliced_copy(lay, inp.row_ptr, inp.col, inp.val, seg=8192, max_seg=32)
 
 
+def test_layout3_takes_the_breadth_first_order_when_morton_gives_no_tiles():
+    """P from the 30 nearest neighbours of 400,000 points uniform in the unit
+    square (one component), a random 3-D embedding: in Morton order of Y a row
+    block reaches all 49 windows of 8192 points, more than the 32 a 3-D tile
+    row allows, so the build takes the breadth-first levels of P's graph; the
+    copy's order is exactly (component, level, index), the tiles engage and
+    the gradient matches the oracle's."""
+    from layout_tables import bfs_perm, layout_arrays
+
+    n = 400_000
+    rp, col, val = synth.geometric_p(n, 43, k=30)
+    y = synth.random_y3(n, seed=43, scale=1e-2)
+    Y = dev_y(y)
+    P = bh.Csr.from_numpy(rp, col, val)
+    lay = bh.Layout3(P, Y)
+    say(f"[layout3-bfs] order {lay.order}, tiles {lay.tiles}")
+    assert lay.order == bh.ORDER_BFS and lay.tiles > 0
+    assert np.array_equal(layout_arrays(lay)[0], bfs_perm(rp, col, n))
+    go, Zo, _, _ = oracle.gradient3(y, rp, col, val, 0.5, 12.0)
+    g, Z = bh.gradient_3d(Y, lay, 0.5, 12.0)
+    err = rel_l2(g.cpu().numpy(), go)
+    say(f"[layout3-bfs] rel-L2 {err:.2e}")
+    assert err <= 1e-3 and abs(Z - Zo) <= 1e-5 * Zo
+
+
 def test_layout3_steps_track_plain_steps():
     inp = synth.make_inputs(0, dim=3)
     w = inp.workload

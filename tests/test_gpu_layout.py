@@ -33,6 +33,7 @@ def rel_l2(a, b):
 
 from layout_tables import (CHUNK, ITEM_MAX_TILES, SLICE, SLICES, TILE_MAX_SEG, TILE_ROWS,  # noqa: E402,F401
                            TILE_SEG, check_sliced_copy)
+from layout_tables import bfs_perm as _bfs_perm  # noqa: E402
 from layout_tables import layout_arrays as _layout_arrays  # noqa: E402
 
 
@@ -374,24 +375,6 @@ def test_windowed_segments_are_p_and_match_the_oracle(case):
 
 
 # ------------------------------------------------------------------ point orders
-def _bfs_perm(rp, col, n):
-    """The order (component, breadth-first level from the component's smallest
-    point along P's rows, index), from scipy's graph routines."""
-    import scipy.sparse.csgraph as cg
-    A = sp.csr_matrix((np.ones(col.size), col, rp), shape=(n, n))
-    nc, lab = cg.connected_components(A, directed=False)
-    root = np.full(nc, n, np.int64)
-    np.minimum.at(root, lab, np.arange(n))
-    level = np.full(n, -1, np.int64)
-    for r in root:
-        order, pred = cg.breadth_first_order(A, int(r), directed=True, return_predecessors=True)
-        level[r] = 0
-        for v in order[1:]:  # breadth-first: a predecessor's level is set before its children's
-            level[v] = level[pred[v]] + 1
-    assert np.all(level >= 0)
-    return np.lexsort((np.arange(n), level, root[lab])).astype(np.uint32)
-
-
 @pytest.mark.parametrize("blobs", [1, 2])
 def test_bfs_order_tiles_a_geometric_p_from_a_random_y(blobs):
     """P from the 30 nearest neighbours of 400,000 points uniform in the unit
