@@ -447,8 +447,9 @@ int bhtsne_step_3d(float *Y, const bhtsne_csr *P, float theta, float exaggeratio
  * tagged as a 3-D layout: the 2-D layout calls refuse it and these calls
  * refuse a 2-D one.  bhtsne_gradient_layout_3d / bhtsne_step_layout_3d are
  * bhtsne_gradient_3d / bhtsne_step_3d taking P through such a layout: the
- * attractive forces run on the library's second stream beside the sort,
- * tree and walk; results come back in the caller's order.  Errors as the
+ * attractive forces run on the library's second stream beside the walk
+ * (BHTSNE_FORK3 = 0 or 1 forks them after the codes or the sort instead);
+ * results come back in the caller's order.  Errors as the
  * plain 3-D calls, and BHTSNE_EINPUT from the build for malformed row
  * pointers. */
 size_t bhtsne_layout_size_3d(int64_t n, int64_t nnz);
