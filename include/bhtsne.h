@@ -396,8 +396,9 @@ int bhtsne_step_f64(double *Y, const bhtsne_csr_f64 *P, double theta, double exa
  * fp32 layout calls refuse it, and these calls refuse an fp32 one.
  * bhtsne_gradient_layout_f64 / bhtsne_step_layout_f64 are bhtsne_gradient_f64
  * / bhtsne_step_f64 taking P through such a layout: the attraction runs on
- * the library's second stream, beside the sort, tree and walk; results come
- * back in the caller's order.  Errors as the plain fp64 calls, and
+ * the library's second stream beside the walk (BHTSNE_FORK64 = 0 or 1 forks
+ * it after the codes or the sort instead); results come back in the caller's
+ * order.  Errors as the plain fp64 calls, and
  * BHTSNE_EINPUT from the build for malformed row pointers. */
 size_t bhtsne_layout_size_f64(int64_t n, int64_t nnz);
 int bhtsne_layout_build_f64(const bhtsne_csr_f64 *P, const double *Y, void *layout_mem, size_t layout_bytes,

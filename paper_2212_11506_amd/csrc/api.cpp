@@ -214,6 +214,20 @@ int fork_point3()
     return v;
 }
 
+// the same for fp64 layouts (BHTSNE_FORK64; default 2, after the tree): the
+// fp64 tree phase slows from 0.14 to 0.51 ms beside the attraction, while the
+// fp64 walk, 2.6 times the fp32 one, absorbs it; 412.4 iterations/s at 1.3M
+// points against 402.7 forked after the codes and 389.7 after the sort.
+int fork_point64()
+{
+    static int v = [] {
+        const char *e = std::getenv("BHTSNE_FORK64");
+        int x = e ? std::atoi(e) : 2;
+        return x < 0 ? 0 : (x > 2 ? 2 : x);
+    }();
+    return v;
+}
+
 int device_cus()
 {
     int dev = 0, cus = 0;
@@ -379,9 +393,9 @@ int run64(double *Y, const bhtsne_csr_f64 *P, double theta, const StepArgsT<doub
     return finish(Z, ws, st);
 }
 
-// The fp64 variant through a layout: the windowed-segment attraction (or the
-// plain one when the layout has no segments) on the second stream, forked
-// after the codes, beside the sort, tree and walk.
+// The fp64 variant through a layout: the sliced or windowed-segment
+// attraction on the second stream, by default forked after the tree, beside
+// the walk.
 int run_layout64(double *Y, const bhtsne_layout *lay, double theta, const StepArgsT<double> &a, double *update,
                  double *gains, double *grad, double *Z, void *ws, hipStream_t st)
 {
@@ -392,6 +406,15 @@ int run_layout64(double *Y, const bhtsne_layout *lay, double theta, const StepAr
         PhaseTimer pt(BHTSNE_PHASE_BBOX_MORTON, st);
         launch_bbox(Y, n, ws, L, st);
         launch_morton(static_cast<const double *>(Y), n, lv.rank, ws, L, st);
+    }
+    const int fork = fork_point64();
+    if (fork >= 1) {
+        PhaseTimer pt(BHTSNE_PHASE_SORT, st);
+        launch_sort(n, static_cast<const double *>(Y), ws, L, st);
+    }
+    if (fork >= 2) {
+        PhaseTimer pt(BHTSNE_PHASE_TREE, st);
+        launch_tree<2, double>(n, theta * theta, ws, L, TreeDebug{}, st);
     }
     Side *side = overlap_enabled() ? side_stream() : nullptr;
     std::unique_lock<std::mutex> lk;
@@ -408,11 +431,11 @@ int run_layout64(double *Y, const bhtsne_layout *lay, double theta, const StepAr
                                       int(lay->windows), ws, L, sa);
     }
     if (side && hipEventRecord(side->join, sa) != hipSuccess) return BHTSNE_EDEVICE;
-    {
+    if (fork < 1) {
         PhaseTimer pt(BHTSNE_PHASE_SORT, st);
         launch_sort(n, static_cast<const double *>(Y), ws, L, st);
     }
-    {
+    if (fork < 2) {
         PhaseTimer pt(BHTSNE_PHASE_TREE, st);
         launch_tree<2, double>(n, theta * theta, ws, L, TreeDebug{}, st);
     }
