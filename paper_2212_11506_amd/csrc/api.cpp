@@ -184,47 +184,44 @@ bool overlap_enabled()
     return v;
 }
 
-// where the attractive forces fork off: 0 after the codes, 1 after the sort,
-// 2 after the tree (BHTSNE_FORK; default 0).  Measured at 1.3M points the
+// Where a layout step forks the attractive forces off to the second stream:
+// 0 after the codes, 1 after the sort, 2 after the tree (an environment
+// variable, read once, else the default).
+int env_fork(const char *name, int dflt)
+{
+    const char *e = std::getenv(name);
+    const int x = e ? std::atoi(e) : dflt;
+    return x < 0 ? 0 : (x > 2 ? 2 : x);
+}
+
+// fp32 2-D layouts (BHTSNE_FORK; default 0).  Measured at 1.3M points the
 // sort, a chain of latency-bound passes, does best on the CUs the attractive
 // kernel leaves free (its blocks cannot share a CU's LDS with one), and the
-// tree and the repulsive walk lose more than they hide when forked later.
+// tree and the repulsive walk lose more than they hide when forked later:
+// 844 iterations/s, against 752 after the sort and 754 after the tree.
 int fork_point()
 {
-    static int v = [] {
-        const char *e = std::getenv("BHTSNE_FORK");
-        int x = e ? std::atoi(e) : 0;
-        return x < 0 ? 0 : (x > 2 ? 2 : x);
-    }();
+    static const int v = env_fork("BHTSNE_FORK", 0);
     return v;
 }
 
-// the same for 3-D layouts (BHTSNE_FORK3; default 2, after the tree).  The
-// 3-D walk is four times longer than the 2-D one, so the attraction it
-// absorbs costs it less than the attraction costs the sort and tree beside
-// them: 337.9 iterations/s at 1.3M points, against 324.9 forked after the
-// codes and 297.0 after the sort.
+// 3-D layouts (BHTSNE_FORK3; default 2, after the tree).  The 3-D walk is four
+// times longer than the 2-D one, so the attraction it absorbs costs it less
+// than the attraction costs the sort and tree beside them: 337.9 iterations/s
+// at 1.3M points, against 324.9 forked after the codes and 297.0 after the sort.
 int fork_point3()
 {
-    static int v = [] {
-        const char *e = std::getenv("BHTSNE_FORK3");
-        int x = e ? std::atoi(e) : 2;
-        return x < 0 ? 0 : (x > 2 ? 2 : x);
-    }();
+    static const int v = env_fork("BHTSNE_FORK3", 2);
     return v;
 }
 
-// the same for fp64 layouts (BHTSNE_FORK64; default 2, after the tree): the
-// fp64 tree phase slows from 0.14 to 0.51 ms beside the attraction, while the
-// fp64 walk, 2.6 times the fp32 one, absorbs it; 412.4 iterations/s at 1.3M
-// points against 402.7 forked after the codes and 389.7 after the sort.
+// fp64 layouts (BHTSNE_FORK64; default 2, after the tree): the fp64 tree phase
+// slows from 0.14 to 0.51 ms beside the attraction, while the fp64 walk, 2.6
+// times the fp32 one, absorbs it; 412.4 iterations/s at 1.3M points against
+// 402.7 forked after the codes and 389.7 after the sort.
 int fork_point64()
 {
-    static int v = [] {
-        const char *e = std::getenv("BHTSNE_FORK64");
-        int x = e ? std::atoi(e) : 2;
-        return x < 0 ? 0 : (x > 2 ? 2 : x);
-    }();
+    static const int v = env_fork("BHTSNE_FORK64", 2);
     return v;
 }
 
