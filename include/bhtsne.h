@@ -200,8 +200,9 @@ size_t bhtsne_layout_size(int64_t n, int64_t nnz);
  * slice.  Without that copy (rows whose neighbours spread over a large
  * component), the build lists instead, for each column window of 2^18
  * points, the (row, entry range) segments of the rows with entries there
- * (out->windows > 0): the attraction then takes one pass per window, with
- * that window of Y held in the L2 caches.  The gradient does not depend on the order; only the speed of the
+ * (out->windows > 0; out->segments = 0 for a P with no entries): the
+ * attraction then takes one pass per window, with that window of Y held in
+ * the L2 caches.  The gradient does not depend on the order; only the speed of the
  * attractive step does.
  *   P      the matrix (as for bhtsne_gradient; nnz < 2^31).
  *   Y      device, n x 2, nullable: without it points keep their index order
@@ -387,7 +388,7 @@ int bhtsne_step_f64(double *Y, const bhtsne_csr_f64 *P, double theta, double exa
  * does, with fp64 values over column windows of 8192 points (128 KB of fp64 Y
  * in LDS) and at most 32 tiles per block of 1024 rows (out->tiles > 0);
  * without it, the (row, entry range) segments of each column window of 2^18
- * points (out->windows > 0, out->segments > 0).  A row longer than 4096
+ * points (out->windows > 0; out->segments > 0 unless P has no entries).  A row longer than 4096
  * entries keeps its order, which rules out the sliced copy and, with more
  * than one column window, the segments (out->tiles = out->windows = 0); such
  * a layout is refused by the two calls below (BHTSNE_EINVAL): use the plain
@@ -441,8 +442,8 @@ int bhtsne_step_3d(float *Y, const bhtsne_csr *P, float theta, float exaggeratio
  * tiles), over column windows of 8192 points (96 KB of LDS) and up to 32
  * tiles per row block.  There are no windowed segments: when no order gives
  * tiles (or a row is too long to sort) the build succeeds with tiles == 0 and
- * the 3-D layout calls refuse the handle with BHTSNE_EINVAL; the plain 3-D
- * calls serve such a P.  layout_mem holds bhtsne_layout_size_3d bytes (256-byte
+ * the 3-D layout calls refuse the handle with BHTSNE_EINVAL, unless P has no
+ * entries (its attraction is zero); the plain 3-D calls serve such a P.  layout_mem holds bhtsne_layout_size_3d bytes (256-byte
  * aligned, owned by the caller and kept alive and unchanged while the handle
  * is used); the workspace is bhtsne_workspace_size_3d bytes.  The handle is
  * tagged as a 3-D layout: the 2-D layout calls refuse it and these calls

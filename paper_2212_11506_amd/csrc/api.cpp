@@ -353,7 +353,9 @@ int check_layout(const bhtsne_layout *lay, int vbytes = 4, int dim = 2)
     if (lay->tiles < 0 || lay->tiles > v.max_tiles) return BHTSNE_EINVAL;
     if (lay->items < 0 || lay->items > lay->tiles || (lay->tiles > 0) != (lay->items > 0)) return BHTSNE_EINVAL;
     if (lay->windows < 0 || lay->windows > kMaxWindows || (lay->windows > 0 && lay->tiles > 0)) return BHTSNE_EINVAL;
-    if (lay->segments < 0 || lay->segments > v.max_segments || (lay->windows > 0) != (lay->segments > 0))
+    // windowed segments need windows; windows without segments are a P with no
+    // entries (F_attr = 0)
+    if (lay->segments < 0 || lay->segments > v.max_segments || (lay->segments > 0 && lay->windows == 0))
         return BHTSNE_EINVAL;
     if (lay->order != BHTSNE_ORDER_MORTON && lay->order != BHTSNE_ORDER_BFS) return BHTSNE_EINVAL;
     return BHTSNE_OK;
@@ -864,8 +866,9 @@ static int check_layout3_step(const bhtsne_layout *layout, const float *Y, float
 {
     int rc = check_layout(layout, 4, 3);
     if (rc != BHTSNE_OK) return rc;
-    // no sliced copy (no tile locality, or rows too long to sort): use the plain 3-D calls
-    if (layout->tiles == 0 || layout->windows != 0) return BHTSNE_EINVAL;
+    // no sliced copy (no tile locality, or rows too long to sort): use the plain
+    // 3-D calls; a P with no entries has no tiles and F_attr = 0
+    if ((layout->tiles == 0 && layout->nnz > 0) || layout->windows != 0) return BHTSNE_EINVAL;
     if (!Y) return BHTSNE_EINVAL;
     if (!finite_f(theta) || theta < 0.0f) return BHTSNE_EINVAL;
     if (!finite_f(exaggeration) || !(exaggeration > 0.0f)) return BHTSNE_EINVAL;

@@ -674,6 +674,12 @@ __global__ void seg_windows_kernel(const int64_t *__restrict__ off, int nw, int6
     if (k == nw) wstart[k] = *total;
 }
 
+__global__ __launch_bounds__(256) void fill_zero_f32_kernel(float *__restrict__ f, int64_t m)
+{
+    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < m; i += int64_t(gridDim.x) * blockDim.x)
+        f[i] = 0.0f;
+}
+
 template <typename T> __global__ __launch_bounds__(256) void zero_vec2_kernel(vec2_t<T> *__restrict__ f, int64_t n)
 {
     for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x)
@@ -1733,7 +1739,11 @@ template void launch_update<double>(const LayoutView &, int64_t, bool, const Ste
 void launch_attract_layout3(const LayoutView &lv, int64_t n, int tiles, int items, int blocks, void *ws,
                             const Layout &L, hipStream_t st)
 {
-    if (tiles <= 0 || items <= 0) return;
+    if (tiles <= 0 || items <= 0) { // a P with no entries: F_attr = 0
+        fill_zero_f32_kernel<<<unsigned(std::min<int64_t>((3 * n + 255) / 256, 4096)), 256, 0, st>>>(
+            at<float>(ws, L.fattr), 3 * n);
+        return;
+    }
     const unsigned grid = unsigned(blocks < items ? blocks : items);
     attract_sell_kernel<float, 3><<<grid, kTileBlock, 0, st>>>(
         lv.item_tiles, lv.item_units, lv.wave_units, lv.tile_blk, lv.tile_seg, lv.unit_chunks, lv.unit_tj, lv.tperm,

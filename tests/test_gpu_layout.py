@@ -170,6 +170,51 @@ def test_layout_steps_track_plain_steps():
     assert np.abs(a - b).max() <= 1e-4 * np.abs(a).max()
 
 
+def _ragged_and_empty_p(n, seed):
+    """P with the rows (and columns) of its first 500 points emptied, and a P
+    with no entries at all."""
+    rp, col, val = synth.random_p(n, seed=seed, k=6)
+    r = np.repeat(np.arange(n), np.diff(rp))
+    keep = (r >= 500) & (col >= 500)
+    rp2 = np.concatenate([[0], np.cumsum(np.bincount(r[keep], minlength=n))]).astype(np.int64)
+    return [(rp2, col[keep], val[keep]),
+            (np.zeros(n + 1, np.int64), np.zeros(0, np.int32), np.zeros(0, np.float32))]
+
+
+@pytest.mark.parametrize("form", ["fp32", "fp64", "3d"])
+def test_layouts_of_ragged_and_empty_p(form):
+    """Rows without entries, and a P without any, through the three layout
+    forms: the oracle's gradient (zero attraction where rows are empty)."""
+    n = 3000
+    for rp, col, val in _ragged_and_empty_p(n, seed=21):
+        say(f"[layout-ragged] form={form} nnz={col.size}")
+        if form == "3d":
+            y = synth.random_y3(n, seed=21, scale=2.0)
+            Y = torch.from_numpy(y).cuda()
+            lay = bh.Layout3(bh.Csr.from_numpy(rp, col, val), Y)
+            g, Z = bh.gradient_3d(Y, lay, 0.5, 4.0)
+            go, Zo, _, _ = oracle.gradient3(y, rp, col, val, 0.5, 4.0)
+            tol = 1e-3
+        elif form == "fp64":
+            y = synth.random_y(n, seed=21, scale=2.0).astype(np.float64)
+            Y = torch.from_numpy(y).cuda()
+            lay = bh.LayoutF64(bh.CsrF64.from_numpy(rp, col, val.astype(np.float64)), Y)
+            g, Z = bh.gradient_f64(Y, lay, 0.5, 4.0)
+            go, Zo, _, _ = oracle.gradient(y, rp, col, val.astype(np.float64), 0.5, 4.0)
+            tol = 1e-9
+        else:
+            y = synth.random_y(n, seed=21, scale=2.0)
+            Y = torch.from_numpy(y).cuda()
+            lay = bh.Layout(bh.Csr.from_numpy(rp, col, val), Y)
+            g, Z = bh.gradient(Y, lay, 0.5, 4.0)
+            go, Zo, _, _ = oracle.gradient(y, rp, col, val, 0.5, 4.0)
+            tol = 1e-3
+        say(f"[layout-ragged] tiles {lay.tiles} windows {lay.windows} segments {lay.segments}")
+        assert lay.tiles > 0 or col.size == 0
+        assert rel_l2(g.cpu().numpy(), go) <= tol
+        assert abs(Z - Zo) <= (1e-12 if form == "fp64" else 1e-5) * Zo
+
+
 def test_direct_gather_fallback_in_subprocess():
     # with LDS staging disabled every block takes y_j straight from memory
     code = (
