@@ -257,17 +257,21 @@ template <int N> struct StaticFor<N, N> {
 };
 
 // entropy (nats) of the Gaussian weights at sigma^2 = s2 over a row held as
-// in aff_search_quad_kernel; the same value in the row's four lanes
-template <int kPer> __device__ __forceinline__ double row_entropy_quad(const double (&dp)[kPer], double s2)
+// in aff_search_quad_kernel; the same value in the row's four lanes.  With
+// kVar, also *var = the weights' variance of a = d'^2 / 2 sigma^2, which is
+// dH / d ln sigma^2 (the entropy's own sums are formed exactly as without it).
+template <int kPer, bool kVar = false>
+__device__ __forceinline__ double row_entropy_quad(const double (&dp)[kPer], double s2, double *var = nullptr)
 {
     const double inv = isinf(s2) ? 0.0 : 1.0 / (2.0 * s2);
-    double sw = 0.0, tw = 0.0;
+    double sw = 0.0, tw = 0.0, t2 = 0.0;
     if (!isinf(inv)) {
         StaticFor<0, kPer>::run([&](auto qc) {
             const double x = fmin(dp[decltype(qc)::value] * inv, kExp2Clamp); // a / ln 2
             const double w = exp2_neg(x);
             sw += w;
             tw = fma(x, w, tw);
+            if (kVar) t2 = fma(x, x * w, t2);
         });
     } else {
         // a = 0 or +inf: a w = 0
@@ -275,8 +279,22 @@ template <int kPer> __device__ __forceinline__ double row_entropy_quad(const dou
     }
     sw = quad_sum(sw);
     tw = quad_sum(tw);
+    if (kVar) {
+        t2 = quad_sum(t2);
+        const double m = kLn2 * tw / sw;
+        *var = fmax(kLn2 * kLn2 * t2 / sw - m * m, 0.0);
+    }
     return log(sw) + kLn2 * tw / sw;
 }
+
+// Margin of the entropy, in nats, beyond which a comparison with log u is
+// taken as settled: the evaluation's rounding (up to 128 terms summed in
+// fp64, each within a few ulps, then a log and a quotient of at most about
+// ten) stays below 3e-13, so a point whose computed entropy is more than
+// kAffMargin below log u has every smaller sigma^2 below it too (the entropy
+// increases with sigma^2), and likewise above.
+constexpr double kAffMargin = 1e-11;
+constexpr int kAffNewtonMax = 12;
 
 template <int kPer>
 __device__ __forceinline__ void search_row_quad(const float *__restrict__ dist, int64_t i, int g, int k,
@@ -311,15 +329,57 @@ __device__ __forceinline__ void search_row_quad(const float *__restrict__ dist, 
     // from here on the slots hold d'^2 / ln 2, so that a / ln 2 = slot / 2 sigma^2
     StaticFor<0, kPer>::run([&](auto qc) { dp[decltype(qc)::value] *= kLog2e; });
     auto entropy = [&](double s2) { return row_entropy_quad<kPer>(dp, s2); };
+    auto entropy_var = [&](double s2, double &v) { return row_entropy_quad<kPer, true>(dp, s2, &v); };
     double lo = 0.0, hi = mx > 0.0 ? mx : 1.0;
     if (mx > 0.0) {
+        // Settled bounds: every sigma^2 <= A has entropy below log u and every
+        // sigma^2 >= B at or above it, by more than the margin at A and B.
+        double A = 0.0, B = INFINITY, h = 0.0, v = 0.0;
+        auto settle = [&](double s2, double hs) {
+            if (hs < log_u - kAffMargin) A = fmax(A, s2);
+            else if (hs > log_u + kAffMargin) B = fmin(B, s2);
+        };
         // grow the top of the interval until the perplexity there reaches u
-        while (!isinf(hi) && entropy(hi) < log_u) hi *= 2.0;
+        for (;;) {
+            if (isinf(hi)) break;
+            h = entropy_var(hi, v);
+            settle(hi, h);
+            if (h >= log_u) break;
+            hi *= 2.0;
+        }
         if (!isinf(hi)) {
+            // Newton's method on ln sigma^2 (dH / d ln sigma^2 = v), kept inside
+            // the settled bounds, to bring them close around the root; then,
+            // from a point within the margin, one probe on either side.  The
+            // bounds only spare evaluations below: the bisection's outcome
+            // does not depend on them.
+            double s2 = hi;
+            for (int it = 0; it < kAffNewtonMax && B > A; ++it) {
+                const double r = (h - log_u) / v;
+                if (fabs(h - log_u) <= kAffMargin) {
+                    const double d = v > 0.0 ? fmin(4.0 * kAffMargin / v, 0.25) : 0.25;
+                    const double sa = s2 * (1.0 - d), sb = s2 * (1.0 + d);
+                    settle(sa, entropy(sa));
+                    settle(sb, entropy(sb));
+                    break;
+                }
+                double sn = s2 * (1.0 - r);
+                if (!(v > 0.0) || !(sn > A) || !(sn < B) || !(r < 1.0)) {
+                    // outside the bounds: halve them on the log scale (a far
+                    // start, where the entropy is flat, drops 64-fold)
+                    sn = isinf(B) ? 2.0 * fmax(A, s2) : (A > 0.0 ? sqrt(A * B) : B * (1.0 / 64.0));
+                }
+                if (sn == s2) break;
+                s2 = sn;
+                h = entropy_var(s2, v);
+                settle(s2, h);
+            }
+            // the bisection, as if every step were evaluated
             for (int s = 0; s < kAffMaxSteps; ++s) {
                 const double mid = 0.5 * (lo + hi);
                 if (mid <= lo || mid >= hi) break;
-                if (entropy(mid) < log_u)
+                const bool below = mid <= A ? true : (mid >= B ? false : entropy(mid) < log_u);
+                if (below)
                     lo = mid;
                 else
                     hi = mid;
