@@ -244,7 +244,10 @@ int bhtsne_layout_build_ordered(const bhtsne_csr *P, const float *Y, int order, 
  * priority), forked from `stream` after the Morton codes and joined back
  * before the gradient assembly, so they overlap the sort, tree and repulsive
  * phases; to the caller the call is ordered on `stream` as usual.  The
- * device is the current one, which must be the device of `stream`. */
+ * device is the current one, which must be the device of `stream`.  The
+ * environment variable BHTSNE_FORK = 1 or 2 (read once) forks them after the
+ * sort or the tree instead, and BHTSNE_OVERLAP = 0 keeps them on `stream`;
+ * the results are the same bit for bit. */
 int bhtsne_gradient_layout(const float *Y, const bhtsne_layout *layout, float theta, float exaggeration,
                            float *grad, double *Z, void *workspace, size_t workspace_bytes, hipStream_t stream);
 int bhtsne_step_layout(float *Y, const bhtsne_layout *layout, float theta, float exaggeration, float learning_rate,
