@@ -87,10 +87,12 @@ __device__ inline double scaled(double dp, double inv) { return dp > 0.0 ? dp * 
 // Entropy (nats) of the Gaussian weights at sigma^2 = s2 over this lane's
 // shifted squared distances (an infinite s2 gives log k).  a e^-a is taken as
 // 0 where the weight underflows.  The result is lane 0's, in every lane.
-template <int kPer> __device__ inline double row_entropy(const double (&dp)[kPer], int k, double s2)
+// With kVar, also *var = the weights' variance of a (see search_sigma2).
+template <int kPer, bool kVar = false>
+__device__ inline double row_entropy(const double (&dp)[kPer], int k, double s2, double *var = nullptr)
 {
     const double inv = isinf(s2) ? 0.0 : 1.0 / (2.0 * s2);
-    double s = 0.0, t = 0.0;
+    double s = 0.0, t = 0.0, t2 = 0.0;
 #pragma unroll
     for (int q = 0; q < kPer; ++q) {
         if (q < kPer - 1 || (kPer - 1) * kWave + lane_id() < k) {
@@ -98,11 +100,93 @@ template <int kPer> __device__ inline double row_entropy(const double (&dp)[kPer
             const double w = exp(-a);
             s += w;
             t += w > 0.0 ? a * w : 0.0;
+            if (kVar) t2 += w > 0.0 ? a * (a * w) : 0.0;
         }
     }
     s = uniform_d(wave_sum(s));
     t = uniform_d(wave_sum(t));
+    if (kVar) {
+        t2 = uniform_d(wave_sum(t2));
+        const double m = t / s;
+        *var = fmax(t2 / s - m * m, 0.0);
+    }
     return log(s) + t / s;
+}
+
+// Margin of the entropy, in nats, beyond which a comparison with log u is
+// taken as settled: the evaluation's rounding (up to 256 terms summed in
+// fp64, each within a few ulps, then a log and a quotient of at most about
+// ten) stays below 3e-13, so a point whose computed entropy is more than
+// kAffMargin below log u has every smaller sigma^2 below it too (the entropy
+// increases with sigma^2), and likewise above.
+constexpr double kAffMargin = 1e-11;
+constexpr int kAffNewtonMax = 12;
+
+// sigma^2 of one row: the upper end of the bisection interval [0, hi], hi
+// doubled from mx until the entropy there reaches log u, halved until the
+// midpoint equals an end (each midpoint goes below when its entropy is under
+// log u).  The decisions depend only on the sign of H(mid) - log u, and H
+// increases with sigma^2; so first Newton's method on ln sigma^2 (dH / d ln
+// sigma^2 = v, the weights' variance of a), kept inside the settled bounds,
+// brings a settled bound A below the root and B above it close together,
+// and the bisection then evaluates only the midpoints between them: the same
+// decisions, hence the same result bit for bit, with about half the
+// evaluations.  `entropy(s2)` and `entropy_var(s2, v)` give the row's
+// entropy, equal in every lane of the row's group, so the group branches alike.
+template <typename E, typename EV>
+__device__ __forceinline__ double search_sigma2(double mx, double log_u, E &&entropy, EV &&entropy_var)
+{
+    double lo = 0.0, hi = mx > 0.0 ? mx : 1.0;
+    if (!(mx > 0.0)) return hi;
+    double A = 0.0, B = INFINITY, h = 0.0, v = 0.0;
+    auto settle = [&](double s2, double hs) {
+        if (hs < log_u - kAffMargin)
+            A = fmax(A, s2);
+        else if (hs > log_u + kAffMargin)
+            B = fmin(B, s2);
+    };
+    // grow the top of the interval until the perplexity there reaches u
+    for (;;) {
+        if (isinf(hi)) return hi;
+        h = entropy_var(hi, v);
+        settle(hi, h);
+        if (h >= log_u) break;
+        hi *= 2.0;
+    }
+    // the bounds only spare evaluations below; from a point within the
+    // margin, one probe on either side
+    double s2 = hi;
+    for (int it = 0; it < kAffNewtonMax && B > A; ++it) {
+        if (fabs(h - log_u) <= kAffMargin) {
+            const double d = v > 0.0 ? fmin(4.0 * kAffMargin / v, 0.25) : 0.25;
+            const double sa = s2 * (1.0 - d), sb = s2 * (1.0 + d);
+            settle(sa, entropy(sa));
+            settle(sb, entropy(sb));
+            break;
+        }
+        const double r = (h - log_u) / v;
+        double sn = s2 * (1.0 - r);
+        if (!(v > 0.0) || !(sn > A) || !(sn < B) || !(r < 1.0)) {
+            // outside the bounds: halve them on the log scale (a far start,
+            // where the entropy is flat, drops 64-fold)
+            sn = isinf(B) ? 2.0 * fmax(A, s2) : (A > 0.0 ? sqrt(A * B) : B * (1.0 / 64.0));
+        }
+        if (sn == s2) break;
+        s2 = sn;
+        h = entropy_var(s2, v);
+        settle(s2, h);
+    }
+    // the bisection, as if every midpoint were evaluated
+    for (int s = 0; s < kAffMaxSteps; ++s) {
+        const double mid = 0.5 * (lo + hi);
+        if (mid <= lo || mid >= hi) break;
+        const bool below = mid <= A ? true : (mid >= B ? false : entropy(mid) < log_u);
+        if (below)
+            lo = mid;
+        else
+            hi = mid;
+    }
+    return hi;
 }
 
 // 1. the search; writes p_{j|i} in the neighbour order and sigma_i^2.  kPer
@@ -139,21 +223,9 @@ __global__ __launch_bounds__(kAffSearchBlock) void aff_search_kernel(const float
         mx = fmax(mx, dp[q]);
     }
     mx = uniform_d(wave_max_d(mx));
-    double lo = 0.0, hi = mx > 0.0 ? mx : 1.0;
-    if (mx > 0.0) {
-        // grow the top of the interval until the perplexity there reaches u
-        while (!isinf(hi) && row_entropy<kPer>(dp, k, hi) < log_u) hi *= 2.0;
-        if (!isinf(hi)) {
-            for (int s = 0; s < kAffMaxSteps; ++s) {
-                const double mid = 0.5 * (lo + hi);
-                if (mid <= lo || mid >= hi) break;
-                if (row_entropy<kPer>(dp, k, mid) < log_u)
-                    lo = mid;
-                else
-                    hi = mid;
-            }
-        }
-    }
+    const double hi = search_sigma2(
+        mx, log_u, [&](double s2) { return row_entropy<kPer>(dp, k, s2); },
+        [&](double s2, double &v) { return row_entropy<kPer, true>(dp, k, s2, &v); });
     // p_{j|i} at sigma^2 = hi
     const double inv = isinf(hi) ? 0.0 : 1.0 / (2.0 * hi);
     double w[kPer], s = 0.0;
@@ -287,14 +359,6 @@ __device__ __forceinline__ double row_entropy_quad(const double (&dp)[kPer], dou
     return log(sw) + kLn2 * tw / sw;
 }
 
-// Margin of the entropy, in nats, beyond which a comparison with log u is
-// taken as settled: the evaluation's rounding (up to 128 terms summed in
-// fp64, each within a few ulps, then a log and a quotient of at most about
-// ten) stays below 3e-13, so a point whose computed entropy is more than
-// kAffMargin below log u has every smaller sigma^2 below it too (the entropy
-// increases with sigma^2), and likewise above.
-constexpr double kAffMargin = 1e-11;
-constexpr int kAffNewtonMax = 12;
 
 template <int kPer>
 __device__ __forceinline__ void search_row_quad(const float *__restrict__ dist, int64_t i, int g, int k,
@@ -328,64 +392,9 @@ __device__ __forceinline__ void search_row_quad(const float *__restrict__ dist, 
     mx = quad_max(mx);
     // from here on the slots hold d'^2 / ln 2, so that a / ln 2 = slot / 2 sigma^2
     StaticFor<0, kPer>::run([&](auto qc) { dp[decltype(qc)::value] *= kLog2e; });
-    auto entropy = [&](double s2) { return row_entropy_quad<kPer>(dp, s2); };
-    auto entropy_var = [&](double s2, double &v) { return row_entropy_quad<kPer, true>(dp, s2, &v); };
-    double lo = 0.0, hi = mx > 0.0 ? mx : 1.0;
-    if (mx > 0.0) {
-        // Settled bounds: every sigma^2 <= A has entropy below log u and every
-        // sigma^2 >= B at or above it, by more than the margin at A and B.
-        double A = 0.0, B = INFINITY, h = 0.0, v = 0.0;
-        auto settle = [&](double s2, double hs) {
-            if (hs < log_u - kAffMargin) A = fmax(A, s2);
-            else if (hs > log_u + kAffMargin) B = fmin(B, s2);
-        };
-        // grow the top of the interval until the perplexity there reaches u
-        for (;;) {
-            if (isinf(hi)) break;
-            h = entropy_var(hi, v);
-            settle(hi, h);
-            if (h >= log_u) break;
-            hi *= 2.0;
-        }
-        if (!isinf(hi)) {
-            // Newton's method on ln sigma^2 (dH / d ln sigma^2 = v), kept inside
-            // the settled bounds, to bring them close around the root; then,
-            // from a point within the margin, one probe on either side.  The
-            // bounds only spare evaluations below: the bisection's outcome
-            // does not depend on them.
-            double s2 = hi;
-            for (int it = 0; it < kAffNewtonMax && B > A; ++it) {
-                const double r = (h - log_u) / v;
-                if (fabs(h - log_u) <= kAffMargin) {
-                    const double d = v > 0.0 ? fmin(4.0 * kAffMargin / v, 0.25) : 0.25;
-                    const double sa = s2 * (1.0 - d), sb = s2 * (1.0 + d);
-                    settle(sa, entropy(sa));
-                    settle(sb, entropy(sb));
-                    break;
-                }
-                double sn = s2 * (1.0 - r);
-                if (!(v > 0.0) || !(sn > A) || !(sn < B) || !(r < 1.0)) {
-                    // outside the bounds: halve them on the log scale (a far
-                    // start, where the entropy is flat, drops 64-fold)
-                    sn = isinf(B) ? 2.0 * fmax(A, s2) : (A > 0.0 ? sqrt(A * B) : B * (1.0 / 64.0));
-                }
-                if (sn == s2) break;
-                s2 = sn;
-                h = entropy_var(s2, v);
-                settle(s2, h);
-            }
-            // the bisection, as if every step were evaluated
-            for (int s = 0; s < kAffMaxSteps; ++s) {
-                const double mid = 0.5 * (lo + hi);
-                if (mid <= lo || mid >= hi) break;
-                const bool below = mid <= A ? true : (mid >= B ? false : entropy(mid) < log_u);
-                if (below)
-                    lo = mid;
-                else
-                    hi = mid;
-            }
-        }
-    }
+    const double hi = search_sigma2(
+        mx, log_u, [&](double s2) { return row_entropy_quad<kPer>(dp, s2); },
+        [&](double s2, double &v) { return row_entropy_quad<kPer, true>(dp, s2, &v); });
     // p_{j|i} at sigma^2 = hi
     const double inv = isinf(hi) ? 0.0 : 1.0 / (2.0 * hi);
     double sw = 0.0;
