@@ -819,6 +819,34 @@ int bhtsne_debug_tree_3d(const float *Y, int64_t n, float theta, int64_t *n_node
     return flags_status(h.flags);
 }
 
+// The end of a layout build: its status, the device flags of the build's
+// sort, and the handle (the forms the plan allows and the switches leave on;
+// 3-D layouts have no windowed segments).
+static int finish_layout(int built, const TilePlan &plan, int64_t n, int64_t nnz, void *layout_mem,
+                         size_t layout_bytes, uint64_t magic, bhtsne_layout *out, void *workspace, hipStream_t stream)
+{
+    if (built == 1) return BHTSNE_EINPUT;
+    if (built != 0) return BHTSNE_EDEVICE;
+    Header h;
+    const int rc = read_header(workspace, &h, stream);
+    if (rc != BHTSNE_OK) return rc;
+    if (h.flags & (kErrLookback | kErrRange)) return BHTSNE_EDEVICE;
+    out->n = n;
+    out->nnz = nnz;
+    out->mem = layout_mem;
+    out->bytes = layout_bytes;
+    out->order = plan.order;
+    const bool tiled = plan.tiled && tile_path_enabled();
+    out->tiles = tiled ? plan.tiles : 0;
+    out->items = tiled ? plan.items : 0;
+    out->entries = tiled ? plan.entries : 0;
+    const bool windowed = magic != kLayoutMagic3 && !tiled && plan.windows > 0 && window_path_enabled();
+    out->windows = windowed ? plan.windows : 0;
+    out->segments = windowed ? plan.segments : 0;
+    out->magic = magic;
+    return BHTSNE_OK;
+}
+
 size_t bhtsne_layout_size_3d(int64_t n, int64_t nnz)
 {
     if (n < 2 || n > kMaxPoints || nnz < 0) return 0;
@@ -840,25 +868,7 @@ int bhtsne_layout_build_3d(const bhtsne_csr *P, const float *Y, void *layout_mem
     TilePlan plan;
     const int built = launch_layout_build<float, 3>(P->row_ptr, P->col, P->val, P->n, P->nnz, Y, kOrderAuto, lv,
                                                     &plan, workspace, L, stream);
-    if (built == 1) return BHTSNE_EINPUT;
-    if (built != 0) return BHTSNE_EDEVICE;
-    Header h;
-    rc = read_header(workspace, &h, stream);
-    if (rc != BHTSNE_OK) return rc;
-    if (h.flags & (kErrLookback | kErrRange)) return BHTSNE_EDEVICE;
-    out->n = P->n;
-    out->nnz = P->nnz;
-    out->mem = layout_mem;
-    out->bytes = layout_bytes;
-    out->order = plan.order;
-    const bool tiled = plan.tiled && tile_path_enabled();
-    out->tiles = tiled ? plan.tiles : 0;
-    out->items = tiled ? plan.items : 0;
-    out->entries = tiled ? plan.entries : 0;
-    out->windows = 0;
-    out->segments = 0;
-    out->magic = kLayoutMagic3;
-    return BHTSNE_OK;
+    return finish_layout(built, plan, P->n, P->nnz, layout_mem, layout_bytes, kLayoutMagic3, out, workspace, stream);
 }
 
 static int check_layout3_step(const bhtsne_layout *layout, const float *Y, float theta, float exaggeration,
@@ -933,26 +943,7 @@ int bhtsne_layout_build_ordered(const bhtsne_csr *P, const float *Y, int order, 
     TilePlan plan;
     const int built = launch_layout_build<float, 2>(P->row_ptr, P->col, P->val, P->n, P->nnz, Y, order, lv, &plan,
                                                     workspace, L, stream);
-    if (built == 1) return BHTSNE_EINPUT;
-    if (built != 0) return BHTSNE_EDEVICE;
-    Header h;
-    rc = read_header(workspace, &h, stream);
-    if (rc != BHTSNE_OK) return rc;
-    if (h.flags & (kErrLookback | kErrRange)) return BHTSNE_EDEVICE;
-    out->n = P->n;
-    out->nnz = P->nnz;
-    out->mem = layout_mem;
-    out->bytes = layout_bytes;
-    out->order = plan.order;
-    const bool tiled = plan.tiled && tile_path_enabled();
-    out->tiles = tiled ? plan.tiles : 0;
-    out->items = tiled ? plan.items : 0;
-    out->entries = tiled ? plan.entries : 0;
-    const bool windowed = !tiled && plan.windows > 0 && window_path_enabled();
-    out->windows = windowed ? plan.windows : 0;
-    out->segments = windowed ? plan.segments : 0;
-    out->magic = kLayoutMagic;
-    return BHTSNE_OK;
+    return finish_layout(built, plan, P->n, P->nnz, layout_mem, layout_bytes, kLayoutMagic, out, workspace, stream);
 }
 
 size_t bhtsne_layout_size_f64(int64_t n, int64_t nnz)
@@ -976,26 +967,8 @@ int bhtsne_layout_build_f64(const bhtsne_csr_f64 *P, const double *Y, void *layo
     TilePlan plan;
     const int built = launch_layout_build<double, 2>(P->row_ptr, P->col, P->val, P->n, P->nnz, Y, kOrderAuto, lv,
                                                      &plan, workspace, L, stream);
-    if (built == 1) return BHTSNE_EINPUT;
-    if (built != 0) return BHTSNE_EDEVICE;
-    Header h;
-    rc = read_header(workspace, &h, stream);
-    if (rc != BHTSNE_OK) return rc;
-    if (h.flags & (kErrLookback | kErrRange)) return BHTSNE_EDEVICE;
-    out->n = P->n;
-    out->nnz = P->nnz;
-    out->mem = layout_mem;
-    out->bytes = layout_bytes;
-    out->order = plan.order;
-    const bool tiled = plan.tiled && tile_path_enabled();
-    out->tiles = tiled ? plan.tiles : 0;
-    out->items = tiled ? plan.items : 0;
-    out->entries = tiled ? plan.entries : 0;
-    const bool windowed = !tiled && plan.windows > 0 && window_path_enabled();
-    out->windows = windowed ? plan.windows : 0;
-    out->segments = windowed ? plan.segments : 0;
-    out->magic = kLayoutMagic64;
-    return BHTSNE_OK;
+    return finish_layout(built, plan, P->n, P->nnz, layout_mem, layout_bytes, kLayoutMagic64, out, workspace,
+                         stream);
 }
 
 static int check_layout64_step(const bhtsne_layout *layout, const double *Y, double theta, double exaggeration,
