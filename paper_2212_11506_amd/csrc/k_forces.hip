@@ -148,16 +148,16 @@ __device__ inline void repulsive_walk3(const char *nbase, uint32_t end, float3 y
     }
 }
 
-// 1/x in fp64 for x >= 1: the hardware's approximate reciprocal refined by
-// two Newton-Raphson steps r <- r + r (1 - x r), each of which squares the
-// relative error, so the result is within about an ulp of the quotient (the
-// IEEE division sequence costs twice the instructions); 1/inf stays 0.
+// 1/x in fp64 for x >= 1: the hardware's approximate reciprocal (measured on
+// gfx950 within 2^-24.4 relative over x in [1, 1e8]) refined by one
+// Newton-Raphson step r <- r + r (1 - x r), which squares the relative error:
+// within 2^-48.7 (11 ulps) of the quotient, so a weight and its square carry
+// below 5e-15 relative error, and Z, a sum of positive weights, no more (the
+// IEEE division sequence costs three times the instructions); 1/inf stays 0.
 __device__ inline double recip(double x)
 {
-    double r = __builtin_amdgcn_rcp(x);
-    r = fma(r, fma(-x, r, 1.0), r);
-    r = fma(r, fma(-x, r, 1.0), r);
-    return x != __builtin_huge_val() ? r : 0.0;
+    const double r = __builtin_amdgcn_rcp(x);
+    return x != __builtin_huge_val() ? fma(r, fma(-x, r, 1.0), r) : 0.0;
 }
 __device__ inline float recip(float x) { return fast_rcp(x); }
 
