@@ -237,7 +237,8 @@ int device_cus()
 // Blocks of the persistent sliced attractive kernel (one per CU it holds):
 // all CUs when it runs alone; beside the tree phases a share of them
 // (BHTSNE_ATTRACT_CUS, percent of the CUs, default 75), so that the critical
-// path keeps CUs of its own; 0 gives one block per item.
+// path keeps CUs of its own; 0 gives one block per item (the windowed
+// segments, which have no items, then take all CUs).
 int attract_blocks(bool beside, int items)
 {
     static int pct = [] {
@@ -245,7 +246,7 @@ int attract_blocks(bool beside, int items)
         int x = e ? std::atoi(e) : 75;
         return x < 0 ? 0 : (x > 100 ? 100 : x);
     }();
-    if (beside && pct == 0) return items > 0 ? items : 1;
+    if (beside && pct == 0) return items > 0 ? items : device_cus();
     const int cus = device_cus();
     const int b = beside ? cus * pct / 100 : cus;
     return b < 1 ? 1 : b;
