@@ -237,8 +237,9 @@ int device_cus()
 // Blocks of the persistent sliced attractive kernel (one per CU it holds):
 // all CUs when it runs alone; beside the tree phases a share of them
 // (BHTSNE_ATTRACT_CUS, percent of the CUs, default 75), so that the critical
-// path keeps CUs of its own; 0 gives one block per item (the windowed
-// segments, which have no items, then take all CUs).
+// path keeps CUs of its own; 0 gives one block per item.  The windowed
+// segments (no items) take all CUs: without tile locality the attraction is
+// the longest phase (at 5M points 9.5 ms on 75% against 3.9 for the walk).
 int attract_blocks(bool beside, int items)
 {
     static int pct = [] {
@@ -246,7 +247,8 @@ int attract_blocks(bool beside, int items)
         int x = e ? std::atoi(e) : 75;
         return x < 0 ? 0 : (x > 100 ? 100 : x);
     }();
-    if (beside && pct == 0) return items > 0 ? items : device_cus();
+    if (items <= 0) return device_cus();
+    if (beside && pct == 0) return items;
     const int cus = device_cus();
     const int b = beside ? cus * pct / 100 : cus;
     return b < 1 ? 1 : b;
