@@ -52,20 +52,33 @@ constexpr uint32_t kNodeCell = 0xFFFFFFFFu;
 constexpr int64_t kMaxPoints = (int64_t(1) << 24) - 1;
 constexpr int64_t kYPad = 16384 + 2;                   // padding points after the private copy of Y
 // tiled attractive step: rows in blocks of kTileRows, columns in segments of
-// kTileSeg points; row blocks spanning more than kTileMaxSeg segments keep the
-// row-block kernel
+// kTileSeg points; row blocks spanning more than max_tiles_per_block segments
+// keep the row-block kernel
 constexpr int kTileRows = 1024;
 constexpr int kTileSeg = 16384; // 128 KB of Y in LDS
 constexpr int kTileMaxSeg = 16;
 // Column windows of a sliced copy (points of Y held in LDS) and the tiles a
 // row block may span: 16384 fp32 2-D points (128 KB), 8192 fp64 2-D points
 // (128 KB) or 8192 3-D points (96 KB); the narrower windows take twice as many
-// tiles, so every form covers the same column span.
+// tiles, so every form covers the same column span of 2^18 points.
 constexpr int window_points_of(int vbytes, int dim) { return vbytes == 4 && dim == 2 ? kTileSeg : kTileSeg / 2; }
-constexpr int max_tiles_per_block(int vbytes, int dim = 2)
+constexpr int narrow_tiles_per_block(int vbytes, int dim = 2)
 {
     return kTileMaxSeg * (kTileSeg / window_points_of(vbytes, dim));
 }
+// fp32 2-D row blocks may also span up to kTileWideSeg windows (2^21 points, a
+// large cluster's rows) when the layout's tiles hold at least
+// kTileWideEntries entries on average (four per row): sparser tiles cost more
+// in partials and padding than another order or the windowed segments
+constexpr int kTileWideSeg = 128;
+constexpr int64_t kTileWideEntries = 4096;
+constexpr int max_tiles_per_block(int vbytes, int dim = 2)
+{
+    return vbytes == 4 && dim == 2 ? kTileWideSeg : narrow_tiles_per_block(vbytes, dim);
+}
+// partial sums: kTileSlots per row, so a layout has at most kTileSlots tiles
+// per row block on average
+constexpr int kTileSlots = 32;
 constexpr int kItemMaxTiles = 128; // tiles of one segment handled by one block
 // sliced copy of a tile: 64 rows per slice (one per lane), chunks of 4 entries per lane
 constexpr int kSellSlice = 64;
@@ -162,10 +175,10 @@ inline Layout make_layout(int64_t n, int64_t nnz, int fbytes = 4, int dim = 2)
     L.nodes = take((dim == 3 ? kNodeBytes3 : (fbytes == 8 ? kNodeBytes64 : kNodeBytes)) * size_t(2 * n) + 8);
     L.frep = take(size_t(dim) * size_t(fbytes) * size_t(n));
     L.fattr = take(size_t(dim) * size_t(fbytes) * size_t(n));
-    // partial attractive sums, one per (tile, sorted row slot): up to
-    // max_tiles_per_block tiles of kTileRows rows per row block
+    // partial attractive sums, one per (tile, sorted row slot): kTileSlots
+    // tiles of kTileRows rows per row block
     L.partial = take(size_t(dim) * size_t(fbytes) * size_t((n + kTileRows - 1) / kTileRows) * kTileRows *
-                     size_t(max_tiles_per_block(fbytes, dim)));
+                     size_t(kTileSlots));
     L.zpart = take(8 * size_t(L.rep_blocks));
     const int64_t zb = (n + kZEvalPoints - 1) / kZEvalPoints;
     L.eval_part = take(8 * size_t(zb > kEvalMaxBlocks ? zb : kEvalMaxBlocks));

@@ -461,7 +461,8 @@ __device__ inline int64_t row_lower_bound(const int32_t *__restrict__ col, int64
 }
 
 // Run length (entries in the tile's segment) of every (row, tile) of the tiled
-// row blocks; one wave per row, one lane per segment of the row's block.
+// row blocks; one wave per row, one lane per segment of the row's block (a
+// lane takes segments 64 apart in a block that spans more).
 // Rows past n get empty runs.
 template <int kSeg, int kMaxSeg>
 __global__ __launch_bounds__(256) void tile_run_len_kernel(const int64_t *__restrict__ row_ptr,
@@ -476,14 +477,15 @@ __global__ __launch_bounds__(256) void tile_run_len_kernel(const int64_t *__rest
          r += int64_t(gridDim.x) * (blockDim.x / kWave)) {
         const int64_t b = r / kTileRows, rl = r % kTileRows;
         const int ns = nseg[b];
-        if (lane >= ns) continue;
-        int32_t len = 0;
-        if (r < n) {
-            const int64_t a = row_ptr[r], e = row_ptr[r + 1];
-            const int32_t s0 = (seg_lo[b] + lane) * kSeg;
-            len = int32_t(row_lower_bound(col, a, e, s0 + kSeg) - row_lower_bound(col, a, e, s0));
+        for (int k = lane; k < ns; k += kWave) {
+            int32_t len = 0;
+            if (r < n) {
+                const int64_t a = row_ptr[r], e = row_ptr[r + 1];
+                const int32_t s0 = (seg_lo[b] + k) * kSeg;
+                len = int32_t(row_lower_bound(col, a, e, s0 + kSeg) - row_lower_bound(col, a, e, s0));
+            }
+            run_len[int64_t(blk_tiles[b * kMaxSeg + k]) * kTileRows + rl] = len;
         }
-        run_len[int64_t(blk_tiles[b * kMaxSeg + lane]) * kTileRows + rl] = len;
     }
 }
 
@@ -1234,14 +1236,16 @@ LayoutView layout_view(void *mem, int64_t n, int64_t nnz, int vbytes, int dim)
     // rows are padded to multiples of 4 entries, plus one 4-entry sentinel vector at the end
     const size_t cap = size_t(nnz) + 3 * size_t(n) + 4;
     size_t o_col = take(4 * cap), o_val = take(size_t(vbytes) * cap);
-    // tiled copy: at most max_tiles_per_block tiles per row block, sliced
+    // tiled copy: at most max_tiles_per_block tiles per row block and
+    // kTileSlots per row block in all (the partial sums' slots), sliced
     const int64_t blocks = (n + kTileRows - 1) / kTileRows;
     const int max_seg = max_tiles_per_block(vbytes, dim);
-    v.max_tiles = blocks * max_seg;
+    v.max_tiles = blocks * kTileSlots;
     // the sliced copy pads every run to its slice's longest run, rounded up to
     // whole chunks; it is built only when that fits in a quarter of nnz plus
-    // one chunk per slice (else the row-block kernel is used)
-    v.max_entries = nnz + nnz / 4 + int64_t(kSellChunk) * kSlicesPerTile * v.max_tiles + kSellChunk;
+    // one chunk per slice of the narrow span's tiles (else another kernel is used)
+    v.max_entries = nnz + nnz / 4 +
+                    int64_t(kSellChunk) * kSlicesPerTile * blocks * narrow_tiles_per_block(vbytes, dim) + kSellChunk;
     const int64_t max_units = v.max_tiles * kSlicesPerTile;
     size_t o_lo = take(4 * size_t(blocks)), o_ns = take(4 * size_t(blocks)),
            o_bt = take(4 * size_t(blocks) * max_seg), o_tb = take(4 * size_t(v.max_tiles)),
@@ -1295,12 +1299,17 @@ LayoutView layout_view(void *mem, int64_t n, int64_t nnz, int vbytes, int dim)
 }
 
 // The tiled copy of a built (sorted, padded) layout; plan->tiled stays false when
-// some row block spans more than max_tiles_per_block segments.
+// some row block spans more than max_tiles_per_block segments, when the tiles
+// outnumber the partial slots (kTileSlots per row block), when a row block
+// spans more than the narrow limit while the tiles hold fewer than
+// kTileWideEntries entries on average, or when the padding is too large.
 template <typename T, int D>
-static int build_tiles(const LayoutView &lv, int64_t n, TilePlan *plan, void *ws, const Layout &L, hipStream_t st)
+static int build_tiles(const LayoutView &lv, int64_t n, int64_t nnz, TilePlan *plan, void *ws, const Layout &L,
+                       hipStream_t st)
 {
     constexpr int kSeg = window_points<T, D>();
     constexpr int kMaxSeg = max_tiles_per_block(sizeof(T), D);
+    constexpr int kNarrow = narrow_tiles_per_block(sizeof(T), D);
     T *tval = sizeof(T) == 4 ? reinterpret_cast<T *>(lv.tval) : reinterpret_cast<T *>(lv.tval64);
     const T *val = sizeof(T) == 4 ? reinterpret_cast<const T *>(lv.val) : reinterpret_cast<const T *>(lv.val64);
     *plan = TilePlan{};
@@ -1320,12 +1329,15 @@ static int build_tiles(const LayoutView &lv, int64_t n, TilePlan *plan, void *ws
     // tiles in segment-major order, (block, k) -> tile, then items of up to
     // `per` tiles that never straddle a segment (a few items per CU)
     std::vector<std::pair<int32_t, int32_t>> order; // (segment, block)
+    bool wide = false;
     for (int64_t b = 0; b < blocks; ++b) {
         if (ns[b] > kMaxSeg) return 0; // too wide: keep the row-block kernel
+        wide |= ns[b] > kNarrow;
         for (int k = 0; k < ns[b]; ++k) order.emplace_back(lo[b] + k, int32_t(b));
     }
     const int64_t tiles = int64_t(order.size());
     if (tiles == 0 || tiles > lv.max_tiles) return 0;
+    if (wide && nnz < tiles * kTileWideEntries) return 0; // wide and sparse
     std::sort(order.begin(), order.end());
     std::vector<int32_t> bt(size_t(blocks) * kMaxSeg, -1), tb(tiles), ts(tiles), tk(tiles);
     for (int64_t t = 0; t < tiles; ++t) {
@@ -1624,7 +1636,7 @@ int launch_layout_build(const int64_t *row_ptr, const int32_t *col, const V *val
     if (relabel<V, D>(row_ptr, col, val, n, nnz, Y, chosen, lv, ws, L, st) != 0) return -1;
     *plan = TilePlan{};
     {
-        int rc = build_tiles<V, D>(lv, n, plan, ws, L, st);
+        int rc = build_tiles<V, D>(lv, n, nnz, plan, ws, L, st);
         if (rc != 0) return rc;
         if (plan->tiled) {
             plan->order = chosen;
@@ -1638,7 +1650,7 @@ int launch_layout_build(const int64_t *row_ptr, const int32_t *col, const V *val
             if (rc < 0) return -1;
             if (rc == 1) {
                 if (relabel<V, D>(row_ptr, col, val, n, nnz, Y, kOrderBfs, lv, ws, L, st) != 0) return -1;
-                rc = build_tiles<V, D>(lv, n, plan, ws, L, st);
+                rc = build_tiles<V, D>(lv, n, nnz, plan, ws, L, st);
                 if (rc != 0) return rc;
                 if (plan->tiled) {
                     plan->order = kOrderBfs;

@@ -4,11 +4,14 @@ library lays it out, and checking its sliced copy against P (shared by the
 import numpy as np
 import scipy.sparse as sp
 
-TILE_ROWS, TILE_SEG, TILE_MAX_SEG, ITEM_MAX_TILES = 1024, 16384, 16, 128
+TILE_ROWS, TILE_SEG, ITEM_MAX_TILES = 1024, 16384, 128
+# tiles a row block may span (fp32 2-D: 16 always, up to 128 when the tiles are
+# dense) and partial slots per row (so at most 32 tiles per row block on average)
+TILE_MAX_SEG, TILE_NARROW_SEG, TILE_SLOTS, TILE_WIDE_ENTRIES = 128, 16, 32, 4096
 SLICE, SLICES, CHUNK = 64, 16, 256  # rows per unit, units per tile, entries per chunk
 
 
-def layout_arrays(lay, tiles=False, max_seg=None):
+def layout_arrays(lay, tiles=False, max_seg=None, narrow=None):
     """perm, rank, row_ptr, col, val of a layout (and the tile tables), read back
     from device memory in the order the library lays them out."""
     n, nnz = lay.n, lay.nnz
@@ -30,10 +33,11 @@ def layout_arrays(lay, tiles=False, max_seg=None):
     if not tiles:
         return perm, rank, rp, col, val
     max_seg = TILE_MAX_SEG if max_seg is None else max_seg
+    narrow = TILE_NARROW_SEG if narrow is None else narrow
     blocks = (n + TILE_ROWS - 1) // TILE_ROWS
-    max_tiles = blocks * max_seg
+    max_tiles = blocks * TILE_SLOTS
     max_units = max_tiles * SLICES
-    max_entries = nnz + nnz // 4 + CHUNK * SLICES * max_tiles + CHUNK
+    max_entries = nnz + nnz // 4 + CHUNK * SLICES * blocks * narrow + CHUNK
     t = dict(seg_lo=take(4 * blocks, np.int32, blocks), nseg=take(4 * blocks, np.int32, blocks))
     t["blk_tiles"] = take(4 * blocks * max_seg, np.int32, blocks * max_seg).reshape(blocks, max_seg)
     for k in ("tile_blk", "tile_seg", "tile_k"):
@@ -51,11 +55,13 @@ def layout_arrays(lay, tiles=False, max_seg=None):
     return (perm, rank, rp, col, val), t
 
 
-def check_sliced_copy(lay, row_ptr, col_in, val_in, seg=TILE_SEG, max_seg=TILE_MAX_SEG):
+def check_sliced_copy(lay, row_ptr, col_in, val_in, seg=TILE_SEG, max_seg=TILE_MAX_SEG, narrow=TILE_NARROW_SEG):
     """The tile tables of a tiled layout are consistent and its sliced copy
-    (columns as offsets in windows of `seg` points) holds exactly P, relabelled."""
+    (columns as offsets in windows of `seg` points) holds exactly P, relabelled.
+    max_seg: tiles a row block may span; narrow: the span whose tiles bound the
+    padding."""
     n = lay.n
-    (perm, rank, rp, col, val), tt = layout_arrays(lay, tiles=True, max_seg=max_seg)
+    (perm, rank, rp, col, val), tt = layout_arrays(lay, tiles=True, max_seg=max_seg, narrow=narrow)
     T, I = lay.tiles, lay.items
     seg_lo, nseg, tile_blk, tile_seg = (tt[k] for k in ("seg_lo", "nseg", "tile_blk", "tile_seg"))
     blocks = (n + TILE_ROWS - 1) // TILE_ROWS

@@ -377,7 +377,7 @@ def test_layout3_sliced_copy_is_p():
     P = bh.Csr.from_numpy(inp.row_ptr, inp.col, inp.val)
     lay = bh.Layout3(P, dev_y(inp.Y))
     assert lay.tiles > 0
-    check_sliced_copy(lay, inp.row_ptr, inp.col, inp.val, seg=8192, max_seg=32)
+    check_sliced_copy(lay, inp.row_ptr, inp.col, inp.val, seg=8192, max_seg=32, narrow=32)
 
 
 def test_layout3_takes_the_breadth_first_order_when_morton_gives_no_tiles():

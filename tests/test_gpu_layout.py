@@ -32,7 +32,8 @@ def rel_l2(a, b):
 
 
 from layout_tables import (CHUNK, ITEM_MAX_TILES, SLICE, SLICES, TILE_MAX_SEG, TILE_ROWS,  # noqa: E402,F401
-                           TILE_SEG, check_sliced_copy)
+                           TILE_NARROW_SEG, TILE_SEG, TILE_SLOTS, TILE_WIDE_ENTRIES,
+                           check_sliced_copy)
 from layout_tables import bfs_perm as _bfs_perm  # noqa: E402
 from layout_tables import layout_arrays as _layout_arrays  # noqa: E402
 
@@ -55,9 +56,9 @@ def _tcol_offset(n, nnz):
     for nbytes in (4 * n, 4 * n, 8 * (n + 1), 4 * cap, 4 * cap):
         take(nbytes)
     blocks = (n + TILE_ROWS - 1) // TILE_ROWS
-    max_tiles = blocks * TILE_MAX_SEG
+    max_tiles = blocks * TILE_SLOTS
     max_units = max_tiles * SLICES
-    max_entries = nnz + nnz // 4 + CHUNK * SLICES * max_tiles + CHUNK
+    max_entries = nnz + nnz // 4 + CHUNK * SLICES * blocks * TILE_NARROW_SEG + CHUNK
     for nbytes in (4 * blocks, 4 * blocks, 4 * blocks * TILE_MAX_SEG, 4 * max_tiles, 4 * max_tiles, 4 * max_tiles,
                    8 * max_tiles, 4 * max_tiles * TILE_ROWS, 2 * max_tiles * TILE_ROWS, 2 * max_tiles * TILE_ROWS,
                    4 * max_units, 4 * max_units, 4 * max_units, 4 * max_units, 16 * max_tiles, 16 * max_tiles * 16):
@@ -324,6 +325,43 @@ def test_wide_row_blocks_fall_back_to_row_blocks_without_windows():
     assert _subprocess_gradient({"BHTSNE_WINDOWS": "0"}, wide=True) == 4
 
 
+def test_wide_dense_row_blocks_take_the_sliced_copy():
+    """Uniform random neighbours (48 drawn per row, about 96 per row after
+    symmetrisation) over 300,000 points with a random Y: a block of 1024 rows
+    in Morton order reaches all 19 column windows of 16384 points, more than
+    the 16 every layout may tile, but its tiles hold about 5,200 entries each
+    (a wide layout needs 4,096 on average) and 19 tiles per row block fit the
+    32 partial slots per row.  So the sliced copy is built over 19 windows per
+    row block, holds exactly P, and the gradient matches the oracle.  With six
+    neighbours per row (the tests above) the tiles are too sparse and the
+    windowed segments serve the layout."""
+    n, k = 300_000, 48
+    rng = np.random.default_rng(51)
+    rows = np.repeat(np.arange(n), k)
+    cols = rng.integers(0, n - 1, size=rows.size)
+    cols += cols >= rows  # no self-pairs
+    A = sp.csr_matrix((rng.uniform(0.1, 1.0, rows.size), (rows, cols)), shape=(n, n))
+    A = (A + A.T).tocsr()
+    A.sum_duplicates()
+    A.sort_indices()
+    A.data /= A.data.sum()
+    rp, col, val = A.indptr.astype(np.int64), A.indices.astype(np.int32), A.data.astype(np.float32)
+    y = synth.random_y(n, seed=51, scale=3.0)
+    Y = torch.from_numpy(np.ascontiguousarray(y)).cuda()
+    lay = bh.Layout(bh.Csr.from_numpy(rp, col, val), Y)
+    blocks, windows = (n + TILE_ROWS - 1) // TILE_ROWS, (n + TILE_SEG - 1) // TILE_SEG
+    say(f"[wide] n={n} nnz={col.size}: order {lay.order}, tiles {lay.tiles}, items {lay.items}, "
+        f"entries {lay.entries}, windows {lay.windows}")
+    assert lay.order == bh.ORDER_MORTON and lay.tiles == blocks * windows and lay.windows == 0
+    assert windows > 16 and col.size >= TILE_WIDE_ENTRIES * lay.tiles
+    check_sliced_copy(lay, rp, col, val)
+    g, Z = bh.gradient(Y, lay, 0.5, 12.0)
+    go, Zo, _, _ = oracle.gradient(y, rp, col, val, 0.5, 12.0)
+    err = rel_l2(g.cpu().numpy(), go)
+    say(f"[wide] rel-L2 {err:.2e}, Z rel {abs(Z - Zo) / Zo:.2e}")
+    assert err <= 1e-3 and abs(Z - Zo) <= 1e-5 * Zo
+
+
 def test_rows_longer_than_the_row_sort_keep_the_row_block_kernel():
     """A row of 9000 entries is longer than the layout's in-LDS row sort takes,
     so its columns stay out of window order: no segments are built, the
@@ -424,9 +462,12 @@ def test_windowed_segments_are_p_and_match_the_oracle(case):
 def test_bfs_order_tiles_a_geometric_p_from_a_random_y(blobs):
     """P from the 30 nearest neighbours of 400,000 points uniform in the unit
     square (one component; two squares apart: two), Y a random initial
-    embedding.  Morton order of Y brings nothing together (a block of 1024
-    rows then reaches all 25 column windows, more than the 16 a tile row
-    allows), so the automatic build takes the breadth-first levels of P's
+    embedding.  Morton order of Y brings nothing together: a block of 1024
+    rows then reaches all 25 column windows of its component (one component:
+    about 1,330 entries per tile; two: 13 windows, 25 for the block across
+    both, about 2,550 entries per tile), more than 16 and too sparse for a
+    wide layout (4,096 entries per tile).  So the automatic build takes the
+    breadth-first levels of P's
     graph (250 or 180 levels of at most 3,700 points: a row block reaches two
     windows): the sliced tiles engage.  The copy's order is exactly
     (component, level, index), and both layouts give the oracle's
