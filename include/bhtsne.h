@@ -181,7 +181,7 @@ int bhtsne_step_noalloc(float *Y, const bhtsne_csr *P, float theta, float exagge
                         hipStream_t stream);
 
 /* Bytes of device memory a layout of P needs (0 if n or nnz is out of range):
- * about 15.5 bytes per stored entry + 560 bytes per point (a row-sorted copy,
+ * about 15.5 bytes per stored entry + 700 bytes per point (a row-sorted copy,
  * and room for a sliced copy with 16-bit column offsets and its tables). */
 size_t bhtsne_layout_size(int64_t n, int64_t nnz);
 
@@ -191,14 +191,16 @@ size_t bhtsne_layout_size(int64_t n, int64_t nnz);
  * the Morton order does not (bhtsne_layout_build_ordered, BHTSNE_ORDER_AUTO);
  * the copy stores P's rows in that order with renumbered columns, so the
  * columns of consecutive rows fall into compact index windows.  When every
- * block of 1024 rows spans at most 16 windows of 16384 columns, a second,
- * sliced copy is built: for each (row block, window) tile the rows are sorted
- * by their number of entries in the window and cut into slices of 64 rows,
+ * block of 1024 rows spans at most 16 windows of 16384 columns, or at most
+ * 128 with at most 32 tiles per row block on average holding at least 4096
+ * entries each on average (the rows of large clusters), a second, sliced
+ * copy is built: for each (row block, window) tile the rows are sorted by
+ * their number of entries in the window and cut into slices of 64 rows,
  * stored entry-major, so that one window of Y in LDS serves many tiles and
  * every load is contiguous (out->tiles > 0, out->items > 0).  The copy is
  * skipped when its padding would exceed a quarter of nnz plus one chunk per
- * slice.  Without that copy (rows whose neighbours spread over a large
- * component), the build lists instead, for each column window of 2^18
+ * slice of 16 tiles per row block.  Without that copy (rows whose neighbours
+ * spread sparsely over a large component), the build lists instead, for each column window of 2^18
  * points, the (row, entry range) segments of the rows with entries there
  * (out->windows > 0; out->segments = 0 for a P with no entries): the
  * attraction then takes one pass per window, with that window of Y held in
