@@ -169,7 +169,7 @@ int bhtsne_step(float *Y, const bhtsne_csr *P, float theta, float exaggeration, 
  * array of bhtsne_noalloc_max_bytes() bytes (64 MiB) in the library's device
  * image, one per GPU, reserved when the library is loaded and held until the
  * process ends; the call allocates nothing.  Sizes whose
- * bhtsne_workspace_size(n, nnz) exceeds it (n above about 249,000 points)
+ * bhtsne_workspace_size(n, nnz) exceeds it (n above about 168,000 points)
  * are BHTSNE_EINVAL.  Every call on a GPU shares that GPU's array: calls
  * that may overlap on one GPU (different streams or threads) race and must
  * be serialised by the caller; the kernels clear every counter they need,
