@@ -111,12 +111,13 @@ int read_header(const void *ws, Header *h, hipStream_t st)
     return BHTSNE_OK;
 }
 
-// Box and codes.  `rank` (nullable) puts the private copy of Y in a layout's order.
-void build_codes(const float *Y, int64_t n, const uint32_t *rank, void *ws, const Layout &L, hipStream_t st)
+// Box and codes.  `perm` (nullable; a layout's position -> caller's index)
+// puts the private copy of Y in the layout's order.
+void build_codes(const float *Y, int64_t n, const uint32_t *perm, void *ws, const Layout &L, hipStream_t st)
 {
     PhaseTimer pt(BHTSNE_PHASE_BBOX_MORTON, st);
     launch_bbox(Y, n, ws, L, st);
-    launch_morton(Y, n, rank, ws, L, st);
+    launch_morton(Y, n, perm, ws, L, st);
 }
 
 // Sort, tree and summaries.
@@ -133,10 +134,10 @@ void build_sorted_tree(const float *Y, int64_t n, float theta, void *ws, const L
     }
 }
 
-void build_tree(const float *Y, int64_t n, float theta, const uint32_t *rank, void *ws, const Layout &L,
+void build_tree(const float *Y, int64_t n, float theta, const uint32_t *perm, void *ws, const Layout &L,
                 const TreeDebug &dbg, hipStream_t st)
 {
-    build_codes(Y, n, rank, ws, L, st);
+    build_codes(Y, n, perm, ws, L, st);
     build_sorted_tree(Y, n, theta, ws, L, dbg, st);
 }
 
@@ -407,7 +408,7 @@ int run_layout64(double *Y, const bhtsne_layout *lay, double theta, const StepAr
     {
         PhaseTimer pt(BHTSNE_PHASE_BBOX_MORTON, st);
         launch_bbox(Y, n, ws, L, st);
-        launch_morton(static_cast<const double *>(Y), n, lv.rank, ws, L, st);
+        launch_morton(static_cast<const double *>(Y), n, lv.perm, ws, L, st);
     }
     const int fork = fork_point64();
     if (fork >= 1) {
@@ -464,7 +465,7 @@ int run_layout(float *Y, const bhtsne_layout *lay, float theta, const StepArgs &
     // the attractive forces need only the layout-order copy of Y written with
     // the codes, so they can run beside the sort, tree and repulsive phases
     const int fork = fork_point();
-    build_codes(Y, n, lv.rank, ws, L, st);
+    build_codes(Y, n, lv.perm, ws, L, st);
     if (fork >= 1) {
         PhaseTimer pt(BHTSNE_PHASE_SORT, st);
         launch_sort(n, Y, ws, L, st);
@@ -550,7 +551,7 @@ int run_layout3(float *Y, const bhtsne_layout *lay, float theta, const StepArgs 
     const LayoutView lv = layout_view(lay->mem, n, lay->nnz, 4, 3);
     {
         PhaseTimer pt(BHTSNE_PHASE_BBOX_MORTON, st);
-        launch_bbox_morton3(Y, n, lv.rank, ws, L, st);
+        launch_bbox_morton3(Y, n, lv.perm, ws, L, st);
     }
     const int fork = fork_point3();
     if (fork >= 1) {

@@ -176,12 +176,14 @@ __device__ inline uint64_t spread_by_bytes(const uint16_t *__restrict__ tab, uin
 }
 
 // Codes of one tile of points, the private copy of Y (in the caller's order,
-// or in a layout order when `rank` is given), the 8 global digit histograms; also clears the per-position tree masks and this tile's
-// look-back status words of every pass.
+// or in a layout order when `perm` is given: position i holds the point
+// perm[i], gathered, which costs less than scattering each point to its
+// position), the 8 global digit histograms; also clears the per-position tree
+// masks and this tile's look-back status words of every pass.
 template <typename T>
 __global__ __launch_bounds__(kSortBlock) void morton_kernel(
     const vec2_t<T> *__restrict__ Y, int64_t n, const Header *__restrict__ hdr,
-    uint64_t *__restrict__ codes, vec2_t<T> *__restrict__ ycopy, const uint32_t *__restrict__ rank,
+    uint64_t *__restrict__ codes, vec2_t<T> *__restrict__ ycopy, const uint32_t *__restrict__ perm,
     uint32_t *__restrict__ hist, uint32_t *__restrict__ levelmask, uint32_t *__restrict__ status, int64_t tiles)
 {
     __shared__ uint32_t sh[kSortPasses * kRadix];
@@ -202,9 +204,9 @@ __global__ __launch_bounds__(kSortBlock) void morton_kernel(
         int64_t i = base + r * kSortBlock + threadIdx.x;
         if (i < n) {
             const vec2_t<T> y = Y[i];
-            if (rank) {
-                const uint32_t r = rank[i];
-                if (r < uint32_t(n)) ycopy[r] = y;
+            if (perm) {
+                const uint32_t p = perm[i];
+                if (p < uint32_t(n)) ycopy[i] = Y[p];
             } else {
                 ycopy[i] = y;
             }
@@ -365,7 +367,7 @@ __device__ inline uint64_t spread3_by_bytes(const uint32_t *__restrict__ tab, ui
 
 __global__ __launch_bounds__(kSortBlock) void morton3_kernel(
     const float3 *__restrict__ Y, int64_t n, const Header *__restrict__ hdr, uint64_t *__restrict__ codes,
-    float3 *__restrict__ ycopy, const uint32_t *__restrict__ rank, uint32_t *__restrict__ hist,
+    float3 *__restrict__ ycopy, const uint32_t *__restrict__ perm, uint32_t *__restrict__ hist,
     uint32_t *__restrict__ levelmask, uint32_t *__restrict__ status, int64_t tiles)
 {
     __shared__ uint32_t sh[kSortPasses * kRadix];
@@ -385,8 +387,8 @@ __global__ __launch_bounds__(kSortBlock) void morton3_kernel(
         const int64_t i = base + r * kSortBlock + threadIdx.x;
         if (i < n) {
             const float3 y = Y[i];
-            const uint32_t o = rank ? rank[i] : uint32_t(i); // a layout's order, or the caller's
-            ycopy[o < uint32_t(n) ? o : uint32_t(i)] = y;
+            const uint32_t p = perm ? perm[i] : uint32_t(i); // a layout's order, or the caller's
+            ycopy[i] = p == uint32_t(i) ? y : Y[p < uint32_t(n) ? p : uint32_t(i)];
             const uint64_t code = spread3_by_bytes(s_spread, quantise21(y.x, yr0, sc)) |
                                   (spread3_by_bytes(s_spread, quantise21(y.y, yr1, sc)) << 1) |
                                   (spread3_by_bytes(s_spread, quantise21(y.z, yr2, sc)) << 2);
@@ -595,7 +597,7 @@ template <typename T> void launch_bbox(const T *Y, int64_t n, void *ws, const La
 template void launch_bbox<float>(const float *, int64_t, void *, const Layout &, hipStream_t);
 template void launch_bbox<double>(const double *, int64_t, void *, const Layout &, hipStream_t);
 
-void launch_bbox_morton3(const float *Y, int64_t n, const uint32_t *rank, void *ws, const Layout &L, hipStream_t st)
+void launch_bbox_morton3(const float *Y, int64_t n, const uint32_t *perm, void *ws, const Layout &L, hipStream_t st)
 {
     int blocks = int((n + 255) / 256);
     if (blocks > kBBoxBlocks) blocks = kBBoxBlocks;
@@ -604,16 +606,16 @@ void launch_bbox_morton3(const float *Y, int64_t n, const uint32_t *rank, void *
     bbox3_final_kernel<<<1, 256, 0, st>>>(at<float>(ws, L.bbox_part), blocks, at<Header>(ws, L.header),
                                           at<uint32_t>(ws, L.hist));
     morton3_kernel<<<unsigned(L.sort_tiles), kSortBlock, 0, st>>>(
-        y3, n, at<Header>(ws, L.header), at<uint64_t>(ws, L.codes0), at<float3>(ws, L.ycopy), rank,
+        y3, n, at<Header>(ws, L.header), at<uint64_t>(ws, L.codes0), at<float3>(ws, L.ycopy), perm,
         at<uint32_t>(ws, L.hist), at<uint32_t>(ws, L.levelmask), at<uint32_t>(ws, L.status), L.sort_tiles);
 }
 
 template <typename T>
-void launch_morton(const T *Y, int64_t n, const uint32_t *rank, void *ws, const Layout &L, hipStream_t st)
+void launch_morton(const T *Y, int64_t n, const uint32_t *perm, void *ws, const Layout &L, hipStream_t st)
 {
     morton_kernel<T><<<unsigned(L.sort_tiles), kSortBlock, 0, st>>>(
         reinterpret_cast<const vec2_t<T> *>(Y), n, at<Header>(ws, L.header), at<uint64_t>(ws, L.codes0),
-        at<vec2_t<T>>(ws, L.ycopy), rank, at<uint32_t>(ws, L.hist), at<uint32_t>(ws, L.levelmask),
+        at<vec2_t<T>>(ws, L.ycopy), perm, at<uint32_t>(ws, L.hist), at<uint32_t>(ws, L.levelmask),
         at<uint32_t>(ws, L.status), L.sort_tiles);
 }
 template void launch_morton<float>(const float *, int64_t, const uint32_t *, void *, const Layout &, hipStream_t);

@@ -115,7 +115,7 @@ __device__ inline int64_t run_end(const uint64_t *__restrict__ codes, int64_t x,
 // whole block: 64 probes per round narrow the range 65-fold, so four or five
 // rounds of loads replace the twenty-odd dependent loads of a gallop through
 // global memory, which the other lanes of its wave would have waited for.
-constexpr int kSplitBlock = 256;
+constexpr int kSplitBlock = 512;
 constexpr int kSplitWin = 1024;
 
 __device__ inline bool same_cell(uint64_t c, uint64_t key, int sh) { return ((c ^ key) >> sh) == 0; }
@@ -648,7 +648,7 @@ void launch_tree(int64_t n, double theta2, void *ws, const Layout &L, const Tree
     uint32_t *tc = at<uint32_t>(ws, L.scan_cnt);
     double *ts = at<double>(ws, L.scan_sum);
     unsigned gn = unsigned((n + 255) / 256);
-    tree_splits_kernel<D><<<gn, 256, 0, st>>>(codes, n, lm, sb, se);
+    tree_splits_kernel<D><<<unsigned((n + kSplitBlock - 1) / kSplitBlock), kSplitBlock, 0, st>>>(codes, n, lm, sb, se);
     scan_reduce_kernel<D, T><<<unsigned(L.scan_tiles), kScanBlock, 0, st>>>(codes, lm, ys, hdr, n, tc, ts);
     scan_top_kernel<D><<<1, kScanBlock, 0, st>>>(tc, ts, L.scan_tiles, n, base, psum, hdr);
     scan_down_kernel<D, T><<<unsigned(L.scan_tiles), kScanBlock, 0, st>>>(codes, lm, ys, hdr, n, tc, ts, base, psum);

@@ -80,12 +80,13 @@ constexpr int kOrderBfs = 1;    // breadth-first level from the component's root
 constexpr int kOrderAuto = 2;   // Morton; BFS levels when Morton gives no tiles and BFS does
 
 template <typename T> void launch_bbox(const T *Y, int64_t n, void *ws, const Layout &L, hipStream_t st);
-// rank (nullable): write the private copy of Y in that order instead of the caller's
+// perm (nullable; a layout's position -> caller's index): the private copy of
+// Y in the layout's order, ycopy[i] = Y[perm[i]], instead of the caller's
 template <typename T>
-void launch_morton(const T *Y, int64_t n, const uint32_t *rank, void *ws, const Layout &L, hipStream_t st);
+void launch_morton(const T *Y, int64_t n, const uint32_t *perm, void *ws, const Layout &L, hipStream_t st);
 // 3-D embeddings (Y n x 3 fp32): box, cube, 63-bit codes, digit histograms and
-// the private copy of Y in the caller's order, or in rank's (nullable) order
-void launch_bbox_morton3(const float *Y, int64_t n, const uint32_t *rank, void *ws, const Layout &L,
+// the private copy of Y in the caller's order, or in perm's (nullable) order
+void launch_bbox_morton3(const float *Y, int64_t n, const uint32_t *perm, void *ws, const Layout &L,
                          hipStream_t st);
 // ysrc: Y in the original order, gathered into Morton order by the last pass
 template <typename T> void launch_sort(int64_t n, const T *ysrc, void *ws, const Layout &L, hipStream_t st);
